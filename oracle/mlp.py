@@ -1,0 +1,109 @@
+"""One base model: forward, loss, backward, AdamW -- plain float64 numpy.
+
+§3.3 Model Pack defines the base model as a sequence of Linear-ReLU-Dropout
+blocks; the output head is a plain Linear layer with no activation or dropout.
+Parameters use nn.Linear's layout: W is [out, in], b is [out], so a layer maps
+H -> H @ W.T + b.
+
+Losses (App. F, training of DL models): cross-entropy for classification
+(binary cross-entropy with logits for two classes) and mean squared error for
+regression, each averaged over the member's base batch of B rows.
+"""
+import numpy as np
+
+from .philox import philox4x32_10
+from .sampling import TAG_DROPOUT, stream_key
+
+TASK_REG, TASK_BIN, TASK_MULTI = "reg", "bin", "multi"
+
+
+def dropout_mask(seed, k, step, layer, B, width, t):
+    """Keep mask (bool [B, width]) of member k, hidden layer ``layer`` (1-based).
+
+    Element (r, c) reads word (r & 3) of the Philox4x32-10 block with counter
+    (r >> 2, c, (k << 8) | layer, step mod 2**32) under the dropout stream key,
+    and is kept iff that word >= t (t = floor(p * 2**32)); p = 0 keeps all.
+    """
+    k0, k1 = stream_key(seed, TAG_DROPOUT)
+    r = np.arange(B, dtype=np.uint64)[:, None]
+    c = np.arange(width, dtype=np.uint64)[None, :]
+    words = philox4x32_10(r >> np.uint64(2), c, (int(k) << 8) | int(layer),
+                          int(step) & 0xFFFFFFFF, k0, k1)
+    sel = np.broadcast_to((r & np.uint64(3)).astype(np.int64), (B, width))
+    return np.choose(sel, words) >= np.uint32(t)
+
+
+def forward(params, X, masks=None, scale=1.0):
+    """Returns (Y, cache).  masks[l] is the keep mask of hidden layer l+1 or None."""
+    H = np.asarray(X, dtype=np.float64)
+    cache = {"H": [H], "Z": []}
+    L = len(params) - 1
+    for l in range(L):
+        W, b = params[l]
+        Z = H @ W.T + b
+        H = np.maximum(Z, 0.0)
+        if masks is not None:
+            H = H * masks[l] * scale
+        cache["Z"].append(Z)
+        cache["H"].append(H)
+    Wo, bo = params[L]
+    return H @ Wo.T + bo, cache
+
+
+def loss_and_dy(Y, y, task):
+    """Batch-mean loss and dLoss/dY for one member."""
+    B = Y.shape[0]
+    if task == TASK_REG:
+        diff = Y[:, 0] - np.asarray(y, dtype=np.float64)
+        return float(np.mean(diff * diff)), (2.0 * diff / B)[:, None]
+    if task == TASK_BIN:
+        z = Y[:, 0]
+        t = np.asarray(y, dtype=np.float64)
+        loss = np.maximum(z, 0.0) - z * t + np.log1p(np.exp(-np.abs(z)))
+        sig = 1.0 / (1.0 + np.exp(-z))
+        return float(np.mean(loss)), ((sig - t) / B)[:, None]
+    if task == TASK_MULTI:
+        lab = np.asarray(y, dtype=np.int64)
+        mx = Y.max(axis=1, keepdims=True)
+        lse = mx[:, 0] + np.log(np.exp(Y - mx).sum(axis=1))
+        loss = lse - Y[np.arange(B), lab]
+        P = np.exp(Y - lse[:, None])
+        P[np.arange(B), lab] -= 1.0
+        return float(np.mean(loss)), P / B
+    raise ValueError(task)
+
+
+def backward(params, cache, dY, masks=None, scale=1.0):
+    """Gradients [(dW, db), ...] in the layout of ``params``."""
+    L = len(params) - 1
+    grads = [None] * (L + 1)
+    H = cache["H"]
+    Wo, _ = params[L]
+    grads[L] = (dY.T @ H[L], dY.sum(axis=0))
+    dH = dY @ Wo
+    for l in range(L - 1, -1, -1):
+        dZ = dH * (cache["Z"][l] > 0.0)
+        if masks is not None:
+            dZ = dZ * masks[l] * scale
+        W, _ = params[l]
+        grads[l] = (dZ.T @ H[l], dZ.sum(axis=0))
+        if l > 0:
+            dH = dZ @ W
+    return grads
+
+
+def adamw_step(theta, g, m, v, t, lr, wd, beta1, beta2, eps, decay=True):
+    """One decoupled-weight-decay Adam step (Loshchilov & Hutter), torch order.
+
+    theta <- theta * (1 - lr*wd); m <- b1 m + (1-b1) g; v <- b2 v + (1-b2) g^2;
+    theta <- theta - lr/(1-b1^t) * m / (sqrt(v)/sqrt(1-b2^t) + eps).
+    Returns new (theta, m, v).
+    """
+    if decay:
+        theta = theta * (1.0 - lr * wd)
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    bc1 = 1.0 - beta1 ** t
+    bc2 = 1.0 - beta2 ** t
+    denom = np.sqrt(v) / np.sqrt(bc2) + eps
+    return theta - (lr / bc1) * m / denom, m, v

@@ -1,0 +1,122 @@
+"""The pack: K independent base models, one Python loop iteration each.
+
+§3.3 Model Pack: packing must reproduce the original base models exactly, so
+the reference result of a packed step is simply K separate MLP steps.
+§3.6 Training: member k trains on its own base batch X[idx[k]], and the pack's
+objective is the *sum* of the members' batch-mean losses (losses aggregated,
+predictions not), which gives every member exactly its standalone gradient.
+§3.4 Optimizer Pack: member k is updated by its own AdamW with (lr_k, wd_k).
+"""
+import numpy as np
+
+from . import mlp
+from .sampling import init_member, sample_hparams
+
+
+class OraclePack:
+    """Holds fp64 parameters and AdamW moments of K members."""
+
+    def __init__(self, cfg, hparams=None, params=None):
+        self.cfg = dict(cfg)
+        self.hp = hparams if hparams is not None else sample_hparams(cfg)
+        if params is None:
+            params = [init_member(cfg, k, h["width"]) for k, h in enumerate(self.hp)]
+        self.params = [[(W.copy(), b.copy()) for W, b in p] for p in params]
+        self.m = [[(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
+        self.v = [[(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
+        self.t = 0
+        self.last_grads = None
+
+    def masks(self, k, step):
+        c, h = self.cfg, self.hp[k]
+        return [mlp.dropout_mask(c["seed"], k, step, l + 1, c["B"], h["width"], h["t"])
+                for l in range(c["L"])]
+
+    def member_step(self, k, X, y, idx_k, step):
+        """Forward, loss, backward and AdamW for member k; returns (loss, grads)."""
+        c, h = self.cfg, self.hp[k]
+        rows = np.asarray(idx_k, dtype=np.int64)
+        masks = self.masks(k, step)
+        Y, cache = mlp.forward(self.params[k], X[rows], masks, h["s"])
+        loss, dY = mlp.loss_and_dy(Y, y[rows], c["task"])
+        grads = mlp.backward(self.params[k], cache, dY, masks, h["s"])
+        new_p, new_m, new_v = [], [], []
+        for i, ((W, b), (gW, gb), (mW, mb), (vW, vb)) in enumerate(
+                zip(self.params[k], grads, self.m[k], self.v[k])):
+            args = (step, h["lr"], h["wd"], c["beta1"], c["beta2"], c["eps"])
+            W2, mW2, vW2 = mlp.adamw_step(W, gW, mW, vW, *args)
+            b2, mb2, vb2 = mlp.adamw_step(b, gb, mb, vb, *args, decay=bool(c["decay_bias"]))
+            new_p.append((W2, b2))
+            new_m.append((mW2, mb2))
+            new_v.append((vW2, vb2))
+        self.params[k], self.m[k], self.v[k] = new_p, new_m, new_v
+        return loss, grads
+
+    def train_step(self, X, y, idx, step, members=None):
+        """One step for every member (or for ``members`` only); returns losses [K].
+
+        ``step`` is the 1-based AdamW step t, also the dropout counter.
+        Members left out keep their state; their loss is reported as NaN.
+        """
+        K = self.cfg["K"]
+        X = np.asarray(X, dtype=np.float64)
+        losses = np.full(K, np.nan)
+        self.last_grads = [None] * K
+        for k in (range(K) if members is None else members):
+            losses[k], self.last_grads[k] = self.member_step(k, X, y, idx[k], step)
+        self.t = step
+        return losses
+
+    def predict(self, k, Xv):
+        """Score-ready prediction of member k on Xv (no dropout)."""
+        Y, _ = mlp.forward(self.params[k], np.asarray(Xv, dtype=np.float64))
+        return Y
+
+    def eval_members(self, Xv, yv, members=None):
+        """(pred [K, Nv], score [K]) as in ``prediction`` and ``score``."""
+        K = self.cfg["K"]
+        preds = np.full((K, len(yv)), np.nan)
+        scores = np.full(K, np.nan)
+        for k in (range(K) if members is None else members):
+            preds[k] = prediction(self.predict(k, Xv), yv, self.cfg["task"])
+            scores[k] = score(preds[k], yv, self.cfg["task"])
+        return preds, scores
+
+
+def prediction(Y, yv, task):
+    """Per-row candidate value used for scoring and ensembling.
+
+    Regression: the output itself.  Binary: the probability of class 1.
+    Multiclass: the probability assigned to the true class (ensembles average
+    probabilities, and the cross-entropy of an average needs only that column).
+    """
+    if task == mlp.TASK_REG:
+        return Y[:, 0]
+    if task == mlp.TASK_BIN:
+        return 1.0 / (1.0 + np.exp(-Y[:, 0]))
+    mx = Y.max(axis=1, keepdims=True)
+    P = np.exp(Y - mx)
+    P /= P.sum(axis=1, keepdims=True)
+    return P[np.arange(len(yv)), np.asarray(yv, dtype=np.int64)]
+
+
+PROB_CLIP = 1e-15
+
+
+def score(pred, yv, task):
+    """Validation score (lower is better): RMSE, binary CE, or multiclass CE.
+
+    Probabilities are clipped to [1e-15, 1 - 1e-15] before the logarithm.  A
+    non-finite result is reported as +inf.
+    """
+    p = np.asarray(pred, dtype=np.float64)
+    if task == mlp.TASK_REG:
+        d = p - np.asarray(yv, dtype=np.float64)
+        s = np.sqrt(np.mean(d * d))
+    elif task == mlp.TASK_BIN:
+        y = np.asarray(yv, dtype=np.float64)
+        q = np.clip(p, PROB_CLIP, 1.0 - PROB_CLIP)
+        s = np.mean(-y * np.log(q) - (1.0 - y) * np.log1p(-q))
+    else:
+        s = np.mean(-np.log(np.clip(p, PROB_CLIP, 1.0)))
+    return float(s) if np.isfinite(s) else float("inf")

@@ -1,0 +1,126 @@
+"""Seeded synthetic tabular data and batch orders.
+
+Holds no arithmetic of the packed method: it only makes inputs (features,
+targets, per-member batch index lists) that both the HIP library and the CPU
+oracle consume.  Random numbers come from numpy Generator(Philox(key=[seed,
+stream])) with stream 0 = data and stream 4 = batch order.
+
+Recipes (per workload, see ``configs``):
+  normal              d_in columns ~ N(0, 1)
+  onehot              (d_in - 16) columns ~ N(0,1) followed by 4 categorical
+                      features uniform over 4 levels, one-hot encoded (16 cols)
+  lognormal_rankgauss exp(N(0,1)) columns mapped by the rank-Gauss transform
+                      Phi^-1((rank + 0.5) / N_train) fitted on the training
+                      rows and applied to validation rows by interpolation
+  zero_inflated       N(0,1) columns; a seeded 20% of the columns have each
+                      entry set to exactly 0 with probability 0.5
+  block_correlated    blocks of 30 columns, x = sqrt(.6) z_block + sqrt(.4) e
+Teacher: a tanh MLP with 32 hidden units, W ~ N(0, 1/fan_in), zero biases.
+Labels: 'sign' -> 1[teacher > 0]; 'argmax' -> argmax of d_out teacher logits;
+'teacher_noise' -> teacher + N(0, 0.1^2), standardised on train;
+'teacher_t3' -> unit-variance teacher + 0.1 * Student-t(3), standardised.
+"""
+import numpy as np
+from scipy.special import ndtri
+
+
+def _rng(seed, stream):
+    return np.random.Generator(np.random.Philox(key=np.array([seed, stream], dtype=np.uint64)))
+
+
+def _features(cfg, rng, n):
+    d = cfg["d_in"]
+    kind = cfg["features"]
+    if kind in ("normal", "lognormal_rankgauss", "zero_inflated"):
+        X = rng.standard_normal((n, d), dtype=np.float32)
+        if kind == "lognormal_rankgauss":
+            np.exp(X, out=X)
+        elif kind == "zero_inflated":
+            cols = rng.choice(d, size=max(1, int(round(0.2 * d))), replace=False)
+            for c in np.sort(cols):
+                X[rng.random(n) < 0.5, c] = 0.0
+        return X
+    if kind == "onehot":
+        n_num = d - 16
+        X = np.zeros((n, d), dtype=np.float32)
+        X[:, :n_num] = rng.standard_normal((n, n_num), dtype=np.float32)
+        for j in range(4):
+            lev = rng.integers(0, 4, size=n)
+            X[np.arange(n), n_num + 4 * j + lev] = 1.0
+        return X
+    if kind == "block_correlated":
+        X = np.empty((n, d), dtype=np.float32)
+        nb = (d + 29) // 30
+        chunk = 65536
+        for r0 in range(0, n, chunk):
+            r1 = min(n, r0 + chunk)
+            z = rng.standard_normal((r1 - r0, nb), dtype=np.float32)
+            e = rng.standard_normal((r1 - r0, d), dtype=np.float32)
+            zb = np.repeat(z, 30, axis=1)[:, :d]
+            X[r0:r1] = np.float32(np.sqrt(0.6)) * zb + np.float32(np.sqrt(0.4)) * e
+        return X
+    raise ValueError(kind)
+
+
+def _rank_gauss(Xtr, Xva):
+    n = Xtr.shape[0]
+    out_tr = np.empty_like(Xtr)
+    out_va = np.empty_like(Xva)
+    q = ndtri((np.arange(n) + 0.5) / n)
+    for j in range(Xtr.shape[1]):
+        order = np.argsort(Xtr[:, j], kind="stable")
+        col = np.empty(n)
+        col[order] = q
+        out_tr[:, j] = col
+        out_va[:, j] = np.interp(Xva[:, j], Xtr[order, j], q)
+    return out_tr, out_va
+
+
+def _teacher(rng, X, d_out):
+    d = X.shape[1]
+    W1 = rng.standard_normal((d, 32)) / np.sqrt(d)
+    W2 = rng.standard_normal((32, d_out)) / np.sqrt(32)
+    out = np.empty((X.shape[0], d_out))
+    for r0 in range(0, X.shape[0], 65536):
+        out[r0:r0 + 65536] = np.tanh(X[r0:r0 + 65536] @ W1) @ W2
+    return out
+
+
+def make_data(cfg, n_train=None, n_val=None):
+    """(X_train fp32 [Ntr, d_in], y_train, X_val, y_val); y is fp32 or int32 labels."""
+    n_tr = cfg["n_train"] if n_train is None else n_train
+    n_va = cfg["n_val"] if n_val is None else n_val
+    rng = _rng(cfg["seed"], 0)
+    X = _features(cfg, rng, n_tr + n_va)
+    Xtr, Xva = X[:n_tr], X[n_tr:]
+    if cfg["features"] == "lognormal_rankgauss":
+        Xtr, Xva = _rank_gauss(Xtr, Xva)
+    Xtr = np.ascontiguousarray(Xtr, dtype=np.float32)
+    Xva = np.ascontiguousarray(Xva, dtype=np.float32)
+    lab = cfg["label"]
+    T = _teacher(rng, np.concatenate([Xtr, Xva]), cfg["d_out"])
+    if lab == "sign":
+        y = (T[:, 0] > 0).astype(np.float32)
+    elif lab == "argmax":
+        y = np.argmax(T, axis=1).astype(np.int32)
+    else:
+        t = T[:, 0]
+        if lab == "teacher_noise":
+            t = t + 0.1 * rng.standard_normal(len(t))
+        else:
+            t = t / max(np.std(t[:n_tr]), 1e-12) + 0.1 * rng.standard_t(3, size=len(t))
+        mu, sd = t[:n_tr].mean(), t[:n_tr].std()
+        y = ((t - mu) / max(sd, 1e-12)).astype(np.float32)
+    return Xtr, y[:n_tr], Xva, y[n_tr:]
+
+
+def epoch_orders(cfg, epoch, n_train):
+    """Per-member permutations of the training rows for one epoch: int64 [K, n_train]."""
+    rng = _rng(cfg["seed"], 4 + (int(epoch) << 8))
+    return np.stack([rng.permutation(n_train) for _ in range(cfg["K"])])
+
+
+def batch_indices(orders, step_in_epoch, B):
+    """idx [K, B] int32 of one step (drop-last batching of each member's order)."""
+    s = int(step_in_epoch)
+    return np.ascontiguousarray(orders[:, s * B:(s + 1) * B], dtype=np.int32)
