@@ -1,0 +1,192 @@
+/*
+ * tabpack.h -- C ABI of the packed-MLP hot path for AMD Instinct MI355X (gfx950).
+ *
+ * The method (arXiv 2607.05380, "TabPack"): K base MLPs, each with its own
+ * sampled hidden width, dropout rate, learning rate and weight decay, are
+ * trained in parallel as one "model pack" (Section 3.3) with one "optimizer
+ * pack" (Section 3.4), each member on its own base batch with the members'
+ * losses summed (Section 3.6); after an epoch every member is scored on
+ * validation data and an ensemble is built greedily from the pool of
+ * candidates (Section 3.5).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Return value: PACK_OK (0) or a negative PACK_E* code.  The message of the
+ *   last failure on the calling thread is available from pack_last_error().
+ *   No C++ exception crosses this boundary.
+ * - Device pointers are plain HIP device addresses owned by the caller; the
+ *   library keeps only non-owning pointers into the workspace bound with
+ *   pack_bind() and never allocates device memory.  Host pointers are read or
+ *   written synchronously inside the call.
+ * - Work is enqueued asynchronously on the given hipStream_t (0 = the null
+ *   stream); outputs in device memory are valid once that stream is done.
+ * - A handle is not thread-safe; concurrent calls on one handle race.
+ * - Row-major storage everywhere.  Feature matrices X are fp32 [N, d_in].
+ *   Targets y are fp32 [N] (regression value or binary label 0/1) or int32
+ *   [N] class indices for PACK_TASK_MULTI_CE.
+ */
+#ifndef TABPACK_H
+#define TABPACK_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PACK_OK 0
+#define PACK_EINVAL (-1)       /* an argument is out of range or inconsistent */
+#define PACK_ESTATE (-2)       /* call not valid in the handle's current state */
+#define PACK_EHIP (-3)         /* a HIP runtime call failed */
+#define PACK_EUNSUPPORTED (-4) /* a valid request this build does not implement */
+
+enum { PACK_TASK_REG_MSE = 0, PACK_TASK_BIN_BCE = 1, PACK_TASK_MULTI_CE = 2 };
+enum { PACK_PREC_BF16 = 0, PACK_PREC_FP32 = 1 };
+
+/* Hyperparameters of one base model (Section 3.7: drawn per member from
+ * user-given ranges; one hidden width shared by all hidden layers of the
+ * member).  As input (pack_config.members) only width, dropout, lr and wd are
+ * read; pack_get_hparams() also fills the derived fields. */
+typedef struct pack_member_hp {
+  int32_t width;           /* hidden width d_k, >= 1 */
+  int32_t padded_width;    /* out: d_k rounded up to the quantum q */
+  uint32_t drop_threshold; /* out: t_k = floor(p_k * 2^32); an element is kept iff its word >= t_k */
+  int32_t reserved;
+  double dropout;          /* p_k in [0, 1) */
+  double lr;               /* AdamW learning rate, > 0 */
+  double wd;               /* AdamW decoupled weight decay, >= 0 */
+  double scale;            /* out: inverted-dropout scale s_k = 1 / (1 - p_k) */
+} pack_member_hp;
+
+/* Description of a pack.  Ranges are inclusive: width ~ UniformInt[lo, hi],
+ * dropout ~ Uniform[lo, hi], lr and wd ~ LogUniform[lo, hi] (Section 3.7;
+ * the paper's hyperparameter-space table in App. F lists the same kinds of
+ * distributions). */
+typedef struct pack_config {
+  int32_t K;          /* number of members, 1 .. 65535 */
+  int32_t d_in;       /* input features, >= 1 */
+  int32_t d_out;      /* outputs: 1 for PACK_TASK_REG_MSE / PACK_TASK_BIN_BCE, classes (2..16) for CE */
+  int32_t L;          /* hidden Linear-ReLU-Dropout blocks per member, 1 .. 8 */
+  int32_t B;          /* rows per member per step (base batch), 1 .. 65536 */
+  int32_t task;       /* PACK_TASK_* */
+  int32_t precision;  /* PACK_PREC_BF16: bf16 MFMA GEMMs, fp32 master weights; PACK_PREC_FP32: fp32 MFMA */
+  int32_t width_lo, width_hi;
+  int32_t quantum;    /* padding quantum q for widths (multiple of 8); 0 selects 32 */
+  int32_t decay_bias; /* 1: weight decay also on biases (torch default), 0: weights only */
+  int32_t reserved;
+  double dropout_lo, dropout_hi;
+  double lr_lo, lr_hi;
+  double wd_lo, wd_hi;
+  double beta1, beta2, eps; /* AdamW constants, e.g. 0.9, 0.999, 1e-8 */
+  uint64_t seed;            /* hyperparameters, initial parameters and dropout masks derive from it */
+  const pack_member_hp* members; /* optional [K] explicit hyperparameters; NULL: sample from the ranges */
+} pack_config;
+
+typedef struct pack_handle pack_handle;
+
+/* Message of the last failed call on this thread ("" if none).  Never NULL. */
+const char* pack_last_error(void);
+
+/* Create a pack (host only, allocates no device memory): validate cfg, draw
+ * every member's hyperparameters (Section 3.7) unless cfg->members is given,
+ * plan the packed layout and generate the initial parameters on the host
+ * (torch.nn.Linear's default U(-1/sqrt(fan_in), 1/sqrt(fan_in)) for weights
+ * and biases, fan_in = the member's true input width; padding exactly zero).
+ * On success *out owns the handle; release it with pack_destroy(). */
+int pack_init(const pack_config* cfg, pack_handle** out);
+
+/* Release the handle and its host memory.  The bound workspace stays the
+ * caller's.  NULL is accepted. */
+int pack_destroy(pack_handle* h);
+
+/* Copy the K members' hyperparameters (inputs and derived fields) to out[K]. */
+int pack_get_hparams(const pack_handle* h, pack_member_hp* out);
+
+/* Device workspace (bytes) that pack_bind() needs: parameters, gradients,
+ * AdamW moments, bf16 weight shadow, activations and launch tables. */
+int pack_workspace_size(const pack_handle* h, size_t* bytes);
+
+/* Bind a caller-owned device workspace of at least pack_workspace_size()
+ * bytes (256-byte aligned) and upload the initial parameters; moments and the
+ * step counter are reset to zero.  May be called again to move the pack to a
+ * new workspace (state is re-initialised from the host copy). */
+int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream);
+
+/* One training step of all K members (Sections 3.3, 3.4, 3.6): member k runs
+ * forward on its base batch X[idx[k*B + b], :] (b < B) through L blocks
+ * H = Dropout_k(ReLU(H W^T + b)) and a linear head, computes its batch-mean
+ * loss (MSE, binary CE with logits, or multiclass CE), backpropagates, and
+ * takes one AdamW step with its own (lr_k, wd_k).  The pack objective is the
+ * sum of the members' losses, so each member receives exactly its own
+ * gradient.
+ *   X        device fp32 [N, d_in]; y device fp32 [N] or int32 [N] (CE)
+ *   idx      device int32 [K, B], every entry in [0, N)
+ *   step     1-based AdamW step t; must be the previous step + 1 (PACK_ESTATE
+ *            otherwise).  It is also the dropout counter of this step.
+ *   loss_out device fp32 [K]: batch-mean loss of each member before the update
+ * Dropout masks: element (r, c) of hidden layer l of member k is kept iff word
+ * (r & 3) of Philox4x32-10(counter = (r >> 2, c, (k << 8) | l, step mod 2^32),
+ * key = (seed mod 2^32, (seed >> 32) ^ (3 << 28))) is >= t_k. */
+int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N,
+                    const int32_t* idx, uint64_t step, float* loss_out, hipStream_t stream);
+
+/* Evaluate every member on validation rows without dropout (Section 3.5 /
+ * 3.6: per-epoch validation scoring feeds early stopping and selection).
+ *   pred_out  device fp32 [K, Nv]: the per-row value an ensemble averages --
+ *             the output (regression), P(class 1) (binary), or the
+ *             probability of the true class (multiclass)
+ *   score_out device fp64 [K]: RMSE, mean binary CE or mean CE of pred_out
+ *             (probabilities clipped to [1e-15, 1 - 1e-15]); non-finite -> +inf */
+int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t Nv,
+                      float* pred_out, double* score_out, hipStream_t stream);
+
+/* Scratch bytes pack_select() needs for C candidates over Nv rows. */
+int pack_select_workspace_size(int32_t C, int64_t Nv, size_t* bytes);
+
+/* Greedy ensemble selection (Section 3.5): start from the best single
+ * candidate, then repeatedly add -- without replacement -- the candidate whose
+ * addition gives the best score of the averaged ensemble; stop at m_ens
+ * members or when no addition strictly improves the score.  Ties go to the
+ * lowest candidate index; non-finite scores count as +inf and are never
+ * picked.  Scores are computed in fp64 with the rule of pack_eval_members.
+ *   cand      device fp32 [C, Nv] candidate values (rows of pred_out; for the
+ *             online ensemble the K current members followed by the previous
+ *             ensemble's frozen members, each a separate candidate)
+ *   work      device scratch of pack_select_workspace_size() bytes
+ *   sel_out   device int32 [m_ens]: picks in order; n_sel_out device int32 [1];
+ *   score_out device fp64 [1]: the final ensemble's score (+inf if empty) */
+int pack_select(pack_handle* h, const float* cand, const void* yv, int32_t C, int64_t Nv,
+                int32_t m_ens, void* work, size_t work_bytes, int32_t* sel_out,
+                int32_t* n_sel_out, double* score_out, hipStream_t stream);
+
+/* Number of floats in member k's dense parameter vector: for l = 1..L the
+ * row-major [d_k, fan_in] weight then its [d_k] bias, then the head's
+ * [d_out, d_k] weight and [d_out] bias (torch.nn.Linear layout). */
+int pack_member_param_count(const pack_handle* h, int32_t member, int64_t* count);
+
+/* Copy member k's parameters to / from a host buffer in the dense layout
+ * above.  Before pack_bind() they read/write the host initial values; after
+ * it, the device state (synchronous on the null stream). */
+int pack_get_params(pack_handle* h, int32_t member, float* host_out);
+int pack_set_params(pack_handle* h, int32_t member, const float* host_in);
+
+/* Gradients of the last pack_train_step() and the AdamW moments of member k,
+ * dense layout, copied to host buffers (synchronous). */
+int pack_get_grads(pack_handle* h, int32_t member, float* host_out);
+int pack_get_moments(pack_handle* h, int32_t member, float* m_out, float* v_out);
+
+/* Test hooks.  pack_debug_dropout_mask writes the keep mask (uint8 0/1,
+ * [B, d_k]) of hidden layer `layer` (1-based) of member k at `step` to device
+ * memory using the same device function as the training epilogue.
+ * pack_debug_activation copies the stored post-dropout activation H_layer of
+ * member k ([B, d_k] as fp32) of the last forward pass to a host buffer. */
+int pack_debug_dropout_mask(pack_handle* h, uint64_t step, int32_t layer, int32_t member,
+                            uint8_t* dev_out, hipStream_t stream);
+int pack_debug_activation(pack_handle* h, int32_t layer, int32_t member, float* host_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TABPACK_H */

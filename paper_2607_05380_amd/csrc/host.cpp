@@ -1,0 +1,739 @@
+// Host runtime of the packed-MLP library: argument checking, hyperparameter
+// sampling, the packed layout planner, initial parameters, workspace binding,
+// launch sequencing of the training step / evaluation / greedy selection, and
+// the C ABI declared in include/tabpack.h.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/tabpack.h"
+#include "pack_internal.h"
+#include "philox.h"
+
+using namespace tabpack;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess) return fail(PACK_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr uint32_t kTagHparam = 1, kTagInit = 2;
+constexpr int kTileM = 128, kTileN = 128;  // grouped-GEMM output tile
+
+int64_t round_up(int64_t x, int64_t q) { return (x + q - 1) / q * q; }
+
+struct Key {
+  uint32_t k0, k1;
+};
+Key stream_key(uint64_t seed, uint32_t tag) {
+  return Key{(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32) ^ (tag << 28)};
+}
+
+// Double in [0, 1) with 53 random bits from two 32-bit words.
+double u53(uint32_t a, uint32_t b) {
+  return ((double)(a >> 5) * 67108864.0 + (double)(b >> 6)) * (1.0 / 9007199254740992.0);
+}
+
+double log_uniform(double lo, double hi, double u) {
+  if (lo == hi) return lo;
+  return std::exp(std::log(lo) + u * (std::log(hi) - std::log(lo)));
+}
+
+struct Member {
+  int width, dp;
+  double dropout, lr, wd, scale;
+  uint32_t t;
+  std::vector<int64_t> toff;  // packed offsets of W_1, b_1, ..., W_L, b_L, W_out, b_out
+  int64_t act_off;
+};
+
+struct Launch {
+  int desc0, ndesc;
+  int tile0, ntiles;
+};
+
+}  // namespace
+
+// Device buffers carved out of the caller's workspace.
+struct Bufs {
+  float *theta = nullptr, *grad = nullptr, *m = nullptr, *v = nullptr;
+  uint16_t* shadow = nullptr;
+  char* H = nullptr;   // L activation buffers H_1..H_L
+  char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
+  float *dY = nullptr, *rowloss = nullptr;
+  MemberDev* d_mem = nullptr;
+  uint32_t* d_chunks = nullptr;
+  int64_t* d_bias_off = nullptr;  // [L][K] offsets of b_l
+  GemmDesc* d_descs = nullptr;
+  Tile* d_tiles = nullptr;
+  ColTile* d_coltiles = nullptr;
+};
+
+struct pack_handle {
+  pack_config cfg;
+  Prec prec;
+  Task task;
+  int q, Bp, Pin;
+  std::vector<Member> mem;
+  int64_t P = 0;     // packed parameter count (multiple of kChunk)
+  int64_t A = 0;     // elements of one activation buffer (all members)
+  std::vector<float> theta_host;  // host copy of the parameters, packed layout
+  std::vector<uint32_t> chunk_tab;
+
+  bool bound = false;
+  Bufs b;
+  std::vector<Launch> fwd, dx, dw;  // per layer (index l-1)
+  int ncoltiles = 0;
+  uint64_t t = 0;
+
+  size_t elt() const { return prec == Prec::BF16 ? 2 : 4; }
+  void* Hl(int l) const { return b.H + (size_t)(l - 1) * A * elt(); }  // H_l, l = 1..L
+  void* dzb(int l) const { return b.dz + (size_t)(l & 1) * A * elt(); } // buffer holding dZ_l
+};
+
+namespace {
+
+int validate(const pack_config* c) {
+  if (!c) return fail(PACK_EINVAL, "cfg is NULL");
+  if (c->K < 1 || c->K > 65535) return fail(PACK_EINVAL, "K=%d out of [1, 65535]", c->K);
+  if (c->d_in < 1 || c->d_in > (1 << 20)) return fail(PACK_EINVAL, "d_in=%d out of range", c->d_in);
+  if (c->L < 1 || c->L > 8) return fail(PACK_EINVAL, "L=%d out of [1, 8]", c->L);
+  if (c->B < 1 || c->B > 65536) return fail(PACK_EINVAL, "B=%d out of [1, 65536]", c->B);
+  if (c->task < 0 || c->task > 2) return fail(PACK_EINVAL, "unknown task %d", c->task);
+  if (c->precision != PACK_PREC_BF16 && c->precision != PACK_PREC_FP32)
+    return fail(PACK_EINVAL, "unknown precision %d", c->precision);
+  if (c->task == PACK_TASK_MULTI_CE) {
+    if (c->d_out < 2 || c->d_out > kMaxOut) return fail(PACK_EINVAL, "CE needs 2 <= d_out <= %d", kMaxOut);
+  } else if (c->d_out != 1) {
+    return fail(PACK_EINVAL, "MSE/BCE tasks need d_out == 1");
+  }
+  const int q = c->quantum ? c->quantum : 32;
+  if (q < 8 || q > 512 || q % 8) return fail(PACK_EINVAL, "quantum %d must be a multiple of 8 in [8, 512]", q);
+  if (!(c->beta1 >= 0 && c->beta1 < 1 && c->beta2 >= 0 && c->beta2 < 1 && c->eps > 0))
+    return fail(PACK_EINVAL, "AdamW constants out of range");
+  if (!c->members) {
+    if (c->width_lo < 1 || c->width_hi < c->width_lo || c->width_hi > 16384)
+      return fail(PACK_EINVAL, "width range [%d, %d] invalid", c->width_lo, c->width_hi);
+    if (!(c->dropout_lo >= 0 && c->dropout_hi >= c->dropout_lo && c->dropout_hi < 1))
+      return fail(PACK_EINVAL, "dropout range invalid");
+    if (!(c->lr_lo > 0 && c->lr_hi >= c->lr_lo) || !(c->wd_lo > 0 && c->wd_hi >= c->wd_lo))
+      return fail(PACK_EINVAL, "lr/wd ranges must be positive and ordered");
+  }
+  return PACK_OK;
+}
+
+void sample_members(pack_handle* h) {
+  const pack_config& c = h->cfg;
+  const Key key = stream_key(c.seed, kTagHparam);
+  for (int k = 0; k < c.K; ++k) {
+    const Words4 a = philox4x32_10((uint32_t)k, 0, 0, 0, key.k0, key.k1);
+    const Words4 b = philox4x32_10((uint32_t)k, 1, 0, 0, key.k0, key.k1);
+    Member& m = h->mem[k];
+    m.width = c.width_lo + (int)std::floor(u53(a.w0, a.w1) * (double)(c.width_hi - c.width_lo + 1));
+    m.dropout = c.dropout_lo + u53(a.w2, a.w3) * (c.dropout_hi - c.dropout_lo);
+    m.lr = log_uniform(c.lr_lo, c.lr_hi, u53(b.w0, b.w1));
+    m.wd = log_uniform(c.wd_lo, c.wd_hi, u53(b.w2, b.w3));
+  }
+}
+
+// Packed layout: per member, tensors W_1 [dp, Pin], b_1 [dp], W_l [dp, dp],
+// b_l [dp], W_out [d_out, dp], b_out [d_out]; every tensor starts on a
+// kChunk-element boundary so an AdamW chunk never mixes members or
+// weights with biases.  Padding rows/columns hold exact zeros forever: their
+// inputs or output gradients are zero, so their gradients and AdamW moments
+// stay zero.
+void plan_layout(pack_handle* h) {
+  const pack_config& c = h->cfg;
+  int64_t off = 0, aoff = 0;
+  h->chunk_tab.clear();
+  for (int k = 0; k < c.K; ++k) {
+    Member& m = h->mem[k];
+    m.dp = (int)round_up(m.width, h->q);
+    m.toff.assign(2 * c.L + 2, 0);
+    for (int l = 0; l <= c.L; ++l) {
+      const int64_t rows = l < c.L ? m.dp : c.d_out;
+      const int64_t cols = l == 0 ? h->Pin : m.dp;
+      for (int part = 0; part < 2; ++part) {
+        const int64_t n = part == 0 ? rows * cols : rows;
+        m.toff[2 * l + part] = off;
+        const int64_t nc = round_up(n, kChunk) / kChunk;
+        const uint32_t flag = (part == 1 && !c.decay_bias) ? 0x80000000u : 0u;
+        for (int64_t i = 0; i < nc; ++i) h->chunk_tab.push_back((uint32_t)k | flag);
+        off += nc * kChunk;
+      }
+    }
+    m.act_off = aoff;
+    aoff += (int64_t)h->Bp * m.dp;
+  }
+  h->P = off;
+  h->A = aoff;
+}
+
+// torch.nn.Linear default initialisation, U(-1/sqrt(fan_in), 1/sqrt(fan_in)),
+// drawn from the init stream: element e of tensor t of member k uses word
+// (e & 3) of block (e >> 2, e >> 34, t, k); u = (word >> 8) * 2^-24.
+void init_params(pack_handle* h) {
+  const pack_config& c = h->cfg;
+  h->theta_host.assign((size_t)h->P, 0.0f);
+  const Key key = stream_key(c.seed, kTagInit);
+  for (int k = 0; k < c.K; ++k) {
+    const Member& m = h->mem[k];
+    for (int l = 0; l <= c.L; ++l) {
+      const int rows = l < c.L ? m.width : c.d_out;
+      const int fan_in = l == 0 ? c.d_in : m.width;
+      const int64_t ld = l == 0 ? h->Pin : m.dp;
+      const double bound = 1.0 / std::sqrt((double)fan_in);
+      for (int part = 0; part < 2; ++part) {
+        const uint32_t tid = (uint32_t)(2 * l + part);
+        const int64_t n = part == 0 ? (int64_t)rows * fan_in : rows;
+        float* dst = h->theta_host.data() + m.toff[2 * l + part];
+        Words4 w{};
+        for (int64_t e = 0; e < n; ++e) {
+          if ((e & 3) == 0 || e == 0)
+            w = philox4x32_10((uint32_t)(e >> 2), (uint32_t)(e >> 34), tid, (uint32_t)k, key.k0, key.k1);
+          const uint32_t word = (e & 3) == 0 ? w.w0 : (e & 3) == 1 ? w.w1 : (e & 3) == 2 ? w.w2 : w.w3;
+          const double u = (double)(word >> 8) * (1.0 / 16777216.0);
+          const float val = (float)((2.0 * u - 1.0) * bound);
+          if (part == 0)
+            dst[(e / fan_in) * ld + (e % fan_in)] = val;
+          else
+            dst[e] = val;
+        }
+      }
+    }
+  }
+}
+
+// Dense <-> packed copies of one member's tensors.
+int64_t dense_count(const pack_handle* h, int k) {
+  const Member& m = h->mem[k];
+  const pack_config& c = h->cfg;
+  return (int64_t)m.width * c.d_in + m.width + (int64_t)(c.L - 1) * ((int64_t)m.width * m.width + m.width) +
+         (int64_t)c.d_out * m.width + c.d_out;
+}
+
+template <typename F>
+void for_each_dense(const pack_handle* h, int k, F f) {  // f(dense_index, packed_index)
+  const Member& m = h->mem[k];
+  const pack_config& c = h->cfg;
+  int64_t di = 0;
+  for (int l = 0; l <= c.L; ++l) {
+    const int rows = l < c.L ? m.width : c.d_out;
+    const int cols = l == 0 ? c.d_in : m.width;
+    const int64_t ld = l == 0 ? h->Pin : m.dp;
+    for (int r = 0; r < rows; ++r)
+      for (int cc = 0; cc < cols; ++cc) f(di++, m.toff[2 * l] + (int64_t)r * ld + cc);
+    for (int r = 0; r < rows; ++r) f(di++, m.toff[2 * l + 1] + r);
+  }
+}
+
+int64_t member_span_begin(const pack_handle* h, int k) { return h->mem[k].toff[0]; }
+int64_t member_span_end(const pack_handle* h, int k) {
+  return k + 1 < h->cfg.K ? h->mem[k + 1].toff[0] : h->P;
+}
+
+// Device-table sizes.
+struct Plan {
+  std::vector<GemmDesc> descs;
+  std::vector<Tile> tiles;
+  std::vector<ColTile> coltiles;
+  std::vector<Launch> fwd, dx, dw;
+};
+
+void add_tiles(Plan& p, Launch& ln, int d, int M, int N, int kdepth) {
+  for (int m0 = 0; m0 < M; m0 += kTileM)
+    for (int n0 = 0; n0 < N; n0 += kTileN) p.tiles.push_back(Tile{d, m0, n0, kdepth});
+  ln.ntiles = (int)p.tiles.size() - ln.tile0;
+}
+
+// Longest-processing-time order: deepest K loops first, so the ragged tail of
+// the launch is made of short tiles.
+void sort_launch(Plan& p, const Launch& ln) {
+  std::stable_sort(p.tiles.begin() + ln.tile0, p.tiles.begin() + ln.tile0 + ln.ntiles,
+                   [](const Tile& a, const Tile& b) { return a.kdepth > b.kdepth; });
+}
+
+Plan build_plan(const pack_handle* h, const Bufs& bf) {
+  Plan p;
+  const pack_config& c = h->cfg;
+  const size_t es = h->elt();
+  const void* wsrc = h->prec == Prec::BF16 ? (const void*)bf.shadow : (const void*)bf.theta;
+  auto Hl = [&](int l) -> void* { return bf.H + (size_t)(l - 1) * h->A * es; };
+  auto dzb = [&](int l) -> void* { return bf.dz + (size_t)(l & 1) * h->A * es; };
+  auto wptr = [&](int k, int l) -> const void* {  // weight of hidden layer l (1-based) for GEMM reads
+    return (const char*)wsrc + (size_t)h->mem[k].toff[2 * (l - 1)] * es;
+  };
+  auto act = [&](void* base, int k) -> void* { return (char*)base + (size_t)h->mem[k].act_off * es; };
+  for (int l = 1; l <= c.L; ++l) {
+    // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
+    Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0};
+    for (int k = 0; k < c.K; ++k) {
+      const Member& m = h->mem[k];
+      GemmDesc d{};
+      d.A = l == 1 ? nullptr : act(Hl(l - 1), k);
+      d.lda = m.dp;
+      d.B = wptr(k, l);
+      d.ldb = l == 1 ? h->Pin : m.dp;
+      d.C = act(Hl(l), k);
+      d.ldc = m.dp;
+      d.bias = bf.theta + m.toff[2 * (l - 1) + 1];
+      d.M = h->Bp;
+      d.N = m.dp;
+      d.Kd = l == 1 ? h->Pin : m.dp;
+      d.width = m.width;
+      d.member = k;
+      d.drop_t = m.t;
+      d.drop_s = (float)m.scale;
+      p.descs.push_back(d);
+      add_tiles(p, f, f.desc0 + k, h->Bp, m.dp, d.Kd);
+    }
+    sort_launch(p, f);
+    p.fwd.push_back(f);
+  }
+  for (int l = 1; l <= c.L; ++l) {
+    // weight gradient: dW_l^T[out, in] = sum_rows dZ_l[row, out] H_{l-1}[row, in]
+    Launch w{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0};
+    for (int k = 0; k < c.K; ++k) {
+      const Member& m = h->mem[k];
+      GemmDesc d{};
+      d.A = act(dzb(l), k);
+      d.lda = m.dp;
+      d.B = l == 1 ? nullptr : act(Hl(l - 1), k);
+      d.ldb = m.dp;
+      d.C = bf.grad + m.toff[2 * (l - 1)];
+      d.ldc = l == 1 ? h->Pin : m.dp;
+      d.M = m.dp;
+      d.N = l == 1 ? h->Pin : m.dp;
+      d.Kd = h->Bp;
+      d.member = k;
+      p.descs.push_back(d);
+      add_tiles(p, w, w.desc0 + k, d.M, d.N, d.Kd);
+    }
+    sort_launch(p, w);
+    p.dw.push_back(w);
+    // data gradient (l >= 2): dZ_{l-1} = (dZ_l W_l) * [H_{l-1} > 0] * s_k
+    Launch x{(int)p.descs.size(), 0, (int)p.tiles.size(), 0};
+    if (l >= 2) {
+      x.ndesc = c.K;
+      for (int k = 0; k < c.K; ++k) {
+        const Member& m = h->mem[k];
+        GemmDesc d{};
+        d.A = act(dzb(l), k);
+        d.lda = m.dp;
+        d.B = wptr(k, l);
+        d.ldb = m.dp;
+        d.C = act(dzb(l - 1), k);
+        d.Haux = act(Hl(l - 1), k);
+        d.ldc = m.dp;
+        d.M = h->Bp;
+        d.N = m.dp;
+        d.Kd = m.dp;
+        d.member = k;
+        d.drop_s = (float)m.scale;
+        p.descs.push_back(d);
+        add_tiles(p, x, x.desc0 + k, h->Bp, m.dp, d.Kd);
+      }
+      sort_launch(p, x);
+    }
+    p.dx.push_back(x);
+  }
+  for (int k = 0; k < c.K; ++k)
+    for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
+  return p;
+}
+
+struct Carve {
+  char* base;
+  size_t off = 0;
+  template <typename T>
+  T* take(size_t count) {
+    off = (size_t)round_up((int64_t)off, 256);
+    T* p = reinterpret_cast<T*>(reinterpret_cast<uintptr_t>(base) + off);
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+// Lays out the workspace.  With base == nullptr it only measures: the
+// pointers are then offsets from address 0 and are never dereferenced.
+size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
+  const pack_config& c = h->cfg;
+  Carve cv{base};
+  bf.theta = cv.take<float>(h->P);
+  bf.grad = cv.take<float>(h->P);
+  bf.m = cv.take<float>(h->P);
+  bf.v = cv.take<float>(h->P);
+  bf.shadow = h->prec == Prec::BF16 ? cv.take<uint16_t>(h->P) : nullptr;
+  bf.H = cv.take<char>((size_t)c.L * h->A * h->elt());
+  bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
+  bf.dY = cv.take<float>((size_t)c.K * h->Bp * c.d_out);
+  bf.rowloss = cv.take<float>((size_t)c.K * h->Bp);
+  bf.d_mem = cv.take<MemberDev>(c.K);
+  bf.d_chunks = cv.take<uint32_t>(h->chunk_tab.size());
+  bf.d_bias_off = cv.take<int64_t>((size_t)c.L * c.K);
+  Plan plan = build_plan(h, bf);
+  bf.d_descs = cv.take<GemmDesc>(plan.descs.size());
+  bf.d_tiles = cv.take<Tile>(plan.tiles.size());
+  bf.d_coltiles = cv.take<ColTile>(plan.coltiles.size());
+  if (plan_out) *plan_out = std::move(plan);
+  return (size_t)round_up((int64_t)cv.off, 256);
+}
+
+int check_member(const pack_handle* h, int32_t k) {
+  if (!h) return fail(PACK_EINVAL, "handle is NULL");
+  if (k < 0 || k >= h->cfg.K) return fail(PACK_EINVAL, "member %d out of [0, %d)", k, h->cfg.K);
+  return PACK_OK;
+}
+
+uint32_t as_u32(uint64_t x) { return (uint32_t)(x & 0xFFFFFFFFu); }
+
+GemmArgs base_args(const pack_handle* h) {
+  GemmArgs a{};
+  a.descs = h->b.d_descs;
+  a.tiles = h->b.d_tiles;
+  const Key kd = stream_key(h->cfg.seed, kTagDropout);
+  a.key0 = kd.k0;
+  a.key1 = kd.k1;
+  a.d_in = h->cfg.d_in;
+  a.idx_stride = h->cfg.B;
+  return a;
+}
+
+GemmArgs for_launch(GemmArgs a, const Launch& ln) {
+  a.tiles += ln.tile0;
+  a.ntiles = ln.ntiles;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pack_last_error(void) { return g_err.c_str(); }
+
+int pack_init(const pack_config* cfg, pack_handle** out) {
+  if (!out) return fail(PACK_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = validate(cfg);
+  if (rc) return rc;
+  pack_handle* h = new (std::nothrow) pack_handle();
+  if (!h) return fail(PACK_EINVAL, "out of host memory");
+  h->cfg = *cfg;
+  h->cfg.members = nullptr;
+  h->prec = cfg->precision == PACK_PREC_BF16 ? Prec::BF16 : Prec::FP32;
+  h->task = (Task)cfg->task;
+  h->q = cfg->quantum ? cfg->quantum : 32;
+  h->Bp = (int)round_up(cfg->B, kRowAlign);
+  h->Pin = (int)round_up(cfg->d_in, 8);
+  h->mem.resize(cfg->K);
+  if (cfg->members) {
+    for (int k = 0; k < cfg->K; ++k) {
+      const pack_member_hp& e = cfg->members[k];
+      if (e.width < 1 || e.width > 16384 || !(e.dropout >= 0 && e.dropout < 1) || !(e.lr > 0) ||
+          !(e.wd >= 0)) {
+        delete h;
+        return fail(PACK_EINVAL, "explicit hyperparameters of member %d out of range", k);
+      }
+      h->mem[k].width = e.width;
+      h->mem[k].dropout = e.dropout;
+      h->mem[k].lr = e.lr;
+      h->mem[k].wd = e.wd;
+    }
+  } else {
+    sample_members(h);
+  }
+  for (Member& m : h->mem) {
+    m.t = (uint32_t)std::min(std::floor(m.dropout * 4294967296.0), 4294967295.0);
+    m.scale = 1.0 / (1.0 - m.dropout);
+  }
+  plan_layout(h);
+  init_params(h);
+  *out = h;
+  g_err.clear();
+  return PACK_OK;
+}
+
+int pack_destroy(pack_handle* h) {
+  delete h;
+  return PACK_OK;
+}
+
+int pack_get_hparams(const pack_handle* h, pack_member_hp* out) {
+  if (!h || !out) return fail(PACK_EINVAL, "NULL argument");
+  for (int k = 0; k < h->cfg.K; ++k) {
+    const Member& m = h->mem[k];
+    out[k] = pack_member_hp{m.width, m.dp, m.t, 0, m.dropout, m.lr, m.wd, m.scale};
+  }
+  return PACK_OK;
+}
+
+int pack_workspace_size(const pack_handle* h, size_t* bytes) {
+  if (!h || !bytes) return fail(PACK_EINVAL, "NULL argument");
+  Bufs tmp;
+  *bytes = carve(h, nullptr, tmp, nullptr);
+  return PACK_OK;
+}
+
+int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream) {
+  if (!h || !workspace) return fail(PACK_EINVAL, "NULL argument");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256) return fail(PACK_EINVAL, "workspace must be 256-byte aligned");
+  size_t need = 0;
+  pack_workspace_size(h, &need);
+  if (bytes < need) return fail(PACK_EINVAL, "workspace has %zu bytes, %zu needed", bytes, need);
+  Plan plan;
+  carve(h, static_cast<char*>(workspace), h->b, &plan);
+  HIP_TRY(hipMemsetAsync(workspace, 0, need, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.theta, h->theta_host.data(), h->P * sizeof(float), hipMemcpyHostToDevice, stream));
+  std::vector<MemberDev> md(h->cfg.K);
+  std::vector<int64_t> boff((size_t)h->cfg.L * h->cfg.K);
+  for (int k = 0; k < h->cfg.K; ++k) {
+    const Member& m = h->mem[k];
+    md[k] = MemberDev{m.width, m.dp, m.t, (float)m.scale, (float)m.lr, (float)m.wd, m.act_off,
+                      m.toff[2 * h->cfg.L], m.toff[2 * h->cfg.L + 1], m.toff[2 * h->cfg.L - 1]};
+    for (int l = 1; l <= h->cfg.L; ++l) boff[(size_t)(l - 1) * h->cfg.K + k] = m.toff[2 * (l - 1) + 1];
+  }
+  HIP_TRY(hipMemcpyAsync(h->b.d_mem, md.data(), md.size() * sizeof(MemberDev), hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.d_chunks, h->chunk_tab.data(), h->chunk_tab.size() * 4, hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.d_bias_off, boff.data(), boff.size() * 8, hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.d_descs, plan.descs.data(), plan.descs.size() * sizeof(GemmDesc), hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.d_tiles, plan.tiles.data(), plan.tiles.size() * sizeof(Tile), hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.d_coltiles, plan.coltiles.data(), plan.coltiles.size() * sizeof(ColTile), hipMemcpyHostToDevice, stream));
+  if (h->prec == Prec::BF16) HIP_TRY(launch_to_shadow(h->b.theta, h->b.shadow, h->P, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  h->fwd = plan.fwd;
+  h->dx = plan.dx;
+  h->dw = plan.dw;
+  h->ncoltiles = (int)plan.coltiles.size();
+  h->t = 0;
+  h->bound = true;
+  return PACK_OK;
+}
+
+int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, const int32_t* idx,
+                    uint64_t step, float* loss_out, hipStream_t stream) {
+  if (!h) return fail(PACK_EINVAL, "handle is NULL");
+  if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
+  if (!X || !y || !idx || !loss_out) return fail(PACK_EINVAL, "NULL device pointer");
+  if (N < 1) return fail(PACK_EINVAL, "N=%lld must be positive", (long long)N);
+  if (step != h->t + 1) return fail(PACK_ESTATE, "step %llu given, %llu expected", (unsigned long long)step,
+                                    (unsigned long long)(h->t + 1));
+  const pack_config& c = h->cfg;
+  GemmArgs a = base_args(h);
+  a.X = X;
+  a.idx = idx;
+  a.rows_valid = c.B;
+  a.step = as_u32(step);
+  for (int l = 1; l <= c.L; ++l) {
+    GemmArgs al = for_launch(a, h->fwd[l - 1]);
+    al.layer = l;
+    HIP_TRY(launch_gemm(h->prec, l == 1 ? OP_XGK : OP_KMAJ, OP_KMAJ, EPI_FWD, al, stream));
+  }
+  HIP_TRY(launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, y,
+                          idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, stream));
+  HIP_TRY(launch_loss_reduce(h->b.rowloss, h->b.dY, h->b.d_mem, c.K, h->Bp, c.B, c.d_out, h->b.grad, loss_out, stream));
+  HIP_TRY(launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp, c.d_out,
+                          h->b.dY, h->dzb(c.L), h->b.grad, stream));
+  for (int l = c.L; l >= 1; --l) {
+    GemmArgs aw = for_launch(a, h->dw[l - 1]);
+    aw.layer = l;
+    HIP_TRY(launch_gemm(h->prec, OP_RMAJ, l == 1 ? OP_XGR : OP_RMAJ, EPI_DW, aw, stream));
+    if (l < c.L)
+      HIP_TRY(launch_colsum(h->prec, h->dzb(l), h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp,
+                            h->b.d_bias_off + (size_t)(l - 1) * c.K, h->b.grad, stream));
+    if (l > 1) {
+      GemmArgs ax = for_launch(a, h->dx[l - 1]);
+      ax.layer = l;
+      HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_RMAJ, EPI_DX, ax, stream));
+    }
+  }
+  const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
+  const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
+  HIP_TRY(launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, h->b.shadow, h->b.d_chunks, h->b.d_mem,
+                       (int64_t)h->chunk_tab.size(), (float)bc1, (float)std::sqrt(bc2), (float)c.beta1,
+                       (float)c.beta2, (float)c.eps, stream));
+  h->t = step;
+  return PACK_OK;
+}
+
+int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t Nv, float* pred_out,
+                      double* score_out, hipStream_t stream) {
+  if (!h) return fail(PACK_EINVAL, "handle is NULL");
+  if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
+  if (!Xv || !yv || !pred_out || !score_out) return fail(PACK_EINVAL, "NULL device pointer");
+  if (Nv < 1) return fail(PACK_EINVAL, "Nv=%lld must be positive", (long long)Nv);
+  const pack_config& c = h->cfg;
+  GemmArgs a = base_args(h);
+  a.X = Xv;
+  a.idx = nullptr;
+  for (int64_t r0 = 0; r0 < Nv; r0 += h->Bp) {
+    a.row_base = r0;
+    a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
+    for (int l = 1; l <= c.L; ++l) {
+      GemmArgs al = for_launch(a, h->fwd[l - 1]);
+      al.layer = l;
+      HIP_TRY(launch_gemm(h->prec, l == 1 ? OP_XGK : OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
+    }
+    HIP_TRY(launch_head_fwd(h->prec, h->task, true, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, yv,
+                            nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, stream));
+  }
+  HIP_TRY(launch_eval_score(h->task, pred_out, yv, c.K, Nv, score_out, stream));
+  return PACK_OK;
+}
+
+int pack_select_workspace_size(int32_t C, int64_t Nv, size_t* bytes) {
+  if (!bytes || C < 1 || Nv < 1) return fail(PACK_EINVAL, "C and Nv must be positive");
+  const size_t nblk = (size_t)select_blocks(Nv);
+  *bytes = (size_t)round_up(Nv * 8, 256) + (size_t)round_up((int64_t)(C * nblk * 8), 256) + 256 + 256;
+  return PACK_OK;
+}
+
+int pack_select(pack_handle* h, const float* cand, const void* yv, int32_t C, int64_t Nv, int32_t m_ens,
+                void* work, size_t work_bytes, int32_t* sel_out, int32_t* n_sel_out, double* score_out,
+                hipStream_t stream) {
+  if (!h) return fail(PACK_EINVAL, "handle is NULL");
+  if (!cand || !yv || !work || !n_sel_out || !score_out || (m_ens > 0 && !sel_out))
+    return fail(PACK_EINVAL, "NULL device pointer");
+  if (C < 1 || C > 65535 || Nv < 1 || m_ens < 0)
+    return fail(PACK_EINVAL, "need 1 <= C <= 65535, Nv >= 1 and m_ens >= 0");
+  size_t need = 0;
+  pack_select_workspace_size(C, Nv, &need);
+  if (work_bytes < need) return fail(PACK_EINVAL, "select workspace has %zu bytes, %zu needed", work_bytes, need);
+  if (reinterpret_cast<uintptr_t>(work) % 256) return fail(PACK_EINVAL, "select workspace must be 256-byte aligned");
+  const int nblk = select_blocks(Nv);
+  char* w = static_cast<char*>(work);
+  double* sum = reinterpret_cast<double*>(w);
+  double* partial = reinterpret_cast<double*>(w + round_up(Nv * 8, 256));
+  int32_t* state = reinterpret_cast<int32_t*>(w + round_up(Nv * 8, 256) + round_up((int64_t)C * nblk * 8, 256));
+  double* best = reinterpret_cast<double*>(reinterpret_cast<char*>(state) + 256);
+  HIP_TRY(launch_select_init(sum, Nv, state, best, n_sel_out, score_out, stream));
+  const int iters = std::min(m_ens, C);
+  for (int it = 0; it < iters; ++it)
+    HIP_TRY(launch_select_iter(h->task, cand, yv, C, Nv, m_ens, sum, partial, nblk, state, best, sel_out, stream));
+  HIP_TRY(launch_select_final(state, best, n_sel_out, score_out, stream));
+  return PACK_OK;
+}
+
+int pack_member_param_count(const pack_handle* h, int32_t member, int64_t* count) {
+  int rc = check_member(h, member);
+  if (rc) return rc;
+  if (!count) return fail(PACK_EINVAL, "count is NULL");
+  *count = dense_count(h, member);
+  return PACK_OK;
+}
+
+namespace {
+int copy_member(pack_handle* h, int k, const float* dev_base, float* host_out) {
+  const int64_t b = member_span_begin(h, k), e = member_span_end(h, k);
+  std::vector<float> tmp((size_t)(e - b));
+  if (dev_base) {
+    HIP_TRY(hipDeviceSynchronize());
+    HIP_TRY(hipMemcpy(tmp.data(), dev_base + b, tmp.size() * 4, hipMemcpyDeviceToHost));
+  } else {
+    std::memcpy(tmp.data(), h->theta_host.data() + b, tmp.size() * 4);
+  }
+  for_each_dense(h, k, [&](int64_t di, int64_t pi) { host_out[di] = tmp[(size_t)(pi - b)]; });
+  return PACK_OK;
+}
+}  // namespace
+
+int pack_get_params(pack_handle* h, int32_t member, float* host_out) {
+  int rc = check_member(h, member);
+  if (rc) return rc;
+  if (!host_out) return fail(PACK_EINVAL, "host_out is NULL");
+  return copy_member(h, member, h->bound ? h->b.theta : nullptr, host_out);
+}
+
+int pack_set_params(pack_handle* h, int32_t member, const float* host_in) {
+  int rc = check_member(h, member);
+  if (rc) return rc;
+  if (!host_in) return fail(PACK_EINVAL, "host_in is NULL");
+  for_each_dense(h, member, [&](int64_t di, int64_t pi) { h->theta_host[(size_t)pi] = host_in[di]; });
+  if (h->bound) {
+    const int64_t b = member_span_begin(h, member), e = member_span_end(h, member);
+    HIP_TRY(hipDeviceSynchronize());
+    HIP_TRY(hipMemcpy(h->b.theta + b, h->theta_host.data() + b, (size_t)(e - b) * 4, hipMemcpyHostToDevice));
+    if (h->prec == Prec::BF16) HIP_TRY(launch_to_shadow(h->b.theta + b, h->b.shadow + b, e - b, 0));
+    HIP_TRY(hipDeviceSynchronize());
+  }
+  return PACK_OK;
+}
+
+int pack_get_grads(pack_handle* h, int32_t member, float* host_out) {
+  int rc = check_member(h, member);
+  if (rc) return rc;
+  if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
+  if (!host_out) return fail(PACK_EINVAL, "host_out is NULL");
+  return copy_member(h, member, h->b.grad, host_out);
+}
+
+int pack_get_moments(pack_handle* h, int32_t member, float* m_out, float* v_out) {
+  int rc = check_member(h, member);
+  if (rc) return rc;
+  if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
+  if (!m_out || !v_out) return fail(PACK_EINVAL, "NULL output");
+  rc = copy_member(h, member, h->b.m, m_out);
+  if (rc) return rc;
+  return copy_member(h, member, h->b.v, v_out);
+}
+
+int pack_debug_dropout_mask(pack_handle* h, uint64_t step, int32_t layer, int32_t member, uint8_t* dev_out,
+                            hipStream_t stream) {
+  int rc = check_member(h, member);
+  if (rc) return rc;
+  if (layer < 1 || layer > h->cfg.L) return fail(PACK_EINVAL, "layer %d out of [1, %d]", layer, h->cfg.L);
+  if (!dev_out) return fail(PACK_EINVAL, "dev_out is NULL");
+  const Key kd = stream_key(h->cfg.seed, kTagDropout);
+  HIP_TRY(launch_dropout_mask(kd.k0, kd.k1, as_u32(step), layer, member, h->mem[member].t, h->cfg.B,
+                              h->mem[member].width, dev_out, stream));
+  return PACK_OK;
+}
+
+int pack_debug_activation(pack_handle* h, int32_t layer, int32_t member, float* host_out) {
+  int rc = check_member(h, member);
+  if (rc) return rc;
+  if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
+  if (layer < 1 || layer > h->cfg.L) return fail(PACK_EINVAL, "layer %d out of [1, %d]", layer, h->cfg.L);
+  if (!host_out) return fail(PACK_EINVAL, "host_out is NULL");
+  const Member& m = h->mem[member];
+  const size_t n = (size_t)h->Bp * m.dp;
+  std::vector<uint8_t> tmp(n * h->elt());
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(tmp.data(), (char*)h->Hl(layer) + (size_t)m.act_off * h->elt(), tmp.size(), hipMemcpyDeviceToHost));
+  for (int r = 0; r < h->cfg.B; ++r)
+    for (int c = 0; c < m.width; ++c) {
+      const size_t i = (size_t)r * m.dp + c;
+      float val;
+      if (h->prec == Prec::BF16) {
+        uint16_t b16;
+        std::memcpy(&b16, tmp.data() + 2 * i, 2);
+        const uint32_t bits = (uint32_t)b16 << 16;
+        std::memcpy(&val, &bits, 4);
+      } else {
+        std::memcpy(&val, tmp.data() + 4 * i, 4);
+      }
+      host_out[(size_t)r * m.width + c] = val;
+    }
+  return PACK_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,115 @@
+// Internal declarations shared by the host runtime and the gfx950 kernels of
+// the packed-MLP library: device-side descriptors, launch arguments and the
+// kernel launchers.  Nothing here is part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tabpack {
+
+constexpr int kChunk = 256;        // AdamW chunk: elements of one member, one kind (weight / bias)
+constexpr int kMaxOut = 16;        // largest head width d_out supported by the head kernels
+constexpr int kRowAlign = 256;     // base-batch rows are padded to a multiple of this (largest GEMM row tile)
+constexpr uint32_t kTagDropout = 3;
+
+enum class Prec : int { BF16 = 0, FP32 = 1 };
+enum class Task : int { REG = 0, BIN = 1, MULTI = 2 };
+
+// Operand access kinds of the grouped GEMM.  For an operand tile of R rows
+// (the GEMM's M or N index) by BK depth (its K index):
+//   KMAJ    element (r, k) at P[r * ld + k]         -- depth contiguous
+//   RMAJ    element (r, k) at P[k * ld + r]         -- rows contiguous (transposed on load)
+//   XGK     element (r, k) = X[row(r) * d_in + k]   -- gathered fp32 feature rows, depth contiguous
+//   XGR     element (r, k) = X[row(k) * d_in + r]   -- gathered fp32 feature rows, transposed on load
+// with row(i) = idx[member * idx_stride + i] or row_base + i when idx is null.
+enum OpKind : int { OP_KMAJ = 0, OP_RMAJ = 1, OP_XGK = 2, OP_XGR = 3 };
+enum EpiKind : int { EPI_FWD = 0, EPI_FWD_EVAL = 1, EPI_DX = 2, EPI_DW = 3 };
+
+// One member's GEMM problem C[m, n] = sum_k A(m, k) B(n, k) in one grouped launch.
+struct GemmDesc {
+  const void* A;
+  const void* B;
+  void* C;
+  const float* bias;   // EPI_FWD*: [N] fp32
+  const void* Haux;    // EPI_DX: activation H_{l-1}, same layout as C
+  int64_t lda, ldb, ldc;
+  int32_t M, N, Kd;    // A rows in bounds (< M), B rows in bounds (< N), depth (< Kd)
+  int32_t width;       // EPI_FWD*: true width; columns >= width are written as 0
+  int32_t member;
+  uint32_t drop_t;     // t_k
+  float drop_s;        // s_k
+  int32_t pad_;
+};
+
+struct Tile {
+  int32_t desc;
+  int32_t m0;
+  int32_t n0;
+  int32_t kdepth;      // planner's cost key (depth of this tile's K loop)
+};
+
+struct GemmArgs {
+  const GemmDesc* descs;
+  const Tile* tiles;
+  int32_t ntiles;
+  int32_t layer;        // 1-based hidden layer (dropout counter)
+  const float* X;       // XGK / XGR source
+  const int32_t* idx;   // per-member row lists, or null for contiguous rows
+  int64_t row_base;     // first row when idx is null
+  int32_t d_in;
+  int32_t idx_stride;   // B
+  int32_t rows_valid;   // batch rows that exist (B in training, chunk rows in eval)
+  uint32_t key0, key1;  // dropout stream key
+  uint32_t step;        // dropout counter word
+};
+
+// Per-member table used by the small kernels.
+struct MemberDev {
+  int32_t width, dp;
+  uint32_t drop_t;
+  float drop_s;
+  float lr, wd;
+  int64_t act_off;          // member offset inside one activation buffer (elements)
+  int64_t w_out_off, b_out_off, b_last_off;  // head weight, head bias, last hidden bias (elements of theta)
+};
+
+struct ColTile {            // (member, first column) work item of the column-sweep kernels
+  int32_t member;
+  int32_t c0;
+};
+
+// Launchers (kernels_gemm.hip).
+hipError_t launch_gemm(Prec prec, OpKind a, OpKind b, EpiKind e, const GemmArgs& args, hipStream_t s);
+
+// Launchers (kernels_aux.hip).
+hipError_t launch_head_fwd(Prec prec, Task task, bool eval, const void* H, const float* theta,
+                           const MemberDev* mem, int K, int Bp, int d_out, const void* y,
+                           const int32_t* idx, int B, int rows_valid, int64_t row_base, int64_t Nv,
+                           float* dY, float* rowloss, float* pred, hipStream_t s);
+hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const MemberDev* mem, int K,
+                              int Bp, int B, int d_out, float* grad, float* loss_out, hipStream_t s);
+hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const MemberDev* mem,
+                           const ColTile* tiles, int ntiles, int Bp, int d_out, const float* dY,
+                           void* dZ, float* grad, hipStream_t s);
+hipError_t launch_colsum(Prec prec, const void* dZ, const MemberDev* mem, const ColTile* tiles,
+                         int ntiles, int Bp, const int64_t* bias_off, float* grad, hipStream_t s);
+hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, float* v,
+                        uint16_t* shadow, const uint32_t* chunk_tab, const MemberDev* mem,
+                        int64_t nchunks, float bc1, float bc2_sqrt, float beta1, float beta2,
+                        float eps, hipStream_t s);
+hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hipStream_t s);
+hipError_t launch_eval_score(Task task, const float* pred, const void* yv, int K, int64_t Nv,
+                             double* score_out, hipStream_t s);
+hipError_t launch_dropout_mask(uint32_t key0, uint32_t key1, uint32_t step, int layer, int member,
+                               uint32_t t, int B, int width, uint8_t* out, hipStream_t s);
+hipError_t launch_select_iter(Task task, const float* cand, const void* yv, int C, int64_t Nv,
+                              int m_ens, double* sum, double* partial, int nblk, int32_t* state,
+                              double* best, int32_t* sel_out, hipStream_t s);
+hipError_t launch_select_init(double* sum, int64_t Nv, int32_t* state, double* best,
+                              int32_t* n_sel_out, double* score_out, hipStream_t s);
+hipError_t launch_select_final(const int32_t* state, const double* best, int32_t* n_sel_out,
+                               double* score_out, hipStream_t s);
+int select_blocks(int64_t Nv);
+
+}  // namespace tabpack

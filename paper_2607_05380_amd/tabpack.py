@@ -1,0 +1,269 @@
+"""Thin Python binding of libtabpack.so (argument marshalling only).
+
+Every step of the packed training step, evaluation and selection runs in the
+library's HIP kernels; PyTorch only provides device memory (the workspace and
+the caller's tensors) and the current HIP stream.  Importing works without a
+GPU; the library is loaded on first use and a missing library is an error
+(there is no fallback path).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtabpack.so")
+
+PACK_OK = 0
+TASKS = {"reg": 0, "bin": 1, "multi": 2}
+PRECISIONS = {"bf16": 0, "fp32": 1}
+
+SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "pack_workspace_size",
+           "pack_bind", "pack_train_step", "pack_eval_members", "pack_select_workspace_size",
+           "pack_select", "pack_member_param_count", "pack_get_params", "pack_set_params",
+           "pack_get_grads", "pack_get_moments", "pack_debug_dropout_mask", "pack_debug_activation"]
+
+
+class MemberHP(ctypes.Structure):
+    _fields_ = [("width", ctypes.c_int32), ("padded_width", ctypes.c_int32),
+                ("drop_threshold", ctypes.c_uint32), ("reserved", ctypes.c_int32),
+                ("dropout", ctypes.c_double), ("lr", ctypes.c_double), ("wd", ctypes.c_double),
+                ("scale", ctypes.c_double)]
+
+
+class PackConfig(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("d_in", ctypes.c_int32), ("d_out", ctypes.c_int32),
+                ("L", ctypes.c_int32), ("B", ctypes.c_int32), ("task", ctypes.c_int32),
+                ("precision", ctypes.c_int32), ("width_lo", ctypes.c_int32),
+                ("width_hi", ctypes.c_int32), ("quantum", ctypes.c_int32),
+                ("decay_bias", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("dropout_lo", ctypes.c_double), ("dropout_hi", ctypes.c_double),
+                ("lr_lo", ctypes.c_double), ("lr_hi", ctypes.c_double),
+                ("wd_lo", ctypes.c_double), ("wd_hi", ctypes.c_double),
+                ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
+                ("seed", ctypes.c_uint64), ("members", ctypes.POINTER(MemberHP))]
+
+
+class PackError(RuntimeError):
+    pass
+
+
+_LIB = None
+
+
+def load_library(path=LIB_PATH):
+    """Load libtabpack.so (once) and declare the C signatures."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(path):
+        raise PackError(f"{path} is missing: build it first (python -m paper_2607_05380_amd.build)")
+    L = ctypes.CDLL(path)
+    vp, i32, i64, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
+    H = vp
+    sig = {
+        "pack_last_error": ([], ctypes.c_char_p),
+        "pack_init": ([ctypes.POINTER(PackConfig), ctypes.POINTER(vp)], ctypes.c_int),
+        "pack_destroy": ([H], ctypes.c_int),
+        "pack_get_hparams": ([H, ctypes.POINTER(MemberHP)], ctypes.c_int),
+        "pack_workspace_size": ([H, ctypes.POINTER(sz)], ctypes.c_int),
+        "pack_bind": ([H, vp, sz, vp], ctypes.c_int),
+        "pack_train_step": ([H, vp, vp, i64, vp, u64, vp, vp], ctypes.c_int),
+        "pack_eval_members": ([H, vp, vp, i64, vp, vp, vp], ctypes.c_int),
+        "pack_select_workspace_size": ([i32, i64, ctypes.POINTER(sz)], ctypes.c_int),
+        "pack_select": ([H, vp, vp, i32, i64, i32, vp, sz, vp, vp, vp, vp], ctypes.c_int),
+        "pack_member_param_count": ([H, i32, ctypes.POINTER(i64)], ctypes.c_int),
+        "pack_get_params": ([H, i32, vp], ctypes.c_int),
+        "pack_set_params": ([H, i32, vp], ctypes.c_int),
+        "pack_get_grads": ([H, i32, vp], ctypes.c_int),
+        "pack_get_moments": ([H, i32, vp, vp], ctypes.c_int),
+        "pack_debug_dropout_mask": ([H, u64, i32, i32, vp, vp], ctypes.c_int),
+        "pack_debug_activation": ([H, i32, i32, vp], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    _LIB = L
+    return L
+
+
+def _check(rc):
+    if rc != PACK_OK:
+        raise PackError(f"tabpack error {rc}: {load_library().pack_last_error().decode()}")
+
+
+def make_config(cfg, members=None):
+    """PackConfig from a workload dict (see ``configs``); members: optional list of
+    dicts {width, dropout, lr, wd} overriding the sampled hyperparameters."""
+    c = PackConfig()
+    for f in ("K", "d_in", "d_out", "L", "B", "width_lo", "width_hi"):
+        setattr(c, f, int(cfg.get(f, 0)))
+    c.task = TASKS[cfg["task"]]
+    c.precision = PRECISIONS[cfg.get("precision", "bf16")]
+    c.quantum = int(cfg.get("quantum", 0))
+    c.decay_bias = int(cfg.get("decay_bias", 1))
+    for f in ("dropout_lo", "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi"):
+        setattr(c, f, float(cfg.get(f, 0.0)))
+    c.beta1 = float(cfg.get("beta1", 0.9))
+    c.beta2 = float(cfg.get("beta2", 0.999))
+    c.eps = float(cfg.get("eps", 1e-8))
+    c.seed = int(cfg["seed"])
+    keep = None
+    if members is not None:
+        keep = (MemberHP * len(members))()
+        for i, m in enumerate(members):
+            keep[i].width = int(m["width"])
+            keep[i].dropout = float(m["dropout"])
+            keep[i].lr = float(m["lr"])
+            keep[i].wd = float(m["wd"])
+        c.members = ctypes.cast(keep, ctypes.POINTER(MemberHP))
+    return c, keep
+
+
+def _stream(stream=None):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Pack:
+    """A packed ensemble of K MLPs living in one library handle."""
+
+    def __init__(self, cfg, members=None):
+        self.lib = load_library()
+        self.cfg = dict(cfg)
+        c, keep = make_config(cfg, members)
+        h = ctypes.c_void_p()
+        _check(self.lib.pack_init(ctypes.byref(c), ctypes.byref(h)))
+        del keep
+        self.h = h
+        self.K, self.L, self.B = c.K, c.L, c.B
+        self.d_in, self.d_out = c.d_in, c.d_out
+        self.workspace = None
+        self._select_ws = None
+
+    def __del__(self):
+        h = getattr(self, "h", None)
+        if h is not None and h.value:
+            self.lib.pack_destroy(h)
+            self.h = None
+
+    # ------------------------------------------------------------ set-up
+    def hparams(self):
+        arr = (MemberHP * self.K)()
+        _check(self.lib.pack_get_hparams(self.h, arr))
+        return [dict(width=a.width, padded_width=a.padded_width, t=a.drop_threshold,
+                     dropout=a.dropout, lr=a.lr, wd=a.wd, s=a.scale) for a in arr]
+
+    def workspace_bytes(self):
+        n = ctypes.c_size_t()
+        _check(self.lib.pack_workspace_size(self.h, ctypes.byref(n)))
+        return n.value
+
+    def bind(self, device="cuda"):
+        import torch
+        self.workspace = torch.empty(self.workspace_bytes(), dtype=torch.uint8, device=device)
+        _check(self.lib.pack_bind(self.h, ctypes.c_void_p(self.workspace.data_ptr()),
+                                  self.workspace.numel(), _stream()))
+        return self
+
+    # ------------------------------------------------------------ hot path
+    def train_step(self, X, y, idx, step, loss_out=None):
+        """X fp32 [N, d_in], y fp32/int32 [N], idx int32 [K, B] (device tensors)."""
+        import torch
+        assert X.is_cuda and X.dtype == torch.float32 and X.is_contiguous() and X.shape[1] == self.d_in
+        assert idx.dtype == torch.int32 and idx.is_contiguous() and tuple(idx.shape) == (self.K, self.B)
+        assert y.is_contiguous() and y.shape[0] == X.shape[0]
+        if loss_out is None:
+            loss_out = torch.empty(self.K, dtype=torch.float32, device=X.device)
+        _check(self.lib.pack_train_step(self.h, X.data_ptr(), y.data_ptr(), X.shape[0], idx.data_ptr(),
+                                        int(step), loss_out.data_ptr(), _stream()))
+        return loss_out
+
+    def eval_members(self, Xv, yv):
+        import torch
+        assert Xv.is_cuda and Xv.dtype == torch.float32 and Xv.is_contiguous() and Xv.shape[1] == self.d_in
+        Nv = Xv.shape[0]
+        pred = torch.empty((self.K, Nv), dtype=torch.float32, device=Xv.device)
+        score = torch.empty(self.K, dtype=torch.float64, device=Xv.device)
+        _check(self.lib.pack_eval_members(self.h, Xv.data_ptr(), yv.data_ptr(), Nv, pred.data_ptr(),
+                                          score.data_ptr(), _stream()))
+        return pred, score
+
+    def select(self, cand, yv, m_ens):
+        """Greedy selection over cand fp32 [C, Nv]; returns (picks, score) on the host."""
+        import torch
+        C, Nv = cand.shape
+        n = ctypes.c_size_t()
+        _check(self.lib.pack_select_workspace_size(C, Nv, ctypes.byref(n)))
+        if self._select_ws is None or self._select_ws.numel() < n.value:
+            self._select_ws = torch.empty(n.value, dtype=torch.uint8, device=cand.device)
+        sel = torch.full((max(m_ens, 1),), -1, dtype=torch.int32, device=cand.device)
+        nsel = torch.zeros(1, dtype=torch.int32, device=cand.device)
+        score = torch.zeros(1, dtype=torch.float64, device=cand.device)
+        _check(self.lib.pack_select(self.h, cand.data_ptr(), yv.data_ptr(), C, Nv, m_ens,
+                                    self._select_ws.data_ptr(), self._select_ws.numel(), sel.data_ptr(),
+                                    nsel.data_ptr(), score.data_ptr(), _stream()))
+        torch.cuda.current_stream().synchronize()
+        k = int(nsel.item())
+        return [int(x) for x in sel[:k].cpu()], float(score.item())
+
+    # ------------------------------------------------------------ state access
+    def param_count(self, k):
+        n = ctypes.c_int64()
+        _check(self.lib.pack_member_param_count(self.h, k, ctypes.byref(n)))
+        return n.value
+
+    def _dense(self, fn, k):
+        out = np.empty(self.param_count(k), dtype=np.float32)
+        _check(fn(self.h, k, out.ctypes.data))
+        return out
+
+    def get_params(self, k):
+        return self.split(k, self._dense(self.lib.pack_get_params, k))
+
+    def get_grads(self, k):
+        return self.split(k, self._dense(self.lib.pack_get_grads, k))
+
+    def get_moments(self, k):
+        n = self.param_count(k)
+        m = np.empty(n, dtype=np.float32)
+        v = np.empty(n, dtype=np.float32)
+        _check(self.lib.pack_get_moments(self.h, k, m.ctypes.data, v.ctypes.data))
+        return self.split(k, m), self.split(k, v)
+
+    def set_params(self, k, params):
+        flat = np.concatenate([np.concatenate([np.asarray(W, np.float32).ravel(), np.asarray(b, np.float32)])
+                               for W, b in params])
+        assert flat.size == self.param_count(k)
+        flat = np.ascontiguousarray(flat)
+        _check(self.lib.pack_set_params(self.h, k, flat.ctypes.data))
+
+    def split(self, k, flat):
+        """Dense member vector -> [(W [out, in], b [out]), ...] for the L blocks and the head."""
+        w = self.hparams()[k]["width"] if not hasattr(self, "_widths") else self._widths[k]
+        dims = [self.d_in] + [w] * self.L + [self.d_out]
+        out, o = [], 0
+        for i in range(self.L + 1):
+            n_in, n_out = dims[i], dims[i + 1]
+            W = flat[o:o + n_in * n_out].reshape(n_out, n_in)
+            o += n_in * n_out
+            b = flat[o:o + n_out]
+            o += n_out
+            out.append((W, b))
+        return out
+
+    def debug_dropout_mask(self, step, layer, k):
+        import torch
+        w = self.hparams()[k]["width"]
+        out = torch.empty((self.B, w), dtype=torch.uint8, device="cuda")
+        _check(self.lib.pack_debug_dropout_mask(self.h, int(step), layer, k, out.data_ptr(), _stream()))
+        torch.cuda.current_stream().synchronize()
+        return out.cpu().numpy().astype(bool)
+
+    def debug_activation(self, layer, k):
+        w = self.hparams()[k]["width"]
+        out = np.empty((self.B, w), dtype=np.float32)
+        _check(self.lib.pack_debug_activation(self.h, layer, k, out.ctypes.data))
+        return out

@@ -1,0 +1,105 @@
+"""Helpers shared by the GPU parity tests: run the HIP library and the fp64 oracle
+on the same seeded inputs and compare them element by element.
+
+Tolerances (element test |gpu - ref| <= atol + rtol * |ref|):
+  bf16 GEMMs (fp32 master weights) vs the fp64 oracle: rtol 2e-2, atol 1e-3 for
+  losses, outputs, parameters and AdamW moments; gradients are O(1/B), so their
+  absolute floor scales with the tensor: atol 1e-3 * max|g_ref|, plus a relative
+  Frobenius error <= 2e-2.
+  fp32 MFMA mode: rtol 1e-4 everywhere, gradient floor 1e-4 * max|g_ref|,
+  Frobenius <= 1e-4.
+Parameters after a step: the first AdamW step moves an element by about
+lr * sign(g), so an element whose oracle gradient lies inside its own gradient
+tolerance band may legitimately move the other way; for those elements only
+|delta| <= 2 lr (1 + 1e-6) + tol is accepted, and their share is reported.
+"""
+import numpy as np
+
+from oracle.pack import OraclePack
+from oracle.sampling import member_hparams, sample_hparams
+from paper_2607_05380_amd import synth
+
+TOL = {"bf16": dict(rtol=2e-2, atol=1e-3, gfloor=1e-3, frob=2e-2),
+       "fp32": dict(rtol=1e-4, atol=1e-6, gfloor=1e-4, frob=1e-4)}
+
+ORACLE_KEYS = ("seed", "K", "d_in", "d_out", "L", "B", "task", "beta1", "beta2", "eps", "decay_bias",
+               "width_lo", "width_hi", "dropout_lo", "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi")
+
+
+def oracle_cfg(cfg):
+    return {k: cfg[k] for k in ORACLE_KEYS}
+
+
+def oracle_hparams(cfg, members=None):
+    if members is None:
+        return sample_hparams(oracle_cfg(cfg))
+    return [member_hparams(m["width"], m["dropout"], m["lr"], m["wd"]) for m in members]
+
+
+def close_mask(gpu, ref, rtol, atol):
+    return np.abs(np.asarray(gpu, np.float64) - ref) <= atol + rtol * np.abs(ref)
+
+
+def check_tensor(name, gpu, ref, tol, grad=False, report=None):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert gpu.shape == ref.shape, (name, gpu.shape, ref.shape)
+    assert np.isfinite(gpu).all(), name
+    mx = np.abs(ref).max() if ref.size else 0.0
+    atol = tol["gfloor"] * mx if grad else tol["atol"]
+    ok = close_mask(gpu, ref, tol["rtol"], atol)
+    frob = np.linalg.norm(gpu - ref) / max(np.linalg.norm(ref), 1e-30)
+    if report is not None:
+        report.append((name, float(frob), int((~ok).sum())))
+    assert ok.all(), f"{name}: {(~ok).sum()} of {ok.size} elements out of tolerance; worst " \
+                     f"{np.abs(gpu - ref)[~ok].max():.3e} (max|ref| {mx:.3e}), frob {frob:.2e}"
+    if grad and mx > 0:
+        assert frob <= tol["frob"], f"{name}: relative Frobenius error {frob:.3e}"
+    return frob
+
+
+def check_params_after_step(name, gpu, ref, before, grad_ref, lr, tol, report=None):
+    """Parameter check with the sign-flip allowance of the first AdamW steps."""
+    gpu = np.asarray(gpu, np.float64)
+    ok = close_mask(gpu, ref, tol["rtol"], tol["atol"])
+    band = np.abs(grad_ref) <= tol["gfloor"] * np.abs(grad_ref).max() + tol["rtol"] * np.abs(grad_ref)
+    flip_ok = np.abs(gpu - ref) <= 2 * lr * (1 + 1e-6) + tol["atol"] + tol["rtol"] * np.abs(ref)
+    good = ok | (band & flip_ok)
+    if report is not None:
+        report.append((name, float((~ok & good).mean()), int((~good).sum())))
+    assert good.all(), f"{name}: {(~good).sum()} of {good.size} params out of tolerance; worst " \
+                       f"{np.abs(gpu - ref)[~good].max():.3e}"
+    return float((~ok).mean())
+
+
+def make_inputs(cfg, n_train, n_val, epoch=0, step_in_epoch=0):
+    Xtr, ytr, Xva, yva = synth.make_data(cfg, n_train=n_train, n_val=n_val)
+    orders = synth.epoch_orders(cfg, epoch, n_train)
+    idx = synth.batch_indices(orders, step_in_epoch, cfg["B"])
+    return Xtr, ytr, Xva, yva, orders, idx
+
+
+def to_dev(*arrays):
+    import torch
+    return [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in arrays]
+
+
+def compare_member(pk, op, k, tol, grads_gpu=True, report=None, prefix=""):
+    """Compare member k of the GPU pack with member k of the oracle pack after a step."""
+    lr = op.hp[k]["lr"]
+    g_gpu = pk.get_grads(k) if grads_gpu else None
+    p_gpu = pk.get_params(k)
+    m_gpu, v_gpu = pk.get_moments(k)
+    names = [f"W{l+1}" for l in range(len(op.params[k]) - 1)] + ["Wout"]
+    for l, nm in enumerate(names):
+        gW, gb = op.last_grads[k][l]
+        tag = f"{prefix}m{k}.{nm}"
+        if grads_gpu:
+            check_tensor(tag + ".grad", g_gpu[l][0], gW, tol, grad=True, report=report)
+            check_tensor(tag + ".bgrad", g_gpu[l][1], gb, tol, grad=True, report=report)
+        check_params_after_step(tag, p_gpu[l][0], op.params[k][l][0], None, gW, lr, tol, report)
+        check_params_after_step(tag + ".b", p_gpu[l][1], op.params[k][l][1], None, gb, lr, tol, report)
+        check_tensor(tag + ".m", m_gpu[l][0], op.m[k][l][0], tol, grad=True, report=report)
+        # v = sum of (1-b2) b2^i g^2: compare sqrt(v), which scales like |g|
+        check_tensor(tag + ".sqrtv", np.sqrt(v_gpu[l][0]), np.sqrt(op.v[k][l][0]), tol, grad=True,
+                     report=report)

@@ -1,0 +1,185 @@
+"""GPU parity of the packed training step, evaluation and selection against the
+fp64 oracle on identical seeded inputs (run on an MI355X)."""
+import numpy as np
+import pytest
+
+from oracle.greedy import greedy_select
+from oracle.mlp import dropout_mask
+from oracle.pack import OraclePack
+from paper_2607_05380_amd import configs, tabpack
+from parity import TOL, check_tensor, compare_member, make_inputs, oracle_cfg, oracle_hparams, to_dev
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+# Reduced versions of the five workloads: same feature counts, depths, width and
+# dropout ranges and precision; fewer members and a ragged base batch so that
+# every GEMM spans several 128-wide tiles plus a partial one.
+SMALL = {
+    "binary_small": dict(),
+    "regression_onehot": dict(K=6, B=300),
+    "multiclass_lognormal": dict(K=5, B=700),
+    "binary_wide": dict(K=4, B=260),
+    "regression_large": dict(K=5, B=500),
+}
+
+
+def run_step(cfg, members=None, n_train=4096, n_val=600, steps=1):
+    Xtr, ytr, Xva, yva, orders, idx = make_inputs(cfg, n_train, n_val)
+    pk = tabpack.Pack(cfg, members=members).bind()
+    op = OraclePack(oracle_cfg(cfg), hparams=oracle_hparams(cfg, members))
+    X, y = to_dev(Xtr, ytr)
+    losses = []
+    for s in range(1, steps + 1):
+        from paper_2607_05380_amd import synth
+        idx = synth.batch_indices(orders, s - 1, cfg["B"])
+        (idx_d,) = to_dev(idx)
+        lg = pk.train_step(X, y, idx_d, s)
+        torch.cuda.synchronize()
+        lo = op.train_step(Xtr, ytr, idx, s)
+        losses.append((lg.cpu().numpy(), lo))
+    return pk, op, losses, (Xtr, ytr, Xva, yva)
+
+
+@pytest.mark.parametrize("name", configs.ORDER)
+def test_train_step_parity(name):
+    cfg = configs.workload(name, **SMALL[name])
+    tol = TOL[cfg["precision"]]
+    print(f"[parity] {name} K={cfg['K']} B={cfg['B']} prec={cfg['precision']}", flush=True)
+    pk, op, losses, _ = run_step(cfg)
+    lg, lo = losses[0]
+    check_tensor("loss", lg, lo, tol)
+    report = []
+    for k in range(cfg["K"]):
+        compare_member(pk, op, k, tol, report=report)
+    worst = max(report, key=lambda r: r[1])
+    print(f"[parity] {name}: worst {worst}", flush=True)
+
+
+def test_three_steps_parity_bf16():
+    cfg = configs.workload("regression_large", K=3, B=256)
+    tol = TOL["bf16"]
+    pk, op, losses, _ = run_step(cfg, steps=3)
+    for lg, lo in losses:
+        check_tensor("loss", lg, lo, tol)
+    for k in range(3):
+        compare_member(pk, op, k, tol, prefix="t3.")
+
+
+def test_explicit_edge_members_fp32():
+    # widths at and around the quantum and tile edges, p = 0 and large p
+    cfg = configs.workload("regression_onehot", K=5, B=129, precision="fp32")
+    members = [dict(width=w, dropout=p, lr=2e-3, wd=1e-3)
+               for w, p in ((1, 0.0), (32, 0.45), (127, 0.0), (128, 0.2), (129, 0.3))]
+    pk, op, losses, _ = run_step(cfg, members=members)
+    check_tensor("loss", losses[0][0], losses[0][1], TOL["fp32"])
+    for k in range(5):
+        compare_member(pk, op, k, TOL["fp32"])
+
+
+def test_dropout_masks_bit_exact_and_applied():
+    cfg = configs.workload("regression_large", K=4, B=300)
+    pk, op, _, _ = run_step(cfg)
+    hp = pk.hparams()
+    for k in range(4):
+        for layer in range(1, 4):
+            for step in (1, 2, 1234567):
+                got = pk.debug_dropout_mask(step, layer, k)
+                ref = dropout_mask(cfg["seed"], k, step, layer, cfg["B"], hp[k]["width"], hp[k]["t"])
+                np.testing.assert_array_equal(got, ref)
+            H = pk.debug_activation(layer, k)
+            m1 = dropout_mask(cfg["seed"], k, 1, layer, cfg["B"], hp[k]["width"], hp[k]["t"])
+            assert (H[~m1] == 0).all() and (H >= 0).all()
+            assert (H[m1] > 0).mean() > 0.2
+
+
+def test_determinism_and_member_independence():
+    cfg = configs.workload("multiclass_lognormal", K=4, B=256)
+    Xtr, ytr, _, _, orders, idx = make_inputs(cfg, 3000, 10)
+    X, y, idx_d = to_dev(Xtr, ytr, idx)
+    runs = []
+    for perturb in (False, False, True):
+        pk = tabpack.Pack(cfg).bind()
+        if perturb:
+            p = pk.get_params(2)
+            p[0][0][0, 0] += 0.5
+            pk.set_params(2, p)
+        l1 = pk.train_step(X, y, idx_d, 1).cpu().numpy()
+        l2 = pk.train_step(X, y, idx_d, 2).cpu().numpy()
+        runs.append((l1, l2, [pk.get_params(k) for k in range(4)], [pk.get_grads(k) for k in range(4)]))
+    a, b, c = runs
+    for k in range(4):
+        same = [(a, b)] + ([(a, c)] if k != 2 else [])
+        for r1, r2 in same:
+            assert r1[0][k] == r2[0][k] and r1[1][k] == r2[1][k]
+            for (W1, b1), (W2, b2) in zip(r1[2][k], r2[2][k]):
+                np.testing.assert_array_equal(W1, W2)
+                np.testing.assert_array_equal(b1, b2)
+            for (W1, b1), (W2, b2) in zip(r1[3][k], r2[3][k]):
+                np.testing.assert_array_equal(W1, W2)
+                np.testing.assert_array_equal(b1, b2)
+    assert c[0][2] != a[0][2]
+
+
+def test_k1_pack_equals_standalone_member():
+    # one-member pack vs the oracle's standalone MLP with the same hyperparameters
+    cfg = configs.workload("binary_small", K=1)
+    pk, op, losses, _ = run_step(cfg)
+    check_tensor("loss", losses[0][0], losses[0][1], TOL["fp32"])
+    compare_member(pk, op, 0, TOL["fp32"])
+
+
+def test_step_counter_enforced():
+    cfg = configs.workload("binary_small")
+    Xtr, ytr, _, _, _, idx = make_inputs(cfg, 2048, 10)
+    X, y, idx_d = to_dev(Xtr, ytr, idx)
+    pk = tabpack.Pack(cfg).bind()
+    with pytest.raises(tabpack.PackError, match="step 2 given"):
+        pk.train_step(X, y, idx_d, 2)
+    pk.train_step(X, y, idx_d, 1)
+
+
+@pytest.mark.parametrize("name", configs.ORDER)
+def test_eval_members_parity(name):
+    cfg = configs.workload(name, **SMALL[name])
+    tol = TOL[cfg["precision"]]
+    Xtr, ytr, Xva, yva, _, _ = make_inputs(cfg, 2000, 1300 if name != "binary_small" else 512)
+    pk = tabpack.Pack(cfg).bind()
+    op = OraclePack(oracle_cfg(cfg), hparams=oracle_hparams(cfg))
+    Xv, yv = to_dev(Xva, yva)
+    pred, score = pk.eval_members(Xv, yv)
+    torch.cuda.synchronize()
+    pr, sr = op.eval_members(Xva, yva)
+    check_tensor("pred", pred.cpu().numpy(), pr, tol)
+    check_tensor("score", score.cpu().numpy(), sr, tol)
+
+
+@pytest.mark.parametrize("task", ["reg", "bin", "multi"])
+@pytest.mark.parametrize("C,Nv,m_ens", [(5, 37, 4), (40, 3000, 32), (96, 2500, 32)])
+def test_select_matches_oracle(task, C, Nv, m_ens):
+    rng = np.random.default_rng(C * 1000 + Nv)
+    if task == "reg":
+        y = rng.standard_normal(Nv).astype(np.float32)
+        cand = (y[None, :] + rng.standard_normal((C, Nv)) * rng.uniform(0.3, 2, (C, 1))).astype(np.float32)
+    elif task == "bin":
+        y = (rng.random(Nv) < 0.4).astype(np.float32)
+        cand = np.clip(0.5 * y[None, :] + 0.5 * rng.random((C, Nv)), 0, 1).astype(np.float32)
+    else:
+        y = rng.integers(0, 10, Nv).astype(np.int32)
+        cand = rng.uniform(0.02, 0.9, (C, Nv)).astype(np.float32)
+    cfg = configs.workload({"reg": "regression_onehot", "bin": "binary_small", "multi": "multiclass_lognormal"}[task], K=2)
+    pk = tabpack.Pack(cfg)
+    c_d, y_d = to_dev(cand, y)
+    sel, s = pk.select(c_d, y_d, m_ens)
+    sel_o, s_o = greedy_select(cand.astype(np.float64), y, task, m_ens)
+    assert sel == sel_o
+    assert s == pytest.approx(s_o, rel=1e-12)
+
+
+def test_select_skips_non_finite():
+    cfg = configs.workload("regression_onehot", K=2)
+    pk = tabpack.Pack(cfg)
+    y = np.zeros(3, np.float32)
+    cand = np.array([[np.nan, 0, 0], [0.5, 0.5, 0.5], [np.inf, 1, 1]], np.float32)
+    c_d, y_d = to_dev(cand, y)
+    assert pk.select(c_d, y_d, 3) == ([1], 0.5)
