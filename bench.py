@@ -1,0 +1,150 @@
+"""Throughput of the packed training step (fwd + bwd + AdamW for all K members).
+
+Default workload: the 700K x 900 regression workload with K = 64 members, 3
+hidden layers, widths UniformInt[256, 1024], dropout U[0, 0.5], batch 1024,
+bf16 MFMA GEMMs with fp32 master weights.  Inputs are synthetic, generated on
+the device and resident in HBM before timing.  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "member-samples/sec (fwd+bwd+AdamW) at K=64; % bf16 MFMA peak; % HBM BW"
+PEAK = {"mfma_bf16": 2516.6, "mfma_fp32": 157.3, "hbm": 8000.0}  # TFLOP/s, TFLOP/s, GB/s
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(cfg, X, y, idx0, budget_s=15.0):
+    """The fp64 oracle, timed on the host cores on a bounded sample: members
+    0, 1, ... of the first step until the time budget is spent."""
+    import numpy as np
+    from oracle.pack import OraclePack
+    keys = ("seed", "K", "d_in", "d_out", "L", "B", "task", "beta1", "beta2", "eps", "decay_bias",
+            "width_lo", "width_hi", "dropout_lo", "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi")
+    op = OraclePack({k: cfg[k] for k in keys})
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count()
+    B = cfg["B"]
+    done, dt = 0, 0.0
+    while done < cfg["K"] and dt < budget_s:
+        rows = idx0[done].long()
+        Xk = X[rows].double().cpu().numpy()  # this member's base batch, copied before timing
+        yk = y[rows].cpu().numpy()
+        t0 = time.perf_counter()
+        op.member_step(done, Xk, yk, np.arange(B), 1)
+        dt += time.perf_counter() - t0
+        done += 1
+    return {"value": done * B / dt, "unit": "member-samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"members 0..{done - 1} of step 1 of {cfg['name']} (fp64 numpy, one member at a time), "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="regression_large")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=10)
+    a = ap.parse_args()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU: the packed step runs all members on one device and this "
+              f"build has no multi-GPU path (asked for --gpus {a.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_05380_amd import configs, synth, tabpack
+
+    cfg = configs.workload(a.workload)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"generating {cfg['name']} on device: {cfg['n_train']} x {cfg['d_in']}")
+    Xtr, ytr, _, _ = synth.make_data_device(cfg, dev)
+    orders = synth.epoch_orders_device(cfg, 0, cfg["n_train"], dev)
+    steps_per_epoch = cfg["n_train"] // cfg["B"]
+    total = a.warmup + a.steps + a.profile_steps
+    idx_all = torch.stack([orders[:, (s % steps_per_epoch) * cfg["B"]:(s % steps_per_epoch + 1) * cfg["B"]]
+                           for s in range(total)]).contiguous()
+    pk = tabpack.Pack(cfg).bind(dev)
+    log(f"bound: workspace {pk.workspace_bytes() / 2**30:.2f} GiB")
+    loss = torch.empty(cfg["K"], dtype=torch.float32, device=dev)
+    step = 0
+    for _ in range(a.warmup):
+        step += 1
+        pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
+    torch.cuda.synchronize()
+    log(f"warmup done, losses[:4] = {loss[:4].tolist()}")
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(a.steps):
+        step += 1
+        pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = ev0.elapsed_time(ev1)
+    if not torch.isfinite(loss).all():
+        raise RuntimeError("non-finite member loss in the timed region")
+    ms_per_step = ms / a.steps
+    msamples = cfg["K"] * cfg["B"] * a.steps / (ms / 1e3)
+    log(f"timed {a.steps} steps: {ms_per_step:.3f} ms/step (wall {wall:.3f} s), {msamples / 1e6:.2f} M member-samples/s")
+
+    # per-kernel durations: HIP events recorded by the library around each launch
+    pk.profile(True)
+    for _ in range(a.profile_steps):
+        step += 1
+        pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
+    stats = pk.profile_read()
+    pk.profile(False)
+    for s in sorted(stats, key=lambda s: -s["total_ms"]):
+        unit = "TFLOP/s" if s["kind"] == "mfma" else "GB/s"
+        rate = s["work"] / (s["avg_ms"] / 1e3) / (1e12 if s["kind"] == "mfma" else 1e9)
+        log(f"  {s['name']:34s} launches {s['launches']:4d}  avg {s['avg_ms'] * 1e3:9.1f} us  "
+            f"total/step {s['total_ms'] / a.profile_steps:7.3f} ms  {rate:9.1f} {unit}")
+    dom = max(stats, key=lambda s: s["total_ms"])
+    if dom["kind"] == "mfma":
+        peak = PEAK["mfma_bf16"] if cfg["precision"] == "bf16" else PEAK["mfma_fp32"]
+        achieved = dom["work"] / (dom["avg_ms"] / 1e3) / 1e12
+        unit = "TFLOP/s"
+    else:
+        peak, unit = PEAK["hbm"], "GB/s"
+        achieved = dom["work"] / (dom["avg_ms"] / 1e3) / 1e9
+    roofline = {"bound": dom["kind"], "kernel": dom["name"], "achieved": round(achieved, 2), "peak": peak,
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "avg_launch_us": round(dom["avg_ms"] * 1e3, 2), "work_per_launch": dom["work"]}
+    out = {
+        "metric": METRIC, "value": round(msamples, 1), "unit": "member-samples/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg["precision"], "data": "synthetic",
+        "config": {"workload": cfg["name"], "K": cfg["K"], "B": cfg["B"], "d_in": cfg["d_in"], "L": cfg["L"],
+                   "widths": [cfg["width_lo"], cfg["width_hi"]], "n_train": cfg["n_train"],
+                   "task": cfg["task"]},
+        "roofline": roofline,
+        "kernels": [{"name": s["name"], "bound": s["kind"], "avg_us": round(s["avg_ms"] * 1e3, 2),
+                     "per_step_ms": round(s["total_ms"] / a.profile_steps, 4), "work_per_launch": s["work"]}
+                    for s in sorted(stats, key=lambda s: -s["total_ms"])],
+    }
+    if not a.no_cpu_baseline:
+        log("timing the fp64 oracle on the host (bounded sample)")
+        out["cpu_baseline"] = cpu_baseline(cfg, Xtr, ytr, idx_all[0])
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -8,6 +8,17 @@ H -> H @ W.T + b.
 Losses (App. F, training of DL models): cross-entropy for classification
 (binary cross-entropy with logits for two classes) and mean squared error for
 regression, each averaged over the member's base batch of B rows.
+
+Precision.  By default everything is float64 (the exact definition).  With
+``rnd=to_bf16`` the same steps follow a bf16 mixed-precision policy: the
+operands of every hidden-layer matrix product are bfloat16 values -- the
+network input X, the hidden weights W_1..W_L, the stored activations H_l (after
+bias, ReLU, dropout and scaling) and the stored pre-activation gradients dZ_l
+-- while the head weights, biases, bias gradients (summed from dZ before it is
+rounded), losses and all accumulations stay in high precision.  Rounding is
+round-to-nearest-even of the float32 value.  The ReLU/dropout decisions of
+the backward pass are then taken on the same bf16-rounded forward values the
+bf16 kernels use, which is what makes an element-wise comparison meaningful.
 """
 import numpy as np
 
@@ -33,17 +44,30 @@ def dropout_mask(seed, k, step, layer, B, width, t):
     return np.choose(sel, words) >= np.uint32(t)
 
 
-def forward(params, X, masks=None, scale=1.0):
+def to_bf16(x):
+    """Round to the nearest bfloat16 value (ties to even) via float32; float64 result."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))) & np.uint64(0xFFFF0000)
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def _same(x):
+    return x
+
+
+def forward(params, X, masks=None, scale=1.0, rnd=None):
     """Returns (Y, cache).  masks[l] is the keep mask of hidden layer l+1 or None."""
-    H = np.asarray(X, dtype=np.float64)
-    cache = {"H": [H], "Z": []}
+    rnd = rnd or _same
+    H = rnd(np.asarray(X, dtype=np.float64))
+    cache = {"H": [H], "Z": [], "rnd": rnd}
     L = len(params) - 1
     for l in range(L):
         W, b = params[l]
-        Z = H @ W.T + b
+        Z = H @ rnd(W).T + b
         H = np.maximum(Z, 0.0)
         if masks is not None:
             H = H * masks[l] * scale
+        H = rnd(H)
         cache["Z"].append(Z)
         cache["H"].append(H)
     Wo, bo = params[L]
@@ -76,6 +100,7 @@ def loss_and_dy(Y, y, task):
 def backward(params, cache, dY, masks=None, scale=1.0):
     """Gradients [(dW, db), ...] in the layout of ``params``."""
     L = len(params) - 1
+    rnd = cache.get("rnd", _same)
     grads = [None] * (L + 1)
     H = cache["H"]
     Wo, _ = params[L]
@@ -85,10 +110,12 @@ def backward(params, cache, dY, masks=None, scale=1.0):
         dZ = dH * (cache["Z"][l] > 0.0)
         if masks is not None:
             dZ = dZ * masks[l] * scale
+        db = dZ.sum(axis=0)
+        dZ = rnd(dZ)
         W, _ = params[l]
-        grads[l] = (dZ.T @ H[l], dZ.sum(axis=0))
+        grads[l] = (dZ.T @ H[l], db)
         if l > 0:
-            dH = dZ @ W
+            dH = dZ @ rnd(W)
     return grads
 
 

@@ -14,10 +14,16 @@ from .sampling import init_member, sample_hparams
 
 
 class OraclePack:
-    """Holds fp64 parameters and AdamW moments of K members."""
+    """Holds fp64 parameters and AdamW moments of K members.
 
-    def __init__(self, cfg, hparams=None, params=None):
+    precision "fp64" is the exact definition; "bf16" applies the bf16
+    mixed-precision rounding policy described in ``mlp`` to the matrix-product
+    operands (parameters, moments and updates stay float64).
+    """
+
+    def __init__(self, cfg, hparams=None, params=None, precision="fp64"):
         self.cfg = dict(cfg)
+        self.rnd = mlp.to_bf16 if precision == "bf16" else None
         self.hp = hparams if hparams is not None else sample_hparams(cfg)
         if params is None:
             params = [init_member(cfg, k, h["width"]) for k, h in enumerate(self.hp)]
@@ -37,7 +43,7 @@ class OraclePack:
         c, h = self.cfg, self.hp[k]
         rows = np.asarray(idx_k, dtype=np.int64)
         masks = self.masks(k, step)
-        Y, cache = mlp.forward(self.params[k], X[rows], masks, h["s"])
+        Y, cache = mlp.forward(self.params[k], X[rows], masks, h["s"], rnd=self.rnd)
         loss, dY = mlp.loss_and_dy(Y, y[rows], c["task"])
         grads = mlp.backward(self.params[k], cache, dY, masks, h["s"])
         new_p, new_m, new_v = [], [], []
@@ -69,7 +75,7 @@ class OraclePack:
 
     def predict(self, k, Xv):
         """Score-ready prediction of member k on Xv (no dropout)."""
-        Y, _ = mlp.forward(self.params[k], np.asarray(Xv, dtype=np.float64))
+        Y, _ = mlp.forward(self.params[k], np.asarray(Xv, dtype=np.float64), rnd=self.rnd)
         return Y
 
     def eval_members(self, Xv, yv, members=None):

@@ -70,6 +70,20 @@ struct Member {
 struct Launch {
   int desc0, ndesc;
   int tile0, ntiles;
+  double flops;  // algorithmic flops of the launch (true member shapes)
+};
+
+// One timed launch: events recorded on the launch stream around it.
+struct TimedLaunch {
+  int group;
+  hipEvent_t start, stop;
+};
+
+struct ProfGroup {
+  std::string name;
+  int kind;
+  int launches = 0;
+  double total_ms = 0.0, work = 0.0;
 };
 
 }  // namespace
@@ -80,6 +94,7 @@ struct Bufs {
   uint16_t* shadow = nullptr;
   char* H = nullptr;   // L activation buffers H_1..H_L
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
+  float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / 64 floats
   float *dY = nullptr, *rowloss = nullptr;
   MemberDev* d_mem = nullptr;
   uint32_t* d_chunks = nullptr;
@@ -105,6 +120,13 @@ struct pack_handle {
   std::vector<Launch> fwd, dx, dw;  // per layer (index l-1)
   int ncoltiles = 0;
   uint64_t t = 0;
+
+  // optional per-kernel timing
+  bool prof = false;
+  std::vector<TimedLaunch> timed;
+  std::vector<hipEvent_t> event_pool;
+  size_t pool_used = 0;
+  std::vector<ProfGroup> groups;
 
   size_t elt() const { return prec == Prec::BF16 ? 2 : 4; }
   void* Hl(int l) const { return b.H + (size_t)(l - 1) * A * elt(); }  // H_l, l = 1..L
@@ -286,7 +308,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   auto act = [&](void* base, int k) -> void* { return (char*)base + (size_t)h->mem[k].act_off * es; };
   for (int l = 1; l <= c.L; ++l) {
     // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
-    Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0};
+    Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
     for (int k = 0; k < c.K; ++k) {
       const Member& m = h->mem[k];
       GemmDesc d{};
@@ -306,13 +328,14 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.drop_s = (float)m.scale;
       p.descs.push_back(d);
       add_tiles(p, f, f.desc0 + k, h->Bp, m.dp, d.Kd);
+      f.flops += 2.0 * c.B * m.width * (l == 1 ? c.d_in : m.width);
     }
     sort_launch(p, f);
     p.fwd.push_back(f);
   }
   for (int l = 1; l <= c.L; ++l) {
     // weight gradient: dW_l^T[out, in] = sum_rows dZ_l[row, out] H_{l-1}[row, in]
-    Launch w{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0};
+    Launch w{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
     for (int k = 0; k < c.K; ++k) {
       const Member& m = h->mem[k];
       GemmDesc d{};
@@ -328,11 +351,12 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.member = k;
       p.descs.push_back(d);
       add_tiles(p, w, w.desc0 + k, d.M, d.N, d.Kd);
+      w.flops += 2.0 * c.B * m.width * (l == 1 ? c.d_in : m.width);
     }
     sort_launch(p, w);
     p.dw.push_back(w);
     // data gradient (l >= 2): dZ_{l-1} = (dZ_l W_l) * [H_{l-1} > 0] * s_k
-    Launch x{(int)p.descs.size(), 0, (int)p.tiles.size(), 0};
+    Launch x{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
     if (l >= 2) {
       x.ndesc = c.K;
       for (int k = 0; k < c.K; ++k) {
@@ -344,6 +368,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
         d.ldb = m.dp;
         d.C = act(dzb(l - 1), k);
         d.Haux = act(Hl(l - 1), k);
+        d.colpart = bf.colpart + h->mem[k].act_off / 64;
         d.ldc = m.dp;
         d.M = h->Bp;
         d.N = m.dp;
@@ -352,6 +377,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
         d.drop_s = (float)m.scale;
         p.descs.push_back(d);
         add_tiles(p, x, x.desc0 + k, h->Bp, m.dp, d.Kd);
+        x.flops += 2.0 * c.B * m.width * m.width;
       }
       sort_launch(p, x);
     }
@@ -386,6 +412,7 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
   bf.shadow = h->prec == Prec::BF16 ? cv.take<uint16_t>(h->P) : nullptr;
   bf.H = cv.take<char>((size_t)c.L * h->A * h->elt());
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
+  bf.colpart = cv.take<float>((size_t)h->A / 64);
   bf.dY = cv.take<float>((size_t)c.K * h->Bp * c.d_out);
   bf.rowloss = cv.take<float>((size_t)c.K * h->Bp);
   bf.d_mem = cv.take<MemberDev>(c.K);
@@ -423,6 +450,48 @@ GemmArgs for_launch(GemmArgs a, const Launch& ln) {
   a.tiles += ln.tile0;
   a.ntiles = ln.ntiles;
   return a;
+}
+
+hipEvent_t pool_event(pack_handle* h) {
+  if (h->pool_used == h->event_pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    h->event_pool.push_back(e);
+  }
+  return h->event_pool[h->pool_used++];
+}
+
+int group_id(pack_handle* h, const std::string& name, int kind) {
+  for (size_t i = 0; i < h->groups.size(); ++i)
+    if (h->groups[i].name == name) return (int)i;
+  h->groups.push_back(ProfGroup{name, kind});
+  return (int)h->groups.size() - 1;
+}
+
+// Runs `fn` (which enqueues one kernel on `stream`) and, when profiling,
+// brackets it with events and attributes `work` to the named kernel.
+template <typename F>
+hipError_t timed(pack_handle* h, const char* name, int kind, double work, hipStream_t stream, F fn) {
+  if (!h->prof) return fn();
+  hipEvent_t a = pool_event(h), b = pool_event(h);
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, stream);
+  if (e != hipSuccess) return e;
+  e = fn();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, stream);
+  const int g = group_id(h, name, kind);
+  h->groups[g].work += work;  // summed here, averaged per launch when read
+  h->timed.push_back(TimedLaunch{g, a, b});
+  return e;
+}
+
+const char* gemm_name(Prec p, OpKind a, OpKind b, EpiKind e) {
+  static const char* ops[] = {"kmaj", "rmaj", "xgk", "xgr"};
+  static const char* epis[] = {"fwd", "fwd_eval", "dx", "dw"};
+  static thread_local char buf[64];
+  snprintf(buf, sizeof buf, "gemm_%s_%s_%s_%s", p == Prec::BF16 ? "bf16" : "f32", ops[a], ops[b], epis[e]);
+  return buf;
 }
 
 }  // namespace
@@ -474,6 +543,8 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
 }
 
 int pack_destroy(pack_handle* h) {
+  if (h)
+    for (hipEvent_t e : h->event_pool) (void)hipEventDestroy(e);
   delete h;
   return PACK_OK;
 }
@@ -543,34 +614,49 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   a.idx = idx;
   a.rows_valid = c.B;
   a.step = as_u32(step);
-  for (int l = 1; l <= c.L; ++l) {
-    GemmArgs al = for_launch(a, h->fwd[l - 1]);
-    al.layer = l;
-    HIP_TRY(launch_gemm(h->prec, l == 1 ? OP_XGK : OP_KMAJ, OP_KMAJ, EPI_FWD, al, stream));
-  }
-  HIP_TRY(launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, y,
-                          idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, stream));
-  HIP_TRY(launch_loss_reduce(h->b.rowloss, h->b.dY, h->b.d_mem, c.K, h->Bp, c.B, c.d_out, h->b.grad, loss_out, stream));
-  HIP_TRY(launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp, c.d_out,
-                          h->b.dY, h->dzb(c.L), h->b.grad, stream));
+  const double act_bytes = (double)c.B * h->elt() * [&] {
+    double s = 0;
+    for (const Member& m : h->mem) s += m.width;
+    return s;
+  }();
+  auto gemm = [&](OpKind ak, OpKind bk, EpiKind e, const Launch& ln, int layer) {
+    GemmArgs al = for_launch(a, ln);
+    al.layer = layer;
+    return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, stream,
+                 [&] { return launch_gemm(h->prec, ak, bk, e, al, stream); });
+  };
+  for (int l = 1; l <= c.L; ++l) HIP_TRY(gemm(l == 1 ? OP_XGK : OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[l - 1], l));
+  HIP_TRY(timed(h, "head_fwd", 1, act_bytes, stream, [&] {
+    return launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, y,
+                           idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, stream);
+  }));
+  HIP_TRY(timed(h, "loss_reduce", 1, (double)c.K * c.B * 4 * (1 + c.d_out), stream, [&] {
+    return launch_loss_reduce(h->b.rowloss, h->b.dY, h->b.d_mem, c.K, h->Bp, c.B, c.d_out, h->b.grad, loss_out,
+                              stream);
+  }));
+  HIP_TRY(timed(h, "head_bwd", 1, 2.0 * act_bytes, stream, [&] {
+    return launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp,
+                           c.d_out, h->b.dY, h->dzb(c.L), h->b.grad, stream);
+  }));
   for (int l = c.L; l >= 1; --l) {
-    GemmArgs aw = for_launch(a, h->dw[l - 1]);
-    aw.layer = l;
-    HIP_TRY(launch_gemm(h->prec, OP_RMAJ, l == 1 ? OP_XGR : OP_RMAJ, EPI_DW, aw, stream));
-    if (l < c.L)
-      HIP_TRY(launch_colsum(h->prec, h->dzb(l), h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp,
-                            h->b.d_bias_off + (size_t)(l - 1) * c.K, h->b.grad, stream));
+    HIP_TRY(gemm(OP_RMAJ, l == 1 ? OP_XGR : OP_RMAJ, EPI_DW, h->dw[l - 1], l));
     if (l > 1) {
-      GemmArgs ax = for_launch(a, h->dx[l - 1]);
-      ax.layer = l;
-      HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_RMAJ, EPI_DX, ax, stream));
+      HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[l - 1], l));
+      HIP_TRY(timed(h, "bias_from_partials", 1, act_bytes * 4 / h->elt() / 64, stream, [&] {
+        return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp / 64,
+                                         h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, stream);
+      }));
     }
   }
   const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
   const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
-  HIP_TRY(launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, h->b.shadow, h->b.d_chunks, h->b.d_mem,
-                       (int64_t)h->chunk_tab.size(), (float)bc1, (float)std::sqrt(bc2), (float)c.beta1,
-                       (float)c.beta2, (float)c.eps, stream));
+  double nparam = 0;
+  for (int k = 0; k < c.K; ++k) nparam += (double)dense_count(h, k);
+  HIP_TRY(timed(h, "adamw", 1, nparam * (h->prec == Prec::BF16 ? 30.0 : 28.0), stream, [&] {
+    return launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, h->b.shadow, h->b.d_chunks, h->b.d_mem,
+                        (int64_t)h->chunk_tab.size(), (float)bc1, (float)std::sqrt(bc2), (float)c.beta1,
+                        (float)c.beta2, (float)c.eps, stream);
+  }));
   h->t = step;
   return PACK_OK;
 }
@@ -733,6 +819,40 @@ int pack_debug_activation(pack_handle* h, int32_t layer, int32_t member, float* 
       }
       host_out[(size_t)r * m.width + c] = val;
     }
+  return PACK_OK;
+}
+
+int pack_profile_enable(pack_handle* h, int32_t enable) {
+  if (!h) return fail(PACK_EINVAL, "handle is NULL");
+  HIP_TRY(hipDeviceSynchronize());
+  h->prof = enable != 0;
+  h->timed.clear();
+  h->pool_used = 0;
+  h->groups.clear();
+  return PACK_OK;
+}
+
+int pack_profile_read(pack_handle* h, pack_kernel_stat* out, int32_t max, int32_t* n) {
+  if (!h || !n || (max > 0 && !out)) return fail(PACK_EINVAL, "NULL argument");
+  std::vector<ProfGroup> g = h->groups;
+  for (ProfGroup& x : g) x.launches = 0, x.total_ms = 0.0;
+  for (const TimedLaunch& t : h->timed) {
+    HIP_TRY(hipEventSynchronize(t.stop));
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, t.start, t.stop));
+    g[t.group].launches += 1;
+    g[t.group].total_ms += ms;
+  }
+  *n = (int32_t)g.size();
+  for (int i = 0; i < (int)g.size() && i < max; ++i) {
+    pack_kernel_stat& s = out[i];
+    std::memset(&s, 0, sizeof s);
+    snprintf(s.name, sizeof s.name, "%s", g[i].name.c_str());
+    s.kind = g[i].kind;
+    s.launches = g[i].launches;
+    s.total_ms = g[i].total_ms;
+    s.work = g[i].launches ? g[i].work / g[i].launches : 0.0;
+  }
   return PACK_OK;
 }
 

@@ -217,24 +217,19 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* 
   }
 }
 
-// db_l = sum over rows of dZ_l, 64 columns of one member per workgroup.
-template <typename T>
-__global__ __launch_bounds__(256) void colsum_kernel(const T* dZ, const MemberDev* mem,
-                                                     const ColTile* tiles, int Bp,
-                                                     const int64_t* bias_off, float* grad) {
-  __shared__ float sh[4][64];
+// db_l[c] = sum of the per-64-row column partials written by the dX epilogue,
+// in a fixed order; 64 columns of one member per workgroup.
+__global__ __launch_bounds__(64) void bias_from_partials_kernel(const float* part, const MemberDev* mem,
+                                                                const ColTile* tiles, int nparts,
+                                                                const int64_t* bias_off, float* grad) {
   const ColTile ct = tiles[blockIdx.x];
   const MemberDev md = mem[ct.member];
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int c = ct.c0 + tx;
-  const bool valid = c < md.dp;
-  const T* z = dZ + md.act_off;
+  const int c = ct.c0 + threadIdx.x;
+  if (c >= md.dp) return;
+  const float* p = part + md.act_off / 64;
   float s = 0.0f;
-  if (valid)
-    for (int b = ty; b < Bp; b += 4) s += ld_act(z, (int64_t)b * md.dp + c);
-  sh[ty][tx] = s;
-  __syncthreads();
-  if (ty == 0 && valid) grad[bias_off[ct.member] + c] = (sh[0][tx] + sh[1][tx]) + (sh[2][tx] + sh[3][tx]);
+  for (int r = 0; r < nparts; ++r) s += p[(int64_t)r * md.dp + c];
+  grad[bias_off[ct.member] + c] = s;
 }
 
 // ------------------------------------------------------------------ AdamW --
@@ -473,14 +468,11 @@ hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const M
   return hipGetLastError();
 }
 
-hipError_t launch_colsum(Prec prec, const void* dZ, const MemberDev* mem, const ColTile* tiles,
-                         int ntiles, int Bp, const int64_t* bias_off, float* grad, hipStream_t s) {
-  if (prec == Prec::BF16)
-    hipLaunchKernelGGL((colsum_kernel<__bf16>), dim3(ntiles), dim3(256), 0, s,
-                       static_cast<const __bf16*>(dZ), mem, tiles, Bp, bias_off, grad);
-  else
-    hipLaunchKernelGGL((colsum_kernel<float>), dim3(ntiles), dim3(256), 0, s,
-                       static_cast<const float*>(dZ), mem, tiles, Bp, bias_off, grad);
+hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, const ColTile* tiles,
+                                     int ntiles, int nparts, const int64_t* bias_off, float* grad,
+                                     hipStream_t s) {
+  hipLaunchKernelGGL(bias_from_partials_kernel, dim3(ntiles), dim3(64), 0, s, part, mem, tiles, nparts,
+                     bias_off, grad);
   return hipGetLastError();
 }
 

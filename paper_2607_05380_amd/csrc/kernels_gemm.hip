@@ -382,6 +382,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
     } else if constexpr (EPI == EPI_DX) {
       T* C = static_cast<T*>(d.C);
       const T* Hp = static_cast<const T*>(d.Haux);
+      float cs = 0.0f;  // column sum over this wave's 64 rows (this lane's 32 of them)
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -391,9 +392,14 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
           for (int q = 0; q < 4; ++q) {
             const int64_t o = (int64_t)(row + q) * d.ldc + col;
             const float hp = to_float(Hp[o]);
-            C[o] = from_float<T>(hp > 0.0f ? acc[i][j][4 * g + q] * d.drop_s : 0.0f);
+            const float dz = hp > 0.0f ? acc[i][j][4 * g + q] * d.drop_s : 0.0f;
+            cs += dz;
+            C[o] = from_float<T>(dz);
           }
         }
+      // lanes l and l^32 hold the two interleaved halves of the same column
+      cs += __shfl_xor(cs, 32, 64);
+      if (hv == 0) d.colpart[(int64_t)(t.m0 / 64 + wm) * d.N + col] = cs;
     } else {
       T* C = static_cast<T*>(d.C);
       const float bias = d.bias[col];

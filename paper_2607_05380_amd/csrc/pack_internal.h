@@ -33,6 +33,7 @@ struct GemmDesc {
   void* C;
   const float* bias;   // EPI_FWD*: [N] fp32
   const void* Haux;    // EPI_DX: activation H_{l-1}, same layout as C
+  float* colpart;      // EPI_DX: [M / 64, N] column sums of the unrounded output per 64-row block
   int64_t lda, ldb, ldc;
   int32_t M, N, Kd;    // A rows in bounds (< M), B rows in bounds (< N), depth (< Kd)
   int32_t width;       // EPI_FWD*: true width; columns >= width are written as 0
@@ -92,8 +93,9 @@ hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const Membe
 hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const MemberDev* mem,
                            const ColTile* tiles, int ntiles, int Bp, int d_out, const float* dY,
                            void* dZ, float* grad, hipStream_t s);
-hipError_t launch_colsum(Prec prec, const void* dZ, const MemberDev* mem, const ColTile* tiles,
-                         int ntiles, int Bp, const int64_t* bias_off, float* grad, hipStream_t s);
+hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, const ColTile* tiles,
+                                     int ntiles, int nparts, const int64_t* bias_off, float* grad,
+                                     hipStream_t s);
 hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, float* v,
                         uint16_t* shadow, const uint32_t* chunk_tab, const MemberDev* mem,
                         int64_t nchunks, float bc1, float bc2_sqrt, float beta1, float beta2,

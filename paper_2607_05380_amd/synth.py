@@ -124,3 +124,85 @@ def batch_indices(orders, step_in_epoch, B):
     """idx [K, B] int32 of one step (drop-last batching of each member's order)."""
     s = int(step_in_epoch)
     return np.ascontiguousarray(orders[:, s * B:(s + 1) * B], dtype=np.int32)
+
+
+# ----------------------------------------------------------------------------
+# Device-side generator for full-size workloads (same recipes, torch's seeded
+# generator on the GPU instead of numpy's; the values differ from make_data's).
+# ----------------------------------------------------------------------------
+def make_data_device(cfg, device="cuda", n_train=None, n_val=None, chunk=131072):
+    """(X_train, y_train, X_val, y_val) as device tensors, generated on ``device``."""
+    import torch
+    n_tr = cfg["n_train"] if n_train is None else n_train
+    n_va = cfg["n_val"] if n_val is None else n_val
+    n = n_tr + n_va
+    d = cfg["d_in"]
+    g = torch.Generator(device=device)
+    g.manual_seed(int(cfg["seed"]) * 16 + 0)
+    X = torch.empty((n, d), dtype=torch.float32, device=device)
+    kind = cfg["features"]
+    for r0 in range(0, n, chunk):
+        r1 = min(n, r0 + chunk)
+        if kind == "block_correlated":
+            nb = (d + 29) // 30
+            z = torch.randn((r1 - r0, nb), generator=g, device=device)
+            e = torch.randn((r1 - r0, d), generator=g, device=device)
+            X[r0:r1] = (0.6 ** 0.5) * z.repeat_interleave(30, dim=1)[:, :d] + (0.4 ** 0.5) * e
+        elif kind == "onehot":
+            n_num = d - 16
+            X[r0:r1, :n_num] = torch.randn((r1 - r0, n_num), generator=g, device=device)
+            X[r0:r1, n_num:] = 0
+            for j in range(4):
+                lev = torch.randint(0, 4, (r1 - r0,), generator=g, device=device)
+                X[torch.arange(r0, r1, device=device), n_num + 4 * j + lev] = 1.0
+        else:
+            X[r0:r1] = torch.randn((r1 - r0, d), generator=g, device=device)
+            if kind == "lognormal_rankgauss":
+                X[r0:r1].exp_()
+    if kind == "zero_inflated":
+        cols = torch.randperm(d, generator=g, device=device)[:max(1, int(round(0.2 * d)))]
+        for c in cols.tolist():
+            X[:, c].masked_fill_(torch.rand(n, generator=g, device=device) < 0.5, 0.0)
+    if kind == "lognormal_rankgauss":
+        q = torch.special.ndtri((torch.arange(n_tr, device=device, dtype=torch.float64) + 0.5) / n_tr).float()
+        for j in range(d):
+            col = X[:n_tr, j]
+            srt, order = torch.sort(col)
+            ranks = torch.empty_like(order)
+            ranks[order] = torch.arange(n_tr, device=device)
+            va = X[n_tr:, j]
+            pos = torch.searchsorted(srt, va).clamp(1, n_tr - 1)
+            lo, hi = srt[pos - 1], srt[pos]
+            w = ((va - lo) / (hi - lo).clamp_min(1e-30)).clamp(0, 1)
+            X[n_tr:, j] = q[pos - 1] + w * (q[pos] - q[pos - 1])
+            X[:n_tr, j] = q[ranks]
+    W1 = torch.randn((d, 32), generator=g, device=device) / d ** 0.5
+    W2 = torch.randn((32, cfg["d_out"]), generator=g, device=device) / 32 ** 0.5
+    T = torch.empty((n, cfg["d_out"]), dtype=torch.float32, device=device)
+    for r0 in range(0, n, chunk):
+        T[r0:r0 + chunk] = torch.tanh(X[r0:r0 + chunk] @ W1) @ W2
+    lab = cfg["label"]
+    if lab == "sign":
+        y = (T[:, 0] > 0).float()
+    elif lab == "argmax":
+        y = T.argmax(dim=1).to(torch.int32)
+    else:
+        t = T[:, 0].double()
+        if lab == "teacher_noise":
+            t = t + 0.1 * torch.randn(n, generator=g, device=device, dtype=torch.float64)
+        else:
+            t = t / t[:n_tr].std().clamp_min(1e-12)
+            z = torch.randn(n, generator=g, device=device, dtype=torch.float64)
+            chi2 = (torch.randn((n, 3), generator=g, device=device, dtype=torch.float64) ** 2).sum(dim=1)
+            t = t + 0.1 * z / torch.sqrt(chi2 / 3.0)  # Student-t with 3 degrees of freedom
+        y = ((t - t[:n_tr].mean()) / t[:n_tr].std().clamp_min(1e-12)).float()
+    return X[:n_tr], y[:n_tr].contiguous(), X[n_tr:], y[n_tr:].contiguous()
+
+
+def epoch_orders_device(cfg, epoch, n_train, device="cuda"):
+    """Per-member permutations of the training rows on the device: int32 [K, n_train]."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(cfg["seed"]) * 16 + 4 + 256 * int(epoch))
+    return torch.stack([torch.randperm(n_train, generator=g, device=device, dtype=torch.int64)
+                        for _ in range(cfg["K"])]).to(torch.int32)

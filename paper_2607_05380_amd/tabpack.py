@@ -21,7 +21,8 @@ PRECISIONS = {"bf16": 0, "fp32": 1}
 SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "pack_workspace_size",
            "pack_bind", "pack_train_step", "pack_eval_members", "pack_select_workspace_size",
            "pack_select", "pack_member_param_count", "pack_get_params", "pack_set_params",
-           "pack_get_grads", "pack_get_moments", "pack_debug_dropout_mask", "pack_debug_activation"]
+           "pack_get_grads", "pack_get_moments", "pack_debug_dropout_mask", "pack_debug_activation",
+           "pack_profile_enable", "pack_profile_read"]
 
 
 class MemberHP(ctypes.Structure):
@@ -42,6 +43,11 @@ class PackConfig(ctypes.Structure):
                 ("wd_lo", ctypes.c_double), ("wd_hi", ctypes.c_double),
                 ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
                 ("seed", ctypes.c_uint64), ("members", ctypes.POINTER(MemberHP))]
+
+
+class KernelStat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 64), ("kind", ctypes.c_int32), ("launches", ctypes.c_int32),
+                ("total_ms", ctypes.c_double), ("work", ctypes.c_double)]
 
 
 class PackError(RuntimeError):
@@ -79,6 +85,8 @@ def load_library(path=LIB_PATH):
         "pack_get_moments": ([H, i32, vp, vp], ctypes.c_int),
         "pack_debug_dropout_mask": ([H, u64, i32, i32, vp, vp], ctypes.c_int),
         "pack_debug_activation": ([H, i32, i32, vp], ctypes.c_int),
+        "pack_profile_enable": ([H, i32], ctypes.c_int),
+        "pack_profile_read": ([H, ctypes.POINTER(KernelStat), i32, ctypes.POINTER(i32)], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -261,6 +269,20 @@ class Pack:
         _check(self.lib.pack_debug_dropout_mask(self.h, int(step), layer, k, out.data_ptr(), _stream()))
         torch.cuda.current_stream().synchronize()
         return out.cpu().numpy().astype(bool)
+
+    def profile(self, enable):
+        _check(self.lib.pack_profile_enable(self.h, 1 if enable else 0))
+
+    def profile_read(self):
+        """[{name, kind ('mfma'|'hbm'), launches, total_ms, avg_ms, work_per_launch}]"""
+        arr = (KernelStat * 64)()
+        n = ctypes.c_int32()
+        _check(self.lib.pack_profile_read(self.h, arr, 64, ctypes.byref(n)))
+        out = []
+        for s in arr[:n.value]:
+            out.append(dict(name=s.name.decode(), kind="mfma" if s.kind == 0 else "hbm", launches=s.launches,
+                            total_ms=s.total_ms, avg_ms=s.total_ms / max(s.launches, 1), work=s.work))
+        return out
 
     def debug_activation(self, layer, k):
         w = self.hparams()[k]["width"]

@@ -8,6 +8,13 @@ Tolerances (element test |gpu - ref| <= atol + rtol * |ref|):
   Frobenius error <= 2e-2.
   fp32 MFMA mode: rtol 1e-4 everywhere, gradient floor 1e-4 * max|g_ref|,
   Frobenius <= 1e-4.
+In bf16 mode the reference is the oracle's bf16 policy (bf16 operands of the
+hidden matrix products, see oracle.mlp): the ReLU/dropout decisions then rest
+on the same rounded forward values as the kernels'.  Against the exact fp64
+oracle, about 0.1-0.5% of the ReLU decisions legitimately flip (|Z| below the
+bf16 rounding noise), and each flip moves a whole dZ element, so gradients
+there are checked by their relative Frobenius error against FP64_GRAD_FROB and
+parameters with the sign-flip allowance on elements with |g| < 0.25 rms(g).
 Parameters after a step: the first AdamW step moves an element by about
 lr * sign(g), so an element whose oracle gradient lies inside its own gradient
 tolerance band may legitimately move the other way; for those elements only
@@ -21,6 +28,8 @@ from paper_2607_05380_amd import synth
 
 TOL = {"bf16": dict(rtol=2e-2, atol=1e-3, gfloor=1e-3, frob=2e-2),
        "fp32": dict(rtol=1e-4, atol=1e-6, gfloor=1e-4, frob=1e-4)}
+
+FP64_GRAD_FROB = 0.25
 
 ORACLE_KEYS = ("seed", "K", "d_in", "d_out", "L", "B", "task", "beta1", "beta2", "eps", "decay_bias",
                "width_lo", "width_hi", "dropout_lo", "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi")
@@ -58,11 +67,12 @@ def check_tensor(name, gpu, ref, tol, grad=False, report=None):
     return frob
 
 
-def check_params_after_step(name, gpu, ref, before, grad_ref, lr, tol, report=None):
+def check_params_after_step(name, gpu, ref, before, grad_ref, lr, tol, report=None, band=None):
     """Parameter check with the sign-flip allowance of the first AdamW steps."""
     gpu = np.asarray(gpu, np.float64)
     ok = close_mask(gpu, ref, tol["rtol"], tol["atol"])
-    band = np.abs(grad_ref) <= tol["gfloor"] * np.abs(grad_ref).max() + tol["rtol"] * np.abs(grad_ref)
+    if band is None:
+        band = np.abs(grad_ref) <= tol["gfloor"] * np.abs(grad_ref).max() + tol["rtol"] * np.abs(grad_ref)
     flip_ok = np.abs(gpu - ref) <= 2 * lr * (1 + 1e-6) + tol["atol"] + tol["rtol"] * np.abs(ref)
     good = ok | (band & flip_ok)
     if report is not None:
@@ -103,3 +113,24 @@ def compare_member(pk, op, k, tol, grads_gpu=True, report=None, prefix=""):
         # v = sum of (1-b2) b2^i g^2: compare sqrt(v), which scales like |g|
         check_tensor(tag + ".sqrtv", np.sqrt(v_gpu[l][0]), np.sqrt(op.v[k][l][0]), tol, grad=True,
                      report=report)
+
+
+def compare_member_fp64(pk, op64, k, report=None, prefix=""):
+    """bf16 GPU member vs the exact fp64 oracle: losses and parameters at the
+    2e-2 / 1e-3 tolerance (sign-flip allowance on small gradients), gradient
+    Frobenius error bounded by FP64_GRAD_FROB."""
+    tol = TOL["bf16"]
+    lr = op64.hp[k]["lr"]
+    g_gpu = pk.get_grads(k)
+    p_gpu = pk.get_params(k)
+    worst = 0.0
+    for l in range(len(op64.params[k])):
+        gW, gb = op64.last_grads[k][l]
+        for nm, g, r, pg, pr in (("W", g_gpu[l][0], gW, p_gpu[l][0], op64.params[k][l][0]),
+                                 ("b", g_gpu[l][1], gb, p_gpu[l][1], op64.params[k][l][1])):
+            frob = np.linalg.norm(np.asarray(g, np.float64) - r) / max(np.linalg.norm(r), 1e-30)
+            worst = max(worst, frob)
+            assert frob <= FP64_GRAD_FROB, f"{prefix}m{k}.{nm}{l}: grad frob vs fp64 {frob:.3f}"
+            band = np.abs(r) <= 0.25 * np.sqrt(np.mean(r * r))
+            check_params_after_step(f"{prefix}m{k}.{nm}{l}", pg, pr, None, r, lr, tol, report, band=band)
+    return worst

@@ -7,7 +7,8 @@ from oracle.greedy import greedy_select
 from oracle.mlp import dropout_mask
 from oracle.pack import OraclePack
 from paper_2607_05380_amd import configs, tabpack
-from parity import TOL, check_tensor, compare_member, make_inputs, oracle_cfg, oracle_hparams, to_dev
+from parity import (TOL, check_tensor, compare_member, compare_member_fp64, make_inputs, oracle_cfg,
+                    oracle_hparams, to_dev)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -24,20 +25,26 @@ SMALL = {
 }
 
 
-def run_step(cfg, members=None, n_train=4096, n_val=600, steps=1):
+def run_step(cfg, members=None, n_train=4096, n_val=600, steps=1, with_fp64=False):
+    """Train the GPU pack and the oracle (in the pack's precision policy; plus the
+    exact fp64 oracle when asked) for ``steps`` steps on the same batches."""
+    from paper_2607_05380_amd import synth
     Xtr, ytr, Xva, yva, orders, idx = make_inputs(cfg, n_train, n_val)
     pk = tabpack.Pack(cfg, members=members).bind()
-    op = OraclePack(oracle_cfg(cfg), hparams=oracle_hparams(cfg, members))
+    prec = "bf16" if cfg["precision"] == "bf16" else "fp64"
+    op = OraclePack(oracle_cfg(cfg), hparams=oracle_hparams(cfg, members), precision=prec)
+    op64 = OraclePack(oracle_cfg(cfg), hparams=oracle_hparams(cfg, members)) if with_fp64 else None
     X, y = to_dev(Xtr, ytr)
     losses = []
     for s in range(1, steps + 1):
-        from paper_2607_05380_amd import synth
         idx = synth.batch_indices(orders, s - 1, cfg["B"])
         (idx_d,) = to_dev(idx)
         lg = pk.train_step(X, y, idx_d, s)
         torch.cuda.synchronize()
         lo = op.train_step(Xtr, ytr, idx, s)
-        losses.append((lg.cpu().numpy(), lo))
+        lo64 = op64.train_step(Xtr, ytr, idx, s) if with_fp64 else None
+        losses.append((lg.cpu().numpy(), lo, lo64))
+    run_step.op64 = op64
     return pk, op, losses, (Xtr, ytr, Xva, yva)
 
 
@@ -46,21 +53,26 @@ def test_train_step_parity(name):
     cfg = configs.workload(name, **SMALL[name])
     tol = TOL[cfg["precision"]]
     print(f"[parity] {name} K={cfg['K']} B={cfg['B']} prec={cfg['precision']}", flush=True)
-    pk, op, losses, _ = run_step(cfg)
-    lg, lo = losses[0]
+    bf16 = cfg["precision"] == "bf16"
+    pk, op, losses, _ = run_step(cfg, with_fp64=bf16)
+    lg, lo, lo64 = losses[0]
     check_tensor("loss", lg, lo, tol)
     report = []
     for k in range(cfg["K"]):
         compare_member(pk, op, k, tol, report=report)
     worst = max(report, key=lambda r: r[1])
-    print(f"[parity] {name}: worst {worst}", flush=True)
+    print(f"[parity] {name}: worst vs oracle ({'bf16 policy' if bf16 else 'fp64'}) {worst}", flush=True)
+    if bf16:
+        check_tensor("loss64", lg, lo64, tol)
+        w64 = max(compare_member_fp64(pk, run_step.op64, k) for k in range(cfg["K"]))
+        print(f"[parity] {name}: worst gradient frob vs exact fp64 oracle {w64:.4f}", flush=True)
 
 
 def test_three_steps_parity_bf16():
     cfg = configs.workload("regression_large", K=3, B=256)
     tol = TOL["bf16"]
     pk, op, losses, _ = run_step(cfg, steps=3)
-    for lg, lo in losses:
+    for lg, lo, _ in losses:
         check_tensor("loss", lg, lo, tol)
     for k in range(3):
         compare_member(pk, op, k, tol, prefix="t3.")
@@ -145,7 +157,8 @@ def test_eval_members_parity(name):
     tol = TOL[cfg["precision"]]
     Xtr, ytr, Xva, yva, _, _ = make_inputs(cfg, 2000, 1300 if name != "binary_small" else 512)
     pk = tabpack.Pack(cfg).bind()
-    op = OraclePack(oracle_cfg(cfg), hparams=oracle_hparams(cfg))
+    op = OraclePack(oracle_cfg(cfg), hparams=oracle_hparams(cfg),
+                    precision="bf16" if cfg["precision"] == "bf16" else "fp64")
     Xv, yv = to_dev(Xva, yva)
     pred, score = pk.eval_members(Xv, yv)
     torch.cuda.synchronize()

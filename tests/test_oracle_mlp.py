@@ -207,3 +207,59 @@ def test_pack_members_match_standalone_and_are_independent():
             np.testing.assert_array_equal(pack2.params[k][l][0], pack.params[k][l][0])
             np.testing.assert_array_equal(pack2.last_grads[k][l][1], pack.last_grads[k][l][1])
     assert losses2[1] != losses[1]
+
+
+def test_to_bf16_matches_torch_rounding():
+    rng = np.random.default_rng(9)
+    x = np.concatenate([rng.standard_normal(20000) * 10 ** rng.uniform(-30, 30, 20000),
+                        # exact ties between two bf16 neighbours, both parities
+                        (np.arange(1, 2001, dtype=np.float64) * 2 ** -7 + 2 ** -16) * 3.0,
+                        [0.0, -0.0, 1.0, -2.5, 3.0e38]])
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(mlp.to_bf16(x), ref)
+
+
+class _RoundFwd(torch.autograd.Function):
+    """bf16 rounding of a value, gradient passed straight through."""
+    @staticmethod
+    def forward(ctx, x):
+        return x.float().to(torch.bfloat16).to(torch.float64)
+
+    @staticmethod
+    def backward(ctx, g):
+        return g
+
+
+class _RoundGrad(torch.autograd.Function):
+    """Identity forward, bf16 rounding of the incoming gradient."""
+    @staticmethod
+    def forward(ctx, x):
+        return x.clone()
+
+    @staticmethod
+    def backward(ctx, g):
+        return g.float().to(torch.bfloat16).to(torch.float64)
+
+
+@pytest.mark.parametrize("task,d_out", TASKS)
+def test_bf16_policy_matches_torch_straight_through(task, d_out):
+    # The bf16 policy built independently in torch: bf16 operands of every hidden
+    # matrix product (straight-through), rounded dZ for dW/dH but not for db.
+    params, X, y, masks = _tiny(task, d_out, 7, d_in=9, widths=(12, 10), B=17)
+    s = 1.0 / (1 - 0.3)
+    Y, cache = mlp.forward(params, X, masks, s, rnd=mlp.to_bf16)
+    loss, dY = mlp.loss_and_dy(Y, y, task)
+    grads = mlp.backward(params, cache, dY, masks, s)
+    tW = [torch.tensor(W, requires_grad=True) for W, _ in params]
+    tb = [torch.tensor(b, requires_grad=True) for _, b in params]
+    H = _RoundFwd.apply(torch.from_numpy(X))
+    for l in range(2):
+        Z = _RoundGrad.apply(H @ _RoundFwd.apply(tW[l]).T) + tb[l]
+        H = _RoundFwd.apply(torch.relu(Z) * torch.from_numpy(masks[l].astype(np.float64)) * s)
+    Yt = H @ tW[2].T + tb[2]
+    lt = _torch_loss(Yt, y, task)
+    lt.backward()
+    assert lt.item() == pytest.approx(loss, rel=1e-12)
+    for l in range(3):
+        np.testing.assert_allclose(grads[l][0], tW[l].grad.numpy(), rtol=1e-10, atol=1e-14)
+        np.testing.assert_allclose(grads[l][1], tb[l].grad.numpy(), rtol=1e-10, atol=1e-14)
