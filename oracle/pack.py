@@ -21,15 +21,18 @@ class OraclePack:
     operands (parameters, moments and updates stay float64).
     """
 
-    def __init__(self, cfg, hparams=None, params=None, precision="fp64"):
+    def __init__(self, cfg, hparams=None, params=None, precision="fp64", members=None):
+        """``members``: optional subset of member indices to materialise (the
+        others stay None and must not be stepped)."""
         self.cfg = dict(cfg)
         self.rnd = mlp.to_bf16 if precision == "bf16" else None
         self.hp = hparams if hparams is not None else sample_hparams(cfg)
+        keep = set(range(len(self.hp)) if members is None else members)
         if params is None:
-            params = [init_member(cfg, k, h["width"]) for k, h in enumerate(self.hp)]
-        self.params = [[(W.copy(), b.copy()) for W, b in p] for p in params]
-        self.m = [[(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
-        self.v = [[(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
+            params = [init_member(cfg, k, h["width"]) if k in keep else None for k, h in enumerate(self.hp)]
+        self.params = [None if p is None else [(W.copy(), b.copy()) for W, b in p] for p in params]
+        self.m = [None if p is None else [(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
+        self.v = [None if p is None else [(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
         self.t = 0
         self.last_grads = None
 
