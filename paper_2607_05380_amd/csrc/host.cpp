@@ -38,7 +38,6 @@ int fail(int code, const char* fmt, ...) {
   } while (0)
 
 constexpr uint32_t kTagHparam = 1, kTagInit = 2;
-constexpr int kTileM = 128, kTileN = 128;  // grouped-GEMM output tile
 
 int64_t round_up(int64_t x, int64_t q) { return (x + q - 1) / q * q; }
 
@@ -92,9 +91,11 @@ struct ProfGroup {
 struct Bufs {
   float *theta = nullptr, *grad = nullptr, *m = nullptr, *v = nullptr;
   uint16_t* shadow = nullptr;
+  char* H0 = nullptr;  // gathered batches (K x [Bp, Pin]) in the GEMM precision
   char* H = nullptr;   // L activation buffers H_1..H_L
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
-  float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / 64 floats
+  float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / kPartRows floats
+  char* zeros = nullptr;     // 256 zero bytes: GEMM loads of out-of-range elements read them
   float *dY = nullptr, *rowloss = nullptr;
   MemberDev* d_mem = nullptr;
   uint32_t* d_chunks = nullptr;
@@ -118,6 +119,7 @@ struct pack_handle {
   bool bound = false;
   Bufs b;
   std::vector<Launch> fwd, dx, dw;  // per layer (index l-1)
+  Launch fwd1_eval{};                // layer 1 over the shared validation rows in H_0 block 0
   int ncoltiles = 0;
   uint64_t t = 0;
 
@@ -130,6 +132,7 @@ struct pack_handle {
 
   size_t elt() const { return prec == Prec::BF16 ? 2 : 4; }
   void* Hl(int l) const { return b.H + (size_t)(l - 1) * A * elt(); }  // H_l, l = 1..L
+  size_t h0_elems() const { return (size_t)Bp * Pin; }                  // one member's H_0
   void* dzb(int l) const { return b.dz + (size_t)(l & 1) * A * elt(); } // buffer holding dZ_l
 };
 
@@ -276,27 +279,90 @@ int64_t member_span_end(const pack_handle* h, int k) {
 
 // Device-table sizes.
 struct Plan {
+  bool small_only = false;    // fp32 GEMMs run small tiles only
   std::vector<GemmDesc> descs;
   std::vector<Tile> tiles;
+  std::vector<int64_t> cost;  // planner's cost of each tile (depth x valid area)
   std::vector<ColTile> coltiles;
   std::vector<Launch> fwd, dx, dw;
+  Launch fwd1_eval{};
 };
 
+// Tiles of one member's M x N output: big 256 x 256 tiles, except that a
+// remainder of at most 128 rows or columns is covered by a strip of small
+// 128 x 128 tiles (a larger remainder takes one more, partly filled, big tile).
 void add_tiles(Plan& p, Launch& ln, int d, int M, int N, int kdepth) {
-  for (int m0 = 0; m0 < M; m0 += kTileM)
-    for (int n0 = 0; n0 < N; n0 += kTileN) p.tiles.push_back(Tile{d, m0, n0, kdepth});
+  auto big_end = [&](int E) {
+    if (p.small_only) return 0;
+    const int r = E % kBigTile;
+    return r == 0 ? E : (r > kSmallTile ? E - r + kBigTile : E - r);
+  };
+  const int Mb = big_end(M), Nb = big_end(N);
+  auto push = [&](int m0, int n0, int shape) {
+    const int ts = shape == kShapeBig ? kBigTile : kSmallTile;
+    const int mb = std::min(ts, M - m0), nb = std::min(ts, N - n0);
+    p.tiles.push_back(Tile{d, m0, n0, shape});
+    p.cost.push_back((int64_t)kdepth * std::max(mb, 0) * std::max(nb, 0));
+  };
+  for (int m0 = 0; m0 < Mb; m0 += kBigTile)
+    for (int n0 = 0; n0 < Nb; n0 += kBigTile) push(m0, n0, kShapeBig);
+  for (int m0 = 0; m0 < Mb; m0 += kSmallTile)
+    for (int n0 = Nb; n0 < N; n0 += kSmallTile) push(m0, n0, kShapeSmall);
+  for (int m0 = Mb; m0 < M; m0 += kSmallTile)
+    for (int n0 = 0; n0 < N; n0 += kSmallTile) push(m0, n0, kShapeSmall);
   ln.ntiles = (int)p.tiles.size() - ln.tile0;
 }
 
-// Longest-processing-time order: deepest K loops first, so the ragged tail of
-// the launch is made of short tiles.
+// Launch order of one grouped GEMM.  Workgroup i runs on XCD i % 8, and each
+// XCD has its own L2, so all tiles of a member go to one XCD (members are
+// packed into the 8 XCD bins longest-first by total cost), and within a bin
+// tiles run longest-first so the launch ends on short tiles.
 void sort_launch(Plan& p, const Launch& ln) {
-  std::stable_sort(p.tiles.begin() + ln.tile0, p.tiles.begin() + ln.tile0 + ln.ntiles,
-                   [](const Tile& a, const Tile& b) { return a.kdepth > b.kdepth; });
+  struct Item {
+    Tile t;
+    int64_t cost;
+  };
+  std::vector<Item> items;
+  for (int i = 0; i < ln.ntiles; ++i) items.push_back(Item{p.tiles[ln.tile0 + i], p.cost[ln.tile0 + i]});
+  std::vector<std::pair<int64_t, int>> member_cost;  // (cost, desc)
+  for (const Item& it : items) {
+    auto f = std::find_if(member_cost.begin(), member_cost.end(),
+                          [&](const std::pair<int64_t, int>& e) { return e.second == it.t.desc; });
+    if (f == member_cost.end())
+      member_cost.push_back({it.cost, it.t.desc});
+    else
+      f->first += it.cost;
+  }
+  std::stable_sort(member_cost.begin(), member_cost.end(),
+                   [](const std::pair<int64_t, int>& a, const std::pair<int64_t, int>& b) { return a.first > b.first; });
+  std::vector<int64_t> load(kXcds, 0);
+  std::vector<int> bin_of(p.descs.size() + 1, 0);
+  for (const auto& mc : member_cost) {
+    const int b = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    load[b] += mc.first;
+    bin_of[mc.second] = b;
+  }
+  std::vector<std::vector<Item>> bins(kXcds);
+  for (const Item& it : items) bins[bin_of[it.t.desc]].push_back(it);
+  for (auto& b : bins)
+    std::stable_sort(b.begin(), b.end(), [](const Item& x, const Item& y) { return x.cost > y.cost; });
+  std::vector<size_t> next(kXcds, 0);
+  for (int i = 0; i < ln.ntiles; ++i) {
+    int b = i % kXcds;
+    if (next[b] == bins[b].size()) {  // this XCD's bin is empty: take from the fullest remaining
+      size_t best = 0;
+      for (int c = 0; c < kXcds; ++c)
+        if (bins[c].size() - next[c] > best) best = bins[c].size() - next[c], b = c;
+    }
+    p.tiles[ln.tile0 + i] = bins[b][next[b]].t;
+    p.cost[ln.tile0 + i] = bins[b][next[b]].cost;
+    ++next[b];
+  }
 }
 
 Plan build_plan(const pack_handle* h, const Bufs& bf) {
   Plan p;
+  p.small_only = h->prec == Prec::FP32;
   const pack_config& c = h->cfg;
   const size_t es = h->elt();
   const void* wsrc = h->prec == Prec::BF16 ? (const void*)bf.shadow : (const void*)bf.theta;
@@ -306,14 +372,15 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     return (const char*)wsrc + (size_t)h->mem[k].toff[2 * (l - 1)] * es;
   };
   auto act = [&](void* base, int k) -> void* { return (char*)base + (size_t)h->mem[k].act_off * es; };
+  auto h0 = [&](int k) -> void* { return bf.H0 + (size_t)k * h->h0_elems() * es; };
   for (int l = 1; l <= c.L; ++l) {
     // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
     Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
     for (int k = 0; k < c.K; ++k) {
       const Member& m = h->mem[k];
       GemmDesc d{};
-      d.A = l == 1 ? nullptr : act(Hl(l - 1), k);
-      d.lda = m.dp;
+      d.A = l == 1 ? h0(k) : act(Hl(l - 1), k);
+      d.lda = l == 1 ? h->Pin : m.dp;
       d.B = wptr(k, l);
       d.ldb = l == 1 ? h->Pin : m.dp;
       d.C = act(Hl(l), k);
@@ -333,6 +400,18 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     sort_launch(p, f);
     p.fwd.push_back(f);
   }
+  {
+    // evaluation, layer 1: every member reads the same validation rows (H_0 block 0)
+    Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
+    for (int k = 0; k < c.K; ++k) {
+      GemmDesc d = p.descs[p.fwd[0].desc0 + k];
+      d.A = h0(0);
+      p.descs.push_back(d);
+      add_tiles(p, f, f.desc0 + k, h->Bp, h->mem[k].dp, d.Kd);
+    }
+    sort_launch(p, f);
+    p.fwd1_eval = f;
+  }
   for (int l = 1; l <= c.L; ++l) {
     // weight gradient: dW_l^T[out, in] = sum_rows dZ_l[row, out] H_{l-1}[row, in]
     Launch w{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
@@ -341,8 +420,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       GemmDesc d{};
       d.A = act(dzb(l), k);
       d.lda = m.dp;
-      d.B = l == 1 ? nullptr : act(Hl(l - 1), k);
-      d.ldb = m.dp;
+      d.B = l == 1 ? h0(k) : act(Hl(l - 1), k);
+      d.ldb = l == 1 ? h->Pin : m.dp;
       d.C = bf.grad + m.toff[2 * (l - 1)];
       d.ldc = l == 1 ? h->Pin : m.dp;
       d.M = m.dp;
@@ -368,7 +447,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
         d.ldb = m.dp;
         d.C = act(dzb(l - 1), k);
         d.Haux = act(Hl(l - 1), k);
-        d.colpart = bf.colpart + h->mem[k].act_off / 64;
+        d.colpart = bf.colpart + h->mem[k].act_off / kPartRows;
         d.ldc = m.dp;
         d.M = h->Bp;
         d.N = m.dp;
@@ -410,9 +489,11 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
   bf.m = cv.take<float>(h->P);
   bf.v = cv.take<float>(h->P);
   bf.shadow = h->prec == Prec::BF16 ? cv.take<uint16_t>(h->P) : nullptr;
+  bf.H0 = cv.take<char>((size_t)c.K * h->h0_elems() * h->elt());
   bf.H = cv.take<char>((size_t)c.L * h->A * h->elt());
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
-  bf.colpart = cv.take<float>((size_t)h->A / 64);
+  bf.colpart = cv.take<float>((size_t)h->A / kPartRows);
+  bf.zeros = cv.take<char>(256);
   bf.dY = cv.take<float>((size_t)c.K * h->Bp * c.d_out);
   bf.rowloss = cv.take<float>((size_t)c.K * h->Bp);
   bf.d_mem = cv.take<MemberDev>(c.K);
@@ -438,11 +519,10 @@ GemmArgs base_args(const pack_handle* h) {
   GemmArgs a{};
   a.descs = h->b.d_descs;
   a.tiles = h->b.d_tiles;
+  a.zeros = h->b.zeros;
   const Key kd = stream_key(h->cfg.seed, kTagDropout);
   a.key0 = kd.k0;
   a.key1 = kd.k1;
-  a.d_in = h->cfg.d_in;
-  a.idx_stride = h->cfg.B;
   return a;
 }
 
@@ -594,6 +674,7 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   h->fwd = plan.fwd;
   h->dx = plan.dx;
   h->dw = plan.dw;
+  h->fwd1_eval = plan.fwd1_eval;
   h->ncoltiles = (int)plan.coltiles.size();
   h->t = 0;
   h->bound = true;
@@ -610,8 +691,6 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                                     (unsigned long long)(h->t + 1));
   const pack_config& c = h->cfg;
   GemmArgs a = base_args(h);
-  a.X = X;
-  a.idx = idx;
   a.rows_valid = c.B;
   a.step = as_u32(step);
   const double act_bytes = (double)c.B * h->elt() * [&] {
@@ -625,7 +704,10 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, stream,
                  [&] { return launch_gemm(h->prec, ak, bk, e, al, stream); });
   };
-  for (int l = 1; l <= c.L; ++l) HIP_TRY(gemm(l == 1 ? OP_XGK : OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[l - 1], l));
+  HIP_TRY(timed(h, "gather", 1, (double)c.K * c.B * c.d_in * (4.0 + h->elt()), stream, [&] {
+    return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, c.K, h->Bp, h->b.H0, stream);
+  }));
+  for (int l = 1; l <= c.L; ++l) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[l - 1], l));
   HIP_TRY(timed(h, "head_fwd", 1, act_bytes, stream, [&] {
     return launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, y,
                            idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, stream);
@@ -639,11 +721,11 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                            c.d_out, h->b.dY, h->dzb(c.L), h->b.grad, stream);
   }));
   for (int l = c.L; l >= 1; --l) {
-    HIP_TRY(gemm(OP_RMAJ, l == 1 ? OP_XGR : OP_RMAJ, EPI_DW, h->dw[l - 1], l));
+    HIP_TRY(gemm(OP_RMAJ, OP_RMAJ, EPI_DW, h->dw[l - 1], l));
     if (l > 1) {
       HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[l - 1], l));
-      HIP_TRY(timed(h, "bias_from_partials", 1, act_bytes * 4 / h->elt() / 64, stream, [&] {
-        return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp / 64,
+      HIP_TRY(timed(h, "bias_from_partials", 1, act_bytes * 4 / h->elt() / kPartRows, stream, [&] {
+        return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp / kPartRows,
                                          h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, stream);
       }));
     }
@@ -669,15 +751,13 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
   if (Nv < 1) return fail(PACK_EINVAL, "Nv=%lld must be positive", (long long)Nv);
   const pack_config& c = h->cfg;
   GemmArgs a = base_args(h);
-  a.X = Xv;
-  a.idx = nullptr;
   for (int64_t r0 = 0; r0 < Nv; r0 += h->Bp) {
-    a.row_base = r0;
     a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
+    HIP_TRY(launch_gather(h->prec, Xv, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, stream));
     for (int l = 1; l <= c.L; ++l) {
-      GemmArgs al = for_launch(a, h->fwd[l - 1]);
+      GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[l - 1]);
       al.layer = l;
-      HIP_TRY(launch_gemm(h->prec, l == 1 ? OP_XGK : OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
+      HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
     }
     HIP_TRY(launch_head_fwd(h->prec, h->task, true, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, yv,
                             nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, stream));

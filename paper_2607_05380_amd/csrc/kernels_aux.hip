@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* 
   }
 }
 
-// db_l[c] = sum of the per-64-row column partials written by the dX epilogue,
+// db_l[c] = sum of the per-row-block column partials written by the dX epilogue,
 // in a fixed order; 64 columns of one member per workgroup.
 __global__ __launch_bounds__(64) void bias_from_partials_kernel(const float* part, const MemberDev* mem,
                                                                 const ColTile* tiles, int nparts,
@@ -226,10 +226,47 @@ __global__ __launch_bounds__(64) void bias_from_partials_kernel(const float* par
   const MemberDev md = mem[ct.member];
   const int c = ct.c0 + threadIdx.x;
   if (c >= md.dp) return;
-  const float* p = part + md.act_off / 64;
+  const float* p = part + md.act_off / kPartRows;
   float s = 0.0f;
   for (int r = 0; r < nparts; ++r) s += p[(int64_t)r * md.dp + c];
   grad[bias_off[ct.member] + c] = s;
+}
+
+// ----------------------------------------------------------------- gather --
+// H_0 of member k, row r: the feature row X[idx[k * B + r]] (or X[row_base + r]
+// for contiguous rows) in the GEMM precision, zero-padded to Pin columns; rows
+// r >= rows_valid are zero.  One wave per row, float4 reads.
+template <typename T>
+__global__ __launch_bounds__(256) void gather_kernel(const float* X, int d_in, int Pin, const int32_t* idx,
+                                                     int B, int64_t row_base, int rows_valid, int Bp, T* H0) {
+  const int k = blockIdx.y;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= Bp) return;
+  T* dst = H0 + ((int64_t)k * Bp + r) * Pin;
+  const bool valid = r < rows_valid;
+  const int64_t src = valid ? (idx ? (int64_t)idx[(int64_t)k * B + r] : row_base + r) : 0;
+  const float* x = X + src * d_in;
+  const bool vec = (d_in % 4 == 0) && ((reinterpret_cast<uintptr_t>(X) & 15) == 0);
+  for (int c = lane * 4; c < Pin; c += 256) {
+    float v[4];
+    if (valid && vec && c + 4 <= d_in) {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(x + c);
+      v[0] = q[0], v[1] = q[1], v[2] = q[2], v[3] = q[3];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = (valid && c + e < d_in) ? x[c + e] : 0.0f;
+    }
+    if constexpr (sizeof(T) == 2) {
+      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[0]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[1]) << 16);
+      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[3]) << 16);
+      *reinterpret_cast<u32x2*>(dst + c) = u32x2{lo, hi};
+    } else {
+      *reinterpret_cast<f32x4*>(dst + c) = f32x4{v[0], v[1], v[2], v[3]};
+    }
+  }
 }
 
 // ------------------------------------------------------------------ AdamW --
@@ -473,6 +510,18 @@ hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, co
                                      hipStream_t s) {
   hipLaunchKernelGGL(bias_from_partials_kernel, dim3(ntiles), dim3(64), 0, s, part, mem, tiles, nparts,
                      bias_off, grad);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
+                         int64_t row_base, int rows_valid, int members, int Bp, void* H0, hipStream_t s) {
+  const dim3 grid((Bp + 3) / 4, members);
+  if (prec == Prec::BF16)
+    hipLaunchKernelGGL((gather_kernel<__bf16>), grid, dim3(256), 0, s, X, d_in, Pin, idx, B, row_base,
+                       rows_valid, Bp, static_cast<__bf16*>(H0));
+  else
+    hipLaunchKernelGGL((gather_kernel<float>), grid, dim3(256), 0, s, X, d_in, Pin, idx, B, row_base,
+                       rows_valid, Bp, static_cast<float*>(H0));
   return hipGetLastError();
 }
 

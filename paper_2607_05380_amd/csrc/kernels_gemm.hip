@@ -1,24 +1,51 @@
 // Grouped ragged GEMM for the packed MLP step on gfx950 (CDNA4).
 //
 // One launch covers one GEMM kind of one layer for all K members: the host
-// planner emits a list of 128x128 output tiles (member, m0, n0) over each
-// member's own, q-padded extents, so members of different widths share a
-// launch without padding to the widest member (the paper's packing grows
-// every member to the maximum width and uses a batched matmul, Section 3.3;
-// here only the tile quantum is wasted).
+// planner emits a list of output tiles (member, m0, n0, shape) over each
+// member's own q-padded extents, so members of different widths share a launch
+// without padding to the widest member (the paper's packing grows every member
+// to the maximum width and uses a batched matmul, Section 3.3).
 //
-// Per workgroup: 256 threads = 4 wave64s in a 2x2 grid, each wave owning a
-// 64x64 sub-tile as 2x2 MFMA 32x32 blocks (bf16: v_mfma_f32_32x32x16_bf16,
-// fp32: v_mfma_f32_32x32x2_f32), fp32 accumulation.  Operand tiles are staged
-// through LDS (double-buffered, one barrier per K step) in a depth-contiguous
-// [row][16-byte vectors] layout; operands stored rows-contiguous in HBM are
-// transposed in registers while being written to LDS, and the first layer
-// gathers its member's fp32 feature rows straight from X (no materialised
-// batch).  Epilogues are fused:
+// Workgroup: 256 threads = 4 wave64s in a 2 x 2 grid.  Two tile shapes share
+// one kernel (the shape is uniform per workgroup):
+//   big   256 x 256: each wave owns 128 x 128 = 4 x 4 MFMA 32x32 blocks.  Per K
+//         step of 16 a wave reads 8 KB of fragments from LDS for 16 MFMAs,
+//         64 B/clk per CU at the MFMA rate -- inside gfx950's LDS bandwidth
+//         (about 96 B/clk measured for 16-byte reads), which a 64 x 64 wave
+//         tile exceeds by 2x.
+//   small 128 x 128 (waves 64 x 64) covers the ragged edge of a member when
+//         its remainder is at most 128 rows or columns.
+// MFMA: v_mfma_f32_32x32x16_bf16 (fp32 mode: v_mfma_f32_32x32x2_f32), fp32
+// accumulators in AGPRs.  A wave whose sub-tile lies wholly outside the
+// member's extents skips its MFMAs.
+//
+// Staging: per K step (128 bytes of depth per row: 64 bf16 / 32 fp32) each
+// operand tile goes HBM -> LDS, double-buffered with one barrier per step; the
+// loads of step k + 1 are in flight during the MFMAs of step k.  bf16 uses
+// direct-to-LDS loads (global_load_lds_dwordx4, no staging registers, which
+// the 256 accumulator registers of a big tile leave no room for); fp32 stages
+// through registers with raw buffer loads and runs small tiles only.
+// LDS layouts:
+//   depth-contiguous operands (element (r, k) at P[r * ld + k]), bf16: 4 planes
+//     (one per 16-deep MFMA step) of [row][32 B], the halves of row r swapped
+//     when bit 2 of r is set; fragments are 16-byte reads (8 consecutive rows
+//     conflict-free).  fp32: [row][8 x 16 B], vector s of row r in slot
+//     s ^ (r & 7) ^ ((r >> 3) & 7).
+//   rows-contiguous operands (element (r, k) at P[k * ld + r]), bf16: stored as
+//     loaded, [depth row][R], the 32-byte chunk c of depth row k at c ^ 2(k & 3);
+//     fragments come from two ds_read_b64_tr_b16 each.  Within a 16-lane group
+//     that instruction hands lane i the element i % 4 of the 8 bytes addressed
+//     by lane 4j + i / 4 as its j-th value, so lane (s, group g) addressing
+//     depth row 8h + s/4 (+4) at rows 16(g & 1) + 4(s & 3) receives rows
+//     16(g & 1) + s at depths 8h..8h+3 (+4) -- exactly an MFMA operand.
+//   rows-contiguous operands, fp32: transposed in registers into the first layout.
+//
+// Fused epilogues:
 //   EPI_FWD       bias + ReLU + inverted dropout (Philox4x32-10 per member) -> H
 //   EPI_FWD_EVAL  bias + ReLU -> H
-//   EPI_DX        dH * [H_prev > 0] * s_k  -> dZ_prev  (ReLU' and dropout' from H)
-//   EPI_DW        fp32 store of the weight gradient tile
+//   EPI_DX        dH * [H_prev > 0] * s_k -> dZ_prev, plus column sums of the
+//                 unrounded values per 64-row block (bias-gradient partials)
+//   EPI_DW        fp32 store of the weight-gradient tile
 // Every output element is owned by exactly one workgroup and reduced over the
 // full depth in a fixed order: no atomics, bit-reproducible.
 #include "pack_internal.h"
@@ -28,16 +55,28 @@ namespace tabpack {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int NT = 256;       // threads per workgroup
-constexpr int TM = 128;       // tile rows (GEMM M)
-constexpr int TN = 128;       // tile cols (GEMM N)
-constexpr int KV = 4;         // 16-byte vectors per LDS row per K step
-constexpr int PITCH = KV * 16 + 16;  // LDS row pitch in bytes (one vector of padding)
+constexpr int NT = 256;                 // threads per workgroup (2 x 2 waves)
+constexpr int KV = 8;                   // 16-byte vectors of depth per row per K step
+constexpr int ROW = KV * 16;            // 128 bytes of depth per row per K step
+constexpr int kTileBytes = 256 * ROW;   // one operand tile of the big shape: 32 KB
+constexpr int kStageBytes = 2 * kTileBytes;
+
+template <int SH>
+struct Shape;
+template <>
+struct Shape<kShapeBig> {
+  static constexpr int MB = 4, NB = 4, TM = 256, TN = 256;
+};
+template <>
+struct Shape<kShapeSmall> {
+  static constexpr int MB = 2, NB = 2, TM = 128, TN = 128;
+};
 
 template <typename T>
 struct Elem;
@@ -50,9 +89,25 @@ struct Elem<float> {
   static constexpr int VE = 4;
 };
 
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-  __bf16 b = (__bf16)f;  // round to nearest even (v_cvt_pk_bf16_f32)
-  return (uint32_t)__builtin_bit_cast(uint16_t, b);
+// depth-contiguous layout: byte offset of 16-byte vector `slot` of row `row`
+__device__ __forceinline__ int kmaj_off(int row, int slot) {
+  return row * ROW + ((slot ^ (row & 7) ^ ((row >> 3) & 7)) << 4);
+}
+
+// depth-contiguous bf16 layout used with direct-to-LDS loads: 4 planes (one per
+// 16-deep MFMA step) of R rows x 32 bytes; the two 16-byte halves of row r are
+// swapped when bit 2 of r is set, so the 16-byte fragment reads of 8
+// consecutive rows hit 8 distinct bank groups, and every fragment address is a
+// per-lane base plus compile-time offsets.
+template <int R>
+__device__ __forceinline__ int kmaj16_off(int row, int ks, int h) {
+  return ks * (R * 32) + row * 32 + ((h ^ ((row >> 2) & 1)) << 4);
+}
+
+// rows-contiguous bf16 layout (R rows): byte offset of element `col` of depth row k
+template <int R>
+__device__ __forceinline__ int rmaj_off(int k, int col) {
+  return k * (R * 2) + ((((col >> 4) ^ ((k & 3) << 1))) << 5) + ((col & 15) << 1);
 }
 
 __device__ __forceinline__ float to_float(__bf16 x) { return (float)x; }
@@ -69,288 +124,301 @@ __device__ __forceinline__ float from_float<float>(float f) {
   return f;
 }
 
-// Pack VE fp32 values (one 16-byte LDS vector worth of T) into 4 dwords.
-template <typename T>
-__device__ __forceinline__ u32x4 pack_vec(const float* f);
-template <>
-__device__ __forceinline__ u32x4 pack_vec<__bf16>(const float* f) {
-  u32x4 r;
-  r[0] = bf16_bits(f[0]) | (bf16_bits(f[1]) << 16);
-  r[1] = bf16_bits(f[2]) | (bf16_bits(f[3]) << 16);
-  r[2] = bf16_bits(f[4]) | (bf16_bits(f[5]) << 16);
-  r[3] = bf16_bits(f[6]) | (bf16_bits(f[7]) << 16);
-  return r;
-}
-template <>
-__device__ __forceinline__ u32x4 pack_vec<float>(const float* f) {
-  u32x4 r;
-  r[0] = __float_as_uint(f[0]);
-  r[1] = __float_as_uint(f[1]);
-  r[2] = __float_as_uint(f[2]);
-  r[3] = __float_as_uint(f[3]);
-  return r;
-}
-
-__device__ __forceinline__ int64_t gather_row(const GemmArgs& a, int member, int r) {
-  return a.idx ? (int64_t)a.idx[(int64_t)member * a.idx_stride + r] : a.row_base + r;
-}
-
 // ---------------------------------------------------------------- loaders --
-// Each loader moves one R x (KV*VE) operand tile per K step: load() issues the
-// global reads for depth offset k0 into registers, store() writes them to LDS.
+// A loader moves one R x 128-byte-depth operand tile per K step: load() issues
+// raw buffer loads for depth offset k0 into registers, store() writes them to
+// LDS.  An element outside the operand (row beyond the member's extent, depth
+// beyond K) gets an offset past the buffer's range, which the hardware returns
+// as zero -- no branch and no select on the data, so the loads stay in flight
+// across the MFMAs of the current step.
+constexpr uint32_t kOob = 0x80000000u;   // an offset outside every operand buffer
+constexpr int kRsrcWord3 = 0x00020000;   // gfx9 raw buffer descriptor: 32-bit data format, no swizzle
 
-// Depth-contiguous operand stored as T.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)(bytes < kOob ? bytes : kOob - 16),
+                                           kRsrcWord3);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
+// Depth-contiguous operand (T), element (r, k) at P[r * ld + k] -> depth-contiguous LDS.
 template <typename T, int R>
 struct LoadKmaj {
   static constexpr int VE = Elem<T>::VE;
   static constexpr int NV = R * KV / NT;
   u32x4 reg[NV];
-  const T* ptr[NV];
-  bool ok[NV];
-  int kv[NV];
-  int r[NV];
-  __device__ void init(const T* P, int64_t ld, int row0, int rbound, int tid) {
+  __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t off[NV];  // byte offset of this thread's vector at depth 0, or kOob
+  int slot;
+  __device__ void init(const T* P, int64_t ld, int row0, int rbound, int, int tid) {
+    rsrc = make_rsrc(P, (int64_t)rbound * ld * (int64_t)sizeof(T));
+    slot = tid % KV;  // NT is a multiple of KV: every vector of a thread has this slot
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      const int v = tid + i * NT;
-      r[i] = v / KV;
-      kv[i] = v % KV;
-      ok[i] = row0 + r[i] < rbound;
-      ptr[i] = P + (int64_t)(row0 + r[i]) * ld + kv[i] * VE;
+      const int r = (tid + i * NT) / KV;
+      off[i] = row0 + r < rbound ? (uint32_t)(((int64_t)(row0 + r) * ld + slot * VE) * sizeof(T)) : kOob;
     }
   }
-  __device__ void load(int k0, int kd) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const bool in = ok[i] && (k0 + kv[i] * VE < kd);
-      reg[i] = in ? *reinterpret_cast<const u32x4*>(ptr[i] + k0) : u32x4{0u, 0u, 0u, 0u};
-    }
-  }
-  __device__ void store(char* lds) const {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) *reinterpret_cast<u32x4*>(lds + r[i] * PITCH + kv[i] * 16) = reg[i];
-  }
-};
-
-// Rows-contiguous operand stored as T: each thread reads 2 depth rows of VE
-// consecutive tile rows and writes VE LDS rows of 2 depth values.
-template <typename T, int R>
-struct LoadRmaj {
-  static constexpr int VE = Elem<T>::VE;
-  static constexpr int RB = R / VE;
-  static_assert(RB * (KV * VE / 2) == NT, "one 2 x VE block per thread");
-  u32x4 reg[2];
-  const T* ptr;
-  int64_t ld;
-  int rb, kp;
-  bool ok;
-  __device__ void init(const T* P, int64_t ld_, int row0, int rbound, int tid) {
-    rb = tid % RB;
-    kp = tid / RB;
-    ld = ld_;
-    ok = row0 + rb * VE < rbound;
-    ptr = P + row0 + rb * VE;
-  }
-  __device__ void load(int k0, int kd) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int k = k0 + 2 * kp + j;
-      reg[j] = (ok && k < kd) ? *reinterpret_cast<const u32x4*>(ptr + (int64_t)k * ld)
-                              : u32x4{0u, 0u, 0u, 0u};
-    }
-  }
-  __device__ void store(char* lds) const {
-    if constexpr (sizeof(T) == 2) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t a = reg[0][e >> 1], b = reg[1][e >> 1];
-        const uint32_t w = (e & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
-        *reinterpret_cast<uint32_t*>(lds + (rb * 8 + e) * PITCH + kp * 4) = w;
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        *reinterpret_cast<u32x2*>(lds + (rb * 4 + e) * PITCH + kp * 8) = u32x2{reg[0][e], reg[1][e]};
-    }
-  }
-};
-
-// Gathered fp32 feature rows, depth (feature) contiguous; converted to T.
-template <typename T, int R>
-struct LoadXgk {
-  static constexpr int VE = Elem<T>::VE;
-  static constexpr int NV = R * KV / NT;
-  float f[NV][VE];
-  const float* ptr[NV];
-  bool ok[NV];
-  int kv[NV];
-  int r[NV];
-  int d_in;
-  bool vec;
-  __device__ void init(const GemmArgs& a, int member, int row0, int tid) {
-    d_in = a.d_in;
-    vec = (a.d_in % 4 == 0) && ((reinterpret_cast<uintptr_t>(a.X) & 15) == 0);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int v = tid + i * NT;
-      r[i] = v / KV;
-      kv[i] = v % KV;
-      const int br = row0 + r[i];
-      ok[i] = br < a.rows_valid;
-      const int64_t src = ok[i] ? gather_row(a, member, br) : 0;
-      ptr[i] = a.X + src * a.d_in + kv[i] * VE;
-    }
-  }
-  __device__ void load(int k0, int) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int kk = k0 + kv[i] * VE;
-      if (ok[i] && vec && kk + VE <= d_in) {
-#pragma unroll
-        for (int q = 0; q < VE / 4; ++q) {
-          const f32x4 x = *reinterpret_cast<const f32x4*>(ptr[i] + k0 + 4 * q);
-          f[i][4 * q + 0] = x[0];
-          f[i][4 * q + 1] = x[1];
-          f[i][4 * q + 2] = x[2];
-          f[i][4 * q + 3] = x[3];
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < VE; ++e) f[i][e] = (ok[i] && kk + e < d_in) ? ptr[i][k0 + e] : 0.0f;
-      }
-    }
-  }
-  __device__ void store(char* lds) const {
+  __device__ void load(int k0, int kd, int) {
+    const bool kin = k0 + slot * VE < kd;
 #pragma unroll
     for (int i = 0; i < NV; ++i)
-      *reinterpret_cast<u32x4*>(lds + r[i] * PITCH + kv[i] * 16) = pack_vec<T>(f[i]);
+      reg[i] = buf_load16(rsrc, (kin && off[i] != kOob) ? off[i] + k0 * (uint32_t)sizeof(T) : kOob);
+  }
+  __device__ void store(char* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int v = tid + i * NT;
+      *reinterpret_cast<u32x4*>(lds + kmaj_off(v / KV, v % KV)) = reg[i];
+    }
   }
 };
 
-// Gathered fp32 feature rows used transposed: tile rows are features, depth is
-// the batch row.  Each thread reads 2 batch rows x VE features.
-template <typename T, int R>
-struct LoadXgr {
-  static constexpr int VE = Elem<T>::VE;
-  static constexpr int RB = R / VE;
-  static_assert(RB * (KV * VE / 2) == NT, "one 2 x VE block per thread");
-  float f[2][VE];
-  const float* X;
-  const int32_t* idx;
-  int64_t row_base;
-  int d_in, rows_valid;
-  int rb, kp, f0;
-  bool vec;
-  __device__ void init(const GemmArgs& args, int member, int row0, int tid) {
-    X = args.X;
-    idx = args.idx ? args.idx + (int64_t)member * args.idx_stride : nullptr;
-    row_base = args.row_base;
-    d_in = args.d_in;
-    rows_valid = args.rows_valid;
-    rb = tid % RB;
-    kp = tid / RB;
-    f0 = row0 + rb * VE;
-    vec = (args.d_in % 4 == 0) && ((reinterpret_cast<uintptr_t>(args.X) & 15) == 0);
+// Rows-contiguous fp32 operand: 4 x 4 blocks transposed in registers into the
+// depth-contiguous LDS layout.
+template <int R>
+struct LoadRmajF32 {
+  static constexpr int RB = R / 4;              // row blocks
+  static constexpr int NBLK = RB * KV;          // blocks per tile
+  static constexpr int PER = NBLK / NT;
+  u32x4 reg[PER][4];
+  __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t off[PER];
+  int64_t ldb;
+  __device__ void init(const float* P, int64_t ld, int row0, int rbound, int kd, int tid) {
+    ldb = ld * 4;
+    rsrc = make_rsrc(P, (int64_t)kd * ldb);
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int b = tid + p * NT;
+      const int rb = b % RB, kb = b / RB;
+      off[p] = row0 + rb * 4 < rbound ? (uint32_t)(kb * 4 * ldb + (int64_t)(row0 + rb * 4) * 4) : kOob;
+    }
   }
-  __device__ void load(int k0, int) {
+  __device__ void load(int k0, int kd, int tid) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int br = k0 + 2 * kp + j;
-      const bool okr = br < rows_valid;
-      const int64_t src = okr ? (idx ? (int64_t)idx[br] : row_base + br) : 0;
-      const float* p = X + src * d_in + f0;
-      if (okr && vec && f0 + VE <= d_in) {
+    for (int p = 0; p < PER; ++p) {
+      const int kb = (tid + p * NT) / RB;
 #pragma unroll
-        for (int q = 0; q < VE / 4; ++q) {
-          const f32x4 x = *reinterpret_cast<const f32x4*>(p + 4 * q);
-          f[j][4 * q + 0] = x[0];
-          f[j][4 * q + 1] = x[1];
-          f[j][4 * q + 2] = x[2];
-          f[j][4 * q + 3] = x[3];
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < VE; ++e) f[j][e] = (okr && f0 + e < d_in) ? p[e] : 0.0f;
+      for (int e = 0; e < 4; ++e) {
+        const bool in = off[p] != kOob && k0 + kb * 4 + e < kd;
+        reg[p][e] = buf_load16(rsrc, in ? off[p] + (uint32_t)((k0 + e) * ldb) : kOob);
       }
     }
   }
-  __device__ void store(char* lds) const {
+  __device__ void store(char* lds, int tid) const {
 #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      if constexpr (sizeof(T) == 2) {
-        *reinterpret_cast<uint32_t*>(lds + (rb * 8 + e) * PITCH + kp * 4) =
-            bf16_bits(f[0][e]) | (bf16_bits(f[1][e]) << 16);
-      } else {
-        *reinterpret_cast<u32x2*>(lds + (rb * 4 + e) * PITCH + kp * 8) =
-            u32x2{__float_as_uint(f[0][e]), __float_as_uint(f[1][e])};
+    for (int p = 0; p < PER; ++p) {
+      const int b = tid + p * NT;
+      const int rb = b % RB, kb = b / RB;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const u32x4 o{reg[p][0][i], reg[p][1][i], reg[p][2][i], reg[p][3][i]};
+        *reinterpret_cast<u32x4*>(lds + kmaj_off(rb * 4 + i, kb)) = o;
       }
+    }
+  }
+};
+
+// Direct-to-LDS loaders (bf16): global_load_lds_dwordx4 writes lane i's 16
+// bytes at the instruction's LDS base + 16 i, so each wave fills whole 1 KB
+// chunks of the LDS tile and every lane fetches the global vector that belongs
+// at its position in the swizzled layout.  Nothing is staged in registers.
+// Elements outside the operand are fetched from a block of zeros.
+typedef const void __attribute__((address_space(1)))* gptr_t;
+typedef void __attribute__((address_space(3)))* lptr_t;
+
+__device__ __forceinline__ void dma16(const void* src, char* lds) {
+  __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)lds, 16, 0, 0);
+}
+
+// Depth-contiguous bf16 operand -> planar depth-contiguous LDS layout.  Wave w
+// fills plane w (depths 16w .. 16w+15 of the K step), 32 rows per 1 KB chunk;
+// a lane fetches 16 bytes (8 depths) of one row.
+template <int R>
+struct DmaKmaj {
+  static constexpr int PER = R / 32;  // chunks per wave (= per plane)
+  const char* base;
+  const void* zeros;
+  uint32_t off0;       // byte offset (depth 0) of this lane's vector in chunk 0
+  uint32_t rstep;      // bytes between the rows of consecutive chunks (32 rows)
+  int kofs;            // depth offset (elements) of this lane's vector inside a K step
+  uint32_t okmask;     // bit p: this lane's row of chunk p exists
+  int wave;
+  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int, int wave_, int lane,
+                       const void* z) {
+    base = reinterpret_cast<const char*>(P);
+    zeros = z;
+    wave = wave_;
+    const int r = lane >> 1;                         // row inside a 32-row chunk
+    const int h = (lane & 1) ^ ((r >> 2) & 1);       // logical 16-byte half of the plane row
+    kofs = wave * 16 + h * 8;
+    off0 = (uint32_t)(((int64_t)(row0 + r) * ld + kofs) * 2);
+    rstep = (uint32_t)(32 * ld * 2);
+    okmask = 0;
+#pragma unroll
+    for (int p = 0; p < PER; ++p)
+      if (row0 + p * 32 + r < rbound) okmask |= 1u << p;
+  }
+  __device__ void issue(char* lds, int k0, int kd) const {
+    const bool kin = k0 + kofs < kd;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const bool in = kin && ((okmask >> p) & 1);
+      dma16(in ? base + off0 + p * rstep + (uint32_t)k0 * 2u : zeros, lds + wave * (R * 32) + p * 1024);
+    }
+  }
+};
+
+// Rows-contiguous bf16 operand -> rows-contiguous LDS layout (64 depth rows x R).
+template <int R>
+struct DmaRmaj {
+  static constexpr int RBYTES = 2 * R;                 // bytes per depth row in LDS
+  static constexpr int PER = 64 * RBYTES / 1024 / 4;   // chunks per wave
+  const char* base;
+  const void* zeros;
+  int64_t ldb;         // bytes per depth row in HBM
+  uint32_t off[PER];   // byte offset (depth 0) of the vector this lane fetches for chunk p
+  int krow[PER];       // its depth row inside a K step
+  bool ok[PER];        // its rows exist
+  int wave;
+  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int, int wave_, int lane,
+                       const void* z) {
+    base = reinterpret_cast<const char*>(P);
+    zeros = z;
+    wave = wave_;
+    ldb = ld * 2;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int pos = (wave * PER + p) * 1024 + lane * 16;
+      const int k = pos / RBYTES, b = pos % RBYTES;
+      const int chunk = (b >> 5) ^ ((k & 3) << 1);
+      const int col = chunk * 16 + ((b >> 4) & 1) * 8;
+      krow[p] = k;
+      ok[p] = row0 + col < rbound;
+      off[p] = (uint32_t)(k * ldb + (int64_t)(row0 + col) * 2);
+    }
+  }
+  __device__ void issue(char* lds, int k0, int kd) const {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const bool in = ok[p] && k0 + krow[p] < kd;
+      dma16(in ? base + off[p] + (uint32_t)(k0 * ldb) : zeros, lds + (wave * PER + p) * 1024);
     }
   }
 };
 
 template <typename T, int KIND, int R>
 struct LoaderFor;
-template <typename T, int R>
-struct LoaderFor<T, OP_KMAJ, R> {
-  using type = LoadKmaj<T, R>;
+template <int R>
+struct LoaderFor<__bf16, OP_KMAJ, R> {
+  using type = DmaKmaj<R>;
+  static constexpr bool tr = false;  // fragments read from the depth-contiguous layout
+  static constexpr bool dma = true;
 };
-template <typename T, int R>
-struct LoaderFor<T, OP_RMAJ, R> {
-  using type = LoadRmaj<T, R>;
+template <int R>
+struct LoaderFor<__bf16, OP_RMAJ, R> {
+  using type = DmaRmaj<R>;
+  static constexpr bool tr = true;   // fragments read with ds_read_b64_tr_b16
+  static constexpr bool dma = true;
 };
-template <typename T, int R>
-struct LoaderFor<T, OP_XGK, R> {
-  using type = LoadXgk<T, R>;
+template <int R>
+struct LoaderFor<float, OP_KMAJ, R> {
+  using type = LoadKmaj<float, R>;
+  static constexpr bool tr = false;
+  static constexpr bool dma = false;
 };
-template <typename T, int R>
-struct LoaderFor<T, OP_XGR, R> {
-  using type = LoadXgr<T, R>;
+template <int R>
+struct LoaderFor<float, OP_RMAJ, R> {
+  using type = LoadRmajF32<R>;
+  static constexpr bool tr = false;
+  static constexpr bool dma = false;
 };
 
-template <typename L, int KIND, typename T>
-__device__ __forceinline__ void loader_init(L& ld, const GemmArgs& a, const GemmDesc& d,
-                                            const void* P, int64_t lp, int row0, int rbound,
-                                            int tid) {
-  if constexpr (KIND == OP_XGK || KIND == OP_XGR)
-    ld.init(a, d.member, row0, tid);
+// ------------------------------------------------------------- fragments --
+// 8 bf16 of depth 16*ks + 8*h .. +7 (h = lane / 32) of operand row
+// row_block + lane % 32, from the rows-contiguous layout.
+template <int R>
+__device__ __forceinline__ bf16x8 frag_tr(const char* lds, int row_block, int ks, int lane) {
+  const int s = lane & 15, g = lane >> 4;
+  const int k = 16 * ks + 8 * (g >> 1) + (s >> 2);
+  const int col = row_block + 16 * (g & 1) + 4 * (s & 3);
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds + rmaj_off<R>(k, col)));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds + rmaj_off<R>(k + 4, col)));
+  const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+  return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], b[0], b[1]});
+}
+
+template <int R>
+__device__ __forceinline__ bf16x8 frag_kmaj_bf16(const char* lds, int row_block, int ks, int lane) {
+  return *reinterpret_cast<const bf16x8*>(lds + kmaj16_off<R>(row_block + (lane & 31), ks, lane >> 5));
+}
+
+template <bool TR, int R>
+__device__ __forceinline__ bf16x8 frag_bf16(const char* lds, int row_block, int ks, int lane) {
+  if constexpr (TR)
+    return frag_tr<R>(lds, row_block, ks, lane);
   else
-    ld.init(static_cast<const T*>(P), lp, row0, rbound, tid);
+    return frag_kmaj_bf16<R>(lds, row_block, ks, lane);
 }
 
 // ------------------------------------------------------------------- MFMA --
-template <typename T>
-__device__ __forceinline__ void mma_step(const char* As, const char* Bs, f32x16 (&acc)[2][2],
-                                         int wm, int wn, int lane) {
-  const int rl = lane & 31;
-  const int hv = lane >> 5;
+// One K step (128 bytes of depth) for this wave's MB x NB blocks.  Blocks
+// outside the member's extents hold zeros and are computed anyway: the loop
+// stays free of branches so LDS reads and MFMAs overlap.
+template <typename T, int SH, bool TRA, bool TRB>
+__device__ __forceinline__ void mma_step(const char* As, const char* Bs,
+                                         f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn,
+                                         int lane) {
+  constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM, TN = Shape<SH>::TN;
+  if constexpr (sizeof(T) == 2) {
+    // Fragments of the next 16-deep step are read while the MFMAs of this one
+    // run; the loop stays rolled (a full unroll hoists every step's reads and
+    // does not fit beside 256 accumulators).  The last step re-reads step 0,
+    // which is harmless.
+    bf16x8 a[MB], b[NB];
 #pragma unroll
-  for (int ks = 0; ks < KV / 2; ++ks) {
-    const int vo = (2 * ks + hv) * 16;
-    if constexpr (sizeof(T) == 2) {
-      bf16x8 a[2], b[2];
+    for (int i = 0; i < MB; ++i) a[i] = frag_bf16<TRA, TM>(As, wm * MB * 32 + i * 32, 0, lane);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        a[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 64 + i * 32 + rl) * PITCH + vo);
-        b[i] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + i * 32 + rl) * PITCH + vo);
-      }
+    for (int j = 0; j < NB; ++j) b[j] = frag_bf16<TRB, TN>(Bs, wn * NB * 32 + j * 32, 0, lane);
+#pragma unroll 1
+    for (int ks = 0; ks < KV / 2; ++ks) {
+      const int kn = (ks + 1) & (KV / 2 - 1);
+      bf16x8 na[MB], nb[NB];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < MB; ++i) na[i] = frag_bf16<TRA, TM>(As, wm * MB * 32 + i * 32, kn, lane);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NB; ++j) nb[j] = frag_bf16<TRB, TN>(Bs, wn * NB * 32 + j * 32, kn, lane);
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    } else {
-      f32x4 a[2], b[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        a[i] = *reinterpret_cast<const f32x4*>(As + (wm * 64 + i * 32 + rl) * PITCH + vo);
-        b[i] = *reinterpret_cast<const f32x4*>(Bs + (wn * 64 + i * 32 + rl) * PITCH + vo);
-      }
+      for (int i = 0; i < MB; ++i) a[i] = na[i];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b[j] = nb[j];
+    }
+  } else {
+    const int rl = lane & 31, hv = lane >> 5;
+#pragma unroll
+    for (int ks = 0; ks < KV / 2; ++ks) {
+      f32x4 a[MB], b[NB];
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+        a[i] = *reinterpret_cast<const f32x4*>(As + kmaj_off(wm * MB * 32 + i * 32 + rl, 2 * ks + hv));
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        b[j] = *reinterpret_cast<const f32x4*>(Bs + kmaj_off(wn * NB * 32 + j * 32 + rl, 2 * ks + hv));
 #pragma unroll
       for (int e = 0; e < 4; ++e)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < MB; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
+          for (int j = 0; j < NB; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
     }
   }
@@ -360,120 +428,223 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs, f32x16 
 // Accumulator register r of a 32x32 block held by lane l is element
 // (row 8*(r/4) + 4*(l/32) + r%4, col l%32): each lane owns 4 runs of 4
 // consecutive rows of one column, so one Philox block (4 words) serves a run.
-template <typename T, int EPI>
+template <typename T, int EPI, int SH>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, const Tile& t,
-                                         f32x16 (&acc)[2][2], int wm, int wn, int lane) {
+                                         f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn, int lane,
+                                         int mv, int nv) {
+  constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB;
   const int hv = lane >> 5;
+  // Rows outer, the NB column blocks inner: a row's offset is formed once and
+  // serves NB stores at compile-time distances, so no per-row addresses have
+  // to stay live beside the accumulators.
+  const int col0 = t.n0 + wn * NB * 32 + (lane & 31);
+  const int rbase = t.m0 + wm * MB * 32 + 4 * hv;
+  bool colin[NB];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int col = t.n0 + wn * 64 + j * 32 + (lane & 31);
-    if (col >= d.N) continue;
-    if constexpr (EPI == EPI_DW) {
-      float* C = static_cast<float*>(d.C);
+  for (int j = 0; j < NB; ++j) colin[j] = j < nv && col0 + 32 * j < d.N;
+  if constexpr (EPI == EPI_DW) {
+    float* C = static_cast<float*>(d.C) + col0;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MB; ++i) {
+      if (i >= mv) continue;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int row = t.m0 + wm * 64 + i * 32 + 8 * g + 4 * hv;
+      for (int g = 0; g < 4; ++g)
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (row + q < d.M) C[(int64_t)(row + q) * d.ldc + col] = acc[i][j][4 * g + q];
+        for (int q = 0; q < 4; ++q) {
+          const int row = rbase + 32 * i + 8 * g + q;
+          if (row >= d.M) continue;
+          float* Cr = C + (int64_t)row * d.ldc;
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            if (colin[j]) Cr[32 * j] = acc[i][j][4 * g + q];
         }
-    } else if constexpr (EPI == EPI_DX) {
-      T* C = static_cast<T*>(d.C);
-      const T* Hp = static_cast<const T*>(d.Haux);
-      float cs = 0.0f;  // column sum over this wave's 64 rows (this lane's 32 of them)
+    }
+  } else if constexpr (EPI == EPI_DX) {
+    // dZ = dH * (H_prev > 0) * s; H_prev already carries the dropout keep and
+    // the ReLU of the forward pass.  Column sums of dZ per 64-row half go to
+    // colpart (bias gradient partials, reduced by a later kernel).
+    T* C = static_cast<T*>(d.C) + col0;
+    const T* Hp = static_cast<const T*>(d.Haux) + col0;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+    for (int ih = 0; ih < MB / 2; ++ih) {
+      float cs[NB];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int row = t.m0 + wm * 64 + i * 32 + 8 * g + 4 * hv;
+      for (int j = 0; j < NB; ++j) cs[j] = 0.0f;
+#pragma unroll
+      for (int ii = 0; ii < 2; ++ii) {
+        const int i = 2 * ih + ii;
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int64_t o = (int64_t)(row + q) * d.ldc + col;
-            const float hp = to_float(Hp[o]);
-            const float dz = hp > 0.0f ? acc[i][j][4 * g + q] * d.drop_s : 0.0f;
-            cs += dz;
-            C[o] = from_float<T>(dz);
+            const int row = rbase + 32 * i + 8 * g + q;
+            const int64_t o = (int64_t)row * d.ldc;
+#pragma unroll
+            for (int j = 0; j < NB; ++j)
+              if (colin[j] && row < d.M) {
+                const float hp = to_float(Hp[o + 32 * j]);
+                const float dz = hp > 0.0f ? acc[i][j][4 * g + q] * d.drop_s : 0.0f;
+                cs[j] += dz;
+                C[o + 32 * j] = from_float<T>(dz);
+              }
           }
+      }
+      const int64_t prow = (int64_t)((t.m0 + wm * MB * 32 + ih * 64) / kPartRows) * d.N;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        // lanes l and l^32 hold the two interleaved row halves of one column
+        const float c = cs[j] + __shfl_xor(cs[j], 32, 64);
+        if (hv == 0 && colin[j] && t.m0 + wm * MB * 32 + ih * 64 < d.M) d.colpart[prow + col0 + 32 * j] = c;
+      }
+    }
+  } else {
+    T* C = static_cast<T*>(d.C) + col0;
+    float bias[NB];
+    bool colok[NB];
+    uint64_t keep[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      bias[j] = colin[j] ? d.bias[col0 + 32 * j] : 0.0f;
+      colok[j] = col0 + 32 * j < d.width;
+      keep[j] = ~0ull;
+    }
+    if ((EPI == EPI_FWD) && d.drop_t != 0u) {
+      // Keep bits of this lane's 4*MB runs of 4 rows: run r = 4*i + g covers
+      // rows rbase + 32*i + 8*g + (0..3), i.e. Philox block
+      // (m0 + wm*MB*32)/4 + 2*r + hv, words 0..3.  The loop over runs stays
+      // rolled and never touches the accumulators.
+      const uint32_t c0 = (uint32_t)((t.m0 + wm * MB * 32) >> 2) + (uint32_t)hv;
+      const uint32_t c2 = ((uint32_t)d.member << 8) | (uint32_t)a.layer;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        if (!colin[j]) continue;
+        uint64_t k = 0;
+#pragma unroll 1
+        for (int r = 0; r < 4 * MB; ++r) {
+          const Words4 w = philox4x32_10(c0 + 2u * (uint32_t)r, (uint32_t)(col0 + 32 * j), c2, a.step, a.key0,
+                                         a.key1);
+          const uint64_t bits = (uint64_t)(w.w0 >= d.drop_t) | ((uint64_t)(w.w1 >= d.drop_t) << 1) |
+                                ((uint64_t)(w.w2 >= d.drop_t) << 2) | ((uint64_t)(w.w3 >= d.drop_t) << 3);
+          k |= bits << (4 * r);
         }
-      // lanes l and l^32 hold the two interleaved halves of the same column
-      cs += __shfl_xor(cs, 32, 64);
-      if (hv == 0) d.colpart[(int64_t)(t.m0 / 64 + wm) * d.N + col] = cs;
-    } else {
-      T* C = static_cast<T*>(d.C);
-      const float bias = d.bias[col];
-      const bool colok = col < d.width;
-      const bool drop = (EPI == EPI_FWD) && d.drop_t != 0u;
+        keep[j] = k;
+      }
+    }
+    const float s_keep = (EPI == EPI_FWD) ? d.drop_s : 1.0f;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MB; ++i) {
+      if (i >= mv) continue;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int row = t.m0 + wm * 64 + i * 32 + 8 * g + 4 * hv;
-          Words4 w{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
-          if (drop)
-            w = philox4x32_10((uint32_t)row >> 2, (uint32_t)col,
-                              ((uint32_t)d.member << 8) | (uint32_t)a.layer, a.step, a.key0,
-                              a.key1);
-          const uint32_t wq[4] = {w.w0, w.w1, w.w2, w.w3};
+      for (int g = 0; g < 4; ++g)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            float h = fmaxf(acc[i][j][4 * g + q] + bias, 0.0f);
-            if (EPI == EPI_FWD) h = (wq[q] >= d.drop_t) ? h * d.drop_s : 0.0f;
-            if (!colok || row + q >= a.rows_valid) h = 0.0f;
-            C[(int64_t)(row + q) * d.ldc + col] = from_float<T>(h);
-          }
+        for (int q = 0; q < 4; ++q) {
+          const int row = rbase + 32 * i + 8 * g + q;
+          if (row >= d.M) continue;
+          const bool rv = row < a.rows_valid;
+          T* Cr = C + (int64_t)row * d.ldc;
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            if (colin[j]) {
+              float h = fmaxf(acc[i][j][4 * g + q] + bias[j], 0.0f);
+              h = ((keep[j] >> (16 * i + 4 * g + q)) & 1) ? h * s_keep : 0.0f;
+              if (!colok[j] || !rv) h = 0.0f;
+              Cr[32 * j] = from_float<T>(h);
+            }
         }
     }
   }
 }
 
-// ----------------------------------------------------------------- kernel --
-template <typename T, int AK, int BK_, int EPI>
-__global__ __launch_bounds__(NT) void gemm_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2][(TM + TN) * PITCH];
-  const Tile t = a.tiles[blockIdx.x];
-  const GemmDesc d = a.descs[t.desc];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+// ------------------------------------------------------------------- tile --
+template <typename T, int AK, int BK_, int EPI, int SH>
+__device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, const Tile& t, char* lds0,
+                                         char* lds1, int tid, int wave) {
+  constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM, TN = Shape<SH>::TN;
   constexpr int BKE = KV * Elem<T>::VE;  // depth per K step
+  using LA = LoaderFor<T, AK, TM>;
+  using LB = LoaderFor<T, BK_, TN>;
+  const int lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  // this wave's 32-blocks inside the member's extents (wave-uniform); a wave
+  // with none skips its MFMAs but still takes part in loads and barriers
+  const int mrem = d.M - (t.m0 + wm * MB * 32), nrem = d.N - (t.n0 + wn * NB * 32);
+  const int mv = mrem <= 0 ? 0 : (mrem >= MB * 32 ? MB : (mrem + 31) / 32);
+  const int nv = nrem <= 0 ? 0 : (nrem >= NB * 32 ? NB : (nrem + 31) / 32);
+  const bool compute = mv > 0 && nv > 0;
 
-  typename LoaderFor<T, AK, TM>::type la;
-  typename LoaderFor<T, BK_, TN>::type lb;
-  loader_init<decltype(la), AK, T>(la, a, d, d.A, d.lda, t.m0, d.M, tid);
-  loader_init<decltype(lb), BK_, T>(lb, a, d, d.B, d.ldb, t.n0, d.N, tid);
+  typename LA::type la;
+  typename LB::type lb;
 
-  f32x16 acc[2][2];
+  f32x16 acc[MB][NB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MB; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NB; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int nk = (d.Kd + BKE - 1) / BKE;
-  la.load(0, d.Kd);
-  lb.load(0, d.Kd);
-  la.store(smem[0]);
-  lb.store(smem[0] + TM * PITCH);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      la.load((kt + 1) * BKE, d.Kd);
-      lb.load((kt + 1) * BKE, d.Kd);
-    }
-    mma_step<T>(smem[cur], smem[cur] + TM * PITCH, acc, wm, wn, lane);
-    if (more) {
-      la.store(smem[cur ^ 1]);
-      lb.store(smem[cur ^ 1] + TM * PITCH);
-    }
+  if constexpr (LA::dma) {
+    static_assert(LB::dma, "both operands staged the same way");
+    la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane, a.zeros);
+    lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane, a.zeros);
+    la.issue(lds0, 0, d.Kd);
+    lb.issue(lds0 + kTileBytes, 0, d.Kd);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      char* cur = (kt & 1) ? lds1 : lds0;
+      char* nxt = (kt & 1) ? lds0 : lds1;
+      if (kt + 1 < nk) {  // the next step streams into the other buffer during the MFMAs
+        la.issue(nxt, (kt + 1) * BKE, d.Kd);
+        lb.issue(nxt + kTileBytes, (kt + 1) * BKE, d.Kd);
+      }
+      if (compute) mma_step<T, SH, LA::tr, LB::tr>(cur, cur + kTileBytes, acc, wm, wn, lane);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
+  } else {
+    la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, tid);
+    lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, tid);
+    la.load(0, d.Kd, tid);
+    lb.load(0, d.Kd, tid);
+    la.store(lds0, tid);
+    lb.store(lds0 + kTileBytes, tid);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      char* cur = (kt & 1) ? lds1 : lds0;
+      char* nxt = (kt & 1) ? lds0 : lds1;
+      const bool more = kt + 1 < nk;
+      if (more) {
+        la.load((kt + 1) * BKE, d.Kd, tid);
+        lb.load((kt + 1) * BKE, d.Kd, tid);
+      }
+      if (compute) mma_step<T, SH, LA::tr, LB::tr>(cur, cur + kTileBytes, acc, wm, wn, lane);
+      if (more) {
+        la.store(nxt, tid);
+        lb.store(nxt + kTileBytes, tid);
+      }
+      __syncthreads();
+    }
   }
-  epilogue<T, EPI>(a, d, t, acc, wm, wn, lane);
+  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv);
+}
+
+// ----------------------------------------------------------------- kernel --
+template <typename T, int AK, int BK_, int EPI>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[2][kStageBytes];
+  const Tile t = a.tiles[blockIdx.x];
+  const GemmDesc d = a.descs[t.desc];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  if constexpr (sizeof(T) == 2) {
+    if (t.shape == kShapeBig) {
+      run_tile<T, AK, BK_, EPI, kShapeBig>(a, d, t, smem[0], smem[1], tid, wave);
+      return;
+    }
+  }
+  run_tile<T, AK, BK_, EPI, kShapeSmall>(a, d, t, smem[0], smem[1], tid, wave);  // fp32: small tiles only
 }
 
 template <typename T, int AK, int BK_, int EPI>
@@ -485,15 +656,11 @@ hipError_t launch_t(const GemmArgs& args, hipStream_t s) {
 
 template <typename T>
 hipError_t launch_prec(OpKind ak, OpKind bk, EpiKind e, const GemmArgs& args, hipStream_t s) {
-  if (ak == OP_XGK && bk == OP_KMAJ && e == EPI_FWD) return launch_t<T, OP_XGK, OP_KMAJ, EPI_FWD>(args, s);
-  if (ak == OP_XGK && bk == OP_KMAJ && e == EPI_FWD_EVAL)
-    return launch_t<T, OP_XGK, OP_KMAJ, EPI_FWD_EVAL>(args, s);
   if (ak == OP_KMAJ && bk == OP_KMAJ && e == EPI_FWD) return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_FWD>(args, s);
   if (ak == OP_KMAJ && bk == OP_KMAJ && e == EPI_FWD_EVAL)
     return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL>(args, s);
   if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DX) return launch_t<T, OP_KMAJ, OP_RMAJ, EPI_DX>(args, s);
   if (ak == OP_RMAJ && bk == OP_RMAJ && e == EPI_DW) return launch_t<T, OP_RMAJ, OP_RMAJ, EPI_DW>(args, s);
-  if (ak == OP_RMAJ && bk == OP_XGR && e == EPI_DW) return launch_t<T, OP_RMAJ, OP_XGR, EPI_DW>(args, s);
   return hipErrorInvalidValue;
 }
 

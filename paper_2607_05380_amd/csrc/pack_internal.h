@@ -13,6 +13,14 @@ constexpr int kMaxOut = 16;        // largest head width d_out supported by the 
 constexpr int kRowAlign = 256;     // base-batch rows are padded to a multiple of this (largest GEMM row tile)
 constexpr uint32_t kTagDropout = 3;
 
+// Grouped-GEMM output tiles: big 256 x 256 (4 waves of 128 x 128) and small
+// 128 x 128 (4 waves of 64 x 64) for the ragged edges of a member.
+constexpr int kShapeBig = 0, kShapeSmall = 1;
+constexpr int kBigTile = 256, kSmallTile = 128;
+constexpr int kPartRows = 64;   // rows per bias-gradient partial written by the dX epilogue
+constexpr int kXcds = 8;        // MI355X: workgroups go round-robin to 8 XCDs
+static_assert(kRowAlign % kBigTile == 0, "row padding must cover whole GEMM row tiles");
+
 enum class Prec : int { BF16 = 0, FP32 = 1 };
 enum class Task : int { REG = 0, BIN = 1, MULTI = 2 };
 
@@ -20,10 +28,7 @@ enum class Task : int { REG = 0, BIN = 1, MULTI = 2 };
 // (the GEMM's M or N index) by BK depth (its K index):
 //   KMAJ    element (r, k) at P[r * ld + k]         -- depth contiguous
 //   RMAJ    element (r, k) at P[k * ld + r]         -- rows contiguous (transposed on load)
-//   XGK     element (r, k) = X[row(r) * d_in + k]   -- gathered fp32 feature rows, depth contiguous
-//   XGR     element (r, k) = X[row(k) * d_in + r]   -- gathered fp32 feature rows, transposed on load
-// with row(i) = idx[member * idx_stride + i] or row_base + i when idx is null.
-enum OpKind : int { OP_KMAJ = 0, OP_RMAJ = 1, OP_XGK = 2, OP_XGR = 3 };
+enum OpKind : int { OP_KMAJ = 0, OP_RMAJ = 1 };
 enum EpiKind : int { EPI_FWD = 0, EPI_FWD_EVAL = 1, EPI_DX = 2, EPI_DW = 3 };
 
 // One member's GEMM problem C[m, n] = sum_k A(m, k) B(n, k) in one grouped launch.
@@ -33,7 +38,7 @@ struct GemmDesc {
   void* C;
   const float* bias;   // EPI_FWD*: [N] fp32
   const void* Haux;    // EPI_DX: activation H_{l-1}, same layout as C
-  float* colpart;      // EPI_DX: [M / 64, N] column sums of the unrounded output per 64-row block
+  float* colpart;      // EPI_DX: [M / kPartRows, N] column sums of the unrounded output per row block
   int64_t lda, ldb, ldc;
   int32_t M, N, Kd;    // A rows in bounds (< M), B rows in bounds (< N), depth (< Kd)
   int32_t width;       // EPI_FWD*: true width; columns >= width are written as 0
@@ -47,7 +52,7 @@ struct Tile {
   int32_t desc;
   int32_t m0;
   int32_t n0;
-  int32_t kdepth;      // planner's cost key (depth of this tile's K loop)
+  int32_t shape;       // kShapeBig or kShapeSmall
 };
 
 struct GemmArgs {
@@ -55,14 +60,10 @@ struct GemmArgs {
   const Tile* tiles;
   int32_t ntiles;
   int32_t layer;        // 1-based hidden layer (dropout counter)
-  const float* X;       // XGK / XGR source
-  const int32_t* idx;   // per-member row lists, or null for contiguous rows
-  int64_t row_base;     // first row when idx is null
-  int32_t d_in;
-  int32_t idx_stride;   // B
   int32_t rows_valid;   // batch rows that exist (B in training, chunk rows in eval)
   uint32_t key0, key1;  // dropout stream key
   uint32_t step;        // dropout counter word
+  const void* zeros;    // >= 16 bytes of zeros in device memory (source for out-of-range elements)
 };
 
 // Per-member table used by the small kernels.
@@ -96,6 +97,8 @@ hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const M
 hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, const ColTile* tiles,
                                      int ntiles, int nparts, const int64_t* bias_off, float* grad,
                                      hipStream_t s);
+hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
+                         int64_t row_base, int rows_valid, int members, int Bp, void* H0, hipStream_t s);
 hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, float* v,
                         uint16_t* shadow, const uint32_t* chunk_tab, const MemberDev* mem,
                         int64_t nchunks, float bc1, float bc2_sqrt, float beta1, float beta2,
