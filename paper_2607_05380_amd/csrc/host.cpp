@@ -95,6 +95,7 @@ struct Bufs {
   char* H = nullptr;   // L activation buffers H_1..H_L
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
   float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / kPartRows floats
+  uint32_t* mask = nullptr;  // ReLU/dropout keep bits of H_1..H_L, L * A / 32 words
   char* zeros = nullptr;     // 256 zero bytes: GEMM loads of out-of-range elements read them
   float *dY = nullptr, *rowloss = nullptr;
   MemberDev* d_mem = nullptr;
@@ -373,6 +374,9 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   };
   auto act = [&](void* base, int k) -> void* { return (char*)base + (size_t)h->mem[k].act_off * es; };
   auto h0 = [&](int k) -> void* { return bf.H0 + (size_t)k * h->h0_elems() * es; };
+  auto maskp = [&](int l, int k) -> uint32_t* {  // keep bits of H_l (1-based) of member k
+    return bf.mask + (size_t)(l - 1) * (h->A / 32) + h->mem[k].act_off / 32;
+  };
   for (int l = 1; l <= c.L; ++l) {
     // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
     Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
@@ -393,6 +397,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.member = k;
       d.drop_t = m.t;
       d.drop_s = (float)m.scale;
+      d.mask = maskp(l, k);
       p.descs.push_back(d);
       add_tiles(p, f, f.desc0 + k, h->Bp, m.dp, d.Kd);
       f.flops += 2.0 * c.B * m.width * (l == 1 ? c.d_in : m.width);
@@ -446,7 +451,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
         d.B = wptr(k, l);
         d.ldb = m.dp;
         d.C = act(dzb(l - 1), k);
-        d.Haux = act(Hl(l - 1), k);
+        d.mask = maskp(l - 1, k);
         d.colpart = bf.colpart + h->mem[k].act_off / kPartRows;
         d.ldc = m.dp;
         d.M = h->Bp;
@@ -493,6 +498,7 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
   bf.H = cv.take<char>((size_t)c.L * h->A * h->elt());
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
   bf.colpart = cv.take<float>((size_t)h->A / kPartRows);
+  bf.mask = cv.take<uint32_t>((size_t)c.L * (h->A / 32));
   bf.zeros = cv.take<char>(256);
   bf.dY = cv.take<float>((size_t)c.K * h->Bp * c.d_out);
   bf.rowloss = cv.take<float>((size_t)c.K * h->Bp);

@@ -94,14 +94,17 @@ __device__ __forceinline__ int kmaj_off(int row, int slot) {
   return row * ROW + ((slot ^ (row & 7) ^ ((row >> 3) & 7)) << 4);
 }
 
-// depth-contiguous bf16 layout used with direct-to-LDS loads: 4 planes (one per
-// 16-deep MFMA step) of R rows x 32 bytes; the two 16-byte halves of row r are
-// swapped when bit 2 of r is set, so the 16-byte fragment reads of 8
-// consecutive rows hit 8 distinct bank groups, and every fragment address is a
-// per-lane base plus compile-time offsets.
-template <int R>
+// depth-contiguous bf16 layout used with direct-to-LDS loads: 1 KB blocks of
+// 8 rows; inside a block, 4 planes (one per 16-deep MFMA step) of 8 rows x
+// 32 bytes.  The two 16-byte halves of a row's plane slice are swapped when
+// bit 2 xor bit 3 of the row is set, which keeps the 16-byte fragment reads of
+// 8 (and of 16) consecutive rows on distinct banks.  A block is exactly 8 full
+// 128-byte row segments of HBM, so one 64-lane direct load fills it with
+// whole cache lines, and every fragment address is a per-lane base plus
+// compile-time offsets.
+__device__ __forceinline__ int kmaj_sw(int row) { return ((row >> 2) ^ (row >> 3)) & 1; }
 __device__ __forceinline__ int kmaj16_off(int row, int ks, int h) {
-  return ks * (R * 32) + row * 32 + ((h ^ ((row >> 2) & 1)) << 4);
+  return (row >> 3) * 1024 + ks * 256 + (row & 7) * 32 + ((h ^ kmaj_sw(row)) << 4);
 }
 
 // rows-contiguous bf16 layout (R rows): byte offset of element `col` of depth row k
@@ -234,40 +237,48 @@ __device__ __forceinline__ void dma16(const void* src, char* lds) {
   __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)lds, 16, 0, 0);
 }
 
-// Depth-contiguous bf16 operand -> planar depth-contiguous LDS layout.  Wave w
-// fills plane w (depths 16w .. 16w+15 of the K step), 32 rows per 1 KB chunk;
-// a lane fetches 16 bytes (8 depths) of one row.
+// Depth-contiguous bf16 operand -> blocked depth-contiguous LDS layout.  Wave w
+// fills blocks w*PER .. w*PER+PER-1 (8 rows each); lane i fetches the 16 bytes
+// of plane i/16 of row (i/2)%8 that belong at LDS position 16*i, i.e. logical
+// half (i&1) ^ sw(row).  sw(row) depends on the block's parity, so a lane has
+// two source offsets, one per parity.
 template <int R>
 struct DmaKmaj {
-  static constexpr int PER = R / 32;  // chunks per wave (= per plane)
+  static constexpr int PER = R / 32;  // 1 KB blocks per wave
+  static_assert(PER % 2 == 0, "block parity follows p");
   const char* base;
   const void* zeros;
-  uint32_t off0;       // byte offset (depth 0) of this lane's vector in chunk 0
-  uint32_t rstep;      // bytes between the rows of consecutive chunks (32 rows)
-  int kofs;            // depth offset (elements) of this lane's vector inside a K step
-  uint32_t okmask;     // bit p: this lane's row of chunk p exists
+  uint32_t off[2];     // byte offset (depth 0) of this lane's vector in block 0 / 1
+  uint32_t bstep;      // bytes between the rows of blocks 2 apart (16 rows)
+  int kofs[2];         // depth offset (elements) of this lane's vector per block parity
+  uint32_t okmask;     // bit p: this lane's row of block p exists
   int wave;
   __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int, int wave_, int lane,
                        const void* z) {
     base = reinterpret_cast<const char*>(P);
     zeros = z;
     wave = wave_;
-    const int r = lane >> 1;                         // row inside a 32-row chunk
-    const int h = (lane & 1) ^ ((r >> 2) & 1);       // logical 16-byte half of the plane row
-    kofs = wave * 16 + h * 8;
-    off0 = (uint32_t)(((int64_t)(row0 + r) * ld + kofs) * 2);
-    rstep = (uint32_t)(32 * ld * 2);
+    const int r8 = (lane >> 1) & 7, ks = lane >> 4;
+#pragma unroll
+    for (int par = 0; par < 2; ++par) {
+      const int row = (wave * PER + par) * 8 + r8;  // PER is even: parity of p = parity of the block
+      const int h = (lane & 1) ^ kmaj_sw(row);
+      kofs[par] = ks * 16 + h * 8;
+      off[par] = (uint32_t)(((int64_t)(row0 + row) * ld + kofs[par]) * 2);
+    }
+    bstep = (uint32_t)(16 * ld * 2);
     okmask = 0;
 #pragma unroll
     for (int p = 0; p < PER; ++p)
-      if (row0 + p * 32 + r < rbound) okmask |= 1u << p;
+      if (row0 + (wave * PER + p) * 8 + r8 < rbound) okmask |= 1u << p;
   }
   __device__ void issue(char* lds, int k0, int kd) const {
-    const bool kin = k0 + kofs < kd;
+    const bool kin0 = k0 + kofs[0] < kd, kin1 = k0 + kofs[1] < kd;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
-      const bool in = kin && ((okmask >> p) & 1);
-      dma16(in ? base + off0 + p * rstep + (uint32_t)k0 * 2u : zeros, lds + wave * (R * 32) + p * 1024);
+      const bool in = ((p & 1) ? kin1 : kin0) && ((okmask >> p) & 1);
+      dma16(in ? base + off[p & 1] + (p >> 1) * bstep + (uint32_t)k0 * 2u : zeros,
+            lds + (wave * PER + p) * 1024);
     }
   }
 };
@@ -354,7 +365,7 @@ __device__ __forceinline__ bf16x8 frag_tr(const char* lds, int row_block, int ks
 
 template <int R>
 __device__ __forceinline__ bf16x8 frag_kmaj_bf16(const char* lds, int row_block, int ks, int lane) {
-  return *reinterpret_cast<const bf16x8*>(lds + kmaj16_off<R>(row_block + (lane & 31), ks, lane >> 5));
+  return *reinterpret_cast<const bf16x8*>(lds + kmaj16_off(row_block + (lane & 31), ks, lane >> 5));
 }
 
 template <bool TR, int R>
@@ -428,92 +439,142 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
 // Accumulator register r of a 32x32 block held by lane l is element
 // (row 8*(r/4) + 4*(l/32) + r%4, col l%32): each lane owns 4 runs of 4
 // consecutive rows of one column, so one Philox block (4 words) serves a run.
+//
+// Results leave through LDS: each wave stages one 32-row block of its
+// 32 x (32*NB) output at a time in a private region (row stride padded so the
+// two half-waves' column writes fall on disjoint banks), then reads it back as
+// 16-byte row vectors and stores whole row segments; a store instruction then
+// covers full 256- or 512-byte row pieces instead of 64-byte column strips.
+constexpr int kStageWave = 17408;  // bytes of LDS per wave for the staged block
+
+template <typename OT, int NB>
+struct Stage {
+  static constexpr int ES = sizeof(OT);
+  static constexpr int RS = NB * 32 * ES + (ES == 2 ? 16 : 32);  // padded row stride (bytes)
+  static constexpr int VPR = NB * 32 * ES / 16;                  // 16-byte vectors per row
+  static constexpr int PER_LANE = 32 * VPR / 64;
+  static_assert(32 * RS <= kStageWave, "stage region");
+};
+
+// Makes the staged block written by every lane of the wave visible to the
+// reads that follow (LDS executes one wave's operations in order; this keeps
+// the compiler from moving them across each other).
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <typename OT, int NB>
+__device__ __forceinline__ void stage_put(char* stage, int j, int g, int q, int lane, OT v) {
+  using S = Stage<OT, NB>;
+  *reinterpret_cast<OT*>(stage + (8 * g + 4 * (lane >> 5) + q) * S::RS + (32 * j + (lane & 31)) * S::ES) = v;
+}
+
+// Stores the staged 32-row block: rows row0.., columns col0.. of C (ld in
+// elements); rows >= M and vectors starting at or beyond N are skipped
+// (N is a multiple of the vector width).
+template <typename OT, int NB>
+__device__ __forceinline__ void stage_flush(const char* stage, OT* C, int64_t ld, int row0, int col0, int M, int N,
+                                            int lane) {
+  using S = Stage<OT, NB>;
+  constexpr int VE = 16 / S::ES;
+#pragma unroll
+  for (int it = 0; it < S::PER_LANE; ++it) {
+    const int v = it * 64 + lane;
+    const int r = v / S::VPR, c = v % S::VPR;
+    const uint4 x = *reinterpret_cast<const uint4*>(stage + r * S::RS + c * 16);
+    const int row = row0 + r, col = col0 + c * VE;
+    if (row < M && col < N) *reinterpret_cast<uint4*>(C + (int64_t)row * ld + col) = x;
+  }
+}
+
 template <typename T, int EPI, int SH>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, const Tile& t,
                                          f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn, int lane,
-                                         int mv, int nv) {
+                                         int mv, int nv, char* stage) {
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB;
   const int hv = lane >> 5;
-  // Rows outer, the NB column blocks inner: a row's offset is formed once and
-  // serves NB stores at compile-time distances, so no per-row addresses have
-  // to stay live beside the accumulators.
-  const int col0 = t.n0 + wn * NB * 32 + (lane & 31);
-  const int rbase = t.m0 + wm * MB * 32 + 4 * hv;
+  const int col0 = t.n0 + wn * NB * 32;  // the wave's first column
+  const int row0 = t.m0 + wm * MB * 32;  // the wave's first row
+  const int colL = col0 + (lane & 31);   // this lane's column in block j: colL + 32 j
   bool colin[NB];
 #pragma unroll
-  for (int j = 0; j < NB; ++j) colin[j] = j < nv && col0 + 32 * j < d.N;
+  for (int j = 0; j < NB; ++j) colin[j] = j < nv && colL + 32 * j < d.N;
   if constexpr (EPI == EPI_DW) {
-    float* C = static_cast<float*>(d.C) + col0;
+    float* C = static_cast<float*>(d.C);
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
       if (i >= mv) continue;
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = rbase + 32 * i + 8 * g + q;
-          if (row >= d.M) continue;
-          float* Cr = C + (int64_t)row * d.ldc;
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
-          for (int j = 0; j < NB; ++j)
-            if (colin[j]) Cr[32 * j] = acc[i][j][4 * g + q];
-        }
+          for (int q = 0; q < 4; ++q) stage_put<float, NB>(stage, j, g, q, lane, acc[i][j][4 * g + q]);
+      wave_sync_lds();
+      stage_flush<float, NB>(stage, C, d.ldc, row0 + 32 * i, col0, d.M, d.N, lane);
+      wave_sync_lds();
     }
   } else if constexpr (EPI == EPI_DX) {
-    // dZ = dH * (H_prev > 0) * s; H_prev already carries the dropout keep and
-    // the ReLU of the forward pass.  Column sums of dZ per 64-row half go to
-    // colpart (bias gradient partials, reduced by a later kernel).
-    T* C = static_cast<T*>(d.C) + col0;
-    const T* Hp = static_cast<const T*>(d.Haux) + col0;
+    // dZ = dH * [H_prev > 0] * s; the keep/ReLU decisions of the forward pass
+    // come as mask words (bit r of word (row/32, col) = row 32*(row/32) + r).
+    // Column sums of dZ per 64-row half go to colpart (bias-gradient
+    // partials, reduced by a later kernel).
+    T* C = static_cast<T*>(d.C);
+    float cs[NB];
 #pragma unroll
-    for (int ih = 0; ih < MB / 2; ++ih) {
-      float cs[NB];
+    for (int i = 0; i < MB; ++i) {
+      const int rb = row0 + 32 * i;
+      if ((i & 1) == 0) {
 #pragma unroll
-      for (int j = 0; j < NB; ++j) cs[j] = 0.0f;
+        for (int j = 0; j < NB; ++j) cs[j] = 0.0f;
+      }
+      uint32_t mw[NB];
 #pragma unroll
-      for (int ii = 0; ii < 2; ++ii) {
-        const int i = 2 * ih + ii;
+      for (int j = 0; j < NB; ++j)
+        mw[j] = (colin[j] && rb < d.M) ? d.mask[(int64_t)(rb >> 5) * d.N + colL + 32 * j] : 0u;
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int row = rbase + 32 * i + 8 * g + q;
-            const int64_t o = (int64_t)row * d.ldc;
-#pragma unroll
-            for (int j = 0; j < NB; ++j)
-              if (colin[j] && row < d.M) {
-                const float hp = to_float(Hp[o + 32 * j]);
-                const float dz = hp > 0.0f ? acc[i][j][4 * g + q] * d.drop_s : 0.0f;
-                cs[j] += dz;
-                C[o + 32 * j] = from_float<T>(dz);
-              }
+            const float dz = ((mw[j] >> (8 * g + 4 * hv + q)) & 1) ? acc[i][j][4 * g + q] * d.drop_s : 0.0f;
+            cs[j] += dz;
+            stage_put<T, NB>(stage, j, g, q, lane, from_float<T>(dz));
           }
-      }
-      const int64_t prow = (int64_t)((t.m0 + wm * MB * 32 + ih * 64) / kPartRows) * d.N;
+      wave_sync_lds();
+      stage_flush<T, NB>(stage, C, d.ldc, rb, col0, d.M, d.N, lane);
+      wave_sync_lds();
+      if (i & 1) {
+        const int hb = row0 + 32 * (i - 1);  // first row of this 64-row half
+        const int64_t prow = (int64_t)(hb / kPartRows) * d.N;
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        // lanes l and l^32 hold the two interleaved row halves of one column
-        const float c = cs[j] + __shfl_xor(cs[j], 32, 64);
-        if (hv == 0 && colin[j] && t.m0 + wm * MB * 32 + ih * 64 < d.M) d.colpart[prow + col0 + 32 * j] = c;
+        for (int j = 0; j < NB; ++j) {
+          // lanes l and l^32 hold the two interleaved row halves of one column
+          const float c = cs[j] + __shfl_xor(cs[j], 32, 64);
+          if (hv == 0 && colin[j] && hb < d.M) d.colpart[prow + colL + 32 * j] = c;
+        }
       }
     }
   } else {
-    T* C = static_cast<T*>(d.C) + col0;
+    T* C = static_cast<T*>(d.C);
     float bias[NB];
     bool colok[NB];
     uint64_t keep[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      bias[j] = colin[j] ? d.bias[col0 + 32 * j] : 0.0f;
-      colok[j] = col0 + 32 * j < d.width;
+      bias[j] = colin[j] ? d.bias[colL + 32 * j] : 0.0f;
+      colok[j] = colL + 32 * j < d.width;
       keep[j] = ~0ull;
     }
     if ((EPI == EPI_FWD) && d.drop_t != 0u) {
       // Keep bits of this lane's 4*MB runs of 4 rows: run r = 4*i + g covers
-      // rows rbase + 32*i + 8*g + (0..3), i.e. Philox block
-      // (m0 + wm*MB*32)/4 + 2*r + hv, words 0..3.  The loop over runs stays
-      // rolled and never touches the accumulators.
-      const uint32_t c0 = (uint32_t)((t.m0 + wm * MB * 32) >> 2) + (uint32_t)hv;
+      // rows row0 + 32*i + 8*g + 4*hv + (0..3), i.e. Philox block
+      // row0/4 + 2*r + hv, words 0..3.  The loop over runs stays rolled and
+      // never touches the accumulators.
+      const uint32_t c0 = (uint32_t)(row0 >> 2) + (uint32_t)hv;
       const uint32_t c2 = ((uint32_t)d.member << 8) | (uint32_t)a.layer;
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
@@ -521,7 +582,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
         uint64_t k = 0;
 #pragma unroll 1
         for (int r = 0; r < 4 * MB; ++r) {
-          const Words4 w = philox4x32_10(c0 + 2u * (uint32_t)r, (uint32_t)(col0 + 32 * j), c2, a.step, a.key0,
+          const Words4 w = philox4x32_10(c0 + 2u * (uint32_t)r, (uint32_t)(colL + 32 * j), c2, a.step, a.key0,
                                          a.key1);
           const uint64_t bits = (uint64_t)(w.w0 >= d.drop_t) | ((uint64_t)(w.w1 >= d.drop_t) << 1) |
                                 ((uint64_t)(w.w2 >= d.drop_t) << 2) | ((uint64_t)(w.w3 >= d.drop_t) << 3);
@@ -534,23 +595,36 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
       if (i >= mv) continue;
+      const int rb = row0 + 32 * i;
+      uint32_t mw[NB];
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+      for (int j = 0; j < NB; ++j) {
+        mw[j] = 0u;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = rbase + 32 * i + 8 * g + q;
-          if (row >= d.M) continue;
-          const bool rv = row < a.rows_valid;
-          T* Cr = C + (int64_t)row * d.ldc;
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
-          for (int j = 0; j < NB; ++j)
-            if (colin[j]) {
-              float h = fmaxf(acc[i][j][4 * g + q] + bias[j], 0.0f);
-              h = ((keep[j] >> (16 * i + 4 * g + q)) & 1) ? h * s_keep : 0.0f;
-              if (!colok[j] || !rv) h = 0.0f;
-              Cr[32 * j] = from_float<T>(h);
-            }
+          for (int q = 0; q < 4; ++q) {
+            const int row = rb + 8 * g + 4 * hv + q;
+            float h = fmaxf(acc[i][j][4 * g + q] + bias[j], 0.0f);
+            h = ((keep[j] >> (16 * i + 4 * g + q)) & 1) ? h * s_keep : 0.0f;
+            if (!colok[j] || row >= a.rows_valid) h = 0.0f;
+            const T hs = from_float<T>(h);
+            if (to_float(hs) > 0.0f) mw[j] |= 1u << (8 * g + 4 * hv + q);
+            stage_put<T, NB>(stage, j, g, q, lane, hs);
+          }
+      }
+      wave_sync_lds();
+      stage_flush<T, NB>(stage, C, d.ldc, rb, col0, d.M, d.N, lane);
+      wave_sync_lds();
+      if constexpr (EPI == EPI_FWD) {
+        // mask words for the backward pass: the two half-waves hold
+        // complementary bits of the same (32-row block, column) word
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const uint32_t w = mw[j] | (uint32_t)__shfl_xor((int)mw[j], 32, 64);
+          if (hv == 0 && colin[j] && rb < d.M) d.mask[(int64_t)(rb >> 5) * d.N + colL + 32 * j] = w;
         }
+      }
     }
   }
 }
@@ -627,7 +701,7 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
       __syncthreads();
     }
   }
-  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv);
+  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * kStageWave);
 }
 
 // ----------------------------------------------------------------- kernel --

@@ -37,7 +37,8 @@ struct GemmDesc {
   const void* B;
   void* C;
   const float* bias;   // EPI_FWD*: [N] fp32
-  const void* Haux;    // EPI_DX: activation H_{l-1}, same layout as C
+  uint32_t* mask;      // EPI_FWD: written, EPI_DX: read -- ReLU/dropout keep bits of the activation,
+                       // word (row/32, col) at mask[(row/32) * N + col], bit row % 32
   float* colpart;      // EPI_DX: [M / kPartRows, N] column sums of the unrounded output per row block
   int64_t lda, ldb, ldc;
   int32_t M, N, Kd;    // A rows in bounds (< M), B rows in bounds (< N), depth (< Kd)
