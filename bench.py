@@ -60,6 +60,8 @@ def main():
     ap.add_argument("--workload", default="regression_large")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=10)
+    ap.add_argument("--keep-grads", action="store_true",
+                    help="also write every gradient out (an inspection aid; the optimizer does not need it)")
     a = ap.parse_args()
     if a.gpus != 1:
         print(f"bench.py measures one GPU: the packed step runs all members on one device and this "
@@ -79,7 +81,9 @@ def main():
     total = a.warmup + a.steps + a.profile_steps
     idx_all = torch.stack([orders[:, (s % steps_per_epoch) * cfg["B"]:(s % steps_per_epoch + 1) * cfg["B"]]
                            for s in range(total)]).contiguous()
-    pk = tabpack.Pack(cfg).bind(dev)
+    # keep_grads=0: hidden-layer weight gradients go straight into the fused
+    # AdamW update of the weight-gradient GEMM instead of being stored as well
+    pk = tabpack.Pack(dict(cfg, keep_grads=int(a.keep_grads))).bind(dev)
     log(f"bound: workspace {pk.workspace_bytes() / 2**30:.2f} GiB")
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=dev)
     step = 0
@@ -134,7 +138,7 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": cfg["precision"], "data": "synthetic",
         "config": {"workload": cfg["name"], "K": cfg["K"], "B": cfg["B"], "d_in": cfg["d_in"], "L": cfg["L"],
                    "widths": [cfg["width_lo"], cfg["width_hi"]], "n_train": cfg["n_train"],
-                   "task": cfg["task"]},
+                   "task": cfg["task"], "keep_grads": int(a.keep_grads)},
         "roofline": roofline,
         "kernels": [{"name": s["name"], "bound": s["kind"], "avg_us": round(s["avg_ms"] * 1e3, 2),
                      "per_step_ms": round(s["total_ms"] / a.profile_steps, 4), "work_per_launch": s["work"]}

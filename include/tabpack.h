@@ -75,7 +75,9 @@ typedef struct pack_config {
   int32_t width_lo, width_hi;
   int32_t quantum;    /* padding quantum q for widths (multiple of 8); 0 selects 32 */
   int32_t decay_bias; /* 1: weight decay also on biases (torch default), 0: weights only */
-  int32_t reserved;
+  int32_t keep_grads; /* 1: pack_train_step() also stores every gradient for pack_get_grads();
+                         0: the hidden-layer weight gradients are consumed by the fused optimizer
+                         update without being written out (pack_get_grads() then fails) */
   double dropout_lo, dropout_hi;
   double lr_lo, lr_hi;
   double wd_lo, wd_hi;
@@ -172,8 +174,9 @@ int pack_member_param_count(const pack_handle* h, int32_t member, int64_t* count
 int pack_get_params(pack_handle* h, int32_t member, float* host_out);
 int pack_set_params(pack_handle* h, int32_t member, const float* host_in);
 
-/* Gradients of the last pack_train_step() and the AdamW moments of member k,
- * dense layout, copied to host buffers (synchronous). */
+/* Gradients of the last pack_train_step() (PACK_ESTATE unless the pack was
+ * created with keep_grads = 1) and the AdamW moments of member k, dense
+ * layout, copied to host buffers (synchronous). */
 int pack_get_grads(pack_handle* h, int32_t member, float* host_out);
 int pack_get_moments(pack_handle* h, int32_t member, float* m_out, float* v_out);
 

@@ -96,14 +96,18 @@ struct Bufs {
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
   float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / kPartRows floats
   uint32_t* mask = nullptr;  // ReLU/dropout keep bits of H_1..H_L, L * A / 32 words
+  uint32_t* keepw = nullptr; // dropout keep words of the current step, L * A / 32 words
   char* zeros = nullptr;     // 256 zero bytes: GEMM loads of out-of-range elements read them
   float *dY = nullptr, *rowloss = nullptr;
   MemberDev* d_mem = nullptr;
   uint32_t* d_chunks = nullptr;
+  uint32_t* d_aux = nullptr;
   int64_t* d_bias_off = nullptr;  // [L][K] offsets of b_l
   GemmDesc* d_descs = nullptr;
   Tile* d_tiles = nullptr;
   ColTile* d_coltiles = nullptr;
+  HeadTile* d_headtiles = nullptr;
+  float* headpart = nullptr;  // head backward partials, (Bp / RB) * (d_out + 1) * A / Bp floats
 };
 
 struct pack_handle {
@@ -116,13 +120,21 @@ struct pack_handle {
   int64_t A = 0;     // elements of one activation buffer (all members)
   std::vector<float> theta_host;  // host copy of the parameters, packed layout
   std::vector<uint32_t> chunk_tab;
+  std::vector<uint32_t> aux_chunks;  // chunks the separate AdamW pass updates (biases, head)
 
   bool bound = false;
   Bufs b;
   std::vector<Launch> fwd, dx, dw;  // per layer (index l-1)
   Launch fwd1_eval{};                // layer 1 over the shared validation rows in H_0 block 0
   int ncoltiles = 0;
+  int nheadtiles = 0;
+  int head_rb = 0;  // rows per head-backward block
   uint64_t t = 0;
+  bool small_tiles = true;  // plan every GEMM with 128x128 tiles only
+  // side stream for ALU-bound work that overlaps memory-bound kernels of the
+  // caller's stream, joined back through events (created by pack_bind)
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
 
   // optional per-kernel timing
   bool prof = false;
@@ -155,6 +167,7 @@ int validate(const pack_config* c) {
   }
   const int q = c->quantum ? c->quantum : 32;
   if (q < 8 || q > 512 || q % 8) return fail(PACK_EINVAL, "quantum %d must be a multiple of 8 in [8, 512]", q);
+  if (c->keep_grads != 0 && c->keep_grads != 1) return fail(PACK_EINVAL, "keep_grads must be 0 or 1");
   if (!(c->beta1 >= 0 && c->beta1 < 1 && c->beta2 >= 0 && c->beta2 < 1 && c->eps > 0))
     return fail(PACK_EINVAL, "AdamW constants out of range");
   if (!c->members) {
@@ -192,6 +205,7 @@ void plan_layout(pack_handle* h) {
   const pack_config& c = h->cfg;
   int64_t off = 0, aoff = 0;
   h->chunk_tab.clear();
+  h->aux_chunks.clear();
   for (int k = 0; k < c.K; ++k) {
     Member& m = h->mem[k];
     m.dp = (int)round_up(m.width, h->q);
@@ -204,7 +218,12 @@ void plan_layout(pack_handle* h) {
         m.toff[2 * l + part] = off;
         const int64_t nc = round_up(n, kChunk) / kChunk;
         const uint32_t flag = (part == 1 && !c.decay_bias) ? 0x80000000u : 0u;
-        for (int64_t i = 0; i < nc; ++i) h->chunk_tab.push_back((uint32_t)k | flag);
+        // hidden-layer weights are updated inside their weight-gradient GEMM
+        const bool fused = part == 0 && l < c.L;
+        for (int64_t i = 0; i < nc; ++i) {
+          if (!fused) h->aux_chunks.push_back((uint32_t)h->chunk_tab.size());
+          h->chunk_tab.push_back((uint32_t)k | flag);
+        }
         off += nc * kChunk;
       }
     }
@@ -285,6 +304,7 @@ struct Plan {
   std::vector<Tile> tiles;
   std::vector<int64_t> cost;  // planner's cost of each tile (depth x valid area)
   std::vector<ColTile> coltiles;
+  std::vector<HeadTile> headtiles;
   std::vector<Launch> fwd, dx, dw;
   Launch fwd1_eval{};
 };
@@ -361,9 +381,12 @@ void sort_launch(Plan& p, const Launch& ln) {
   }
 }
 
+// Rows per head-backward block: up to 256, dividing Bp.
+int head_rows(const pack_handle* h) { return h->Bp % 256 == 0 ? 256 : h->Bp; }
+
 Plan build_plan(const pack_handle* h, const Bufs& bf) {
   Plan p;
-  p.small_only = h->prec == Prec::FP32;
+  p.small_only = h->prec == Prec::FP32 || h->small_tiles;
   const pack_config& c = h->cfg;
   const size_t es = h->elt();
   const void* wsrc = h->prec == Prec::BF16 ? (const void*)bf.shadow : (const void*)bf.theta;
@@ -398,6 +421,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.drop_t = m.t;
       d.drop_s = (float)m.scale;
       d.mask = maskp(l, k);
+      d.keepw = bf.keepw + (maskp(l, k) - bf.mask);
       p.descs.push_back(d);
       add_tiles(p, f, f.desc0 + k, h->Bp, m.dp, d.Kd);
       f.flops += 2.0 * c.B * m.width * (l == 1 ? c.d_in : m.width);
@@ -433,6 +457,9 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.N = l == 1 ? h->Pin : m.dp;
       d.Kd = h->Bp;
       d.member = k;
+      d.poff = m.toff[2 * (l - 1)];
+      d.lr = (float)m.lr;
+      d.wd = (float)m.wd;
       p.descs.push_back(d);
       add_tiles(p, w, w.desc0 + k, d.M, d.N, d.Kd);
       w.flops += 2.0 * c.B * m.width * (l == 1 ? c.d_in : m.width);
@@ -469,6 +496,10 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   }
   for (int k = 0; k < c.K; ++k)
     for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
+  const int hcols = head_bwd_cols(c.d_out), hrb = head_rows(h);
+  for (int r0 = 0; r0 < h->Bp; r0 += hrb)
+    for (int k = 0; k < c.K; ++k)
+      for (int c0 = 0; c0 < h->mem[k].dp; c0 += hcols) p.headtiles.push_back(HeadTile{k, c0, r0});
   return p;
 }
 
@@ -499,16 +530,20 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
   bf.colpart = cv.take<float>((size_t)h->A / kPartRows);
   bf.mask = cv.take<uint32_t>((size_t)c.L * (h->A / 32));
+  bf.keepw = cv.take<uint32_t>((size_t)c.L * (h->A / 32));
   bf.zeros = cv.take<char>(256);
   bf.dY = cv.take<float>((size_t)c.K * h->Bp * c.d_out);
   bf.rowloss = cv.take<float>((size_t)c.K * h->Bp);
   bf.d_mem = cv.take<MemberDev>(c.K);
   bf.d_chunks = cv.take<uint32_t>(h->chunk_tab.size());
+  bf.d_aux = cv.take<uint32_t>(h->aux_chunks.size());
   bf.d_bias_off = cv.take<int64_t>((size_t)c.L * c.K);
   Plan plan = build_plan(h, bf);
   bf.d_descs = cv.take<GemmDesc>(plan.descs.size());
   bf.d_tiles = cv.take<Tile>(plan.tiles.size());
   bf.d_coltiles = cv.take<ColTile>(plan.coltiles.size());
+  bf.d_headtiles = cv.take<HeadTile>(plan.headtiles.size());
+  bf.headpart = cv.take<float>((size_t)(h->Bp / head_rows(h)) * (c.d_out + 1) * (h->A / h->Bp));
   if (plan_out) *plan_out = std::move(plan);
   return (size_t)round_up((int64_t)cv.off, 256);
 }
@@ -526,6 +561,7 @@ GemmArgs base_args(const pack_handle* h) {
   a.descs = h->b.d_descs;
   a.tiles = h->b.d_tiles;
   a.zeros = h->b.zeros;
+  a.small_only = (h->prec == Prec::FP32 || h->small_tiles) ? 1 : 0;
   const Key kd = stream_key(h->cfg.seed, kTagDropout);
   a.key0 = kd.k0;
   a.key1 = kd.k1;
@@ -598,6 +634,10 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
   h->prec = cfg->precision == PACK_PREC_BF16 ? Prec::BF16 : Prec::FP32;
   h->task = (Task)cfg->task;
   h->q = cfg->quantum ? cfg->quantum : 32;
+  // 128x128 tiles at two workgroups per CU measure faster on the packed
+  // workloads than 256x256 tiles at one; TABPACK_GEMM_TILES=big selects the latter
+  h->small_tiles = true;
+  if (const char* e = getenv("TABPACK_GEMM_TILES")) h->small_tiles = std::string(e) != "big";
   h->Bp = (int)round_up(cfg->B, kRowAlign);
   h->Pin = (int)round_up(cfg->d_in, 8);
   h->mem.resize(cfg->K);
@@ -629,8 +669,12 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
 }
 
 int pack_destroy(pack_handle* h) {
-  if (h)
+  if (h) {
     for (hipEvent_t e : h->event_pool) (void)hipEventDestroy(e);
+    if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+    if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+    if (h->side) (void)hipStreamDestroy(h->side);
+  }
   delete h;
   return PACK_OK;
 }
@@ -659,6 +703,11 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   if (bytes < need) return fail(PACK_EINVAL, "workspace has %zu bytes, %zu needed", bytes, need);
   Plan plan;
   carve(h, static_cast<char*>(workspace), h->b, &plan);
+  if (!h->side) {
+    HIP_TRY(hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
+    HIP_TRY(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming));
+  }
   HIP_TRY(hipMemsetAsync(workspace, 0, need, stream));
   HIP_TRY(hipMemcpyAsync(h->b.theta, h->theta_host.data(), h->P * sizeof(float), hipMemcpyHostToDevice, stream));
   std::vector<MemberDev> md(h->cfg.K);
@@ -671,10 +720,12 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   }
   HIP_TRY(hipMemcpyAsync(h->b.d_mem, md.data(), md.size() * sizeof(MemberDev), hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_chunks, h->chunk_tab.data(), h->chunk_tab.size() * 4, hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.d_aux, h->aux_chunks.data(), h->aux_chunks.size() * 4, hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_bias_off, boff.data(), boff.size() * 8, hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_descs, plan.descs.data(), plan.descs.size() * sizeof(GemmDesc), hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_tiles, plan.tiles.data(), plan.tiles.size() * sizeof(Tile), hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_coltiles, plan.coltiles.data(), plan.coltiles.size() * sizeof(ColTile), hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.d_headtiles, plan.headtiles.data(), plan.headtiles.size() * sizeof(HeadTile), hipMemcpyHostToDevice, stream));
   if (h->prec == Prec::BF16) HIP_TRY(launch_to_shadow(h->b.theta, h->b.shadow, h->P, stream));
   HIP_TRY(hipStreamSynchronize(stream));
   h->fwd = plan.fwd;
@@ -682,6 +733,8 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   h->dw = plan.dw;
   h->fwd1_eval = plan.fwd1_eval;
   h->ncoltiles = (int)plan.coltiles.size();
+  h->nheadtiles = (int)plan.headtiles.size();
+  h->head_rb = head_rows(h);
   h->t = 0;
   h->bound = true;
   return PACK_OK;
@@ -710,9 +763,25 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, stream,
                  [&] { return launch_gemm(h->prec, ak, bk, e, al, stream); });
   };
+  int max_dp = 0;
+  double nkeep = 0;
+  for (const Member& m : h->mem) {
+    max_dp = std::max(max_dp, m.dp);
+    nkeep += (double)c.L * h->Bp * m.dp / 8;
+  }
+  // the dropout keep words (Philox, ALU-bound) are generated on the side
+  // stream while the gather (HBM-bound) runs; the forward GEMMs wait for both
+  HIP_TRY(hipEventRecord(h->ev_fork, stream));
+  HIP_TRY(hipStreamWaitEvent(h->side, h->ev_fork, 0));
+  HIP_TRY(timed(h, "dropout_words", 1, nkeep, h->side, [&] {
+    return launch_dropout_words(a.key0, a.key1, a.step, h->b.d_mem, c.K, c.L, max_dp, h->Bp, c.B, h->A / 32,
+                                h->b.keepw, h->side);
+  }));
+  HIP_TRY(hipEventRecord(h->ev_join, h->side));
   HIP_TRY(timed(h, "gather", 1, (double)c.K * c.B * c.d_in * (4.0 + h->elt()), stream, [&] {
     return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, c.K, h->Bp, h->b.H0, stream);
   }));
+  HIP_TRY(hipStreamWaitEvent(stream, h->ev_join, 0));
   for (int l = 1; l <= c.L; ++l) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[l - 1], l));
   HIP_TRY(timed(h, "head_fwd", 1, act_bytes, stream, [&] {
     return launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, y,
@@ -723,11 +792,18 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                               stream);
   }));
   HIP_TRY(timed(h, "head_bwd", 1, 2.0 * act_bytes, stream, [&] {
-    return launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp,
-                           c.d_out, h->b.dY, h->dzb(c.L), h->b.grad, stream);
+    return launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_headtiles, h->nheadtiles, h->Bp,
+                           h->head_rb, c.d_out, h->b.dY, h->dzb(c.L), h->b.headpart, stream);
   }));
+  HIP_TRY(timed(h, "head_grad_reduce", 1, 4.0 * (h->Bp / h->head_rb) * (c.d_out + 1) * (h->A / h->Bp), stream, [&] {
+    return launch_head_grad_reduce(h->b.headpart, h->b.d_mem, c.K, max_dp, h->Bp, h->head_rb, c.d_out, h->b.grad,
+                                   stream);
+  }));
+  const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
+  const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
+  const AdamConst ac{(float)c.beta1, (float)c.beta2, (float)c.eps, (float)bc1, (float)std::sqrt(bc2)};
   for (int l = c.L; l >= 1; --l) {
-    HIP_TRY(gemm(OP_RMAJ, OP_RMAJ, EPI_DW, h->dw[l - 1], l));
+    // dX_l reads W_l, so it runs before the weight-gradient GEMM updates W_l in place
     if (l > 1) {
       HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[l - 1], l));
       HIP_TRY(timed(h, "bias_from_partials", 1, act_bytes * 4 / h->elt() / kPartRows, stream, [&] {
@@ -735,15 +811,29 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                                          h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, stream);
       }));
     }
+    GemmArgs al = for_launch(a, h->dw[l - 1]);
+    al.layer = l;
+    al.theta = h->b.theta;
+    al.am = h->b.m;
+    al.av = h->b.v;
+    al.shadow = h->b.shadow;
+    al.beta1 = ac.beta1;
+    al.beta2 = ac.beta2;
+    al.eps = ac.eps;
+    al.bc1 = ac.bc1;
+    al.bc2_sqrt = ac.bc2_sqrt;
+    al.keep_grad = c.keep_grads ? 1 : 0;
+    HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW), 0, h->dw[l - 1].flops, stream,
+                  [&] { return launch_gemm(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW, al, stream); }));
   }
-  const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
-  const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
-  double nparam = 0;
-  for (int k = 0; k < c.K; ++k) nparam += (double)dense_count(h, k);
-  HIP_TRY(timed(h, "adamw", 1, nparam * (h->prec == Prec::BF16 ? 30.0 : 28.0), stream, [&] {
-    return launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, h->b.shadow, h->b.d_chunks, h->b.d_mem,
-                        (int64_t)h->chunk_tab.size(), (float)bc1, (float)std::sqrt(bc2), (float)c.beta1,
-                        (float)c.beta2, (float)c.eps, stream);
+  double naux = 0;
+  for (int k = 0; k < c.K; ++k) {
+    const Member& m = h->mem[k];
+    naux += (double)c.L * m.width + (double)c.d_out * m.width + c.d_out;
+  }
+  HIP_TRY(timed(h, "adamw", 1, naux * (h->prec == Prec::BF16 ? 30.0 : 28.0), stream, [&] {
+    return launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, h->b.shadow, h->b.d_chunks, h->b.d_aux,
+                        h->b.d_mem, (int64_t)h->aux_chunks.size(), ac, stream);
   }));
   h->t = step;
   return PACK_OK;
@@ -855,6 +945,7 @@ int pack_get_grads(pack_handle* h, int32_t member, float* host_out) {
   if (rc) return rc;
   if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
   if (!host_out) return fail(PACK_EINVAL, "host_out is NULL");
+  if (!h->cfg.keep_grads) return fail(PACK_ESTATE, "gradients are kept only with pack_config.keep_grads = 1");
   return copy_member(h, member, h->b.grad, host_out);
 }
 

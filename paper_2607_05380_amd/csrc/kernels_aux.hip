@@ -7,6 +7,7 @@
 #include <math.h>
 
 #include "pack_internal.h"
+#include "adamw.h"
 #include "philox.h"
 
 namespace tabpack {
@@ -68,34 +69,86 @@ __device__ __forceinline__ double finish_score(Task task, double sum, int64_t n)
 }
 
 // ------------------------------------------------------------------- head --
-// One wave per (member, row): Y = H_L[row] . W_out^T + b_out, then either the
-// training loss and dLoss/dY of the row, or the eval prediction.
-template <typename T, bool EVAL>
+// 8 consecutive activations (one 16-byte bf16 vector, two fp32 vectors).
+template <typename T>
+struct Vec8;
+template <>
+struct Vec8<__bf16> {
+  __device__ static void load(const __bf16* p, float (&x)[8]) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+  __device__ static void store(__bf16* p, const float (&x)[8]) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[2 * i]) |
+             ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[2 * i + 1]) << 16);
+    *reinterpret_cast<uint4*>(p) = uint4{w[0], w[1], w[2], w[3]};
+  }
+};
+template <>
+struct Vec8<float> {
+  __device__ static void load(const float* p, float (&x)[8]) {
+    const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  }
+  __device__ static void store(float* p, const float (&x)[8]) {
+    *reinterpret_cast<float4*>(p) = float4{x[0], x[1], x[2], x[3]};
+    *reinterpret_cast<float4*>(p + 4) = float4{x[4], x[5], x[6], x[7]};
+  }
+};
+
+// Y = H_L[row] . W_out^T + b_out for 8 rows per wave (8 lanes per row, each
+// lane a 16-byte column vector per step), then either the training loss and
+// dLoss/dY of the row, or the eval prediction.  D >= d_out is the output count
+// rounded up to a power of two.
+template <typename T, bool EVAL, int D>
 __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, const float* theta,
                                                        const MemberDev* mem, int Bp, int d_out,
                                                        const void* y, const int32_t* idx, int B,
                                                        int rows_valid, int64_t row_base, int64_t Nv,
                                                        float* dY, float* rowloss, float* pred) {
   const int k = blockIdx.y;
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= Bp) return;
+  const int lane = threadIdx.x & 63, sub = lane & 7;
+  const int row = blockIdx.x * 32 + (threadIdx.x >> 3);
+  if (row >= Bp) return;  // Bp is a multiple of 32: whole 8-lane groups leave together
   const MemberDev md = mem[k];
   const T* h = H + md.act_off + (int64_t)row * md.dp;
   const float* Wo = theta + md.w_out_off;
-  float acc[kMaxOut];
+  float acc[D];
 #pragma unroll
-  for (int o = 0; o < kMaxOut; ++o) acc[o] = 0.0f;
-  for (int c = lane; c < md.dp; c += 64) {
-    const float hv = ld_act(h, c);
+  for (int o = 0; o < D; ++o) acc[o] = 0.0f;
+  for (int c = sub * 8; c < md.dp; c += 64) {
+    float x[8];
+    Vec8<T>::load(h + c, x);
 #pragma unroll
-    for (int o = 0; o < kMaxOut; ++o)
-      if (o < d_out) acc[o] += hv * Wo[(int64_t)o * md.dp + c];
+    for (int o = 0; o < D; ++o) {
+      if (o >= d_out) break;
+      const float4 w0 = *reinterpret_cast<const float4*>(Wo + (int64_t)o * md.dp + c);
+      const float4 w1 = *reinterpret_cast<const float4*>(Wo + (int64_t)o * md.dp + c + 4);
+      acc[o] += ((x[0] * w0.x + x[1] * w0.y) + (x[2] * w0.z + x[3] * w0.w)) +
+                ((x[4] * w1.x + x[5] * w1.y) + (x[6] * w1.z + x[7] * w1.w));
+    }
   }
   float z[kMaxOut];
 #pragma unroll
-  for (int o = 0; o < kMaxOut; ++o) z[o] = (o < d_out) ? wave_sum(acc[o]) + theta[md.b_out_off + o] : 0.0f;
-  if (lane != 0) return;
+  for (int o = 0; o < kMaxOut; ++o) z[o] = 0.0f;
+#pragma unroll
+  for (int o = 0; o < D; ++o) {
+    float v = acc[o];
+    v += __shfl_xor(v, 1, 64);
+    v += __shfl_xor(v, 2, 64);
+    v += __shfl_xor(v, 4, 64);
+    if (o < d_out) z[o] = v + theta[md.b_out_off + o];
+  }
+  if (sub != 0) return;
 
   const bool valid = EVAL ? row < rows_valid : row < B;
   int64_t src = 0;
@@ -166,54 +219,130 @@ __global__ __launch_bounds__(256) void loss_reduce_kernel(const float* rowloss, 
   }
 }
 
-// Column sweep of the head backward for 64 columns of one member:
-//   dH_L = dY W_out, dZ_L = dH_L * [H_L > 0] * s_k, dW_out = dY^T H_L, db_L = sum_rows dZ_L.
+// CPT consecutive activations of one row.
+template <typename T, int CPT>
+struct VecN;
 template <typename T>
-__global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* theta,
-                                                       const MemberDev* mem, const ColTile* tiles,
-                                                       int Bp, int d_out, const float* dY, T* dZ,
-                                                       float* grad) {
-  __shared__ float shw[4][kMaxOut + 1][64];
-  const ColTile ct = tiles[blockIdx.x];
-  const MemberDev md = mem[ct.member];
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int c = ct.c0 + tx;
-  const bool valid = c < md.dp;
-  float wo[kMaxOut], accw[kMaxOut];
-#pragma unroll
-  for (int o = 0; o < kMaxOut; ++o) {
-    wo[o] = (valid && o < d_out) ? theta[md.w_out_off + (int64_t)o * md.dp + c] : 0.0f;
-    accw[o] = 0.0f;
+struct VecN<T, 8> {
+  __device__ static void load(const T* p, float (&x)[8]) { Vec8<T>::load(p, x); }
+  __device__ static void store(T* p, const float (&x)[8]) { Vec8<T>::store(p, x); }
+};
+template <>
+struct VecN<__bf16, 4> {
+  __device__ static void load(const __bf16* p, float (&x)[4]) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    x[0] = __uint_as_float(u.x << 16);
+    x[1] = __uint_as_float(u.x & 0xFFFF0000u);
+    x[2] = __uint_as_float(u.y << 16);
+    x[3] = __uint_as_float(u.y & 0xFFFF0000u);
   }
-  float accb = 0.0f;
+  __device__ static void store(__bf16* p, const float (&x)[4]) {
+    const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[0]) |
+                        ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[1]) << 16);
+    const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[2]) |
+                        ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[3]) << 16);
+    *reinterpret_cast<uint2*>(p) = uint2{lo, hi};
+  }
+};
+template <>
+struct VecN<float, 4> {
+  __device__ static void load(const float* p, float (&x)[4]) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  }
+  __device__ static void store(float* p, const float (&x)[4]) {
+    *reinterpret_cast<float4*>(p) = float4{x[0], x[1], x[2], x[3]};
+  }
+};
+
+// Head backward over one (member, 32*CPT columns, RB rows) block:
+//   dH_L = dY W_out, dZ_L = dH_L * [H_L > 0] * s_k (written out),
+//   and this row block's partial sums of dW_out = dY^T H_L and db_L = sum dZ_L,
+//   reduced over the block's 8 row slots in a fixed order and stored to part
+//   (part[(rb * (d_out + 1) + o) * dp + c]; o = d_out holds db_L).
+template <typename T, int D, int CPT>
+__global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* theta, const MemberDev* mem,
+                                                       const HeadTile* tiles, int Bp, int d_out, int RB,
+                                                       const float* dY, T* dZ, float* part) {
+  __shared__ float red[8][32 * CPT];
+  const HeadTile ht = tiles[blockIdx.x];
+  const MemberDev md = mem[ht.member];
+  const int cv = threadIdx.x & 31, slot = threadIdx.x >> 5;
+  const int c = ht.c0 + cv * CPT;
+  const bool valid = c < md.dp;
+  float wo[D][CPT], accw[D][CPT], accb[CPT];
+#pragma unroll
+  for (int o = 0; o < D; ++o)
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      wo[o][j] = (valid && o < d_out) ? theta[md.w_out_off + (int64_t)o * md.dp + c + j] : 0.0f;
+      accw[o][j] = 0.0f;
+    }
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) accb[j] = 0.0f;
   const T* h = H + md.act_off;
   T* dz = dZ + md.act_off;
-  const float* dyk = dY + (int64_t)ct.member * Bp * d_out;
-  for (int b = ty; b < Bp; b += 4) {
-    float dy[kMaxOut];
+  const float* dyk = dY + (int64_t)ht.member * Bp * d_out;
+  const int r1 = min(ht.r0 + RB, Bp);
+  for (int r = ht.r0 + slot; r < r1; r += 8) {
+    float dy[D];
 #pragma unroll
-    for (int o = 0; o < kMaxOut; ++o) dy[o] = (o < d_out) ? dyk[(int64_t)b * d_out + o] : 0.0f;
-    const float hv = valid ? ld_act(h, (int64_t)b * md.dp + c) : 0.0f;
-    float dh = 0.0f;
+    for (int o = 0; o < D; ++o) dy[o] = o < d_out ? dyk[(int64_t)r * d_out + o] : 0.0f;
+    if (!valid) continue;
+    float hv[CPT], g[CPT];
+    VecN<T, CPT>::load(h + (int64_t)r * md.dp + c, hv);
 #pragma unroll
-    for (int o = 0; o < kMaxOut; ++o) {
-      dh += dy[o] * wo[o];
-      accw[o] += dy[o] * hv;
+    for (int j = 0; j < CPT; ++j) {
+      float dh = 0.0f;
+#pragma unroll
+      for (int o = 0; o < D; ++o) {
+        dh += dy[o] * wo[o][j];
+        accw[o][j] += dy[o] * hv[j];
+      }
+      g[j] = hv[j] > 0.0f ? dh * md.drop_s : 0.0f;
+      accb[j] += g[j];
     }
-    const float g = hv > 0.0f ? dh * md.drop_s : 0.0f;
-    if (valid) st_act(dz, (int64_t)b * md.dp + c, g);
-    accb += g;
+    VecN<T, CPT>::store(dz + (int64_t)r * md.dp + c, g);
   }
+  // fixed-order reduction over the 8 row slots, one quantity at a time
+  float* pk = part + (int64_t)(Bp / RB) * (d_out + 1) * (md.act_off / Bp);
+  const int rb = ht.r0 / RB;
+  for (int o = 0; o <= d_out; ++o) {
 #pragma unroll
-  for (int o = 0; o < kMaxOut; ++o) shw[ty][o][tx] = accw[o];
-  shw[ty][kMaxOut][tx] = accb;
-  __syncthreads();
-  if (ty == 0 && valid) {
-    for (int o = 0; o < d_out; ++o)
-      grad[md.w_out_off + (int64_t)o * md.dp + c] =
-          (shw[0][o][tx] + shw[1][o][tx]) + (shw[2][o][tx] + shw[3][o][tx]);
-    grad[md.b_last_off + c] =
-        (shw[0][kMaxOut][tx] + shw[1][kMaxOut][tx]) + (shw[2][kMaxOut][tx] + shw[3][kMaxOut][tx]);
+    for (int j = 0; j < CPT; ++j) {
+      float v = accb[j];  // o == d_out: the bias partial
+#pragma unroll
+      for (int oo = 0; oo < D; ++oo)
+        if (oo == o && o < d_out) v = accw[oo][j];
+      red[slot][cv * CPT + j] = v;
+    }
+    __syncthreads();
+    const int cc = threadIdx.x;  // one column of the block per thread
+    if (cc < 32 * CPT && ht.c0 + cc < md.dp) {
+      const float v = ((red[0][cc] + red[1][cc]) + (red[2][cc] + red[3][cc])) +
+                      ((red[4][cc] + red[5][cc]) + (red[6][cc] + red[7][cc]));
+      pk[((int64_t)rb * (d_out + 1) + o) * md.dp + ht.c0 + cc] = v;
+    }
+    __syncthreads();
+  }
+}
+
+// dW_out and db_L of every member from the head backward's row-block partials
+// (fixed order over the row blocks).
+__global__ __launch_bounds__(256) void head_grad_reduce_kernel(const float* part, const MemberDev* mem, int Bp,
+                                                               int nrb, int d_out, float* grad) {
+  const int k = blockIdx.y;
+  const MemberDev md = mem[k];
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= md.dp) return;
+  const float* pk = part + (int64_t)nrb * (d_out + 1) * (md.act_off / Bp);
+  for (int o = 0; o <= d_out; ++o) {
+    float s = 0.0f;
+    for (int rb = 0; rb < nrb; ++rb) s += pk[((int64_t)rb * (d_out + 1) + o) * md.dp + c];
+    if (o < d_out)
+      grad[md.w_out_off + (int64_t)o * md.dp + c] = s;
+    else
+      grad[md.b_last_off + c] = s;
   }
 }
 
@@ -277,28 +406,23 @@ __global__ __launch_bounds__(256) void gather_kernel(const float* X, int d_in, i
 template <bool SHADOW>
 __global__ __launch_bounds__(256) void adamw_kernel(float* theta, const float* grad, float* m,
                                                     float* v, uint16_t* shadow,
-                                                    const uint32_t* chunk_tab, const MemberDev* mem,
-                                                    int64_t nchunks, float bc1, float bc2_sqrt,
-                                                    float beta1, float beta2, float eps) {
+                                                    const uint32_t* chunk_tab, const uint32_t* list,
+                                                    const MemberDev* mem, int64_t nchunks, AdamConst ac) {
   const int lane = threadIdx.x & 63;
   const int64_t nw = (int64_t)gridDim.x * 4;
-  for (int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); c < nchunks; c += nw) {
+  const int64_t w0 = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (int64_t w = w0; w < nchunks; w += nw) {
+    const int64_t c = list ? (int64_t)list[w] : w;
     const uint32_t e = chunk_tab[c];
     const MemberDev md = mem[e & 0x7FFFFFFFu];
     const float decay = (e >> 31) ? 1.0f : 1.0f - md.lr * md.wd;
-    const float step = md.lr / bc1;
+    const float step = md.lr / ac.bc1;
     const int64_t i = c * kChunk + lane * 4;
     f32x4 th = *reinterpret_cast<const f32x4*>(theta + i);
     const f32x4 g = *reinterpret_cast<const f32x4*>(grad + i);
     f32x4 mm = *reinterpret_cast<const f32x4*>(m + i);
     f32x4 vv = *reinterpret_cast<const f32x4*>(v + i);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      th[q] *= decay;
-      mm[q] = beta1 * mm[q] + (1.0f - beta1) * g[q];
-      vv[q] = beta2 * vv[q] + (1.0f - beta2) * g[q] * g[q];
-      th[q] -= step * mm[q] / (sqrtf(vv[q]) / bc2_sqrt + eps);
-    }
+    adamw_vec4(th, g, mm, vv, decay, step, ac);
     *reinterpret_cast<f32x4*>(theta + i) = th;
     *reinterpret_cast<f32x4*>(m + i) = mm;
     *reinterpret_cast<f32x4*>(v + i) = vv;
@@ -330,16 +454,50 @@ __global__ __launch_bounds__(256) void eval_score_kernel(Task task, const float*
   if (threadIdx.x == 0) score_out[k] = finish_score(task, s, Nv);
 }
 
+// Keep word of a dropout mask: bit r is set iff row 32*rb + r of column c is
+// kept, i.e. word (r & 3) of Philox block (r >> 2, c, c2, step) is >= t.  The
+// training path (dropout_words_kernel -> forward epilogue) and the test hook
+// below both go through this function.
+__device__ __forceinline__ uint32_t keep_word(uint32_t key0, uint32_t key1, uint32_t step, uint32_t c2, int rb,
+                                              int c, uint32_t t) {
+  uint32_t w = 0;
+#pragma unroll 2
+  for (int b = 0; b < 8; ++b) {
+    const Words4 x = philox4x32_10((uint32_t)(rb * 8 + b), (uint32_t)c, c2, step, key0, key1);
+    w |= ((uint32_t)(x.w0 >= t) | ((uint32_t)(x.w1 >= t) << 1) | ((uint32_t)(x.w2 >= t) << 2) |
+          ((uint32_t)(x.w3 >= t) << 3))
+         << (4 * b);
+  }
+  return w;
+}
+
+// Keep words of every hidden layer of every member for one training step:
+// word (rb, c) of layer l, member k at out[(l-1)*A32 + act_off/32 + rb*dp + c].
+// Rows >= rows_valid and columns >= width get 0 (the epilogue zeroes them).
+__global__ __launch_bounds__(256) void dropout_words_kernel(uint32_t key0, uint32_t key1, uint32_t step,
+                                                            const MemberDev* mem, int Bp, int rows_valid,
+                                                            int64_t A32, uint32_t* out) {
+  const int k = blockIdx.y, l = blockIdx.z + 1;
+  const MemberDev md = mem[k];
+  const int64_t nw = (int64_t)(Bp / 32) * md.dp;
+  const int64_t w = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (w >= nw) return;
+  const int rb = (int)(w / md.dp), c = (int)(w % md.dp);
+  uint32_t word = 0;
+  if (rb * 32 < rows_valid && c < md.width)
+    word = md.drop_t == 0u ? ~0u : keep_word(key0, key1, step, ((uint32_t)k << 8) | (uint32_t)l, rb, c, md.drop_t);
+  out[(int64_t)(l - 1) * A32 + md.act_off / 32 + w] = word;
+}
+
+// Test hook: the keep mask of one (layer, member) as bytes [B, width].
 __global__ void dropout_mask_kernel(uint32_t key0, uint32_t key1, uint32_t step, int layer,
                                     int member, uint32_t t, int B, int width, uint8_t* out) {
-  const int64_t n = (int64_t)B * width;
+  const int64_t n = (int64_t)((B + 31) / 32) * width;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const int r = (int)(i / width), c = (int)(i % width);
-    const Words4 w = philox4x32_10((uint32_t)r >> 2, (uint32_t)c,
-                                   ((uint32_t)member << 8) | (uint32_t)layer, step, key0, key1);
-    const uint32_t wq[4] = {w.w0, w.w1, w.w2, w.w3};
-    out[i] = wq[r & 3] >= t ? 1 : 0;
+    const int rb = (int)(i / width), c = (int)(i % width);
+    const uint32_t w = keep_word(key0, key1, step, ((uint32_t)member << 8) | (uint32_t)layer, rb, c, t);
+    for (int r = 0; r < 32 && rb * 32 + r < B; ++r) out[(int64_t)(rb * 32 + r) * width + c] = (w >> r) & 1;
   }
 }
 
@@ -457,32 +615,72 @@ inline int grid_for(int64_t n, int per) {
 
 int select_blocks(int64_t Nv) { return (int)((Nv + kSelRows - 1) / kSelRows); }
 
+namespace {
+template <typename T, bool EVAL, int D>
+void head_fwd_t(dim3 grid, hipStream_t s, Task task, const void* H, const float* theta, const MemberDev* mem,
+                int Bp, int d_out, const void* y, const int32_t* idx, int B, int rows_valid, int64_t row_base,
+                int64_t Nv, float* dY, float* rowloss, float* pred) {
+  hipLaunchKernelGGL((head_fwd_kernel<T, EVAL, D>), grid, dim3(256), 0, s, task, static_cast<const T*>(H), theta,
+                     mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, rowloss, pred);
+}
+
+template <typename T, bool EVAL>
+void head_fwd_d(int d_out, dim3 grid, hipStream_t s, Task task, const void* H, const float* theta,
+                const MemberDev* mem, int Bp, const void* y, const int32_t* idx, int B, int rows_valid,
+                int64_t row_base, int64_t Nv, float* dY, float* rowloss, float* pred) {
+#define TABPACK_HEAD_FWD(DD) \
+  head_fwd_t<T, EVAL, DD>(grid, s, task, H, theta, mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, rowloss, pred)
+  if (d_out <= 1) TABPACK_HEAD_FWD(1);
+  else if (d_out <= 2) TABPACK_HEAD_FWD(2);
+  else if (d_out <= 4) TABPACK_HEAD_FWD(4);
+  else if (d_out <= 8) TABPACK_HEAD_FWD(8);
+  else TABPACK_HEAD_FWD(16);
+#undef TABPACK_HEAD_FWD
+}
+
+}  // namespace
+
 hipError_t launch_head_fwd(Prec prec, Task task, bool eval, const void* H, const float* theta,
                            const MemberDev* mem, int K, int Bp, int d_out, const void* y,
                            const int32_t* idx, int B, int rows_valid, int64_t row_base, int64_t Nv,
                            float* dY, float* rowloss, float* pred, hipStream_t s) {
-  const dim3 grid((Bp + 3) / 4, K);
+  if (Bp % 32 != 0 || d_out < 1 || d_out > kMaxOut) return hipErrorInvalidValue;
+  const dim3 grid(Bp / 32, K);
   if (prec == Prec::BF16) {
     if (eval)
-      hipLaunchKernelGGL((head_fwd_kernel<__bf16, true>), grid, dim3(256), 0, s, task,
-                         static_cast<const __bf16*>(H), theta, mem, Bp, d_out, y, idx, B, rows_valid,
-                         row_base, Nv, dY, rowloss, pred);
+      head_fwd_d<__bf16, true>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
+                               rowloss, pred);
     else
-      hipLaunchKernelGGL((head_fwd_kernel<__bf16, false>), grid, dim3(256), 0, s, task,
-                         static_cast<const __bf16*>(H), theta, mem, Bp, d_out, y, idx, B, rows_valid,
-                         row_base, Nv, dY, rowloss, pred);
+      head_fwd_d<__bf16, false>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
+                                rowloss, pred);
   } else {
     if (eval)
-      hipLaunchKernelGGL((head_fwd_kernel<float, true>), grid, dim3(256), 0, s, task,
-                         static_cast<const float*>(H), theta, mem, Bp, d_out, y, idx, B, rows_valid,
-                         row_base, Nv, dY, rowloss, pred);
+      head_fwd_d<float, true>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
+                              rowloss, pred);
     else
-      hipLaunchKernelGGL((head_fwd_kernel<float, false>), grid, dim3(256), 0, s, task,
-                         static_cast<const float*>(H), theta, mem, Bp, d_out, y, idx, B, rows_valid,
-                         row_base, Nv, dY, rowloss, pred);
+      head_fwd_d<float, false>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
+                               rowloss, pred);
   }
   return hipGetLastError();
 }
+
+namespace {
+template <typename T>
+void head_bwd_d(int d_out, int ntiles, hipStream_t s, const void* H, const float* theta, const MemberDev* mem,
+                const HeadTile* tiles, int Bp, int RB, const float* dY, void* dZ, float* part) {
+#define TABPACK_HEAD_BWD(DD, CC)                                                                             \
+  hipLaunchKernelGGL((head_bwd_kernel<T, DD, CC>), dim3(ntiles), dim3(256), 0, s, static_cast<const T*>(H), \
+                     theta, mem, tiles, Bp, d_out, RB, dY, static_cast<T*>(dZ), part)
+  if (d_out <= 1) TABPACK_HEAD_BWD(1, 8);
+  else if (d_out <= 2) TABPACK_HEAD_BWD(2, 8);
+  else if (d_out <= 4) TABPACK_HEAD_BWD(4, 8);
+  else if (d_out <= 8) TABPACK_HEAD_BWD(8, 4);
+  else TABPACK_HEAD_BWD(16, 4);
+#undef TABPACK_HEAD_BWD
+}
+}  // namespace
+
+int head_bwd_cols(int d_out) { return d_out <= 4 ? 256 : 128; }
 
 hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const MemberDev* mem, int K,
                               int Bp, int B, int d_out, float* grad, float* loss_out, hipStream_t s) {
@@ -492,16 +690,21 @@ hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const Membe
 }
 
 hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const MemberDev* mem,
-                           const ColTile* tiles, int ntiles, int Bp, int d_out, const float* dY,
-                           void* dZ, float* grad, hipStream_t s) {
+                           const HeadTile* tiles, int ntiles, int Bp, int RB, int d_out, const float* dY,
+                           void* dZ, float* part, hipStream_t s) {
+  if (RB <= 0 || Bp % RB != 0 || d_out < 1 || d_out > kMaxOut) return hipErrorInvalidValue;
+  if (ntiles <= 0) return hipSuccess;
   if (prec == Prec::BF16)
-    hipLaunchKernelGGL((head_bwd_kernel<__bf16>), dim3(ntiles), dim3(256), 0, s,
-                       static_cast<const __bf16*>(H), theta, mem, tiles, Bp, d_out, dY,
-                       static_cast<__bf16*>(dZ), grad);
+    head_bwd_d<__bf16>(d_out, ntiles, s, H, theta, mem, tiles, Bp, RB, dY, dZ, part);
   else
-    hipLaunchKernelGGL((head_bwd_kernel<float>), dim3(ntiles), dim3(256), 0, s,
-                       static_cast<const float*>(H), theta, mem, tiles, Bp, d_out, dY,
-                       static_cast<float*>(dZ), grad);
+    head_bwd_d<float>(d_out, ntiles, s, H, theta, mem, tiles, Bp, RB, dY, dZ, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int K, int max_dp, int Bp, int RB,
+                                   int d_out, float* grad, hipStream_t s) {
+  hipLaunchKernelGGL(head_grad_reduce_kernel, dim3((max_dp + 255) / 256, K), dim3(256), 0, s, part, mem, Bp, Bp / RB,
+                     d_out, grad);
   return hipGetLastError();
 }
 
@@ -526,16 +729,16 @@ hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int
 }
 
 hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, float* v,
-                        uint16_t* shadow, const uint32_t* chunk_tab, const MemberDev* mem,
-                        int64_t nchunks, float bc1, float bc2_sqrt, float beta1, float beta2,
-                        float eps, hipStream_t s) {
+                        uint16_t* shadow, const uint32_t* chunk_tab, const uint32_t* list,
+                        const MemberDev* mem, int64_t nchunks, const AdamConst& ac, hipStream_t s) {
+  if (nchunks <= 0) return hipSuccess;
   const int grid = grid_for(nchunks, 4);
   if (prec == Prec::BF16)
     hipLaunchKernelGGL((adamw_kernel<true>), dim3(grid), dim3(256), 0, s, theta, grad, m, v, shadow,
-                       chunk_tab, mem, nchunks, bc1, bc2_sqrt, beta1, beta2, eps);
+                       chunk_tab, list, mem, nchunks, ac);
   else
     hipLaunchKernelGGL((adamw_kernel<false>), dim3(grid), dim3(256), 0, s, theta, grad, m, v, shadow,
-                       chunk_tab, mem, nchunks, bc1, bc2_sqrt, beta1, beta2, eps);
+                       chunk_tab, list, mem, nchunks, ac);
   return hipGetLastError();
 }
 
@@ -552,8 +755,16 @@ hipError_t launch_eval_score(Task task, const float* pred, const void* yv, int K
 
 hipError_t launch_dropout_mask(uint32_t key0, uint32_t key1, uint32_t step, int layer, int member,
                                uint32_t t, int B, int width, uint8_t* out, hipStream_t s) {
-  hipLaunchKernelGGL(dropout_mask_kernel, dim3(grid_for((int64_t)B * width, 256)), dim3(256), 0, s,
+  hipLaunchKernelGGL(dropout_mask_kernel, dim3(grid_for((int64_t)((B + 31) / 32) * width, 256)), dim3(256), 0, s,
                      key0, key1, step, layer, member, t, B, width, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_dropout_words(uint32_t key0, uint32_t key1, uint32_t step, const MemberDev* mem, int K, int L,
+                                int max_dp, int Bp, int rows_valid, int64_t A32, uint32_t* out, hipStream_t s) {
+  const int64_t nw = (int64_t)(Bp / 32) * max_dp;
+  hipLaunchKernelGGL(dropout_words_kernel, dim3((unsigned)((nw + 255) / 256), K, L), dim3(256), 0, s, key0, key1, step,
+                     mem, Bp, rows_valid, A32, out);
   return hipGetLastError();
 }
 

@@ -49,7 +49,7 @@
 // Every output element is owned by exactly one workgroup and reduced over the
 // full depth in a fixed order: no atomics, bit-reproducible.
 #include "pack_internal.h"
-#include "philox.h"
+#include "adamw.h"
 
 namespace tabpack {
 namespace {
@@ -64,18 +64,22 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int NT = 256;                 // threads per workgroup (2 x 2 waves)
 constexpr int KV = 8;                   // 16-byte vectors of depth per row per K step
 constexpr int ROW = KV * 16;            // 128 bytes of depth per row per K step
-constexpr int kTileBytes = 256 * ROW;   // one operand tile of the big shape: 32 KB
-constexpr int kStageBytes = 2 * kTileBytes;
+constexpr int kStageBytes = 2 * 256 * ROW;       // both operand tiles of one K step, big shape (64 KB)
+constexpr int kStageBytesSmall = 2 * 128 * ROW;  // the same for the small shape (32 KB)
 
 template <int SH>
 struct Shape;
 template <>
 struct Shape<kShapeBig> {
   static constexpr int MB = 4, NB = 4, TM = 256, TN = 256;
+  static constexpr int TILE = TM * ROW;               // bytes of one operand tile per K step
+  static constexpr int STAGE = 32 * (NB * 128 + 32);  // epilogue staging bytes per wave
 };
 template <>
 struct Shape<kShapeSmall> {
   static constexpr int MB = 2, NB = 2, TM = 128, TN = 128;
+  static constexpr int TILE = TM * ROW;
+  static constexpr int STAGE = 32 * (NB * 128 + 32);
 };
 
 template <typename T>
@@ -437,15 +441,15 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
 
 // --------------------------------------------------------------- epilogue --
 // Accumulator register r of a 32x32 block held by lane l is element
-// (row 8*(r/4) + 4*(l/32) + r%4, col l%32): each lane owns 4 runs of 4
-// consecutive rows of one column, so one Philox block (4 words) serves a run.
+// (row 8*(r/4) + 4*(l/32) + r%4, col l%32): each lane owns 16 of the 32 rows
+// of one column, i.e. half of the bits of one (32-row block, column) keep or
+// mask word.
 //
 // Results leave through LDS: each wave stages one 32-row block of its
 // 32 x (32*NB) output at a time in a private region (row stride padded so the
 // two half-waves' column writes fall on disjoint banks), then reads it back as
 // 16-byte row vectors and stores whole row segments; a store instruction then
 // covers full 256- or 512-byte row pieces instead of 64-byte column strips.
-constexpr int kStageWave = 17408;  // bytes of LDS per wave for the staged block
 
 template <typename OT, int NB>
 struct Stage {
@@ -453,7 +457,7 @@ struct Stage {
   static constexpr int RS = NB * 32 * ES + (ES == 2 ? 16 : 32);  // padded row stride (bytes)
   static constexpr int VPR = NB * 32 * ES / 16;                  // 16-byte vectors per row
   static constexpr int PER_LANE = 32 * VPR / 64;
-  static_assert(32 * RS <= kStageWave, "stage region");
+  static_assert(32 * RS <= 32 * (NB * 128 + 32), "stage region");
 };
 
 // Makes the staged block written by every lane of the wave visible to the
@@ -489,10 +493,63 @@ __device__ __forceinline__ void stage_flush(const char* stage, OT* C, int64_t ld
   }
 }
 
+// Weight-gradient block with the optimizer fused: each staged vector holds the
+// gradients of 4 consecutive weights, which are updated in place (theta, both
+// moments, the bf16 shadow); the gradient itself is stored only on request.
+template <int NB>
+__device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmDesc& d, const char* stage, int row0,
+                                                  int col0, int lane) {
+  using S = Stage<float, NB>;
+  // vectors whose optimizer state is in flight at once (fewer beside the big
+  // tile's 256 accumulators)
+  constexpr int G = NB == 2 ? 8 : 4;
+  const AdamConst ac{a.beta1, a.beta2, a.eps, a.bc1, a.bc2_sqrt};
+  const float decay = 1.0f - d.lr * d.wd;
+  const float step = d.lr / a.bc1;
+#pragma unroll 1
+  for (int it0 = 0; it0 < S::PER_LANE; it0 += G) {
+    f32x4 g[G], th[G], m[G], vv[G];
+    int64_t e[G];
+    bool ok[G];
+    // all loads of the group first, so their latencies overlap
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const int v = (it0 + u) * 64 + lane;
+      const int r = v / S::VPR, c = v % S::VPR;
+      const int row = row0 + r, col = col0 + c * 4;
+      ok[u] = row < d.M && col < d.N;
+      g[u] = *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16);
+      e[u] = (int64_t)row * d.ldc + col;
+      if (ok[u]) {
+        th[u] = *reinterpret_cast<const f32x4*>(a.theta + d.poff + e[u]);
+        m[u] = *reinterpret_cast<const f32x4*>(a.am + d.poff + e[u]);
+        vv[u] = *reinterpret_cast<const f32x4*>(a.av + d.poff + e[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      if (!ok[u]) continue;
+      if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e[u]) = g[u];
+      adamw_vec4(th[u], g[u], m[u], vv[u], decay, step, ac);
+      *reinterpret_cast<f32x4*>(a.theta + d.poff + e[u]) = th[u];
+      *reinterpret_cast<f32x4*>(a.am + d.poff + e[u]) = m[u];
+      *reinterpret_cast<f32x4*>(a.av + d.poff + e[u]) = vv[u];
+      if (a.shadow) {
+        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][0]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][1]) << 16);
+        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][2]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][3]) << 16);
+        *reinterpret_cast<u32x2*>(a.shadow + d.poff + e[u]) = u32x2{lo, hi};
+      }
+    }
+  }
+}
+
 template <typename T, int EPI, int SH>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, const Tile& t,
                                          f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn, int lane,
-                                         int mv, int nv, char* stage) {
+                                         int mv, int nv, char* stage,
+                                         const uint32_t (&kw)[Shape<SH>::MB][Shape<SH>::NB]) {
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB;
   const int hv = lane >> 5;
   const int col0 = t.n0 + wn * NB * 32;  // the wave's first column
@@ -513,7 +570,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
 #pragma unroll
           for (int q = 0; q < 4; ++q) stage_put<float, NB>(stage, j, g, q, lane, acc[i][j][4 * g + q]);
       wave_sync_lds();
-      stage_flush<float, NB>(stage, C, d.ldc, row0 + 32 * i, col0, d.M, d.N, lane);
+      if (a.theta)
+        stage_flush_adamw<NB>(a, d, stage, row0 + 32 * i, col0, lane);
+      else
+        stage_flush<float, NB>(stage, C, d.ldc, row0 + 32 * i, col0, d.M, d.N, lane);
       wave_sync_lds();
     }
   } else if constexpr (EPI == EPI_DX) {
@@ -562,34 +622,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
     T* C = static_cast<T*>(d.C);
     float bias[NB];
     bool colok[NB];
-    uint64_t keep[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       bias[j] = colin[j] ? d.bias[colL + 32 * j] : 0.0f;
       colok[j] = colL + 32 * j < d.width;
-      keep[j] = ~0ull;
-    }
-    if ((EPI == EPI_FWD) && d.drop_t != 0u) {
-      // Keep bits of this lane's 4*MB runs of 4 rows: run r = 4*i + g covers
-      // rows row0 + 32*i + 8*g + 4*hv + (0..3), i.e. Philox block
-      // row0/4 + 2*r + hv, words 0..3.  The loop over runs stays rolled and
-      // never touches the accumulators.
-      const uint32_t c0 = (uint32_t)(row0 >> 2) + (uint32_t)hv;
-      const uint32_t c2 = ((uint32_t)d.member << 8) | (uint32_t)a.layer;
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        if (!colin[j]) continue;
-        uint64_t k = 0;
-#pragma unroll 1
-        for (int r = 0; r < 4 * MB; ++r) {
-          const Words4 w = philox4x32_10(c0 + 2u * (uint32_t)r, (uint32_t)(colL + 32 * j), c2, a.step, a.key0,
-                                         a.key1);
-          const uint64_t bits = (uint64_t)(w.w0 >= d.drop_t) | ((uint64_t)(w.w1 >= d.drop_t) << 1) |
-                                ((uint64_t)(w.w2 >= d.drop_t) << 2) | ((uint64_t)(w.w3 >= d.drop_t) << 3);
-          k |= bits << (4 * r);
-        }
-        keep[j] = k;
-      }
     }
     const float s_keep = (EPI == EPI_FWD) ? d.drop_s : 1.0f;
 #pragma unroll
@@ -606,7 +642,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
           for (int q = 0; q < 4; ++q) {
             const int row = rb + 8 * g + 4 * hv + q;
             float h = fmaxf(acc[i][j][4 * g + q] + bias[j], 0.0f);
-            h = ((keep[j] >> (16 * i + 4 * g + q)) & 1) ? h * s_keep : 0.0f;
+            if constexpr (EPI == EPI_FWD) h = ((kw[i][j] >> (8 * g + 4 * hv + q)) & 1) ? h * s_keep : 0.0f;
             if (!colok[j] || row >= a.rows_valid) h = 0.0f;
             const T hs = from_float<T>(h);
             if (to_float(hs) > 0.0f) mw[j] |= 1u << (8 * g + 4 * hv + q);
@@ -657,13 +693,28 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  // dropout keep words of this wave's output blocks, fetched before the
+  // main loop so their latency hides behind it (bit r of word (i, j) = row
+  // 32*i + r of the block, column lane%32 of block j)
+  uint32_t kw[MB][NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      kw[i][j] = ~0u;
+      if constexpr (EPI == EPI_FWD) {
+        const int rb = (t.m0 + wm * MB * 32) / 32 + i, col = t.n0 + wn * NB * 32 + (lane & 31) + 32 * j;
+        if (d.drop_t != 0u && rb * 32 < d.M && col < d.N) kw[i][j] = d.keepw[(int64_t)rb * d.N + col];
+      }
+    }
+
   const int nk = (d.Kd + BKE - 1) / BKE;
   if constexpr (LA::dma) {
     static_assert(LB::dma, "both operands staged the same way");
     la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane, a.zeros);
     lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane, a.zeros);
     la.issue(lds0, 0, d.Kd);
-    lb.issue(lds0 + kTileBytes, 0, d.Kd);
+    lb.issue(lds0 + Shape<SH>::TILE, 0, d.Kd);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
@@ -671,9 +722,9 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
       char* nxt = (kt & 1) ? lds0 : lds1;
       if (kt + 1 < nk) {  // the next step streams into the other buffer during the MFMAs
         la.issue(nxt, (kt + 1) * BKE, d.Kd);
-        lb.issue(nxt + kTileBytes, (kt + 1) * BKE, d.Kd);
+        lb.issue(nxt + Shape<SH>::TILE, (kt + 1) * BKE, d.Kd);
       }
-      if (compute) mma_step<T, SH, LA::tr, LB::tr>(cur, cur + kTileBytes, acc, wm, wn, lane);
+      if (compute) mma_step<T, SH, LA::tr, LB::tr>(cur, cur + Shape<SH>::TILE, acc, wm, wn, lane);
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
     }
@@ -683,7 +734,7 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
     la.load(0, d.Kd, tid);
     lb.load(0, d.Kd, tid);
     la.store(lds0, tid);
-    lb.store(lds0 + kTileBytes, tid);
+    lb.store(lds0 + Shape<SH>::TILE, tid);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
       char* cur = (kt & 1) ? lds1 : lds0;
@@ -693,18 +744,20 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
         la.load((kt + 1) * BKE, d.Kd, tid);
         lb.load((kt + 1) * BKE, d.Kd, tid);
       }
-      if (compute) mma_step<T, SH, LA::tr, LB::tr>(cur, cur + kTileBytes, acc, wm, wn, lane);
+      if (compute) mma_step<T, SH, LA::tr, LB::tr>(cur, cur + Shape<SH>::TILE, acc, wm, wn, lane);
       if (more) {
         la.store(nxt, tid);
-        lb.store(nxt + kTileBytes, tid);
+        lb.store(nxt + Shape<SH>::TILE, tid);
       }
       __syncthreads();
     }
   }
-  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * kStageWave);
+  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * Shape<SH>::STAGE, kw);
 }
 
 // ----------------------------------------------------------------- kernel --
+// Launches whose tiles include the big shape: 128 KB of LDS, one workgroup
+// (one wave per SIMD) per CU.
 template <typename T, int AK, int BK_, int EPI>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[2][kStageBytes];
@@ -712,19 +765,36 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
   const GemmDesc d = a.descs[t.desc];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  if constexpr (sizeof(T) == 2) {
-    if (t.shape == kShapeBig) {
-      run_tile<T, AK, BK_, EPI, kShapeBig>(a, d, t, smem[0], smem[1], tid, wave);
-      return;
-    }
+  if (t.shape == kShapeBig) {
+    run_tile<T, AK, BK_, EPI, kShapeBig>(a, d, t, smem[0], smem[1], tid, wave);
+    return;
   }
-  run_tile<T, AK, BK_, EPI, kShapeSmall>(a, d, t, smem[0], smem[1], tid, wave);  // fp32: small tiles only
+  run_tile<T, AK, BK_, EPI, kShapeSmall>(a, d, t, smem[0], smem[1], tid, wave);
+}
+
+// Launches of small tiles only: 64 KB of LDS, two workgroups per CU, so one
+// workgroup's epilogue overlaps the other's MFMA loop.
+template <typename T, int AK, int BK_, int EPI>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_kernel_small(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[2][kStageBytesSmall];
+  const Tile t = a.tiles[blockIdx.x];
+  const GemmDesc d = a.descs[t.desc];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  run_tile<T, AK, BK_, EPI, kShapeSmall>(a, d, t, smem[0], smem[1], tid, wave);
 }
 
 template <typename T, int AK, int BK_, int EPI>
 hipError_t launch_t(const GemmArgs& args, hipStream_t s) {
   if (args.ntiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+  if constexpr (sizeof(T) == 4) {  // fp32 operands: small tiles only
+    hipLaunchKernelGGL((gemm_kernel_small<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+  } else {
+    if (args.small_only)
+      hipLaunchKernelGGL((gemm_kernel_small<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+    else
+      hipLaunchKernelGGL((gemm_kernel<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+  }
   return hipGetLastError();
 }
 

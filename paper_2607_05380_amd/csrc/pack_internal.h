@@ -39,6 +39,7 @@ struct GemmDesc {
   const float* bias;   // EPI_FWD*: [N] fp32
   uint32_t* mask;      // EPI_FWD: written, EPI_DX: read -- ReLU/dropout keep bits of the activation,
                        // word (row/32, col) at mask[(row/32) * N + col], bit row % 32
+  const uint32_t* keepw;  // EPI_FWD: dropout keep words of this layer, same layout as mask
   float* colpart;      // EPI_DX: [M / kPartRows, N] column sums of the unrounded output per row block
   int64_t lda, ldb, ldc;
   int32_t M, N, Kd;    // A rows in bounds (< M), B rows in bounds (< N), depth (< Kd)
@@ -46,7 +47,9 @@ struct GemmDesc {
   int32_t member;
   uint32_t drop_t;     // t_k
   float drop_s;        // s_k
+  float lr, wd;        // EPI_DW with fused AdamW: the member's learning rate and weight decay
   int32_t pad_;
+  int64_t poff;        // EPI_DW with fused AdamW: element offset of the weight tensor
 };
 
 struct Tile {
@@ -65,6 +68,23 @@ struct GemmArgs {
   uint32_t key0, key1;  // dropout stream key
   uint32_t step;        // dropout counter word
   const void* zeros;    // >= 16 bytes of zeros in device memory (source for out-of-range elements)
+  int32_t small_only;   // every tile has the small shape (selects the two-workgroups-per-CU kernel)
+  // EPI_DW only: when theta is set the epilogue applies AdamW to the weight
+  // elements it produces (theta, m, v and the bf16 shadow at desc.poff + the
+  // element's index) and stores the gradient itself only if keep_grad is set.
+  float* theta;
+  float* am;
+  float* av;
+  uint16_t* shadow;
+  float beta1, beta2, eps, bc1, bc2_sqrt;
+  int32_t keep_grad;
+};
+
+// AdamW constants of one step.
+struct AdamConst {
+  float beta1, beta2, eps;
+  float bc1;       // 1 - beta1^t
+  float bc2_sqrt;  // sqrt(1 - beta2^t)
 };
 
 // Per-member table used by the small kernels.
@@ -75,6 +95,10 @@ struct MemberDev {
   float lr, wd;
   int64_t act_off;          // member offset inside one activation buffer (elements)
   int64_t w_out_off, b_out_off, b_last_off;  // head weight, head bias, last hidden bias (elements of theta)
+};
+
+struct HeadTile {            // (member, first column, first row) block of the head backward
+  int32_t member, c0, r0;
 };
 
 struct ColTile {            // (member, first column) work item of the column-sweep kernels
@@ -93,22 +117,26 @@ hipError_t launch_head_fwd(Prec prec, Task task, bool eval, const void* H, const
 hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const MemberDev* mem, int K,
                               int Bp, int B, int d_out, float* grad, float* loss_out, hipStream_t s);
 hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const MemberDev* mem,
-                           const ColTile* tiles, int ntiles, int Bp, int d_out, const float* dY,
-                           void* dZ, float* grad, hipStream_t s);
+                           const HeadTile* tiles, int ntiles, int Bp, int RB, int d_out, const float* dY,
+                           void* dZ, float* part, hipStream_t s);
+hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int K, int max_dp, int Bp, int RB,
+                                   int d_out, float* grad, hipStream_t s);
+int head_bwd_cols(int d_out);  // columns one head-backward block covers
 hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, const ColTile* tiles,
                                      int ntiles, int nparts, const int64_t* bias_off, float* grad,
                                      hipStream_t s);
 hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
                          int64_t row_base, int rows_valid, int members, int Bp, void* H0, hipStream_t s);
 hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, float* v,
-                        uint16_t* shadow, const uint32_t* chunk_tab, const MemberDev* mem,
-                        int64_t nchunks, float bc1, float bc2_sqrt, float beta1, float beta2,
-                        float eps, hipStream_t s);
+                        uint16_t* shadow, const uint32_t* chunk_tab, const uint32_t* list,
+                        const MemberDev* mem, int64_t nchunks, const AdamConst& ac, hipStream_t s);
 hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hipStream_t s);
 hipError_t launch_eval_score(Task task, const float* pred, const void* yv, int K, int64_t Nv,
                              double* score_out, hipStream_t s);
 hipError_t launch_dropout_mask(uint32_t key0, uint32_t key1, uint32_t step, int layer, int member,
                                uint32_t t, int B, int width, uint8_t* out, hipStream_t s);
+hipError_t launch_dropout_words(uint32_t key0, uint32_t key1, uint32_t step, const MemberDev* mem, int K, int L,
+                                int max_dp, int Bp, int rows_valid, int64_t A32, uint32_t* out, hipStream_t s);
 hipError_t launch_select_iter(Task task, const float* cand, const void* yv, int C, int64_t Nv,
                               int m_ens, double* sum, double* partial, int nblk, int32_t* state,
                               double* best, int32_t* sel_out, hipStream_t s);

@@ -37,7 +37,7 @@ class PackConfig(ctypes.Structure):
                 ("L", ctypes.c_int32), ("B", ctypes.c_int32), ("task", ctypes.c_int32),
                 ("precision", ctypes.c_int32), ("width_lo", ctypes.c_int32),
                 ("width_hi", ctypes.c_int32), ("quantum", ctypes.c_int32),
-                ("decay_bias", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("decay_bias", ctypes.c_int32), ("keep_grads", ctypes.c_int32),
                 ("dropout_lo", ctypes.c_double), ("dropout_hi", ctypes.c_double),
                 ("lr_lo", ctypes.c_double), ("lr_hi", ctypes.c_double),
                 ("wd_lo", ctypes.c_double), ("wd_hi", ctypes.c_double),
@@ -111,6 +111,7 @@ def make_config(cfg, members=None):
     c.precision = PRECISIONS[cfg.get("precision", "bf16")]
     c.quantum = int(cfg.get("quantum", 0))
     c.decay_bias = int(cfg.get("decay_bias", 1))
+    c.keep_grads = int(cfg.get("keep_grads", 1))
     for f in ("dropout_lo", "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi"):
         setattr(c, f, float(cfg.get(f, 0.0)))
     c.beta1 = float(cfg.get("beta1", 0.9))

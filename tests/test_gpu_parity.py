@@ -153,6 +153,32 @@ def test_determinism_and_member_independence():
     assert c[0][2] != a[0][2]
 
 
+def test_fused_update_without_stored_grads_is_identical():
+    # keep_grads=0 skips storing the hidden weight gradients (the fused AdamW of
+    # the weight-gradient GEMM consumes them); parameters and moments must be
+    # bit-identical to the run that stores them, and get_grads must refuse
+    cfg = configs.workload("regression_large", K=3, B=300)
+    Xtr, ytr, _, _, orders, idx = make_inputs(cfg, 3000, 10)
+    X, y, idx_d = to_dev(Xtr, ytr, idx)
+    runs = []
+    for keep in (1, 0):
+        pk = tabpack.Pack(dict(cfg, keep_grads=keep)).bind()
+        for s in (1, 2):
+            pk.train_step(X, y, idx_d, s)
+        runs.append([(pk.get_params(k), pk.get_moments(k)) for k in range(cfg["K"])])
+        if not keep:
+            with pytest.raises(tabpack.PackError, match="keep_grads"):
+                pk.get_grads(0)
+    for (p1, m1), (p2, m2) in zip(*runs):
+        for (W1, b1), (W2, b2) in zip(p1, p2):
+            np.testing.assert_array_equal(W1, W2)
+            np.testing.assert_array_equal(b1, b2)
+        for x1, x2 in zip(m1, m2):
+            for (W1, b1), (W2, b2) in zip(x1, x2):
+                np.testing.assert_array_equal(W1, W2)
+                np.testing.assert_array_equal(b1, b2)
+
+
 def test_k1_pack_equals_standalone_member():
     # one-member pack vs the oracle's standalone MLP with the same hyperparameters
     cfg = configs.workload("binary_small", K=1)
