@@ -18,6 +18,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "member-samples/sec (fwd+bwd+AdamW) at K=64; % bf16 MFMA peak; % HBM BW"
 PEAK = {"mfma_bf16": 2516.6, "mfma_fp32": 157.3, "hbm": 8000.0}  # TFLOP/s, TFLOP/s, GB/s
+COPY_BYTES = 256 << 20  # the calibration copy of --copy-calibration
 
 
 def log(msg):
@@ -52,6 +53,22 @@ def cpu_baseline(cfg, X, y, idx0, budget_s=15.0):
                       f"{dt:.1f} s"}
 
 
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed profiler counters
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's reading), or None when
+    no record exists or the library sources changed since it was taken."""
+    from paper_2607_05380_amd.profiles_summary import source_digest
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != source_digest():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else round(k["fetch_bytes"] + k["write_bytes"], 1)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -60,6 +77,9 @@ def main():
     ap.add_argument("--workload", default="regression_large")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=10)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="before the timed steps, copy a 256 MiB buffer 3 times (the reference dispatches that "
+                         "scale hardware byte counters in a profiler run)")
     ap.add_argument("--keep-grads", action="store_true",
                     help="also write every gradient out (an inspection aid; the optimizer does not need it)")
     a = ap.parse_args()
@@ -92,6 +112,14 @@ def main():
         pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
     torch.cuda.synchronize()
     log(f"warmup done, losses[:4] = {loss[:4].tolist()}")
+    if a.copy_calibration:
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -110,28 +138,32 @@ def main():
     log(f"timed {a.steps} steps: {ms_per_step:.3f} ms/step (wall {wall:.3f} s), {msamples / 1e6:.2f} M member-samples/s")
 
     # per-kernel durations: HIP events recorded by the library around each launch
-    pk.profile(True)
-    for _ in range(a.profile_steps):
-        step += 1
-        pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
-    stats = pk.profile_read()
-    pk.profile(False)
+    stats = []
+    if a.profile_steps > 0:
+        pk.profile(True)
+        for _ in range(a.profile_steps):
+            step += 1
+            pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
+        stats = pk.profile_read()
+        pk.profile(False)
     for s in sorted(stats, key=lambda s: -s["total_ms"]):
-        unit = "TFLOP/s" if s["kind"] == "mfma" else "GB/s"
-        rate = s["work"] / (s["avg_ms"] / 1e3) / (1e12 if s["kind"] == "mfma" else 1e9)
         log(f"  {s['name']:34s} launches {s['launches']:4d}  avg {s['avg_ms'] * 1e3:9.1f} us  "
-            f"total/step {s['total_ms'] / a.profile_steps:7.3f} ms  {rate:9.1f} {unit}")
-    dom = max(stats, key=lambda s: s["total_ms"])
-    if dom["kind"] == "mfma":
-        peak = PEAK["mfma_bf16"] if cfg["precision"] == "bf16" else PEAK["mfma_fp32"]
-        achieved = dom["work"] / (dom["avg_ms"] / 1e3) / 1e12
-        unit = "TFLOP/s"
-    else:
-        peak, unit = PEAK["hbm"], "GB/s"
-        achieved = dom["work"] / (dom["avg_ms"] / 1e3) / 1e9
-    roofline = {"bound": dom["kind"], "kernel": dom["name"], "achieved": round(achieved, 2), "peak": peak,
-                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
-                "avg_launch_us": round(dom["avg_ms"] * 1e3, 2), "work_per_launch": dom["work"]}
+            f"total/step {s['total_ms'] / a.profile_steps:7.3f} ms  {s['flops'] / s['avg_ms'] / 1e9:8.1f} TFLOP/s "
+            f"{s['bytes'] / s['avg_ms'] / 1e6:8.1f} GB/s  [{s['kind']}]")
+    roofline = None
+    if stats:
+        dom = max(stats, key=lambda s: s["total_ms"])
+        if dom["kind"] == "mfma":
+            peak = PEAK["mfma_bf16"] if cfg["precision"] == "bf16" else PEAK["mfma_fp32"]
+            work, unit, scale = dom["flops"], "TFLOP/s", 1e12
+        else:
+            peak, work, unit, scale = PEAK["hbm"], dom["bytes"], "GB/s", 1e9
+        achieved = work / (dom["avg_ms"] / 1e3) / scale
+        roofline = {"bound": dom["kind"], "kernel": dom["name"], "achieved": round(achieved, 2), "peak": peak,
+                    "unit": unit, "frac": round(achieved / peak, 4),
+                    "traffic": measured_traffic(cfg["name"], dom["name"]),
+                    "avg_launch_us": round(dom["avg_ms"] * 1e3, 2), "work_per_launch": work,
+                    "flops_per_launch": dom["flops"], "bytes_per_launch": dom["bytes"]}
     out = {
         "metric": METRIC, "value": round(msamples, 1), "unit": "member-samples/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
@@ -141,7 +173,8 @@ def main():
                    "task": cfg["task"], "keep_grads": int(a.keep_grads)},
         "roofline": roofline,
         "kernels": [{"name": s["name"], "bound": s["kind"], "avg_us": round(s["avg_ms"] * 1e3, 2),
-                     "per_step_ms": round(s["total_ms"] / a.profile_steps, 4), "work_per_launch": s["work"]}
+                     "per_step_ms": round(s["total_ms"] / a.profile_steps, 4), "flops_per_launch": s["flops"],
+                     "bytes_per_launch": s["bytes"]}
                     for s in sorted(stats, key=lambda s: -s["total_ms"])],
     }
     if not a.no_cpu_baseline:

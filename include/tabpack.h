@@ -190,20 +190,21 @@ int pack_debug_dropout_mask(pack_handle* h, uint64_t step, int32_t layer, int32_
 int pack_debug_activation(pack_handle* h, int32_t layer, int32_t member, float* host_out);
 
 /* Per-kernel timing of pack_train_step() with HIP events recorded on the
- * caller's stream around every launch (measurement aid; it adds two event
- * records per launch).  pack_profile_enable(h, 1) clears and starts
+ * stream each kernel runs on, around every launch (measurement aid; it adds
+ * two event records per launch).  pack_profile_enable(h, 1) clears and starts
  * recording, 0 stops it.  pack_profile_read() waits for the recorded events
  * and reports, per kernel (one entry per compiled kernel variant, as a
  * profiler names them), the launches seen, their summed duration and the
- * algorithmic work of one launch: flops of the true (unpadded) member shapes
- * for the matrix-product kernels (kind 0), or the bytes an ideal kernel must
- * move for the streaming kernels (kind 1). */
+ * algorithmic work of one launch on the true (unpadded) member shapes: flops,
+ * and the bytes an ideal kernel must move to or from HBM (operands read once,
+ * outputs written once).  kind names the roofline that bounds the kernel. */
 typedef struct pack_kernel_stat {
   char name[64];
-  int32_t kind;      /* 0: work = flops (MFMA roofline), 1: work = bytes (HBM roofline) */
+  int32_t kind;      /* 0: MFMA-bound (roofline in flops), 1: HBM-bound (roofline in bytes) */
   int32_t launches;
   double total_ms;
-  double work;       /* per launch */
+  double flops;      /* per launch */
+  double bytes;      /* per launch */
 } pack_kernel_stat;
 
 int pack_profile_enable(pack_handle* h, int32_t enable);

@@ -70,6 +70,7 @@ struct Launch {
   int desc0, ndesc;
   int tile0, ntiles;
   double flops;  // algorithmic flops of the launch (true member shapes)
+  double bytes;  // algorithmic HBM bytes: operands read once, outputs written once
 };
 
 // One timed launch: events recorded on the launch stream around it.
@@ -82,7 +83,7 @@ struct ProfGroup {
   std::string name;
   int kind;
   int launches = 0;
-  double total_ms = 0.0, work = 0.0;
+  double total_ms = 0.0, flops = 0.0, bytes = 0.0;
 };
 
 }  // namespace
@@ -424,7 +425,12 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.keepw = bf.keepw + (maskp(l, k) - bf.mask);
       p.descs.push_back(d);
       add_tiles(p, f, f.desc0 + k, h->Bp, m.dp, d.Kd);
-      f.flops += 2.0 * c.B * m.width * (l == 1 ? c.d_in : m.width);
+      {
+        const double fi = l == 1 ? c.d_in : m.width, w = m.width;
+        f.flops += 2.0 * c.B * w * fi;
+        // H_{l-1} and W_l read, H_l written (2-byte elements in bf16), keep words read, mask words written
+        f.bytes += (double)h->elt() * (c.B * fi + fi * w + c.B * w) + c.B * w / 4.0;
+      }
     }
     sort_launch(p, f);
     p.fwd.push_back(f);
@@ -462,7 +468,14 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.wd = (float)m.wd;
       p.descs.push_back(d);
       add_tiles(p, w, w.desc0 + k, d.M, d.N, d.Kd);
-      w.flops += 2.0 * c.B * m.width * (l == 1 ? c.d_in : m.width);
+      {
+        const double fi = l == 1 ? c.d_in : m.width, wd = m.width;
+        w.flops += 2.0 * c.B * wd * fi;
+        // dZ_l and H_{l-1} read; per weight: the fused AdamW's theta, m, v read and written
+        // (24 B) and the bf16 shadow written (2 B), plus the fp32 gradient when it is kept
+        w.bytes += (double)h->elt() * c.B * (wd + fi) +
+                   wd * fi * (24.0 + (h->prec == Prec::BF16 ? 2.0 : 0.0) + (c.keep_grads ? 4.0 : 0.0));
+      }
     }
     sort_launch(p, w);
     p.dw.push_back(w);
@@ -489,6 +502,9 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
         p.descs.push_back(d);
         add_tiles(p, x, x.desc0 + k, h->Bp, m.dp, d.Kd);
         x.flops += 2.0 * c.B * m.width * m.width;
+        // dZ_l and W_l read, dZ_{l-1} written, mask words read, bias partials written
+        x.bytes += (double)h->elt() * (2.0 * c.B * m.width + (double)m.width * m.width) + c.B * m.width / 8.0 +
+                   4.0 * (h->Bp / kPartRows) * m.width;
       }
       sort_launch(p, x);
     }
@@ -593,7 +609,7 @@ int group_id(pack_handle* h, const std::string& name, int kind) {
 // Runs `fn` (which enqueues one kernel on `stream`) and, when profiling,
 // brackets it with events and attributes `work` to the named kernel.
 template <typename F>
-hipError_t timed(pack_handle* h, const char* name, int kind, double work, hipStream_t stream, F fn) {
+hipError_t timed(pack_handle* h, const char* name, int kind, double flops, double bytes, hipStream_t stream, F fn) {
   if (!h->prof) return fn();
   hipEvent_t a = pool_event(h), b = pool_event(h);
   if (!a || !b) return hipErrorOutOfMemory;
@@ -603,7 +619,8 @@ hipError_t timed(pack_handle* h, const char* name, int kind, double work, hipStr
   if (e != hipSuccess) return e;
   e = hipEventRecord(b, stream);
   const int g = group_id(h, name, kind);
-  h->groups[g].work += work;  // summed here, averaged per launch when read
+  h->groups[g].flops += flops;  // summed here, averaged per launch when read
+  h->groups[g].bytes += bytes;
   h->timed.push_back(TimedLaunch{g, a, b});
   return e;
 }
@@ -760,7 +777,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   auto gemm = [&](OpKind ak, OpKind bk, EpiKind e, const Launch& ln, int layer) {
     GemmArgs al = for_launch(a, ln);
     al.layer = layer;
-    return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, stream,
+    return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, ln.bytes, stream,
                  [&] { return launch_gemm(h->prec, ak, bk, e, al, stream); });
   };
   int max_dp = 0;
@@ -773,29 +790,29 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   // stream while the gather (HBM-bound) runs; the forward GEMMs wait for both
   HIP_TRY(hipEventRecord(h->ev_fork, stream));
   HIP_TRY(hipStreamWaitEvent(h->side, h->ev_fork, 0));
-  HIP_TRY(timed(h, "dropout_words", 1, nkeep, h->side, [&] {
+  HIP_TRY(timed(h, "dropout_words", 1, 0.0, nkeep, h->side, [&] {
     return launch_dropout_words(a.key0, a.key1, a.step, h->b.d_mem, c.K, c.L, max_dp, h->Bp, c.B, h->A / 32,
                                 h->b.keepw, h->side);
   }));
   HIP_TRY(hipEventRecord(h->ev_join, h->side));
-  HIP_TRY(timed(h, "gather", 1, (double)c.K * c.B * c.d_in * (4.0 + h->elt()), stream, [&] {
+  HIP_TRY(timed(h, "gather", 1, 0.0, (double)c.K * c.B * c.d_in * (4.0 + h->elt()), stream, [&] {
     return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, c.K, h->Bp, h->b.H0, stream);
   }));
   HIP_TRY(hipStreamWaitEvent(stream, h->ev_join, 0));
   for (int l = 1; l <= c.L; ++l) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[l - 1], l));
-  HIP_TRY(timed(h, "head_fwd", 1, act_bytes, stream, [&] {
+  HIP_TRY(timed(h, "head_fwd", 1, 0.0, act_bytes, stream, [&] {
     return launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, y,
                            idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, stream);
   }));
-  HIP_TRY(timed(h, "loss_reduce", 1, (double)c.K * c.B * 4 * (1 + c.d_out), stream, [&] {
+  HIP_TRY(timed(h, "loss_reduce", 1, 0.0, (double)c.K * c.B * 4 * (1 + c.d_out), stream, [&] {
     return launch_loss_reduce(h->b.rowloss, h->b.dY, h->b.d_mem, c.K, h->Bp, c.B, c.d_out, h->b.grad, loss_out,
                               stream);
   }));
-  HIP_TRY(timed(h, "head_bwd", 1, 2.0 * act_bytes, stream, [&] {
+  HIP_TRY(timed(h, "head_bwd", 1, 0.0, 2.0 * act_bytes, stream, [&] {
     return launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_headtiles, h->nheadtiles, h->Bp,
                            h->head_rb, c.d_out, h->b.dY, h->dzb(c.L), h->b.headpart, stream);
   }));
-  HIP_TRY(timed(h, "head_grad_reduce", 1, 4.0 * (h->Bp / h->head_rb) * (c.d_out + 1) * (h->A / h->Bp), stream, [&] {
+  HIP_TRY(timed(h, "head_grad_reduce", 1, 0.0, 4.0 * (h->Bp / h->head_rb) * (c.d_out + 1) * (h->A / h->Bp), stream, [&] {
     return launch_head_grad_reduce(h->b.headpart, h->b.d_mem, c.K, max_dp, h->Bp, h->head_rb, c.d_out, h->b.grad,
                                    stream);
   }));
@@ -806,7 +823,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     // dX_l reads W_l, so it runs before the weight-gradient GEMM updates W_l in place
     if (l > 1) {
       HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[l - 1], l));
-      HIP_TRY(timed(h, "bias_from_partials", 1, act_bytes * 4 / h->elt() / kPartRows, stream, [&] {
+      HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 / h->elt() / kPartRows, stream, [&] {
         return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp / kPartRows,
                                          h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, stream);
       }));
@@ -823,7 +840,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     al.bc1 = ac.bc1;
     al.bc2_sqrt = ac.bc2_sqrt;
     al.keep_grad = c.keep_grads ? 1 : 0;
-    HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW), 0, h->dw[l - 1].flops, stream,
+    // AdamW fused: the weight update traffic dominates, so the HBM roofline applies
+    HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW), 1, h->dw[l - 1].flops, h->dw[l - 1].bytes, stream,
                   [&] { return launch_gemm(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW, al, stream); }));
   }
   double naux = 0;
@@ -831,7 +849,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     const Member& m = h->mem[k];
     naux += (double)c.L * m.width + (double)c.d_out * m.width + c.d_out;
   }
-  HIP_TRY(timed(h, "adamw", 1, naux * (h->prec == Prec::BF16 ? 30.0 : 28.0), stream, [&] {
+  HIP_TRY(timed(h, "adamw", 1, 0.0, naux * (h->prec == Prec::BF16 ? 30.0 : 28.0), stream, [&] {
     return launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, h->b.shadow, h->b.d_chunks, h->b.d_aux,
                         h->b.d_mem, (int64_t)h->aux_chunks.size(), ac, stream);
   }));
@@ -1028,7 +1046,8 @@ int pack_profile_read(pack_handle* h, pack_kernel_stat* out, int32_t max, int32_
     s.kind = g[i].kind;
     s.launches = g[i].launches;
     s.total_ms = g[i].total_ms;
-    s.work = g[i].launches ? g[i].work / g[i].launches : 0.0;
+    s.flops = g[i].launches ? g[i].flops / g[i].launches : 0.0;
+    s.bytes = g[i].launches ? g[i].bytes / g[i].launches : 0.0;
   }
   return PACK_OK;
 }

@@ -48,6 +48,8 @@
 //   EPI_DW        fp32 store of the weight-gradient tile
 // Every output element is owned by exactly one workgroup and reduced over the
 // full depth in a fixed order: no atomics, bit-reproducible.
+#include <algorithm>
+
 #include "pack_internal.h"
 #include "adamw.h"
 
@@ -73,13 +75,13 @@ template <>
 struct Shape<kShapeBig> {
   static constexpr int MB = 4, NB = 4, TM = 256, TN = 256;
   static constexpr int TILE = TM * ROW;               // bytes of one operand tile per K step
-  static constexpr int STAGE = 32 * (NB * 128 + 32);  // epilogue staging bytes per wave
+  static constexpr int STAGE = 32 * (NB * 64 + 16);   // epilogue staging bytes per wave
 };
 template <>
 struct Shape<kShapeSmall> {
   static constexpr int MB = 2, NB = 2, TM = 128, TN = 128;
   static constexpr int TILE = TM * ROW;
-  static constexpr int STAGE = 32 * (NB * 128 + 32);
+  static constexpr int STAGE = 32 * (NB * 64 + 16);
 };
 
 template <typename T>
@@ -445,19 +447,25 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
 // of one column, i.e. half of the bits of one (32-row block, column) keep or
 // mask word.
 //
-// Results leave through LDS: each wave stages one 32-row block of its
-// 32 x (32*NB) output at a time in a private region (row stride padded so the
-// two half-waves' column writes fall on disjoint banks), then reads it back as
-// 16-byte row vectors and stores whole row segments; a store instruction then
+// Results leave through LDS: each wave stages ROWS rows (32 for 2-byte
+// outputs, 16 for fp32: 4 or 2 of the lane's 4 row runs) of its
+// 32 x (32*NB) block at a time in a private region (row stride padded so the
+// two half-waves' column writes fall on disjoint banks), then reads them back
+// as 16-byte row vectors and stores whole row segments; a store instruction
 // covers full 256- or 512-byte row pieces instead of 64-byte column strips.
+// The region of a wave is 32 * (NB * 64 + 16) bytes for either element size.
 
 template <typename OT, int NB>
 struct Stage {
   static constexpr int ES = sizeof(OT);
+  static constexpr int ROWS = ES == 2 ? 32 : 16;                 // rows per pass
+  static constexpr int GP = ROWS / 8;                            // row runs (g values) per pass
+  static constexpr int NPASS = 32 / ROWS;
   static constexpr int RS = NB * 32 * ES + (ES == 2 ? 16 : 32);  // padded row stride (bytes)
   static constexpr int VPR = NB * 32 * ES / 16;                  // 16-byte vectors per row
-  static constexpr int PER_LANE = 32 * VPR / 64;
-  static_assert(32 * RS <= 32 * (NB * 128 + 32), "stage region");
+  static constexpr int PER_LANE = ROWS * VPR / 64;
+  static constexpr int BYTES = 32 * (NB * 64 + 16);
+  static_assert(ROWS * RS <= BYTES, "stage region");
 };
 
 // Makes the staged block written by every lane of the wave visible to the
@@ -469,15 +477,16 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// g: the row run relative to the pass (0 .. GP-1)
 template <typename OT, int NB>
 __device__ __forceinline__ void stage_put(char* stage, int j, int g, int q, int lane, OT v) {
   using S = Stage<OT, NB>;
   *reinterpret_cast<OT*>(stage + (8 * g + 4 * (lane >> 5) + q) * S::RS + (32 * j + (lane & 31)) * S::ES) = v;
 }
 
-// Stores the staged 32-row block: rows row0.., columns col0.. of C (ld in
-// elements); rows >= M and vectors starting at or beyond N are skipped
-// (N is a multiple of the vector width).
+// Stores the staged rows: rows row0.., columns col0.. of C (ld in elements);
+// rows >= M and vectors starting at or beyond N are skipped (N is a multiple
+// of the vector width).
 template <typename OT, int NB>
 __device__ __forceinline__ void stage_flush(const char* stage, OT* C, int64_t ld, int row0, int col0, int M, int N,
                                             int lane) {
@@ -493,53 +502,85 @@ __device__ __forceinline__ void stage_flush(const char* stage, OT* C, int64_t ld
   }
 }
 
-// Weight-gradient block with the optimizer fused: each staged vector holds the
+// Weight-gradient rows with the optimizer fused: each staged vector holds the
 // gradients of 4 consecutive weights, which are updated in place (theta, both
 // moments, the bf16 shadow); the gradient itself is stored only on request.
+// The optimizer state of all the lane's vectors is loaded before any update so
+// the loads' latencies overlap.
 template <int NB>
 __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmDesc& d, const char* stage, int row0,
                                                   int col0, int lane) {
   using S = Stage<float, NB>;
-  // vectors whose optimizer state is in flight at once (fewer beside the big
-  // tile's 256 accumulators)
-  constexpr int G = NB == 2 ? 8 : 4;
+  constexpr int G = S::PER_LANE;
   const AdamConst ac{a.beta1, a.beta2, a.eps, a.bc1, a.bc2_sqrt};
   const float decay = 1.0f - d.lr * d.wd;
   const float step = d.lr / a.bc1;
-#pragma unroll 1
-  for (int it0 = 0; it0 < S::PER_LANE; it0 += G) {
-    f32x4 g[G], th[G], m[G], vv[G];
-    int64_t e[G];
-    bool ok[G];
-    // all loads of the group first, so their latencies overlap
+  f32x4 g[G], th[G], m[G], vv[G];
+  int64_t e[G];
+  bool ok[G];
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      const int v = (it0 + u) * 64 + lane;
-      const int r = v / S::VPR, c = v % S::VPR;
-      const int row = row0 + r, col = col0 + c * 4;
-      ok[u] = row < d.M && col < d.N;
-      g[u] = *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16);
-      e[u] = (int64_t)row * d.ldc + col;
-      if (ok[u]) {
-        th[u] = *reinterpret_cast<const f32x4*>(a.theta + d.poff + e[u]);
-        m[u] = *reinterpret_cast<const f32x4*>(a.am + d.poff + e[u]);
-        vv[u] = *reinterpret_cast<const f32x4*>(a.av + d.poff + e[u]);
-      }
+  for (int u = 0; u < G; ++u) {
+    const int v = u * 64 + lane;
+    const int r = v / S::VPR, c = v % S::VPR;
+    const int row = row0 + r, col = col0 + c * 4;
+    ok[u] = row < d.M && col < d.N;
+    g[u] = *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16);
+    e[u] = (int64_t)row * d.ldc + col;
+    if (ok[u]) {
+      th[u] = *reinterpret_cast<const f32x4*>(a.theta + d.poff + e[u]);
+      m[u] = *reinterpret_cast<const f32x4*>(a.am + d.poff + e[u]);
+      vv[u] = *reinterpret_cast<const f32x4*>(a.av + d.poff + e[u]);
     }
+  }
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      if (!ok[u]) continue;
-      if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e[u]) = g[u];
-      adamw_vec4(th[u], g[u], m[u], vv[u], decay, step, ac);
-      *reinterpret_cast<f32x4*>(a.theta + d.poff + e[u]) = th[u];
-      *reinterpret_cast<f32x4*>(a.am + d.poff + e[u]) = m[u];
-      *reinterpret_cast<f32x4*>(a.av + d.poff + e[u]) = vv[u];
-      if (a.shadow) {
-        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][0]) |
-                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][1]) << 16);
-        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][2]) |
-                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][3]) << 16);
-        *reinterpret_cast<u32x2*>(a.shadow + d.poff + e[u]) = u32x2{lo, hi};
+  for (int u = 0; u < G; ++u) {
+    if (!ok[u]) continue;
+    if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e[u]) = g[u];
+    adamw_vec4(th[u], g[u], m[u], vv[u], decay, step, ac);
+    *reinterpret_cast<f32x4*>(a.theta + d.poff + e[u]) = th[u];
+    *reinterpret_cast<f32x4*>(a.am + d.poff + e[u]) = m[u];
+    *reinterpret_cast<f32x4*>(a.av + d.poff + e[u]) = vv[u];
+    if (a.shadow) {
+      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][0]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][1]) << 16);
+      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][2]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][3]) << 16);
+      *reinterpret_cast<u32x2*>(a.shadow + d.poff + e[u]) = u32x2{lo, hi};
+    }
+  }
+}
+
+// Small per-lane inputs of the epilogue, loaded when a tile starts so that
+// their latency hides behind the main loop: the dropout keep words (forward),
+// the bias (forward), the keep/ReLU mask words of the previous layer (dX).
+// Word (i, j) covers rows 32*i .. 32*i+31 of the wave's block, column
+// lane%32 of block j.
+template <int SH>
+struct EpiPre {
+  uint32_t w[Shape<SH>::MB][Shape<SH>::NB];
+  float bias[Shape<SH>::NB];
+};
+
+template <int EPI, int SH>
+__device__ __forceinline__ void epi_prefetch(const GemmDesc& d, const Tile& t, int wm, int wn, int lane,
+                                             EpiPre<SH>& pre) {
+  constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB;
+  const int colL = t.n0 + wn * NB * 32 + (lane & 31);
+  const int rb0 = (t.m0 + wm * MB * 32) / 32;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const bool colin = colL + 32 * j < d.N;
+    pre.bias[j] = 0.0f;
+    if constexpr (EPI == EPI_FWD || EPI == EPI_FWD_EVAL)
+      if (colin) pre.bias[j] = d.bias[colL + 32 * j];
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      const bool in = colin && (rb0 + i) * 32 < d.M;
+      pre.w[i][j] = EPI == EPI_DX ? 0u : ~0u;
+      if constexpr (EPI == EPI_FWD) {
+        if (d.drop_t != 0u && in) pre.w[i][j] = d.keepw[(int64_t)(rb0 + i) * d.N + colL + 32 * j];
+      } else if constexpr (EPI == EPI_DX) {
+        if (in) pre.w[i][j] = d.mask[(int64_t)(rb0 + i) * d.N + colL + 32 * j];
       }
     }
   }
@@ -548,8 +589,7 @@ __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmD
 template <typename T, int EPI, int SH>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, const Tile& t,
                                          f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn, int lane,
-                                         int mv, int nv, char* stage,
-                                         const uint32_t (&kw)[Shape<SH>::MB][Shape<SH>::NB]) {
+                                         int mv, int nv, char* stage, const EpiPre<SH>& pre) {
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB;
   const int hv = lane >> 5;
   const int col0 = t.n0 + wn * NB * 32;  // the wave's first column
@@ -559,28 +599,34 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
 #pragma unroll
   for (int j = 0; j < NB; ++j) colin[j] = j < nv && colL + 32 * j < d.N;
   if constexpr (EPI == EPI_DW) {
+    using S = Stage<float, NB>;
     float* C = static_cast<float*>(d.C);
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
       if (i >= mv) continue;
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
+      for (int p = 0; p < S::NPASS; ++p) {
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+        for (int j = 0; j < NB; ++j)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) stage_put<float, NB>(stage, j, g, q, lane, acc[i][j][4 * g + q]);
-      wave_sync_lds();
-      if (a.theta)
-        stage_flush_adamw<NB>(a, d, stage, row0 + 32 * i, col0, lane);
-      else
-        stage_flush<float, NB>(stage, C, d.ldc, row0 + 32 * i, col0, d.M, d.N, lane);
-      wave_sync_lds();
+          for (int g = 0; g < S::GP; ++g)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              stage_put<float, NB>(stage, j, g, q, lane, acc[i][j][4 * (p * S::GP + g) + q]);
+        wave_sync_lds();
+        if (a.theta)
+          stage_flush_adamw<NB>(a, d, stage, row0 + 32 * i + S::ROWS * p, col0, lane);
+        else
+          stage_flush<float, NB>(stage, C, d.ldc, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
+        wave_sync_lds();
+      }
     }
   } else if constexpr (EPI == EPI_DX) {
     // dZ = dH * [H_prev > 0] * s; the keep/ReLU decisions of the forward pass
     // come as mask words (bit r of word (row/32, col) = row 32*(row/32) + r).
     // Column sums of dZ per 64-row half go to colpart (bias-gradient
     // partials, reduced by a later kernel).
+    using S = Stage<T, NB>;
     T* C = static_cast<T*>(d.C);
     float cs[NB];
 #pragma unroll
@@ -590,23 +636,25 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
 #pragma unroll
         for (int j = 0; j < NB; ++j) cs[j] = 0.0f;
       }
-      uint32_t mw[NB];
+      const uint32_t(&mw)[NB] = pre.w[i];
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
-        mw[j] = (colin[j] && rb < d.M) ? d.mask[(int64_t)(rb >> 5) * d.N + colL + 32 * j] : 0u;
+      for (int p = 0; p < S::NPASS; ++p) {
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
+        for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+          for (int g = 0; g < S::GP; ++g)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float dz = ((mw[j] >> (8 * g + 4 * hv + q)) & 1) ? acc[i][j][4 * g + q] * d.drop_s : 0.0f;
-            cs[j] += dz;
-            stage_put<T, NB>(stage, j, g, q, lane, from_float<T>(dz));
-          }
-      wave_sync_lds();
-      stage_flush<T, NB>(stage, C, d.ldc, rb, col0, d.M, d.N, lane);
-      wave_sync_lds();
+            for (int q = 0; q < 4; ++q) {
+              const int gg = p * S::GP + g;
+              const float dz =
+                  ((mw[j] >> (8 * gg + 4 * hv + q)) & 1) ? acc[i][j][4 * gg + q] * d.drop_s : 0.0f;
+              cs[j] += dz;
+              stage_put<T, NB>(stage, j, g, q, lane, from_float<T>(dz));
+            }
+        wave_sync_lds();
+        stage_flush<T, NB>(stage, C, d.ldc, rb + S::ROWS * p, col0, d.M, d.N, lane);
+        wave_sync_lds();
+      }
       if (i & 1) {
         const int hb = row0 + 32 * (i - 1);  // first row of this 64-row half
         const int64_t prow = (int64_t)(hb / kPartRows) * d.N;
@@ -619,14 +667,12 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
       }
     }
   } else {
+    using S = Stage<T, NB>;
     T* C = static_cast<T*>(d.C);
-    float bias[NB];
+    const float(&bias)[NB] = pre.bias;
     bool colok[NB];
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      bias[j] = colin[j] ? d.bias[colL + 32 * j] : 0.0f;
-      colok[j] = colL + 32 * j < d.width;
-    }
+    for (int j = 0; j < NB; ++j) colok[j] = colL + 32 * j < d.width;
     const float s_keep = (EPI == EPI_FWD) ? d.drop_s : 1.0f;
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
@@ -634,24 +680,28 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
       const int rb = row0 + 32 * i;
       uint32_t mw[NB];
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        mw[j] = 0u;
+      for (int j = 0; j < NB; ++j) mw[j] = 0u;
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+      for (int p = 0; p < S::NPASS; ++p) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int row = rb + 8 * g + 4 * hv + q;
-            float h = fmaxf(acc[i][j][4 * g + q] + bias[j], 0.0f);
-            if constexpr (EPI == EPI_FWD) h = ((kw[i][j] >> (8 * g + 4 * hv + q)) & 1) ? h * s_keep : 0.0f;
-            if (!colok[j] || row >= a.rows_valid) h = 0.0f;
-            const T hs = from_float<T>(h);
-            if (to_float(hs) > 0.0f) mw[j] |= 1u << (8 * g + 4 * hv + q);
-            stage_put<T, NB>(stage, j, g, q, lane, hs);
-          }
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int g = 0; g < S::GP; ++g)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int gg = p * S::GP + g;
+              const int bit = 8 * gg + 4 * hv + q;
+              float h = fmaxf(acc[i][j][4 * gg + q] + bias[j], 0.0f);
+              if constexpr (EPI == EPI_FWD) h = ((pre.w[i][j] >> bit) & 1) ? h * s_keep : 0.0f;
+              if (!colok[j] || rb + bit >= a.rows_valid) h = 0.0f;
+              const T hs = from_float<T>(h);
+              if (to_float(hs) > 0.0f) mw[j] |= 1u << bit;
+              stage_put<T, NB>(stage, j, g, q, lane, hs);
+            }
+        wave_sync_lds();
+        stage_flush<T, NB>(stage, C, d.ldc, rb + S::ROWS * p, col0, d.M, d.N, lane);
+        wave_sync_lds();
       }
-      wave_sync_lds();
-      stage_flush<T, NB>(stage, C, d.ldc, rb, col0, d.M, d.N, lane);
-      wave_sync_lds();
       if constexpr (EPI == EPI_FWD) {
         // mask words for the backward pass: the two half-waves hold
         // complementary bits of the same (32-row block, column) word
@@ -693,20 +743,8 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  // dropout keep words of this wave's output blocks, fetched before the
-  // main loop so their latency hides behind it (bit r of word (i, j) = row
-  // 32*i + r of the block, column lane%32 of block j)
-  uint32_t kw[MB][NB];
-#pragma unroll
-  for (int i = 0; i < MB; ++i)
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      kw[i][j] = ~0u;
-      if constexpr (EPI == EPI_FWD) {
-        const int rb = (t.m0 + wm * MB * 32) / 32 + i, col = t.n0 + wn * NB * 32 + (lane & 31) + 32 * j;
-        if (d.drop_t != 0u && rb * 32 < d.M && col < d.N) kw[i][j] = d.keepw[(int64_t)rb * d.N + col];
-      }
-    }
+  EpiPre<SH> pre;
+  epi_prefetch<EPI, SH>(d, t, wm, wn, lane, pre);
 
   const int nk = (d.Kd + BKE - 1) / BKE;
   if constexpr (LA::dma) {
@@ -752,7 +790,7 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
       __syncthreads();
     }
   }
-  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * Shape<SH>::STAGE, kw);
+  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * Shape<SH>::STAGE, pre);
 }
 
 // ----------------------------------------------------------------- kernel --

@@ -1,0 +1,168 @@
+"""Summaries of rocprofv3 output for the profiles/ folder.
+
+  python -m paper_2607_05380_amd.profiles_summary stats DIR OUT.md --command "..."
+      per-kernel launch counts and average durations from a
+      `rocprofv3 --kernel-trace --stats --output-format csv` run
+  python -m paper_2607_05380_amd.profiles_summary traffic FETCH_DIR WRITE_DIR WORKLOAD OUT_PREFIX --command "..."
+      HBM bytes per launch of every library kernel from two `--pmc FETCH_SIZE` /
+      `--pmc WRITE_SIZE` runs of `bench.py --copy-calibration`: each counter (KiB per
+      dispatch) is scaled by what it reads for the 256 MiB device-to-device copies of
+      that run; writes OUT_PREFIX.json (read by bench.py) and OUT_PREFIX.md
+
+Kernel names are mapped to the names the library's own profiler uses.
+"""
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import re
+import statistics
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+COPY_BYTES = 256 << 20
+OPS = ["kmaj", "rmaj"]
+EPIS = ["fwd", "fwd_eval", "dx", "dw"]
+SIMPLE = ["dropout_words", "head_grad_reduce", "head_fwd", "head_bwd", "loss_reduce", "bias_from_partials",
+          "gather", "adamw", "to_shadow", "eval_score", "dropout_mask"]
+
+
+def source_digest():
+    """sha256 over the library sources (kernel and host code)."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(PKG, "csrc", "*"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+PAIR = {0: ("kmaj", "kmaj"), 1: ("kmaj", "kmaj"), 2: ("kmaj", "rmaj"), 3: ("rmaj", "rmaj")}  # by epilogue
+
+
+def short_name(kernel):
+    """Library profiler name of a rocprofv3 kernel name (mangled, or demangled
+    with the template arguments partly lost), or None for other kernels."""
+    if "gemm_kernel" in kernel:
+        m = re.search(r"gemm_kernel(?:_small)?I(DF16b|f)Li(\d)ELi(\d)ELi(\d)E", kernel)
+        if m:
+            t, epi = ("bf16" if m.group(1) == "DF16b" else "f32"), int(m.group(4))
+        else:
+            m = re.search(r"gemm_kernel(?:_small)?<(.*), (\d)>", kernel)
+            if not m:
+                return None
+            t, epi = ("f32" if "float" in m.group(1) else "bf16"), int(m.group(2))
+        a, b = PAIR[epi]
+        return f"gemm_{t}_{a}_{b}_{EPIS[epi]}"
+    for s in sorted(SIMPLE, key=len, reverse=True):
+        if s + "_kernel" in kernel:
+            return s
+    if "select_" in kernel:
+        return "select"
+    return None
+
+
+def is_copy(kernel):
+    return "copyBuffer" in kernel or "CopyBuffer" in kernel
+
+
+def stats(args):
+    rows = []
+    for f in glob.glob(os.path.join(args.dir, "**", "*kernel_stats.csv"), recursive=True):
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    if not rows:
+        sys.exit(f"no kernel_stats.csv under {args.dir}")
+    agg, other = {}, [0, 0.0]
+    for r in rows:
+        name = short_name(r["Name"])
+        a = agg.setdefault(name, [0, 0.0]) if name else other
+        a[0] += int(r["Calls"])
+        a[1] += float(r["TotalDurationNs"])
+    total = sum(v[1] for v in agg.values())
+    lines = [f"# Kernel time summary ({os.path.basename(args.out)[:-3]})", "", "Command:", "", "```",
+             args.command, "```", "",
+             "Library kernels only; the share is of the library's kernel time.  Other dispatches of the run "
+             f"(synthetic data generation in torch): {other[0]} calls, {other[1] / 1e6:.3f} ms.", "",
+             "| kernel | calls | avg us | total ms | share |", "|---|---|---|---|---|"]
+    for name, (calls, ns) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        lines.append(f"| {name} | {calls} | {ns / calls / 1e3:.1f} | {ns / 1e6:.3f} | {100 * ns / total:.1f}% |")
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def per_dispatch(d, counter):
+    """{dispatch id: (kernel name, counter value)} of one --pmc run."""
+    out = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                k = r["Dispatch_Id"]
+                name, v = out.get(k, (r["Kernel_Name"], 0.0))
+                out[k] = (name, v + float(r["Counter_Value"]))
+    if not out:
+        sys.exit(f"no {counter} rows under {d}")
+    return out
+
+
+def traffic(args):
+    res = {}
+    factors = {}
+    for counter, d in (("FETCH_SIZE", args.fetch), ("WRITE_SIZE", args.write)):
+        disp = per_dispatch(d, counter)
+        copies = [v for name, v in disp.values() if is_copy(name) and v * 1024 >= 0.5 * COPY_BYTES]
+        if not copies:
+            sys.exit(f"no calibration copy found in the {counter} run")
+        factor = statistics.median(copies) * 1024 / COPY_BYTES  # counter bytes per true byte
+        factors[counter] = factor
+        per = {}
+        for name, v in disp.values():
+            s = short_name(name)
+            if s:
+                per.setdefault(s, []).append(v * 1024 / factor)
+        for s, vals in per.items():
+            res.setdefault(s, {})["fetch_bytes" if counter == "FETCH_SIZE" else "write_bytes"] = statistics.mean(vals)
+            res[s]["dispatches"] = len(vals)
+    rec = {"workload": args.workload, "source_sha256": source_digest(), "command": args.command,
+           "copy_factor": {"fetch": factors["FETCH_SIZE"], "write": factors["WRITE_SIZE"]},
+           "kernels": {k: v for k, v in res.items() if "fetch_bytes" in v and "write_bytes" in v}}
+    with open(args.out_prefix + ".json", "w") as f:
+        json.dump(rec, f, indent=1)
+    lines = [f"# HBM traffic per launch, {args.workload}", "", "Commands (FETCH_SIZE run, then WRITE_SIZE run):",
+             "", "```", args.command, "```", "",
+             f"Copy calibration: a 256 MiB device-to-device copy reads FETCH_SIZE x {factors['FETCH_SIZE']:.3f} "
+             f"and WRITE_SIZE x {factors['WRITE_SIZE']:.3f} of its true bytes; the figures below are divided "
+             "by these factors.", "",
+             "| kernel | dispatches | fetch MB | write MB | total MB |", "|---|---|---|---|---|"]
+    for k, v in sorted(rec["kernels"].items(), key=lambda kv: -(kv[1]["fetch_bytes"] + kv[1]["write_bytes"])):
+        lines.append(f"| {k} | {v['dispatches']} | {v['fetch_bytes'] / 1e6:.1f} | {v['write_bytes'] / 1e6:.1f} | "
+                     f"{(v['fetch_bytes'] + v['write_bytes']) / 1e6:.1f} |")
+    with open(args.out_prefix + ".md", "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    a = sub.add_parser("stats")
+    a.add_argument("dir")
+    a.add_argument("out")
+    a.add_argument("--command", default="")
+    b = sub.add_parser("traffic")
+    b.add_argument("fetch")
+    b.add_argument("write")
+    b.add_argument("workload")
+    b.add_argument("out_prefix")
+    b.add_argument("--command", default="")
+    args = ap.parse_args()
+    stats(args) if args.cmd == "stats" else traffic(args)
+
+
+if __name__ == "__main__":
+    main()
