@@ -66,21 +66,29 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int NT = 256;                 // threads per workgroup (2 x 2 waves)
 constexpr int KV = 8;                   // 16-byte vectors of depth per row per K step
 constexpr int ROW = KV * 16;            // 128 bytes of depth per row per K step
-constexpr int kStageBytes = 2 * 256 * ROW;       // both operand tiles of one K step, big shape (64 KB)
-constexpr int kStageBytesSmall = 2 * 128 * ROW;  // the same for the small shape (32 KB)
+constexpr int kLdsBig = 2 * 2 * 256 * ROW;    // two 64-deep stages of both 256-row operand tiles (128 KB)
+// Small-tile bf16 pipeline: kSmallNs stages of kSmallKs 16-deep MFMA steps.
+#ifndef TABPACK_SMALL_KS
+#define TABPACK_SMALL_KS 4
+#endif
+#ifndef TABPACK_SMALL_NS
+#define TABPACK_SMALL_NS 2
+#endif
+constexpr int kSmallKs = TABPACK_SMALL_KS, kSmallNs = TABPACK_SMALL_NS;
+constexpr int kLdsSmallBf16 = kSmallNs * 2 * 128 * 32 * kSmallKs;
+constexpr int kLdsSmall = kLdsSmallBf16 > 2 * 2 * 128 * ROW ? kLdsSmallBf16 : 2 * 2 * 128 * ROW;
+constexpr int kSmallWpe = kLdsSmall <= 80 * 1024 ? 2 : 1;  // workgroups (waves per SIMD) that fit per CU
 
 template <int SH>
 struct Shape;
 template <>
 struct Shape<kShapeBig> {
   static constexpr int MB = 4, NB = 4, TM = 256, TN = 256;
-  static constexpr int TILE = TM * ROW;               // bytes of one operand tile per K step
   static constexpr int STAGE = 32 * (NB * 64 + 16);   // epilogue staging bytes per wave
 };
 template <>
 struct Shape<kShapeSmall> {
   static constexpr int MB = 2, NB = 2, TM = 128, TN = 128;
-  static constexpr int TILE = TM * ROW;
   static constexpr int STAGE = 32 * (NB * 64 + 16);
 };
 
@@ -100,17 +108,19 @@ __device__ __forceinline__ int kmaj_off(int row, int slot) {
   return row * ROW + ((slot ^ (row & 7) ^ ((row >> 3) & 7)) << 4);
 }
 
-// depth-contiguous bf16 layout used with direct-to-LDS loads: 1 KB blocks of
-// 8 rows; inside a block, 4 planes (one per 16-deep MFMA step) of 8 rows x
-// 32 bytes.  The two 16-byte halves of a row's plane slice are swapped when
-// bit 2 xor bit 3 of the row is set, which keeps the 16-byte fragment reads of
-// 8 (and of 16) consecutive rows on distinct banks.  A block is exactly 8 full
-// 128-byte row segments of HBM, so one 64-lane direct load fills it with
-// whole cache lines, and every fragment address is a per-lane base plus
-// compile-time offsets.
+// depth-contiguous bf16 layout used with direct-to-LDS loads, for K steps of
+// KS 16-deep MFMA steps: 1 KB blocks of BR = 32/KS rows; inside a block, KS
+// planes (one per 16-deep step) of BR rows x 32 bytes.  The two 16-byte halves
+// of a row's plane slice are swapped when bit 2 xor bit 3 of the row is set,
+// which keeps the 16-byte fragment reads of 8 (and of 16) consecutive rows on
+// distinct banks.  A block is exactly BR full row segments of HBM (32*KS bytes
+// each), so one 64-lane direct load fills it with whole segments, and every
+// fragment address is a per-lane base plus compile-time offsets.
 __device__ __forceinline__ int kmaj_sw(int row) { return ((row >> 2) ^ (row >> 3)) & 1; }
+template <int KS>
 __device__ __forceinline__ int kmaj16_off(int row, int ks, int h) {
-  return (row >> 3) * 1024 + ks * 256 + (row & 7) * 32 + ((h ^ kmaj_sw(row)) << 4);
+  constexpr int BR = 32 / KS;
+  return (row / BR) * 1024 + ks * (BR * 32) + (row % BR) * 32 + ((h ^ kmaj_sw(row)) << 4);
 }
 
 // rows-contiguous bf16 layout (R rows): byte offset of element `col` of depth row k
@@ -244,18 +254,19 @@ __device__ __forceinline__ void dma16(const void* src, char* lds) {
 }
 
 // Depth-contiguous bf16 operand -> blocked depth-contiguous LDS layout.  Wave w
-// fills blocks w*PER .. w*PER+PER-1 (8 rows each); lane i fetches the 16 bytes
-// of plane i/16 of row (i/2)%8 that belong at LDS position 16*i, i.e. logical
-// half (i&1) ^ sw(row).  sw(row) depends on the block's parity, so a lane has
-// two source offsets, one per parity.
-template <int R>
+// fills blocks w*PER .. w*PER+PER-1 (BR rows each); lane i fetches the 16 bytes
+// of plane i/(2 BR) of row (i/2)%BR that belong at LDS position 16*i, i.e.
+// logical half (i&1) ^ sw(row).  For BR = 8, sw(row) depends on the block's
+// parity, so a lane keeps one source offset per parity.
+template <int R, int KS>
 struct DmaKmaj {
-  static constexpr int PER = R / 32;  // 1 KB blocks per wave
+  static constexpr int BR = 32 / KS;           // rows per 1 KB block
+  static constexpr int PER = R / BR / 4;       // blocks per wave
   static_assert(PER % 2 == 0, "block parity follows p");
   const char* base;
   const void* zeros;
   uint32_t off[2];     // byte offset (depth 0) of this lane's vector in block 0 / 1
-  uint32_t bstep;      // bytes between the rows of blocks 2 apart (16 rows)
+  uint32_t bstep;      // bytes between the rows of blocks 2 apart
   int kofs[2];         // depth offset (elements) of this lane's vector per block parity
   uint32_t okmask;     // bit p: this lane's row of block p exists
   int wave;
@@ -264,19 +275,19 @@ struct DmaKmaj {
     base = reinterpret_cast<const char*>(P);
     zeros = z;
     wave = wave_;
-    const int r8 = (lane >> 1) & 7, ks = lane >> 4;
+    const int r = (lane >> 1) % BR, ks = lane / (2 * BR);
 #pragma unroll
     for (int par = 0; par < 2; ++par) {
-      const int row = (wave * PER + par) * 8 + r8;  // PER is even: parity of p = parity of the block
+      const int row = (wave * PER + par) * BR + r;  // PER is even: parity of p = parity of the block
       const int h = (lane & 1) ^ kmaj_sw(row);
       kofs[par] = ks * 16 + h * 8;
       off[par] = (uint32_t)(((int64_t)(row0 + row) * ld + kofs[par]) * 2);
     }
-    bstep = (uint32_t)(16 * ld * 2);
+    bstep = (uint32_t)(2 * BR * ld * 2);
     okmask = 0;
 #pragma unroll
     for (int p = 0; p < PER; ++p)
-      if (row0 + (wave * PER + p) * 8 + r8 < rbound) okmask |= 1u << p;
+      if (row0 + (wave * PER + p) * BR + r < rbound) okmask |= 1u << p;
   }
   __device__ void issue(char* lds, int k0, int kd) const {
     const bool kin0 = k0 + kofs[0] < kd, kin1 = k0 + kofs[1] < kd;
@@ -289,11 +300,11 @@ struct DmaKmaj {
   }
 };
 
-// Rows-contiguous bf16 operand -> rows-contiguous LDS layout (64 depth rows x R).
-template <int R>
+// Rows-contiguous bf16 operand -> rows-contiguous LDS layout (16*KS depth rows x R).
+template <int R, int KS>
 struct DmaRmaj {
-  static constexpr int RBYTES = 2 * R;                 // bytes per depth row in LDS
-  static constexpr int PER = 64 * RBYTES / 1024 / 4;   // chunks per wave
+  static constexpr int RBYTES = 2 * R;                      // bytes per depth row in LDS
+  static constexpr int PER = 16 * KS * RBYTES / 1024 / 4;   // chunks per wave
   const char* base;
   const void* zeros;
   int64_t ldb;         // bytes per depth row in HBM
@@ -327,28 +338,28 @@ struct DmaRmaj {
   }
 };
 
-template <typename T, int KIND, int R>
+template <typename T, int KIND, int R, int KS>
 struct LoaderFor;
-template <int R>
-struct LoaderFor<__bf16, OP_KMAJ, R> {
-  using type = DmaKmaj<R>;
+template <int R, int KS>
+struct LoaderFor<__bf16, OP_KMAJ, R, KS> {
+  using type = DmaKmaj<R, KS>;
   static constexpr bool tr = false;  // fragments read from the depth-contiguous layout
   static constexpr bool dma = true;
 };
-template <int R>
-struct LoaderFor<__bf16, OP_RMAJ, R> {
-  using type = DmaRmaj<R>;
+template <int R, int KS>
+struct LoaderFor<__bf16, OP_RMAJ, R, KS> {
+  using type = DmaRmaj<R, KS>;
   static constexpr bool tr = true;   // fragments read with ds_read_b64_tr_b16
   static constexpr bool dma = true;
 };
-template <int R>
-struct LoaderFor<float, OP_KMAJ, R> {
+template <int R, int KS>
+struct LoaderFor<float, OP_KMAJ, R, KS> {
   using type = LoadKmaj<float, R>;
   static constexpr bool tr = false;
   static constexpr bool dma = false;
 };
-template <int R>
-struct LoaderFor<float, OP_RMAJ, R> {
+template <int R, int KS>
+struct LoaderFor<float, OP_RMAJ, R, KS> {
   using type = LoadRmajF32<R>;
   static constexpr bool tr = false;
   static constexpr bool dma = false;
@@ -369,46 +380,64 @@ __device__ __forceinline__ bf16x8 frag_tr(const char* lds, int row_block, int ks
   return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], b[0], b[1]});
 }
 
-template <int R>
+template <int KS>
 __device__ __forceinline__ bf16x8 frag_kmaj_bf16(const char* lds, int row_block, int ks, int lane) {
-  return *reinterpret_cast<const bf16x8*>(lds + kmaj16_off(row_block + (lane & 31), ks, lane >> 5));
+  return *reinterpret_cast<const bf16x8*>(lds + kmaj16_off<KS>(row_block + (lane & 31), ks, lane >> 5));
 }
 
-template <bool TR, int R>
+template <bool TR, int R, int KS>
 __device__ __forceinline__ bf16x8 frag_bf16(const char* lds, int row_block, int ks, int lane) {
   if constexpr (TR)
     return frag_tr<R>(lds, row_block, ks, lane);
   else
-    return frag_kmaj_bf16<R>(lds, row_block, ks, lane);
+    return frag_kmaj_bf16<KS>(lds, row_block, ks, lane);
 }
 
 // ------------------------------------------------------------------- MFMA --
 // One K step (128 bytes of depth) for this wave's MB x NB blocks.  Blocks
 // outside the member's extents hold zeros and are computed anyway: the loop
 // stays free of branches so LDS reads and MFMAs overlap.
-template <typename T, int SH, bool TRA, bool TRB>
+template <typename T, int SH, bool TRA, bool TRB, int KS>
 __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
                                          f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn,
                                          int lane) {
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM, TN = Shape<SH>::TN;
-  if constexpr (sizeof(T) == 2) {
-    // Fragments of the next 16-deep step are read while the MFMAs of this one
-    // run; the loop stays rolled (a full unroll hoists every step's reads and
-    // does not fit beside 256 accumulators).  The last step re-reads step 0,
-    // which is harmless.
+  if constexpr (sizeof(T) == 2 && SH == kShapeSmall) {
+    // Small tiles: every fragment of the K step is read up front (16 VGPRs per
+    // 16-deep step), so the MFMAs only wait for the LDS reads they use.
+    bf16x8 a[KS][MB], b[KS][NB];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int i = 0; i < MB; ++i) a[ks][i] = frag_bf16<TRA, TM, KS>(As, wm * MB * 32 + i * 32, ks, lane);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b[ks][j] = frag_bf16<TRB, TN, KS>(Bs, wn * NB * 32 + j * 32, ks, lane);
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][i], b[ks][j], acc[i][j], 0, 0, 0);
+  } else if constexpr (sizeof(T) == 2) {
+    // Big tiles: fragments of the next 16-deep step are read while the MFMAs
+    // of this one run; the loop stays rolled (a full unroll hoists every step's
+    // reads and does not fit beside 256 accumulators).  The last step re-reads
+    // step 0, which is harmless.
     bf16x8 a[MB], b[NB];
 #pragma unroll
-    for (int i = 0; i < MB; ++i) a[i] = frag_bf16<TRA, TM>(As, wm * MB * 32 + i * 32, 0, lane);
+    for (int i = 0; i < MB; ++i) a[i] = frag_bf16<TRA, TM, KS>(As, wm * MB * 32 + i * 32, 0, lane);
 #pragma unroll
-    for (int j = 0; j < NB; ++j) b[j] = frag_bf16<TRB, TN>(Bs, wn * NB * 32 + j * 32, 0, lane);
+    for (int j = 0; j < NB; ++j) b[j] = frag_bf16<TRB, TN, KS>(Bs, wn * NB * 32 + j * 32, 0, lane);
 #pragma unroll 1
-    for (int ks = 0; ks < KV / 2; ++ks) {
-      const int kn = (ks + 1) & (KV / 2 - 1);
+    for (int ks = 0; ks < KS; ++ks) {
+      const int kn = (ks + 1) & (KS - 1);
       bf16x8 na[MB], nb[NB];
 #pragma unroll
-      for (int i = 0; i < MB; ++i) na[i] = frag_bf16<TRA, TM>(As, wm * MB * 32 + i * 32, kn, lane);
+      for (int i = 0; i < MB; ++i) na[i] = frag_bf16<TRA, TM, KS>(As, wm * MB * 32 + i * 32, kn, lane);
 #pragma unroll
-      for (int j = 0; j < NB; ++j) nb[j] = frag_bf16<TRB, TN>(Bs, wn * NB * 32 + j * 32, kn, lane);
+      for (int j = 0; j < NB; ++j) nb[j] = frag_bf16<TRB, TN, KS>(Bs, wn * NB * 32 + j * 32, kn, lane);
 #pragma unroll
       for (int i = 0; i < MB; ++i)
 #pragma unroll
@@ -716,13 +745,46 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
 }
 
 // ------------------------------------------------------------------- tile --
-template <typename T, int AK, int BK_, int EPI, int SH>
-__device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, const Tile& t, char* lds0,
-                                         char* lds1, int tid, int wave) {
+// vmcnt <= N, every other counter at its maximum (gfx9 s_waitcnt encoding),
+// plus lgkmcnt(0) when LDS is set.
+template <int N, bool LDS>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((LDS ? 0 : 15) << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without a memory fence: the waits that make data visible
+// are explicit around it, and the empty asm statements keep the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void bar() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Waits until at most `newer` K steps (of PS direct loads per wave each) are
+// still in flight and this wave's LDS reads are done.
+template <int PS, int NS>
+__device__ __forceinline__ void wait_stage(int newer) {
+  static_assert(NS <= 4 && 2 * PS < 64, "up to 2 newer steps");
+  if (newer <= 0)
+    wait_vm<0, true>();
+  else if (newer == 1)
+    wait_vm<PS, true>();
+  else
+    wait_vm<2 * PS, true>();
+}
+
+// One output tile over the member's whole depth.  bf16 operands stream into
+// LDS with direct loads in NS stages of KS 16-deep MFMA steps: NS-1 K steps are
+// in flight while one is computed.  fp32 operands go through registers with
+// two stages.
+template <typename T, int AK, int BK_, int EPI, int SH, int KS, int NS>
+__device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, const Tile& t, char* lds0, int tid,
+                                         int wave) {
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM, TN = Shape<SH>::TN;
-  constexpr int BKE = KV * Elem<T>::VE;  // depth per K step
-  using LA = LoaderFor<T, AK, TM>;
-  using LB = LoaderFor<T, BK_, TN>;
+  using LA = LoaderFor<T, AK, TM, KS>;
+  using LB = LoaderFor<T, BK_, TN, KS>;
   const int lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   // this wave's 32-blocks inside the member's extents (wave-uniform); a wave
@@ -746,33 +808,47 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
   EpiPre<SH> pre;
   epi_prefetch<EPI, SH>(d, t, wm, wn, lane, pre);
 
-  const int nk = (d.Kd + BKE - 1) / BKE;
   if constexpr (LA::dma) {
     static_assert(LB::dma, "both operands staged the same way");
+    constexpr int BKE = 16 * KS;                      // depth (elements) per K step
+    constexpr int TA = TM * 32 * KS, TB = TN * 32 * KS;  // operand tile bytes per K step
+    constexpr int PS = LA::type::PER + LB::type::PER;  // direct loads per wave per K step
+    const int nk = (d.Kd + BKE - 1) / BKE;
     la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane, a.zeros);
     lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane, a.zeros);
-    la.issue(lds0, 0, d.Kd);
-    lb.issue(lds0 + Shape<SH>::TILE, 0, d.Kd);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      char* cur = (kt & 1) ? lds1 : lds0;
-      char* nxt = (kt & 1) ? lds0 : lds1;
-      if (kt + 1 < nk) {  // the next step streams into the other buffer during the MFMAs
-        la.issue(nxt, (kt + 1) * BKE, d.Kd);
-        lb.issue(nxt + Shape<SH>::TILE, (kt + 1) * BKE, d.Kd);
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < nk) {
+        char* b = lds0 + s * (TA + TB);
+        la.issue(b, s * BKE, d.Kd);
+        lb.issue(b + TA, s * BKE, d.Kd);
       }
-      if (compute) mma_step<T, SH, LA::tr, LB::tr>(cur, cur + Shape<SH>::TILE, acc, wm, wn, lane);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      // step kt has landed in every wave's share and every wave is done with
+      // the buffer the next load overwrites (it held step kt-1)
+      wait_stage<PS, NS>(min(NS - 2, nk - 1 - kt));
+      bar();
+      if (kt + NS - 1 < nk) {
+        char* b = lds0 + ((kt + NS - 1) % NS) * (TA + TB);
+        la.issue(b, (kt + NS - 1) * BKE, d.Kd);
+        lb.issue(b + TA, (kt + NS - 1) * BKE, d.Kd);
+      }
+      char* cur = lds0 + (kt % NS) * (TA + TB);
+      if (compute) mma_step<T, SH, LA::tr, LB::tr, KS>(cur, cur + TA, acc, wm, wn, lane);
     }
+    wait_vm<0, true>();
+    bar();  // the epilogue stages results in the operand buffers
   } else {
+    constexpr int BKE = KV * Elem<T>::VE;
+    constexpr int TA = TM * ROW, TB = TN * ROW;
+    char* lds1 = lds0 + TA + TB;
+    const int nk = (d.Kd + BKE - 1) / BKE;
     la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, tid);
     lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, tid);
     la.load(0, d.Kd, tid);
     lb.load(0, d.Kd, tid);
     la.store(lds0, tid);
-    lb.store(lds0 + Shape<SH>::TILE, tid);
+    lb.store(lds0 + TA, tid);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
       char* cur = (kt & 1) ? lds1 : lds0;
@@ -782,10 +858,10 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
         la.load((kt + 1) * BKE, d.Kd, tid);
         lb.load((kt + 1) * BKE, d.Kd, tid);
       }
-      if (compute) mma_step<T, SH, LA::tr, LB::tr>(cur, cur + Shape<SH>::TILE, acc, wm, wn, lane);
+      if (compute) mma_step<T, SH, LA::tr, LB::tr, KS>(cur, cur + TA, acc, wm, wn, lane);
       if (more) {
         la.store(nxt, tid);
-        lb.store(nxt + Shape<SH>::TILE, tid);
+        lb.store(nxt + TA, tid);
       }
       __syncthreads();
     }
@@ -794,32 +870,37 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
 }
 
 // ----------------------------------------------------------------- kernel --
-// Launches whose tiles include the big shape: 128 KB of LDS, one workgroup
-// (one wave per SIMD) per CU.
+// Launches whose tiles include the big shape: 256x256 tiles with two 64-deep
+// stages (128 KB of LDS), one workgroup (one wave per SIMD) per CU.
 template <typename T, int AK, int BK_, int EPI>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2][kStageBytes];
+  __shared__ __attribute__((aligned(16))) char smem[kLdsBig];
   const Tile t = a.tiles[blockIdx.x];
   const GemmDesc d = a.descs[t.desc];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   if (t.shape == kShapeBig) {
-    run_tile<T, AK, BK_, EPI, kShapeBig>(a, d, t, smem[0], smem[1], tid, wave);
+    run_tile<T, AK, BK_, EPI, kShapeBig, 4, 2>(a, d, t, smem, tid, wave);
     return;
   }
-  run_tile<T, AK, BK_, EPI, kShapeSmall>(a, d, t, smem[0], smem[1], tid, wave);
+  run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave);
 }
 
 // Launches of small tiles only: 64 KB of LDS, two workgroups per CU, so one
-// workgroup's epilogue overlaps the other's MFMA loop.
+// workgroup's epilogue overlaps the other's MFMA loop.  bf16: four stages of
+// 32-deep K steps (three in flight); fp32: two register-staged stages.
 template <typename T, int AK, int BK_, int EPI>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_kernel_small(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2][kStageBytesSmall];
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSmallWpe, kSmallWpe))) void gemm_kernel_small(
+    GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[kLdsSmall];
   const Tile t = a.tiles[blockIdx.x];
   const GemmDesc d = a.descs[t.desc];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  run_tile<T, AK, BK_, EPI, kShapeSmall>(a, d, t, smem[0], smem[1], tid, wave);
+  if constexpr (sizeof(T) == 2)
+    run_tile<T, AK, BK_, EPI, kShapeSmall, kSmallKs, kSmallNs>(a, d, t, smem, tid, wave);
+  else
+    run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave);
 }
 
 template <typename T, int AK, int BK_, int EPI>
