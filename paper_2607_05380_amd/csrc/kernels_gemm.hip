@@ -555,10 +555,10 @@ __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmD
     ok[u] = row < d.M && col < d.N;
     g[u] = *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16);
     e[u] = (int64_t)row * d.ldc + col;
-    if (ok[u]) {
-      th[u] = *reinterpret_cast<const f32x4*>(a.theta + d.poff + e[u]);
-      m[u] = *reinterpret_cast<const f32x4*>(a.am + d.poff + e[u]);
-      vv[u] = *reinterpret_cast<const f32x4*>(a.av + d.poff + e[u]);
+    if (ok[u]) {  // the optimizer state streams: non-temporal, so it does not evict GEMM operands
+      th[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.theta + d.poff + e[u]));
+      m[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.am + d.poff + e[u]));
+      vv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.av + d.poff + e[u]));
     }
   }
 #pragma unroll
@@ -566,10 +566,10 @@ __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmD
     if (!ok[u]) continue;
     if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e[u]) = g[u];
     adamw_vec4(th[u], g[u], m[u], vv[u], decay, step, ac);
-    *reinterpret_cast<f32x4*>(a.theta + d.poff + e[u]) = th[u];
-    *reinterpret_cast<f32x4*>(a.am + d.poff + e[u]) = m[u];
-    *reinterpret_cast<f32x4*>(a.av + d.poff + e[u]) = vv[u];
-    if (a.shadow) {
+    __builtin_nontemporal_store(th[u], reinterpret_cast<f32x4*>(a.theta + d.poff + e[u]));
+    __builtin_nontemporal_store(m[u], reinterpret_cast<f32x4*>(a.am + d.poff + e[u]));
+    __builtin_nontemporal_store(vv[u], reinterpret_cast<f32x4*>(a.av + d.poff + e[u]));
+    if (a.shadow) {  // read by the next forward and dX GEMMs: a normal store
       const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][0]) |
                           ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][1]) << 16);
       const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][2]) |
