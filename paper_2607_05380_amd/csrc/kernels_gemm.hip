@@ -84,12 +84,12 @@ struct Shape;
 template <>
 struct Shape<kShapeBig> {
   static constexpr int MB = 4, NB = 4, TM = 256, TN = 256;
-  static constexpr int STAGE = 32 * (NB * 64 + 16);   // epilogue staging bytes per wave
+  static constexpr int STAGE = 32 * (NB * 128 + 32);  // epilogue staging bytes per wave
 };
 template <>
 struct Shape<kShapeSmall> {
   static constexpr int MB = 2, NB = 2, TM = 128, TN = 128;
-  static constexpr int STAGE = 32 * (NB * 64 + 16);
+  static constexpr int STAGE = 32 * (NB * 128 + 32);
 };
 
 template <typename T>
@@ -476,24 +476,23 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
 // of one column, i.e. half of the bits of one (32-row block, column) keep or
 // mask word.
 //
-// Results leave through LDS: each wave stages ROWS rows (32 for 2-byte
-// outputs, 16 for fp32: 4 or 2 of the lane's 4 row runs) of its
-// 32 x (32*NB) block at a time in a private region (row stride padded so the
-// two half-waves' column writes fall on disjoint banks), then reads them back
-// as 16-byte row vectors and stores whole row segments; a store instruction
+// Results leave through LDS: each wave stages one 32-row block of its
+// 32 x (32*NB) output at a time in a private region of 32 * (NB*128 + 32)
+// bytes (row stride padded so the two half-waves' column writes fall on
+// disjoint banks; the operand buffers are free by then), then reads it back as
+// 16-byte row vectors and stores whole row segments: a store instruction
 // covers full 256- or 512-byte row pieces instead of 64-byte column strips.
-// The region of a wave is 32 * (NB * 64 + 16) bytes for either element size.
 
 template <typename OT, int NB>
 struct Stage {
   static constexpr int ES = sizeof(OT);
-  static constexpr int ROWS = ES == 2 ? 32 : 16;                 // rows per pass
+  static constexpr int ROWS = 32;                                // rows per pass
   static constexpr int GP = ROWS / 8;                            // row runs (g values) per pass
   static constexpr int NPASS = 32 / ROWS;
   static constexpr int RS = NB * 32 * ES + (ES == 2 ? 16 : 32);  // padded row stride (bytes)
   static constexpr int VPR = NB * 32 * ES / 16;                  // 16-byte vectors per row
   static constexpr int PER_LANE = ROWS * VPR / 64;
-  static constexpr int BYTES = 32 * (NB * 64 + 16);
+  static constexpr int BYTES = 32 * (NB * 128 + 32);
   static_assert(ROWS * RS <= BYTES, "stage region");
 };
 
@@ -540,41 +539,48 @@ template <int NB>
 __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmDesc& d, const char* stage, int row0,
                                                   int col0, int lane) {
   using S = Stage<float, NB>;
-  constexpr int G = S::PER_LANE;
+  // vectors whose optimizer state is loaded before any of them is updated:
+  // all of the lane's 8 for the small tile, 4 at a time beside the big tile's
+  // 256 accumulators
+  constexpr int G = NB == 2 ? S::PER_LANE : 4;
+  static_assert(S::PER_LANE % G == 0, "whole groups");
   const AdamConst ac{a.beta1, a.beta2, a.eps, a.bc1, a.bc2_sqrt};
   const float decay = 1.0f - d.lr * d.wd;
   const float step = d.lr / a.bc1;
-  f32x4 g[G], th[G], m[G], vv[G];
-  int64_t e[G];
-  bool ok[G];
+#pragma unroll 1
+  for (int it0 = 0; it0 < S::PER_LANE; it0 += G) {
+    f32x4 g[G], th[G], m[G], vv[G];
+    int64_t e[G];
+    bool ok[G];
 #pragma unroll
-  for (int u = 0; u < G; ++u) {
-    const int v = u * 64 + lane;
-    const int r = v / S::VPR, c = v % S::VPR;
-    const int row = row0 + r, col = col0 + c * 4;
-    ok[u] = row < d.M && col < d.N;
-    g[u] = *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16);
-    e[u] = (int64_t)row * d.ldc + col;
-    if (ok[u]) {  // the optimizer state streams: non-temporal, so it does not evict GEMM operands
-      th[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.theta + d.poff + e[u]));
-      m[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.am + d.poff + e[u]));
-      vv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.av + d.poff + e[u]));
+    for (int u = 0; u < G; ++u) {
+      const int v = (it0 + u) * 64 + lane;
+      const int r = v / S::VPR, c = v % S::VPR;
+      const int row = row0 + r, col = col0 + c * 4;
+      ok[u] = row < d.M && col < d.N;
+      g[u] = *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16);
+      e[u] = (int64_t)row * d.ldc + col;
+      if (ok[u]) {  // the optimizer state streams: non-temporal, so it does not evict GEMM operands
+        th[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.theta + d.poff + e[u]));
+        m[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.am + d.poff + e[u]));
+        vv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.av + d.poff + e[u]));
+      }
     }
-  }
 #pragma unroll
-  for (int u = 0; u < G; ++u) {
-    if (!ok[u]) continue;
-    if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e[u]) = g[u];
-    adamw_vec4(th[u], g[u], m[u], vv[u], decay, step, ac);
-    __builtin_nontemporal_store(th[u], reinterpret_cast<f32x4*>(a.theta + d.poff + e[u]));
-    __builtin_nontemporal_store(m[u], reinterpret_cast<f32x4*>(a.am + d.poff + e[u]));
-    __builtin_nontemporal_store(vv[u], reinterpret_cast<f32x4*>(a.av + d.poff + e[u]));
-    if (a.shadow) {  // read by the next forward and dX GEMMs: a normal store
-      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][0]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][1]) << 16);
-      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][2]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][3]) << 16);
-      *reinterpret_cast<u32x2*>(a.shadow + d.poff + e[u]) = u32x2{lo, hi};
+    for (int u = 0; u < G; ++u) {
+      if (!ok[u]) continue;
+      if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e[u]) = g[u];
+      adamw_vec4(th[u], g[u], m[u], vv[u], decay, step, ac);
+      __builtin_nontemporal_store(th[u], reinterpret_cast<f32x4*>(a.theta + d.poff + e[u]));
+      __builtin_nontemporal_store(m[u], reinterpret_cast<f32x4*>(a.am + d.poff + e[u]));
+      __builtin_nontemporal_store(vv[u], reinterpret_cast<f32x4*>(a.av + d.poff + e[u]));
+      if (a.shadow) {  // read by the next forward and dX GEMMs: a normal store
+        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][0]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][1]) << 16);
+        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][2]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][3]) << 16);
+        *reinterpret_cast<u32x2*>(a.shadow + d.poff + e[u]) = u32x2{lo, hi};
+      }
     }
   }
 }
