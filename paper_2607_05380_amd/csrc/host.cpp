@@ -97,7 +97,7 @@ struct Bufs {
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
   float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / kPartRows floats
   uint32_t* mask = nullptr;  // ReLU/dropout keep bits of H_1..H_L, L * A / 32 words
-  uint32_t* keepw = nullptr; // dropout keep words of the current step, L * A / 32 words
+  uint32_t* keepw = nullptr; // dropout keep words, 2 copies of L * A / 32 words
   char* zeros = nullptr;     // 256 zero bytes: GEMM loads of out-of-range elements read them
   float *dY = nullptr, *rowloss = nullptr;
   MemberDev* d_mem = nullptr;
@@ -125,7 +125,10 @@ struct pack_handle {
 
   bool bound = false;
   Bufs b;
-  std::vector<Launch> fwd, dx, dw;  // per layer (index l-1)
+  // per layer (index l-1); the forward launches exist once per keep-word
+  // buffer: the dropout keep words alternate between two copies by step
+  // parity, so the next step's are produced while this step's backward runs
+  std::vector<Launch> fwd[2], dx, dw;
   Launch fwd1_eval{};                // layer 1 over the shared validation rows in H_0 block 0
   int ncoltiles = 0;
   int nheadtiles = 0;
@@ -136,6 +139,8 @@ struct pack_handle {
   // caller's stream, joined back through events (created by pack_bind)
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipEvent_t ev_keep[2] = {nullptr, nullptr};  // keep words of the step with that parity are ready
+  uint64_t keep_ready = 0;                     // step whose keep words are (being) produced ahead
 
   // optional per-kernel timing
   bool prof = false;
@@ -306,7 +311,7 @@ struct Plan {
   std::vector<int64_t> cost;  // planner's cost of each tile (depth x valid area)
   std::vector<ColTile> coltiles;
   std::vector<HeadTile> headtiles;
-  std::vector<Launch> fwd, dx, dw;
+  std::vector<Launch> fwd[2], dx, dw;
   Launch fwd1_eval{};
 };
 
@@ -397,10 +402,14 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     return (const char*)wsrc + (size_t)h->mem[k].toff[2 * (l - 1)] * es;
   };
   auto act = [&](void* base, int k) -> void* { return (char*)base + (size_t)h->mem[k].act_off * es; };
-  auto h0 = [&](int k) -> void* { return bf.H0 + (size_t)k * h->h0_elems() * es; };
   auto maskp = [&](int l, int k) -> uint32_t* {  // keep bits of H_l (1-based) of member k
     return bf.mask + (size_t)(l - 1) * (h->A / 32) + h->mem[k].act_off / 32;
   };
+  auto h0 = [&](int k) -> void* { return bf.H0 + (size_t)k * h->h0_elems() * es; };
+  auto keepw = [&](int par, int l, int k) -> const uint32_t* {
+    return bf.keepw + (size_t)par * c.L * (h->A / 32) + (maskp(l, k) - bf.mask);
+  };
+  for (int par = 0; par < 2; ++par)
   for (int l = 1; l <= c.L; ++l) {
     // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
     Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
@@ -422,7 +431,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.drop_t = m.t;
       d.drop_s = (float)m.scale;
       d.mask = maskp(l, k);
-      d.keepw = bf.keepw + (maskp(l, k) - bf.mask);
+      d.keepw = keepw(par, l, k);
       p.descs.push_back(d);
       add_tiles(p, f, f.desc0 + k, h->Bp, m.dp, d.Kd);
       {
@@ -433,13 +442,13 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       }
     }
     sort_launch(p, f);
-    p.fwd.push_back(f);
+    p.fwd[par].push_back(f);
   }
   {
     // evaluation, layer 1: every member reads the same validation rows (H_0 block 0)
     Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
     for (int k = 0; k < c.K; ++k) {
-      GemmDesc d = p.descs[p.fwd[0].desc0 + k];
+      GemmDesc d = p.descs[p.fwd[0][0].desc0 + k];
       d.A = h0(0);
       p.descs.push_back(d);
       add_tiles(p, f, f.desc0 + k, h->Bp, h->mem[k].dp, d.Kd);
@@ -546,7 +555,7 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
   bf.colpart = cv.take<float>((size_t)h->A / kPartRows);
   bf.mask = cv.take<uint32_t>((size_t)c.L * (h->A / 32));
-  bf.keepw = cv.take<uint32_t>((size_t)c.L * (h->A / 32));
+  bf.keepw = cv.take<uint32_t>((size_t)2 * c.L * (h->A / 32));
   bf.zeros = cv.take<char>(256);
   bf.dY = cv.take<float>((size_t)c.K * h->Bp * c.d_out);
   bf.rowloss = cv.take<float>((size_t)c.K * h->Bp);
@@ -690,6 +699,8 @@ int pack_destroy(pack_handle* h) {
     for (hipEvent_t e : h->event_pool) (void)hipEventDestroy(e);
     if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
     if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+    for (hipEvent_t e : h->ev_keep)
+      if (e) (void)hipEventDestroy(e);
     if (h->side) (void)hipStreamDestroy(h->side);
   }
   delete h;
@@ -724,7 +735,9 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
     HIP_TRY(hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
     HIP_TRY(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
     HIP_TRY(hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming));
+    for (hipEvent_t& e : h->ev_keep) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
+  h->keep_ready = 0;
   HIP_TRY(hipMemsetAsync(workspace, 0, need, stream));
   HIP_TRY(hipMemcpyAsync(h->b.theta, h->theta_host.data(), h->P * sizeof(float), hipMemcpyHostToDevice, stream));
   std::vector<MemberDev> md(h->cfg.K);
@@ -745,10 +758,11 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   HIP_TRY(hipMemcpyAsync(h->b.d_headtiles, plan.headtiles.data(), plan.headtiles.size() * sizeof(HeadTile), hipMemcpyHostToDevice, stream));
   if (h->prec == Prec::BF16) HIP_TRY(launch_to_shadow(h->b.theta, h->b.shadow, h->P, stream));
   HIP_TRY(hipStreamSynchronize(stream));
-  h->fwd = plan.fwd;
-  h->dx = plan.dx;
+  h->fwd[0] = plan.fwd[0];
+  h->fwd[1] = plan.fwd[1];
   h->dw = plan.dw;
   h->fwd1_eval = plan.fwd1_eval;
+  h->dx = plan.dx;
   h->ncoltiles = (int)plan.coltiles.size();
   h->nheadtiles = (int)plan.headtiles.size();
   h->head_rb = head_rows(h);
@@ -786,20 +800,35 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     max_dp = std::max(max_dp, m.dp);
     nkeep += (double)c.L * h->Bp * m.dp / 8;
   }
-  // the dropout keep words (Philox, ALU-bound) are generated on the side
-  // stream while the gather (HBM-bound) runs; the forward GEMMs wait for both
-  HIP_TRY(hipEventRecord(h->ev_fork, stream));
-  HIP_TRY(hipStreamWaitEvent(h->side, h->ev_fork, 0));
-  HIP_TRY(timed(h, "dropout_words", 1, 0.0, nkeep, h->side, [&] {
-    return launch_dropout_words(a.key0, a.key1, a.step, h->b.d_mem, c.K, c.L, max_dp, h->Bp, c.B, h->A / 32,
-                                h->b.keepw, h->side);
-  }));
-  HIP_TRY(hipEventRecord(h->ev_join, h->side));
+  // Dropout keep words (Philox, ALU-bound) run on the side stream: normally
+  // they were produced during the previous step's backward pass; otherwise
+  // (first step, or after a break in the sequence) they are produced now,
+  // beside the HBM-bound gather.  Either way the forward GEMMs wait for them.
+  const int par = (int)(step & 1);
+  auto keep_words = [&](uint64_t s_step, int p) {
+    return timed(h, "dropout_words", 1, 0.0, nkeep, h->side, [&] {
+      return launch_dropout_words(a.key0, a.key1, as_u32(s_step), h->b.d_mem, c.K, c.L, max_dp, h->Bp, c.B,
+                                  h->A / 32, h->b.keepw + (size_t)p * c.L * (h->A / 32), h->side);
+    });
+  };
+  if (h->keep_ready != step) {
+    HIP_TRY(hipEventRecord(h->ev_fork, stream));
+    HIP_TRY(hipStreamWaitEvent(h->side, h->ev_fork, 0));
+    HIP_TRY(keep_words(step, par));
+    HIP_TRY(hipEventRecord(h->ev_keep[par], h->side));
+  }
   HIP_TRY(timed(h, "gather", 1, 0.0, (double)c.K * c.B * c.d_in * (4.0 + h->elt()), stream, [&] {
     return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, c.K, h->Bp, h->b.H0, stream);
   }));
-  HIP_TRY(hipStreamWaitEvent(stream, h->ev_join, 0));
-  for (int l = 1; l <= c.L; ++l) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[l - 1], l));
+  HIP_TRY(hipStreamWaitEvent(stream, h->ev_keep[par], 0));
+  for (int l = 1; l <= c.L; ++l) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][l - 1], l));
+  // the next step's keep words go to the other buffer (last read by the
+  // previous step's forward pass) while this step's backward runs
+  HIP_TRY(hipEventRecord(h->ev_fork, stream));
+  HIP_TRY(hipStreamWaitEvent(h->side, h->ev_fork, 0));
+  HIP_TRY(keep_words(step + 1, par ^ 1));
+  HIP_TRY(hipEventRecord(h->ev_keep[par ^ 1], h->side));
+  h->keep_ready = step + 1;
   HIP_TRY(timed(h, "head_fwd", 1, 0.0, act_bytes, stream, [&] {
     return launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, y,
                            idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, stream);
@@ -869,7 +898,7 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
     a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
     HIP_TRY(launch_gather(h->prec, Xv, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, stream));
     for (int l = 1; l <= c.L; ++l) {
-      GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[l - 1]);
+      GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][l - 1]);
       al.layer = l;
       HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
     }
