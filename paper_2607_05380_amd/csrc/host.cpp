@@ -128,8 +128,15 @@ struct pack_handle {
   // per layer (index l-1); the forward launches exist once per keep-word
   // buffer: the dropout keep words alternate between two copies by step
   // parity, so the next step's are produced while this step's backward runs
-  std::vector<Launch> fwd[2], dx, dw;
+  std::vector<Launch> fwd[2][2], dx[2], dw[2];  // [keep-word parity][half] / [half]
   Launch fwd1_eval{};                // layer 1 over the shared validation rows in H_0 block 0
+  // The members are split into two halves of about equal GEMM work; each
+  // half's GEMM chain runs on its own stream (the caller's and side_b), which
+  // measured faster than one launch over all members.
+  std::vector<int> half[2];
+  int coltile0[3] = {0, 0, 0};       // bias-partial column tiles of half h: [coltile0[h], coltile0[h+1])
+  hipStream_t side_b = nullptr;
+  hipEvent_t ev_split = nullptr, ev_merge = nullptr;
   int ncoltiles = 0;
   int nheadtiles = 0;
   int head_rb = 0;  // rows per head-backward block
@@ -311,8 +318,9 @@ struct Plan {
   std::vector<int64_t> cost;  // planner's cost of each tile (depth x valid area)
   std::vector<ColTile> coltiles;
   std::vector<HeadTile> headtiles;
-  std::vector<Launch> fwd[2], dx, dw;
+  std::vector<Launch> fwd[2][2], dx[2], dw[2];
   Launch fwd1_eval{};
+  int coltile0[3] = {0, 0, 0};
 };
 
 // Tiles of one member's M x N output: big 256 x 256 tiles, except that a
@@ -387,6 +395,29 @@ void sort_launch(Plan& p, const Launch& ln) {
   }
 }
 
+// Members into two halves of about equal GEMM work (longest first, each to
+// the lighter half); TABPACK_STREAMS=1 keeps every member in half 0.
+void split_members(pack_handle* h) {
+  const pack_config& c = h->cfg;
+  h->half[0].clear();
+  h->half[1].clear();
+  bool two = true;
+  if (const char* e = getenv("TABPACK_STREAMS")) two = std::string(e) != "1";
+  std::vector<std::pair<double, int>> cost;
+  for (int k = 0; k < c.K; ++k) {
+    const double w = h->mem[k].dp;
+    cost.push_back({w * (h->Pin + (c.L - 1) * w), k});
+  }
+  std::stable_sort(cost.begin(), cost.end(), [](const auto& x, const auto& y) { return x.first > y.first; });
+  double load[2] = {0.0, 0.0};
+  for (const auto& ck : cost) {
+    const int hf = two && load[1] < load[0] ? 1 : 0;
+    load[hf] += ck.first;
+    h->half[hf].push_back(ck.second);
+  }
+  for (auto& v : h->half) std::sort(v.begin(), v.end());
+}
+
 // Rows per head-backward block: up to 256, dividing Bp.
 int head_rows(const pack_handle* h) { return h->Bp % 256 == 0 ? 256 : h->Bp; }
 
@@ -410,10 +441,11 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     return bf.keepw + (size_t)par * c.L * (h->A / 32) + (maskp(l, k) - bf.mask);
   };
   for (int par = 0; par < 2; ++par)
+  for (int hf = 0; hf < 2; ++hf)
   for (int l = 1; l <= c.L; ++l) {
     // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
-    Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
-    for (int k = 0; k < c.K; ++k) {
+    Launch f{(int)p.descs.size(), (int)h->half[hf].size(), (int)p.tiles.size(), 0, 0.0};
+    for (int k : h->half[hf]) {
       const Member& m = h->mem[k];
       GemmDesc d{};
       d.A = l == 1 ? h0(k) : act(Hl(l - 1), k);
@@ -432,8 +464,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.drop_s = (float)m.scale;
       d.mask = maskp(l, k);
       d.keepw = keepw(par, l, k);
+      add_tiles(p, f, (int)p.descs.size(), h->Bp, m.dp, d.Kd);
       p.descs.push_back(d);
-      add_tiles(p, f, f.desc0 + k, h->Bp, m.dp, d.Kd);
       {
         const double fi = l == 1 ? c.d_in : m.width, w = m.width;
         f.flops += 2.0 * c.B * w * fi;
@@ -442,24 +474,27 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       }
     }
     sort_launch(p, f);
-    p.fwd[par].push_back(f);
+    p.fwd[par][hf].push_back(f);
   }
   {
     // evaluation, layer 1: every member reads the same validation rows (H_0 block 0)
     Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
-    for (int k = 0; k < c.K; ++k) {
-      GemmDesc d = p.descs[p.fwd[0][0].desc0 + k];
-      d.A = h0(0);
-      p.descs.push_back(d);
-      add_tiles(p, f, f.desc0 + k, h->Bp, h->mem[k].dp, d.Kd);
-    }
+    for (int hf = 0; hf < 2; ++hf)
+      for (int i = 0; i < (int)h->half[hf].size(); ++i) {
+        const int k = h->half[hf][i];
+        GemmDesc d = p.descs[p.fwd[0][hf][0].desc0 + i];
+        d.A = h0(0);
+        add_tiles(p, f, (int)p.descs.size(), h->Bp, h->mem[k].dp, d.Kd);
+        p.descs.push_back(d);
+      }
     sort_launch(p, f);
     p.fwd1_eval = f;
   }
+  for (int hf = 0; hf < 2; ++hf)
   for (int l = 1; l <= c.L; ++l) {
     // weight gradient: dW_l^T[out, in] = sum_rows dZ_l[row, out] H_{l-1}[row, in]
-    Launch w{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
-    for (int k = 0; k < c.K; ++k) {
+    Launch w{(int)p.descs.size(), (int)h->half[hf].size(), (int)p.tiles.size(), 0, 0.0};
+    for (int k : h->half[hf]) {
       const Member& m = h->mem[k];
       GemmDesc d{};
       d.A = act(dzb(l), k);
@@ -475,8 +510,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       d.poff = m.toff[2 * (l - 1)];
       d.lr = (float)m.lr;
       d.wd = (float)m.wd;
+      add_tiles(p, w, (int)p.descs.size(), d.M, d.N, d.Kd);
       p.descs.push_back(d);
-      add_tiles(p, w, w.desc0 + k, d.M, d.N, d.Kd);
       {
         const double fi = l == 1 ? c.d_in : m.width, wd = m.width;
         w.flops += 2.0 * c.B * wd * fi;
@@ -487,12 +522,12 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       }
     }
     sort_launch(p, w);
-    p.dw.push_back(w);
+    p.dw[hf].push_back(w);
     // data gradient (l >= 2): dZ_{l-1} = (dZ_l W_l) * [H_{l-1} > 0] * s_k
     Launch x{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
     if (l >= 2) {
-      x.ndesc = c.K;
-      for (int k = 0; k < c.K; ++k) {
+      x.ndesc = (int)h->half[hf].size();
+      for (int k : h->half[hf]) {
         const Member& m = h->mem[k];
         GemmDesc d{};
         d.A = act(dzb(l), k);
@@ -508,8 +543,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
         d.Kd = m.dp;
         d.member = k;
         d.drop_s = (float)m.scale;
+        add_tiles(p, x, (int)p.descs.size(), h->Bp, m.dp, d.Kd);
         p.descs.push_back(d);
-        add_tiles(p, x, x.desc0 + k, h->Bp, m.dp, d.Kd);
         x.flops += 2.0 * c.B * m.width * m.width;
         // dZ_l and W_l read, dZ_{l-1} written, mask words read, bias partials written
         x.bytes += (double)h->elt() * (2.0 * c.B * m.width + (double)m.width * m.width) + c.B * m.width / 8.0 +
@@ -517,10 +552,14 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
       }
       sort_launch(p, x);
     }
-    p.dx.push_back(x);
+    p.dx[hf].push_back(x);
   }
-  for (int k = 0; k < c.K; ++k)
-    for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
+  for (int hf = 0; hf < 2; ++hf) {
+    p.coltile0[hf] = (int)p.coltiles.size();
+    for (int k : h->half[hf])
+      for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
+  }
+  p.coltile0[2] = (int)p.coltiles.size();
   const int hcols = head_bwd_cols(c.d_out), hrb = head_rows(h);
   for (int r0 = 0; r0 < h->Bp; r0 += hrb)
     for (int k = 0; k < c.K; ++k)
@@ -688,6 +727,7 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
     m.scale = 1.0 / (1.0 - m.dropout);
   }
   plan_layout(h);
+  split_members(h);
   init_params(h);
   *out = h;
   g_err.clear();
@@ -702,6 +742,9 @@ int pack_destroy(pack_handle* h) {
     for (hipEvent_t e : h->ev_keep)
       if (e) (void)hipEventDestroy(e);
     if (h->side) (void)hipStreamDestroy(h->side);
+    if (h->ev_split) (void)hipEventDestroy(h->ev_split);
+    if (h->ev_merge) (void)hipEventDestroy(h->ev_merge);
+    if (h->side_b) (void)hipStreamDestroy(h->side_b);
   }
   delete h;
   return PACK_OK;
@@ -736,6 +779,9 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
     HIP_TRY(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
     HIP_TRY(hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming));
     for (hipEvent_t& e : h->ev_keep) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    HIP_TRY(hipStreamCreateWithFlags(&h->side_b, hipStreamNonBlocking));
+    HIP_TRY(hipEventCreateWithFlags(&h->ev_split, hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&h->ev_merge, hipEventDisableTiming));
   }
   h->keep_ready = 0;
   HIP_TRY(hipMemsetAsync(workspace, 0, need, stream));
@@ -758,11 +804,14 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   HIP_TRY(hipMemcpyAsync(h->b.d_headtiles, plan.headtiles.data(), plan.headtiles.size() * sizeof(HeadTile), hipMemcpyHostToDevice, stream));
   if (h->prec == Prec::BF16) HIP_TRY(launch_to_shadow(h->b.theta, h->b.shadow, h->P, stream));
   HIP_TRY(hipStreamSynchronize(stream));
-  h->fwd[0] = plan.fwd[0];
-  h->fwd[1] = plan.fwd[1];
-  h->dw = plan.dw;
+  for (int hf = 0; hf < 2; ++hf) {
+    h->fwd[0][hf] = plan.fwd[0][hf];
+    h->fwd[1][hf] = plan.fwd[1][hf];
+    h->dx[hf] = plan.dx[hf];
+    h->dw[hf] = plan.dw[hf];
+  }
   h->fwd1_eval = plan.fwd1_eval;
-  h->dx = plan.dx;
+  for (int i = 0; i < 3; ++i) h->coltile0[i] = plan.coltile0[i];
   h->ncoltiles = (int)plan.coltiles.size();
   h->nheadtiles = (int)plan.headtiles.size();
   h->head_rb = head_rows(h);
@@ -788,11 +837,21 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     for (const Member& m : h->mem) s += m.width;
     return s;
   }();
-  auto gemm = [&](OpKind ak, OpKind bk, EpiKind e, const Launch& ln, int layer) {
+  auto gemm = [&](OpKind ak, OpKind bk, EpiKind e, const Launch& ln, int layer, hipStream_t s) {
     GemmArgs al = for_launch(a, ln);
     al.layer = layer;
-    return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, ln.bytes, stream,
-                 [&] { return launch_gemm(h->prec, ak, bk, e, al, stream); });
+    return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, ln.bytes, s,
+                 [&] { return launch_gemm(h->prec, ak, bk, e, al, s); });
+  };
+  // the two member halves: half 0 on the caller's stream, half 1 on side_b
+  const hipStream_t hs[2] = {stream, h->side_b};
+  auto split = [&]() -> hipError_t {
+    hipError_t e = hipEventRecord(h->ev_split, stream);
+    return e != hipSuccess ? e : hipStreamWaitEvent(h->side_b, h->ev_split, 0);
+  };
+  auto merge = [&]() -> hipError_t {
+    hipError_t e = hipEventRecord(h->ev_merge, h->side_b);
+    return e != hipSuccess ? e : hipStreamWaitEvent(stream, h->ev_merge, 0);
   };
   int max_dp = 0;
   double nkeep = 0;
@@ -821,7 +880,10 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, c.K, h->Bp, h->b.H0, stream);
   }));
   HIP_TRY(hipStreamWaitEvent(stream, h->ev_keep[par], 0));
-  for (int l = 1; l <= c.L; ++l) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][l - 1], l));
+  HIP_TRY(split());
+  for (int l = 1; l <= c.L; ++l)
+    for (int hf = 0; hf < 2; ++hf) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
+  HIP_TRY(merge());
   // the next step's keep words go to the other buffer (last read by the
   // previous step's forward pass) while this step's backward runs
   HIP_TRY(hipEventRecord(h->ev_fork, stream));
@@ -848,31 +910,36 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
   const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
   const AdamConst ac{(float)c.beta1, (float)c.beta2, (float)c.eps, (float)bc1, (float)std::sqrt(bc2)};
-  for (int l = c.L; l >= 1; --l) {
-    // dX_l reads W_l, so it runs before the weight-gradient GEMM updates W_l in place
-    if (l > 1) {
-      HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[l - 1], l));
-      HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 / h->elt() / kPartRows, stream, [&] {
-        return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles, h->ncoltiles, h->Bp / kPartRows,
-                                         h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, stream);
-      }));
+  HIP_TRY(split());
+  for (int l = c.L; l >= 1; --l)
+    for (int hf = 0; hf < 2; ++hf) {
+      const hipStream_t s = hs[hf];
+      // dX_l reads W_l, so it runs before the weight-gradient GEMM updates W_l in place
+      if (l > 1) {
+        HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[hf][l - 1], l, s));
+        HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 / h->elt() / kPartRows / 2, s, [&] {
+          return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles + h->coltile0[hf],
+                                           h->coltile0[hf + 1] - h->coltile0[hf], h->Bp / kPartRows,
+                                           h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, s);
+        }));
+      }
+      GemmArgs al = for_launch(a, h->dw[hf][l - 1]);
+      al.layer = l;
+      al.theta = h->b.theta;
+      al.am = h->b.m;
+      al.av = h->b.v;
+      al.shadow = h->b.shadow;
+      al.beta1 = ac.beta1;
+      al.beta2 = ac.beta2;
+      al.eps = ac.eps;
+      al.bc1 = ac.bc1;
+      al.bc2_sqrt = ac.bc2_sqrt;
+      al.keep_grad = c.keep_grads ? 1 : 0;
+      // AdamW fused: the weight update traffic dominates, so the HBM roofline applies
+      HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW), 1, h->dw[hf][l - 1].flops,
+                    h->dw[hf][l - 1].bytes, s, [&] { return launch_gemm(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW, al, s); }));
     }
-    GemmArgs al = for_launch(a, h->dw[l - 1]);
-    al.layer = l;
-    al.theta = h->b.theta;
-    al.am = h->b.m;
-    al.av = h->b.v;
-    al.shadow = h->b.shadow;
-    al.beta1 = ac.beta1;
-    al.beta2 = ac.beta2;
-    al.eps = ac.eps;
-    al.bc1 = ac.bc1;
-    al.bc2_sqrt = ac.bc2_sqrt;
-    al.keep_grad = c.keep_grads ? 1 : 0;
-    // AdamW fused: the weight update traffic dominates, so the HBM roofline applies
-    HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW), 1, h->dw[l - 1].flops, h->dw[l - 1].bytes, stream,
-                  [&] { return launch_gemm(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW, al, stream); }));
-  }
+  HIP_TRY(merge());
   double naux = 0;
   for (int k = 0; k < c.K; ++k) {
     const Member& m = h->mem[k];
@@ -898,9 +965,11 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
     a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
     HIP_TRY(launch_gather(h->prec, Xv, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, stream));
     for (int l = 1; l <= c.L; ++l) {
-      GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][l - 1]);
-      al.layer = l;
-      HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
+      for (int hf = 0; hf < (l == 1 ? 1 : 2); ++hf) {
+        GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][hf][l - 1]);
+        al.layer = l;
+        HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
+      }
     }
     HIP_TRY(launch_head_fwd(h->prec, h->task, true, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, yv,
                             nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, stream));

@@ -711,6 +711,7 @@ hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int 
 hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, const ColTile* tiles,
                                      int ntiles, int nparts, const int64_t* bias_off, float* grad,
                                      hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
   hipLaunchKernelGGL(bias_from_partials_kernel, dim3(ntiles), dim3(64), 0, s, part, mem, tiles, nparts,
                      bias_off, grad);
   return hipGetLastError();
