@@ -38,6 +38,7 @@ int fail(int code, const char* fmt, ...) {
   } while (0)
 
 constexpr uint32_t kTagHparam = 1, kTagInit = 2;
+constexpr int kGroups = 4;  // at most this many member groups run their GEMM chains concurrently
 
 int64_t round_up(int64_t x, int64_t q) { return (x + q - 1) / q * q; }
 
@@ -128,15 +129,16 @@ struct pack_handle {
   // per layer (index l-1); the forward launches exist once per keep-word
   // buffer: the dropout keep words alternate between two copies by step
   // parity, so the next step's are produced while this step's backward runs
-  std::vector<Launch> fwd[2][2], dx[2], dw[2];  // [keep-word parity][half] / [half]
+  std::vector<Launch> fwd[2][kGroups], dx[kGroups], dw[kGroups];  // [keep-word parity][group] / [group]
   Launch fwd1_eval{};                // layer 1 over the shared validation rows in H_0 block 0
-  // The members are split into two halves of about equal GEMM work; each
-  // half's GEMM chain runs on its own stream (the caller's and side_b), which
+  // The members are split into ngroups groups of about equal GEMM work; each
+  // group's GEMM chain runs on its own stream (group 0 on the caller's), which
   // measured faster than one launch over all members.
-  std::vector<int> half[2];
-  int coltile0[3] = {0, 0, 0};       // bias-partial column tiles of half h: [coltile0[h], coltile0[h+1])
-  hipStream_t side_b = nullptr;
-  hipEvent_t ev_split = nullptr, ev_merge = nullptr;
+  int ngroups = 1;
+  std::vector<int> group[kGroups];
+  int coltile0[kGroups + 1] = {};    // bias-partial column tiles of group g: [coltile0[g], coltile0[g+1])
+  hipStream_t gstream[kGroups] = {};  // streams of groups 1.. (entry 0 unused)
+  hipEvent_t ev_split = nullptr, ev_merge[kGroups] = {};
   int ncoltiles = 0;
   int nheadtiles = 0;
   int head_rb = 0;  // rows per head-backward block
@@ -318,9 +320,9 @@ struct Plan {
   std::vector<int64_t> cost;  // planner's cost of each tile (depth x valid area)
   std::vector<ColTile> coltiles;
   std::vector<HeadTile> headtiles;
-  std::vector<Launch> fwd[2][2], dx[2], dw[2];
+  std::vector<Launch> fwd[2][kGroups], dx[kGroups], dw[kGroups];
   Launch fwd1_eval{};
-  int coltile0[3] = {0, 0, 0};
+  int coltile0[kGroups + 1] = {};
 };
 
 // Tiles of one member's M x N output: big 256 x 256 tiles, except that a
@@ -395,27 +397,27 @@ void sort_launch(Plan& p, const Launch& ln) {
   }
 }
 
-// Members into two halves of about equal GEMM work (longest first, each to
-// the lighter half); TABPACK_STREAMS=1 keeps every member in half 0.
+// Members into ngroups groups of about equal GEMM work (longest first, each
+// to the lightest group).  TABPACK_STREAMS (1 .. 4) overrides the default 2.
 void split_members(pack_handle* h) {
   const pack_config& c = h->cfg;
-  h->half[0].clear();
-  h->half[1].clear();
-  bool two = true;
-  if (const char* e = getenv("TABPACK_STREAMS")) two = std::string(e) != "1";
+  int ng = 2;
+  if (const char* e = getenv("TABPACK_STREAMS")) ng = std::max(1, std::min(kGroups, atoi(e)));
+  h->ngroups = std::min(ng, c.K);
+  for (auto& v : h->group) v.clear();
   std::vector<std::pair<double, int>> cost;
   for (int k = 0; k < c.K; ++k) {
     const double w = h->mem[k].dp;
     cost.push_back({w * (h->Pin + (c.L - 1) * w), k});
   }
   std::stable_sort(cost.begin(), cost.end(), [](const auto& x, const auto& y) { return x.first > y.first; });
-  double load[2] = {0.0, 0.0};
+  std::vector<double> load(h->ngroups, 0.0);
   for (const auto& ck : cost) {
-    const int hf = two && load[1] < load[0] ? 1 : 0;
-    load[hf] += ck.first;
-    h->half[hf].push_back(ck.second);
+    const int g = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    load[g] += ck.first;
+    h->group[g].push_back(ck.second);
   }
-  for (auto& v : h->half) std::sort(v.begin(), v.end());
+  for (auto& v : h->group) std::sort(v.begin(), v.end());
 }
 
 // Rows per head-backward block: up to 256, dividing Bp.
@@ -441,11 +443,11 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     return bf.keepw + (size_t)par * c.L * (h->A / 32) + (maskp(l, k) - bf.mask);
   };
   for (int par = 0; par < 2; ++par)
-  for (int hf = 0; hf < 2; ++hf)
+  for (int hf = 0; hf < kGroups; ++hf)
   for (int l = 1; l <= c.L; ++l) {
     // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
-    Launch f{(int)p.descs.size(), (int)h->half[hf].size(), (int)p.tiles.size(), 0, 0.0};
-    for (int k : h->half[hf]) {
+    Launch f{(int)p.descs.size(), (int)h->group[hf].size(), (int)p.tiles.size(), 0, 0.0};
+    for (int k : h->group[hf]) {
       const Member& m = h->mem[k];
       GemmDesc d{};
       d.A = l == 1 ? h0(k) : act(Hl(l - 1), k);
@@ -479,9 +481,9 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   {
     // evaluation, layer 1: every member reads the same validation rows (H_0 block 0)
     Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
-    for (int hf = 0; hf < 2; ++hf)
-      for (int i = 0; i < (int)h->half[hf].size(); ++i) {
-        const int k = h->half[hf][i];
+    for (int hf = 0; hf < kGroups; ++hf)
+      for (int i = 0; i < (int)h->group[hf].size(); ++i) {
+        const int k = h->group[hf][i];
         GemmDesc d = p.descs[p.fwd[0][hf][0].desc0 + i];
         d.A = h0(0);
         add_tiles(p, f, (int)p.descs.size(), h->Bp, h->mem[k].dp, d.Kd);
@@ -490,11 +492,11 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     sort_launch(p, f);
     p.fwd1_eval = f;
   }
-  for (int hf = 0; hf < 2; ++hf)
+  for (int hf = 0; hf < kGroups; ++hf)
   for (int l = 1; l <= c.L; ++l) {
     // weight gradient: dW_l^T[out, in] = sum_rows dZ_l[row, out] H_{l-1}[row, in]
-    Launch w{(int)p.descs.size(), (int)h->half[hf].size(), (int)p.tiles.size(), 0, 0.0};
-    for (int k : h->half[hf]) {
+    Launch w{(int)p.descs.size(), (int)h->group[hf].size(), (int)p.tiles.size(), 0, 0.0};
+    for (int k : h->group[hf]) {
       const Member& m = h->mem[k];
       GemmDesc d{};
       d.A = act(dzb(l), k);
@@ -526,8 +528,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     // data gradient (l >= 2): dZ_{l-1} = (dZ_l W_l) * [H_{l-1} > 0] * s_k
     Launch x{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
     if (l >= 2) {
-      x.ndesc = (int)h->half[hf].size();
-      for (int k : h->half[hf]) {
+      x.ndesc = (int)h->group[hf].size();
+      for (int k : h->group[hf]) {
         const Member& m = h->mem[k];
         GemmDesc d{};
         d.A = act(dzb(l), k);
@@ -554,12 +556,12 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     }
     p.dx[hf].push_back(x);
   }
-  for (int hf = 0; hf < 2; ++hf) {
+  for (int hf = 0; hf < kGroups; ++hf) {
     p.coltile0[hf] = (int)p.coltiles.size();
-    for (int k : h->half[hf])
+    for (int k : h->group[hf])
       for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
   }
-  p.coltile0[2] = (int)p.coltiles.size();
+  p.coltile0[kGroups] = (int)p.coltiles.size();
   const int hcols = head_bwd_cols(c.d_out), hrb = head_rows(h);
   for (int r0 = 0; r0 < h->Bp; r0 += hrb)
     for (int k = 0; k < c.K; ++k)
@@ -743,8 +745,10 @@ int pack_destroy(pack_handle* h) {
       if (e) (void)hipEventDestroy(e);
     if (h->side) (void)hipStreamDestroy(h->side);
     if (h->ev_split) (void)hipEventDestroy(h->ev_split);
-    if (h->ev_merge) (void)hipEventDestroy(h->ev_merge);
-    if (h->side_b) (void)hipStreamDestroy(h->side_b);
+    for (int g = 1; g < kGroups; ++g) {
+      if (h->ev_merge[g]) (void)hipEventDestroy(h->ev_merge[g]);
+      if (h->gstream[g]) (void)hipStreamDestroy(h->gstream[g]);
+    }
   }
   delete h;
   return PACK_OK;
@@ -779,9 +783,11 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
     HIP_TRY(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
     HIP_TRY(hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming));
     for (hipEvent_t& e : h->ev_keep) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    HIP_TRY(hipStreamCreateWithFlags(&h->side_b, hipStreamNonBlocking));
     HIP_TRY(hipEventCreateWithFlags(&h->ev_split, hipEventDisableTiming));
-    HIP_TRY(hipEventCreateWithFlags(&h->ev_merge, hipEventDisableTiming));
+    for (int g = 1; g < kGroups; ++g) {
+      HIP_TRY(hipStreamCreateWithFlags(&h->gstream[g], hipStreamNonBlocking));
+      HIP_TRY(hipEventCreateWithFlags(&h->ev_merge[g], hipEventDisableTiming));
+    }
   }
   h->keep_ready = 0;
   HIP_TRY(hipMemsetAsync(workspace, 0, need, stream));
@@ -804,14 +810,14 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   HIP_TRY(hipMemcpyAsync(h->b.d_headtiles, plan.headtiles.data(), plan.headtiles.size() * sizeof(HeadTile), hipMemcpyHostToDevice, stream));
   if (h->prec == Prec::BF16) HIP_TRY(launch_to_shadow(h->b.theta, h->b.shadow, h->P, stream));
   HIP_TRY(hipStreamSynchronize(stream));
-  for (int hf = 0; hf < 2; ++hf) {
+  for (int hf = 0; hf < kGroups; ++hf) {
     h->fwd[0][hf] = plan.fwd[0][hf];
     h->fwd[1][hf] = plan.fwd[1][hf];
     h->dx[hf] = plan.dx[hf];
     h->dw[hf] = plan.dw[hf];
   }
   h->fwd1_eval = plan.fwd1_eval;
-  for (int i = 0; i < 3; ++i) h->coltile0[i] = plan.coltile0[i];
+  for (int i = 0; i <= kGroups; ++i) h->coltile0[i] = plan.coltile0[i];
   h->ncoltiles = (int)plan.coltiles.size();
   h->nheadtiles = (int)plan.headtiles.size();
   h->head_rb = head_rows(h);
@@ -843,15 +849,22 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, ln.bytes, s,
                  [&] { return launch_gemm(h->prec, ak, bk, e, al, s); });
   };
-  // the two member halves: half 0 on the caller's stream, half 1 on side_b
-  const hipStream_t hs[2] = {stream, h->side_b};
+  // member groups: group 0 on the caller's stream, group g on gstream[g]
+  hipStream_t hs[kGroups] = {stream};
+  for (int g = 1; g < kGroups; ++g) hs[g] = h->gstream[g];
+  const int ng = h->ngroups;
   auto split = [&]() -> hipError_t {
     hipError_t e = hipEventRecord(h->ev_split, stream);
-    return e != hipSuccess ? e : hipStreamWaitEvent(h->side_b, h->ev_split, 0);
+    for (int g = 1; g < ng && e == hipSuccess; ++g) e = hipStreamWaitEvent(hs[g], h->ev_split, 0);
+    return e;
   };
   auto merge = [&]() -> hipError_t {
-    hipError_t e = hipEventRecord(h->ev_merge, h->side_b);
-    return e != hipSuccess ? e : hipStreamWaitEvent(stream, h->ev_merge, 0);
+    hipError_t e = hipSuccess;
+    for (int g = 1; g < ng && e == hipSuccess; ++g) {
+      e = hipEventRecord(h->ev_merge[g], hs[g]);
+      if (e == hipSuccess) e = hipStreamWaitEvent(stream, h->ev_merge[g], 0);
+    }
+    return e;
   };
   int max_dp = 0;
   double nkeep = 0;
@@ -882,7 +895,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   HIP_TRY(hipStreamWaitEvent(stream, h->ev_keep[par], 0));
   HIP_TRY(split());
   for (int l = 1; l <= c.L; ++l)
-    for (int hf = 0; hf < 2; ++hf) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
+    for (int hf = 0; hf < ng; ++hf) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
   HIP_TRY(merge());
   // the next step's keep words go to the other buffer (last read by the
   // previous step's forward pass) while this step's backward runs
@@ -912,12 +925,12 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   const AdamConst ac{(float)c.beta1, (float)c.beta2, (float)c.eps, (float)bc1, (float)std::sqrt(bc2)};
   HIP_TRY(split());
   for (int l = c.L; l >= 1; --l)
-    for (int hf = 0; hf < 2; ++hf) {
+    for (int hf = 0; hf < ng; ++hf) {
       const hipStream_t s = hs[hf];
       // dX_l reads W_l, so it runs before the weight-gradient GEMM updates W_l in place
       if (l > 1) {
         HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[hf][l - 1], l, s));
-        HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 / h->elt() / kPartRows / 2, s, [&] {
+        HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 / h->elt() / kPartRows / ng, s, [&] {
           return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles + h->coltile0[hf],
                                            h->coltile0[hf + 1] - h->coltile0[hf], h->Bp / kPartRows,
                                            h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, s);
@@ -965,7 +978,7 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
     a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
     HIP_TRY(launch_gather(h->prec, Xv, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, stream));
     for (int l = 1; l <= c.L; ++l) {
-      for (int hf = 0; hf < (l == 1 ? 1 : 2); ++hf) {
+      for (int hf = 0; hf < (l == 1 ? 1 : h->ngroups); ++hf) {
         GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][hf][l - 1]);
         al.layer = l;
         HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
