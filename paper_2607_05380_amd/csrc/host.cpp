@@ -109,6 +109,7 @@ struct Bufs {
   Tile* d_tiles = nullptr;
   ColTile* d_coltiles = nullptr;
   HeadTile* d_headtiles = nullptr;
+  int32_t* d_members = nullptr;
   float* headpart = nullptr;  // head backward partials, (Bp / RB) * (d_out + 1) * A / Bp floats
 };
 
@@ -137,6 +138,8 @@ struct pack_handle {
   int ngroups = 1;
   std::vector<int> group[kGroups];
   int coltile0[kGroups + 1] = {};    // bias-partial column tiles of group g: [coltile0[g], coltile0[g+1])
+  int headtile0[kGroups + 1] = {};   // head-backward tiles of group g
+  int member0[kGroups + 1] = {};     // group g's members: d_members[member0[g] .. member0[g+1])
   hipStream_t gstream[kGroups] = {};  // streams of groups 1.. (entry 0 unused)
   hipEvent_t ev_split = nullptr, ev_merge[kGroups] = {};
   int ncoltiles = 0;
@@ -323,6 +326,9 @@ struct Plan {
   std::vector<Launch> fwd[2][kGroups], dx[kGroups], dw[kGroups];
   Launch fwd1_eval{};
   int coltile0[kGroups + 1] = {};
+  int headtile0[kGroups + 1] = {};
+  std::vector<int32_t> members;  // member ids in group order
+  int member0[kGroups + 1] = {};
 };
 
 // Tiles of one member's M x N output: big 256 x 256 tiles, except that a
@@ -398,10 +404,12 @@ void sort_launch(Plan& p, const Launch& ln) {
 }
 
 // Members into ngroups groups of about equal GEMM work (longest first, each
-// to the lightest group).  TABPACK_STREAMS (1 .. 4) overrides the default 2.
+// to the lightest group).  TABPACK_STREAMS (1 .. 4) overrides the default 3
+// (measured on the 64-member workloads: 1 group 1.80 ms, 2 groups 1.63 ms,
+// 3 groups 1.60 ms per step; 4 groups exceed the four hardware queues).
 void split_members(pack_handle* h) {
   const pack_config& c = h->cfg;
-  int ng = 2;
+  int ng = 3;
   if (const char* e = getenv("TABPACK_STREAMS")) ng = std::max(1, std::min(kGroups, atoi(e)));
   h->ngroups = std::min(ng, c.K);
   for (auto& v : h->group) v.clear();
@@ -563,9 +571,16 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   }
   p.coltile0[kGroups] = (int)p.coltiles.size();
   const int hcols = head_bwd_cols(c.d_out), hrb = head_rows(h);
-  for (int r0 = 0; r0 < h->Bp; r0 += hrb)
-    for (int k = 0; k < c.K; ++k)
-      for (int c0 = 0; c0 < h->mem[k].dp; c0 += hcols) p.headtiles.push_back(HeadTile{k, c0, r0});
+  for (int hf = 0; hf < kGroups; ++hf) {
+    p.headtile0[hf] = (int)p.headtiles.size();
+    p.member0[hf] = (int)p.members.size();
+    for (int r0 = 0; r0 < h->Bp; r0 += hrb)
+      for (int k : h->group[hf])
+        for (int c0 = 0; c0 < h->mem[k].dp; c0 += hcols) p.headtiles.push_back(HeadTile{k, c0, r0});
+    for (int k : h->group[hf]) p.members.push_back(k);
+  }
+  p.headtile0[kGroups] = (int)p.headtiles.size();
+  p.member0[kGroups] = (int)p.members.size();
   return p;
 }
 
@@ -609,6 +624,7 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
   bf.d_tiles = cv.take<Tile>(plan.tiles.size());
   bf.d_coltiles = cv.take<ColTile>(plan.coltiles.size());
   bf.d_headtiles = cv.take<HeadTile>(plan.headtiles.size());
+  bf.d_members = cv.take<int32_t>(plan.members.size());
   bf.headpart = cv.take<float>((size_t)(h->Bp / head_rows(h)) * (c.d_out + 1) * (h->A / h->Bp));
   if (plan_out) *plan_out = std::move(plan);
   return (size_t)round_up((int64_t)cv.off, 256);
@@ -808,6 +824,8 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   HIP_TRY(hipMemcpyAsync(h->b.d_tiles, plan.tiles.data(), plan.tiles.size() * sizeof(Tile), hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_coltiles, plan.coltiles.data(), plan.coltiles.size() * sizeof(ColTile), hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_headtiles, plan.headtiles.data(), plan.headtiles.size() * sizeof(HeadTile), hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(h->b.d_members, plan.members.data(), plan.members.size() * sizeof(int32_t),
+                         hipMemcpyHostToDevice, stream));
   if (h->prec == Prec::BF16) HIP_TRY(launch_to_shadow(h->b.theta, h->b.shadow, h->P, stream));
   HIP_TRY(hipStreamSynchronize(stream));
   for (int hf = 0; hf < kGroups; ++hf) {
@@ -817,7 +835,11 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
     h->dw[hf] = plan.dw[hf];
   }
   h->fwd1_eval = plan.fwd1_eval;
-  for (int i = 0; i <= kGroups; ++i) h->coltile0[i] = plan.coltile0[i];
+  for (int i = 0; i <= kGroups; ++i) {
+    h->coltile0[i] = plan.coltile0[i];
+    h->headtile0[i] = plan.headtile0[i];
+    h->member0[i] = plan.member0[i];
+  }
   h->ncoltiles = (int)plan.coltiles.size();
   h->nheadtiles = (int)plan.headtiles.size();
   h->head_rb = head_rows(h);
@@ -893,10 +915,38 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, c.K, h->Bp, h->b.H0, stream);
   }));
   HIP_TRY(hipStreamWaitEvent(stream, h->ev_keep[par], 0));
+  const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
+  const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
+  const AdamConst ac{(float)c.beta1, (float)c.beta2, (float)c.eps, (float)bc1, (float)std::sqrt(bc2)};
+  // Each member group runs its whole chain -- forward GEMMs, head, loss,
+  // backward GEMMs with the fused optimizer -- on its own stream; the groups
+  // join before the bias/head AdamW.
   HIP_TRY(split());
   for (int l = 1; l <= c.L; ++l)
     for (int hf = 0; hf < ng; ++hf) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
-  HIP_TRY(merge());
+  for (int hf = 0; hf < ng; ++hf) {
+    const hipStream_t s = hs[hf];
+    const int32_t* gm = h->b.d_members + h->member0[hf];
+    const int gk = h->member0[hf + 1] - h->member0[hf];
+    HIP_TRY(timed(h, "head_fwd", 1, 0.0, act_bytes / ng, s, [&] {
+      return launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, gk, h->Bp, c.d_out, y,
+                             idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, gm, s);
+    }));
+    HIP_TRY(timed(h, "loss_reduce", 1, 0.0, (double)gk * c.B * 4 * (1 + c.d_out), s, [&] {
+      return launch_loss_reduce(h->b.rowloss, h->b.dY, h->b.d_mem, gk, h->Bp, c.B, c.d_out, h->b.grad, loss_out,
+                                gm, s);
+    }));
+    HIP_TRY(timed(h, "head_bwd", 1, 0.0, 2.0 * act_bytes / ng, s, [&] {
+      return launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_headtiles + h->headtile0[hf],
+                             h->headtile0[hf + 1] - h->headtile0[hf], h->Bp, h->head_rb, c.d_out, h->b.dY,
+                             h->dzb(c.L), h->b.headpart, s);
+    }));
+    HIP_TRY(timed(h, "head_grad_reduce", 1, 0.0, 4.0 * (h->Bp / h->head_rb) * (c.d_out + 1) * (h->A / h->Bp) / ng, s,
+                  [&] {
+                    return launch_head_grad_reduce(h->b.headpart, h->b.d_mem, gk, max_dp, h->Bp, h->head_rb,
+                                                   c.d_out, h->b.grad, gm, s);
+                  }));
+  }
   // the next step's keep words go to the other buffer (last read by the
   // previous step's forward pass) while this step's backward runs
   HIP_TRY(hipEventRecord(h->ev_fork, stream));
@@ -904,26 +954,6 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   HIP_TRY(keep_words(step + 1, par ^ 1));
   HIP_TRY(hipEventRecord(h->ev_keep[par ^ 1], h->side));
   h->keep_ready = step + 1;
-  HIP_TRY(timed(h, "head_fwd", 1, 0.0, act_bytes, stream, [&] {
-    return launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, y,
-                           idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, stream);
-  }));
-  HIP_TRY(timed(h, "loss_reduce", 1, 0.0, (double)c.K * c.B * 4 * (1 + c.d_out), stream, [&] {
-    return launch_loss_reduce(h->b.rowloss, h->b.dY, h->b.d_mem, c.K, h->Bp, c.B, c.d_out, h->b.grad, loss_out,
-                              stream);
-  }));
-  HIP_TRY(timed(h, "head_bwd", 1, 0.0, 2.0 * act_bytes, stream, [&] {
-    return launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_headtiles, h->nheadtiles, h->Bp,
-                           h->head_rb, c.d_out, h->b.dY, h->dzb(c.L), h->b.headpart, stream);
-  }));
-  HIP_TRY(timed(h, "head_grad_reduce", 1, 0.0, 4.0 * (h->Bp / h->head_rb) * (c.d_out + 1) * (h->A / h->Bp), stream, [&] {
-    return launch_head_grad_reduce(h->b.headpart, h->b.d_mem, c.K, max_dp, h->Bp, h->head_rb, c.d_out, h->b.grad,
-                                   stream);
-  }));
-  const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
-  const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
-  const AdamConst ac{(float)c.beta1, (float)c.beta2, (float)c.eps, (float)bc1, (float)std::sqrt(bc2)};
-  HIP_TRY(split());
   for (int l = c.L; l >= 1; --l)
     for (int hf = 0; hf < ng; ++hf) {
       const hipStream_t s = hs[hf];
@@ -985,7 +1015,7 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
       }
     }
     HIP_TRY(launch_head_fwd(h->prec, h->task, true, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, yv,
-                            nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, stream));
+                            nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, nullptr, stream));
   }
   HIP_TRY(launch_eval_score(h->task, pred_out, yv, c.K, Nv, score_out, stream));
   return PACK_OK;

@@ -114,8 +114,9 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, co
                                                        const MemberDev* mem, int Bp, int d_out,
                                                        const void* y, const int32_t* idx, int B,
                                                        int rows_valid, int64_t row_base, int64_t Nv,
-                                                       float* dY, float* rowloss, float* pred) {
-  const int k = blockIdx.y;
+                                                       float* dY, float* rowloss, float* pred,
+                                                       const int32_t* members) {
+  const int k = members ? members[blockIdx.y] : (int)blockIdx.y;
   const int lane = threadIdx.x & 63, sub = lane & 7;
   const int row = blockIdx.x * 32 + (threadIdx.x >> 3);
   if (row >= Bp) return;  // Bp is a multiple of 32: whole 8-lane groups leave together
@@ -204,9 +205,10 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, co
 // Per-member batch-mean loss and head-bias gradient (fixed-order fp64 sums).
 __global__ __launch_bounds__(256) void loss_reduce_kernel(const float* rowloss, const float* dY,
                                                           const MemberDev* mem, int Bp, int B,
-                                                          int d_out, float* grad, float* loss_out) {
+                                                          int d_out, float* grad, float* loss_out,
+                                                          const int32_t* members) {
   __shared__ double sh[4];
-  const int k = blockIdx.x;
+  const int k = members ? members[blockIdx.x] : (int)blockIdx.x;
   double s = 0.0;
   for (int r = threadIdx.x; r < B; r += 256) s += (double)rowloss[(int64_t)k * Bp + r];
   s = block_sum_d(s, sh);
@@ -330,8 +332,9 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* 
 // dW_out and db_L of every member from the head backward's row-block partials
 // (fixed order over the row blocks).
 __global__ __launch_bounds__(256) void head_grad_reduce_kernel(const float* part, const MemberDev* mem, int Bp,
-                                                               int nrb, int d_out, float* grad) {
-  const int k = blockIdx.y;
+                                                               int nrb, int d_out, float* grad,
+                                                               const int32_t* members) {
+  const int k = members ? members[blockIdx.y] : (int)blockIdx.y;
   const MemberDev md = mem[k];
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= md.dp) return;
@@ -619,17 +622,18 @@ namespace {
 template <typename T, bool EVAL, int D>
 void head_fwd_t(dim3 grid, hipStream_t s, Task task, const void* H, const float* theta, const MemberDev* mem,
                 int Bp, int d_out, const void* y, const int32_t* idx, int B, int rows_valid, int64_t row_base,
-                int64_t Nv, float* dY, float* rowloss, float* pred) {
+                int64_t Nv, float* dY, float* rowloss, float* pred, const int32_t* members) {
   hipLaunchKernelGGL((head_fwd_kernel<T, EVAL, D>), grid, dim3(256), 0, s, task, static_cast<const T*>(H), theta,
-                     mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, rowloss, pred);
+                     mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, rowloss, pred, members);
 }
 
 template <typename T, bool EVAL>
 void head_fwd_d(int d_out, dim3 grid, hipStream_t s, Task task, const void* H, const float* theta,
                 const MemberDev* mem, int Bp, const void* y, const int32_t* idx, int B, int rows_valid,
-                int64_t row_base, int64_t Nv, float* dY, float* rowloss, float* pred) {
-#define TABPACK_HEAD_FWD(DD) \
-  head_fwd_t<T, EVAL, DD>(grid, s, task, H, theta, mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, rowloss, pred)
+                int64_t row_base, int64_t Nv, float* dY, float* rowloss, float* pred, const int32_t* members) {
+#define TABPACK_HEAD_FWD(DD)                                                                                   \
+  head_fwd_t<T, EVAL, DD>(grid, s, task, H, theta, mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, \
+                          rowloss, pred, members)
   if (d_out <= 1) TABPACK_HEAD_FWD(1);
   else if (d_out <= 2) TABPACK_HEAD_FWD(2);
   else if (d_out <= 4) TABPACK_HEAD_FWD(4);
@@ -643,23 +647,24 @@ void head_fwd_d(int d_out, dim3 grid, hipStream_t s, Task task, const void* H, c
 hipError_t launch_head_fwd(Prec prec, Task task, bool eval, const void* H, const float* theta,
                            const MemberDev* mem, int K, int Bp, int d_out, const void* y,
                            const int32_t* idx, int B, int rows_valid, int64_t row_base, int64_t Nv,
-                           float* dY, float* rowloss, float* pred, hipStream_t s) {
+                           float* dY, float* rowloss, float* pred, const int32_t* members, hipStream_t s) {
   if (Bp % 32 != 0 || d_out < 1 || d_out > kMaxOut) return hipErrorInvalidValue;
+  if (K <= 0) return hipSuccess;
   const dim3 grid(Bp / 32, K);
   if (prec == Prec::BF16) {
     if (eval)
       head_fwd_d<__bf16, true>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
-                               rowloss, pred);
+                               rowloss, pred, members);
     else
       head_fwd_d<__bf16, false>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
-                                rowloss, pred);
+                                rowloss, pred, members);
   } else {
     if (eval)
       head_fwd_d<float, true>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
-                              rowloss, pred);
+                              rowloss, pred, members);
     else
       head_fwd_d<float, false>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
-                               rowloss, pred);
+                               rowloss, pred, members);
   }
   return hipGetLastError();
 }
@@ -683,9 +688,11 @@ void head_bwd_d(int d_out, int ntiles, hipStream_t s, const void* H, const float
 int head_bwd_cols(int d_out) { return d_out <= 4 ? 256 : 128; }
 
 hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const MemberDev* mem, int K,
-                              int Bp, int B, int d_out, float* grad, float* loss_out, hipStream_t s) {
+                              int Bp, int B, int d_out, float* grad, float* loss_out, const int32_t* members,
+                              hipStream_t s) {
+  if (K <= 0) return hipSuccess;
   hipLaunchKernelGGL(loss_reduce_kernel, dim3(K), dim3(256), 0, s, rowloss, dY, mem, Bp, B, d_out,
-                     grad, loss_out);
+                     grad, loss_out, members);
   return hipGetLastError();
 }
 
@@ -702,9 +709,10 @@ hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const M
 }
 
 hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int K, int max_dp, int Bp, int RB,
-                                   int d_out, float* grad, hipStream_t s) {
+                                   int d_out, float* grad, const int32_t* members, hipStream_t s) {
+  if (K <= 0) return hipSuccess;
   hipLaunchKernelGGL(head_grad_reduce_kernel, dim3((max_dp + 255) / 256, K), dim3(256), 0, s, part, mem, Bp, Bp / RB,
-                     d_out, grad);
+                     d_out, grad, members);
   return hipGetLastError();
 }
 

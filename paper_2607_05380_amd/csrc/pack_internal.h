@@ -113,14 +113,15 @@ hipError_t launch_gemm(Prec prec, OpKind a, OpKind b, EpiKind e, const GemmArgs&
 hipError_t launch_head_fwd(Prec prec, Task task, bool eval, const void* H, const float* theta,
                            const MemberDev* mem, int K, int Bp, int d_out, const void* y,
                            const int32_t* idx, int B, int rows_valid, int64_t row_base, int64_t Nv,
-                           float* dY, float* rowloss, float* pred, hipStream_t s);
+                           float* dY, float* rowloss, float* pred, const int32_t* members, hipStream_t s);
 hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const MemberDev* mem, int K,
-                              int Bp, int B, int d_out, float* grad, float* loss_out, hipStream_t s);
+                              int Bp, int B, int d_out, float* grad, float* loss_out, const int32_t* members,
+                              hipStream_t s);
 hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const MemberDev* mem,
                            const HeadTile* tiles, int ntiles, int Bp, int RB, int d_out, const float* dY,
                            void* dZ, float* part, hipStream_t s);
 hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int K, int max_dp, int Bp, int RB,
-                                   int d_out, float* grad, hipStream_t s);
+                                   int d_out, float* grad, const int32_t* members, hipStream_t s);
 int head_bwd_cols(int d_out);  // columns one head-backward block covers
 hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, const ColTile* tiles,
                                      int ntiles, int nparts, const int64_t* bias_off, float* grad,
