@@ -911,17 +911,22 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     HIP_TRY(keep_words(step, par));
     HIP_TRY(hipEventRecord(h->ev_keep[par], h->side));
   }
-  HIP_TRY(timed(h, "gather", 1, 0.0, (double)c.K * c.B * c.d_in * (4.0 + h->elt()), stream, [&] {
-    return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, c.K, h->Bp, h->b.H0, stream);
-  }));
-  HIP_TRY(hipStreamWaitEvent(stream, h->ev_keep[par], 0));
   const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
   const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
   const AdamConst ac{(float)c.beta1, (float)c.beta2, (float)c.eps, (float)bc1, (float)std::sqrt(bc2)};
-  // Each member group runs its whole chain -- forward GEMMs, head, loss,
-  // backward GEMMs with the fused optimizer -- on its own stream; the groups
-  // join before the bias/head AdamW.
+  // Each member group runs its whole chain -- gather, forward GEMMs, head,
+  // loss, backward GEMMs with the fused optimizer -- on its own stream; the
+  // groups join before the bias/head AdamW.
   HIP_TRY(split());
+  for (int hf = 0; hf < ng; ++hf) {
+    const hipStream_t s = hs[hf];
+    const int gk = h->member0[hf + 1] - h->member0[hf];
+    HIP_TRY(timed(h, "gather", 1, 0.0, (double)gk * c.B * c.d_in * (4.0 + h->elt()), s, [&] {
+      return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, gk, h->Bp, h->b.H0,
+                           h->b.d_members + h->member0[hf], s);
+    }));
+    HIP_TRY(hipStreamWaitEvent(s, h->ev_keep[par], 0));
+  }
   for (int l = 1; l <= c.L; ++l)
     for (int hf = 0; hf < ng; ++hf) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
   for (int hf = 0; hf < ng; ++hf) {
@@ -1006,7 +1011,8 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
   GemmArgs a = base_args(h);
   for (int64_t r0 = 0; r0 < Nv; r0 += h->Bp) {
     a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
-    HIP_TRY(launch_gather(h->prec, Xv, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, stream));
+    HIP_TRY(launch_gather(h->prec, Xv, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, nullptr,
+                          stream));
     for (int l = 1; l <= c.L; ++l) {
       for (int hf = 0; hf < (l == 1 ? 1 : h->ngroups); ++hf) {
         GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][hf][l - 1]);

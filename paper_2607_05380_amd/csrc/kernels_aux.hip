@@ -370,8 +370,9 @@ __global__ __launch_bounds__(64) void bias_from_partials_kernel(const float* par
 // r >= rows_valid are zero.  One wave per row, float4 reads.
 template <typename T>
 __global__ __launch_bounds__(256) void gather_kernel(const float* X, int d_in, int Pin, const int32_t* idx,
-                                                     int B, int64_t row_base, int rows_valid, int Bp, T* H0) {
-  const int k = blockIdx.y;
+                                                     int B, int64_t row_base, int rows_valid, int Bp, T* H0,
+                                                     const int32_t* members) {
+  const int k = members ? members[blockIdx.y] : (int)blockIdx.y;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (r >= Bp) return;
@@ -380,23 +381,34 @@ __global__ __launch_bounds__(256) void gather_kernel(const float* X, int d_in, i
   const int64_t src = valid ? (idx ? (int64_t)idx[(int64_t)k * B + r] : row_base + r) : 0;
   const float* x = X + src * d_in;
   const bool vec = (d_in % 4 == 0) && ((reinterpret_cast<uintptr_t>(X) & 15) == 0);
-  for (int c = lane * 4; c < Pin; c += 256) {
-    float v[4];
-    if (valid && vec && c + 4 <= d_in) {
-      const f32x4 q = *reinterpret_cast<const f32x4*>(x + c);
-      v[0] = q[0], v[1] = q[1], v[2] = q[2], v[3] = q[3];
-    } else {
+  // 1024 columns per round: the lane's four 16-byte loads are all issued
+  // before any store; X rows are read once, so the loads bypass the caches
+  for (int c0 = 0; c0 < Pin; c0 += 1024) {
+    float v[4][4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = (valid && c + e < d_in) ? x[c + e] : 0.0f;
+    for (int u = 0; u < 4; ++u) {
+      const int c = c0 + u * 256 + lane * 4;
+      if (valid && vec && c + 4 <= d_in) {
+        const f32x4 q = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(x + c));
+        v[u][0] = q[0], v[u][1] = q[1], v[u][2] = q[2], v[u][3] = q[3];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[u][e] = (valid && c + e < d_in) ? x[c + e] : 0.0f;
+      }
     }
-    if constexpr (sizeof(T) == 2) {
-      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[0]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[1]) << 16);
-      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[3]) << 16);
-      *reinterpret_cast<u32x2*>(dst + c) = u32x2{lo, hi};
-    } else {
-      *reinterpret_cast<f32x4*>(dst + c) = f32x4{v[0], v[1], v[2], v[3]};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = c0 + u * 256 + lane * 4;
+      if (c >= Pin) continue;
+      if constexpr (sizeof(T) == 2) {
+        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[u][0]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[u][1]) << 16);
+        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[u][2]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[u][3]) << 16);
+        *reinterpret_cast<u32x2*>(dst + c) = u32x2{lo, hi};
+      } else {
+        *reinterpret_cast<f32x4*>(dst + c) = f32x4{v[u][0], v[u][1], v[u][2], v[u][3]};
+      }
     }
   }
 }
@@ -726,14 +738,16 @@ hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, co
 }
 
 hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
-                         int64_t row_base, int rows_valid, int members, int Bp, void* H0, hipStream_t s) {
+                         int64_t row_base, int rows_valid, int members, int Bp, void* H0,
+                         const int32_t* member_ids, hipStream_t s) {
+  if (members <= 0) return hipSuccess;
   const dim3 grid((Bp + 3) / 4, members);
   if (prec == Prec::BF16)
     hipLaunchKernelGGL((gather_kernel<__bf16>), grid, dim3(256), 0, s, X, d_in, Pin, idx, B, row_base,
-                       rows_valid, Bp, static_cast<__bf16*>(H0));
+                       rows_valid, Bp, static_cast<__bf16*>(H0), member_ids);
   else
     hipLaunchKernelGGL((gather_kernel<float>), grid, dim3(256), 0, s, X, d_in, Pin, idx, B, row_base,
-                       rows_valid, Bp, static_cast<float*>(H0));
+                       rows_valid, Bp, static_cast<float*>(H0), member_ids);
   return hipGetLastError();
 }
 

@@ -127,7 +127,8 @@ hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, co
                                      int ntiles, int nparts, const int64_t* bias_off, float* grad,
                                      hipStream_t s);
 hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
-                         int64_t row_base, int rows_valid, int members, int Bp, void* H0, hipStream_t s);
+                         int64_t row_base, int rows_valid, int members, int Bp, void* H0,
+                         const int32_t* member_ids, hipStream_t s);
 hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, float* v,
                         uint16_t* shadow, const uint32_t* chunk_tab, const uint32_t* list,
                         const MemberDev* mem, int64_t nchunks, const AdamConst& ac, hipStream_t s);
