@@ -146,24 +146,32 @@ def main():
             pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
         stats = pk.profile_read()
         pk.profile(False)
-    for s in sorted(stats, key=lambda s: -s["total_ms"]):
-        log(f"  {s['name']:34s} launches {s['launches']:4d}  avg {s['avg_ms'] * 1e3:9.1f} us  "
-            f"total/step {s['total_ms'] / a.profile_steps:7.3f} ms  {s['flops'] / s['avg_ms'] / 1e9:8.1f} TFLOP/s "
-            f"{s['bytes'] / s['avg_ms'] / 1e6:8.1f} GB/s  [{s['kind']}]")
+    for s in sorted(stats, key=lambda s: -s["busy_ms"]):
+        log(f"  {s['name']:26s} launches {s['launches']:4d}  avg {s['avg_ms'] * 1e3:8.1f} us  "
+            f"busy/step {s['busy_ms'] / a.profile_steps:6.3f} ms  "
+            f"{s['flops'] * s['launches'] / s['busy_ms'] / 1e9:7.1f} TFLOP/s "
+            f"{s['bytes'] * s['launches'] / s['busy_ms'] / 1e6:7.1f} GB/s  [{s['kind']}]")
     roofline = None
     if stats:
-        dom = max(stats, key=lambda s: s["total_ms"])
+        # Launches of the concurrent member groups overlap, so the rate is the
+        # kernel's total work over its busy time (the union of its launches'
+        # intervals); the rate of one launch in isolation of the others is
+        # reported beside it.
+        dom = max(stats, key=lambda s: s["busy_ms"])
         if dom["kind"] == "mfma":
             peak = PEAK["mfma_bf16"] if cfg["precision"] == "bf16" else PEAK["mfma_fp32"]
             work, unit, scale = dom["flops"], "TFLOP/s", 1e12
         else:
             peak, work, unit, scale = PEAK["hbm"], dom["bytes"], "GB/s", 1e9
-        achieved = work / (dom["avg_ms"] / 1e3) / scale
+        achieved = work * dom["launches"] / (dom["busy_ms"] / 1e3) / scale
         roofline = {"bound": dom["kind"], "kernel": dom["name"], "achieved": round(achieved, 2), "peak": peak,
                     "unit": unit, "frac": round(achieved / peak, 4),
                     "traffic": measured_traffic(cfg["name"], dom["name"]),
-                    "avg_launch_us": round(dom["avg_ms"] * 1e3, 2), "work_per_launch": work,
-                    "flops_per_launch": dom["flops"], "bytes_per_launch": dom["bytes"]}
+                    "work_per_launch": work, "flops_per_launch": dom["flops"], "bytes_per_launch": dom["bytes"],
+                    "avg_launch_us": round(dom["avg_ms"] * 1e3, 2),
+                    "busy_us_per_step": round(dom["busy_ms"] * 1e3 / a.profile_steps, 2),
+                    "launches_per_step": dom["launches"] / a.profile_steps,
+                    "achieved_per_launch": round(work / (dom["avg_ms"] / 1e3) / scale, 2)}
     out = {
         "metric": METRIC, "value": round(msamples, 1), "unit": "member-samples/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
@@ -173,9 +181,10 @@ def main():
                    "task": cfg["task"], "keep_grads": int(a.keep_grads)},
         "roofline": roofline,
         "kernels": [{"name": s["name"], "bound": s["kind"], "avg_us": round(s["avg_ms"] * 1e3, 2),
-                     "per_step_ms": round(s["total_ms"] / a.profile_steps, 4), "flops_per_launch": s["flops"],
+                     "busy_ms_per_step": round(s["busy_ms"] / a.profile_steps, 4),
+                     "launches_per_step": s["launches"] / a.profile_steps, "flops_per_launch": s["flops"],
                      "bytes_per_launch": s["bytes"]}
-                    for s in sorted(stats, key=lambda s: -s["total_ms"])],
+                    for s in sorted(stats, key=lambda s: -s["busy_ms"])],
     }
     if not a.no_cpu_baseline:
         log("timing the fp64 oracle on the host (bounded sample)")

@@ -205,6 +205,8 @@ typedef struct pack_kernel_stat {
   double total_ms;
   double flops;      /* per launch */
   double bytes;      /* per launch */
+  double busy_ms;    /* time during which at least one of its launches ran (launches of concurrent
+                        member groups overlap, so this can be less than total_ms) */
 } pack_kernel_stat;
 
 int pack_profile_enable(pack_handle* h, int32_t enable);

@@ -1178,12 +1178,20 @@ int pack_profile_read(pack_handle* h, pack_kernel_stat* out, int32_t max, int32_
   if (!h || !n || (max > 0 && !out)) return fail(PACK_EINVAL, "NULL argument");
   std::vector<ProfGroup> g = h->groups;
   for (ProfGroup& x : g) x.launches = 0, x.total_ms = 0.0;
+  // launch intervals on a common time base (the first recorded event), to
+  // measure each kernel's busy time: the union of its launches' intervals,
+  // which differs from the summed durations when launches of concurrent
+  // member groups overlap
+  std::vector<std::vector<std::pair<double, double>>> iv(g.size());
   for (const TimedLaunch& t : h->timed) {
     HIP_TRY(hipEventSynchronize(t.stop));
-    float ms = 0.0f;
+    float ms = 0.0f, t0 = 0.0f, t1 = 0.0f;
     HIP_TRY(hipEventElapsedTime(&ms, t.start, t.stop));
+    HIP_TRY(hipEventElapsedTime(&t0, h->timed.front().start, t.start));
+    HIP_TRY(hipEventElapsedTime(&t1, h->timed.front().start, t.stop));
     g[t.group].launches += 1;
     g[t.group].total_ms += ms;
+    iv[t.group].push_back({t0, t1});
   }
   *n = (int32_t)g.size();
   for (int i = 0; i < (int)g.size() && i < max; ++i) {
@@ -1195,6 +1203,19 @@ int pack_profile_read(pack_handle* h, pack_kernel_stat* out, int32_t max, int32_
     s.total_ms = g[i].total_ms;
     s.flops = g[i].launches ? g[i].flops / g[i].launches : 0.0;
     s.bytes = g[i].launches ? g[i].bytes / g[i].launches : 0.0;
+    std::sort(iv[i].begin(), iv[i].end());
+    double busy = 0.0, a = 0.0, b = -1.0;
+    for (const auto& x : iv[i]) {
+      if (x.first > b) {
+        if (b > a) busy += b - a;
+        a = x.first;
+        b = x.second;
+      } else {
+        b = std::max(b, x.second);
+      }
+    }
+    if (b > a) busy += b - a;
+    s.busy_ms = busy;
   }
   return PACK_OK;
 }

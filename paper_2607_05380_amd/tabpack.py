@@ -48,7 +48,7 @@ class PackConfig(ctypes.Structure):
 class KernelStat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 64), ("kind", ctypes.c_int32), ("launches", ctypes.c_int32),
                 ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
-                ("bytes", ctypes.c_double)]
+                ("bytes", ctypes.c_double), ("busy_ms", ctypes.c_double)]
 
 
 class PackError(RuntimeError):
@@ -276,15 +276,15 @@ class Pack:
         _check(self.lib.pack_profile_enable(self.h, 1 if enable else 0))
 
     def profile_read(self):
-        """[{name, kind ('mfma'|'hbm'), launches, total_ms, avg_ms, flops, bytes (per launch)}]"""
+        """[{name, kind ('mfma'|'hbm'), launches, total_ms, avg_ms, busy_ms, flops, bytes (per launch)}]"""
         arr = (KernelStat * 64)()
         n = ctypes.c_int32()
         _check(self.lib.pack_profile_read(self.h, arr, 64, ctypes.byref(n)))
         out = []
         for s in arr[:n.value]:
             out.append(dict(name=s.name.decode(), kind="mfma" if s.kind == 0 else "hbm", launches=s.launches,
-                            total_ms=s.total_ms, avg_ms=s.total_ms / max(s.launches, 1), flops=s.flops,
-                            bytes=s.bytes))
+                            total_ms=s.total_ms, avg_ms=s.total_ms / max(s.launches, 1), busy_ms=s.busy_ms,
+                            flops=s.flops, bytes=s.bytes))
         return out
 
     def debug_activation(self, layer, k):
