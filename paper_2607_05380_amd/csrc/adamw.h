@@ -8,8 +8,13 @@
 
 namespace tabpack {
 
+// Contraction into fused multiply-adds is off: the optimizer runs inside
+// several kernels (the weight-gradient GEMM's epilogues of each tile shape and
+// the standalone kernel), and every one of them must round each operation the
+// same way for results not to depend on the tile shape.
 __device__ __forceinline__ void adamw_elem(float& th, float g, float& m, float& v, float decay, float step,
                                            const AdamConst& c) {
+#pragma clang fp contract(off)
   th *= decay;
   m = c.beta1 * m + (1.0f - c.beta1) * g;
   v = c.beta2 * v + (1.0f - c.beta2) * g * g;

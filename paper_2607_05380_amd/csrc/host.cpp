@@ -146,7 +146,7 @@ struct pack_handle {
   int nheadtiles = 0;
   int head_rb = 0;  // rows per head-backward block
   uint64_t t = 0;
-  bool small_tiles = true;  // plan every GEMM with 128x128 tiles only
+  TileSet tiles = TILES_SMALL;  // tile set of the bf16 GEMMs (fp32 GEMMs run small tiles only)
   // side stream for ALU-bound work that overlaps memory-bound kernels of the
   // caller's stream, joined back through events (created by pack_bind)
   hipStream_t side = nullptr;
@@ -317,7 +317,7 @@ int64_t member_span_end(const pack_handle* h, int k) {
 
 // Device-table sizes.
 struct Plan {
-  bool small_only = false;    // fp32 GEMMs run small tiles only
+  TileSet tile_set = TILES_SMALL;
   std::vector<GemmDesc> descs;
   std::vector<Tile> tiles;
   std::vector<int64_t> cost;  // planner's cost of each tile (depth x valid area)
@@ -331,24 +331,30 @@ struct Plan {
   int member0[kGroups + 1] = {};
 };
 
-// Tiles of one member's M x N output: big 256 x 256 tiles, except that a
-// remainder of at most 128 rows or columns is covered by a strip of small
-// 128 x 128 tiles (a larger remainder takes one more, partly filled, big tile).
+// Tiles of one member's M x N output.  Big set: 256 x 256 tiles, except that
+// a remainder of at most 128 rows or columns is covered by a strip of small
+// 128 x 128 tiles (a larger remainder takes one more, partly filled, big
+// tile).  Tall set: 256 x 128 tiles, rows as in the big set, the last column
+// tile partly filled.  Small set: 128 x 128 tiles only.
 void add_tiles(Plan& p, Launch& ln, int d, int M, int N, int kdepth) {
   auto big_end = [&](int E) {
-    if (p.small_only) return 0;
     const int r = E % kBigTile;
     return r == 0 ? E : (r > kSmallTile ? E - r + kBigTile : E - r);
   };
-  const int Mb = big_end(M), Nb = big_end(N);
+  const bool big = p.tile_set == TILES_BIG, tall = p.tile_set == TILES_TALL;
+  const int Mb = big || tall ? big_end(M) : 0;
+  const int Nb = big ? big_end(N) : (tall ? (int)round_up(N, kSmallTile) : 0);
+  const int tn = big ? kBigTile : kSmallTile;  // columns of the large tile
+  const int large = big ? kShapeBig : kShapeTall;
   auto push = [&](int m0, int n0, int shape) {
-    const int ts = shape == kShapeBig ? kBigTile : kSmallTile;
-    const int mb = std::min(ts, M - m0), nb = std::min(ts, N - n0);
+    const int tm = shape == kShapeSmall ? kSmallTile : kBigTile;
+    const int tw = shape == kShapeBig ? kBigTile : kSmallTile;
+    const int mb = std::min(tm, M - m0), nb = std::min(tw, N - n0);
     p.tiles.push_back(Tile{d, m0, n0, shape});
     p.cost.push_back((int64_t)kdepth * std::max(mb, 0) * std::max(nb, 0));
   };
   for (int m0 = 0; m0 < Mb; m0 += kBigTile)
-    for (int n0 = 0; n0 < Nb; n0 += kBigTile) push(m0, n0, kShapeBig);
+    for (int n0 = 0; n0 < Nb; n0 += tn) push(m0, n0, large);
   for (int m0 = 0; m0 < Mb; m0 += kSmallTile)
     for (int n0 = Nb; n0 < N; n0 += kSmallTile) push(m0, n0, kShapeSmall);
   for (int m0 = Mb; m0 < M; m0 += kSmallTile)
@@ -433,7 +439,7 @@ int head_rows(const pack_handle* h) { return h->Bp % 256 == 0 ? 256 : h->Bp; }
 
 Plan build_plan(const pack_handle* h, const Bufs& bf) {
   Plan p;
-  p.small_only = h->prec == Prec::FP32 || h->small_tiles;
+  p.tile_set = h->tiles;
   const pack_config& c = h->cfg;
   const size_t es = h->elt();
   const void* wsrc = h->prec == Prec::BF16 ? (const void*)bf.shadow : (const void*)bf.theta;
@@ -643,7 +649,7 @@ GemmArgs base_args(const pack_handle* h) {
   a.descs = h->b.d_descs;
   a.tiles = h->b.d_tiles;
   a.zeros = h->b.zeros;
-  a.small_only = (h->prec == Prec::FP32 || h->small_tiles) ? 1 : 0;
+  a.tile_set = h->tiles;
   const Key kd = stream_key(h->cfg.seed, kTagDropout);
   a.key0 = kd.k0;
   a.key1 = kd.k1;
@@ -718,9 +724,13 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
   h->task = (Task)cfg->task;
   h->q = cfg->quantum ? cfg->quantum : 32;
   // 128x128 tiles at two workgroups per CU measure faster on the packed
-  // workloads than 256x256 tiles at one; TABPACK_GEMM_TILES=big selects the latter
-  h->small_tiles = true;
-  if (const char* e = getenv("TABPACK_GEMM_TILES")) h->small_tiles = std::string(e) != "big";
+  // workloads than 256x256 tiles at one; TABPACK_GEMM_TILES=big|tall|small overrides
+  h->tiles = TILES_SMALL;
+  if (const char* e = getenv("TABPACK_GEMM_TILES")) {
+    const std::string v(e);
+    h->tiles = v == "big" ? TILES_BIG : (v == "tall" ? TILES_TALL : TILES_SMALL);
+  }
+  if (h->prec == Prec::FP32) h->tiles = TILES_SMALL;
   h->Bp = (int)round_up(cfg->B, kRowAlign);
   h->Pin = (int)round_up(cfg->d_in, 8);
   h->mem.resize(cfg->K);

@@ -6,38 +6,44 @@
 // without padding to the widest member (the paper's packing grows every member
 // to the maximum width and uses a batched matmul, Section 3.3).
 //
-// Workgroup: 256 threads = 4 wave64s in a 2 x 2 grid.  Two tile shapes share
-// one kernel (the shape is uniform per workgroup):
-//   big   256 x 256: each wave owns 128 x 128 = 4 x 4 MFMA 32x32 blocks.  Per K
-//         step of 16 a wave reads 8 KB of fragments from LDS for 16 MFMAs,
-//         64 B/clk per CU at the MFMA rate -- inside gfx950's LDS bandwidth
-//         (about 96 B/clk measured for 16-byte reads), which a 64 x 64 wave
-//         tile exceeds by 2x.
-//   small 128 x 128 (waves 64 x 64) covers the ragged edge of a member when
-//         its remainder is at most 128 rows or columns.
+// Workgroup: 256 threads = 4 wave64s in a 2 x 2 grid.  Tile shapes (uniform
+// per workgroup; one launch runs one tile set, chosen by the host):
+//   small 128 x 128: each wave owns 64 x 64 = 2 x 2 MFMA 32x32 blocks; 64 KB
+//         of LDS, two workgroups per CU.  The default for every GEMM.
+//   tall  256 x 128 (waves 128 x 64), two workgroups per CU, with small tiles
+//         on a member's row edge.
+//   big   256 x 256 (waves 128 x 128), one workgroup per CU, with small tiles
+//         on a member's edges.
+// The small tile is bound by the bytes in flight per CU rather than by LDS or
+// MFMA throughput: each workgroup has one 64-deep K step (32 KB) in flight
+// while it computes the previous one, against a direct-load latency of about
+// 1800 cycles.  Measured per 64-deep step and workgroup pair: about 1800
+// cycles for 1024 cycles of MFMA per SIMD.
 // MFMA: v_mfma_f32_32x32x16_bf16 (fp32 mode: v_mfma_f32_32x32x2_f32), fp32
-// accumulators in AGPRs.  A wave whose sub-tile lies wholly outside the
-// member's extents skips its MFMAs.
+// accumulators.  A wave whose sub-tile lies wholly outside the member's
+// extents skips its MFMAs.
 //
-// Staging: per K step (128 bytes of depth per row: 64 bf16 / 32 fp32) each
-// operand tile goes HBM -> LDS, double-buffered with one barrier per step; the
-// loads of step k + 1 are in flight during the MFMAs of step k.  bf16 uses
-// direct-to-LDS loads (global_load_lds_dwordx4, no staging registers, which
-// the 256 accumulator registers of a big tile leave no room for); fp32 stages
-// through registers with raw buffer loads and runs small tiles only.
+// Staging: per K step each operand tile goes HBM -> LDS in NS stages with one
+// barrier per step; the loads of the next steps are in flight during the MFMAs
+// of the current one.  bf16 uses direct-to-LDS loads (global_load_lds_dwordx4,
+// no staging registers); fp32 stages through registers with raw buffer loads
+// and runs small tiles only.  Inside a K step a wave reads the fragments of
+// 16-deep step ks + 2 while the MFMAs of step ks run.
 // LDS layouts:
-//   depth-contiguous operands (element (r, k) at P[r * ld + k]), bf16: 4 planes
-//     (one per 16-deep MFMA step) of [row][32 B], the halves of row r swapped
-//     when bit 2 of r is set; fragments are 16-byte reads (8 consecutive rows
-//     conflict-free).  fp32: [row][8 x 16 B], vector s of row r in slot
-//     s ^ (r & 7) ^ ((r >> 3) & 7).
+//   depth-contiguous operands (element (r, k) at P[r * ld + k]), bf16:
+//     row-major, the 16-byte chunks of a row XOR-swizzled by row (see
+//     kmaj16_off); fragments are conflict-free 16-byte reads and each quad of
+//     a direct load reads one aligned 64-byte piece of one row.
+//     fp32: [row][8 x 16 B], vector s of row r in slot s ^ (r & 7) ^ ((r >> 3) & 7).
 //   rows-contiguous operands (element (r, k) at P[k * ld + r]), bf16: stored as
 //     loaded, [depth row][R], the 32-byte chunk c of depth row k at c ^ 2(k & 3);
 //     fragments come from two ds_read_b64_tr_b16 each.  Within a 16-lane group
 //     that instruction hands lane i the element i % 4 of the 8 bytes addressed
 //     by lane 4j + i / 4 as its j-th value, so lane (s, group g) addressing
 //     depth row 8h + s/4 (+4) at rows 16(g & 1) + 4(s & 3) receives rows
-//     16(g & 1) + s at depths 8h..8h+3 (+4) -- exactly an MFMA operand.
+//     16(g & 1) + s at depths 8h..8h+3 (+4) -- exactly an MFMA operand.  These
+//     8-byte reads run at half the byte rate of 16-byte reads (measured
+//     ~130 vs ~255 B/clk per CU).
 //   rows-contiguous operands, fp32: transposed in registers into the first layout.
 //
 // Fused epilogues:
@@ -45,7 +51,9 @@
 //   EPI_FWD_EVAL  bias + ReLU -> H
 //   EPI_DX        dH * [H_prev > 0] * s_k -> dZ_prev, plus column sums of the
 //                 unrounded values per 64-row block (bias-gradient partials)
-//   EPI_DW        fp32 store of the weight-gradient tile
+//   EPI_DW        fp32 store of the weight-gradient tile, or AdamW applied to
+//                 the weights it covers (small tiles: the whole tile staged in
+//                 LDS and streamed by the workgroup)
 // Every output element is owned by exactly one workgroup and reduced over the
 // full depth in a fixed order: no atomics, bit-reproducible.
 #include <algorithm>
@@ -78,6 +86,19 @@ constexpr int kSmallKs = TABPACK_SMALL_KS, kSmallNs = TABPACK_SMALL_NS;
 constexpr int kLdsSmallBf16 = kSmallNs * 2 * 128 * 32 * kSmallKs;
 constexpr int kLdsSmall = kLdsSmallBf16 > 2 * 2 * 128 * ROW ? kLdsSmallBf16 : 2 * 2 * 128 * ROW;
 constexpr int kSmallWpe = kLdsSmall <= 80 * 1024 ? 2 : 1;  // workgroups (waves per SIMD) that fit per CU
+// Tall-tile bf16 pipeline: kTallNs stages of kTallKs 16-deep steps of the
+// 256-row and 128-row operand tiles; the small edge tiles of the same launch
+// keep the small pipeline.  Both must fit two workgroups per CU.
+#ifndef TABPACK_TALL_KS
+#define TABPACK_TALL_KS 2
+#endif
+#ifndef TABPACK_TALL_NS
+#define TABPACK_TALL_NS 3
+#endif
+constexpr int kTallKs = TABPACK_TALL_KS, kTallNs = TABPACK_TALL_NS;
+constexpr int kLdsTallBf16 = kTallNs * (256 + 128) * 32 * kTallKs;
+constexpr int kLdsTall = kLdsTallBf16 > kLdsSmallBf16 ? kLdsTallBf16 : kLdsSmallBf16;
+static_assert(kLdsTall <= 80 * 1024, "two tall-tile workgroups per CU");
 
 template <int SH>
 struct Shape;
@@ -89,6 +110,11 @@ struct Shape<kShapeBig> {
 template <>
 struct Shape<kShapeSmall> {
   static constexpr int MB = 2, NB = 2, TM = 128, TN = 128;
+  static constexpr int STAGE = 32 * (NB * 128 + 32);
+};
+template <>
+struct Shape<kShapeTall> {
+  static constexpr int MB = 4, NB = 2, TM = 256, TN = 128;
   static constexpr int STAGE = 32 * (NB * 128 + 32);
 };
 
@@ -109,18 +135,21 @@ __device__ __forceinline__ int kmaj_off(int row, int slot) {
 }
 
 // depth-contiguous bf16 layout used with direct-to-LDS loads, for K steps of
-// KS 16-deep MFMA steps: 1 KB blocks of BR = 32/KS rows; inside a block, KS
-// planes (one per 16-deep step) of BR rows x 32 bytes.  The two 16-byte halves
-// of a row's plane slice are swapped when bit 2 xor bit 3 of the row is set,
-// which keeps the 16-byte fragment reads of 8 (and of 16) consecutive rows on
-// distinct banks.  A block is exactly BR full row segments of HBM (32*KS bytes
-// each), so one 64-lane direct load fills it with whole segments, and every
-// fragment address is a per-lane base plus compile-time offsets.
-__device__ __forceinline__ int kmaj_sw(int row) { return ((row >> 2) ^ (row >> 3)) & 1; }
+// KS 16-deep MFMA steps: row-major, 32*KS bytes (CPR = 2*KS 16-byte chunks) of
+// depth per row, chunk c of row r stored at chunk position c ^ f(r) with
+// f(r) = (r / (16/CPR)) % CPR.  The 16 rows read by a quarter-wave's 16-byte
+// fragment loads then cover all 64 banks, and each quad of lanes of a direct
+// load fills one aligned 64-byte piece of one row, i.e. it reads one aligned
+// 64-byte piece of one global row (in permuted order): one cache-line lookup
+// per quad.
 template <int KS>
-__device__ __forceinline__ int kmaj16_off(int row, int ks, int h) {
-  constexpr int BR = 32 / KS;
-  return (row / BR) * 1024 + ks * (BR * 32) + (row % BR) * 32 + ((h ^ kmaj_sw(row)) << 4);
+__device__ __forceinline__ int kmaj_f(int row) {
+  constexpr int CPR = 2 * KS;
+  return (row / (16 / CPR)) & (CPR - 1);
+}
+template <int KS>
+__device__ __forceinline__ int kmaj16_off(int row, int c) {
+  return row * (32 * KS) + ((c ^ kmaj_f<KS>(row)) << 4);
 }
 
 // rows-contiguous bf16 layout (R rows): byte offset of element `col` of depth row k
@@ -141,6 +170,24 @@ __device__ __forceinline__ __bf16 from_float<__bf16>(float f) {
 template <>
 __device__ __forceinline__ float from_float<float>(float f) {
   return f;
+}
+
+// ------------------------------------------------------------------ waits --
+// vmcnt <= N, every other counter at its maximum (gfx9 s_waitcnt encoding),
+// plus lgkmcnt(0) when LDS is set.
+template <int N, bool LDS>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((LDS ? 0 : 15) << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without a memory fence: the waits that make data visible
+// are explicit around it, and the empty asm statements keep the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void bar() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // ---------------------------------------------------------------- loaders --
@@ -253,14 +300,16 @@ __device__ __forceinline__ void dma16(const void* src, char* lds) {
   __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)lds, 16, 0, 0);
 }
 
-// Depth-contiguous bf16 operand -> blocked depth-contiguous LDS layout.  Wave w
-// fills blocks w*PER .. w*PER+PER-1 (BR rows each); lane i fetches the 16 bytes
-// of plane i/(2 BR) of row (i/2)%BR that belong at LDS position 16*i, i.e.
-// logical half (i&1) ^ sw(row).  For BR = 8, sw(row) depends on the block's
-// parity, so a lane keeps one source offset per parity.
+// Depth-contiguous bf16 operand -> swizzled row-major LDS layout.  Each
+// instruction fills BR = 32/KS whole rows (1 KB); wave w issues blocks
+// w*PER .. w*PER+PER-1.  Lane i lands at row (i / CPR) of the block, chunk
+// position i % CPR, so it fetches the row's chunk (i % CPR) ^ f(row).  f of a
+// block's rows depends only on the block's parity, so a lane keeps one source
+// offset per parity.
 template <int R, int KS>
 struct DmaKmaj {
-  static constexpr int BR = 32 / KS;           // rows per 1 KB block
+  static constexpr int CPR = 2 * KS;           // 16-byte chunks per row
+  static constexpr int BR = 64 / CPR;          // rows per 1 KB block
   static constexpr int PER = R / BR / 4;       // blocks per wave
   static_assert(PER % 2 == 0, "block parity follows p");
   const char* base;
@@ -275,12 +324,12 @@ struct DmaKmaj {
     base = reinterpret_cast<const char*>(P);
     zeros = z;
     wave = wave_;
-    const int r = (lane >> 1) % BR, ks = lane / (2 * BR);
+    const int r = lane / CPR;
 #pragma unroll
     for (int par = 0; par < 2; ++par) {
       const int row = (wave * PER + par) * BR + r;  // PER is even: parity of p = parity of the block
-      const int h = (lane & 1) ^ kmaj_sw(row);
-      kofs[par] = ks * 16 + h * 8;
+      const int c = (lane % CPR) ^ kmaj_f<KS>(row);
+      kofs[par] = c * 8;
       off[par] = (uint32_t)(((int64_t)(row0 + row) * ld + kofs[par]) * 2);
     }
     bstep = (uint32_t)(2 * BR * ld * 2);
@@ -380,9 +429,32 @@ __device__ __forceinline__ bf16x8 frag_tr(const char* lds, int row_block, int ks
   return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], b[0], b[1]});
 }
 
+// The same fragment through inline assembly.  The compiler cannot prove that
+// a transposing read of one stage does not alias the direct-to-LDS loads just
+// issued into the other, and would wait for those loads before every read;
+// through assembly the read is invisible to it, so the caller waits for the
+// result itself (an explicit lgkmcnt before the first use).
+template <int R>
+__device__ __forceinline__ u32x2 ds_tr16_b64(const char* p) {
+  typedef __attribute__((address_space(3))) const char* lds_cptr;
+  const uint32_t a = (uint32_t)(uintptr_t)(lds_cptr)p;
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(a));
+  return r;
+}
+template <int R>
+__device__ __forceinline__ bf16x8 frag_tr_asm(const char* lds, int row_block, int ks, int lane) {
+  const int s = lane & 15, g = lane >> 4;
+  const int k = 16 * ks + 8 * (g >> 1) + (s >> 2);
+  const int col = row_block + 16 * (g & 1) + 4 * (s & 3);
+  const u32x2 a = ds_tr16_b64<R>(lds + rmaj_off<R>(k, col));
+  const u32x2 b = ds_tr16_b64<R>(lds + rmaj_off<R>(k + 4, col));
+  return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], b[0], b[1]});
+}
+
 template <int KS>
 __device__ __forceinline__ bf16x8 frag_kmaj_bf16(const char* lds, int row_block, int ks, int lane) {
-  return *reinterpret_cast<const bf16x8*>(lds + kmaj16_off<KS>(row_block + (lane & 31), ks, lane >> 5));
+  return *reinterpret_cast<const bf16x8*>(lds + kmaj16_off<KS>(row_block + (lane & 31), 2 * ks + (lane >> 5)));
 }
 
 template <bool TR, int R, int KS>
@@ -402,24 +474,61 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
                                          f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn,
                                          int lane) {
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM, TN = Shape<SH>::TN;
-  if constexpr (sizeof(T) == 2 && SH == kShapeSmall) {
-    // Small tiles: every fragment of the K step is read up front (16 VGPRs per
-    // 16-deep step), so the MFMAs only wait for the LDS reads they use.
+  if constexpr (sizeof(T) == 2 && SH != kShapeBig) {
+    // Small and tall tiles: the fragments of 16-deep step ks + 2 are read
+    // while the MFMAs of step ks run.  The scheduling barriers pin that order
+    // (left alone, the scheduler reuses one set of fragment registers and
+    // waits for the LDS before every 16-deep step).  Transposing reads go
+    // through assembly, so the wait for a step's fragments is explicit: every
+    // LDS read issued after them may still be in flight.
+    constexpr int NRD = (TRA ? 2 * MB : MB) + (TRB ? 2 * NB : NB);  // LDS reads per 16-deep step
     bf16x8 a[KS][MB], b[KS][NB];
+    auto rd = [&](int ks) {
+#pragma unroll
+      for (int i = 0; i < MB; ++i) {
+        if constexpr (TRA)
+          a[ks][i] = frag_tr_asm<TM>(As, wm * MB * 32 + i * 32, ks, lane);
+        else
+          a[ks][i] = frag_kmaj_bf16<KS>(As, wm * MB * 32 + i * 32, ks, lane);
+      }
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        if constexpr (TRB)
+          b[ks][j] = frag_tr_asm<TN>(Bs, wn * NB * 32 + j * 32, ks, lane);
+        else
+          b[ks][j] = frag_kmaj_bf16<KS>(Bs, wn * NB * 32 + j * 32, ks, lane);
+      }
+    };
+    rd(0);
+    if constexpr (KS > 1) rd(1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int i = 0; i < MB; ++i) a[ks][i] = frag_bf16<TRA, TM, KS>(As, wm * MB * 32 + i * 32, ks, lane);
-#pragma unroll
-      for (int j = 0; j < NB; ++j) b[ks][j] = frag_bf16<TRB, TN, KS>(Bs, wn * NB * 32 + j * 32, ks, lane);
-    }
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+      if (ks + 2 < KS) rd(ks + 2);
+      if constexpr (TRA || TRB) {
+        const int later = (ks + 1 < KS ? NRD : 0) + (ks + 2 < KS ? NRD : 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (later >= 15)
+          __builtin_amdgcn_s_waitcnt(0xcf7f);  // lgkmcnt(15)
+        else if (later >= 12)
+          __builtin_amdgcn_s_waitcnt(0xcc7f);  // lgkmcnt(12)
+        else if (later >= 8)
+          __builtin_amdgcn_s_waitcnt(0xc87f);  // lgkmcnt(8)
+        else if (later >= 6)
+          __builtin_amdgcn_s_waitcnt(0xc67f);  // lgkmcnt(6)
+        else if (later >= 4)
+          __builtin_amdgcn_s_waitcnt(0xc47f);  // lgkmcnt(4)
+        else
+          __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < MB; ++i)
 #pragma unroll
         for (int j = 0; j < NB; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][i], b[ks][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   } else if constexpr (sizeof(T) == 2) {
     // Big tiles: fragments of the next 16-deep step are read while the MFMAs
     // of this one run; the loop stays rolled (a full unroll hoists every step's
@@ -535,14 +644,14 @@ __device__ __forceinline__ void stage_flush(const char* stage, OT* C, int64_t ld
 // moments, the bf16 shadow); the gradient itself is stored only on request.
 // The optimizer state of all the lane's vectors is loaded before any update so
 // the loads' latencies overlap.
-template <int NB>
+template <int NB, int MB>
 __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmDesc& d, const char* stage, int row0,
                                                   int col0, int lane) {
   using S = Stage<float, NB>;
   // vectors whose optimizer state is loaded before any of them is updated:
-  // all of the lane's 8 for the small tile, 4 at a time beside the big tile's
-  // 256 accumulators
-  constexpr int G = NB == 2 ? S::PER_LANE : 4;
+  // all of the lane's 8 beside the small tile's 64 accumulators, 4 at a time
+  // beside the 128 or 256 of the tall and big tiles
+  constexpr int G = MB * NB <= 4 ? S::PER_LANE : 4;
   static_assert(S::PER_LANE % G == 0, "whole groups");
   const AdamConst ac{a.beta1, a.beta2, a.eps, a.bc1, a.bc2_sqrt};
   const float decay = 1.0f - d.lr * d.wd;
@@ -580,6 +689,84 @@ __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmD
         const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][2]) |
                             ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)th[u][3]) << 16);
         *reinterpret_cast<u32x2*>(a.shadow + d.poff + e[u]) = u32x2{lo, hi};
+      }
+    }
+  }
+}
+
+// Weight-gradient tile of the small shape with the optimizer fused, done by
+// the whole workgroup: the 128 x 128 fp32 gradient tile is staged in LDS (it
+// fills the 64 KB the operand stages used), then the 256 threads stream the
+// optimizer over it in row-contiguous 16-byte vectors, 16 per thread, with the
+// optimizer state of kAdamAhead vectors in flight ahead of the one being
+// updated, so the update of one vector never waits for the stores of the one
+// before.  LDS layout: element (r, c) at r * 512 + 16 ((c / 4) ^ 8 ((r / 4) & 1))
+// + 4 (c % 4): the two half-waves of an accumulator write (rows 4 apart) fall
+// on disjoint banks, and each 16-byte vector stays contiguous.
+constexpr int kAdamAhead = 4;
+__device__ __forceinline__ int dwt_off(int r, int c) {
+  return r * 512 + ((((c >> 2) ^ (((r >> 2) & 1) << 3))) << 4) + ((c & 3) << 2);
+}
+
+__device__ __forceinline__ void dw_adamw_small(const GemmArgs& a, const GemmDesc& d, const Tile& t,
+                                               f32x16 (&acc)[2][2], int wm, int wn, int lane, int tid, char* lds0) {
+  const int hv = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm * 64 + 32 * i + 8 * (r >> 2) + 4 * hv + (r & 3);
+        const int col = wn * 64 + 32 * j + (lane & 31);
+        *reinterpret_cast<float*>(lds0 + dwt_off(row, col)) = acc[i][j][r];
+      }
+  wait_vm<63, true>();  // this wave's LDS writes are done
+  bar();
+  const AdamConst ac{a.beta1, a.beta2, a.eps, a.bc1, a.bc2_sqrt};
+  const float decay = 1.0f - d.lr * d.wd;
+  const float step = d.lr / a.bc1;
+  const int mrows = min(d.M - t.m0, 128), ncols = min(d.N - t.n0, 128);
+  // vector u of this thread: row 8 u + tid / 32, columns 4 (tid % 32) .. +3
+  const int r0 = tid >> 5, c = (tid & 31) * 4;
+  const bool colok = c < ncols;
+  const int64_t e0 = (int64_t)(t.m0 + r0) * d.ldc + t.n0 + c;  // element offset of vector 0
+  const int64_t estep = 8 * d.ldc;
+  float* th_p = a.theta + d.poff;
+  float* m_p = a.am + d.poff;
+  float* v_p = a.av + d.poff;
+  f32x4 th[kAdamAhead], m[kAdamAhead], vv[kAdamAhead];
+  auto ok = [&](int u) { return colok && 8 * u + r0 < mrows; };
+  auto load = [&](int u) {
+    const int64_t e = e0 + u * estep;
+    if (ok(u)) {
+      th[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(th_p + e));
+      m[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(m_p + e));
+      vv[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(v_p + e));
+    }
+  };
+#pragma unroll
+  for (int u = 0; u < kAdamAhead; ++u) load(u);
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int b = u % kAdamAhead;
+    const int64_t e = e0 + u * estep;
+    const bool in = ok(u);
+    f32x4 g = *reinterpret_cast<const f32x4*>(lds0 + dwt_off(8 * u + r0, c));
+    f32x4 t_ = th[b], m_ = m[b], v_ = vv[b];
+    if (u + kAdamAhead < 16) load(u + kAdamAhead);
+    if (in) {
+      if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e) = g;
+      adamw_vec4(t_, g, m_, v_, decay, step, ac);
+      __builtin_nontemporal_store(t_, reinterpret_cast<f32x4*>(th_p + e));
+      __builtin_nontemporal_store(m_, reinterpret_cast<f32x4*>(m_p + e));
+      __builtin_nontemporal_store(v_, reinterpret_cast<f32x4*>(v_p + e));
+      if (a.shadow) {
+        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[0]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[1]) << 16);
+        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[2]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[3]) << 16);
+        *reinterpret_cast<u32x2*>(a.shadow + d.poff + e) = u32x2{lo, hi};
       }
     }
   }
@@ -650,7 +837,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
               stage_put<float, NB>(stage, j, g, q, lane, acc[i][j][4 * (p * S::GP + g) + q]);
         wave_sync_lds();
         if (a.theta)
-          stage_flush_adamw<NB>(a, d, stage, row0 + 32 * i + S::ROWS * p, col0, lane);
+          stage_flush_adamw<NB, MB>(a, d, stage, row0 + 32 * i + S::ROWS * p, col0, lane);
         else
           stage_flush<float, NB>(stage, C, d.ldc, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
         wave_sync_lds();
@@ -751,23 +938,6 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
 }
 
 // ------------------------------------------------------------------- tile --
-// vmcnt <= N, every other counter at its maximum (gfx9 s_waitcnt encoding),
-// plus lgkmcnt(0) when LDS is set.
-template <int N, bool LDS>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((LDS ? 0 : 15) << 8) | ((N >> 4) << 14));
-}
-
-// Workgroup barrier without a memory fence: the waits that make data visible
-// are explicit around it, and the empty asm statements keep the compiler from
-// moving memory accesses across it.
-__device__ __forceinline__ void bar() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
 // Waits until at most `newer` K steps (of PS direct loads per wave each) are
 // still in flight and this wave's LDS reads are done.
 template <int PS, int NS>
@@ -872,6 +1042,12 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
       __syncthreads();
     }
   }
+  if constexpr (EPI == EPI_DW && SH == kShapeSmall && sizeof(T) == 2) {
+    if (a.theta) {  // uniform: the whole workgroup takes the staged-tile path
+      dw_adamw_small(a, d, t, acc, wm, wn, lane, tid, lds0);
+      return;
+    }
+  }
   epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * Shape<SH>::STAGE, pre);
 }
 
@@ -893,8 +1069,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 }
 
 // Launches of small tiles only: 64 KB of LDS, two workgroups per CU, so one
-// workgroup's epilogue overlaps the other's MFMA loop.  bf16: four stages of
-// 32-deep K steps (three in flight); fp32: two register-staged stages.
+// workgroup's epilogue overlaps the other's MFMA loop.  bf16: kSmallNs stages
+// of kSmallKs 16-deep steps; fp32: two register-staged stages.
 template <typename T, int AK, int BK_, int EPI>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSmallWpe, kSmallWpe))) void gemm_kernel_small(
     GemmArgs a) {
@@ -909,16 +1085,42 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSmallWpe, k
     run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave);
 }
 
+// Launches of tall tiles (256 x 128) with small edge tiles, bf16 only: two
+// workgroups per CU, each with kTallNs stages of the tall pipeline.
+template <int AK, int BK_, int EPI>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_kernel_tall(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[kLdsTall];
+  const Tile t = a.tiles[blockIdx.x];
+  const GemmDesc d = a.descs[t.desc];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  if (t.shape == kShapeTall) {
+    run_tile<__bf16, AK, BK_, EPI, kShapeTall, kTallKs, kTallNs>(a, d, t, smem, tid, wave);
+    return;
+  }
+  run_tile<__bf16, AK, BK_, EPI, kShapeSmall, kSmallKs, kSmallNs>(a, d, t, smem, tid, wave);
+}
+
 template <typename T, int AK, int BK_, int EPI>
 hipError_t launch_t(const GemmArgs& args, hipStream_t s) {
   if (args.ntiles <= 0) return hipSuccess;
   if constexpr (sizeof(T) == 4) {  // fp32 operands: small tiles only
+    if (args.tile_set != TILES_SMALL) return hipErrorInvalidValue;
     hipLaunchKernelGGL((gemm_kernel_small<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
   } else {
-    if (args.small_only)
-      hipLaunchKernelGGL((gemm_kernel_small<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
-    else
-      hipLaunchKernelGGL((gemm_kernel<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+    switch (args.tile_set) {
+      case TILES_SMALL:
+        hipLaunchKernelGGL((gemm_kernel_small<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+        break;
+      case TILES_TALL:
+        hipLaunchKernelGGL((gemm_kernel_tall<AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+        break;
+      case TILES_BIG:
+        hipLaunchKernelGGL((gemm_kernel<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+        break;
+      default:
+        return hipErrorInvalidValue;
+    }
   }
   return hipGetLastError();
 }

@@ -13,10 +13,14 @@ constexpr int kMaxOut = 16;        // largest head width d_out supported by the 
 constexpr int kRowAlign = 256;     // base-batch rows are padded to a multiple of this (largest GEMM row tile)
 constexpr uint32_t kTagDropout = 3;
 
-// Grouped-GEMM output tiles: big 256 x 256 (4 waves of 128 x 128) and small
-// 128 x 128 (4 waves of 64 x 64) for the ragged edges of a member.
-constexpr int kShapeBig = 0, kShapeSmall = 1;
+// Grouped-GEMM output tiles: big 256 x 256 (4 waves of 128 x 128), tall
+// 256 x 128 (4 waves of 128 x 64) and small 128 x 128 (4 waves of 64 x 64).
+constexpr int kShapeBig = 0, kShapeSmall = 1, kShapeTall = 2;
 constexpr int kBigTile = 256, kSmallTile = 128;
+// Tile sets of one launch (one kernel each): big tiles with small edge strips
+// (one workgroup per CU), small tiles only, or tall tiles with small edge
+// strips (two workgroups per CU each).
+enum TileSet : int { TILES_BIG = 0, TILES_SMALL = 1, TILES_TALL = 2 };
 constexpr int kPartRows = 64;   // rows per bias-gradient partial written by the dX epilogue
 constexpr int kXcds = 8;        // MI355X: workgroups go round-robin to 8 XCDs
 static_assert(kRowAlign % kBigTile == 0, "row padding must cover whole GEMM row tiles");
@@ -68,7 +72,7 @@ struct GemmArgs {
   uint32_t key0, key1;  // dropout stream key
   uint32_t step;        // dropout counter word
   const void* zeros;    // >= 16 bytes of zeros in device memory (source for out-of-range elements)
-  int32_t small_only;   // every tile has the small shape (selects the two-workgroups-per-CU kernel)
+  int32_t tile_set;     // TileSet of the launch's tiles (selects the kernel)
   // EPI_DW only: when theta is set the epilogue applies AdamW to the weight
   // elements it produces (theta, m, v and the bf16 shadow at desc.poff + the
   // element's index) and stores the gradient itself only if keep_grad is set.

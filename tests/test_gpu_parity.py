@@ -179,6 +179,35 @@ def test_fused_update_without_stored_grads_is_identical():
                 np.testing.assert_array_equal(b1, b2)
 
 
+def test_tile_sets_and_streams_are_bit_identical(monkeypatch):
+    # every GEMM output element is reduced over the full depth in one fixed
+    # order whatever the tile shape or the split of members over streams, so
+    # all tile sets and stream counts must give bit-identical training steps
+    cfg = configs.workload("regression_large", K=6, B=600)
+    members = [dict(width=w, dropout=p, lr=2e-3, wd=1e-3)
+               for w, p in ((96, 0.1), (200, 0.0), (257, 0.3), (384, 0.2), (520, 0.4), (1000, 0.1))]
+    Xtr, ytr, _, _, orders, idx = make_inputs(cfg, 3000, 10)
+    X, y, idx_d = to_dev(Xtr, ytr, idx)
+    runs = {}
+    for tiles, streams in (("small", "3"), ("tall", "3"), ("big", "1"), ("small", "1"), ("small", "4")):
+        monkeypatch.setenv("TABPACK_GEMM_TILES", tiles)
+        monkeypatch.setenv("TABPACK_STREAMS", streams)
+        pk = tabpack.Pack(cfg, members=members).bind()
+        losses = [pk.train_step(X, y, idx_d, s).cpu().numpy() for s in (1, 2)]
+        runs[(tiles, streams)] = (losses, [(pk.get_params(k), pk.get_moments(k)) for k in range(cfg["K"])])
+    ref_losses, ref = runs[("small", "3")]
+    for key, (losses, got) in runs.items():
+        for a, b in zip(ref_losses, losses):
+            np.testing.assert_array_equal(a, b, err_msg=str(key))
+        for (p1, m1), (p2, m2) in zip(ref, got):
+            for (W1, b1), (W2, b2) in zip(p1, p2):
+                np.testing.assert_array_equal(W1, W2, err_msg=str(key))
+                np.testing.assert_array_equal(b1, b2, err_msg=str(key))
+            for x1, x2 in zip(m1, m2):
+                for (W1, b1), (W2, b2) in zip(x1, x2):
+                    np.testing.assert_array_equal(W1, W2, err_msg=str(key))
+
+
 def test_k1_pack_equals_standalone_member():
     # one-member pack vs the oracle's standalone MLP with the same hyperparameters
     cfg = configs.workload("binary_small", K=1)
