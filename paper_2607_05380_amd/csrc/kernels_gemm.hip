@@ -288,63 +288,61 @@ struct LoadRmajF32 {
   }
 };
 
-// Direct-to-LDS loaders (bf16): global_load_lds_dwordx4 writes lane i's 16
+// Direct-to-LDS loaders (bf16): buffer_load_dwordx4 ... lds writes lane i's 16
 // bytes at the instruction's LDS base + 16 i, so each wave fills whole 1 KB
 // chunks of the LDS tile and every lane fetches the global vector that belongs
 // at its position in the swizzled layout.  Nothing is staged in registers.
-// Elements outside the operand are fetched from a block of zeros.
-typedef const void __attribute__((address_space(1)))* gptr_t;
+// A lane's byte offset (the per-lane part of the address) is fixed for the
+// whole tile; the K position moves in the scalar offset, so a K step costs no
+// vector instructions.  A lane whose row lies outside the operand has an
+// offset past the buffer's range and reads zeros; depth beyond K can only
+// occur in the last K step, which checks it per lane.
 typedef void __attribute__((address_space(3)))* lptr_t;
 
-__device__ __forceinline__ void dma16(const void* src, char* lds) {
-  __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)lds, 16, 0, 0);
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lptr_t)lds, 16, voff, soff, 0, 0);
 }
 
 // Depth-contiguous bf16 operand -> swizzled row-major LDS layout.  Each
 // instruction fills BR = 32/KS whole rows (1 KB); wave w issues blocks
 // w*PER .. w*PER+PER-1.  Lane i lands at row (i / CPR) of the block, chunk
 // position i % CPR, so it fetches the row's chunk (i % CPR) ^ f(row).  f of a
-// block's rows depends only on the block's parity, so a lane keeps one source
-// offset per parity.
+// block's rows depends only on the block's parity.
 template <int R, int KS>
 struct DmaKmaj {
   static constexpr int CPR = 2 * KS;           // 16-byte chunks per row
   static constexpr int BR = 64 / CPR;          // rows per 1 KB block
   static constexpr int PER = R / BR / 4;       // blocks per wave
   static_assert(PER % 2 == 0, "block parity follows p");
-  const char* base;
-  const void* zeros;
-  uint32_t off[2];     // byte offset (depth 0) of this lane's vector in block 0 / 1
-  uint32_t bstep;      // bytes between the rows of blocks 2 apart
+  __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t voff[PER];  // byte offset (depth 0) of this lane's vector in block p, or kOob
   int kofs[2];         // depth offset (elements) of this lane's vector per block parity
-  uint32_t okmask;     // bit p: this lane's row of block p exists
   int wave;
-  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int, int wave_, int lane,
-                       const void* z) {
-    base = reinterpret_cast<const char*>(P);
-    zeros = z;
+  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int, int wave_, int lane) {
+    rsrc = make_rsrc(P, (int64_t)rbound * ld * 2);
     wave = wave_;
     const int r = lane / CPR;
 #pragma unroll
     for (int par = 0; par < 2; ++par) {
-      const int row = (wave * PER + par) * BR + r;  // PER is even: parity of p = parity of the block
-      const int c = (lane % CPR) ^ kmaj_f<KS>(row);
-      kofs[par] = c * 8;
-      off[par] = (uint32_t)(((int64_t)(row0 + row) * ld + kofs[par]) * 2);
+      const int row = (wave * PER + par) * BR + r;
+      kofs[par] = ((lane % CPR) ^ kmaj_f<KS>(row)) * 8;
     }
-    bstep = (uint32_t)(2 * BR * ld * 2);
-    okmask = 0;
-#pragma unroll
-    for (int p = 0; p < PER; ++p)
-      if (row0 + (wave * PER + p) * BR + r < rbound) okmask |= 1u << p;
-  }
-  __device__ void issue(char* lds, int k0, int kd) const {
-    const bool kin0 = k0 + kofs[0] < kd, kin1 = k0 + kofs[1] < kd;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
-      const bool in = ((p & 1) ? kin1 : kin0) && ((okmask >> p) & 1);
-      dma16(in ? base + off[p & 1] + (p >> 1) * bstep + (uint32_t)k0 * 2u : zeros,
-            lds + (wave * PER + p) * 1024);
+      const int row = (wave * PER + p) * BR + r;
+      voff[p] = row0 + row < rbound ? (uint32_t)(((int64_t)(row0 + row) * ld + kofs[p & 1]) * 2) : kOob;
+    }
+  }
+  __device__ void issue(char* lds, int k0, int kd) const {
+    const uint32_t soff = (uint32_t)k0 * 2u;
+    if (k0 + 16 * KS <= kd) {
+#pragma unroll
+      for (int p = 0; p < PER; ++p) dma16(rsrc, lds + (wave * PER + p) * 1024, voff[p], soff);
+    } else {
+      const bool kin0 = k0 + kofs[0] < kd, kin1 = k0 + kofs[1] < kd;
+#pragma unroll
+      for (int p = 0; p < PER; ++p)
+        dma16(rsrc, lds + (wave * PER + p) * 1024, ((p & 1) ? kin1 : kin0) ? voff[p] : kOob, soff);
     }
   }
 };
@@ -354,19 +352,15 @@ template <int R, int KS>
 struct DmaRmaj {
   static constexpr int RBYTES = 2 * R;                      // bytes per depth row in LDS
   static constexpr int PER = 16 * KS * RBYTES / 1024 / 4;   // chunks per wave
-  const char* base;
-  const void* zeros;
-  int64_t ldb;         // bytes per depth row in HBM
-  uint32_t off[PER];   // byte offset (depth 0) of the vector this lane fetches for chunk p
+  __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t ldb;        // bytes per depth row in HBM
+  uint32_t voff[PER];  // byte offset (depth 0) of the vector this lane fetches for chunk p, or kOob
   int krow[PER];       // its depth row inside a K step
-  bool ok[PER];        // its rows exist
   int wave;
-  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int, int wave_, int lane,
-                       const void* z) {
-    base = reinterpret_cast<const char*>(P);
-    zeros = z;
+  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int kd, int wave_, int lane) {
+    rsrc = make_rsrc(P, (int64_t)kd * ld * 2);
     wave = wave_;
-    ldb = ld * 2;
+    ldb = (uint32_t)(ld * 2);
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int pos = (wave * PER + p) * 1024 + lane * 16;
@@ -374,15 +368,18 @@ struct DmaRmaj {
       const int chunk = (b >> 5) ^ ((k & 3) << 1);
       const int col = chunk * 16 + ((b >> 4) & 1) * 8;
       krow[p] = k;
-      ok[p] = row0 + col < rbound;
-      off[p] = (uint32_t)(k * ldb + (int64_t)(row0 + col) * 2);
+      voff[p] = row0 + col < rbound ? (uint32_t)(k * (int64_t)ldb + (int64_t)(row0 + col) * 2) : kOob;
     }
   }
   __device__ void issue(char* lds, int k0, int kd) const {
+    const uint32_t soff = (uint32_t)k0 * ldb;
+    if (k0 + 16 * KS <= kd) {
 #pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const bool in = ok[p] && k0 + krow[p] < kd;
-      dma16(in ? base + off[p] + (uint32_t)(k0 * ldb) : zeros, lds + (wave * PER + p) * 1024);
+      for (int p = 0; p < PER; ++p) dma16(rsrc, lds + (wave * PER + p) * 1024, voff[p], soff);
+    } else {
+#pragma unroll
+      for (int p = 0; p < PER; ++p)
+        dma16(rsrc, lds + (wave * PER + p) * 1024, k0 + krow[p] < kd ? voff[p] : kOob, soff);
     }
   }
 };
@@ -453,6 +450,15 @@ __device__ __forceinline__ bf16x8 frag_tr_asm(const char* lds, int row_block, in
 }
 
 template <int KS>
+__device__ __forceinline__ bf16x8 frag_kmaj_asm(const char* lds, int row_block, int ks, int lane) {
+  typedef __attribute__((address_space(3))) const char* lds_cptr;
+  const uint32_t a = (uint32_t)(uintptr_t)(lds_cptr)(lds + kmaj16_off<KS>(row_block + (lane & 31), 2 * ks + (lane >> 5)));
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(a));
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+template <int KS>
 __device__ __forceinline__ bf16x8 frag_kmaj_bf16(const char* lds, int row_block, int ks, int lane) {
   return *reinterpret_cast<const bf16x8*>(lds + kmaj16_off<KS>(row_block + (lane & 31), 2 * ks + (lane >> 5)));
 }
@@ -478,7 +484,7 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
     // Small and tall tiles: the fragments of 16-deep step ks + 2 are read
     // while the MFMAs of step ks run.  The scheduling barriers pin that order
     // (left alone, the scheduler reuses one set of fragment registers and
-    // waits for the LDS before every 16-deep step).  Transposing reads go
+    // waits for the LDS before every 16-deep step).  Fragment reads go
     // through assembly, so the wait for a step's fragments is explicit: every
     // LDS read issued after them may still be in flight.
     constexpr int NRD = (TRA ? 2 * MB : MB) + (TRB ? 2 * NB : NB);  // LDS reads per 16-deep step
@@ -489,14 +495,14 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
         if constexpr (TRA)
           a[ks][i] = frag_tr_asm<TM>(As, wm * MB * 32 + i * 32, ks, lane);
         else
-          a[ks][i] = frag_kmaj_bf16<KS>(As, wm * MB * 32 + i * 32, ks, lane);
+          a[ks][i] = frag_kmaj_asm<KS>(As, wm * MB * 32 + i * 32, ks, lane);
       }
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         if constexpr (TRB)
           b[ks][j] = frag_tr_asm<TN>(Bs, wn * NB * 32 + j * 32, ks, lane);
         else
-          b[ks][j] = frag_kmaj_bf16<KS>(Bs, wn * NB * 32 + j * 32, ks, lane);
+          b[ks][j] = frag_kmaj_asm<KS>(Bs, wn * NB * 32 + j * 32, ks, lane);
       }
     };
     rd(0);
@@ -505,7 +511,7 @@ __device__ __forceinline__ void mma_step(const char* As, const char* Bs,
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       if (ks + 2 < KS) rd(ks + 2);
-      if constexpr (TRA || TRB) {
+      {
         const int later = (ks + 1 < KS ? NRD : 0) + (ks + 2 < KS ? NRD : 0);
         __builtin_amdgcn_sched_barrier(0);
         if (later >= 15)
@@ -990,8 +996,8 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
     constexpr int TA = TM * 32 * KS, TB = TN * 32 * KS;  // operand tile bytes per K step
     constexpr int PS = LA::type::PER + LB::type::PER;  // direct loads per wave per K step
     const int nk = (d.Kd + BKE - 1) / BKE;
-    la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane, a.zeros);
-    lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane, a.zeros);
+    la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane);
+    lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane);
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
       if (s < nk) {
