@@ -1004,7 +1004,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     naux += (double)c.L * m.width + (double)c.d_out * m.width + c.d_out;
   }
   HIP_TRY(timed(h, "adamw", 1, 0.0, naux * (h->prec == Prec::BF16 ? 30.0 : 28.0), stream, [&] {
-    return launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, h->b.shadow, h->b.d_chunks, h->b.d_aux,
+    // biases and head weights: read in fp32 only, so no bf16 copy is written
+    return launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, nullptr, h->b.d_chunks, h->b.d_aux,
                         h->b.d_mem, (int64_t)h->aux_chunks.size(), ac, stream);
   }));
   h->t = step;

@@ -756,7 +756,8 @@ hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, fl
                         const MemberDev* mem, int64_t nchunks, const AdamConst& ac, hipStream_t s) {
   if (nchunks <= 0) return hipSuccess;
   const int grid = grid_for(nchunks, 4);
-  if (prec == Prec::BF16)
+  (void)prec;
+  if (shadow)
     hipLaunchKernelGGL((adamw_kernel<true>), dim3(grid), dim3(256), 0, s, theta, grad, m, v, shadow,
                        chunk_tab, list, mem, nchunks, ac);
   else

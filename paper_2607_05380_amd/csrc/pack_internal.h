@@ -133,6 +133,7 @@ hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, co
 hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
                          int64_t row_base, int rows_valid, int members, int Bp, void* H0,
                          const int32_t* member_ids, hipStream_t s);
+// shadow: where the bf16 copy of the updated parameters goes, or nullptr for none
 hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, float* v,
                         uint16_t* shadow, const uint32_t* chunk_tab, const uint32_t* list,
                         const MemberDev* mem, int64_t nchunks, const AdamConst& ac, hipStream_t s);

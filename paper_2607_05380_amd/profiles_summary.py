@@ -45,6 +45,15 @@ PAIR = {0: ("kmaj", "kmaj"), 1: ("kmaj", "kmaj"), 2: ("kmaj", "rmaj"), 3: ("rmaj
 def short_name(kernel):
     """Library profiler name of a rocprofv3 kernel name (mangled, or demangled
     with the template arguments partly lost), or None for other kernels."""
+    if "gemm_kernel_bwd" in kernel:
+        return "gemm_bf16_bwd"
+    if "gemm_kernel_tall" in kernel:
+        m = re.search(r"gemm_kernel_tall(?:ILi(\d)ELi(\d)ELi|<\d, \d, )(\d)", kernel)
+        if not m:
+            return None
+        epi = int(m.group(3))
+        a, b = PAIR[epi]
+        return f"gemm_bf16_{a}_{b}_{EPIS[epi]}"
     if "gemm_kernel" in kernel:
         m = re.search(r"gemm_kernel(?:_small)?I(DF16b|f)Li(\d)ELi(\d)ELi(\d)E", kernel)
         if m:
