@@ -83,9 +83,16 @@ constexpr int kLdsBig = 2 * 2 * 256 * ROW;    // two 64-deep stages of both 256-
 #define TABPACK_SMALL_NS 2
 #endif
 constexpr int kSmallKs = TABPACK_SMALL_KS, kSmallNs = TABPACK_SMALL_NS;
-constexpr int kLdsSmallBf16 = kSmallNs * 2 * 128 * 32 * kSmallKs;
-constexpr int kLdsSmall = kLdsSmallBf16 > 2 * 2 * 128 * ROW ? kLdsSmallBf16 : 2 * 2 * 128 * ROW;
-constexpr int kSmallWpe = kLdsSmall <= 80 * 1024 ? 2 : 1;  // workgroups (waves per SIMD) that fit per CU
+constexpr int kStageBytes = 4 * 32 * (2 * 128 + 32);  // epilogue staging of the 4 waves of a small tile
+constexpr int kLdsSmallBf16 =
+    kSmallNs * 2 * 128 * 32 * kSmallKs > kStageBytes ? kSmallNs * 2 * 128 * 32 * kSmallKs : kStageBytes;
+constexpr int kLdsSmallF32 = 2 * 2 * 128 * ROW;  // two register-staged 32-deep fp32 stages
+constexpr int kLdsSmall = kLdsSmallBf16 > kLdsSmallF32 ? kLdsSmallBf16 : kLdsSmallF32;
+// workgroups (waves per SIMD) per CU for the small kernel: as many as the
+// 160 KB of LDS hold, at most 3 (the register budget of 3 waves per SIMD)
+constexpr int wpe_for(int lds) { return 160 * 1024 / lds >= 3 ? 3 : (160 * 1024 / lds >= 2 ? 2 : 1); }
+constexpr int kSmallWpeBf16 = wpe_for(kLdsSmallBf16), kSmallWpeF32 = wpe_for(kLdsSmallF32);
+constexpr int kSmallWpe = kSmallWpeBf16;
 // Tall-tile bf16 pipeline: kTallNs stages of kTallKs 16-deep steps of the
 // 256-row and 128-row operand tiles; the small edge tiles of the same launch
 // keep the small pipeline.  Both must fit two workgroups per CU.
@@ -188,6 +195,20 @@ __device__ __forceinline__ void bar() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+}
+
+// Global-memory views of pointers taken from the descriptor tables.  The
+// compiler cannot infer their address space and would use flat accesses,
+// which also count against the LDS counter: every LDS wait of the epilogue
+// would then wait for the global stores before it too.
+#define TABPACK_GLOBAL __attribute__((address_space(1)))
+template <typename V>
+__device__ __forceinline__ TABPACK_GLOBAL V* glob(V* p) {
+  return (TABPACK_GLOBAL V*)p;
+}
+template <typename V>
+__device__ __forceinline__ const TABPACK_GLOBAL V* glob(const V* p) {
+  return (const TABPACK_GLOBAL V*)p;
 }
 
 // ---------------------------------------------------------------- loaders --
@@ -639,9 +660,9 @@ __device__ __forceinline__ void stage_flush(const char* stage, OT* C, int64_t ld
   for (int it = 0; it < S::PER_LANE; ++it) {
     const int v = it * 64 + lane;
     const int r = v / S::VPR, c = v % S::VPR;
-    const uint4 x = *reinterpret_cast<const uint4*>(stage + r * S::RS + c * 16);
+    const u32x4 x = *reinterpret_cast<const u32x4*>(stage + r * S::RS + c * 16);
     const int row = row0 + r, col = col0 + c * VE;
-    if (row < M && col < N) *reinterpret_cast<uint4*>(C + (int64_t)row * ld + col) = x;
+    if (row < M && col < N) *glob(reinterpret_cast<u32x4*>(C + (int64_t)row * ld + col)) = x;
   }
 }
 
@@ -684,7 +705,7 @@ __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmD
 #pragma unroll
     for (int u = 0; u < G; ++u) {
       if (!ok[u]) continue;
-      if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e[u]) = g[u];
+      if (a.keep_grad) *glob(reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e[u])) = g[u];
       adamw_vec4(th[u], g[u], m[u], vv[u], decay, step, ac);
       __builtin_nontemporal_store(th[u], reinterpret_cast<f32x4*>(a.theta + d.poff + e[u]));
       __builtin_nontemporal_store(m[u], reinterpret_cast<f32x4*>(a.am + d.poff + e[u]));
@@ -714,65 +735,79 @@ __device__ __forceinline__ int dwt_off(int r, int c) {
   return r * 512 + ((((c >> 2) ^ (((r >> 2) & 1) << 3))) << 4) + ((c & 3) << 2);
 }
 
+// rows of the gradient tile staged per pass: the whole tile when the small
+// kernel's LDS holds it, else halves (every kernel has at least that much LDS)
+constexpr int kDwPassRows = kLdsSmallBf16 >= 128 * 512 ? 128 : 64;
+
 __device__ __forceinline__ void dw_adamw_small(const GemmArgs& a, const GemmDesc& d, const Tile& t,
                                                f32x16 (&acc)[2][2], int wm, int wn, int lane, int tid, char* lds0) {
+  constexpr int NPASS = 128 / kDwPassRows;
+  constexpr int NV = kDwPassRows / 8;  // vectors per thread per pass
   const int hv = lane >> 5;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm * 64 + 32 * i + 8 * (r >> 2) + 4 * hv + (r & 3);
-        const int col = wn * 64 + 32 * j + (lane & 31);
-        *reinterpret_cast<float*>(lds0 + dwt_off(row, col)) = acc[i][j][r];
-      }
-  wait_vm<63, true>();  // this wave's LDS writes are done
-  bar();
   const AdamConst ac{a.beta1, a.beta2, a.eps, a.bc1, a.bc2_sqrt};
   const float decay = 1.0f - d.lr * d.wd;
   const float step = d.lr / a.bc1;
   const int mrows = min(d.M - t.m0, 128), ncols = min(d.N - t.n0, 128);
-  // vector u of this thread: row 8 u + tid / 32, columns 4 (tid % 32) .. +3
+  // vector u of this thread in a pass: row 8 u + tid / 32 of the pass, columns 4 (tid % 32) .. +3
   const int r0 = tid >> 5, c = (tid & 31) * 4;
   const bool colok = c < ncols;
-  const int64_t e0 = (int64_t)(t.m0 + r0) * d.ldc + t.n0 + c;  // element offset of vector 0
   const int64_t estep = 8 * d.ldc;
   float* th_p = a.theta + d.poff;
   float* m_p = a.am + d.poff;
   float* v_p = a.av + d.poff;
-  f32x4 th[kAdamAhead], m[kAdamAhead], vv[kAdamAhead];
-  auto ok = [&](int u) { return colok && 8 * u + r0 < mrows; };
-  auto load = [&](int u) {
-    const int64_t e = e0 + u * estep;
-    if (ok(u)) {
-      th[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(th_p + e));
-      m[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(m_p + e));
-      vv[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(v_p + e));
+#pragma unroll 1
+  for (int pass = 0; pass < NPASS; ++pass) {
+    const int prow0 = pass * kDwPassRows;  // first tile row of this pass
+    if (pass > 0) {
+      wait_vm<63, true>();
+      bar();  // every thread is done reading the previous pass
     }
-  };
 #pragma unroll
-  for (int u = 0; u < kAdamAhead; ++u) load(u);
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int b = u % kAdamAhead;
-    const int64_t e = e0 + u * estep;
-    const bool in = ok(u);
-    f32x4 g = *reinterpret_cast<const f32x4*>(lds0 + dwt_off(8 * u + r0, c));
-    f32x4 t_ = th[b], m_ = m[b], v_ = vv[b];
-    if (u + kAdamAhead < 16) load(u + kAdamAhead);
-    if (in) {
-      if (a.keep_grad) *reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e) = g;
-      adamw_vec4(t_, g, m_, v_, decay, step, ac);
-      __builtin_nontemporal_store(t_, reinterpret_cast<f32x4*>(th_p + e));
-      __builtin_nontemporal_store(m_, reinterpret_cast<f32x4*>(m_p + e));
-      __builtin_nontemporal_store(v_, reinterpret_cast<f32x4*>(v_p + e));
-      if (a.shadow) {
-        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[0]) |
-                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[1]) << 16);
-        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[2]) |
-                            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[3]) << 16);
-        *reinterpret_cast<u32x2*>(a.shadow + d.poff + e) = u32x2{lo, hi};
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * 64 + 32 * i + 8 * (r >> 2) + 4 * hv + (r & 3) - prow0;
+          const int col = wn * 64 + 32 * j + (lane & 31);
+          if (row >= 0 && row < kDwPassRows) *reinterpret_cast<float*>(lds0 + dwt_off(row, col)) = acc[i][j][r];
+        }
+    wait_vm<63, true>();  // this wave's LDS writes are done
+    bar();
+    const int64_t e0 = (int64_t)(t.m0 + prow0 + r0) * d.ldc + t.n0 + c;  // element offset of vector 0
+    f32x4 th[kAdamAhead], m[kAdamAhead], vv[kAdamAhead];
+    auto ok = [&](int u) { return colok && prow0 + 8 * u + r0 < mrows; };
+    auto load = [&](int u) {
+      const int64_t e = e0 + u * estep;
+      if (ok(u)) {
+        th[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(th_p + e));
+        m[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(m_p + e));
+        vv[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(v_p + e));
+      }
+    };
+#pragma unroll
+    for (int u = 0; u < kAdamAhead; ++u) load(u);
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int b = u % kAdamAhead;
+      const int64_t e = e0 + u * estep;
+      const bool in = ok(u);
+      f32x4 g = *reinterpret_cast<const f32x4*>(lds0 + dwt_off(8 * u + r0, c));
+      f32x4 t_ = th[b], m_ = m[b], v_ = vv[b];
+      if (u + kAdamAhead < NV) load(u + kAdamAhead);
+      if (in) {
+        if (a.keep_grad) *glob(reinterpret_cast<f32x4*>(static_cast<float*>(d.C) + e)) = g;
+        adamw_vec4(t_, g, m_, v_, decay, step, ac);
+        __builtin_nontemporal_store(t_, reinterpret_cast<f32x4*>(th_p + e));
+        __builtin_nontemporal_store(m_, reinterpret_cast<f32x4*>(m_p + e));
+        __builtin_nontemporal_store(v_, reinterpret_cast<f32x4*>(v_p + e));
+        if (a.shadow) {
+          const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[0]) |
+                              ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[1]) << 16);
+          const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[2]) |
+                              ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)t_[3]) << 16);
+          *reinterpret_cast<u32x2*>(a.shadow + d.poff + e) = u32x2{lo, hi};
+        }
       }
     }
   }
@@ -800,15 +835,15 @@ __device__ __forceinline__ void epi_prefetch(const GemmDesc& d, const Tile& t, i
     const bool colin = colL + 32 * j < d.N;
     pre.bias[j] = 0.0f;
     if constexpr (EPI == EPI_FWD || EPI == EPI_FWD_EVAL)
-      if (colin) pre.bias[j] = d.bias[colL + 32 * j];
+      if (colin) pre.bias[j] = *glob(d.bias + colL + 32 * j);
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
       const bool in = colin && (rb0 + i) * 32 < d.M;
       pre.w[i][j] = EPI == EPI_DX ? 0u : ~0u;
       if constexpr (EPI == EPI_FWD) {
-        if (d.drop_t != 0u && in) pre.w[i][j] = d.keepw[(int64_t)(rb0 + i) * d.N + colL + 32 * j];
+        if (d.drop_t != 0u && in) pre.w[i][j] = *glob(d.keepw + (int64_t)(rb0 + i) * d.N + colL + 32 * j);
       } else if constexpr (EPI == EPI_DX) {
-        if (in) pre.w[i][j] = d.mask[(int64_t)(rb0 + i) * d.N + colL + 32 * j];
+        if (in) pre.w[i][j] = *glob(d.mask + (int64_t)(rb0 + i) * d.N + colL + 32 * j);
       }
     }
   }
@@ -890,7 +925,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
         for (int j = 0; j < NB; ++j) {
           // lanes l and l^32 hold the two interleaved row halves of one column
           const float c = cs[j] + __shfl_xor(cs[j], 32, 64);
-          if (hv == 0 && colin[j] && hb < d.M) d.colpart[prow + colL + 32 * j] = c;
+          if (hv == 0 && colin[j] && hb < d.M) *glob(d.colpart + prow + colL + 32 * j) = c;
         }
       }
     }
@@ -898,17 +933,24 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
     using S = Stage<T, NB>;
     T* C = static_cast<T*>(d.C);
     const float(&bias)[NB] = pre.bias;
-    bool colok[NB];
-#pragma unroll
-    for (int j = 0; j < NB; ++j) colok[j] = colL + 32 * j < d.width;
     const float s_keep = (EPI == EPI_FWD) ? d.drop_s : 1.0f;
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
       if (i >= mv) continue;
       const int rb = row0 + 32 * i;
-      uint32_t mw[NB];
+      // one word per column decides which of the block's rows keep their
+      // value: bit r is set when row rb + r is kept by dropout, exists in the
+      // batch, and the column lies in the member's true width.  Shifted by
+      // 4 hv, bit 8 g + q is this lane's element (g, q).
+      const int nrow = a.rows_valid - rb;
+      const uint32_t rowmask = nrow >= 32 ? ~0u : (nrow <= 0 ? 0u : (1u << nrow) - 1u);
+      uint32_t kw[NB], mw[NB];
 #pragma unroll
-      for (int j = 0; j < NB; ++j) mw[j] = 0u;
+      for (int j = 0; j < NB; ++j) {
+        const uint32_t w = (EPI == EPI_FWD ? pre.w[i][j] : ~0u) & rowmask;
+        kw[j] = colL + 32 * j < d.width ? w >> (4 * hv) : 0u;
+        mw[j] = 0u;
+      }
 #pragma unroll
       for (int p = 0; p < S::NPASS; ++p) {
 #pragma unroll
@@ -918,12 +960,16 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const int gg = p * S::GP + g;
-              const int bit = 8 * gg + 4 * hv + q;
+              const int b = 8 * gg + q;
               float h = fmaxf(acc[i][j][4 * gg + q] + bias[j], 0.0f);
-              if constexpr (EPI == EPI_FWD) h = ((pre.w[i][j] >> bit) & 1) ? h * s_keep : 0.0f;
-              if (!colok[j] || rb + bit >= a.rows_valid) h = 0.0f;
+              if constexpr (EPI == EPI_FWD) h *= s_keep;
+              h = ((kw[j] >> b) & 1u) ? h : 0.0f;
               const T hs = from_float<T>(h);
-              if (to_float(hs) > 0.0f) mw[j] |= 1u << bit;
+              // H > 0 (h >= 0, so only a zero of either sign has a zero magnitude)
+              if constexpr (sizeof(T) == 2)
+                mw[j] |= (uint32_t)((__builtin_bit_cast(uint16_t, hs) & 0x7fffu) != 0u) << b;
+              else
+                mw[j] |= (uint32_t)((__builtin_bit_cast(uint32_t, hs) & 0x7fffffffu) != 0u) << b;
               stage_put<T, NB>(stage, j, g, q, lane, hs);
             }
         wave_sync_lds();
@@ -935,8 +981,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
         // complementary bits of the same (32-row block, column) word
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
-          const uint32_t w = mw[j] | (uint32_t)__shfl_xor((int)mw[j], 32, 64);
-          if (hv == 0 && colin[j] && rb < d.M) d.mask[(int64_t)(rb >> 5) * d.N + colL + 32 * j] = w;
+          const uint32_t mine = mw[j] << (4 * hv);
+          const uint32_t w = mine | (uint32_t)__shfl_xor((int)mine, 32, 64);
+          if (hv == 0 && colin[j] && rb < d.M) *glob(d.mask + (int64_t)(rb >> 5) * d.N + colL + 32 * j) = w;
         }
       }
     }
@@ -1078,9 +1125,10 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 // workgroup's epilogue overlaps the other's MFMA loop.  bf16: kSmallNs stages
 // of kSmallKs 16-deep steps; fp32: two register-staged stages.
 template <typename T, int AK, int BK_, int EPI>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(kSmallWpe, kSmallWpe))) void gemm_kernel_small(
-    GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[kLdsSmall];
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
+    sizeof(T) == 2 ? kSmallWpeBf16 : kSmallWpeF32, sizeof(T) == 2 ? kSmallWpeBf16 : kSmallWpeF32))) void
+gemm_kernel_small(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[sizeof(T) == 2 ? kLdsSmallBf16 : kLdsSmallF32];
   const Tile t = a.tiles[blockIdx.x];
   const GemmDesc d = a.descs[t.desc];
   const int tid = threadIdx.x;
