@@ -44,6 +44,7 @@ extern "C" {
 
 enum { PACK_TASK_REG_MSE = 0, PACK_TASK_BIN_BCE = 1, PACK_TASK_MULTI_CE = 2 };
 enum { PACK_PREC_BF16 = 0, PACK_PREC_FP32 = 1 };
+enum { PACK_PREDICT_MEMBERS = 0, PACK_PREDICT_ENSEMBLE = 1 };
 
 /* Hyperparameters of one base model (Section 3.7: drawn per member from
  * user-given ranges; one hidden width shared by all hidden layers of the
@@ -116,6 +117,19 @@ int pack_workspace_size(const pack_handle* h, size_t* bytes);
  * new workspace (state is re-initialised from the host copy). */
 int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream);
 
+/* Choose which members stay in the pack (Section 3.6, early stopping of base
+ * models: a member whose validation score has stopped improving is removed
+ * from the pack so that the compute goes to the members still improving).
+ *   active  host uint8 [K], 1 = member k is trained and evaluated, 0 = removed
+ * A removed member's parameters and AdamW moments are frozen as they are (its
+ * getters keep working, its rows of loss_out / pred_out / score_out are no
+ * longer written) and its GEMM tiles, head work and optimizer chunks leave the
+ * launches.  A member may be re-activated.  All members start active.  With a
+ * bound workspace the call re-plans the launches and uploads the tables on
+ * `stream` and synchronizes it.  Any subset is valid, including the empty one;
+ * training or evaluating an empty pack fails with PACK_ESTATE. */
+int pack_set_active(pack_handle* h, const uint8_t* active, hipStream_t stream);
+
 /* One training step of all K members (Sections 3.3, 3.4, 3.6): member k runs
  * forward on its base batch X[idx[k*B + b], :] (b < B) through L blocks
  * H = Dropout_k(ReLU(H W^T + b)) and a linear head, computes its batch-mean
@@ -134,15 +148,31 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
 int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N,
                     const int32_t* idx, uint64_t step, float* loss_out, hipStream_t stream);
 
-/* Evaluate every member on validation rows without dropout (Section 3.5 /
- * 3.6: per-epoch validation scoring feeds early stopping and selection).
+/* Evaluate every active member on validation rows without dropout (Section
+ * 3.5 / 3.6: per-epoch validation scoring feeds early stopping and selection).
  *   pred_out  device fp32 [K, Nv]: the per-row value an ensemble averages --
  *             the output (regression), P(class 1) (binary), or the
- *             probability of the true class (multiclass)
+ *             probability of the true class (multiclass); row k is written
+ *             for active members only
  *   score_out device fp64 [K]: RMSE, mean binary CE or mean CE of pred_out
- *             (probabilities clipped to [1e-15, 1 - 1e-15]); non-finite -> +inf */
+ *             (probabilities clipped to [1e-15, 1 - 1e-15]); non-finite -> +inf;
+ *             active members only */
 int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t Nv,
                       float* pred_out, double* score_out, hipStream_t stream);
+
+/* Predictions of the active members on N rows without dropout, as the final
+ * ensemble is applied (Section 3.5: the ensemble averages its members'
+ * predictions -- class probabilities for classification).
+ *   X     device fp32 [N, d_in]
+ *   mode  PACK_PREDICT_MEMBERS: out device fp32 [n_active, N, d_out], the
+ *         active members in increasing index order;
+ *         PACK_PREDICT_ENSEMBLE: out device fp32 [N, d_out], the mean over the
+ *         active members (summed in that order in fp64)
+ * Values: the output (regression), P(class 1) (binary, d_out = 1) or the
+ * softmax probabilities (multiclass).  A pack built from the selected
+ * snapshots (explicit hyperparameters, pack_set_params) predicts with the
+ * ensemble. */
+int pack_predict(pack_handle* h, const float* X, int64_t N, int32_t mode, float* out, hipStream_t stream);
 
 /* Scratch bytes pack_select() needs for C candidates over Nv rows. */
 int pack_select_workspace_size(int32_t C, int64_t Nv, size_t* bytes);

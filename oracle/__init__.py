@@ -17,7 +17,10 @@ What it computes (arXiv 2607.05380, "TabPack"):
   and weight decay (AdamW here, see ``mlp.adamw_step``).
 * §3.6 Training -- each member sees its own base batch; the members' losses
   are summed, never their predictions.
-* §3.5 Ensemble -- greedy ensembling over a candidate pool (``greedy``).
+* §3.5 Ensemble -- greedy ensembling over a candidate pool (``greedy``), and
+  the online ensemble rebuilt every epoch from the members' latest states and
+  the previous ensemble, with early stopping of base models and of the
+  ensemble (§3.6) (``online``).
 * §3.7 / App. F hyperparameter space -- members' hyperparameters are drawn
   from ranges (``sampling``).
 
@@ -28,9 +31,12 @@ sampling  hyperparameter draws and nn.Linear-style initial parameters.
 mlp       one member: forward, loss, backward, AdamW, dropout masks.
 pack      K independent members: one training step, evaluation, scores.
 greedy    greedy ensemble selection.
+online    the per-epoch online loop: validation, member removal, ensemble
+          rebuild, early stopping, the final ensemble's prediction.
 
 Parity pins (tests/test_oracle_*.py) tie every function to something other
 than itself: published Philox known-answer vectors and numpy's Philox,
 central finite differences, torch float64 autograd, torch.optim.AdamW,
-closed forms, brute-force greedy search and a hand-worked greedy example.
+closed forms, brute-force greedy search, a hand-worked greedy example, a
+hand-worked online run and closed forms of the online loop's stopping rules.
 """

@@ -81,6 +81,10 @@ class OraclePack:
         Y, _ = mlp.forward(self.params[k], np.asarray(Xv, dtype=np.float64), rnd=self.rnd)
         return Y
 
+    def predict_values(self, k, X):
+        """Member k's prediction values on X, [N, d_out] (see ``prediction_values``)."""
+        return prediction_values(self.predict(k, X), self.cfg["task"])
+
     def eval_members(self, Xv, yv, members=None):
         """(pred [K, Nv], score [K]) as in ``prediction`` and ``score``."""
         K = self.cfg["K"]
@@ -90,6 +94,21 @@ class OraclePack:
             preds[k] = prediction(self.predict(k, Xv), yv, self.cfg["task"])
             scores[k] = score(preds[k], yv, self.cfg["task"])
         return preds, scores
+
+
+def prediction_values(Y, task):
+    """All prediction values of one member, [N, d_out]: the outputs (regression),
+    P(class 1) (binary) or the softmax probabilities (multiclass).  The final
+    ensemble averages these across its members (§3.5: ensembles average
+    predictions; probabilities for classification)."""
+    Y = np.asarray(Y, dtype=np.float64)
+    if task == mlp.TASK_REG:
+        return Y
+    if task == mlp.TASK_BIN:
+        return 1.0 / (1.0 + np.exp(-Y))
+    mx = Y.max(axis=1, keepdims=True)
+    P = np.exp(Y - mx)
+    return P / P.sum(axis=1, keepdims=True)
 
 
 def prediction(Y, yv, task):

@@ -110,6 +110,7 @@ struct Bufs {
   ColTile* d_coltiles = nullptr;
   HeadTile* d_headtiles = nullptr;
   int32_t* d_members = nullptr;
+  int32_t* d_active = nullptr;  // active member ids, increasing
   float* headpart = nullptr;  // head backward partials, (Bp / RB) * (d_out + 1) * A / Bp floats
 };
 
@@ -124,6 +125,11 @@ struct pack_handle {
   std::vector<float> theta_host;  // host copy of the parameters, packed layout
   std::vector<uint32_t> chunk_tab;
   std::vector<uint32_t> aux_chunks;  // chunks the separate AdamW pass updates (biases, head)
+  // Members in the pack's launches (Section 3.6: a base model that stops
+  // improving is removed from the pack); inactive members keep their state.
+  std::vector<uint8_t> active;
+  std::vector<int32_t> active_ids;   // increasing
+  int64_t n_aux_active = 0;          // aux chunks of active members (uploaded first in d_aux)
 
   bool bound = false;
   Bufs b;
@@ -417,10 +423,10 @@ void split_members(pack_handle* h) {
   const pack_config& c = h->cfg;
   int ng = 3;
   if (const char* e = getenv("TABPACK_STREAMS")) ng = std::max(1, std::min(kGroups, atoi(e)));
-  h->ngroups = std::min(ng, c.K);
+  h->ngroups = std::max(1, std::min(ng, (int)h->active_ids.size()));
   for (auto& v : h->group) v.clear();
   std::vector<std::pair<double, int>> cost;
-  for (int k = 0; k < c.K; ++k) {
+  for (int k : h->active_ids) {
     const double w = h->mem[k].dp;
     cost.push_back({w * (h->Pin + (c.L - 1) * w), k});
   }
@@ -437,7 +443,9 @@ void split_members(pack_handle* h) {
 // Rows per head-backward block: up to 256, dividing Bp.
 int head_rows(const pack_handle* h) { return h->Bp % 256 == 0 ? 256 : h->Bp; }
 
-Plan build_plan(const pack_handle* h, const Bufs& bf) {
+// Launch tables over the members of `group` (the active members split into
+// streams; carve() sizes the workspace with every member in one group).
+Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&group)[kGroups]) {
   Plan p;
   p.tile_set = h->tiles;
   const pack_config& c = h->cfg;
@@ -460,8 +468,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   for (int hf = 0; hf < kGroups; ++hf)
   for (int l = 1; l <= c.L; ++l) {
     // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
-    Launch f{(int)p.descs.size(), (int)h->group[hf].size(), (int)p.tiles.size(), 0, 0.0};
-    for (int k : h->group[hf]) {
+    Launch f{(int)p.descs.size(), (int)group[hf].size(), (int)p.tiles.size(), 0, 0.0};
+    for (int k : group[hf]) {
       const Member& m = h->mem[k];
       GemmDesc d{};
       d.A = l == 1 ? h0(k) : act(Hl(l - 1), k);
@@ -494,10 +502,11 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   }
   {
     // evaluation, layer 1: every member reads the same validation rows (H_0 block 0)
-    Launch f{(int)p.descs.size(), c.K, (int)p.tiles.size(), 0, 0.0};
+    Launch f{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
+    for (int hf = 0; hf < kGroups; ++hf) f.ndesc += (int)group[hf].size();
     for (int hf = 0; hf < kGroups; ++hf)
-      for (int i = 0; i < (int)h->group[hf].size(); ++i) {
-        const int k = h->group[hf][i];
+      for (int i = 0; i < (int)group[hf].size(); ++i) {
+        const int k = group[hf][i];
         GemmDesc d = p.descs[p.fwd[0][hf][0].desc0 + i];
         d.A = h0(0);
         add_tiles(p, f, (int)p.descs.size(), h->Bp, h->mem[k].dp, d.Kd);
@@ -509,8 +518,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   for (int hf = 0; hf < kGroups; ++hf)
   for (int l = 1; l <= c.L; ++l) {
     // weight gradient: dW_l^T[out, in] = sum_rows dZ_l[row, out] H_{l-1}[row, in]
-    Launch w{(int)p.descs.size(), (int)h->group[hf].size(), (int)p.tiles.size(), 0, 0.0};
-    for (int k : h->group[hf]) {
+    Launch w{(int)p.descs.size(), (int)group[hf].size(), (int)p.tiles.size(), 0, 0.0};
+    for (int k : group[hf]) {
       const Member& m = h->mem[k];
       GemmDesc d{};
       d.A = act(dzb(l), k);
@@ -542,8 +551,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     // data gradient (l >= 2): dZ_{l-1} = (dZ_l W_l) * [H_{l-1} > 0] * s_k
     Launch x{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
     if (l >= 2) {
-      x.ndesc = (int)h->group[hf].size();
-      for (int k : h->group[hf]) {
+      x.ndesc = (int)group[hf].size();
+      for (int k : group[hf]) {
         const Member& m = h->mem[k];
         GemmDesc d{};
         d.A = act(dzb(l), k);
@@ -572,7 +581,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
   }
   for (int hf = 0; hf < kGroups; ++hf) {
     p.coltile0[hf] = (int)p.coltiles.size();
-    for (int k : h->group[hf])
+    for (int k : group[hf])
       for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
   }
   p.coltile0[kGroups] = (int)p.coltiles.size();
@@ -581,9 +590,9 @@ Plan build_plan(const pack_handle* h, const Bufs& bf) {
     p.headtile0[hf] = (int)p.headtiles.size();
     p.member0[hf] = (int)p.members.size();
     for (int r0 = 0; r0 < h->Bp; r0 += hrb)
-      for (int k : h->group[hf])
+      for (int k : group[hf])
         for (int c0 = 0; c0 < h->mem[k].dp; c0 += hcols) p.headtiles.push_back(HeadTile{k, c0, r0});
-    for (int k : h->group[hf]) p.members.push_back(k);
+    for (int k : group[hf]) p.members.push_back(k);
   }
   p.headtile0[kGroups] = (int)p.headtiles.size();
   p.member0[kGroups] = (int)p.members.size();
@@ -604,7 +613,7 @@ struct Carve {
 
 // Lays out the workspace.  With base == nullptr it only measures: the
 // pointers are then offsets from address 0 and are never dereferenced.
-size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
+size_t carve(const pack_handle* h, char* base, Bufs& bf) {
   const pack_config& c = h->cfg;
   Carve cv{base};
   bf.theta = cv.take<float>(h->P);
@@ -625,14 +634,16 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf, Plan* plan_out) {
   bf.d_chunks = cv.take<uint32_t>(h->chunk_tab.size());
   bf.d_aux = cv.take<uint32_t>(h->aux_chunks.size());
   bf.d_bias_off = cv.take<int64_t>((size_t)c.L * c.K);
-  Plan plan = build_plan(h, bf);
+  std::vector<int> all[kGroups];
+  for (int k = 0; k < c.K; ++k) all[0].push_back(k);
+  Plan plan = build_plan(h, bf, all);
   bf.d_descs = cv.take<GemmDesc>(plan.descs.size());
   bf.d_tiles = cv.take<Tile>(plan.tiles.size());
   bf.d_coltiles = cv.take<ColTile>(plan.coltiles.size());
   bf.d_headtiles = cv.take<HeadTile>(plan.headtiles.size());
   bf.d_members = cv.take<int32_t>(plan.members.size());
+  bf.d_active = cv.take<int32_t>(c.K);
   bf.headpart = cv.take<float>((size_t)(h->Bp / head_rows(h)) * (c.d_out + 1) * (h->A / h->Bp));
-  if (plan_out) *plan_out = std::move(plan);
   return (size_t)round_up((int64_t)cv.off, 256);
 }
 
@@ -697,6 +708,53 @@ hipError_t timed(pack_handle* h, const char* name, int kind, double flops, doubl
   return e;
 }
 
+void set_active_ids(pack_handle* h) {
+  h->active_ids.clear();
+  for (int k = 0; k < h->cfg.K; ++k)
+    if (h->active[k]) h->active_ids.push_back(k);
+}
+
+// Builds the launch tables of the active members, uploads them (and the AdamW
+// list of the active members' biases and heads) into the bound workspace, and
+// records the launches.  Synchronizes `stream`: the host tables are freed on
+// return.  The caller's earlier work on `stream` is ordered before the copies.
+int upload_plan(pack_handle* h, hipStream_t stream) {
+  const pack_config& c = h->cfg;
+  Plan plan = build_plan(h, h->b, h->group);
+  std::vector<uint32_t> aux;
+  for (uint32_t ch : h->aux_chunks)
+    if (h->active[h->chunk_tab[ch] & 0x7FFFFFFFu]) aux.push_back(ch);
+  h->n_aux_active = (int64_t)aux.size();
+  auto up = [&](void* dst, const void* src, size_t bytes) {
+    return bytes ? hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream) : hipSuccess;
+  };
+  HIP_TRY(up(h->b.d_aux, aux.data(), aux.size() * 4));
+  HIP_TRY(up(h->b.d_active, h->active_ids.data(), h->active_ids.size() * 4));
+  HIP_TRY(up(h->b.d_descs, plan.descs.data(), plan.descs.size() * sizeof(GemmDesc)));
+  HIP_TRY(up(h->b.d_tiles, plan.tiles.data(), plan.tiles.size() * sizeof(Tile)));
+  HIP_TRY(up(h->b.d_coltiles, plan.coltiles.data(), plan.coltiles.size() * sizeof(ColTile)));
+  HIP_TRY(up(h->b.d_headtiles, plan.headtiles.data(), plan.headtiles.size() * sizeof(HeadTile)));
+  HIP_TRY(up(h->b.d_members, plan.members.data(), plan.members.size() * sizeof(int32_t)));
+  HIP_TRY(hipStreamSynchronize(stream));
+  for (int hf = 0; hf < kGroups; ++hf) {
+    h->fwd[0][hf] = plan.fwd[0][hf];
+    h->fwd[1][hf] = plan.fwd[1][hf];
+    h->dx[hf] = plan.dx[hf];
+    h->dw[hf] = plan.dw[hf];
+  }
+  h->fwd1_eval = plan.fwd1_eval;
+  for (int i = 0; i <= kGroups; ++i) {
+    h->coltile0[i] = plan.coltile0[i];
+    h->headtile0[i] = plan.headtile0[i];
+    h->member0[i] = plan.member0[i];
+  }
+  h->ncoltiles = (int)plan.coltiles.size();
+  h->nheadtiles = (int)plan.headtiles.size();
+  h->head_rb = head_rows(h);
+  (void)c;
+  return PACK_OK;
+}
+
 const char* gemm_name(Prec p, OpKind a, OpKind b, EpiKind e) {
   static const char* ops[] = {"kmaj", "rmaj", "xgk", "xgr"};
   static const char* epis[] = {"fwd", "fwd_eval", "dx", "dw"};
@@ -755,6 +813,8 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
     m.scale = 1.0 / (1.0 - m.dropout);
   }
   plan_layout(h);
+  h->active.assign(cfg->K, 1);
+  set_active_ids(h);
   split_members(h);
   init_params(h);
   *out = h;
@@ -792,7 +852,7 @@ int pack_get_hparams(const pack_handle* h, pack_member_hp* out) {
 int pack_workspace_size(const pack_handle* h, size_t* bytes) {
   if (!h || !bytes) return fail(PACK_EINVAL, "NULL argument");
   Bufs tmp;
-  *bytes = carve(h, nullptr, tmp, nullptr);
+  *bytes = carve(h, nullptr, tmp);
   return PACK_OK;
 }
 
@@ -802,8 +862,7 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   size_t need = 0;
   pack_workspace_size(h, &need);
   if (bytes < need) return fail(PACK_EINVAL, "workspace has %zu bytes, %zu needed", bytes, need);
-  Plan plan;
-  carve(h, static_cast<char*>(workspace), h->b, &plan);
+  carve(h, static_cast<char*>(workspace), h->b);
   if (!h->side) {
     HIP_TRY(hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
     HIP_TRY(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
@@ -828,34 +887,27 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   }
   HIP_TRY(hipMemcpyAsync(h->b.d_mem, md.data(), md.size() * sizeof(MemberDev), hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_chunks, h->chunk_tab.data(), h->chunk_tab.size() * 4, hipMemcpyHostToDevice, stream));
-  HIP_TRY(hipMemcpyAsync(h->b.d_aux, h->aux_chunks.data(), h->aux_chunks.size() * 4, hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_bias_off, boff.data(), boff.size() * 8, hipMemcpyHostToDevice, stream));
-  HIP_TRY(hipMemcpyAsync(h->b.d_descs, plan.descs.data(), plan.descs.size() * sizeof(GemmDesc), hipMemcpyHostToDevice, stream));
-  HIP_TRY(hipMemcpyAsync(h->b.d_tiles, plan.tiles.data(), plan.tiles.size() * sizeof(Tile), hipMemcpyHostToDevice, stream));
-  HIP_TRY(hipMemcpyAsync(h->b.d_coltiles, plan.coltiles.data(), plan.coltiles.size() * sizeof(ColTile), hipMemcpyHostToDevice, stream));
-  HIP_TRY(hipMemcpyAsync(h->b.d_headtiles, plan.headtiles.data(), plan.headtiles.size() * sizeof(HeadTile), hipMemcpyHostToDevice, stream));
-  HIP_TRY(hipMemcpyAsync(h->b.d_members, plan.members.data(), plan.members.size() * sizeof(int32_t),
-                         hipMemcpyHostToDevice, stream));
   if (h->prec == Prec::BF16) HIP_TRY(launch_to_shadow(h->b.theta, h->b.shadow, h->P, stream));
-  HIP_TRY(hipStreamSynchronize(stream));
-  for (int hf = 0; hf < kGroups; ++hf) {
-    h->fwd[0][hf] = plan.fwd[0][hf];
-    h->fwd[1][hf] = plan.fwd[1][hf];
-    h->dx[hf] = plan.dx[hf];
-    h->dw[hf] = plan.dw[hf];
-  }
-  h->fwd1_eval = plan.fwd1_eval;
-  for (int i = 0; i <= kGroups; ++i) {
-    h->coltile0[i] = plan.coltile0[i];
-    h->headtile0[i] = plan.headtile0[i];
-    h->member0[i] = plan.member0[i];
-  }
-  h->ncoltiles = (int)plan.coltiles.size();
-  h->nheadtiles = (int)plan.headtiles.size();
-  h->head_rb = head_rows(h);
+  const int rc = upload_plan(h, stream);  // synchronizes the stream
+  if (rc) return rc;
   h->t = 0;
   h->bound = true;
   return PACK_OK;
+}
+
+int pack_set_active(pack_handle* h, const uint8_t* active, hipStream_t stream) {
+  if (!h || !active) return fail(PACK_EINVAL, "NULL argument");
+  for (int k = 0; k < h->cfg.K; ++k)
+    if (active[k] > 1) return fail(PACK_EINVAL, "active[%d] = %d is not 0 or 1", k, (int)active[k]);
+  h->active.assign(active, active + h->cfg.K);
+  set_active_ids(h);
+  split_members(h);
+  if (!h->bound) return PACK_OK;
+  // a member that comes back needs keep words for the next step, which were
+  // produced (during the last step) for the previous set only
+  h->keep_ready = 0;
+  return upload_plan(h, stream);
 }
 
 int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, const int32_t* idx,
@@ -866,13 +918,15 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   if (N < 1) return fail(PACK_EINVAL, "N=%lld must be positive", (long long)N);
   if (step != h->t + 1) return fail(PACK_ESTATE, "step %llu given, %llu expected", (unsigned long long)step,
                                     (unsigned long long)(h->t + 1));
+  if (h->active_ids.empty()) return fail(PACK_ESTATE, "no member is active");
   const pack_config& c = h->cfg;
+  const int nact = (int)h->active_ids.size();
   GemmArgs a = base_args(h);
   a.rows_valid = c.B;
   a.step = as_u32(step);
   const double act_bytes = (double)c.B * h->elt() * [&] {
     double s = 0;
-    for (const Member& m : h->mem) s += m.width;
+    for (int k : h->active_ids) s += h->mem[k].width;
     return s;
   }();
   auto gemm = [&](OpKind ak, OpKind bk, EpiKind e, const Launch& ln, int layer, hipStream_t s) {
@@ -900,9 +954,9 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   };
   int max_dp = 0;
   double nkeep = 0;
-  for (const Member& m : h->mem) {
-    max_dp = std::max(max_dp, m.dp);
-    nkeep += (double)c.L * h->Bp * m.dp / 8;
+  for (int k : h->active_ids) {
+    max_dp = std::max(max_dp, h->mem[k].dp);
+    nkeep += (double)c.L * h->Bp * h->mem[k].dp / 8;
   }
   // Dropout keep words (Philox, ALU-bound) run on the side stream: normally
   // they were produced during the previous step's backward pass; otherwise
@@ -911,8 +965,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   const int par = (int)(step & 1);
   auto keep_words = [&](uint64_t s_step, int p) {
     return timed(h, "dropout_words", 1, 0.0, nkeep, h->side, [&] {
-      return launch_dropout_words(a.key0, a.key1, as_u32(s_step), h->b.d_mem, c.K, c.L, max_dp, h->Bp, c.B,
-                                  h->A / 32, h->b.keepw + (size_t)p * c.L * (h->A / 32), h->side);
+      return launch_dropout_words(a.key0, a.key1, as_u32(s_step), h->b.d_mem, nact, c.L, max_dp, h->Bp, c.B,
+                                  h->A / 32, h->b.keepw + (size_t)p * c.L * (h->A / 32), h->b.d_active, h->side);
     });
   };
   if (h->keep_ready != step) {
@@ -944,7 +998,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     const int32_t* gm = h->b.d_members + h->member0[hf];
     const int gk = h->member0[hf + 1] - h->member0[hf];
     HIP_TRY(timed(h, "head_fwd", 1, 0.0, act_bytes / ng, s, [&] {
-      return launch_head_fwd(h->prec, h->task, false, h->Hl(c.L), h->b.theta, h->b.d_mem, gk, h->Bp, c.d_out, y,
+      return launch_head_fwd(h->prec, h->task, kHeadTrain, h->Hl(c.L), h->b.theta, h->b.d_mem, gk, h->Bp, c.d_out, y,
                              idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, gm, s);
     }));
     HIP_TRY(timed(h, "loss_reduce", 1, 0.0, (double)gk * c.B * 4 * (1 + c.d_out), s, [&] {
@@ -999,14 +1053,14 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     }
   HIP_TRY(merge());
   double naux = 0;
-  for (int k = 0; k < c.K; ++k) {
+  for (int k : h->active_ids) {
     const Member& m = h->mem[k];
     naux += (double)c.L * m.width + (double)c.d_out * m.width + c.d_out;
   }
   HIP_TRY(timed(h, "adamw", 1, 0.0, naux * (h->prec == Prec::BF16 ? 30.0 : 28.0), stream, [&] {
     // biases and head weights: read in fp32 only, so no bf16 copy is written
     return launch_adamw(h->prec, h->b.theta, h->b.grad, h->b.m, h->b.v, nullptr, h->b.d_chunks, h->b.d_aux,
-                        h->b.d_mem, (int64_t)h->aux_chunks.size(), ac, stream);
+                        h->b.d_mem, h->n_aux_active, ac, stream);
   }));
   h->t = step;
   return PACK_OK;
@@ -1018,7 +1072,9 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
   if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
   if (!Xv || !yv || !pred_out || !score_out) return fail(PACK_EINVAL, "NULL device pointer");
   if (Nv < 1) return fail(PACK_EINVAL, "Nv=%lld must be positive", (long long)Nv);
+  if (h->active_ids.empty()) return fail(PACK_ESTATE, "no member is active");
   const pack_config& c = h->cfg;
+  const int nact = (int)h->active_ids.size();
   GemmArgs a = base_args(h);
   for (int64_t r0 = 0; r0 < Nv; r0 += h->Bp) {
     a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
@@ -1031,10 +1087,48 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
         HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
       }
     }
-    HIP_TRY(launch_head_fwd(h->prec, h->task, true, h->Hl(c.L), h->b.theta, h->b.d_mem, c.K, h->Bp, c.d_out, yv,
-                            nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, nullptr, stream));
+    HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadEval, h->Hl(c.L), h->b.theta, h->b.d_mem, nact, h->Bp, c.d_out,
+                            yv, nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, h->b.d_active,
+                            stream));
   }
-  HIP_TRY(launch_eval_score(h->task, pred_out, yv, c.K, Nv, score_out, stream));
+  HIP_TRY(launch_eval_score(h->task, pred_out, yv, nact, Nv, score_out, h->b.d_active, stream));
+  return PACK_OK;
+}
+
+int pack_predict(pack_handle* h, const float* X, int64_t N, int32_t mode, float* out, hipStream_t stream) {
+  if (!h) return fail(PACK_EINVAL, "handle is NULL");
+  if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
+  if (!X || !out) return fail(PACK_EINVAL, "NULL device pointer");
+  if (N < 1) return fail(PACK_EINVAL, "N=%lld must be positive", (long long)N);
+  if (mode != PACK_PREDICT_MEMBERS && mode != PACK_PREDICT_ENSEMBLE) return fail(PACK_EINVAL, "unknown mode %d", mode);
+  if (h->active_ids.empty()) return fail(PACK_ESTATE, "no member is active");
+  const pack_config& c = h->cfg;
+  const int nact = (int)h->active_ids.size();
+  GemmArgs a = base_args(h);
+  for (int64_t r0 = 0; r0 < N; r0 += h->Bp) {
+    a.rows_valid = (int)std::min<int64_t>(h->Bp, N - r0);
+    HIP_TRY(launch_gather(h->prec, X, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, nullptr,
+                          stream));
+    for (int l = 1; l <= c.L; ++l) {
+      for (int hf = 0; hf < (l == 1 ? 1 : h->ngroups); ++hf) {
+        GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][hf][l - 1]);
+        al.layer = l;
+        HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
+      }
+    }
+    if (mode == PACK_PREDICT_MEMBERS) {
+      // member i (i-th active id) writes rows r0.. of out[i, :, :]
+      HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadPredict, h->Hl(c.L), h->b.theta, h->b.d_mem, nact, h->Bp,
+                              c.d_out, nullptr, nullptr, c.B, a.rows_valid, r0, N, nullptr, nullptr, out,
+                              h->b.d_active, stream));
+    } else {
+      // the chunk's member predictions go to the dY buffer ([K, Bp, d_out]), then their mean to out
+      HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadPredict, h->Hl(c.L), h->b.theta, h->b.d_mem, nact, h->Bp,
+                              c.d_out, nullptr, nullptr, c.B, a.rows_valid, 0, h->Bp, nullptr, nullptr, h->b.dY,
+                              h->b.d_active, stream));
+      HIP_TRY(launch_ensemble_mean(h->b.dY, nact, h->Bp, a.rows_valid, c.d_out, r0, out, stream));
+    }
+  }
   return PACK_OK;
 }
 

@@ -106,10 +106,13 @@ struct Vec8<float> {
 };
 
 // Y = H_L[row] . W_out^T + b_out for 8 rows per wave (8 lanes per row, each
-// lane a 16-byte column vector per step), then either the training loss and
-// dLoss/dY of the row, or the eval prediction.  D >= d_out is the output count
-// rounded up to a power of two.
-template <typename T, bool EVAL, int D>
+// lane a 16-byte column vector per step), then, by MODE: the training loss and
+// dLoss/dY of the row (kHeadTrain); the score-ready eval value (kHeadEval:
+// output, P(class 1) or P(true class)) at pred[k * Nv + row_base + row]; or
+// all d_out prediction values (kHeadPredict: outputs, P(class 1) or the softmax
+// probabilities) at pred[((blockIdx.y * Nv) + row_base + row) * d_out + o].
+// D >= d_out is the output count rounded up to a power of two.
+template <typename T, int MODE, int D>
 __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, const float* theta,
                                                        const MemberDev* mem, int Bp, int d_out,
                                                        const void* y, const int32_t* idx, int B,
@@ -151,9 +154,26 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, co
   }
   if (sub != 0) return;
 
+  constexpr bool EVAL = MODE != kHeadTrain;
   const bool valid = EVAL ? row < rows_valid : row < B;
   int64_t src = 0;
   if (valid) src = EVAL ? row_base + row : (int64_t)idx[(int64_t)k * B + row];
+  if constexpr (MODE == kHeadPredict) {
+    if (!valid) return;
+    float* out = pred + ((int64_t)blockIdx.y * Nv + row_base + row) * d_out;
+    if (task == Task::REG) {
+      for (int o = 0; o < d_out; ++o) out[o] = z[o];
+    } else if (task == Task::BIN) {
+      out[0] = 1.0f / (1.0f + expf(-z[0]));
+    } else {
+      float mx = z[0];
+      for (int o = 1; o < d_out; ++o) mx = fmaxf(mx, z[o]);
+      float se = 0.0f;
+      for (int o = 0; o < d_out; ++o) se += expf(z[o] - mx);
+      for (int o = 0; o < d_out; ++o) out[o] = expf(z[o] - mx) / se;
+    }
+    return;
+  }
   if (EVAL) {
     if (!valid) return;
     float p;
@@ -460,9 +480,9 @@ __global__ void to_shadow_kernel(const float* theta, uint16_t* shadow, int64_t n
 // ------------------------------------------------------------ eval scores --
 __global__ __launch_bounds__(256) void eval_score_kernel(Task task, const float* pred,
                                                          const void* yv, int64_t Nv,
-                                                         double* score_out) {
+                                                         double* score_out, const int32_t* members) {
   __shared__ double sh[4];
-  const int k = blockIdx.x;
+  const int k = members ? members[blockIdx.x] : (int)blockIdx.x;
   double s = 0.0;
   for (int64_t i = threadIdx.x; i < Nv; i += 256) s += row_score(task, (double)pred[k * Nv + i], yv, i);
   s = block_sum_d(s, sh);
@@ -491,8 +511,8 @@ __device__ __forceinline__ uint32_t keep_word(uint32_t key0, uint32_t key1, uint
 // Rows >= rows_valid and columns >= width get 0 (the epilogue zeroes them).
 __global__ __launch_bounds__(256) void dropout_words_kernel(uint32_t key0, uint32_t key1, uint32_t step,
                                                             const MemberDev* mem, int Bp, int rows_valid,
-                                                            int64_t A32, uint32_t* out) {
-  const int k = blockIdx.y, l = blockIdx.z + 1;
+                                                            int64_t A32, uint32_t* out, const int32_t* members) {
+  const int k = members ? members[blockIdx.y] : (int)blockIdx.y, l = blockIdx.z + 1;
   const MemberDev md = mem[k];
   const int64_t nw = (int64_t)(Bp / 32) * md.dp;
   const int64_t w = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -619,6 +639,19 @@ __global__ void select_final_kernel(const int32_t* state, const double* best, in
   *score = *best;
 }
 
+// Ensemble prediction of one row chunk: out[(row_base + r) * d_out + o] is the
+// mean over the n member predictions part[(i * Bp + r) * d_out + o], summed in
+// member order in fp64.
+__global__ __launch_bounds__(256) void ensemble_mean_kernel(const float* part, int n, int Bp, int rows, int d_out,
+                                                            int64_t row_base, float* out) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)rows * d_out) return;
+  const int64_t stride = (int64_t)Bp * d_out;
+  double s = 0.0;
+  for (int i = 0; i < n; ++i) s += (double)part[i * stride + e];
+  out[row_base * d_out + e] = (float)(s / n);
+}
+
 inline int grid_for(int64_t n, int per) {
   int64_t g = (n + per - 1) / per;
   if (g < 1) g = 1;
@@ -631,20 +664,20 @@ inline int grid_for(int64_t n, int per) {
 int select_blocks(int64_t Nv) { return (int)((Nv + kSelRows - 1) / kSelRows); }
 
 namespace {
-template <typename T, bool EVAL, int D>
+template <typename T, int MODE, int D>
 void head_fwd_t(dim3 grid, hipStream_t s, Task task, const void* H, const float* theta, const MemberDev* mem,
                 int Bp, int d_out, const void* y, const int32_t* idx, int B, int rows_valid, int64_t row_base,
                 int64_t Nv, float* dY, float* rowloss, float* pred, const int32_t* members) {
-  hipLaunchKernelGGL((head_fwd_kernel<T, EVAL, D>), grid, dim3(256), 0, s, task, static_cast<const T*>(H), theta,
+  hipLaunchKernelGGL((head_fwd_kernel<T, MODE, D>), grid, dim3(256), 0, s, task, static_cast<const T*>(H), theta,
                      mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, rowloss, pred, members);
 }
 
-template <typename T, bool EVAL>
+template <typename T, int MODE>
 void head_fwd_d(int d_out, dim3 grid, hipStream_t s, Task task, const void* H, const float* theta,
                 const MemberDev* mem, int Bp, const void* y, const int32_t* idx, int B, int rows_valid,
                 int64_t row_base, int64_t Nv, float* dY, float* rowloss, float* pred, const int32_t* members) {
 #define TABPACK_HEAD_FWD(DD)                                                                                   \
-  head_fwd_t<T, EVAL, DD>(grid, s, task, H, theta, mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, \
+  head_fwd_t<T, MODE, DD>(grid, s, task, H, theta, mem, Bp, d_out, y, idx, B, rows_valid, row_base, Nv, dY, \
                           rowloss, pred, members)
   if (d_out <= 1) TABPACK_HEAD_FWD(1);
   else if (d_out <= 2) TABPACK_HEAD_FWD(2);
@@ -656,28 +689,27 @@ void head_fwd_d(int d_out, dim3 grid, hipStream_t s, Task task, const void* H, c
 
 }  // namespace
 
-hipError_t launch_head_fwd(Prec prec, Task task, bool eval, const void* H, const float* theta,
+hipError_t launch_head_fwd(Prec prec, Task task, int mode, const void* H, const float* theta,
                            const MemberDev* mem, int K, int Bp, int d_out, const void* y,
                            const int32_t* idx, int B, int rows_valid, int64_t row_base, int64_t Nv,
                            float* dY, float* rowloss, float* pred, const int32_t* members, hipStream_t s) {
-  if (Bp % 32 != 0 || d_out < 1 || d_out > kMaxOut) return hipErrorInvalidValue;
+  if (Bp % 32 != 0 || d_out < 1 || d_out > kMaxOut || mode < kHeadTrain || mode > kHeadPredict)
+    return hipErrorInvalidValue;
   if (K <= 0) return hipSuccess;
   const dim3 grid(Bp / 32, K);
+#define TABPACK_HEAD_FWD_MODE(TT, MM)                                                                         \
+  head_fwd_d<TT, MM>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY, rowloss, \
+                     pred, members)
   if (prec == Prec::BF16) {
-    if (eval)
-      head_fwd_d<__bf16, true>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
-                               rowloss, pred, members);
-    else
-      head_fwd_d<__bf16, false>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
-                                rowloss, pred, members);
+    if (mode == kHeadTrain) TABPACK_HEAD_FWD_MODE(__bf16, kHeadTrain);
+    else if (mode == kHeadEval) TABPACK_HEAD_FWD_MODE(__bf16, kHeadEval);
+    else TABPACK_HEAD_FWD_MODE(__bf16, kHeadPredict);
   } else {
-    if (eval)
-      head_fwd_d<float, true>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
-                              rowloss, pred, members);
-    else
-      head_fwd_d<float, false>(d_out, grid, s, task, H, theta, mem, Bp, y, idx, B, rows_valid, row_base, Nv, dY,
-                               rowloss, pred, members);
+    if (mode == kHeadTrain) TABPACK_HEAD_FWD_MODE(float, kHeadTrain);
+    else if (mode == kHeadEval) TABPACK_HEAD_FWD_MODE(float, kHeadEval);
+    else TABPACK_HEAD_FWD_MODE(float, kHeadPredict);
   }
+#undef TABPACK_HEAD_FWD_MODE
   return hipGetLastError();
 }
 
@@ -766,14 +798,24 @@ hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, fl
   return hipGetLastError();
 }
 
+hipError_t launch_ensemble_mean(const float* part, int n, int Bp, int rows, int d_out, int64_t row_base,
+                                float* out, hipStream_t s) {
+  if (n <= 0 || rows <= 0) return hipSuccess;
+  const int64_t ne = (int64_t)rows * d_out;
+  hipLaunchKernelGGL(ensemble_mean_kernel, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, s, part, n, Bp, rows,
+                     d_out, row_base, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(to_shadow_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, theta, shadow, n);
   return hipGetLastError();
 }
 
 hipError_t launch_eval_score(Task task, const float* pred, const void* yv, int K, int64_t Nv,
-                             double* score_out, hipStream_t s) {
-  hipLaunchKernelGGL(eval_score_kernel, dim3(K), dim3(256), 0, s, task, pred, yv, Nv, score_out);
+                             double* score_out, const int32_t* members, hipStream_t s) {
+  if (K <= 0) return hipSuccess;
+  hipLaunchKernelGGL(eval_score_kernel, dim3(K), dim3(256), 0, s, task, pred, yv, Nv, score_out, members);
   return hipGetLastError();
 }
 
@@ -785,10 +827,12 @@ hipError_t launch_dropout_mask(uint32_t key0, uint32_t key1, uint32_t step, int 
 }
 
 hipError_t launch_dropout_words(uint32_t key0, uint32_t key1, uint32_t step, const MemberDev* mem, int K, int L,
-                                int max_dp, int Bp, int rows_valid, int64_t A32, uint32_t* out, hipStream_t s) {
+                                int max_dp, int Bp, int rows_valid, int64_t A32, uint32_t* out,
+                                const int32_t* members, hipStream_t s) {
+  if (K <= 0) return hipSuccess;
   const int64_t nw = (int64_t)(Bp / 32) * max_dp;
   hipLaunchKernelGGL(dropout_words_kernel, dim3((unsigned)((nw + 255) / 256), K, L), dim3(256), 0, s, key0, key1, step,
-                     mem, Bp, rows_valid, A32, out);
+                     mem, Bp, rows_valid, A32, out, members);
   return hipGetLastError();
 }
 

@@ -113,8 +113,11 @@ struct ColTile {            // (member, first column) work item of the column-sw
 // Launchers (kernels_gemm.hip).
 hipError_t launch_gemm(Prec prec, OpKind a, OpKind b, EpiKind e, const GemmArgs& args, hipStream_t s);
 
+// Head forward modes: training loss and dY / score-ready eval value / all prediction values.
+constexpr int kHeadTrain = 0, kHeadEval = 1, kHeadPredict = 2;
+
 // Launchers (kernels_aux.hip).
-hipError_t launch_head_fwd(Prec prec, Task task, bool eval, const void* H, const float* theta,
+hipError_t launch_head_fwd(Prec prec, Task task, int mode, const void* H, const float* theta,
                            const MemberDev* mem, int K, int Bp, int d_out, const void* y,
                            const int32_t* idx, int B, int rows_valid, int64_t row_base, int64_t Nv,
                            float* dY, float* rowloss, float* pred, const int32_t* members, hipStream_t s);
@@ -138,12 +141,17 @@ hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, fl
                         uint16_t* shadow, const uint32_t* chunk_tab, const uint32_t* list,
                         const MemberDev* mem, int64_t nchunks, const AdamConst& ac, hipStream_t s);
 hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hipStream_t s);
+// members: the K member ids whose rows of pred are scored (nullptr: 0 .. K-1)
 hipError_t launch_eval_score(Task task, const float* pred, const void* yv, int K, int64_t Nv,
-                             double* score_out, hipStream_t s);
+                             double* score_out, const int32_t* members, hipStream_t s);
+hipError_t launch_ensemble_mean(const float* part, int n, int Bp, int rows, int d_out, int64_t row_base,
+                                float* out, hipStream_t s);
 hipError_t launch_dropout_mask(uint32_t key0, uint32_t key1, uint32_t step, int layer, int member,
                                uint32_t t, int B, int width, uint8_t* out, hipStream_t s);
+// members: the K member ids to produce words for (nullptr: 0 .. K-1)
 hipError_t launch_dropout_words(uint32_t key0, uint32_t key1, uint32_t step, const MemberDev* mem, int K, int L,
-                                int max_dp, int Bp, int rows_valid, int64_t A32, uint32_t* out, hipStream_t s);
+                                int max_dp, int Bp, int rows_valid, int64_t A32, uint32_t* out,
+                                const int32_t* members, hipStream_t s);
 hipError_t launch_select_iter(Task task, const float* cand, const void* yv, int C, int64_t Nv,
                               int m_ens, double* sum, double* partial, int nblk, int32_t* state,
                               double* best, int32_t* sel_out, hipStream_t s);

@@ -17,12 +17,13 @@ LIB_PATH = os.path.join(HERE, "libtabpack.so")
 PACK_OK = 0
 TASKS = {"reg": 0, "bin": 1, "multi": 2}
 PRECISIONS = {"bf16": 0, "fp32": 1}
+PREDICT_MEMBERS, PREDICT_ENSEMBLE = 0, 1
 
 SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "pack_workspace_size",
            "pack_bind", "pack_train_step", "pack_eval_members", "pack_select_workspace_size",
            "pack_select", "pack_member_param_count", "pack_get_params", "pack_set_params",
            "pack_get_grads", "pack_get_moments", "pack_debug_dropout_mask", "pack_debug_activation",
-           "pack_profile_enable", "pack_profile_read"]
+           "pack_profile_enable", "pack_profile_read", "pack_set_active", "pack_predict"]
 
 
 class MemberHP(ctypes.Structure):
@@ -88,6 +89,8 @@ def load_library(path=LIB_PATH):
         "pack_debug_activation": ([H, i32, i32, vp], ctypes.c_int),
         "pack_profile_enable": ([H, i32], ctypes.c_int),
         "pack_profile_read": ([H, ctypes.POINTER(KernelStat), i32, ctypes.POINTER(i32)], ctypes.c_int),
+        "pack_set_active": ([H, vp, vp], ctypes.c_int),
+        "pack_predict": ([H, vp, i64, i32, vp, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -152,6 +155,7 @@ class Pack:
         self.d_in, self.d_out = c.d_in, c.d_out
         self.workspace = None
         self._select_ws = None
+        self.active = [True] * self.K
 
     def __del__(self):
         h = getattr(self, "h", None)
@@ -191,15 +195,35 @@ class Pack:
                                         int(step), loss_out.data_ptr(), _stream()))
         return loss_out
 
+    def set_active(self, active, stream=None):
+        """active: K booleans; removed members are frozen and leave the launches."""
+        assert len(active) == self.K
+        arr = (ctypes.c_uint8 * self.K)(*[1 if a else 0 for a in active])
+        _check(self.lib.pack_set_active(self.h, arr, _stream(stream)))
+        self.active = [bool(a) for a in active]
+
     def eval_members(self, Xv, yv):
+        """(pred fp32 [K, Nv], score fp64 [K]); rows of inactive members are NaN."""
         import torch
         assert Xv.is_cuda and Xv.dtype == torch.float32 and Xv.is_contiguous() and Xv.shape[1] == self.d_in
         Nv = Xv.shape[0]
-        pred = torch.empty((self.K, Nv), dtype=torch.float32, device=Xv.device)
-        score = torch.empty(self.K, dtype=torch.float64, device=Xv.device)
+        pred = torch.full((self.K, Nv), float("nan"), dtype=torch.float32, device=Xv.device)
+        score = torch.full((self.K,), float("nan"), dtype=torch.float64, device=Xv.device)
         _check(self.lib.pack_eval_members(self.h, Xv.data_ptr(), yv.data_ptr(), Nv, pred.data_ptr(),
                                           score.data_ptr(), _stream()))
         return pred, score
+
+    def predict(self, X, ensemble=False):
+        """Predictions without dropout: [n_active, N, d_out] per active member (increasing
+        index), or the ensemble mean [N, d_out] with ensemble=True."""
+        import torch
+        assert X.is_cuda and X.dtype == torch.float32 and X.is_contiguous() and X.shape[1] == self.d_in
+        N = X.shape[0]
+        shape = (N, self.d_out) if ensemble else (sum(self.active), N, self.d_out)
+        out = torch.empty(shape, dtype=torch.float32, device=X.device)
+        _check(self.lib.pack_predict(self.h, X.data_ptr(), N, PREDICT_ENSEMBLE if ensemble else PREDICT_MEMBERS,
+                                     out.data_ptr(), _stream()))
+        return out
 
     def select(self, cand, yv, m_ens):
         """Greedy selection over cand fp32 [C, Nv]; returns (picks, score) on the host."""
