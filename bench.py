@@ -53,6 +53,83 @@ def cpu_baseline(cfg, X, y, idx0, budget_s=15.0):
                       f"{dt:.1f} s"}
 
 
+def per_epoch(cfg, pk, Xtr, ytr, Xva, yva, step, online_epochs):
+    """The per-epoch work around the training steps, timed on the device: the
+    validation forward and scores of every member (pack_eval_members), the
+    greedy selection over the online pool of the K members plus a previous
+    ensemble of 32 (pack_select), the step time with the cheaper half of the
+    members removed from the pack (pack_set_active), and whole epochs of the
+    online driver (training, validation, selection, snapshots).  Returns
+    (results, last step number used)."""
+    import torch
+    from paper_2607_05380_amd.online import OnlineTrainer
+
+    def timed(fn, reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            r = fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps, r
+
+    K, L, d_in, d_out = cfg["K"], cfg["L"], cfg["d_in"], cfg["d_out"]
+    widths = [h["width"] for h in pk.hparams()]
+    Nv = Xva.shape[0]
+    res = {}
+    ms, (pred, _) = timed(lambda: pk.eval_members(Xva, yva), 3)
+    flops = 2.0 * Nv * sum(d_in * w + (L - 1) * w * w + w * d_out for w in widths)
+    peak = PEAK["mfma_bf16"] if cfg["precision"] == "bf16" else PEAK["mfma_fp32"]
+    res["eval"] = {"ms": round(ms, 3), "rows": Nv, "tflop_per_s": round(flops / ms / 1e9, 1),
+                   "frac_mfma_peak": round(flops / ms / 1e9 / peak, 4)}
+    g = torch.Generator(device=pred.device)
+    g.manual_seed(1)
+    prev = pred[:32] + 0.05 * torch.randn(pred[:32].shape, generator=g, device=pred.device)
+    cand = torch.cat([pred, prev]).contiguous()
+    ms, (picks, _) = timed(lambda: pk.select(cand, yva, 32), 3)
+    sweeps = min(len(picks) + 1, 32)
+    res["select"] = {"ms": round(ms, 3), "candidates": cand.shape[0], "rows": Nv, "picked": len(picks),
+                     "gb_per_s": round(sweeps * cand.numel() * 4 / ms / 1e6, 1)}
+    loss = torch.empty(K, dtype=torch.float32, device=Xtr.device)
+    cost = sorted(range(K), key=lambda k: widths[k] * (d_in + (L - 1) * widths[k]))
+    keep = [False] * K
+    for k in cost[K // 2:]:
+        keep[k] = True
+    idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
+
+    def one():
+        nonlocal step
+        step += 1
+        pk.train_step(Xtr, ytr, idx, step, loss)
+
+    full_ms, _ = timed(one, 20)
+    pk.set_active(keep)
+    half_ms, _ = timed(one, 20)
+    pk.set_active([True] * K)
+    work = [w * (d_in + (L - 1) * w) for w in widths]
+    res["removal"] = {"step_ms_all": round(full_ms, 4), "step_ms_costlier_half": round(half_ms, 4),
+                      "work_share_kept": round(sum(work[k] for k in range(K) if keep[k]) / sum(work), 4)}
+    if online_epochs > 0:
+        tr = OnlineTrainer(dict(cfg, keep_grads=0), max_epochs=online_epochs, device=Xtr.device)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        tr.fit(Xtr, ytr, Xva, yva)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        n = len(tr.history)
+        res["online"] = {"epochs": n, "steps_per_epoch": tr.history[0]["steps"], "s_per_epoch": round(wall / n, 4),
+                         "ensemble_size": len(tr.ensemble), "ensemble_score": tr.ensemble_score}
+        del tr
+    return res, step
+
+
+def synth_idx(cfg, n, device):
+    from paper_2607_05380_amd import synth
+    return synth.epoch_orders_device(cfg, 1, n, device)[:, :cfg["B"]].contiguous()
+
+
 def measured_traffic(workload, kernel):
     """HBM bytes per launch of `kernel` from the committed profiler counters
     (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's reading), or None when
@@ -80,6 +157,9 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the timed steps, copy a 256 MiB buffer 3 times (the reference dispatches that "
                          "scale hardware byte counters in a profiler run)")
+    ap.add_argument("--online-epochs", type=int, default=1,
+                    help="epochs of the online driver timed after the steps (0: none)")
+    ap.add_argument("--no-per-epoch", action="store_true", help="skip the per-epoch measurements")
     ap.add_argument("--keep-grads", action="store_true",
                     help="also write every gradient out (an inspection aid; the optimizer does not need it)")
     a = ap.parse_args()
@@ -95,7 +175,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     log(f"generating {cfg['name']} on device: {cfg['n_train']} x {cfg['d_in']}")
-    Xtr, ytr, _, _ = synth.make_data_device(cfg, dev)
+    Xtr, ytr, Xva, yva = synth.make_data_device(cfg, dev)
     orders = synth.epoch_orders_device(cfg, 0, cfg["n_train"], dev)
     steps_per_epoch = cfg["n_train"] // cfg["B"]
     total = a.warmup + a.steps + a.profile_steps
@@ -186,6 +266,10 @@ def main():
                      "bytes_per_launch": s["bytes"]}
                     for s in sorted(stats, key=lambda s: -s["busy_ms"])],
     }
+    if not a.no_per_epoch:
+        log("per-epoch work: validation, selection, member removal, online driver")
+        out["per_epoch"], step = per_epoch(cfg, pk, Xtr, ytr, Xva, yva, step, a.online_epochs)
+        log(f"  {json.dumps(out['per_epoch'])}")
     if not a.no_cpu_baseline:
         log("timing the fp64 oracle on the host (bounded sample)")
         out["cpu_baseline"] = cpu_baseline(cfg, Xtr, ytr, idx_all[0])
