@@ -125,6 +125,31 @@ def per_epoch(cfg, pk, Xtr, ytr, Xva, yva, step, online_epochs):
     return res, step
 
 
+def variable_depth(cfg, Xtr, ytr, steps=20):
+    """Step time of the same workload with member depths ~ UniformInt[1, L]
+    (App. F samples the number of layers): shallower members leave the deeper
+    layers' launches, so the step should scale with the GEMM work."""
+    import torch
+    from paper_2607_05380_amd import tabpack
+    L, d_in = cfg["L"], cfg["d_in"]
+    pk = tabpack.Pack(dict(cfg, depth_lo=1, depth_hi=L, keep_grads=0)).bind(Xtr.device)
+    hp = pk.hparams()
+    idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
+    loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
+    pk.train_step(Xtr, ytr, idx, 1, loss)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for s in range(steps):
+        pk.train_step(Xtr, ytr, idx, s + 2, loss)
+    e1.record()
+    torch.cuda.synchronize()
+    work = sum(h["width"] * (d_in + (h["depth"] - 1) * h["width"]) for h in hp)
+    full = sum(h["width"] * (d_in + (L - 1) * h["width"]) for h in hp)
+    return {"depths": [sum(h["depth"] == d for h in hp) for d in range(1, L + 1)],
+            "step_ms": round(e0.elapsed_time(e1) / steps, 4), "gemm_work_vs_full_depth": round(work / full, 4)}
+
+
 def synth_idx(cfg, n, device):
     from paper_2607_05380_amd import synth
     return synth.epoch_orders_device(cfg, 1, n, device)[:, :cfg["B"]].contiguous()
@@ -270,6 +295,8 @@ def main():
         log("per-epoch work: validation, selection, member removal, online driver")
         out["per_epoch"], step = per_epoch(cfg, pk, Xtr, ytr, Xva, yva, step, a.online_epochs)
         log(f"  {json.dumps(out['per_epoch'])}")
+        out["variable_depth"] = variable_depth(cfg, Xtr, ytr)
+        log(f"  variable depth: {json.dumps(out['variable_depth'])}")
     if not a.no_cpu_baseline:
         log("timing the fp64 oracle on the host (bounded sample)")
         out["cpu_baseline"] = cpu_baseline(cfg, Xtr, ytr, idx_all[0])

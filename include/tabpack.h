@@ -48,13 +48,14 @@ enum { PACK_PREDICT_MEMBERS = 0, PACK_PREDICT_ENSEMBLE = 1 };
 
 /* Hyperparameters of one base model (Section 3.7: drawn per member from
  * user-given ranges; one hidden width shared by all hidden layers of the
- * member).  As input (pack_config.members) only width, dropout, lr and wd are
- * read; pack_get_hparams() also fills the derived fields. */
+ * member; App. F lists the number of layers among the sampled parameters).
+ * As input (pack_config.members) width, dropout, lr, wd and depth are read;
+ * pack_get_hparams() also fills the derived fields. */
 typedef struct pack_member_hp {
   int32_t width;           /* hidden width d_k, >= 1 */
   int32_t padded_width;    /* out: d_k rounded up to the quantum q */
   uint32_t drop_threshold; /* out: t_k = floor(p_k * 2^32); an element is kept iff its word >= t_k */
-  int32_t reserved;
+  int32_t depth;           /* hidden Linear-ReLU-Dropout blocks L_k in [1, L]; as input 0 means L */
   double dropout;          /* p_k in [0, 1) */
   double lr;               /* AdamW learning rate, > 0 */
   double wd;               /* AdamW decoupled weight decay, >= 0 */
@@ -69,7 +70,7 @@ typedef struct pack_config {
   int32_t K;          /* number of members, 1 .. 65535 */
   int32_t d_in;       /* input features, >= 1 */
   int32_t d_out;      /* outputs: 1 for PACK_TASK_REG_MSE / PACK_TASK_BIN_BCE, classes (2..16) for CE */
-  int32_t L;          /* hidden Linear-ReLU-Dropout blocks per member, 1 .. 8 */
+  int32_t L;          /* hidden Linear-ReLU-Dropout blocks per member (the maximum with a depth range), 1 .. 8 */
   int32_t B;          /* rows per member per step (base batch), 1 .. 65536 */
   int32_t task;       /* PACK_TASK_* */
   int32_t precision;  /* PACK_PREC_BF16: bf16 MFMA GEMMs, fp32 master weights; PACK_PREC_FP32: fp32 MFMA */
@@ -85,6 +86,9 @@ typedef struct pack_config {
   double beta1, beta2, eps; /* AdamW constants, e.g. 0.9, 0.999, 1e-8 */
   uint64_t seed;            /* hyperparameters, initial parameters and dropout masks derive from it */
   const pack_member_hp* members; /* optional [K] explicit hyperparameters; NULL: sample from the ranges */
+  int32_t depth_lo, depth_hi;    /* member depth L_k ~ UniformInt[depth_lo, depth_hi], 1 <= lo <= hi <= L;
+                                    0, 0: every member has L blocks.  L is the deepest member's depth:
+                                    a layer-l launch holds only the members with L_k >= l */
 } pack_config;
 
 typedef struct pack_handle pack_handle;
@@ -193,7 +197,7 @@ int pack_select(pack_handle* h, const float* cand, const void* yv, int32_t C, in
                 int32_t m_ens, void* work, size_t work_bytes, int32_t* sel_out,
                 int32_t* n_sel_out, double* score_out, hipStream_t stream);
 
-/* Number of floats in member k's dense parameter vector: for l = 1..L the
+/* Number of floats in member k's dense parameter vector: for l = 1..L_k the
  * row-major [d_k, fan_in] weight then its [d_k] bias, then the head's
  * [d_out, d_k] weight and [d_out] bias (torch.nn.Linear layout). */
 int pack_member_param_count(const pack_handle* h, int32_t member, int64_t* count);
@@ -214,7 +218,8 @@ int pack_get_moments(pack_handle* h, int32_t member, float* m_out, float* v_out)
  * [B, d_k]) of hidden layer `layer` (1-based) of member k at `step` to device
  * memory using the same device function as the training epilogue.
  * pack_debug_activation copies the stored post-dropout activation H_layer of
- * member k ([B, d_k] as fp32) of the last forward pass to a host buffer. */
+ * member k ([B, d_k] as fp32) of the last forward pass to a host buffer.
+ * layer must lie in [1, L_k]. */
 int pack_debug_dropout_mask(pack_handle* h, uint64_t step, int32_t layer, int32_t member,
                             uint8_t* dev_out, hipStream_t stream);
 int pack_debug_activation(pack_handle* h, int32_t layer, int32_t member, float* host_out);

@@ -10,7 +10,7 @@ predictions not), which gives every member exactly its standalone gradient.
 import numpy as np
 
 from . import mlp
-from .sampling import init_member, sample_hparams
+from .sampling import init_member, member_depth, sample_hparams
 
 
 class OraclePack:
@@ -29,7 +29,8 @@ class OraclePack:
         self.hp = hparams if hparams is not None else sample_hparams(cfg)
         keep = set(range(len(self.hp)) if members is None else members)
         if params is None:
-            params = [init_member(cfg, k, h["width"]) if k in keep else None for k, h in enumerate(self.hp)]
+            params = [init_member(cfg, k, h["width"], member_depth(cfg, h)) if k in keep else None
+                      for k, h in enumerate(self.hp)]
         self.params = [None if p is None else [(W.copy(), b.copy()) for W, b in p] for p in params]
         self.m = [None if p is None else [(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
         self.v = [None if p is None else [(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
@@ -39,7 +40,7 @@ class OraclePack:
     def masks(self, k, step):
         c, h = self.cfg, self.hp[k]
         return [mlp.dropout_mask(c["seed"], k, step, l + 1, c["B"], h["width"], h["t"])
-                for l in range(c["L"])]
+                for l in range(member_depth(c, h))]
 
     def member_step(self, k, X, y, idx_k, step):
         """Forward, loss, backward and AdamW for member k; returns (loss, grads)."""

@@ -10,21 +10,24 @@ weight decay:
     dropout ~ Uniform[dropout_lo, dropout_hi]
     lr      ~ LogUniform[lr_lo, lr_hi]
     wd      ~ LogUniform[wd_lo, wd_hi]
+    depth   ~ UniformInt[depth_lo, depth_hi]   (App. F: "# layers"; only when a
+              depth range is given, otherwise every member has L hidden blocks)
 
 Random words come from Philox4x32-10 (``oracle.philox``) with the stream tag
 folded into the key:  key = (seed mod 2**32, (seed >> 32) XOR (tag << 28)),
 tag 1 = hyperparameters, 2 = initial parameters, 3 = dropout.
 
 * hyperparameters of member k: block (k, 0, 0, 0) gives two doubles u0, u1
-  (width, dropout); block (k, 1, 0, 0) gives u2, u3 (lr, wd).  A double is
+  (width, dropout); block (k, 1, 0, 0) gives u2, u3 (lr, wd); block
+  (k, 2, 0, 0) gives u4 (depth; its last two words are unused).  A double is
   built from two words (a, b) as ((a >> 5) * 2**26 + (b >> 6)) * 2**-53.
 * initial parameters follow torch.nn.Linear's default: W and b uniform on
   [-1/sqrt(fan_in), 1/sqrt(fan_in)], fan_in = the member's true input width.
   Element e (row-major [out][in]) of tensor t of member k takes word (e & 3) of
   block (e >> 2 mod 2**32, e >> 34, t, k); u = (word >> 8) * 2**-24 and the
   value is float32((2u - 1) * bound), evaluated in float64.  Tensor ids:
-  W_l -> 2(l-1), b_l -> 2(l-1)+1 for hidden layers l = 1..L, W_out -> 2L,
-  b_out -> 2L+1.
+  W_l -> 2(l-1), b_l -> 2(l-1)+1 for hidden layers l = 1..L_k (the member's
+  depth), W_out -> 2 L_k, b_out -> 2 L_k + 1.
 
 Dropout: t_k = floor(p_k * 2**32) is the integer keep threshold and
 s_k = 1/(1 - p_k) the inverted-dropout scale (see ``mlp.dropout_mask``).
@@ -54,8 +57,10 @@ def _log_uniform(lo, hi, u):
 
 
 def sample_hparams(cfg):
-    """List of K dicts {width, dropout, lr, wd, t, s} for cfg (a plain dict)."""
+    """List of K dicts {width, dropout, lr, wd, depth, t, s} for cfg (a plain
+    dict; a depth range is given by depth_lo, depth_hi, absent or 0 for none)."""
     k0, k1 = stream_key(cfg["seed"], TAG_HPARAM)
+    dlo, dhi = int(cfg.get("depth_lo", 0) or 0), int(cfg.get("depth_hi", 0) or 0)
     out = []
     for k in range(cfg["K"]):
         w = [int(x) for x in philox4x32_10(k, 0, 0, 0, k0, k1)]
@@ -65,31 +70,43 @@ def sample_hparams(cfg):
         lo, hi = cfg["width_lo"], cfg["width_hi"]
         width = lo + int(math.floor(u0 * (hi - lo + 1)))
         p = cfg["dropout_lo"] + u1 * (cfg["dropout_hi"] - cfg["dropout_lo"])
+        depth = cfg.get("L")
+        if dlo > 0:
+            w = [int(x) for x in philox4x32_10(k, 2, 0, 0, k0, k1)]
+            depth = dlo + int(math.floor(_u53(w[0], w[1]) * (dhi - dlo + 1)))
         out.append(member_hparams(width, p,
                                   _log_uniform(cfg["lr_lo"], cfg["lr_hi"], u2),
-                                  _log_uniform(cfg["wd_lo"], cfg["wd_hi"], u3)))
+                                  _log_uniform(cfg["wd_lo"], cfg["wd_hi"], u3), depth))
     return out
 
 
-def member_hparams(width, dropout, lr, wd):
+def member_hparams(width, dropout, lr, wd, depth=None):
+    """depth None: the pack's L hidden blocks."""
     p = float(dropout)
     t = min(int(math.floor(p * 4294967296.0)), 0xFFFFFFFF)
     return dict(width=int(width), dropout=p, lr=float(lr), wd=float(wd),
-                t=t, s=1.0 / (1.0 - p))
+                t=t, s=1.0 / (1.0 - p), depth=None if depth is None else int(depth))
 
 
-def layer_shapes(cfg, width):
-    """[(out, in), ...] for W_1..W_L and the head W_out of one member."""
-    shapes = [(width, cfg["d_in"])] + [(width, width)] * (cfg["L"] - 1)
+def member_depth(cfg, hp):
+    """Hidden blocks of a member: its own depth, or the pack's L."""
+    d = hp.get("depth") if hp is not None else None
+    return int(cfg["L"]) if d is None else int(d)
+
+
+def layer_shapes(cfg, width, depth=None):
+    """[(out, in), ...] for W_1..W_depth and the head W_out of one member."""
+    L = int(cfg["L"]) if depth is None else int(depth)
+    shapes = [(width, cfg["d_in"])] + [(width, width)] * (L - 1)
     shapes.append((cfg["d_out"], width))
     return shapes
 
 
-def init_member(cfg, k, width):
+def init_member(cfg, k, width, depth=None):
     """Initial (W, b) pairs of member k, float32 values held in float64 arrays."""
     k0, k1 = stream_key(cfg["seed"], TAG_INIT)
     params = []
-    for i, (n_out, n_in) in enumerate(layer_shapes(cfg, width)):
+    for i, (n_out, n_in) in enumerate(layer_shapes(cfg, width, depth)):
         bound = 1.0 / math.sqrt(n_in)
         pair = []
         for t, n in ((2 * i, n_out * n_in), (2 * i + 1, n_out)):

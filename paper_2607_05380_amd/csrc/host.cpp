@@ -61,9 +61,10 @@ double log_uniform(double lo, double hi, double u) {
 
 struct Member {
   int width, dp;
+  int depth;  // hidden Linear-ReLU-Dropout blocks, 1 .. L
   double dropout, lr, wd, scale;
   uint32_t t;
-  std::vector<int64_t> toff;  // packed offsets of W_1, b_1, ..., W_L, b_L, W_out, b_out
+  std::vector<int64_t> toff;  // packed offsets of W_1, b_1, ..., W_depth, b_depth, W_out, b_out
   int64_t act_off;
 };
 
@@ -143,7 +144,7 @@ struct pack_handle {
   // measured faster than one launch over all members.
   int ngroups = 1;
   std::vector<int> group[kGroups];
-  int coltile0[kGroups + 1] = {};    // bias-partial column tiles of group g: [coltile0[g], coltile0[g+1])
+  std::vector<int> coltile0;         // bias-partial column tiles of group g, layer l: [coltile0[g L + l - 1], next)
   int headtile0[kGroups + 1] = {};   // head-backward tiles of group g
   int member0[kGroups + 1] = {};     // group g's members: d_members[member0[g] .. member0[g+1])
   hipStream_t gstream[kGroups] = {};  // streams of groups 1.. (entry 0 unused)
@@ -180,6 +181,9 @@ int validate(const pack_config* c) {
   if (c->K < 1 || c->K > 65535) return fail(PACK_EINVAL, "K=%d out of [1, 65535]", c->K);
   if (c->d_in < 1 || c->d_in > (1 << 20)) return fail(PACK_EINVAL, "d_in=%d out of range", c->d_in);
   if (c->L < 1 || c->L > 8) return fail(PACK_EINVAL, "L=%d out of [1, 8]", c->L);
+  if (!(c->depth_lo == 0 && c->depth_hi == 0) && !(1 <= c->depth_lo && c->depth_lo <= c->depth_hi && c->depth_hi <= c->L))
+    return fail(PACK_EINVAL, "depth range [%d, %d] must lie in [1, L=%d] (0, 0: every member has L blocks)",
+                c->depth_lo, c->depth_hi, c->L);
   if (c->B < 1 || c->B > 65536) return fail(PACK_EINVAL, "B=%d out of [1, 65536]", c->B);
   if (c->task < 0 || c->task > 2) return fail(PACK_EINVAL, "unknown task %d", c->task);
   if (c->precision != PACK_PREC_BF16 && c->precision != PACK_PREC_FP32)
@@ -216,6 +220,11 @@ void sample_members(pack_handle* h) {
     m.dropout = c.dropout_lo + u53(a.w2, a.w3) * (c.dropout_hi - c.dropout_lo);
     m.lr = log_uniform(c.lr_lo, c.lr_hi, u53(b.w0, b.w1));
     m.wd = log_uniform(c.wd_lo, c.wd_hi, u53(b.w2, b.w3));
+    m.depth = c.L;
+    if (c.depth_lo > 0) {  // depth ~ UniformInt[depth_lo, depth_hi] from block (k, 2, 0, 0)
+      const Words4 d = philox4x32_10((uint32_t)k, 2, 0, 0, key.k0, key.k1);
+      m.depth = c.depth_lo + (int)std::floor(u53(d.w0, d.w1) * (double)(c.depth_hi - c.depth_lo + 1));
+    }
   }
 }
 
@@ -233,9 +242,9 @@ void plan_layout(pack_handle* h) {
   for (int k = 0; k < c.K; ++k) {
     Member& m = h->mem[k];
     m.dp = (int)round_up(m.width, h->q);
-    m.toff.assign(2 * c.L + 2, 0);
-    for (int l = 0; l <= c.L; ++l) {
-      const int64_t rows = l < c.L ? m.dp : c.d_out;
+    m.toff.assign(2 * m.depth + 2, 0);
+    for (int l = 0; l <= m.depth; ++l) {
+      const int64_t rows = l < m.depth ? m.dp : c.d_out;
       const int64_t cols = l == 0 ? h->Pin : m.dp;
       for (int part = 0; part < 2; ++part) {
         const int64_t n = part == 0 ? rows * cols : rows;
@@ -243,7 +252,7 @@ void plan_layout(pack_handle* h) {
         const int64_t nc = round_up(n, kChunk) / kChunk;
         const uint32_t flag = (part == 1 && !c.decay_bias) ? 0x80000000u : 0u;
         // hidden-layer weights are updated inside their weight-gradient GEMM
-        const bool fused = part == 0 && l < c.L;
+        const bool fused = part == 0 && l < m.depth;
         for (int64_t i = 0; i < nc; ++i) {
           if (!fused) h->aux_chunks.push_back((uint32_t)h->chunk_tab.size());
           h->chunk_tab.push_back((uint32_t)k | flag);
@@ -267,8 +276,8 @@ void init_params(pack_handle* h) {
   const Key key = stream_key(c.seed, kTagInit);
   for (int k = 0; k < c.K; ++k) {
     const Member& m = h->mem[k];
-    for (int l = 0; l <= c.L; ++l) {
-      const int rows = l < c.L ? m.width : c.d_out;
+    for (int l = 0; l <= m.depth; ++l) {
+      const int rows = l < m.depth ? m.width : c.d_out;
       const int fan_in = l == 0 ? c.d_in : m.width;
       const int64_t ld = l == 0 ? h->Pin : m.dp;
       const double bound = 1.0 / std::sqrt((double)fan_in);
@@ -297,7 +306,7 @@ void init_params(pack_handle* h) {
 int64_t dense_count(const pack_handle* h, int k) {
   const Member& m = h->mem[k];
   const pack_config& c = h->cfg;
-  return (int64_t)m.width * c.d_in + m.width + (int64_t)(c.L - 1) * ((int64_t)m.width * m.width + m.width) +
+  return (int64_t)m.width * c.d_in + m.width + (int64_t)(m.depth - 1) * ((int64_t)m.width * m.width + m.width) +
          (int64_t)c.d_out * m.width + c.d_out;
 }
 
@@ -306,8 +315,8 @@ void for_each_dense(const pack_handle* h, int k, F f) {  // f(dense_index, packe
   const Member& m = h->mem[k];
   const pack_config& c = h->cfg;
   int64_t di = 0;
-  for (int l = 0; l <= c.L; ++l) {
-    const int rows = l < c.L ? m.width : c.d_out;
+  for (int l = 0; l <= m.depth; ++l) {
+    const int rows = l < m.depth ? m.width : c.d_out;
     const int cols = l == 0 ? c.d_in : m.width;
     const int64_t ld = l == 0 ? h->Pin : m.dp;
     for (int r = 0; r < rows; ++r)
@@ -331,7 +340,7 @@ struct Plan {
   std::vector<HeadTile> headtiles;
   std::vector<Launch> fwd[2][kGroups], dx[kGroups], dw[kGroups];
   Launch fwd1_eval{};
-  int coltile0[kGroups + 1] = {};
+  std::vector<int> coltile0;     // [kGroups * L + 1], see build_plan
   int headtile0[kGroups + 1] = {};
   std::vector<int32_t> members;  // member ids in group order
   int member0[kGroups + 1] = {};
@@ -428,7 +437,7 @@ void split_members(pack_handle* h) {
   std::vector<std::pair<double, int>> cost;
   for (int k : h->active_ids) {
     const double w = h->mem[k].dp;
-    cost.push_back({w * (h->Pin + (c.L - 1) * w), k});
+    cost.push_back({w * (h->Pin + (h->mem[k].depth - 1) * w), k});
   }
   std::stable_sort(cost.begin(), cost.end(), [](const auto& x, const auto& y) { return x.first > y.first; });
   std::vector<double> load(h->ngroups, 0.0);
@@ -467,10 +476,13 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
   for (int par = 0; par < 2; ++par)
   for (int hf = 0; hf < kGroups; ++hf)
   for (int l = 1; l <= c.L; ++l) {
-    // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp
-    Launch f{(int)p.descs.size(), (int)group[hf].size(), (int)p.tiles.size(), 0, 0.0};
+    // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp; members
+    // with fewer than l hidden blocks are not in the launch
+    Launch f{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
+      if (m.depth < l) continue;
+      ++f.ndesc;
       GemmDesc d{};
       d.A = l == 1 ? h0(k) : act(Hl(l - 1), k);
       d.lda = l == 1 ? h->Pin : m.dp;
@@ -518,9 +530,11 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
   for (int hf = 0; hf < kGroups; ++hf)
   for (int l = 1; l <= c.L; ++l) {
     // weight gradient: dW_l^T[out, in] = sum_rows dZ_l[row, out] H_{l-1}[row, in]
-    Launch w{(int)p.descs.size(), (int)group[hf].size(), (int)p.tiles.size(), 0, 0.0};
+    Launch w{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
+      if (m.depth < l) continue;
+      ++w.ndesc;
       GemmDesc d{};
       d.A = act(dzb(l), k);
       d.lda = m.dp;
@@ -551,9 +565,10 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     // data gradient (l >= 2): dZ_{l-1} = (dZ_l W_l) * [H_{l-1} > 0] * s_k
     Launch x{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
     if (l >= 2) {
-      x.ndesc = (int)group[hf].size();
       for (int k : group[hf]) {
         const Member& m = h->mem[k];
+        if (m.depth < l) continue;
+        ++x.ndesc;
         GemmDesc d{};
         d.A = act(dzb(l), k);
         d.lda = m.dp;
@@ -579,12 +594,19 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     }
     p.dx[hf].push_back(x);
   }
-  for (int hf = 0; hf < kGroups; ++hf) {
-    p.coltile0[hf] = (int)p.coltiles.size();
-    for (int k : group[hf])
-      for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
-  }
-  p.coltile0[kGroups] = (int)p.coltiles.size();
+  // bias-gradient column tiles of the dX launch of layer l (l >= 2) of group g:
+  // coltiles[coltile0[g * L + l - 1] .. coltile0[g * L + l]), the group's members
+  // with at least l hidden blocks
+  p.coltile0.assign((size_t)kGroups * c.L + 1, 0);
+  for (int hf = 0; hf < kGroups; ++hf)
+    for (int l = 1; l <= c.L; ++l) {
+      p.coltile0[(size_t)hf * c.L + l - 1] = (int)p.coltiles.size();
+      if (l >= 2)
+        for (int k : group[hf])
+          if (h->mem[k].depth >= l)
+            for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
+    }
+  p.coltile0[(size_t)kGroups * c.L] = (int)p.coltiles.size();
   const int hcols = head_bwd_cols(c.d_out), hrb = head_rows(h);
   for (int hf = 0; hf < kGroups; ++hf) {
     p.headtile0[hf] = (int)p.headtiles.size();
@@ -743,8 +765,8 @@ int upload_plan(pack_handle* h, hipStream_t stream) {
     h->dw[hf] = plan.dw[hf];
   }
   h->fwd1_eval = plan.fwd1_eval;
+  h->coltile0 = plan.coltile0;
   for (int i = 0; i <= kGroups; ++i) {
-    h->coltile0[i] = plan.coltile0[i];
     h->headtile0[i] = plan.headtile0[i];
     h->member0[i] = plan.member0[i];
   }
@@ -796,7 +818,7 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
     for (int k = 0; k < cfg->K; ++k) {
       const pack_member_hp& e = cfg->members[k];
       if (e.width < 1 || e.width > 16384 || !(e.dropout >= 0 && e.dropout < 1) || !(e.lr > 0) ||
-          !(e.wd >= 0)) {
+          !(e.wd >= 0) || e.depth < 0 || e.depth > cfg->L) {
         delete h;
         return fail(PACK_EINVAL, "explicit hyperparameters of member %d out of range", k);
       }
@@ -804,6 +826,7 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
       h->mem[k].dropout = e.dropout;
       h->mem[k].lr = e.lr;
       h->mem[k].wd = e.wd;
+      h->mem[k].depth = e.depth ? e.depth : cfg->L;
     }
   } else {
     sample_members(h);
@@ -844,7 +867,7 @@ int pack_get_hparams(const pack_handle* h, pack_member_hp* out) {
   if (!h || !out) return fail(PACK_EINVAL, "NULL argument");
   for (int k = 0; k < h->cfg.K; ++k) {
     const Member& m = h->mem[k];
-    out[k] = pack_member_hp{m.width, m.dp, m.t, 0, m.dropout, m.lr, m.wd, m.scale};
+    out[k] = pack_member_hp{m.width, m.dp, m.t, m.depth, m.dropout, m.lr, m.wd, m.scale};
   }
   return PACK_OK;
 }
@@ -882,8 +905,10 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
   for (int k = 0; k < h->cfg.K; ++k) {
     const Member& m = h->mem[k];
     md[k] = MemberDev{m.width, m.dp, m.t, (float)m.scale, (float)m.lr, (float)m.wd, m.act_off,
-                      m.toff[2 * h->cfg.L], m.toff[2 * h->cfg.L + 1], m.toff[2 * h->cfg.L - 1]};
-    for (int l = 1; l <= h->cfg.L; ++l) boff[(size_t)(l - 1) * h->cfg.K + k] = m.toff[2 * (l - 1) + 1];
+                      m.toff[2 * m.depth], m.toff[2 * m.depth + 1], m.toff[2 * m.depth - 1],
+                      (int64_t)(m.depth - 1) * h->A + m.act_off, (int64_t)(m.depth & 1) * h->A + m.act_off,
+                      m.depth, 0};
+    for (int l = 1; l <= m.depth; ++l) boff[(size_t)(l - 1) * h->cfg.K + k] = m.toff[2 * (l - 1) + 1];
   }
   HIP_TRY(hipMemcpyAsync(h->b.d_mem, md.data(), md.size() * sizeof(MemberDev), hipMemcpyHostToDevice, stream));
   HIP_TRY(hipMemcpyAsync(h->b.d_chunks, h->chunk_tab.data(), h->chunk_tab.size() * 4, hipMemcpyHostToDevice, stream));
@@ -956,7 +981,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   double nkeep = 0;
   for (int k : h->active_ids) {
     max_dp = std::max(max_dp, h->mem[k].dp);
-    nkeep += (double)c.L * h->Bp * h->mem[k].dp / 8;
+    nkeep += (double)h->mem[k].depth * h->Bp * h->mem[k].dp / 8;
   }
   // Dropout keep words (Philox, ALU-bound) run on the side stream: normally
   // they were produced during the previous step's backward pass; otherwise
@@ -998,7 +1023,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     const int32_t* gm = h->b.d_members + h->member0[hf];
     const int gk = h->member0[hf + 1] - h->member0[hf];
     HIP_TRY(timed(h, "head_fwd", 1, 0.0, act_bytes / ng, s, [&] {
-      return launch_head_fwd(h->prec, h->task, kHeadTrain, h->Hl(c.L), h->b.theta, h->b.d_mem, gk, h->Bp, c.d_out, y,
+      return launch_head_fwd(h->prec, h->task, kHeadTrain, h->b.H, h->b.theta, h->b.d_mem, gk, h->Bp, c.d_out, y,
                              idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, gm, s);
     }));
     HIP_TRY(timed(h, "loss_reduce", 1, 0.0, (double)gk * c.B * 4 * (1 + c.d_out), s, [&] {
@@ -1006,9 +1031,9 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                                 gm, s);
     }));
     HIP_TRY(timed(h, "head_bwd", 1, 0.0, 2.0 * act_bytes / ng, s, [&] {
-      return launch_head_bwd(h->prec, h->Hl(c.L), h->b.theta, h->b.d_mem, h->b.d_headtiles + h->headtile0[hf],
+      return launch_head_bwd(h->prec, h->b.H, h->b.theta, h->b.d_mem, h->b.d_headtiles + h->headtile0[hf],
                              h->headtile0[hf + 1] - h->headtile0[hf], h->Bp, h->head_rb, c.d_out, h->b.dY,
-                             h->dzb(c.L), h->b.headpart, s);
+                             h->b.dz, h->b.headpart, s);
     }));
     HIP_TRY(timed(h, "head_grad_reduce", 1, 0.0, 4.0 * (h->Bp / h->head_rb) * (c.d_out + 1) * (h->A / h->Bp) / ng, s,
                   [&] {
@@ -1030,8 +1055,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       if (l > 1) {
         HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[hf][l - 1], l, s));
         HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 / h->elt() / kPartRows / ng, s, [&] {
-          return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles + h->coltile0[hf],
-                                           h->coltile0[hf + 1] - h->coltile0[hf], h->Bp / kPartRows,
+          const int t0 = h->coltile0[(size_t)hf * c.L + l - 1], t1 = h->coltile0[(size_t)hf * c.L + l];
+          return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles + t0, t1 - t0, h->Bp / kPartRows,
                                            h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, s);
         }));
       }
@@ -1055,7 +1080,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   double naux = 0;
   for (int k : h->active_ids) {
     const Member& m = h->mem[k];
-    naux += (double)c.L * m.width + (double)c.d_out * m.width + c.d_out;
+    naux += (double)m.depth * m.width + (double)c.d_out * m.width + c.d_out;
   }
   HIP_TRY(timed(h, "adamw", 1, 0.0, naux * (h->prec == Prec::BF16 ? 30.0 : 28.0), stream, [&] {
     // biases and head weights: read in fp32 only, so no bf16 copy is written
@@ -1087,7 +1112,7 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
         HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
       }
     }
-    HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadEval, h->Hl(c.L), h->b.theta, h->b.d_mem, nact, h->Bp, c.d_out,
+    HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadEval, h->b.H, h->b.theta, h->b.d_mem, nact, h->Bp, c.d_out,
                             yv, nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, h->b.d_active,
                             stream));
   }
@@ -1118,12 +1143,12 @@ int pack_predict(pack_handle* h, const float* X, int64_t N, int32_t mode, float*
     }
     if (mode == PACK_PREDICT_MEMBERS) {
       // member i (i-th active id) writes rows r0.. of out[i, :, :]
-      HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadPredict, h->Hl(c.L), h->b.theta, h->b.d_mem, nact, h->Bp,
+      HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadPredict, h->b.H, h->b.theta, h->b.d_mem, nact, h->Bp,
                               c.d_out, nullptr, nullptr, c.B, a.rows_valid, r0, N, nullptr, nullptr, out,
                               h->b.d_active, stream));
     } else {
       // the chunk's member predictions go to the dY buffer ([K, Bp, d_out]), then their mean to out
-      HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadPredict, h->Hl(c.L), h->b.theta, h->b.d_mem, nact, h->Bp,
+      HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadPredict, h->b.H, h->b.theta, h->b.d_mem, nact, h->Bp,
                               c.d_out, nullptr, nullptr, c.B, a.rows_valid, 0, h->Bp, nullptr, nullptr, h->b.dY,
                               h->b.d_active, stream));
       HIP_TRY(launch_ensemble_mean(h->b.dY, nact, h->Bp, a.rows_valid, c.d_out, r0, out, stream));
@@ -1233,7 +1258,8 @@ int pack_debug_dropout_mask(pack_handle* h, uint64_t step, int32_t layer, int32_
                             hipStream_t stream) {
   int rc = check_member(h, member);
   if (rc) return rc;
-  if (layer < 1 || layer > h->cfg.L) return fail(PACK_EINVAL, "layer %d out of [1, %d]", layer, h->cfg.L);
+  if (layer < 1 || layer > h->mem[member].depth)
+    return fail(PACK_EINVAL, "layer %d out of [1, %d] for member %d", layer, h->mem[member].depth, member);
   if (!dev_out) return fail(PACK_EINVAL, "dev_out is NULL");
   const Key kd = stream_key(h->cfg.seed, kTagDropout);
   HIP_TRY(launch_dropout_mask(kd.k0, kd.k1, as_u32(step), layer, member, h->mem[member].t, h->cfg.B,
@@ -1245,7 +1271,8 @@ int pack_debug_activation(pack_handle* h, int32_t layer, int32_t member, float* 
   int rc = check_member(h, member);
   if (rc) return rc;
   if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
-  if (layer < 1 || layer > h->cfg.L) return fail(PACK_EINVAL, "layer %d out of [1, %d]", layer, h->cfg.L);
+  if (layer < 1 || layer > h->mem[member].depth)
+    return fail(PACK_EINVAL, "layer %d out of [1, %d] for member %d", layer, h->mem[member].depth, member);
   if (!host_out) return fail(PACK_EINVAL, "host_out is NULL");
   const Member& m = h->mem[member];
   const size_t n = (size_t)h->Bp * m.dp;

@@ -111,7 +111,8 @@ struct Vec8<float> {
 // output, P(class 1) or P(true class)) at pred[k * Nv + row_base + row]; or
 // all d_out prediction values (kHeadPredict: outputs, P(class 1) or the softmax
 // probabilities) at pred[((blockIdx.y * Nv) + row_base + row) * d_out + o].
-// D >= d_out is the output count rounded up to a power of two.
+// D >= d_out is the output count rounded up to a power of two.  H is the start
+// of the activation buffers; member k reads its last hidden layer at H + h_last.
 template <typename T, int MODE, int D>
 __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, const float* theta,
                                                        const MemberDev* mem, int Bp, int d_out,
@@ -124,7 +125,7 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, co
   const int row = blockIdx.x * 32 + (threadIdx.x >> 3);
   if (row >= Bp) return;  // Bp is a multiple of 32: whole 8-lane groups leave together
   const MemberDev md = mem[k];
-  const T* h = H + md.act_off + (int64_t)row * md.dp;
+  const T* h = H + md.h_last + (int64_t)row * md.dp;
   const float* Wo = theta + md.w_out_off;
   float acc[D];
 #pragma unroll
@@ -282,6 +283,8 @@ struct VecN<float, 4> {
 //   and this row block's partial sums of dW_out = dY^T H_L and db_L = sum dZ_L,
 //   reduced over the block's 8 row slots in a fixed order and stored to part
 //   (part[(rb * (d_out + 1) + o) * dp + c]; o = d_out holds db_L).
+//   H and dZ are the starts of the activation buffers and of the dZ pair; a
+//   member's L is its own depth (H + h_last, dZ + dz_last).
 template <typename T, int D, int CPT>
 __global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* theta, const MemberDev* mem,
                                                        const HeadTile* tiles, int Bp, int d_out, int RB,
@@ -302,8 +305,8 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* 
     }
 #pragma unroll
   for (int j = 0; j < CPT; ++j) accb[j] = 0.0f;
-  const T* h = H + md.act_off;
-  T* dz = dZ + md.act_off;
+  const T* h = H + md.h_last;
+  T* dz = dZ + md.dz_last;
   const float* dyk = dY + (int64_t)ht.member * Bp * d_out;
   const int r1 = min(ht.r0 + RB, Bp);
   for (int r = ht.r0 + slot; r < r1; r += 8) {
@@ -514,6 +517,7 @@ __global__ __launch_bounds__(256) void dropout_words_kernel(uint32_t key0, uint3
                                                             int64_t A32, uint32_t* out, const int32_t* members) {
   const int k = members ? members[blockIdx.y] : (int)blockIdx.y, l = blockIdx.z + 1;
   const MemberDev md = mem[k];
+  if (l > md.depth) return;  // the member has no layer l
   const int64_t nw = (int64_t)(Bp / 32) * md.dp;
   const int64_t w = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (w >= nw) return;

@@ -99,6 +99,10 @@ struct MemberDev {
   float lr, wd;
   int64_t act_off;          // member offset inside one activation buffer (elements)
   int64_t w_out_off, b_out_off, b_last_off;  // head weight, head bias, last hidden bias (elements of theta)
+  int64_t h_last;           // the member's last hidden activation H_depth: offset from the start of H_1 (elements)
+  int64_t dz_last;          // its gradient dZ_depth: offset from the start of the dZ ping-pong pair (elements)
+  int32_t depth;            // hidden blocks of the member
+  int32_t pad_;
 };
 
 struct HeadTile {            // (member, first column, first row) block of the head backward

@@ -28,7 +28,7 @@ SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "
 
 class MemberHP(ctypes.Structure):
     _fields_ = [("width", ctypes.c_int32), ("padded_width", ctypes.c_int32),
-                ("drop_threshold", ctypes.c_uint32), ("reserved", ctypes.c_int32),
+                ("drop_threshold", ctypes.c_uint32), ("depth", ctypes.c_int32),
                 ("dropout", ctypes.c_double), ("lr", ctypes.c_double), ("wd", ctypes.c_double),
                 ("scale", ctypes.c_double)]
 
@@ -43,7 +43,8 @@ class PackConfig(ctypes.Structure):
                 ("lr_lo", ctypes.c_double), ("lr_hi", ctypes.c_double),
                 ("wd_lo", ctypes.c_double), ("wd_hi", ctypes.c_double),
                 ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
-                ("seed", ctypes.c_uint64), ("members", ctypes.POINTER(MemberHP))]
+                ("seed", ctypes.c_uint64), ("members", ctypes.POINTER(MemberHP)),
+                ("depth_lo", ctypes.c_int32), ("depth_hi", ctypes.c_int32)]
 
 
 class KernelStat(ctypes.Structure):
@@ -106,8 +107,9 @@ def _check(rc):
 
 
 def make_config(cfg, members=None):
-    """PackConfig from a workload dict (see ``configs``); members: optional list of
-    dicts {width, dropout, lr, wd} overriding the sampled hyperparameters."""
+    """PackConfig from a workload dict (see ``configs``; optional depth_lo/depth_hi
+    give each member a depth drawn from that range); members: optional list of
+    dicts {width, dropout, lr, wd[, depth]} overriding the sampled hyperparameters."""
     c = PackConfig()
     for f in ("K", "d_in", "d_out", "L", "B", "width_lo", "width_hi"):
         setattr(c, f, int(cfg.get(f, 0)))
@@ -122,6 +124,8 @@ def make_config(cfg, members=None):
     c.beta2 = float(cfg.get("beta2", 0.999))
     c.eps = float(cfg.get("eps", 1e-8))
     c.seed = int(cfg["seed"])
+    c.depth_lo = int(cfg.get("depth_lo", 0) or 0)
+    c.depth_hi = int(cfg.get("depth_hi", 0) or 0)
     keep = None
     if members is not None:
         keep = (MemberHP * len(members))()
@@ -130,6 +134,7 @@ def make_config(cfg, members=None):
             keep[i].dropout = float(m["dropout"])
             keep[i].lr = float(m["lr"])
             keep[i].wd = float(m["wd"])
+            keep[i].depth = int(m.get("depth") or 0)
         c.members = ctypes.cast(keep, ctypes.POINTER(MemberHP))
     return c, keep
 
@@ -167,7 +172,7 @@ class Pack:
     def hparams(self):
         arr = (MemberHP * self.K)()
         _check(self.lib.pack_get_hparams(self.h, arr))
-        return [dict(width=a.width, padded_width=a.padded_width, t=a.drop_threshold,
+        return [dict(width=a.width, padded_width=a.padded_width, t=a.drop_threshold, depth=a.depth,
                      dropout=a.dropout, lr=a.lr, wd=a.wd, s=a.scale) for a in arr]
 
     def workspace_bytes(self):
@@ -276,10 +281,11 @@ class Pack:
 
     def split(self, k, flat):
         """Dense member vector -> [(W [out, in], b [out]), ...] for the L blocks and the head."""
-        w = self.hparams()[k]["width"] if not hasattr(self, "_widths") else self._widths[k]
-        dims = [self.d_in] + [w] * self.L + [self.d_out]
+        hp = self.hparams()[k]
+        w, depth = hp["width"], hp["depth"]
+        dims = [self.d_in] + [w] * depth + [self.d_out]
         out, o = [], 0
-        for i in range(self.L + 1):
+        for i in range(depth + 1):
             n_in, n_out = dims[i], dims[i + 1]
             W = flat[o:o + n_in * n_out].reshape(n_out, n_in)
             o += n_in * n_out

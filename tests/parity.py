@@ -51,13 +51,15 @@ ORACLE_KEYS = ("seed", "K", "d_in", "d_out", "L", "B", "task", "beta1", "beta2",
 
 
 def oracle_cfg(cfg):
-    return {k: cfg[k] for k in ORACLE_KEYS}
+    out = {k: cfg[k] for k in ORACLE_KEYS}
+    out["depth_lo"], out["depth_hi"] = cfg.get("depth_lo", 0), cfg.get("depth_hi", 0)
+    return out
 
 
 def oracle_hparams(cfg, members=None):
     if members is None:
         return sample_hparams(oracle_cfg(cfg))
-    return [member_hparams(m["width"], m["dropout"], m["lr"], m["wd"]) for m in members]
+    return [member_hparams(m["width"], m["dropout"], m["lr"], m["wd"], m.get("depth")) for m in members]
 
 
 def close_mask(gpu, ref, rtol, atol):

@@ -29,8 +29,10 @@ def test_library_exports_every_declared_symbol():
 
 
 def oracle_cfg(cfg):
-    return {k: cfg[k] for k in ("seed", "K", "d_in", "d_out", "L", "width_lo", "width_hi", "dropout_lo",
-                                "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi")}
+    out = {k: cfg[k] for k in ("seed", "K", "d_in", "d_out", "L", "width_lo", "width_hi", "dropout_lo",
+                               "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi")}
+    out["depth_lo"], out["depth_hi"] = cfg.get("depth_lo", 0), cfg.get("depth_hi", 0)
+    return out
 
 
 @pytest.mark.parametrize("name", configs.ORDER)
@@ -103,3 +105,33 @@ def test_state_errors_without_bind():
     assert lib.pack_workspace_size(pk.h, ctypes.byref(n)) == 0 and n.value > 0
     assert lib.pack_select_workspace_size(0, 10, ctypes.byref(n)) == -1
     assert lib.pack_init(None, ctypes.byref(ctypes.c_void_p())) == -1
+
+
+def test_sampled_depths_and_init_match_oracle():
+    # App. F samples the number of layers per member: depth ~ UniformInt[lo, hi]
+    cfg = configs.workload("regression_onehot", K=40, L=4, depth_lo=1, depth_hi=4)
+    pk = tabpack.Pack(cfg)
+    got = pk.hparams()
+    ref = sample_hparams(oracle_cfg(cfg))
+    assert [g["depth"] for g in got] == [r["depth"] for r in ref]
+    assert set(g["depth"] for g in got) == {1, 2, 3, 4}
+    for k in range(6):
+        p = pk.get_params(k)
+        r = init_member(oracle_cfg(cfg), k, got[k]["width"], got[k]["depth"])
+        assert len(p) == len(r) == got[k]["depth"] + 1
+        for (W, b), (Wr, br) in zip(p, r):
+            np.testing.assert_array_equal(W, Wr.astype(np.float32))
+            np.testing.assert_array_equal(b, br.astype(np.float32))
+    # without a range every member has L blocks; explicit depths are taken as given
+    assert all(h["depth"] == 4 for h in tabpack.Pack(dict(cfg, depth_lo=0, depth_hi=0)).hparams())
+    one = tabpack.Pack(dict(cfg, K=2), members=[dict(width=9, dropout=0.1, lr=1e-3, wd=1e-3, depth=2),
+                                                 dict(width=9, dropout=0.1, lr=1e-3, wd=1e-3)])
+    assert [h["depth"] for h in one.hparams()] == [2, 4]
+    assert one.param_count(0) == 9 * 64 + 9 + 9 * 9 + 9 + 9 + 1
+
+
+@pytest.mark.parametrize("lo,hi", [(0, 2), (2, 1), (1, 5), (-1, 3)])
+def test_invalid_depth_ranges_rejected(lo, hi):
+    cfg = configs.workload("regression_onehot", K=2, L=4, depth_lo=lo, depth_hi=hi)
+    with pytest.raises(tabpack.PackError, match="depth"):
+        tabpack.Pack(cfg)

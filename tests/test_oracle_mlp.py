@@ -263,3 +263,28 @@ def test_bf16_policy_matches_torch_straight_through(task, d_out):
     for l in range(3):
         np.testing.assert_allclose(grads[l][0], tW[l].grad.numpy(), rtol=1e-10, atol=1e-14)
         np.testing.assert_allclose(grads[l][1], tb[l].grad.numpy(), rtol=1e-10, atol=1e-14)
+
+
+@pytest.mark.parametrize("depths", [(1, 3, 2), (4, 1, 1)])
+def test_pack_members_of_different_depths_match_torch_autograd(depths):
+    # a pack whose members have their own number of hidden blocks: each member's
+    # loss and gradients equal torch float64 autograd of a network of that depth
+    cfg = dict(seed=11, K=len(depths), d_in=4, d_out=1, L=max(depths), B=9, task=mlp.TASK_REG,
+               beta1=0.9, beta2=0.999, eps=1e-8, decay_bias=1)
+    hp = [member_hparams(6 + k, 0.25, 1e-3, 1e-2, d) for k, d in enumerate(depths)]
+    op = OraclePack(cfg, hparams=hp)
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((30, 4))
+    y = rng.standard_normal(30)
+    idx = np.stack([rng.permutation(30)[:9] for _ in depths])
+    p0 = [[(W.copy(), b.copy()) for W, b in p] for p in op.params]
+    losses = op.train_step(X, y, idx, 1)
+    for k, d in enumerate(depths):
+        assert len(p0[k]) == d + 1 and len(op.masks(k, 1)) == d
+        layers, fwd = _torch_member(p0[k], op.masks(k, 1), hp[k]["s"])
+        tl = _torch_loss(fwd(X[idx[k]]), y[idx[k]], mlp.TASK_REG)
+        tl.backward()
+        assert abs(tl.item() - losses[k]) <= 1e-12 * max(1.0, abs(losses[k]))
+        for l, lin in enumerate(layers):
+            np.testing.assert_allclose(op.last_grads[k][l][0], lin.weight.grad.numpy(), rtol=1e-10, atol=1e-13)
+            np.testing.assert_allclose(op.last_grads[k][l][1], lin.bias.grad.numpy(), rtol=1e-10, atol=1e-13)

@@ -32,6 +32,23 @@ def test_sampler_ranges_and_distributions():
     assert sample_hparams(dict(CFG, K=5, seed=1)) != hp[:5]
 
 
+def test_sampler_depths():
+    # depth ~ UniformInt[lo, hi]: every value in range, counts within 5 sigma of
+    # the binomial; the other draws do not change when a depth range is added
+    hp = sample_hparams(dict(CFG, L=4, depth_lo=2, depth_hi=4))
+    d = np.array([h["depth"] for h in hp])
+    assert d.min() == 2 and d.max() == 4
+    n, p = len(d), 1.0 / 3.0
+    for v in (2, 3, 4):
+        assert abs((d == v).sum() - n * p) <= 5 * np.sqrt(n * p * (1 - p))
+    base = sample_hparams(dict(CFG, L=4))
+    assert all(h["depth"] == 4 for h in base)
+    assert [{k: h[k] for k in ("width", "dropout", "lr", "wd")} for h in hp] == \
+        [{k: h[k] for k in ("width", "dropout", "lr", "wd")} for h in base]
+    one = sample_hparams(dict(CFG, K=50, L=3, depth_lo=3, depth_hi=3))
+    assert all(h["depth"] == 3 for h in one)
+
+
 def test_degenerate_ranges():
     hp = sample_hparams(dict(CFG, K=20, width_lo=64, width_hi=64, dropout_lo=0.0, dropout_hi=0.0,
                              lr_lo=1e-3, lr_hi=1e-3))
