@@ -26,7 +26,8 @@ COPY_BYTES = 256 << 20
 OPS = ["kmaj", "rmaj"]
 EPIS = ["fwd", "fwd_eval", "dx", "dw"]
 SIMPLE = ["dropout_words", "head_grad_reduce", "head_fwd", "head_bwd", "loss_reduce", "bias_from_partials",
-          "gather", "adamw", "to_shadow", "eval_score", "dropout_mask"]
+          "gather", "adamw", "to_shadow", "eval_score", "dropout_mask", "select_partial", "select_pick",
+          "select_update", "select_init", "select_final", "ensemble_mean"]
 
 
 def source_digest():
