@@ -9,7 +9,7 @@ predictions not), which gives every member exactly its standalone gradient.
 """
 import numpy as np
 
-from . import mlp
+from . import mlp, muon
 from .sampling import init_member, member_depth, sample_hparams
 
 
@@ -43,8 +43,13 @@ class OraclePack:
                 for l in range(member_depth(c, h))]
 
     def member_step(self, k, X, y, idx_k, step):
-        """Forward, loss, backward and AdamW for member k; returns (loss, grads)."""
+        """Forward, loss, backward and the optimizer step for member k; returns
+        (loss, grads).  With cfg["optimizer"] == "muon" the hidden weights take a
+        Muon step (learning rate hp["muon_lr"], momentum buffer in ``m``) and
+        every other parameter an AdamW step; otherwise everything is AdamW."""
         c, h = self.cfg, self.hp[k]
+        use_muon = c.get("optimizer", "adamw") == "muon"
+        depth = len(self.params[k]) - 1
         rows = np.asarray(idx_k, dtype=np.int64)
         masks = self.masks(k, step)
         Y, cache = mlp.forward(self.params[k], X[rows], masks, h["s"], rnd=self.rnd)
@@ -54,7 +59,13 @@ class OraclePack:
         for i, ((W, b), (gW, gb), (mW, mb), (vW, vb)) in enumerate(
                 zip(self.params[k], grads, self.m[k], self.v[k])):
             args = (step, h["lr"], h["wd"], c["beta1"], c["beta2"], c["eps"])
-            W2, mW2, vW2 = mlp.adamw_step(W, gW, mW, vW, *args)
+            if use_muon and i < depth:
+                W2, mW2 = muon.muon_step(W, gW, mW, h["muon_lr"], h["wd"], c.get("muon_momentum", 0.95),
+                                         bool(c.get("muon_nesterov", 1)), int(c.get("ns_steps", 5)),
+                                         rnd=self.rnd)
+                vW2 = vW
+            else:
+                W2, mW2, vW2 = mlp.adamw_step(W, gW, mW, vW, *args)
             b2, mb2, vb2 = mlp.adamw_step(b, gb, mb, vb, *args, decay=bool(c["decay_bias"]))
             new_p.append((W2, b2))
             new_m.append((mW2, mb2))

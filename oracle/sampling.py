@@ -12,6 +12,8 @@ weight decay:
     wd      ~ LogUniform[wd_lo, wd_hi]
     depth   ~ UniformInt[depth_lo, depth_hi]   (App. F: "# layers"; only when a
               depth range is given, otherwise every member has L hidden blocks)
+    muon_lr ~ LogUniform[muon_lr_lo, muon_lr_hi]  (App. F: "Muon learning rate";
+              only with the Muon optimizer)
 
 Random words come from Philox4x32-10 (``oracle.philox``) with the stream tag
 folded into the key:  key = (seed mod 2**32, (seed >> 32) XOR (tag << 28)),
@@ -19,7 +21,8 @@ tag 1 = hyperparameters, 2 = initial parameters, 3 = dropout.
 
 * hyperparameters of member k: block (k, 0, 0, 0) gives two doubles u0, u1
   (width, dropout); block (k, 1, 0, 0) gives u2, u3 (lr, wd); block
-  (k, 2, 0, 0) gives u4 (depth; its last two words are unused).  A double is
+  (k, 2, 0, 0) gives u4 (depth; its last two words are unused); block
+  (k, 3, 0, 0) gives u5 (the Muon learning rate; last two words unused).  A double is
   built from two words (a, b) as ((a >> 5) * 2**26 + (b >> 6)) * 2**-53.
 * initial parameters follow torch.nn.Linear's default: W and b uniform on
   [-1/sqrt(fan_in), 1/sqrt(fan_in)], fan_in = the member's true input width.
@@ -74,18 +77,24 @@ def sample_hparams(cfg):
         if dlo > 0:
             w = [int(x) for x in philox4x32_10(k, 2, 0, 0, k0, k1)]
             depth = dlo + int(math.floor(_u53(w[0], w[1]) * (dhi - dlo + 1)))
-        out.append(member_hparams(width, p,
-                                  _log_uniform(cfg["lr_lo"], cfg["lr_hi"], u2),
-                                  _log_uniform(cfg["wd_lo"], cfg["wd_hi"], u3), depth))
+        hp = member_hparams(width, p, _log_uniform(cfg["lr_lo"], cfg["lr_hi"], u2),
+                            _log_uniform(cfg["wd_lo"], cfg["wd_hi"], u3), depth)
+        if cfg.get("optimizer", "adamw") == "muon":
+            w = [int(x) for x in philox4x32_10(k, 3, 0, 0, k0, k1)]
+            hp["muon_lr"] = _log_uniform(cfg["muon_lr_lo"], cfg["muon_lr_hi"], _u53(w[0], w[1]))
+        out.append(hp)
     return out
 
 
-def member_hparams(width, dropout, lr, wd, depth=None):
-    """depth None: the pack's L hidden blocks."""
+def member_hparams(width, dropout, lr, wd, depth=None, muon_lr=None):
+    """depth None: the pack's L hidden blocks; muon_lr only for Muon packs."""
     p = float(dropout)
     t = min(int(math.floor(p * 4294967296.0)), 0xFFFFFFFF)
-    return dict(width=int(width), dropout=p, lr=float(lr), wd=float(wd),
-                t=t, s=1.0 / (1.0 - p), depth=None if depth is None else int(depth))
+    out = dict(width=int(width), dropout=p, lr=float(lr), wd=float(wd),
+               t=t, s=1.0 / (1.0 - p), depth=None if depth is None else int(depth))
+    if muon_lr is not None:
+        out["muon_lr"] = float(muon_lr)
+    return out
 
 
 def member_depth(cfg, hp):
