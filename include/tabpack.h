@@ -45,6 +45,7 @@ extern "C" {
 enum { PACK_TASK_REG_MSE = 0, PACK_TASK_BIN_BCE = 1, PACK_TASK_MULTI_CE = 2 };
 enum { PACK_PREC_BF16 = 0, PACK_PREC_FP32 = 1 };
 enum { PACK_PREDICT_MEMBERS = 0, PACK_PREDICT_ENSEMBLE = 1 };
+enum { PACK_OPT_ADAMW = 0, PACK_OPT_MUON = 1 };
 
 /* Hyperparameters of one base model (Section 3.7: drawn per member from
  * user-given ranges; one hidden width shared by all hidden layers of the
@@ -60,6 +61,7 @@ typedef struct pack_member_hp {
   double lr;               /* AdamW learning rate, > 0 */
   double wd;               /* AdamW decoupled weight decay, >= 0 */
   double scale;            /* out: inverted-dropout scale s_k = 1 / (1 - p_k) */
+  double muon_lr;          /* Muon learning rate of the hidden weights (PACK_OPT_MUON), > 0 */
 } pack_member_hp;
 
 /* Description of a pack.  Ranges are inclusive: width ~ UniformInt[lo, hi],
@@ -89,6 +91,22 @@ typedef struct pack_config {
   int32_t depth_lo, depth_hi;    /* member depth L_k ~ UniformInt[depth_lo, depth_hi], 1 <= lo <= hi <= L;
                                     0, 0: every member has L blocks.  L is the deepest member's depth:
                                     a layer-l launch holds only the members with L_k >= l */
+  /* Optimizer pack (Section 3.4; the paper's default trains the main weights of
+   * the backbone's linear layers with Muon and every other parameter with
+   * AdamW).  PACK_OPT_ADAMW: AdamW everywhere.  PACK_OPT_MUON: the hidden
+   * weights W_1..W_Lk take Muon steps (Jordan et al., 2024): momentum buffer
+   * B <- mu B + G, direction U = G + mu B (Nesterov) or B, ns_steps
+   * Newton-Schulz iterations X <- a X + (b A + c A A) X with A = X X^T from
+   * X = U / (||U||_F + 1e-7) (U^T when the true rows exceed the true columns),
+   * (a, b, c) = (3.4445, -4.7750, 2.0315), then W <- W (1 - lr_muon wd) -
+   * lr_muon max(1, rows/cols)^(1/2) X with the true shape; biases and the head
+   * stay on AdamW.  Muon learning rates ~ LogUniform[muon_lr_lo, muon_lr_hi]. */
+  int32_t optimizer;             /* PACK_OPT_* */
+  int32_t ns_steps;              /* Newton-Schulz iterations, 1 .. 16 (0 selects 5) */
+  double muon_lr_lo, muon_lr_hi;
+  double muon_momentum;          /* mu in [0, 1) */
+  int32_t muon_nesterov;         /* 1: Nesterov direction, 0: the momentum buffer */
+  int32_t reserved;
 } pack_config;
 
 typedef struct pack_handle pack_handle;

@@ -63,6 +63,7 @@ struct Member {
   int width, dp;
   int depth;  // hidden Linear-ReLU-Dropout blocks, 1 .. L
   double dropout, lr, wd, scale;
+  double muon_lr = 0.0;  // Muon learning rate of the hidden weights (Muon packs)
   uint32_t t;
   std::vector<int64_t> toff;  // packed offsets of W_1, b_1, ..., W_depth, b_depth, W_out, b_out
   int64_t act_off;
@@ -112,6 +113,16 @@ struct Bufs {
   HeadTile* d_headtiles = nullptr;
   int32_t* d_members = nullptr;
   int32_t* d_active = nullptr;  // active member ids, increasing
+  // Muon scratch: two X buffers, A, B' (GEMM precision), tile partial norms,
+  // inverse norms and the matrix / tile tables
+  char* mX[2] = {nullptr, nullptr};
+  char* mA = nullptr;
+  char* mB = nullptr;
+  double* mpart = nullptr;
+  float* minv = nullptr;
+  MuonMat* d_mmats = nullptr;
+  MuonTile* d_mtiles = nullptr;
+  int32_t* d_mtile0 = nullptr;
   float* headpart = nullptr;  // head backward partials, (Bp / RB) * (d_out + 1) * A / Bp floats
 };
 
@@ -131,6 +142,10 @@ struct pack_handle {
   std::vector<uint8_t> active;
   std::vector<int32_t> active_ids;   // increasing
   int64_t n_aux_active = 0;          // aux chunks of active members (uploaded first in d_aux)
+  bool muon = false;                 // hidden weights on Muon (pack_config.optimizer)
+  int ns_steps = 5;
+  int n_mmats = 0, n_mtiles = 0;     // Muon matrices and tiles of the active members
+  Launch nsA[2]{}, nsB{}, nsX[2]{};
 
   bool bound = false;
   Bufs b;
@@ -198,6 +213,14 @@ int validate(const pack_config* c) {
   if (c->keep_grads != 0 && c->keep_grads != 1) return fail(PACK_EINVAL, "keep_grads must be 0 or 1");
   if (!(c->beta1 >= 0 && c->beta1 < 1 && c->beta2 >= 0 && c->beta2 < 1 && c->eps > 0))
     return fail(PACK_EINVAL, "AdamW constants out of range");
+  if (c->optimizer != PACK_OPT_ADAMW && c->optimizer != PACK_OPT_MUON)
+    return fail(PACK_EINVAL, "unknown optimizer %d", c->optimizer);
+  if (c->optimizer == PACK_OPT_MUON) {
+    if (c->ns_steps < 0 || c->ns_steps > 16) return fail(PACK_EINVAL, "ns_steps=%d out of [1, 16]", c->ns_steps);
+    if (!(c->muon_momentum >= 0 && c->muon_momentum < 1)) return fail(PACK_EINVAL, "Muon momentum out of [0, 1)");
+    if (!c->members && !(c->muon_lr_lo > 0 && c->muon_lr_hi >= c->muon_lr_lo))
+      return fail(PACK_EINVAL, "Muon learning-rate range must be positive and ordered");
+  }
   if (!c->members) {
     if (c->width_lo < 1 || c->width_hi < c->width_lo || c->width_hi > 16384)
       return fail(PACK_EINVAL, "width range [%d, %d] invalid", c->width_lo, c->width_hi);
@@ -224,6 +247,10 @@ void sample_members(pack_handle* h) {
     if (c.depth_lo > 0) {  // depth ~ UniformInt[depth_lo, depth_hi] from block (k, 2, 0, 0)
       const Words4 d = philox4x32_10((uint32_t)k, 2, 0, 0, key.k0, key.k1);
       m.depth = c.depth_lo + (int)std::floor(u53(d.w0, d.w1) * (double)(c.depth_hi - c.depth_lo + 1));
+    }
+    if (c.optimizer == PACK_OPT_MUON) {  // Muon learning rate from block (k, 3, 0, 0)
+      const Words4 d = philox4x32_10((uint32_t)k, 3, 0, 0, key.k0, key.k1);
+      m.muon_lr = log_uniform(c.muon_lr_lo, c.muon_lr_hi, u53(d.w0, d.w1));
     }
   }
 }
@@ -344,6 +371,13 @@ struct Plan {
   int headtile0[kGroups + 1] = {};
   std::vector<int32_t> members;  // member ids in group order
   int member0[kGroups + 1] = {};
+  // Muon: the hidden weights, their 64 x 64 tiles (matrix k owns tiles
+  // mtile0[k] .. mtile0[k+1]) and the Newton-Schulz products: A = X X^T and
+  // X' = a X + B' X for each parity of the X buffers, B' = b A + c A A
+  std::vector<MuonMat> mmats;
+  std::vector<MuonTile> mtiles;
+  std::vector<int32_t> mtile0;
+  Launch nsA[2]{}, nsB{}, nsX[2]{};
 };
 
 // Tiles of one member's M x N output.  Big set: 256 x 256 tiles, except that
@@ -451,6 +485,152 @@ void split_members(pack_handle* h) {
 
 // Rows per head-backward block: up to 256, dividing Bp.
 int head_rows(const pack_handle* h) { return h->Bp % 256 == 0 ? 256 : h->Bp; }
+
+// Shape of the Newton-Schulz iterate of member m's hidden weight l (1-based):
+// padded [R x Cp] storage; X is [S x L], U or U^T (tall: true rows > true columns).
+struct MuonShape {
+  int R, Cp, S, L, r, c;
+  bool tall;
+};
+MuonShape muon_shape(const pack_handle* h, const Member& m, int l) {
+  MuonShape q;
+  q.R = m.dp;
+  q.Cp = l == 1 ? h->Pin : m.dp;
+  q.r = m.width;
+  q.c = l == 1 ? h->cfg.d_in : m.width;
+  q.tall = q.r > q.c;
+  q.S = q.tall ? q.Cp : q.R;
+  q.L = q.tall ? q.R : q.Cp;
+  return q;
+}
+
+// Elements of one X buffer and of the A (or B') buffer for the given members.
+template <typename It>
+void muon_sizes(const pack_handle* h, It begin, It end, int64_t& xe, int64_t& ae) {
+  xe = ae = 0;
+  for (It it = begin; it != end; ++it) {
+    const Member& m = h->mem[*it];
+    for (int l = 1; l <= m.depth; ++l) {
+      const MuonShape q = muon_shape(h, m, l);
+      xe += round_up((int64_t)q.S * q.L, kChunk);
+      ae += round_up((int64_t)q.S * q.S, kChunk);
+    }
+  }
+}
+
+void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&group)[kGroups], Plan& p) {
+  const size_t es = h->elt();
+  const TileSet saved = p.tile_set;
+  p.tile_set = TILES_SMALL;  // the Newton-Schulz GEMMs run small tiles only
+  for (int par = 0; par < 2; ++par) {
+    p.nsA[par] = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
+    p.nsX[par] = Launch{};
+  }
+  int64_t xo = 0, ao = 0;
+  struct Item {
+    MuonShape q;
+    int64_t xoff, aoff;
+  };
+  std::vector<Item> items;
+  p.mtile0.push_back(0);
+  for (int hf = 0; hf < kGroups; ++hf)
+    for (int k : group[hf]) {
+      const Member& m = h->mem[k];
+      for (int l = 1; l <= m.depth; ++l) {
+        const MuonShape q = muon_shape(h, m, l);
+        MuonMat mm{};
+        mm.woff = m.toff[2 * (l - 1)];
+        mm.xoff = xo;
+        mm.aoff = ao;
+        mm.R = q.R;
+        mm.Cp = q.Cp;
+        mm.tall = q.tall ? 1 : 0;
+        mm.member = k;
+        mm.decay = (float)(1.0 - m.muon_lr * m.wd);
+        mm.step = (float)(m.muon_lr * std::sqrt(std::max(1.0, (double)q.r / q.c)));
+        const int mi = (int)p.mmats.size();
+        p.mmats.push_back(mm);
+        for (int r0 = 0; r0 < q.R; r0 += 64)
+          for (int c0 = 0; c0 < q.Cp; c0 += 64) p.mtiles.push_back(MuonTile{mi, r0, c0, 0});
+        p.mtile0.push_back((int32_t)p.mtiles.size());
+        items.push_back(Item{q, xo, ao});
+        xo += round_up((int64_t)q.S * q.L, kChunk);
+        ao += round_up((int64_t)q.S * q.S, kChunk);
+      }
+    }
+  auto xp = [&](int par, int64_t off) { return (void*)(bf.mX[par] + (size_t)off * es); };
+  auto ap = [&](const char* base, int64_t off) { return (void*)(base + (size_t)off * es); };
+  // A = X X^T, one launch per parity of the X buffer it reads
+  for (int par = 0; par < 2; ++par) {
+    Launch& ln = p.nsA[par];
+    ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
+    for (const Item& it : items) {
+      GemmDesc d{};
+      d.A = d.B = xp(par, it.xoff);
+      d.lda = d.ldb = it.q.L;
+      d.C = ap(bf.mA, it.aoff);
+      d.ldc = it.q.S;
+      d.M = d.N = it.q.S;
+      d.Kd = it.q.L;
+      add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
+      p.descs.push_back(d);
+      ++ln.ndesc;
+      const double s = std::min(it.q.r, it.q.c), l = std::max(it.q.r, it.q.c);
+      ln.flops += 2.0 * s * s * l;
+      ln.bytes += es * (s * l + s * s);
+    }
+    sort_launch(p, ln);
+  }
+  // B' = b A + c A A (A symmetric in exact arithmetic; read as A A all the same)
+  {
+    Launch& ln = p.nsB;
+    ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
+    for (const Item& it : items) {
+      GemmDesc d{};
+      d.A = d.B = ap(bf.mA, it.aoff);
+      d.lda = d.ldb = it.q.S;
+      d.C = ap(bf.mB, it.aoff);
+      d.ldc = it.q.S;
+      d.Y = ap(bf.mA, it.aoff);
+      d.ldy = it.q.S;
+      d.M = d.N = d.Kd = it.q.S;
+      add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
+      p.descs.push_back(d);
+      ++ln.ndesc;
+      const double s = std::min(it.q.r, it.q.c);
+      ln.flops += 2.0 * s * s * s;
+      ln.bytes += es * 3.0 * s * s;
+    }
+    sort_launch(p, ln);
+  }
+  // X' = a X + B' X, reading X from buffer par and writing buffer 1 - par
+  for (int par = 0; par < 2; ++par) {
+    Launch& ln = p.nsX[par];
+    ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
+    for (const Item& it : items) {
+      GemmDesc d{};
+      d.A = ap(bf.mB, it.aoff);
+      d.lda = it.q.S;
+      d.B = xp(par, it.xoff);
+      d.ldb = it.q.L;
+      d.C = xp(par ^ 1, it.xoff);
+      d.ldc = it.q.L;
+      d.Y = xp(par, it.xoff);
+      d.ldy = it.q.L;
+      d.M = it.q.S;
+      d.N = it.q.L;
+      d.Kd = it.q.S;
+      add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
+      p.descs.push_back(d);
+      ++ln.ndesc;
+      const double s = std::min(it.q.r, it.q.c), l = std::max(it.q.r, it.q.c);
+      ln.flops += 2.0 * s * s * l;
+      ln.bytes += es * (s * s + 2.0 * s * l);
+    }
+    sort_launch(p, ln);
+  }
+  p.tile_set = saved;
+}
 
 // Launch tables over the members of `group` (the active members split into
 // streams; carve() sizes the workspace with every member in one group).
@@ -618,6 +798,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
   }
   p.headtile0[kGroups] = (int)p.headtiles.size();
   p.member0[kGroups] = (int)p.members.size();
+  if (h->muon) plan_muon(h, bf, group, p);
   return p;
 }
 
@@ -658,7 +839,22 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf) {
   bf.d_bias_off = cv.take<int64_t>((size_t)c.L * c.K);
   std::vector<int> all[kGroups];
   for (int k = 0; k < c.K; ++k) all[0].push_back(k);
+  if (h->muon) {
+    int64_t xe = 0, ae = 0;
+    muon_sizes(h, all[0].begin(), all[0].end(), xe, ae);
+    bf.mX[0] = cv.take<char>((size_t)xe * h->elt());
+    bf.mX[1] = cv.take<char>((size_t)xe * h->elt());
+    bf.mA = cv.take<char>((size_t)ae * h->elt());
+    bf.mB = cv.take<char>((size_t)ae * h->elt());
+  }
   Plan plan = build_plan(h, bf, all);
+  if (h->muon) {
+    bf.mpart = cv.take<double>(plan.mtiles.size());
+    bf.minv = cv.take<float>(plan.mmats.size());
+    bf.d_mmats = cv.take<MuonMat>(plan.mmats.size());
+    bf.d_mtiles = cv.take<MuonTile>(plan.mtiles.size());
+    bf.d_mtile0 = cv.take<int32_t>(plan.mtile0.size());
+  }
   bf.d_descs = cv.take<GemmDesc>(plan.descs.size());
   bf.d_tiles = cv.take<Tile>(plan.tiles.size());
   bf.d_coltiles = cv.take<ColTile>(plan.coltiles.size());
@@ -757,7 +953,19 @@ int upload_plan(pack_handle* h, hipStream_t stream) {
   HIP_TRY(up(h->b.d_coltiles, plan.coltiles.data(), plan.coltiles.size() * sizeof(ColTile)));
   HIP_TRY(up(h->b.d_headtiles, plan.headtiles.data(), plan.headtiles.size() * sizeof(HeadTile)));
   HIP_TRY(up(h->b.d_members, plan.members.data(), plan.members.size() * sizeof(int32_t)));
+  if (h->muon) {
+    HIP_TRY(up(h->b.d_mmats, plan.mmats.data(), plan.mmats.size() * sizeof(MuonMat)));
+    HIP_TRY(up(h->b.d_mtiles, plan.mtiles.data(), plan.mtiles.size() * sizeof(MuonTile)));
+    HIP_TRY(up(h->b.d_mtile0, plan.mtile0.data(), plan.mtile0.size() * sizeof(int32_t)));
+  }
   HIP_TRY(hipStreamSynchronize(stream));
+  h->n_mmats = (int)plan.mmats.size();
+  h->n_mtiles = (int)plan.mtiles.size();
+  for (int par = 0; par < 2; ++par) {
+    h->nsA[par] = plan.nsA[par];
+    h->nsX[par] = plan.nsX[par];
+  }
+  h->nsB = plan.nsB;
   for (int hf = 0; hf < kGroups; ++hf) {
     h->fwd[0][hf] = plan.fwd[0][hf];
     h->fwd[1][hf] = plan.fwd[1][hf];
@@ -777,9 +985,58 @@ int upload_plan(pack_handle* h, hipStream_t stream) {
   return PACK_OK;
 }
 
+const char* gemm_name(Prec p, OpKind a, OpKind b, EpiKind e);
+
+// Muon step of every active member's hidden weights (their gradients are in
+// grad): momentum and tile norms, inverse norms, X0, ns_steps Newton-Schulz
+// iterations of three grouped GEMMs, update.  On `stream`, after the members'
+// backward passes.
+hipError_t muon_step(pack_handle* h, const GemmArgs& base, hipStream_t stream) {
+  if (h->n_mmats == 0) return hipSuccess;
+  const pack_config& c = h->cfg;
+  const float mu = (float)c.muon_momentum;
+  const int nest = c.muon_nesterov ? 1 : 0;
+  const double wbytes = (double)h->n_mtiles * 64 * 64;  // upper bound of the weights' elements
+  hipError_t e = timed(h, "muon_prep", 1, 0.0, wbytes * 12.0, stream, [&] {
+    return launch_muon_prep(h->b.d_mmats, h->b.d_mtiles, h->n_mtiles, h->b.grad, h->b.m, mu, nest, h->b.mpart,
+                            stream);
+  });
+  if (e != hipSuccess) return e;
+  e = timed(h, "muon_norm", 1, 0.0, 8.0 * h->n_mtiles, stream,
+            [&] { return launch_muon_norm(h->b.d_mtile0, h->n_mmats, h->b.mpart, h->b.minv, stream); });
+  if (e != hipSuccess) return e;
+  e = timed(h, "muon_convert", 1, 0.0, wbytes * (8.0 + h->elt()), stream, [&] {
+    return launch_muon_convert(h->prec, h->b.d_mmats, h->b.d_mtiles, h->n_mtiles, h->b.grad, h->b.m, mu, nest,
+                               h->b.minv, h->b.mX[0], stream);
+  });
+  if (e != hipSuccess) return e;
+  static const float kA = 3.4445f, kB = -4.7750f, kC = 2.0315f;
+  auto ns = [&](const Launch& ln, OpKind bk, float alpha, float beta) {
+    GemmArgs g = base;
+    g.tiles += ln.tile0;
+    g.ntiles = ln.ntiles;
+    g.tile_set = TILES_SMALL;
+    g.ns_alpha = alpha;
+    g.ns_beta = beta;
+    return timed(h, gemm_name(h->prec, OP_KMAJ, bk, EPI_NS), 0, ln.flops, ln.bytes, stream,
+                 [&] { return launch_gemm(h->prec, OP_KMAJ, bk, EPI_NS, g, stream); });
+  };
+  for (int it = 0; it < h->ns_steps; ++it) {
+    const int par = it & 1;
+    if ((e = ns(h->nsA[par], OP_KMAJ, 0.0f, 1.0f)) != hipSuccess) return e;
+    if ((e = ns(h->nsB, OP_RMAJ, kB, kC)) != hipSuccess) return e;
+    if ((e = ns(h->nsX[par], OP_RMAJ, kA, 1.0f)) != hipSuccess) return e;
+  }
+  return timed(h, "muon_update", 1, 0.0, wbytes * (8.0 + h->elt() + (h->prec == Prec::BF16 ? 2.0 : 0.0)), stream,
+               [&] {
+                 return launch_muon_update(h->prec, h->b.d_mmats, h->b.d_mtiles, h->n_mtiles, h->b.theta,
+                                           h->b.shadow, h->b.mX[h->ns_steps & 1], stream);
+               });
+}
+
 const char* gemm_name(Prec p, OpKind a, OpKind b, EpiKind e) {
   static const char* ops[] = {"kmaj", "rmaj", "xgk", "xgr"};
-  static const char* epis[] = {"fwd", "fwd_eval", "dx", "dw"};
+  static const char* epis[] = {"fwd", "fwd_eval", "dx", "dw", "ns"};
   static thread_local char buf[64];
   snprintf(buf, sizeof buf, "gemm_%s_%s_%s_%s", p == Prec::BF16 ? "bf16" : "f32", ops[a], ops[b], epis[e]);
   return buf;
@@ -811,6 +1068,8 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
     h->tiles = v == "big" ? TILES_BIG : (v == "tall" ? TILES_TALL : TILES_SMALL);
   }
   if (h->prec == Prec::FP32) h->tiles = TILES_SMALL;
+  h->muon = cfg->optimizer == PACK_OPT_MUON;
+  h->ns_steps = cfg->ns_steps ? cfg->ns_steps : 5;
   h->Bp = (int)round_up(cfg->B, kRowAlign);
   h->Pin = (int)round_up(cfg->d_in, 8);
   h->mem.resize(cfg->K);
@@ -818,7 +1077,8 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
     for (int k = 0; k < cfg->K; ++k) {
       const pack_member_hp& e = cfg->members[k];
       if (e.width < 1 || e.width > 16384 || !(e.dropout >= 0 && e.dropout < 1) || !(e.lr > 0) ||
-          !(e.wd >= 0) || e.depth < 0 || e.depth > cfg->L) {
+          !(e.wd >= 0) || e.depth < 0 || e.depth > cfg->L ||
+          (cfg->optimizer == PACK_OPT_MUON && !(e.muon_lr > 0))) {
         delete h;
         return fail(PACK_EINVAL, "explicit hyperparameters of member %d out of range", k);
       }
@@ -827,6 +1087,7 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
       h->mem[k].lr = e.lr;
       h->mem[k].wd = e.wd;
       h->mem[k].depth = e.depth ? e.depth : cfg->L;
+      h->mem[k].muon_lr = cfg->optimizer == PACK_OPT_MUON ? e.muon_lr : 0.0;
     }
   } else {
     sample_members(h);
@@ -867,7 +1128,7 @@ int pack_get_hparams(const pack_handle* h, pack_member_hp* out) {
   if (!h || !out) return fail(PACK_EINVAL, "NULL argument");
   for (int k = 0; k < h->cfg.K; ++k) {
     const Member& m = h->mem[k];
-    out[k] = pack_member_hp{m.width, m.dp, m.t, m.depth, m.dropout, m.lr, m.wd, m.scale};
+    out[k] = pack_member_hp{m.width, m.dp, m.t, m.depth, m.dropout, m.lr, m.wd, m.scale, m.muon_lr};
   }
   return PACK_OK;
 }
@@ -1062,6 +1323,10 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       }
       GemmArgs al = for_launch(a, h->dw[hf][l - 1]);
       al.layer = l;
+      if (h->muon) {  // the gradient is stored; the Muon step below updates W_l
+        HIP_TRY(gemm(OP_RMAJ, OP_RMAJ, EPI_DW, h->dw[hf][l - 1], l, s));
+        continue;
+      }
       al.theta = h->b.theta;
       al.am = h->b.m;
       al.av = h->b.v;
@@ -1077,6 +1342,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                     h->dw[hf][l - 1].bytes, s, [&] { return launch_gemm(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW, al, s); }));
     }
   HIP_TRY(merge());
+  if (h->muon) HIP_TRY(muon_step(h, a, stream));
   double naux = 0;
   for (int k : h->active_ids) {
     const Member& m = h->mem[k];

@@ -54,6 +54,8 @@
 //   EPI_DW        fp32 store of the weight-gradient tile, or AdamW applied to
 //                 the weights it covers (small tiles: the whole tile staged in
 //                 LDS and streamed by the workgroup)
+//   EPI_NS        alpha * Y + beta * acc -> C in the GEMM precision (the
+//                 products of the Newton-Schulz iteration of the Muon optimizer)
 // Every output element is owned by exactly one workgroup and reduced over the
 // full depth in a fixed order: no atomics, bit-reproducible.
 #include <algorithm>
@@ -666,6 +668,41 @@ __device__ __forceinline__ void stage_flush(const char* stage, OT* C, int64_t ld
   }
 }
 
+// Rows of alpha * Y + beta * acc from the staged fp32 accumulators: each lane
+// takes 4 consecutive columns of a row (Y read as 4 elements), rounds once to
+// OT and stores them; rows >= M and columns >= N are skipped (N is a multiple
+// of 4).
+template <typename OT, int NB>
+__device__ __forceinline__ void stage_flush_ns(const char* stage, OT* C, int64_t ldc, const OT* Y, int64_t ldy,
+                                               float alpha, float beta, int row0, int col0, int M, int N,
+                                               int lane) {
+  using S = Stage<float, NB>;
+#pragma unroll
+  for (int it = 0; it < S::PER_LANE; ++it) {
+    const int v = it * 64 + lane;
+    const int r = v / S::VPR, c = v % S::VPR;
+    const f32x4 x = *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16);
+    const int row = row0 + r, col = col0 + c * 4;
+    if (row >= M || col >= N) continue;
+    float o[4] = {beta * x[0], beta * x[1], beta * x[2], beta * x[3]};
+    if (Y) {
+      const OT* yp = Y + (int64_t)row * ldy + col;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = alpha * to_float(yp[q]) + o[q];
+    }
+    OT* cp = C + (int64_t)row * ldc + col;
+    if constexpr (sizeof(OT) == 2) {
+      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)o[0]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)o[1]) << 16);
+      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)o[2]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)o[3]) << 16);
+      *glob(reinterpret_cast<u32x2*>(cp)) = u32x2{lo, hi};
+    } else {
+      *glob(reinterpret_cast<f32x4*>(cp)) = f32x4{o[0], o[1], o[2], o[3]};
+    }
+  }
+}
+
 // Weight-gradient rows with the optimizer fused: each staged vector holds the
 // gradients of 4 consecutive weights, which are updated in place (theta, both
 // moments, the bf16 shadow); the gradient itself is stored only on request.
@@ -886,6 +923,26 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
           stage_flush_adamw<NB, MB>(a, d, stage, row0 + 32 * i + S::ROWS * p, col0, lane);
         else
           stage_flush<float, NB>(stage, C, d.ldc, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
+        wave_sync_lds();
+      }
+    }
+  } else if constexpr (EPI == EPI_NS) {
+    using S = Stage<float, NB>;
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      if (i >= mv) continue;
+#pragma unroll
+      for (int p = 0; p < S::NPASS; ++p) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int g = 0; g < S::GP; ++g)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              stage_put<float, NB>(stage, j, g, q, lane, acc[i][j][4 * (p * S::GP + g) + q]);
+        wave_sync_lds();
+        stage_flush_ns<T, NB>(stage, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.Y), d.ldy, a.ns_alpha,
+                              a.ns_beta, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
         wave_sync_lds();
       }
     }
@@ -1184,6 +1241,13 @@ hipError_t launch_t(const GemmArgs& args, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <typename T, int AK, int BK_, int EPI>
+hipError_t launch_small(const GemmArgs& args, hipStream_t s) {
+  if (args.ntiles <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_kernel_small<T, AK, BK_, EPI>), dim3(args.ntiles), dim3(NT), 0, s, args);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_prec(OpKind ak, OpKind bk, EpiKind e, const GemmArgs& args, hipStream_t s) {
   if (ak == OP_KMAJ && bk == OP_KMAJ && e == EPI_FWD) return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_FWD>(args, s);
@@ -1191,6 +1255,11 @@ hipError_t launch_prec(OpKind ak, OpKind bk, EpiKind e, const GemmArgs& args, hi
     return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL>(args, s);
   if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DX) return launch_t<T, OP_KMAJ, OP_RMAJ, EPI_DX>(args, s);
   if (ak == OP_RMAJ && bk == OP_RMAJ && e == EPI_DW) return launch_t<T, OP_RMAJ, OP_RMAJ, EPI_DW>(args, s);
+  if (e == EPI_NS) {  // Newton-Schulz products: small tiles only
+    if (args.tile_set != TILES_SMALL) return hipErrorInvalidValue;
+    if (ak == OP_KMAJ && bk == OP_KMAJ) return launch_small<T, OP_KMAJ, OP_KMAJ, EPI_NS>(args, s);
+    if (ak == OP_KMAJ && bk == OP_RMAJ) return launch_small<T, OP_KMAJ, OP_RMAJ, EPI_NS>(args, s);
+  }
   return hipErrorInvalidValue;
 }
 

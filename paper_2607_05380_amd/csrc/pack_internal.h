@@ -33,7 +33,7 @@ enum class Task : int { REG = 0, BIN = 1, MULTI = 2 };
 //   KMAJ    element (r, k) at P[r * ld + k]         -- depth contiguous
 //   RMAJ    element (r, k) at P[k * ld + r]         -- rows contiguous (transposed on load)
 enum OpKind : int { OP_KMAJ = 0, OP_RMAJ = 1 };
-enum EpiKind : int { EPI_FWD = 0, EPI_FWD_EVAL = 1, EPI_DX = 2, EPI_DW = 3 };
+enum EpiKind : int { EPI_FWD = 0, EPI_FWD_EVAL = 1, EPI_DX = 2, EPI_DW = 3, EPI_NS = 4 };
 
 // One member's GEMM problem C[m, n] = sum_k A(m, k) B(n, k) in one grouped launch.
 struct GemmDesc {
@@ -54,6 +54,8 @@ struct GemmDesc {
   float lr, wd;        // EPI_DW with fused AdamW: the member's learning rate and weight decay
   int32_t pad_;
   int64_t poff;        // EPI_DW with fused AdamW: element offset of the weight tensor
+  const void* Y;       // EPI_NS: the matrix added to the product (GEMM precision), or nullptr
+  int64_t ldy;
 };
 
 struct Tile {
@@ -82,6 +84,8 @@ struct GemmArgs {
   uint16_t* shadow;
   float beta1, beta2, eps, bc1, bc2_sqrt;
   int32_t keep_grad;
+  // EPI_NS only: C = ns_alpha * Y + ns_beta * (A B^T), stored in the GEMM precision
+  float ns_alpha, ns_beta;
 };
 
 // AdamW constants of one step.
@@ -103,6 +107,25 @@ struct MemberDev {
   int64_t dz_last;          // its gradient dZ_depth: offset from the start of the dZ ping-pong pair (elements)
   int32_t depth;            // hidden blocks of the member
   int32_t pad_;
+};
+
+// One hidden weight W [R x Cp] (padded storage, row stride Cp) updated by Muon.
+// Its Newton-Schulz iterate X is [S x L] row-major in the GEMM precision:
+// X = U (S = R, L = Cp), or X = U^T (S = Cp, L = R) when the weight's true
+// rows exceed its true columns (tall).  A and B' are [S x S].
+struct MuonMat {
+  int64_t woff;    // element offset of W in theta, grad and the momentum buffer
+  int64_t xoff;    // element offset of X in each of the two X buffers
+  int64_t aoff;    // element offset of A in the A buffer and of B' in the B buffer
+  int32_t R, Cp;
+  int32_t tall;
+  int32_t member;
+  float decay;     // 1 - lr wd
+  float step;      // lr max(1, rows / cols)^(1/2), true rows and columns
+};
+
+struct MuonTile {  // 64 x 64 block (rows r0.., columns c0..) of a MuonMat's W
+  int32_t mat, r0, c0, pad_;
 };
 
 struct HeadTile {            // (member, first column, first row) block of the head backward
@@ -156,6 +179,15 @@ hipError_t launch_dropout_mask(uint32_t key0, uint32_t key1, uint32_t step, int 
 hipError_t launch_dropout_words(uint32_t key0, uint32_t key1, uint32_t step, const MemberDev* mem, int K, int L,
                                 int max_dp, int Bp, int rows_valid, int64_t A32, uint32_t* out,
                                 const int32_t* members, hipStream_t s);
+// Muon (kernels_muon.hip): momentum and tile norms, per-matrix inverse norms,
+// the normalised (and for tall weights transposed) iterate X0, the update.
+hipError_t launch_muon_prep(const MuonMat* mats, const MuonTile* tiles, int ntiles, const float* grad, float* buf,
+                            float mu, int nesterov, double* part, hipStream_t s);
+hipError_t launch_muon_norm(const int32_t* tile0, int nmats, const double* part, float* inv, hipStream_t s);
+hipError_t launch_muon_convert(Prec prec, const MuonMat* mats, const MuonTile* tiles, int ntiles, const float* grad,
+                               const float* buf, float mu, int nesterov, const float* inv, void* X, hipStream_t s);
+hipError_t launch_muon_update(Prec prec, const MuonMat* mats, const MuonTile* tiles, int ntiles, float* theta,
+                              uint16_t* shadow, const void* X, hipStream_t s);
 hipError_t launch_select_iter(Task task, const float* cand, const void* yv, int C, int64_t Nv,
                               int m_ens, double* sum, double* partial, int nblk, int32_t* state,
                               double* best, int32_t* sel_out, hipStream_t s);

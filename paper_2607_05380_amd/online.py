@@ -130,7 +130,7 @@ class OnlineTrainer:
         if self._infer is None:
             cfg = dict(self.cfg, K=len(self.ensemble), keep_grads=0)
             hps = [dict(width=s.hp["width"], dropout=s.hp["dropout"], lr=s.hp["lr"], wd=s.hp["wd"],
-                        depth=s.hp["depth"]) for s in self.ensemble]
+                        depth=s.hp["depth"], muon_lr=s.hp.get("muon_lr", 0.0)) for s in self.ensemble]
             pk = tabpack.Pack(cfg, members=hps).bind(self.device)
             for i, snap in enumerate(self.ensemble):
                 pk.set_params(i, snap.params)

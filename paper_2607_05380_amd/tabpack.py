@@ -18,6 +18,7 @@ PACK_OK = 0
 TASKS = {"reg": 0, "bin": 1, "multi": 2}
 PRECISIONS = {"bf16": 0, "fp32": 1}
 PREDICT_MEMBERS, PREDICT_ENSEMBLE = 0, 1
+OPTIMIZERS = {"adamw": 0, "muon": 1}
 
 SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "pack_workspace_size",
            "pack_bind", "pack_train_step", "pack_eval_members", "pack_select_workspace_size",
@@ -30,7 +31,7 @@ class MemberHP(ctypes.Structure):
     _fields_ = [("width", ctypes.c_int32), ("padded_width", ctypes.c_int32),
                 ("drop_threshold", ctypes.c_uint32), ("depth", ctypes.c_int32),
                 ("dropout", ctypes.c_double), ("lr", ctypes.c_double), ("wd", ctypes.c_double),
-                ("scale", ctypes.c_double)]
+                ("scale", ctypes.c_double), ("muon_lr", ctypes.c_double)]
 
 
 class PackConfig(ctypes.Structure):
@@ -44,7 +45,11 @@ class PackConfig(ctypes.Structure):
                 ("wd_lo", ctypes.c_double), ("wd_hi", ctypes.c_double),
                 ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
                 ("seed", ctypes.c_uint64), ("members", ctypes.POINTER(MemberHP)),
-                ("depth_lo", ctypes.c_int32), ("depth_hi", ctypes.c_int32)]
+                ("depth_lo", ctypes.c_int32), ("depth_hi", ctypes.c_int32),
+                ("optimizer", ctypes.c_int32), ("ns_steps", ctypes.c_int32),
+                ("muon_lr_lo", ctypes.c_double), ("muon_lr_hi", ctypes.c_double),
+                ("muon_momentum", ctypes.c_double), ("muon_nesterov", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class KernelStat(ctypes.Structure):
@@ -126,6 +131,12 @@ def make_config(cfg, members=None):
     c.seed = int(cfg["seed"])
     c.depth_lo = int(cfg.get("depth_lo", 0) or 0)
     c.depth_hi = int(cfg.get("depth_hi", 0) or 0)
+    c.optimizer = OPTIMIZERS[cfg.get("optimizer", "adamw")]
+    c.ns_steps = int(cfg.get("ns_steps", 5))
+    c.muon_lr_lo = float(cfg.get("muon_lr_lo", 1e-3))
+    c.muon_lr_hi = float(cfg.get("muon_lr_hi", 1e-1))
+    c.muon_momentum = float(cfg.get("muon_momentum", 0.95))
+    c.muon_nesterov = int(cfg.get("muon_nesterov", 1))
     keep = None
     if members is not None:
         keep = (MemberHP * len(members))()
@@ -135,6 +146,7 @@ def make_config(cfg, members=None):
             keep[i].lr = float(m["lr"])
             keep[i].wd = float(m["wd"])
             keep[i].depth = int(m.get("depth") or 0)
+            keep[i].muon_lr = float(m.get("muon_lr", 0.0) or 0.0)
         c.members = ctypes.cast(keep, ctypes.POINTER(MemberHP))
     return c, keep
 
@@ -173,7 +185,7 @@ class Pack:
         arr = (MemberHP * self.K)()
         _check(self.lib.pack_get_hparams(self.h, arr))
         return [dict(width=a.width, padded_width=a.padded_width, t=a.drop_threshold, depth=a.depth,
-                     dropout=a.dropout, lr=a.lr, wd=a.wd, s=a.scale) for a in arr]
+                     dropout=a.dropout, lr=a.lr, wd=a.wd, s=a.scale, muon_lr=a.muon_lr) for a in arr]
 
     def workspace_bytes(self):
         n = ctypes.c_size_t()

@@ -53,13 +53,17 @@ ORACLE_KEYS = ("seed", "K", "d_in", "d_out", "L", "B", "task", "beta1", "beta2",
 def oracle_cfg(cfg):
     out = {k: cfg[k] for k in ORACLE_KEYS}
     out["depth_lo"], out["depth_hi"] = cfg.get("depth_lo", 0), cfg.get("depth_hi", 0)
+    for k, v in (("optimizer", "adamw"), ("muon_lr_lo", 1e-3), ("muon_lr_hi", 1e-1), ("muon_momentum", 0.95),
+                 ("muon_nesterov", 1), ("ns_steps", 5)):
+        out[k] = cfg.get(k, v)
     return out
 
 
 def oracle_hparams(cfg, members=None):
     if members is None:
         return sample_hparams(oracle_cfg(cfg))
-    return [member_hparams(m["width"], m["dropout"], m["lr"], m["wd"], m.get("depth")) for m in members]
+    return [member_hparams(m["width"], m["dropout"], m["lr"], m["wd"], m.get("depth"), m.get("muon_lr"))
+            for m in members]
 
 
 def close_mask(gpu, ref, rtol, atol):

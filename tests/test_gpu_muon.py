@@ -1,0 +1,151 @@
+"""GPU parity of the Muon optimizer pack: the hidden weights W_1..W_Lk of every
+member take Muon steps (momentum, Newton-Schulz on the grouped MFMA GEMMs,
+true-shape scaling), biases and heads AdamW steps.  Compared with the oracle's
+Muon (fp64, or its bf16 policy for bf16 packs) on the same seeded inputs."""
+import numpy as np
+import pytest
+
+from oracle import mlp, muon
+from oracle.pack import OraclePack
+from paper_2607_05380_amd import configs, synth, tabpack
+from parity import TOL, check_tensor, check_update, make_inputs, oracle_cfg, oracle_hparams, to_dev
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+MUON = dict(optimizer="muon", muon_lr_lo=1e-3, muon_lr_hi=1e-1)
+
+
+def _run(cfg, steps, members=None, n_train=3000, prec=None):
+    Xtr, ytr, _, _, orders, _ = make_inputs(cfg, n_train, 10)
+    X, y = to_dev(Xtr, ytr)
+    pk = tabpack.Pack(cfg, members=members).bind()
+    op = OraclePack(oracle_cfg(cfg), hparams=oracle_hparams(cfg, members),
+                    precision=prec or ("bf16" if cfg["precision"] == "bf16" else "fp64"))
+    p0 = [[(W.copy(), b.copy()) for W, b in p] for p in op.params]
+    for s in range(steps):
+        idx = synth.batch_indices(orders, s, cfg["B"])
+        (idx_d,) = to_dev(idx)
+        lg = pk.train_step(X, y, idx_d, s + 1).cpu().numpy()
+        lo = op.train_step(Xtr, ytr, idx, s + 1)
+        check_tensor(f"loss step {s + 1}", lg, lo, TOL[cfg["precision"]])
+    return pk, op, p0
+
+
+def _compare(pk, op, p0, tol, steps, upd_frob, report):
+    for k in range(len(op.params)):
+        g_gpu = pk.get_grads(k)
+        p_gpu = pk.get_params(k)
+        m_gpu, v_gpu = pk.get_moments(k)
+        depth = len(op.params[k]) - 1
+        h = op.hp[k]
+        for l in range(depth + 1):
+            gW, gb = op.last_grads[k][l]
+            tag = f"m{k}.l{l}"
+            check_tensor(tag + ".grad", g_gpu[l][0], gW, tol, grad=True)
+            check_tensor(tag + ".bgrad", g_gpu[l][1], gb, tol, grad=True)
+            check_update(tag + ".b", p_gpu[l][1], op.params[k][l][1], p0[k][l][1], g_gpu[l][1], gb, h["lr"], tol,
+                         steps)
+            if l == depth:  # the head: AdamW
+                check_update(tag + ".W", p_gpu[l][0], op.params[k][l][0], p0[k][l][0], g_gpu[l][0], gW, h["lr"],
+                             tol, steps)
+                continue
+            # hidden weight: Muon; the momentum buffer is a sum of gradients
+            check_tensor(tag + ".momentum", m_gpu[l][0], op.m[k][l][0], tol, grad=True)
+            assert (v_gpu[l][0] == 0).all()
+            d_gpu = np.asarray(p_gpu[l][0], np.float64) - p0[k][l][0]
+            d_ref = op.params[k][l][0] - p0[k][l][0]
+            r, c = op.params[k][l][0].shape
+            step = h["muon_lr"] * max(1.0, r / c) ** 0.5
+            o_max = np.abs(d_ref + p0[k][l][0] * h["muon_lr"] * h["wd"]).max() / step
+            if steps == 1:
+                # The optimizer alone: the oracle's Muon step fed with the GPU's own
+                # gradient (first step: empty momentum buffer) leaves only the
+                # rounding of the Newton-Schulz products.  In bf16 the iteration
+                # amplifies rounding (slope a = 3.4 at small singular values): two
+                # bf16 runs whose only difference is rounding differ by up to 2% of
+                # max|O| element-wise and 0.4-0.6% in Frobenius norm on these shapes,
+                # so the bounds are 5% of max|O| and 2% Frobenius.
+                G = np.asarray(g_gpu[l][0], np.float64)
+                W_exp, _ = muon.muon_step(p0[k][l][0], G, np.zeros_like(G), h["muon_lr"], h["wd"],
+                                          rnd=mlp.to_bf16 if tol is TOL["bf16"] else None)
+                bf16 = tol is TOL["bf16"]
+                err = np.abs(np.asarray(p_gpu[l][0], np.float64) - W_exp)
+                d_exp = W_exp - p0[k][l][0]
+                frob_g = np.linalg.norm(d_gpu - d_exp) / max(np.linalg.norm(d_exp), 1e-30)
+                report.append((tag + ".given_grad", float(err.max() / (step * o_max))))
+                assert err.max() <= step * o_max * (0.05 if bf16 else 1e-4) + 1e-7, \
+                    f"{tag}: Muon step from the same gradient differs by {err.max():.3e}"
+                assert frob_g <= (2e-2 if bf16 else 1e-5), f"{tag}: same-gradient update frob {frob_g:.3e}"
+            # End to end against the oracle (its own gradients): the whole update
+            # within upd_frob in Frobenius norm -- in bf16 the gradients may differ
+            # by 2% (ReLU decisions flipping on bf16 noise), and the orthogonal
+            # factor of a near-square matrix moves more than its input -- and theta
+            # within the literal tolerance, except for at most 0.1% of the elements
+            # (bf16 only), which stay within 2 lr scale max|O|, the sign-flip bound
+            # of the AdamW checks
+            frob = np.linalg.norm(d_gpu - d_ref) / max(np.linalg.norm(d_ref), 1e-30)
+            report.append((tag + ".frob", frob))
+            assert frob <= upd_frob, f"{tag}: Muon update relative Frobenius error {frob:.3e}"
+            W_ref = op.params[k][l][0]
+            err = np.abs(np.asarray(p_gpu[l][0], np.float64) - W_ref)
+            lit = err <= tol["lit_atol"] + tol["lit_rtol"] * np.abs(W_ref)
+            if not lit.all():
+                assert tol is TOL["bf16"], f"{tag}: {(~lit).sum()} elements outside the literal tolerance"
+                assert (~lit).mean() <= 1e-3, f"{tag}: {(~lit).sum()} elements outside the literal tolerance"
+                assert err[~lit].max() <= 2 * step * o_max, f"{tag}: update error above 2 lr scale max|O|"
+                report.append((tag + ".literal_misses", float((~lit).sum())))
+
+
+def test_muon_fp32_three_steps():
+    # fp32 GEMMs: Newton-Schulz in fp32 against the fp64 oracle.  binary_small's
+    # first layers are tall (width > 8 inputs): the transposed iterate is used
+    cfg = configs.workload("binary_small", **MUON)
+    pk, op, p0 = _run(cfg, 3)
+    report = []
+    _compare(pk, op, p0, TOL["fp32"], 3, 2e-4, report)
+    print(f"[muon] fp32 worst update frob {max(r[1] for r in report if r[0].endswith('.frob')):.3e}", flush=True)
+    assert not any(r[0].endswith("literal_misses") for r in report)
+
+
+@pytest.mark.parametrize("name,over", [("regression_large", dict(K=5, B=300)),
+                                       ("multiclass_lognormal", dict(K=4, B=260, depth_lo=1, depth_hi=3))])
+def test_muon_bf16_step(name, over):
+    # bf16 Newton-Schulz against the oracle's bf16 policy (every stored iterate
+    # rounded to bf16); regression_large mixes wide (width < 900) and tall
+    # first layers
+    cfg = configs.workload(name, **over, **MUON)
+    widths = [h["width"] for h in tabpack.Pack(cfg).hparams()]
+    print(f"[muon] {name} widths {widths}", flush=True)
+    pk, op, p0 = _run(cfg, 1)
+    report = []
+    _compare(pk, op, p0, TOL["bf16"], 1, 0.10, report)
+    frobs = [r[1] for r in report if r[0].endswith(".frob")]
+    misses = sum(r[1] for r in report if r[0].endswith("literal_misses"))
+    given = max(r[1] for r in report if r[0].endswith("given_grad"))
+    print(f"[muon] {name} worst update frob {max(frobs):.3e}; elements outside the literal tolerance {misses:.0f}; "
+          f"same-gradient step error / (lr scale max|O|) {given:.3e}", flush=True)
+
+
+def test_muon_members_independent_of_streams_and_active_set(monkeypatch):
+    cfg = configs.workload("regression_onehot", K=5, B=300, depth_lo=1, depth_hi=3, **MUON)
+    Xtr, ytr, _, _, orders, _ = make_inputs(cfg, 3000, 10)
+    X, y = to_dev(Xtr, ytr)
+    runs = []
+    for streams, active in (("3", [1] * 5), ("1", [1] * 5), ("2", [1, 0, 1, 1, 0])):
+        monkeypatch.setenv("TABPACK_STREAMS", streams)
+        pk = tabpack.Pack(cfg)
+        init = [pk.get_params(k) for k in range(5)]
+        pk.set_active(active)
+        pk.bind()
+        for s in range(2):
+            (idx,) = to_dev(synth.batch_indices(orders, s, cfg["B"]))
+            pk.train_step(X, y, idx, s + 1)
+        runs.append((active, init, [pk.get_params(k) for k in range(5)]))
+    ref = runs[0][2]
+    for active, init, got in runs[1:]:
+        for k in range(5):
+            want = ref[k] if active[k] else init[k]
+            for (W1, b1), (W2, b2) in zip(got[k], want):
+                np.testing.assert_array_equal(W1, W2)
+                np.testing.assert_array_equal(b1, b2)

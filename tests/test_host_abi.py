@@ -32,6 +32,8 @@ def oracle_cfg(cfg):
     out = {k: cfg[k] for k in ("seed", "K", "d_in", "d_out", "L", "width_lo", "width_hi", "dropout_lo",
                                "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi")}
     out["depth_lo"], out["depth_hi"] = cfg.get("depth_lo", 0), cfg.get("depth_hi", 0)
+    for k, v in (("optimizer", "adamw"), ("muon_lr_lo", 1e-3), ("muon_lr_hi", 1e-1)):
+        out[k] = cfg.get(k, v)
     return out
 
 
@@ -135,3 +137,18 @@ def test_invalid_depth_ranges_rejected(lo, hi):
     cfg = configs.workload("regression_onehot", K=2, L=4, depth_lo=lo, depth_hi=hi)
     with pytest.raises(tabpack.PackError, match="depth"):
         tabpack.Pack(cfg)
+
+
+def test_sampled_muon_lrs_match_oracle():
+    cfg = configs.workload("regression_large", K=50, optimizer="muon", muon_lr_lo=1e-3, muon_lr_hi=1e-1)
+    got = tabpack.Pack(cfg).hparams()
+    ref = sample_hparams(oracle_cfg(cfg))
+    for g, r in zip(got, ref):
+        assert g["muon_lr"] == pytest.approx(r["muon_lr"], rel=4e-16, abs=0)
+        assert g["lr"] == pytest.approx(r["lr"], rel=4e-16, abs=0)
+    # the AdamW-only pack draws the same widths, rates and decays
+    base = tabpack.Pack(dict(cfg, optimizer="adamw")).hparams()
+    assert [(b["width"], b["lr"], b["wd"]) for b in base] == [(g["width"], g["lr"], g["wd"]) for g in got]
+    assert all(b["muon_lr"] == 0.0 for b in base)
+    with pytest.raises(tabpack.PackError, match="Muon"):
+        tabpack.Pack(dict(cfg, muon_lr_lo=0.0))
