@@ -150,6 +150,42 @@ def variable_depth(cfg, Xtr, ytr, steps=20):
             "step_ms": round(e0.elapsed_time(e1) / steps, 4), "gemm_work_vs_full_depth": round(work / full, 4)}
 
 
+def muon_optimizer(cfg, Xtr, ytr, steps=20):
+    """Step time of the same workload with the paper's default optimizer split:
+    Muon for the hidden weights (Newton-Schulz on the grouped GEMMs), AdamW for
+    biases and heads; and the Newton-Schulz GEMMs' rate (library events)."""
+    import torch
+    from paper_2607_05380_amd import tabpack
+    pk = tabpack.Pack(dict(cfg, keep_grads=0, optimizer="muon", muon_lr_lo=1e-3, muon_lr_hi=1e-1)).bind(Xtr.device)
+    idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
+    loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
+    pk.train_step(Xtr, ytr, idx, 1, loss)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for s in range(steps):
+        pk.train_step(Xtr, ytr, idx, s + 2, loss)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    pk.profile(True)
+    for s in range(3):
+        pk.train_step(Xtr, ytr, idx, steps + 2 + s, loss)
+    stats = pk.profile_read()
+    pk.profile(False)
+    ns = [x for x in stats if x["name"].endswith("_ns")]
+    ns_flops = sum(x["flops"] * x["launches"] for x in ns) / 3
+    ns_ms = sum(x["busy_ms"] for x in ns) / 3
+    other = sum(x["busy_ms"] for x in stats if x["name"].startswith("muon_")) / 3
+    peak = PEAK["mfma_bf16"] if cfg["precision"] == "bf16" else PEAK["mfma_fp32"]
+    return {"step_ms": round(ms, 4), "ns_gemm_ms_per_step": round(ns_ms, 4),
+            "ns_gemm_gflop_per_step": round(ns_flops / 1e9, 1),
+            "ns_gemm_tflop_per_s": round(ns_flops / ns_ms / 1e9, 1) if ns_ms > 0 else None,
+            "ns_gemm_frac_mfma_peak": round(ns_flops / ns_ms / 1e9 / peak, 4) if ns_ms > 0 else None,
+            "muon_elementwise_ms_per_step": round(other, 4),
+            "kernels_ms_per_step": {x["name"]: round(x["busy_ms"] / 3, 4) for x in stats}}
+
+
 def synth_idx(cfg, n, device):
     from paper_2607_05380_amd import synth
     return synth.epoch_orders_device(cfg, 1, n, device)[:, :cfg["B"]].contiguous()
@@ -297,6 +333,8 @@ def main():
         log(f"  {json.dumps(out['per_epoch'])}")
         out["variable_depth"] = variable_depth(cfg, Xtr, ytr)
         log(f"  variable depth: {json.dumps(out['variable_depth'])}")
+        out["muon"] = muon_optimizer(cfg, Xtr, ytr)
+        log(f"  Muon optimizer: {json.dumps(out['muon'])}")
     if not a.no_cpu_baseline:
         log("timing the fp64 oracle on the host (bounded sample)")
         out["cpu_baseline"] = cpu_baseline(cfg, Xtr, ytr, idx_all[0])
