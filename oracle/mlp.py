@@ -97,8 +97,9 @@ def loss_and_dy(Y, y, task):
     raise ValueError(task)
 
 
-def backward(params, cache, dY, masks=None, scale=1.0):
-    """Gradients [(dW, db), ...] in the layout of ``params``."""
+def backward(params, cache, dY, masks=None, scale=1.0, input_grad=False):
+    """Gradients [(dW, db), ...] in the layout of ``params``; with input_grad
+    also dLoss/dH_0 (the gradient of the network's input), as a second value."""
     L = len(params) - 1
     rnd = cache.get("rnd", _same)
     grads = [None] * (L + 1)
@@ -114,9 +115,9 @@ def backward(params, cache, dY, masks=None, scale=1.0):
         dZ = rnd(dZ)
         W, _ = params[l]
         grads[l] = (dZ.T @ H[l], db)
-        if l > 0:
+        if l > 0 or input_grad:
             dH = dZ @ rnd(W)
-    return grads
+    return (grads, dH) if input_grad else grads
 
 
 def adamw_step(theta, g, m, v, t, lr, wd, beta1, beta2, eps, decay=True):

@@ -9,7 +9,7 @@ predictions not), which gives every member exactly its standalone gradient.
 """
 import numpy as np
 
-from . import mlp, muon
+from . import embed, mlp, muon
 from .sampling import init_member, member_depth, sample_hparams
 
 
@@ -28,14 +28,22 @@ class OraclePack:
         self.rnd = mlp.to_bf16 if precision == "bf16" else None
         self.hp = hparams if hparams is not None else sample_hparams(cfg)
         keep = set(range(len(self.hp)) if members is None else members)
+        # periodic feature embeddings (App. F) when the members have d_emb
+        self.use_emb = bool(self.hp) and "d_emb" in self.hp[0]
+        self.emb = [embed.init_embedding(cfg, k, h["d_emb"], h["sigma"]) if self.use_emb and k in keep else None
+                    for k, h in enumerate(self.hp)]
         if params is None:
-            params = [init_member(cfg, k, h["width"], member_depth(cfg, h)) if k in keep else None
+            params = [init_member(cfg, k, h["width"], member_depth(cfg, h),
+                                  cfg["d_in"] * h["d_emb"] if self.use_emb else None) if k in keep else None
                       for k, h in enumerate(self.hp)]
         self.params = [None if p is None else [(W.copy(), b.copy()) for W, b in p] for p in params]
         self.m = [None if p is None else [(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
         self.v = [None if p is None else [(np.zeros_like(W), np.zeros_like(b)) for W, b in p] for p in self.params]
+        self.emb_m = [None if e is None else {n: np.zeros_like(a) for n, a in e.items()} for e in self.emb]
+        self.emb_v = [None if e is None else {n: np.zeros_like(a) for n, a in e.items()} for e in self.emb]
         self.t = 0
         self.last_grads = None
+        self.last_emb_grads = None
 
     def masks(self, k, step):
         c, h = self.cfg, self.hp[k]
@@ -52,9 +60,21 @@ class OraclePack:
         depth = len(self.params[k]) - 1
         rows = np.asarray(idx_k, dtype=np.int64)
         masks = self.masks(k, step)
-        Y, cache = mlp.forward(self.params[k], X[rows], masks, h["s"], rnd=self.rnd)
+        H0 = X[rows]
+        if self.use_emb:
+            H0, ecache = embed.embed(H0, self.emb[k])
+        Y, cache = mlp.forward(self.params[k], H0, masks, h["s"], rnd=self.rnd)
         loss, dY = mlp.loss_and_dy(Y, y[rows], c["task"])
-        grads = mlp.backward(self.params[k], cache, dY, masks, h["s"])
+        if self.use_emb:
+            grads, dE = mlp.backward(self.params[k], cache, dY, masks, h["s"], input_grad=True)
+            eg = embed.embed_backward(dE, ecache, self.emb[k])
+            self.last_emb_grads[k] = eg
+            args = (step, h["lr"], h["wd"], c["beta1"], c["beta2"], c["eps"])
+            for n in ("w", "b", "alpha", "beta"):  # AdamW, decayed like the weights
+                self.emb[k][n], self.emb_m[k][n], self.emb_v[k][n] = mlp.adamw_step(
+                    self.emb[k][n], eg[n], self.emb_m[k][n], self.emb_v[k][n], *args)
+        else:
+            grads = mlp.backward(self.params[k], cache, dY, masks, h["s"])
         new_p, new_m, new_v = [], [], []
         for i, ((W, b), (gW, gb), (mW, mb), (vW, vb)) in enumerate(
                 zip(self.params[k], grads, self.m[k], self.v[k])):
@@ -83,14 +103,18 @@ class OraclePack:
         X = np.asarray(X, dtype=np.float64)
         losses = np.full(K, np.nan)
         self.last_grads = [None] * K
+        self.last_emb_grads = [None] * K
         for k in (range(K) if members is None else members):
             losses[k], self.last_grads[k] = self.member_step(k, X, y, idx[k], step)
         self.t = step
         return losses
 
     def predict(self, k, Xv):
-        """Score-ready prediction of member k on Xv (no dropout)."""
-        Y, _ = mlp.forward(self.params[k], np.asarray(Xv, dtype=np.float64), rnd=self.rnd)
+        """Output of member k on Xv (no dropout)."""
+        H0 = np.asarray(Xv, dtype=np.float64)
+        if self.use_emb:
+            H0, _ = embed.embed(H0, self.emb[k])
+        Y, _ = mlp.forward(self.params[k], H0, rnd=self.rnd)
         return Y
 
     def predict_values(self, k, X):

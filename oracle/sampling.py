@@ -14,6 +14,9 @@ weight decay:
               depth range is given, otherwise every member has L hidden blocks)
     muon_lr ~ LogUniform[muon_lr_lo, muon_lr_hi]  (App. F: "Muon learning rate";
               only with the Muon optimizer)
+    d_emb   ~ emb_lo + emb_step UniformInt[0, (emb_hi - emb_lo) / emb_step],
+    sigma   ~ LogUniform[sigma_lo, sigma_hi]      (App. F: periodic embeddings;
+              only when emb_lo > 0)
 
 Random words come from Philox4x32-10 (``oracle.philox``) with the stream tag
 folded into the key:  key = (seed mod 2**32, (seed >> 32) XOR (tag << 28)),
@@ -22,7 +25,8 @@ tag 1 = hyperparameters, 2 = initial parameters, 3 = dropout.
 * hyperparameters of member k: block (k, 0, 0, 0) gives two doubles u0, u1
   (width, dropout); block (k, 1, 0, 0) gives u2, u3 (lr, wd); block
   (k, 2, 0, 0) gives u4 (depth; its last two words are unused); block
-  (k, 3, 0, 0) gives u5 (the Muon learning rate; last two words unused).  A double is
+  (k, 3, 0, 0) gives u5 (the Muon learning rate; last two words unused);
+  block (k, 4, 0, 0) gives u6 (d_emb) and u7 (sigma).  A double is
   built from two words (a, b) as ((a >> 5) * 2**26 + (b >> 6)) * 2**-53.
 * initial parameters follow torch.nn.Linear's default: W and b uniform on
   [-1/sqrt(fan_in), 1/sqrt(fan_in)], fan_in = the member's true input width.
@@ -82,6 +86,11 @@ def sample_hparams(cfg):
         if cfg.get("optimizer", "adamw") == "muon":
             w = [int(x) for x in philox4x32_10(k, 3, 0, 0, k0, k1)]
             hp["muon_lr"] = _log_uniform(cfg["muon_lr_lo"], cfg["muon_lr_hi"], _u53(w[0], w[1]))
+        if int(cfg.get("emb_lo", 0) or 0) > 0:
+            w = [int(x) for x in philox4x32_10(k, 4, 0, 0, k0, k1)]
+            lo, hi, st = int(cfg["emb_lo"]), int(cfg["emb_hi"]), int(cfg["emb_step"])
+            hp["d_emb"] = lo + st * int(math.floor(_u53(w[0], w[1]) * ((hi - lo) // st + 1)))
+            hp["sigma"] = _log_uniform(cfg["sigma_lo"], cfg["sigma_hi"], _u53(w[2], w[3]))
         out.append(hp)
     return out
 
@@ -103,19 +112,20 @@ def member_depth(cfg, hp):
     return int(cfg["L"]) if d is None else int(d)
 
 
-def layer_shapes(cfg, width, depth=None):
-    """[(out, in), ...] for W_1..W_depth and the head W_out of one member."""
+def layer_shapes(cfg, width, depth=None, d_first=None):
+    """[(out, in), ...] for W_1..W_depth and the head W_out of one member;
+    d_first: the first layer's input width (d_in * d_emb with embeddings)."""
     L = int(cfg["L"]) if depth is None else int(depth)
-    shapes = [(width, cfg["d_in"])] + [(width, width)] * (L - 1)
+    shapes = [(width, cfg["d_in"] if d_first is None else int(d_first))] + [(width, width)] * (L - 1)
     shapes.append((cfg["d_out"], width))
     return shapes
 
 
-def init_member(cfg, k, width, depth=None):
+def init_member(cfg, k, width, depth=None, d_first=None):
     """Initial (W, b) pairs of member k, float32 values held in float64 arrays."""
     k0, k1 = stream_key(cfg["seed"], TAG_INIT)
     params = []
-    for i, (n_out, n_in) in enumerate(layer_shapes(cfg, width, depth)):
+    for i, (n_out, n_in) in enumerate(layer_shapes(cfg, width, depth, d_first)):
         bound = 1.0 / math.sqrt(n_in)
         pair = []
         for t, n in ((2 * i, n_out * n_in), (2 * i + 1, n_out)):
