@@ -186,6 +186,44 @@ def muon_optimizer(cfg, Xtr, ytr, steps=20):
             "kernels_ms_per_step": {x["name"]: round(x["busy_ms"] / 3, 4) for x in stats}}
 
 
+def embeddings(cfg, Xtr, ytr, steps=10):
+    """Step time of the same workload with periodic feature embeddings
+    (d_emb ~ UniformInt[8, 32] step 4, sigma ~ LogUniform[1e-2, 10]): the first
+    layer then reads d_in * d_emb columns per member; per-kernel rates from the
+    library's events."""
+    import torch
+    from paper_2607_05380_amd import tabpack
+    pk = tabpack.Pack(dict(cfg, keep_grads=0, emb_lo=8, emb_hi=32, emb_step=4, sigma_lo=1e-2,
+                           sigma_hi=10.0)).bind(Xtr.device)
+    hp = pk.hparams()
+    idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
+    loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
+    pk.train_step(Xtr, ytr, idx, 1, loss)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for s in range(steps):
+        pk.train_step(Xtr, ytr, idx, s + 2, loss)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    pk.profile(True)
+    for s in range(2):
+        pk.train_step(Xtr, ytr, idx, steps + 2 + s, loss)
+    stats = pk.profile_read()
+    pk.profile(False)
+    flops = sum(x["flops"] * x["launches"] for x in stats if x["kind"] == "mfma" or "gemm" in x["name"]) / 2
+    out = {"d_emb_mean": round(sum(h["d_emb"] for h in hp) / len(hp), 2), "step_ms": round(ms, 3),
+           "workspace_gib": round(pk.workspace_bytes() / 2 ** 30, 2), "gemm_tflop_per_step": round(flops / 1e12, 3),
+           "kernels": {x["name"]: {"busy_ms_per_step": round(x["busy_ms"] / 2, 4),
+                                   "tflop_per_s": round(x["flops"] * x["launches"] / x["busy_ms"] / 1e9, 1),
+                                   "gb_per_s": round(x["bytes"] * x["launches"] / x["busy_ms"] / 1e6, 1)}
+                       for x in stats}}
+    del pk
+    torch.cuda.empty_cache()
+    return out
+
+
 def synth_idx(cfg, n, device):
     from paper_2607_05380_amd import synth
     return synth.epoch_orders_device(cfg, 1, n, device)[:, :cfg["B"]].contiguous()
@@ -335,6 +373,8 @@ def main():
         log(f"  variable depth: {json.dumps(out['variable_depth'])}")
         out["muon"] = muon_optimizer(cfg, Xtr, ytr)
         log(f"  Muon optimizer: {json.dumps(out['muon'])}")
+        out["embeddings"] = embeddings(cfg, Xtr, ytr)
+        log(f"  periodic embeddings: {json.dumps(out['embeddings'])}")
     if not a.no_cpu_baseline:
         log("timing the fp64 oracle on the host (bounded sample)")
         out["cpu_baseline"] = cpu_baseline(cfg, Xtr, ytr, idx_all[0])

@@ -62,6 +62,9 @@ typedef struct pack_member_hp {
   double wd;               /* AdamW decoupled weight decay, >= 0 */
   double scale;            /* out: inverted-dropout scale s_k = 1 / (1 - p_k) */
   double muon_lr;          /* Muon learning rate of the hidden weights (PACK_OPT_MUON), > 0 */
+  int32_t d_emb;           /* periodic embedding size per feature, 2 .. 32 (packs with embeddings) */
+  int32_t reserved2;
+  double sigma;            /* standard deviation of the embedding frequencies' initial values, > 0 */
 } pack_member_hp;
 
 /* Description of a pack.  Ranges are inclusive: width ~ UniformInt[lo, hi],
@@ -107,6 +110,18 @@ typedef struct pack_config {
   double muon_momentum;          /* mu in [0, 1) */
   int32_t muon_nesterov;         /* 1: Nesterov direction, 0: the momentum buffer */
   int32_t reserved;
+  /* Periodic feature embeddings (App. "Feature Embeddings"): with emb_lo > 0
+   * each member maps feature x_i to d_emb values alpha_i * [x_i, cos(w_i x_i +
+   * b_i)] + beta_i (w_i, b_i of length d_emb - 1; alpha_i, beta_i of length
+   * d_emb), concatenated feature-major into the first layer's d_in * d_emb
+   * inputs.  Initial values: w ~ N(0, sigma), b = alpha = beta = 0; trained
+   * with AdamW.  d_emb ~ emb_lo + emb_step * UniformInt[0, (emb_hi - emb_lo) /
+   * emb_step] (2 <= lo <= hi <= 32), sigma ~ LogUniform[sigma_lo, sigma_hi].
+   * The member's dense parameter vector then starts with w, b, alpha, beta
+   * (row-major [d_in, d_emb - 1] / [d_in, d_emb]). */
+  int32_t emb_lo, emb_hi, emb_step;
+  int32_t reserved3;
+  double sigma_lo, sigma_hi;
 } pack_config;
 
 typedef struct pack_handle pack_handle;

@@ -64,6 +64,11 @@ struct Member {
   int depth;  // hidden Linear-ReLU-Dropout blocks, 1 .. L
   double dropout, lr, wd, scale;
   double muon_lr = 0.0;  // Muon learning rate of the hidden weights (Muon packs)
+  int d_emb = 0;         // periodic embedding size per feature (0: the features feed W_1 directly)
+  double sigma = 0.0;    // standard deviation of the embedding frequencies' initial values
+  int p_in = 0;          // columns of W_1 and of the first layer's input (padded d_in * d_emb, or Pin)
+  int64_t eoff[4] = {};  // embedding parameters w, b, alpha, beta (offsets in theta)
+  int64_t h0_off = 0;    // the member's first-layer input block (elements of the H_0 / E buffer)
   uint32_t t;
   std::vector<int64_t> toff;  // packed offsets of W_1, b_1, ..., W_depth, b_depth, W_out, b_out
   int64_t act_off;
@@ -95,7 +100,8 @@ struct ProfGroup {
 struct Bufs {
   float *theta = nullptr, *grad = nullptr, *m = nullptr, *v = nullptr;
   uint16_t* shadow = nullptr;
-  char* H0 = nullptr;  // gathered batches (K x [Bp, Pin]) in the GEMM precision
+  char* H0 = nullptr;  // first-layer inputs: gathered batches [Bp, Pin], or embedded batches E [Bp, p_in], per member
+  float* dE = nullptr; // embeddings: the gradient of E (fp32), same layout
   char* H = nullptr;   // L activation buffers H_1..H_L
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
   float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / kPartRows floats
@@ -143,6 +149,8 @@ struct pack_handle {
   std::vector<int32_t> active_ids;   // increasing
   int64_t n_aux_active = 0;          // aux chunks of active members (uploaded first in d_aux)
   bool muon = false;                 // hidden weights on Muon (pack_config.optimizer)
+  bool emb = false;                  // periodic feature embeddings (pack_config.emb_lo > 0)
+  Launch de[kGroups]{};
   int ns_steps = 5;
   int n_mmats = 0, n_mtiles = 0;     // Muon matrices and tiles of the active members
   Launch nsA[2]{}, nsB{}, nsX[2]{};
@@ -185,7 +193,7 @@ struct pack_handle {
 
   size_t elt() const { return prec == Prec::BF16 ? 2 : 4; }
   void* Hl(int l) const { return b.H + (size_t)(l - 1) * A * elt(); }  // H_l, l = 1..L
-  size_t h0_elems() const { return (size_t)Bp * Pin; }                  // one member's H_0
+  int64_t H0e = 0;  // elements of the H_0 / E buffer (every member's first-layer input block)
   void* dzb(int l) const { return b.dz + (size_t)(l & 1) * A * elt(); } // buffer holding dZ_l
 };
 
@@ -213,6 +221,14 @@ int validate(const pack_config* c) {
   if (c->keep_grads != 0 && c->keep_grads != 1) return fail(PACK_EINVAL, "keep_grads must be 0 or 1");
   if (!(c->beta1 >= 0 && c->beta1 < 1 && c->beta2 >= 0 && c->beta2 < 1 && c->eps > 0))
     return fail(PACK_EINVAL, "AdamW constants out of range");
+  if (c->emb_lo != 0) {
+    if (c->emb_lo < 2 || c->emb_hi < c->emb_lo || c->emb_hi > 32 || c->emb_step < 1 ||
+        (c->emb_hi - c->emb_lo) % c->emb_step)
+      return fail(PACK_EINVAL, "embedding size range [%d, %d] step %d invalid (2 <= lo <= hi <= 32)", c->emb_lo,
+                  c->emb_hi, c->emb_step);
+    if (!c->members && !(c->sigma_lo > 0 && c->sigma_hi >= c->sigma_lo))
+      return fail(PACK_EINVAL, "embedding sigma range must be positive and ordered");
+  }
   if (c->optimizer != PACK_OPT_ADAMW && c->optimizer != PACK_OPT_MUON)
     return fail(PACK_EINVAL, "unknown optimizer %d", c->optimizer);
   if (c->optimizer == PACK_OPT_MUON) {
@@ -252,6 +268,11 @@ void sample_members(pack_handle* h) {
       const Words4 d = philox4x32_10((uint32_t)k, 3, 0, 0, key.k0, key.k1);
       m.muon_lr = log_uniform(c.muon_lr_lo, c.muon_lr_hi, u53(d.w0, d.w1));
     }
+    if (c.emb_lo > 0) {  // embedding size and sigma from block (k, 4, 0, 0)
+      const Words4 d = philox4x32_10((uint32_t)k, 4, 0, 0, key.k0, key.k1);
+      m.d_emb = c.emb_lo + c.emb_step * (int)std::floor(u53(d.w0, d.w1) * (double)((c.emb_hi - c.emb_lo) / c.emb_step + 1));
+      m.sigma = log_uniform(c.sigma_lo, c.sigma_hi, u53(d.w2, d.w3));
+    }
   }
 }
 
@@ -266,13 +287,30 @@ void plan_layout(pack_handle* h) {
   int64_t off = 0, aoff = 0;
   h->chunk_tab.clear();
   h->aux_chunks.clear();
+  int64_t h0 = 0;
   for (int k = 0; k < c.K; ++k) {
     Member& m = h->mem[k];
     m.dp = (int)round_up(m.width, h->q);
+    m.p_in = m.d_emb ? (int)round_up((int64_t)c.d_in * m.d_emb, 8) : h->Pin;
+    m.h0_off = h0;
+    h0 += (int64_t)h->Bp * m.p_in;
+    if (m.d_emb) {  // embedding parameters first: w, b [d_in, d_emb-1], alpha, beta [d_in, d_emb] (AdamW)
+      const int64_t n[4] = {(int64_t)c.d_in * (m.d_emb - 1), (int64_t)c.d_in * (m.d_emb - 1),
+                            (int64_t)c.d_in * m.d_emb, (int64_t)c.d_in * m.d_emb};
+      for (int t = 0; t < 4; ++t) {
+        m.eoff[t] = off;
+        const int64_t nc = round_up(n[t], kChunk) / kChunk;
+        for (int64_t i = 0; i < nc; ++i) {
+          h->aux_chunks.push_back((uint32_t)h->chunk_tab.size());
+          h->chunk_tab.push_back((uint32_t)k);
+        }
+        off += nc * kChunk;
+      }
+    }
     m.toff.assign(2 * m.depth + 2, 0);
     for (int l = 0; l <= m.depth; ++l) {
       const int64_t rows = l < m.depth ? m.dp : c.d_out;
-      const int64_t cols = l == 0 ? h->Pin : m.dp;
+      const int64_t cols = l == 0 ? m.p_in : m.dp;
       for (int part = 0; part < 2; ++part) {
         const int64_t n = part == 0 ? rows * cols : rows;
         m.toff[2 * l + part] = off;
@@ -292,6 +330,7 @@ void plan_layout(pack_handle* h) {
   }
   h->P = off;
   h->A = aoff;
+  h->H0e = h0;
 }
 
 // torch.nn.Linear default initialisation, U(-1/sqrt(fan_in), 1/sqrt(fan_in)),
@@ -303,10 +342,25 @@ void init_params(pack_handle* h) {
   const Key key = stream_key(c.seed, kTagInit);
   for (int k = 0; k < c.K; ++k) {
     const Member& m = h->mem[k];
+    if (m.d_emb) {
+      // embedding frequencies w ~ N(0, sigma) by Box-Muller: element e takes block
+      // (e >> 1, 0, 100, k); u1 = ((word0 >> 8) + 1) 2^-24, u2 = (word1 >> 8) 2^-24;
+      // cos for even e, sin for odd e.  b, alpha, beta start at zero.
+      const int64_t n = (int64_t)c.d_in * (m.d_emb - 1);
+      float* dst = h->theta_host.data() + m.eoff[0];
+      for (int64_t e = 0; e < n; ++e) {
+        const Words4 w = philox4x32_10((uint32_t)(e >> 1), 0, 100, (uint32_t)k, key.k0, key.k1);
+        const double u1 = (double)((w.w0 >> 8) + 1) * (1.0 / 16777216.0);
+        const double u2 = (double)(w.w1 >> 8) * (1.0 / 16777216.0);
+        const double r = std::sqrt(-2.0 * std::log(u1));
+        const double z = r * ((e & 1) == 0 ? std::cos(2.0 * M_PI * u2) : std::sin(2.0 * M_PI * u2));
+        dst[e] = (float)(m.sigma * z);
+      }
+    }
     for (int l = 0; l <= m.depth; ++l) {
       const int rows = l < m.depth ? m.width : c.d_out;
-      const int fan_in = l == 0 ? c.d_in : m.width;
-      const int64_t ld = l == 0 ? h->Pin : m.dp;
+      const int fan_in = l == 0 ? (m.d_emb ? c.d_in * m.d_emb : c.d_in) : m.width;
+      const int64_t ld = l == 0 ? m.p_in : m.dp;
       const double bound = 1.0 / std::sqrt((double)fan_in);
       for (int part = 0; part < 2; ++part) {
         const uint32_t tid = (uint32_t)(2 * l + part);
@@ -333,7 +387,9 @@ void init_params(pack_handle* h) {
 int64_t dense_count(const pack_handle* h, int k) {
   const Member& m = h->mem[k];
   const pack_config& c = h->cfg;
-  return (int64_t)m.width * c.d_in + m.width + (int64_t)(m.depth - 1) * ((int64_t)m.width * m.width + m.width) +
+  const int64_t fi = m.d_emb ? (int64_t)c.d_in * m.d_emb : c.d_in;
+  const int64_t emb = m.d_emb ? 2 * (int64_t)c.d_in * (2 * m.d_emb - 1) : 0;
+  return emb + (int64_t)m.width * fi + m.width + (int64_t)(m.depth - 1) * ((int64_t)m.width * m.width + m.width) +
          (int64_t)c.d_out * m.width + c.d_out;
 }
 
@@ -342,19 +398,27 @@ void for_each_dense(const pack_handle* h, int k, F f) {  // f(dense_index, packe
   const Member& m = h->mem[k];
   const pack_config& c = h->cfg;
   int64_t di = 0;
+  if (m.d_emb) {  // embedding parameters first: w, b [d_in, d_emb-1], alpha, beta [d_in, d_emb]
+    const int64_t n[4] = {(int64_t)c.d_in * (m.d_emb - 1), (int64_t)c.d_in * (m.d_emb - 1),
+                          (int64_t)c.d_in * m.d_emb, (int64_t)c.d_in * m.d_emb};
+    for (int t = 0; t < 4; ++t)
+      for (int64_t e = 0; e < n[t]; ++e) f(di++, m.eoff[t] + e);
+  }
   for (int l = 0; l <= m.depth; ++l) {
     const int rows = l < m.depth ? m.width : c.d_out;
-    const int cols = l == 0 ? c.d_in : m.width;
-    const int64_t ld = l == 0 ? h->Pin : m.dp;
+    const int cols = l == 0 ? (m.d_emb ? c.d_in * m.d_emb : c.d_in) : m.width;
+    const int64_t ld = l == 0 ? m.p_in : m.dp;
     for (int r = 0; r < rows; ++r)
       for (int cc = 0; cc < cols; ++cc) f(di++, m.toff[2 * l] + (int64_t)r * ld + cc);
     for (int r = 0; r < rows; ++r) f(di++, m.toff[2 * l + 1] + r);
   }
 }
 
-int64_t member_span_begin(const pack_handle* h, int k) { return h->mem[k].toff[0]; }
+int64_t member_span_begin(const pack_handle* h, int k) {
+  return h->mem[k].d_emb ? h->mem[k].eoff[0] : h->mem[k].toff[0];
+}
 int64_t member_span_end(const pack_handle* h, int k) {
-  return k + 1 < h->cfg.K ? h->mem[k + 1].toff[0] : h->P;
+  return k + 1 < h->cfg.K ? member_span_begin(h, k + 1) : h->P;
 }
 
 // Device-table sizes.
@@ -378,6 +442,8 @@ struct Plan {
   std::vector<MuonTile> mtiles;
   std::vector<int32_t> mtile0;
   Launch nsA[2]{}, nsB{}, nsX[2]{};
+  // embeddings: dE = dZ_1 W_1 per group (the first layer's data gradient, fp32)
+  Launch de[kGroups]{};
 };
 
 // Tiles of one member's M x N output.  Big set: 256 x 256 tiles, except that
@@ -471,7 +537,7 @@ void split_members(pack_handle* h) {
   std::vector<std::pair<double, int>> cost;
   for (int k : h->active_ids) {
     const double w = h->mem[k].dp;
-    cost.push_back({w * (h->Pin + (h->mem[k].depth - 1) * w), k});
+    cost.push_back({w * (h->mem[k].p_in + (h->mem[k].depth - 1) * w), k});
   }
   std::stable_sort(cost.begin(), cost.end(), [](const auto& x, const auto& y) { return x.first > y.first; });
   std::vector<double> load(h->ngroups, 0.0);
@@ -495,9 +561,9 @@ struct MuonShape {
 MuonShape muon_shape(const pack_handle* h, const Member& m, int l) {
   MuonShape q;
   q.R = m.dp;
-  q.Cp = l == 1 ? h->Pin : m.dp;
+  q.Cp = l == 1 ? m.p_in : m.dp;
   q.r = m.width;
-  q.c = l == 1 ? h->cfg.d_in : m.width;
+  q.c = l == 1 ? (m.d_emb ? h->cfg.d_in * m.d_emb : h->cfg.d_in) : m.width;
   q.tall = q.r > q.c;
   q.S = q.tall ? q.Cp : q.R;
   q.L = q.tall ? q.R : q.Cp;
@@ -649,7 +715,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
   auto maskp = [&](int l, int k) -> uint32_t* {  // keep bits of H_l (1-based) of member k
     return bf.mask + (size_t)(l - 1) * (h->A / 32) + h->mem[k].act_off / 32;
   };
-  auto h0 = [&](int k) -> void* { return bf.H0 + (size_t)k * h->h0_elems() * es; };
+  auto h0 = [&](int k) -> void* { return bf.H0 + (size_t)h->mem[k].h0_off * es; };
   auto keepw = [&](int par, int l, int k) -> const uint32_t* {
     return bf.keepw + (size_t)par * c.L * (h->A / 32) + (maskp(l, k) - bf.mask);
   };
@@ -665,15 +731,15 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       ++f.ndesc;
       GemmDesc d{};
       d.A = l == 1 ? h0(k) : act(Hl(l - 1), k);
-      d.lda = l == 1 ? h->Pin : m.dp;
+      d.lda = l == 1 ? m.p_in : m.dp;
       d.B = wptr(k, l);
-      d.ldb = l == 1 ? h->Pin : m.dp;
+      d.ldb = l == 1 ? m.p_in : m.dp;
       d.C = act(Hl(l), k);
       d.ldc = m.dp;
       d.bias = bf.theta + m.toff[2 * (l - 1) + 1];
       d.M = h->Bp;
       d.N = m.dp;
-      d.Kd = l == 1 ? h->Pin : m.dp;
+      d.Kd = l == 1 ? m.p_in : m.dp;
       d.width = m.width;
       d.member = k;
       d.drop_t = m.t;
@@ -683,7 +749,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       add_tiles(p, f, (int)p.descs.size(), h->Bp, m.dp, d.Kd);
       p.descs.push_back(d);
       {
-        const double fi = l == 1 ? c.d_in : m.width, w = m.width;
+        const double fi = l == 1 ? (m.d_emb ? (double)c.d_in * m.d_emb : c.d_in) : m.width, w = m.width;
         f.flops += 2.0 * c.B * w * fi;
         // H_{l-1} and W_l read, H_l written (2-byte elements in bf16), keep words read, mask words written
         f.bytes += (double)h->elt() * (c.B * fi + fi * w + c.B * w) + c.B * w / 4.0;
@@ -700,7 +766,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       for (int i = 0; i < (int)group[hf].size(); ++i) {
         const int k = group[hf][i];
         GemmDesc d = p.descs[p.fwd[0][hf][0].desc0 + i];
-        d.A = h0(0);
+        if (h->mem[k].d_emb == 0) d.A = h0(0);  // embedded members read their own E block
         add_tiles(p, f, (int)p.descs.size(), h->Bp, h->mem[k].dp, d.Kd);
         p.descs.push_back(d);
       }
@@ -719,11 +785,11 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       d.A = act(dzb(l), k);
       d.lda = m.dp;
       d.B = l == 1 ? h0(k) : act(Hl(l - 1), k);
-      d.ldb = l == 1 ? h->Pin : m.dp;
+      d.ldb = l == 1 ? m.p_in : m.dp;
       d.C = bf.grad + m.toff[2 * (l - 1)];
-      d.ldc = l == 1 ? h->Pin : m.dp;
+      d.ldc = l == 1 ? m.p_in : m.dp;
       d.M = m.dp;
-      d.N = l == 1 ? h->Pin : m.dp;
+      d.N = l == 1 ? m.p_in : m.dp;
       d.Kd = h->Bp;
       d.member = k;
       d.poff = m.toff[2 * (l - 1)];
@@ -732,7 +798,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       add_tiles(p, w, (int)p.descs.size(), d.M, d.N, d.Kd);
       p.descs.push_back(d);
       {
-        const double fi = l == 1 ? c.d_in : m.width, wd = m.width;
+        const double fi = l == 1 ? (m.d_emb ? (double)c.d_in * m.d_emb : c.d_in) : m.width, wd = m.width;
         w.flops += 2.0 * c.B * wd * fi;
         // dZ_l and H_{l-1} read; per weight: the fused AdamW's theta, m, v read and written
         // (24 B) and the bf16 shadow written (2 B), plus the fp32 gradient when it is kept
@@ -787,6 +853,35 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
             for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
     }
   p.coltile0[(size_t)kGroups * c.L] = (int)p.coltiles.size();
+  const TileSet saved_ts = p.tile_set;
+  p.tile_set = TILES_SMALL;  // the embedding's data-gradient GEMM runs small tiles only
+  for (int hf = 0; hf < kGroups; ++hf) {
+    Launch& ln = p.de[hf];
+    ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
+    for (int k : group[hf]) {
+      const Member& m = h->mem[k];
+      if (!m.d_emb) continue;
+      GemmDesc d{};
+      d.A = act(dzb(1), k);
+      d.lda = m.dp;
+      d.B = wptr(k, 1);  // W_1 [dp, p_in] read as rows-contiguous: element (n, k) at W_1[k * p_in + n]
+      d.ldb = m.p_in;
+      d.C = bf.dE + m.h0_off;
+      d.ldc = m.p_in;
+      d.M = h->Bp;
+      d.N = m.p_in;
+      d.Kd = m.dp;
+      d.member = k;
+      add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
+      p.descs.push_back(d);
+      ++ln.ndesc;
+      const double e = (double)c.d_in * m.d_emb;
+      ln.flops += 2.0 * c.B * m.width * e;
+      ln.bytes += (double)h->elt() * (c.B * m.width + m.width * e) + 4.0 * c.B * e;
+    }
+    sort_launch(p, ln);
+  }
+  p.tile_set = saved_ts;
   const int hcols = head_bwd_cols(c.d_out), hrb = head_rows(h);
   for (int hf = 0; hf < kGroups; ++hf) {
     p.headtile0[hf] = (int)p.headtiles.size();
@@ -824,7 +919,8 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf) {
   bf.m = cv.take<float>(h->P);
   bf.v = cv.take<float>(h->P);
   bf.shadow = h->prec == Prec::BF16 ? cv.take<uint16_t>(h->P) : nullptr;
-  bf.H0 = cv.take<char>((size_t)c.K * h->h0_elems() * h->elt());
+  bf.H0 = cv.take<char>((size_t)h->H0e * h->elt());
+  bf.dE = h->emb ? cv.take<float>((size_t)h->H0e) : nullptr;
   bf.H = cv.take<char>((size_t)c.L * h->A * h->elt());
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
   bf.colpart = cv.take<float>((size_t)h->A / kPartRows);
@@ -966,6 +1062,7 @@ int upload_plan(pack_handle* h, hipStream_t stream) {
     h->nsX[par] = plan.nsX[par];
   }
   h->nsB = plan.nsB;
+  for (int hf = 0; hf < kGroups; ++hf) h->de[hf] = plan.de[hf];
   for (int hf = 0; hf < kGroups; ++hf) {
     h->fwd[0][hf] = plan.fwd[0][hf];
     h->fwd[1][hf] = plan.fwd[1][hf];
@@ -1069,6 +1166,7 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
   }
   if (h->prec == Prec::FP32) h->tiles = TILES_SMALL;
   h->muon = cfg->optimizer == PACK_OPT_MUON;
+  h->emb = cfg->emb_lo > 0;
   h->ns_steps = cfg->ns_steps ? cfg->ns_steps : 5;
   h->Bp = (int)round_up(cfg->B, kRowAlign);
   h->Pin = (int)round_up(cfg->d_in, 8);
@@ -1078,7 +1176,8 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
       const pack_member_hp& e = cfg->members[k];
       if (e.width < 1 || e.width > 16384 || !(e.dropout >= 0 && e.dropout < 1) || !(e.lr > 0) ||
           !(e.wd >= 0) || e.depth < 0 || e.depth > cfg->L ||
-          (cfg->optimizer == PACK_OPT_MUON && !(e.muon_lr > 0))) {
+          (cfg->optimizer == PACK_OPT_MUON && !(e.muon_lr > 0)) ||
+          (cfg->emb_lo > 0 && (e.d_emb < 2 || e.d_emb > 32 || !(e.sigma > 0)))) {
         delete h;
         return fail(PACK_EINVAL, "explicit hyperparameters of member %d out of range", k);
       }
@@ -1088,6 +1187,8 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
       h->mem[k].wd = e.wd;
       h->mem[k].depth = e.depth ? e.depth : cfg->L;
       h->mem[k].muon_lr = cfg->optimizer == PACK_OPT_MUON ? e.muon_lr : 0.0;
+      h->mem[k].d_emb = cfg->emb_lo > 0 ? e.d_emb : 0;
+      h->mem[k].sigma = cfg->emb_lo > 0 ? e.sigma : 0.0;
     }
   } else {
     sample_members(h);
@@ -1128,7 +1229,8 @@ int pack_get_hparams(const pack_handle* h, pack_member_hp* out) {
   if (!h || !out) return fail(PACK_EINVAL, "NULL argument");
   for (int k = 0; k < h->cfg.K; ++k) {
     const Member& m = h->mem[k];
-    out[k] = pack_member_hp{m.width, m.dp, m.t, m.depth, m.dropout, m.lr, m.wd, m.scale, m.muon_lr};
+    out[k] = pack_member_hp{m.width, m.dp, m.t, m.depth, m.dropout, m.lr, m.wd, m.scale, m.muon_lr, m.d_emb, 0,
+                            m.sigma};
   }
   return PACK_OK;
 }
@@ -1168,7 +1270,7 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
     md[k] = MemberDev{m.width, m.dp, m.t, (float)m.scale, (float)m.lr, (float)m.wd, m.act_off,
                       m.toff[2 * m.depth], m.toff[2 * m.depth + 1], m.toff[2 * m.depth - 1],
                       (int64_t)(m.depth - 1) * h->A + m.act_off, (int64_t)(m.depth & 1) * h->A + m.act_off,
-                      m.depth, 0};
+                      m.depth, m.d_emb, m.eoff[0], m.eoff[1], m.eoff[2], m.eoff[3], m.h0_off, m.p_in, 0};
     for (int l = 1; l <= m.depth; ++l) boff[(size_t)(l - 1) * h->cfg.K + k] = m.toff[2 * (l - 1) + 1];
   }
   HIP_TRY(hipMemcpyAsync(h->b.d_mem, md.data(), md.size() * sizeof(MemberDev), hipMemcpyHostToDevice, stream));
@@ -1271,10 +1373,19 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   for (int hf = 0; hf < ng; ++hf) {
     const hipStream_t s = hs[hf];
     const int gk = h->member0[hf + 1] - h->member0[hf];
-    HIP_TRY(timed(h, "gather", 1, 0.0, (double)gk * c.B * c.d_in * (4.0 + h->elt()), s, [&] {
-      return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, gk, h->Bp, h->b.H0,
-                           h->b.d_members + h->member0[hf], s);
-    }));
+    if (h->emb) {
+      double eb = 0;
+      for (int k : h->group[hf]) eb += (double)c.B * h->mem[k].p_in;
+      HIP_TRY(timed(h, "embed_fwd", 1, 0.0, eb * h->elt() + (double)gk * c.B * c.d_in * 4.0, s, [&] {
+        return launch_embed_fwd(h->prec, X, c.d_in, idx, c.B, 0, c.B, h->Bp, h->b.d_mem,
+                                h->b.d_members + h->member0[hf], gk, 0, h->b.theta, h->b.H0, s);
+      }));
+    } else {
+      HIP_TRY(timed(h, "gather", 1, 0.0, (double)gk * c.B * c.d_in * (4.0 + h->elt()), s, [&] {
+        return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, gk, h->Bp, h->b.H0,
+                             h->b.d_members + h->member0[hf], s);
+      }));
+    }
     HIP_TRY(hipStreamWaitEvent(s, h->ev_keep[par], 0));
   }
   for (int l = 1; l <= c.L; ++l)
@@ -1321,6 +1432,18 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                                            h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, s);
         }));
       }
+      if (l == 1 && h->emb) {
+        // dE = dZ_1 W_1 (fp32), before W_1 is updated, then the embedding gradients
+        GemmArgs ae = for_launch(a, h->de[hf]);
+        ae.tile_set = TILES_SMALL;
+        HIP_TRY(timed(h, gemm_name(h->prec, OP_KMAJ, OP_RMAJ, EPI_DW), 0, h->de[hf].flops, h->de[hf].bytes, s,
+                      [&] { return launch_gemm(h->prec, OP_KMAJ, OP_RMAJ, EPI_DW, ae, s); }));
+        const int gk = h->member0[hf + 1] - h->member0[hf];
+        HIP_TRY(timed(h, "embed_bwd", 1, 0.0, h->de[hf].bytes, s, [&] {
+          return launch_embed_bwd(X, c.d_in, idx, c.B, h->b.d_mem, h->b.d_members + h->member0[hf], gk, h->b.theta,
+                                  h->b.dE, h->b.grad, s);
+        }));
+      }
       GemmArgs al = for_launch(a, h->dw[hf][l - 1]);
       al.layer = l;
       if (h->muon) {  // the gradient is stored; the Muon step below updates W_l
@@ -1357,6 +1480,36 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   return PACK_OK;
 }
 
+}  // extern "C"
+
+namespace {
+// Forward pass without dropout of every active member over rows r0 ..
+// r0 + a.rows_valid - 1 of X: the first-layer inputs (the rows gathered once
+// for all members, or each member's embedded rows), then the hidden layers;
+// the last hidden activations are left in H for the head.
+hipError_t eval_forward(pack_handle* h, GemmArgs a, const float* X, int64_t r0, hipStream_t stream) {
+  const pack_config& c = h->cfg;
+  hipError_t e;
+  if (h->emb)
+    e = launch_embed_fwd(h->prec, X, c.d_in, nullptr, c.B, r0, a.rows_valid, h->Bp, h->b.d_mem, h->b.d_active,
+                         (int)h->active_ids.size(), 0, h->b.theta, h->b.H0, stream);
+  else
+    e = launch_gather(h->prec, X, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, nullptr,
+                      stream);
+  if (e != hipSuccess) return e;
+  for (int l = 1; l <= c.L; ++l) {
+    for (int hf = 0; hf < (l == 1 ? 1 : h->ngroups); ++hf) {
+      GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][hf][l - 1]);
+      al.layer = l;
+      if ((e = launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream)) != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+}  // namespace
+
+extern "C" {
+
 int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t Nv, float* pred_out,
                       double* score_out, hipStream_t stream) {
   if (!h) return fail(PACK_EINVAL, "handle is NULL");
@@ -1369,15 +1522,7 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
   GemmArgs a = base_args(h);
   for (int64_t r0 = 0; r0 < Nv; r0 += h->Bp) {
     a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
-    HIP_TRY(launch_gather(h->prec, Xv, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, nullptr,
-                          stream));
-    for (int l = 1; l <= c.L; ++l) {
-      for (int hf = 0; hf < (l == 1 ? 1 : h->ngroups); ++hf) {
-        GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][hf][l - 1]);
-        al.layer = l;
-        HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
-      }
-    }
+    HIP_TRY(eval_forward(h, a, Xv, r0, stream));
     HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadEval, h->b.H, h->b.theta, h->b.d_mem, nact, h->Bp, c.d_out,
                             yv, nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, h->b.d_active,
                             stream));
@@ -1398,15 +1543,7 @@ int pack_predict(pack_handle* h, const float* X, int64_t N, int32_t mode, float*
   GemmArgs a = base_args(h);
   for (int64_t r0 = 0; r0 < N; r0 += h->Bp) {
     a.rows_valid = (int)std::min<int64_t>(h->Bp, N - r0);
-    HIP_TRY(launch_gather(h->prec, X, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, nullptr,
-                          stream));
-    for (int l = 1; l <= c.L; ++l) {
-      for (int hf = 0; hf < (l == 1 ? 1 : h->ngroups); ++hf) {
-        GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][hf][l - 1]);
-        al.layer = l;
-        HIP_TRY(launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream));
-      }
-    }
+    HIP_TRY(eval_forward(h, a, X, r0, stream));
     if (mode == PACK_PREDICT_MEMBERS) {
       // member i (i-th active id) writes rows r0.. of out[i, :, :]
       HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadPredict, h->b.H, h->b.theta, h->b.d_mem, nact, h->Bp,

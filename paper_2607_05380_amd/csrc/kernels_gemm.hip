@@ -1255,6 +1255,10 @@ hipError_t launch_prec(OpKind ak, OpKind bk, EpiKind e, const GemmArgs& args, hi
     return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL>(args, s);
   if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DX) return launch_t<T, OP_KMAJ, OP_RMAJ, EPI_DX>(args, s);
   if (ak == OP_RMAJ && bk == OP_RMAJ && e == EPI_DW) return launch_t<T, OP_RMAJ, OP_RMAJ, EPI_DW>(args, s);
+  if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DW) {  // the embedding's dE: fp32 store, small tiles only
+    if (args.tile_set != TILES_SMALL || args.theta) return hipErrorInvalidValue;
+    return launch_small<T, OP_KMAJ, OP_RMAJ, EPI_DW>(args, s);
+  }
   if (e == EPI_NS) {  // Newton-Schulz products: small tiles only
     if (args.tile_set != TILES_SMALL) return hipErrorInvalidValue;
     if (ak == OP_KMAJ && bk == OP_KMAJ) return launch_small<T, OP_KMAJ, OP_KMAJ, EPI_NS>(args, s);

@@ -106,6 +106,12 @@ struct MemberDev {
   int64_t h_last;           // the member's last hidden activation H_depth: offset from the start of H_1 (elements)
   int64_t dz_last;          // its gradient dZ_depth: offset from the start of the dZ ping-pong pair (elements)
   int32_t depth;            // hidden blocks of the member
+  int32_t d_emb;            // periodic embedding size per feature (0: no embedding)
+  // periodic embeddings: offsets (elements of theta / grad) of w, b [d_in, d_emb-1]
+  // and alpha, beta [d_in, d_emb]; e_act: offset of the member's embedded batch E
+  // [Bp, p_in] in the E buffer and of its gradient in the dE buffer
+  int64_t e_w, e_b, e_a, e_be, e_act;
+  int32_t p_in;             // columns of the first layer's input (padded d_in * d_emb, or d_in)
   int32_t pad_;
 };
 
@@ -168,6 +174,15 @@ hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, fl
                         uint16_t* shadow, const uint32_t* chunk_tab, const uint32_t* list,
                         const MemberDev* mem, int64_t nchunks, const AdamConst& ac, hipStream_t s);
 hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hipStream_t s);
+// Periodic embeddings (kernels_embed.hip).  E of member k = members[g], row r:
+// the embedded row X[idx[k * B + r]] (idx == nullptr: X[row_base + r]) for
+// r < rows_valid, zero above; dE -> the gradients of w, b, alpha, beta.
+hipError_t launch_embed_fwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, int64_t row_base,
+                            int rows_valid, int Bp, const MemberDev* mem, const int32_t* members, int nmembers,
+                            int max_pin, const float* theta, void* E, hipStream_t s);
+hipError_t launch_embed_bwd(const float* X, int d_in, const int32_t* idx, int B, const MemberDev* mem,
+                            const int32_t* members, int nmembers, const float* theta, const float* dE, float* grad,
+                            hipStream_t s);
 // members: the K member ids whose rows of pred are scored (nullptr: 0 .. K-1)
 hipError_t launch_eval_score(Task task, const float* pred, const void* yv, int K, int64_t Nv,
                              double* score_out, const int32_t* members, hipStream_t s);

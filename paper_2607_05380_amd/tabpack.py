@@ -31,7 +31,8 @@ class MemberHP(ctypes.Structure):
     _fields_ = [("width", ctypes.c_int32), ("padded_width", ctypes.c_int32),
                 ("drop_threshold", ctypes.c_uint32), ("depth", ctypes.c_int32),
                 ("dropout", ctypes.c_double), ("lr", ctypes.c_double), ("wd", ctypes.c_double),
-                ("scale", ctypes.c_double), ("muon_lr", ctypes.c_double)]
+                ("scale", ctypes.c_double), ("muon_lr", ctypes.c_double), ("d_emb", ctypes.c_int32),
+                ("reserved2", ctypes.c_int32), ("sigma", ctypes.c_double)]
 
 
 class PackConfig(ctypes.Structure):
@@ -49,7 +50,9 @@ class PackConfig(ctypes.Structure):
                 ("optimizer", ctypes.c_int32), ("ns_steps", ctypes.c_int32),
                 ("muon_lr_lo", ctypes.c_double), ("muon_lr_hi", ctypes.c_double),
                 ("muon_momentum", ctypes.c_double), ("muon_nesterov", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("reserved", ctypes.c_int32), ("emb_lo", ctypes.c_int32), ("emb_hi", ctypes.c_int32),
+                ("emb_step", ctypes.c_int32), ("reserved3", ctypes.c_int32), ("sigma_lo", ctypes.c_double),
+                ("sigma_hi", ctypes.c_double)]
 
 
 class KernelStat(ctypes.Structure):
@@ -137,6 +140,11 @@ def make_config(cfg, members=None):
     c.muon_lr_hi = float(cfg.get("muon_lr_hi", 1e-1))
     c.muon_momentum = float(cfg.get("muon_momentum", 0.95))
     c.muon_nesterov = int(cfg.get("muon_nesterov", 1))
+    c.emb_lo = int(cfg.get("emb_lo", 0) or 0)
+    c.emb_hi = int(cfg.get("emb_hi", 0) or 0)
+    c.emb_step = int(cfg.get("emb_step", 4) or 4)
+    c.sigma_lo = float(cfg.get("sigma_lo", 1e-2))
+    c.sigma_hi = float(cfg.get("sigma_hi", 10.0))
     keep = None
     if members is not None:
         keep = (MemberHP * len(members))()
@@ -147,6 +155,8 @@ def make_config(cfg, members=None):
             keep[i].wd = float(m["wd"])
             keep[i].depth = int(m.get("depth") or 0)
             keep[i].muon_lr = float(m.get("muon_lr", 0.0) or 0.0)
+            keep[i].d_emb = int(m.get("d_emb", 0) or 0)
+            keep[i].sigma = float(m.get("sigma", 0.0) or 0.0)
         c.members = ctypes.cast(keep, ctypes.POINTER(MemberHP))
     return c, keep
 
@@ -185,7 +195,8 @@ class Pack:
         arr = (MemberHP * self.K)()
         _check(self.lib.pack_get_hparams(self.h, arr))
         return [dict(width=a.width, padded_width=a.padded_width, t=a.drop_threshold, depth=a.depth,
-                     dropout=a.dropout, lr=a.lr, wd=a.wd, s=a.scale, muon_lr=a.muon_lr) for a in arr]
+                     dropout=a.dropout, lr=a.lr, wd=a.wd, s=a.scale, muon_lr=a.muon_lr, d_emb=a.d_emb,
+                     sigma=a.sigma) for a in arr]
 
     def workspace_bytes(self):
         n = ctypes.c_size_t()
@@ -285,18 +296,32 @@ class Pack:
         return self.split(k, m), self.split(k, v)
 
     def set_params(self, k, params):
-        flat = np.concatenate([np.concatenate([np.asarray(W, np.float32).ravel(), np.asarray(b, np.float32)])
-                               for W, b in params])
+        """params as ``split`` returns them (embedding dict first when the pack has embeddings)."""
+        parts = []
+        for p in params:
+            if isinstance(p, dict):
+                parts += [np.asarray(p[n], np.float32).ravel() for n in ("w", "b", "alpha", "beta")]
+            else:
+                parts += [np.asarray(p[0], np.float32).ravel(), np.asarray(p[1], np.float32).ravel()]
+        flat = np.concatenate(parts)
         assert flat.size == self.param_count(k)
         flat = np.ascontiguousarray(flat)
         _check(self.lib.pack_set_params(self.h, k, flat.ctypes.data))
 
     def split(self, k, flat):
-        """Dense member vector -> [(W [out, in], b [out]), ...] for the L blocks and the head."""
+        """Dense member vector -> [(W [out, in], b [out]), ...] for the L_k blocks and the head,
+        preceded by a dict of the embedding parameters w, b [d_in, d_emb-1], alpha, beta
+        [d_in, d_emb] when the pack has embeddings."""
         hp = self.hparams()[k]
-        w, depth = hp["width"], hp["depth"]
-        dims = [self.d_in] + [w] * depth + [self.d_out]
+        w, depth, de = hp["width"], hp["depth"], hp["d_emb"]
+        dims = [self.d_in * de if de else self.d_in] + [w] * depth + [self.d_out]
         out, o = [], 0
+        if de:
+            emb = {}
+            for n, cols in (("w", de - 1), ("b", de - 1), ("alpha", de), ("beta", de)):
+                emb[n] = flat[o:o + self.d_in * cols].reshape(self.d_in, cols)
+                o += self.d_in * cols
+            out.append(emb)
         for i in range(depth + 1):
             n_in, n_out = dims[i], dims[i + 1]
             W = flat[o:o + n_in * n_out].reshape(n_out, n_in)

@@ -54,7 +54,8 @@ def oracle_cfg(cfg):
     out = {k: cfg[k] for k in ORACLE_KEYS}
     out["depth_lo"], out["depth_hi"] = cfg.get("depth_lo", 0), cfg.get("depth_hi", 0)
     for k, v in (("optimizer", "adamw"), ("muon_lr_lo", 1e-3), ("muon_lr_hi", 1e-1), ("muon_momentum", 0.95),
-                 ("muon_nesterov", 1), ("ns_steps", 5)):
+                 ("muon_nesterov", 1), ("ns_steps", 5), ("emb_lo", 0), ("emb_hi", 0), ("emb_step", 4),
+                 ("sigma_lo", 1e-2), ("sigma_hi", 10.0)):
         out[k] = cfg.get(k, v)
     return out
 
@@ -62,8 +63,12 @@ def oracle_cfg(cfg):
 def oracle_hparams(cfg, members=None):
     if members is None:
         return sample_hparams(oracle_cfg(cfg))
-    return [member_hparams(m["width"], m["dropout"], m["lr"], m["wd"], m.get("depth"), m.get("muon_lr"))
-            for m in members]
+    out = [member_hparams(m["width"], m["dropout"], m["lr"], m["wd"], m.get("depth"), m.get("muon_lr"))
+           for m in members]
+    for h, m in zip(out, members):
+        if m.get("d_emb"):
+            h["d_emb"], h["sigma"] = int(m["d_emb"]), float(m["sigma"])
+    return out
 
 
 def close_mask(gpu, ref, rtol, atol):

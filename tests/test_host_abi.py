@@ -152,3 +152,26 @@ def test_sampled_muon_lrs_match_oracle():
     assert all(b["muon_lr"] == 0.0 for b in base)
     with pytest.raises(tabpack.PackError, match="Muon"):
         tabpack.Pack(dict(cfg, muon_lr_lo=0.0))
+
+
+def test_embedding_hparams_and_init_match_oracle():
+    from oracle.embed import init_embedding
+    cfg = configs.workload("regression_onehot", K=6, emb_lo=8, emb_hi=32, emb_step=4, sigma_lo=1e-2, sigma_hi=10.0)
+    oc = dict(oracle_cfg(cfg), emb_lo=8, emb_hi=32, emb_step=4, sigma_lo=1e-2, sigma_hi=10.0)
+    pk = tabpack.Pack(cfg)
+    got = pk.hparams()
+    ref = sample_hparams(oc)
+    for g, r in zip(got, ref):
+        assert g["d_emb"] == r["d_emb"] and g["sigma"] == pytest.approx(r["sigma"], rel=4e-16, abs=0)
+    for k in range(3):
+        params = pk.get_params(k)
+        emb, layers = params[0], params[1:]
+        ref_emb = init_embedding(oc, k, got[k]["d_emb"], got[k]["sigma"])
+        for n in ("w", "b", "alpha", "beta"):
+            np.testing.assert_array_equal(emb[n], ref_emb[n].astype(np.float32), err_msg=n)
+        ref_layers = init_member(oc, k, got[k]["width"], None, cfg["d_in"] * got[k]["d_emb"])
+        assert layers[0][0].shape == (got[k]["width"], cfg["d_in"] * got[k]["d_emb"])
+        for (W, b), (Wr, br) in zip(layers, ref_layers):
+            np.testing.assert_array_equal(W, Wr.astype(np.float32))
+            np.testing.assert_array_equal(b, br.astype(np.float32))
+        assert pk.param_count(k) == sum(a.size for a in emb.values()) + sum(W.size + b.size for W, b in layers)
