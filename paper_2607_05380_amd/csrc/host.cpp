@@ -584,6 +584,18 @@ void muon_sizes(const pack_handle* h, It begin, It end, int64_t& xe, int64_t& ae
   }
 }
 
+// Small tiles on and above the diagonal of a symmetric S x S result (the
+// others are written as mirror images by the tiles above the diagonal).
+void add_tiles_sym(Plan& p, Launch& ln, int d, int S, int kdepth) {
+  for (int m0 = 0; m0 < S; m0 += kSmallTile)
+    for (int n0 = m0; n0 < S; n0 += kSmallTile) {
+      const int mb = std::min(kSmallTile, S - m0), nb = std::min(kSmallTile, S - n0);
+      p.tiles.push_back(Tile{d, m0, n0, kShapeSmall});
+      p.cost.push_back((int64_t)kdepth * mb * nb * (m0 < n0 ? 2 : 1));
+    }
+  ln.ntiles = (int)p.tiles.size() - ln.tile0;
+}
+
 void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&group)[kGroups], Plan& p) {
   const size_t es = h->elt();
   const TileSet saved = p.tile_set;
@@ -638,16 +650,17 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
       d.ldc = it.q.S;
       d.M = d.N = it.q.S;
       d.Kd = it.q.L;
-      add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
+      add_tiles_sym(p, ln, (int)p.descs.size(), it.q.S, d.Kd);
       p.descs.push_back(d);
       ++ln.ndesc;
       const double s = std::min(it.q.r, it.q.c), l = std::max(it.q.r, it.q.c);
-      ln.flops += 2.0 * s * s * l;
+      ln.flops += s * (s + 1) * l;  // a symmetric result: the upper triangle
       ln.bytes += es * (s * l + s * s);
     }
     sort_launch(p, ln);
   }
-  // B' = b A + c A A (A symmetric in exact arithmetic; read as A A all the same)
+  // B' = b A + c A A: A is stored exactly symmetric (mirrored tiles), so A A =
+  // A A^T reads both operands depth-contiguous, and B' is symmetric too
   {
     Launch& ln = p.nsB;
     ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
@@ -660,11 +673,11 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
       d.Y = ap(bf.mA, it.aoff);
       d.ldy = it.q.S;
       d.M = d.N = d.Kd = it.q.S;
-      add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
+      add_tiles_sym(p, ln, (int)p.descs.size(), it.q.S, d.Kd);
       p.descs.push_back(d);
       ++ln.ndesc;
       const double s = std::min(it.q.r, it.q.c);
-      ln.flops += 2.0 * s * s * s;
+      ln.flops += s * (s + 1) * s;  // a symmetric result: the upper triangle
       ln.bytes += es * 3.0 * s * s;
     }
     sort_launch(p, ln);
@@ -1108,21 +1121,22 @@ hipError_t muon_step(pack_handle* h, const GemmArgs& base, hipStream_t stream) {
   });
   if (e != hipSuccess) return e;
   static const float kA = 3.4445f, kB = -4.7750f, kC = 2.0315f;
-  auto ns = [&](const Launch& ln, OpKind bk, float alpha, float beta) {
+  auto ns = [&](const Launch& ln, OpKind bk, float alpha, float beta, bool sym) {
     GemmArgs g = base;
     g.tiles += ln.tile0;
     g.ntiles = ln.ntiles;
     g.tile_set = TILES_SMALL;
     g.ns_alpha = alpha;
     g.ns_beta = beta;
+    g.ns_sym = sym ? 1 : 0;
     return timed(h, gemm_name(h->prec, OP_KMAJ, bk, EPI_NS), 0, ln.flops, ln.bytes, stream,
                  [&] { return launch_gemm(h->prec, OP_KMAJ, bk, EPI_NS, g, stream); });
   };
   for (int it = 0; it < h->ns_steps; ++it) {
     const int par = it & 1;
-    if ((e = ns(h->nsA[par], OP_KMAJ, 0.0f, 1.0f)) != hipSuccess) return e;
-    if ((e = ns(h->nsB, OP_RMAJ, kB, kC)) != hipSuccess) return e;
-    if ((e = ns(h->nsX[par], OP_RMAJ, kA, 1.0f)) != hipSuccess) return e;
+    if ((e = ns(h->nsA[par], OP_KMAJ, 0.0f, 1.0f, true)) != hipSuccess) return e;
+    if ((e = ns(h->nsB, OP_KMAJ, kB, kC, true)) != hipSuccess) return e;
+    if ((e = ns(h->nsX[par], OP_RMAJ, kA, 1.0f, false)) != hipSuccess) return e;
   }
   return timed(h, "muon_update", 1, 0.0, wbytes * (8.0 + h->elt() + (h->prec == Prec::BF16 ? 2.0 : 0.0)), stream,
                [&] {

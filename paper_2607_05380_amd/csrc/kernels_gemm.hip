@@ -703,6 +703,42 @@ __device__ __forceinline__ void stage_flush_ns(const char* stage, OT* C, int64_t
   }
 }
 
+// The transpose of the staged block, for symmetric results: staged column c
+// (C column col0 + c) becomes C row col0 + c, whose elements row0 .. row0 + 31
+// each lane writes 4 at a time (Y read at the same transposed positions).
+template <typename OT, int NB>
+__device__ __forceinline__ void stage_flush_ns_mirror(const char* stage, OT* C, int64_t ldc, const OT* Y,
+                                                      int64_t ldy, float alpha, float beta, int row0, int col0,
+                                                      int M, int N, int lane) {
+  using S = Stage<float, NB>;
+  constexpr int CV = 32 / 4;  // 4-row vectors per staged column
+#pragma unroll
+  for (int it = 0; it < NB * 32 * CV / 64; ++it) {
+    const int v = it * 64 + lane;
+    const int c = v / CV, r = (v % CV) * 4;
+    const int orow = col0 + c, ocol = row0 + r;
+    if (orow >= M || ocol >= N) continue;
+    float o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = beta * *reinterpret_cast<const float*>(stage + (r + q) * S::RS + c * 4);
+    if (Y) {
+      const OT* yp = Y + (int64_t)orow * ldy + ocol;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = alpha * to_float(yp[q]) + o[q];
+    }
+    OT* cp = C + (int64_t)orow * ldc + ocol;
+    if constexpr (sizeof(OT) == 2) {
+      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)o[0]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)o[1]) << 16);
+      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)o[2]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)o[3]) << 16);
+      *glob(reinterpret_cast<u32x2*>(cp)) = u32x2{lo, hi};
+    } else {
+      *glob(reinterpret_cast<f32x4*>(cp)) = f32x4{o[0], o[1], o[2], o[3]};
+    }
+  }
+}
+
 // Weight-gradient rows with the optimizer fused: each staged vector holds the
 // gradients of 4 consecutive weights, which are updated in place (theta, both
 // moments, the bf16 shadow); the gradient itself is stored only on request.
@@ -943,6 +979,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
         wave_sync_lds();
         stage_flush_ns<T, NB>(stage, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.Y), d.ldy, a.ns_alpha,
                               a.ns_beta, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
+        if (a.ns_sym && t.m0 < t.n0)  // uniform: a tile above the diagonal also writes its mirror image
+          stage_flush_ns_mirror<T, NB>(stage, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.Y), d.ldy,
+                                       a.ns_alpha, a.ns_beta, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
         wave_sync_lds();
       }
     }

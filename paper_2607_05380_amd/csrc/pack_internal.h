@@ -84,8 +84,11 @@ struct GemmArgs {
   uint16_t* shadow;
   float beta1, beta2, eps, bc1, bc2_sqrt;
   int32_t keep_grad;
-  // EPI_NS only: C = ns_alpha * Y + ns_beta * (A B^T), stored in the GEMM precision
+  // EPI_NS only: C = ns_alpha * Y + ns_beta * (A B^T), stored in the GEMM precision;
+  // with ns_sym the launch holds only tiles on or above the diagonal of a
+  // symmetric C and every tile above it also stores its transpose
   float ns_alpha, ns_beta;
+  int32_t ns_sym;
 };
 
 // AdamW constants of one step.
