@@ -177,6 +177,7 @@ struct pack_handle {
   int head_rb = 0;  // rows per head-backward block
   uint64_t t = 0;
   TileSet tiles = TILES_SMALL;  // tile set of the bf16 GEMMs (fp32 GEMMs run small tiles only)
+  TileSet ns_tiles = TILES_SMALL;  // tile set of the Newton-Schulz GEMMs
   // side stream for ALU-bound work that overlaps memory-bound kernels of the
   // caller's stream, joined back through events (created by pack_bind)
   hipStream_t side = nullptr;
@@ -584,22 +585,48 @@ void muon_sizes(const pack_handle* h, It begin, It end, int64_t& xe, int64_t& ae
   }
 }
 
-// Small tiles on and above the diagonal of a symmetric S x S result (the
-// others are written as mirror images by the tiles above the diagonal).
+// Tiles on and above the diagonal of a symmetric S x S result (the others are
+// written as mirror images by the tiles above the diagonal).  Rows go in
+// blocks as in add_tiles; within its row block a diagonal block takes small
+// tiles on and above its own diagonal, and the columns right of it take the
+// tile set's large tiles (a remainder of at most 128 columns small ones).
 void add_tiles_sym(Plan& p, Launch& ln, int d, int S, int kdepth) {
-  for (int m0 = 0; m0 < S; m0 += kSmallTile)
-    for (int n0 = m0; n0 < S; n0 += kSmallTile) {
-      const int mb = std::min(kSmallTile, S - m0), nb = std::min(kSmallTile, S - n0);
-      p.tiles.push_back(Tile{d, m0, n0, kShapeSmall});
-      p.cost.push_back((int64_t)kdepth * mb * nb * (m0 < n0 ? 2 : 1));
+  auto push = [&](int m0, int n0, int shape) {
+    const int tm = shape == kShapeSmall ? kSmallTile : kBigTile;
+    const int tw = shape == kShapeBig ? kBigTile : kSmallTile;
+    const int mb = std::min(tm, S - m0), nb = std::min(tw, S - n0);
+    p.tiles.push_back(Tile{d, m0, n0, shape});
+    // a tile above the diagonal also stores its mirror image
+    p.cost.push_back((int64_t)kdepth * mb * nb * (m0 < n0 ? 2 : 1));
+  };
+  if (p.tile_set == TILES_SMALL) {
+    for (int m0 = 0; m0 < S; m0 += kSmallTile)
+      for (int n0 = m0; n0 < S; n0 += kSmallTile) push(m0, n0, kShapeSmall);
+  } else {
+    const bool big = p.tile_set == TILES_BIG;
+    const int large = big ? kShapeBig : kShapeTall, tn = big ? kBigTile : kSmallTile;
+    const int r = S % kBigTile;
+    const int Mb = r == 0 ? S : (r > kSmallTile ? S - r + kBigTile : S - r);
+    for (int m0 = 0; m0 < Mb; m0 += kBigTile) {
+      const int e = std::min(m0 + kBigTile, S);  // end of the diagonal block
+      for (int i0 = m0; i0 < e; i0 += kSmallTile)
+        for (int n0 = i0; n0 < e; n0 += kSmallTile) push(i0, n0, kShapeSmall);
+      const int rc = (S - e) % tn;
+      const int Nb = big ? (rc == 0 || rc > kSmallTile ? S : S - rc) : S;
+      for (int n0 = e; n0 < Nb; n0 += tn) push(m0, n0, large);
+      for (int i0 = m0; i0 < e; i0 += kSmallTile)
+        for (int n0 = Nb; n0 < S; n0 += kSmallTile) push(i0, n0, kShapeSmall);
     }
+    for (int m0 = Mb; m0 < S; m0 += kSmallTile)
+      for (int n0 = m0; n0 < S; n0 += kSmallTile) push(m0, n0, kShapeSmall);
+  }
   ln.ntiles = (int)p.tiles.size() - ln.tile0;
 }
 
 void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&group)[kGroups], Plan& p) {
   const size_t es = h->elt();
   const TileSet saved = p.tile_set;
-  p.tile_set = TILES_SMALL;  // the Newton-Schulz GEMMs run small tiles only
+  p.tile_set = h->ns_tiles;
   for (int par = 0; par < 2; ++par) {
     p.nsA[par] = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
     p.nsX[par] = Launch{};
@@ -1125,7 +1152,7 @@ hipError_t muon_step(pack_handle* h, const GemmArgs& base, hipStream_t stream) {
     GemmArgs g = base;
     g.tiles += ln.tile0;
     g.ntiles = ln.ntiles;
-    g.tile_set = TILES_SMALL;
+    g.tile_set = h->ns_tiles;
     g.ns_alpha = alpha;
     g.ns_beta = beta;
     g.ns_sym = sym ? 1 : 0;
@@ -1179,6 +1206,14 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
     h->tiles = v == "big" ? TILES_BIG : (v == "tall" ? TILES_TALL : TILES_SMALL);
   }
   if (h->prec == Prec::FP32) h->tiles = TILES_SMALL;
+  // Newton-Schulz GEMMs: small tiles measured 3.79 ms per Muon step on the
+  // 64-member regression workload, tall 4.03, big 5.53; TABPACK_NS_TILES overrides
+  h->ns_tiles = TILES_SMALL;
+  if (const char* e = getenv("TABPACK_NS_TILES")) {
+    const std::string v(e);
+    h->ns_tiles = v == "big" ? TILES_BIG : (v == "tall" ? TILES_TALL : TILES_SMALL);
+  }
+  if (h->prec == Prec::FP32) h->ns_tiles = TILES_SMALL;
   h->muon = cfg->optimizer == PACK_OPT_MUON;
   h->emb = cfg->emb_lo > 0;
   h->ns_steps = cfg->ns_steps ? cfg->ns_steps : 5;

@@ -1298,10 +1298,9 @@ hipError_t launch_prec(OpKind ak, OpKind bk, EpiKind e, const GemmArgs& args, hi
     if (args.tile_set != TILES_SMALL || args.theta) return hipErrorInvalidValue;
     return launch_small<T, OP_KMAJ, OP_RMAJ, EPI_DW>(args, s);
   }
-  if (e == EPI_NS) {  // Newton-Schulz products: small tiles only
-    if (args.tile_set != TILES_SMALL) return hipErrorInvalidValue;
-    if (ak == OP_KMAJ && bk == OP_KMAJ) return launch_small<T, OP_KMAJ, OP_KMAJ, EPI_NS>(args, s);
-    if (ak == OP_KMAJ && bk == OP_RMAJ) return launch_small<T, OP_KMAJ, OP_RMAJ, EPI_NS>(args, s);
+  if (e == EPI_NS) {  // Newton-Schulz products
+    if (ak == OP_KMAJ && bk == OP_KMAJ) return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_NS>(args, s);
+    if (ak == OP_KMAJ && bk == OP_RMAJ) return launch_t<T, OP_KMAJ, OP_RMAJ, EPI_NS>(args, s);
   }
   return hipErrorInvalidValue;
 }

@@ -36,28 +36,57 @@ __device__ __forceinline__ float to_t<float>(float x) {
 __device__ __forceinline__ float from_t(__bf16 x) { return (float)x; }
 __device__ __forceinline__ float from_t(float x) { return x; }
 
-// Momentum update and the squared norm of U per tile.  Thread t owns column
-// c0 + t % 64 of rows r0 + t / 64 + 4 i (i < 16): every access is a run of 64
-// consecutive floats.  part[tile] = sum of u^2 over the tile (fixed order).
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+// 4 consecutive elements of X (8 bytes in bf16, 16 in fp32)
+__device__ __forceinline__ void store4(__bf16* p, f32x4v x) {
+  const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[0]) |
+                      ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[1]) << 16);
+  const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[2]) |
+                      ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x[3]) << 16);
+  *reinterpret_cast<uint2*>(p) = uint2{lo, hi};
+}
+__device__ __forceinline__ void store4(float* p, f32x4v x) { *reinterpret_cast<f32x4v*>(p) = x; }
+__device__ __forceinline__ f32x4v load4(const __bf16* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  return f32x4v{__builtin_bit_cast(float, u.x << 16), __builtin_bit_cast(float, u.x & 0xffff0000u),
+                __builtin_bit_cast(float, u.y << 16), __builtin_bit_cast(float, u.y & 0xffff0000u)};
+}
+__device__ __forceinline__ f32x4v load4(const float* p) { return *reinterpret_cast<const f32x4v*>(p); }
+
+typedef f32x4v f32x4;
+
+// Thread t of a tile owns the 4 columns c0 + 4 (t % 16) .. + 3 of rows
+// r0 + t / 16 + 16 i (i < 4): every access moves 16 bytes of a row (the padded
+// column counts are multiples of 8, the weights start on 256-element
+// boundaries).
+constexpr int kTPR = kMT / 4;         // threads per tile row
+constexpr int kRPP = 256 / kTPR;      // rows per pass
+
+// Momentum update and the squared norm of U per tile: part[tile] = sum of u^2
+// over the tile, in a fixed order.
 __global__ __launch_bounds__(256) void muon_prep_kernel(const MuonMat* mats, const MuonTile* tiles,
                                                         const float* grad, float* buf, float mu, int nesterov,
                                                         double* part) {
   __shared__ double sh[4];
   const MuonTile t = tiles[blockIdx.x];
   const MuonMat m = mats[t.mat];
-  const int c = t.c0 + (threadIdx.x & 63);
+  const int c = t.c0 + 4 * (threadIdx.x % kTPR);
   double s = 0.0;
   if (c < m.Cp) {
-#pragma unroll 4
-    for (int i = 0; i < kMT / 4; ++i) {
-      const int r = t.r0 + (threadIdx.x >> 6) + 4 * i;
+#pragma unroll
+    for (int i = 0; i < kMT / kRPP; ++i) {
+      const int r = t.r0 + threadIdx.x / kTPR + kRPP * i;
       if (r >= m.R) break;
       const int64_t e = m.woff + (int64_t)r * m.Cp + c;
-      const float g = grad[e];
-      const float b = mu * buf[e] + g;
-      buf[e] = b;
-      const float u = nesterov ? g + mu * b : b;
-      s += (double)u * (double)u;
+      const f32x4 g = *reinterpret_cast<const f32x4*>(grad + e);
+      f32x4 b = *reinterpret_cast<const f32x4*>(buf + e);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        b[q] = mu * b[q] + g[q];
+        const float u = nesterov ? g[q] + mu * b[q] : b[q];
+        s += (double)u * (double)u;
+      }
+      *reinterpret_cast<f32x4*>(buf + e) = b;
     }
   }
   s = wave_sum(s);
@@ -66,18 +95,21 @@ __global__ __launch_bounds__(256) void muon_prep_kernel(const MuonMat* mats, con
   if (threadIdx.x == 0) part[blockIdx.x] = (sh[0] + sh[1]) + (sh[2] + sh[3]);
 }
 
-// inv[k] = 1 / (||U_k|| + 1e-7) from the tile partials of matrix k, in tile order.
-__global__ void muon_norm_kernel(const int32_t* tile0, int nmats, const double* part, float* inv) {
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= nmats) return;
+// inv[k] = 1 / (||U_k|| + 1e-7): one wave per matrix sums its tile partials
+// lane-strided, then in a fixed shuffle tree.
+__global__ __launch_bounds__(256) void muon_norm_kernel(const int32_t* tile0, int nmats, const double* part,
+                                                        float* inv) {
+  const int k = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (k >= nmats) return;  // wave-uniform
   double s = 0.0;
-  for (int i = tile0[k]; i < tile0[k + 1]; ++i) s += part[i];
-  inv[k] = (float)(1.0 / (sqrt(s) + 1e-7));
+  for (int i = tile0[k] + lane; i < tile0[k + 1]; i += 64) s += part[i];
+  s = wave_sum(s);
+  if (lane == 0) inv[k] = (float)(1.0 / (sqrt(s) + 1e-7));
 }
 
 // X0 = U / (||U|| + 1e-7) in the GEMM precision, [S, L] row-major: U itself
 // (S = rows), or U^T for tall weights, transposed through LDS so that reads
-// and writes both run along rows.
+// and writes both move 4 elements of a row.
 template <typename T>
 __global__ __launch_bounds__(256) void muon_convert_kernel(const MuonMat* mats, const MuonTile* tiles,
                                                            const float* grad, const float* buf, float mu,
@@ -86,28 +118,34 @@ __global__ __launch_bounds__(256) void muon_convert_kernel(const MuonMat* mats, 
   const MuonTile t = tiles[blockIdx.x];
   const MuonMat m = mats[t.mat];
   const float sc = inv[t.mat];
-  const int cl = threadIdx.x & 63;
-#pragma unroll 4
-  for (int i = 0; i < kMT / 4; ++i) {
-    const int rl = (threadIdx.x >> 6) + 4 * i;
+  const int cl = 4 * (threadIdx.x % kTPR);
+#pragma unroll
+  for (int i = 0; i < kMT / kRPP; ++i) {
+    const int rl = threadIdx.x / kTPR + kRPP * i;
     const int r = t.r0 + rl, c = t.c0 + cl;
-    float x = 0.0f;
+    f32x4 x = {0.0f, 0.0f, 0.0f, 0.0f};
     if (r < m.R && c < m.Cp) {
       const int64_t e = m.woff + (int64_t)r * m.Cp + c;
-      const float g = grad[e], b = buf[e];
-      x = (nesterov ? g + mu * b : b) * sc;
-      if (!m.tall) X[m.xoff + (int64_t)r * m.Cp + c] = to_t<T>(x);
+      const f32x4 g = *reinterpret_cast<const f32x4*>(grad + e);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(buf + e);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[q] = (nesterov ? g[q] + mu * b[q] : b[q]) * sc;
+      if (!m.tall) store4(X + m.xoff + (int64_t)r * m.Cp + c, x);
     }
-    tr[rl][cl] = x;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tr[rl][cl + q] = x[q];
   }
   if (!m.tall) return;  // uniform
   __syncthreads();
-  // X[c, r] = U[r, c]: thread owns row c0 + 4 i + t / 64 of X, column r0 + t % 64
-#pragma unroll 4
-  for (int i = 0; i < kMT / 4; ++i) {
-    const int cl2 = (threadIdx.x >> 6) + 4 * i, rl2 = threadIdx.x & 63;
+  // X[c, r .. r + 3] = U[r .. r + 3, c]
+#pragma unroll
+  for (int i = 0; i < kMT / kRPP; ++i) {
+    const int cl2 = threadIdx.x / kTPR + kRPP * i, rl2 = 4 * (threadIdx.x % kTPR);
     const int r = t.r0 + rl2, c = t.c0 + cl2;
-    if (r < m.R && c < m.Cp) X[m.xoff + (int64_t)c * m.R + r] = to_t<T>(tr[rl2][cl2]);
+    if (r < m.R && c < m.Cp) {
+      const f32x4 x = {tr[rl2][cl2], tr[rl2 + 1][cl2], tr[rl2 + 2][cl2], tr[rl2 + 3][cl2]};
+      store4(X + m.xoff + (int64_t)c * m.R + r, x);
+    }
   }
 }
 
@@ -120,30 +158,41 @@ __global__ __launch_bounds__(256) void muon_update_kernel(const MuonMat* mats, c
   const MuonTile t = tiles[blockIdx.x];
   const MuonMat m = mats[t.mat];
   if (m.tall) {
-#pragma unroll 4
-    for (int i = 0; i < kMT / 4; ++i) {
-      const int cl2 = (threadIdx.x >> 6) + 4 * i, rl2 = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < kMT / kRPP; ++i) {
+      const int cl2 = threadIdx.x / kTPR + kRPP * i, rl2 = 4 * (threadIdx.x % kTPR);
       const int r = t.r0 + rl2, c = t.c0 + cl2;
-      tr[rl2][cl2] = (r < m.R && c < m.Cp) ? from_t(X[m.xoff + (int64_t)c * m.R + r]) : 0.0f;
+      f32x4 o = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (r < m.R && c < m.Cp) o = load4(X + m.xoff + (int64_t)c * m.R + r);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) tr[rl2 + q][cl2] = o[q];
     }
     __syncthreads();
   }
   const float decay = m.decay, step = m.step;
-  const int cl = threadIdx.x & 63;
-#pragma unroll 4
-  for (int i = 0; i < kMT / 4; ++i) {
-    const int rl = (threadIdx.x >> 6) + 4 * i;
+  const int cl = 4 * (threadIdx.x % kTPR);
+#pragma unroll
+  for (int i = 0; i < kMT / kRPP; ++i) {
+    const int rl = threadIdx.x / kTPR + kRPP * i;
     const int r = t.r0 + rl, c = t.c0 + cl;
     if (r >= m.R || c >= m.Cp) continue;
     const int64_t e = m.woff + (int64_t)r * m.Cp + c;
-    const float o = m.tall ? tr[rl][cl] : from_t(X[m.xoff + (int64_t)r * m.Cp + c]);
-    float w;
-    {
+    const f32x4 o = m.tall ? f32x4{tr[rl][cl], tr[rl][cl + 1], tr[rl][cl + 2], tr[rl][cl + 3]}
+                           : load4(X + m.xoff + (int64_t)r * m.Cp + c);
+    f32x4 w = *reinterpret_cast<const f32x4*>(theta + e);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
 #pragma clang fp contract(off)
-      w = theta[e] * decay - step * o;
+      w[q] = w[q] * decay - step * o[q];
     }
-    theta[e] = w;
-    if (shadow) shadow[e] = __builtin_bit_cast(uint16_t, (__bf16)w);
+    *reinterpret_cast<f32x4*>(theta + e) = w;
+    if (shadow) {
+      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)w[0]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)w[1]) << 16);
+      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)w[2]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)w[3]) << 16);
+      *reinterpret_cast<uint2*>(shadow + e) = uint2{lo, hi};
+    }
   }
 }
 
@@ -158,7 +207,7 @@ hipError_t launch_muon_prep(const MuonMat* mats, const MuonTile* tiles, int ntil
 
 hipError_t launch_muon_norm(const int32_t* tile0, int nmats, const double* part, float* inv, hipStream_t s) {
   if (nmats <= 0) return hipSuccess;
-  hipLaunchKernelGGL(muon_norm_kernel, dim3((nmats + 63) / 64), dim3(64), 0, s, tile0, nmats, part, inv);
+  hipLaunchKernelGGL(muon_norm_kernel, dim3((nmats + 3) / 4), dim3(256), 0, s, tile0, nmats, part, inv);
   return hipGetLastError();
 }
 
