@@ -8,6 +8,11 @@
       `--pmc WRITE_SIZE` runs of `bench.py --copy-calibration`: each counter (KiB per
       dispatch) is scaled by what it reads for the 256 MiB device-to-device copies of
       that run; writes OUT_PREFIX.json (read by bench.py) and OUT_PREFIX.md
+  python -m paper_2607_05380_amd.profiles_summary mfma PMC_DIR BENCH_LOG WORKLOAD OUT.md --command "..."
+      executed MFMA work per launch of every GEMM kernel from a `--pmc
+      SQ_INSTS_VALU_MFMA_MOPS_BF16` (or _F32) run of `bench.py --profile-steps N`
+      (the counter counts in units of 512 flops), against the algorithmic flops
+      per launch that the same run's JSON line reports
 
 Kernel names are mapped to the names the library's own profiler uses.
 """
@@ -24,10 +29,11 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 COPY_BYTES = 256 << 20
 OPS = ["kmaj", "rmaj"]
-EPIS = ["fwd", "fwd_eval", "dx", "dw"]
+EPIS = ["fwd", "fwd_eval", "dx", "dw", "ns"]
 SIMPLE = ["dropout_words", "head_grad_reduce", "head_fwd", "head_bwd", "loss_reduce", "bias_from_partials",
           "gather", "adamw", "to_shadow", "eval_score", "dropout_mask", "select_partial", "select_pick",
-          "select_update", "select_init", "select_final", "ensemble_mean"]
+          "select_update", "select_init", "select_final", "ensemble_mean", "muon_prep", "muon_norm",
+          "muon_convert", "muon_update", "embed_fwd", "embed_bwd"]
 
 
 def source_digest():
@@ -40,32 +46,33 @@ def source_digest():
     return h.hexdigest()
 
 
-PAIR = {0: ("kmaj", "kmaj"), 1: ("kmaj", "kmaj"), 2: ("kmaj", "rmaj"), 3: ("rmaj", "rmaj")}  # by epilogue
-
-
 def short_name(kernel):
-    """Library profiler name of a rocprofv3 kernel name (mangled, or demangled
-    with the template arguments partly lost), or None for other kernels."""
-    if "gemm_kernel_bwd" in kernel:
-        return "gemm_bf16_bwd"
-    if "gemm_kernel_tall" in kernel:
-        m = re.search(r"gemm_kernel_tall(?:ILi(\d)ELi(\d)ELi|<\d, \d, )(\d)", kernel)
-        if not m:
-            return None
-        epi = int(m.group(3))
-        a, b = PAIR[epi]
-        return f"gemm_bf16_{a}_{b}_{EPIS[epi]}"
+    """Library profiler name of a rocprofv3 kernel name (mangled, or demangled),
+    or None for other kernels.  GEMM kernels are named by their template
+    arguments: element type, operand kinds (0 depth-contiguous, 1 row-major) and
+    epilogue."""
     if "gemm_kernel" in kernel:
-        m = re.search(r"gemm_kernel(?:_small)?I(DF16b|f)Li(\d)ELi(\d)ELi(\d)E", kernel)
+        m = re.search(r"gemm_kernel(?:_small|_tall)?I(DF16b|f)?(?:Li(\d)E)(?:Li(\d)E)(?:Li(\d)E)", kernel)
         if m:
-            t, epi = ("bf16" if m.group(1) == "DF16b" else "f32"), int(m.group(4))
+            t = "f32" if m.group(1) == "f" else "bf16"
+            ak, bk, epi = int(m.group(2)), int(m.group(3)), int(m.group(4))
         else:
-            m = re.search(r"gemm_kernel(?:_small)?<(.*), (\d)>", kernel)
-            if not m:
-                return None
-            t, epi = ("f32" if "float" in m.group(1) else "bf16"), int(m.group(2))
-        a, b = PAIR[epi]
-        return f"gemm_{t}_{a}_{b}_{EPIS[epi]}"
+            m = re.search(r"gemm_kernel(?:_small|_tall)?<(?:([^,<>]*), )?(\d), (\d), (\d)>", kernel)
+            if m:
+                t = "f32" if m.group(1) and "float" in m.group(1) else "bf16"
+                ak, bk, epi = int(m.group(2)), int(m.group(3)), int(m.group(4))
+            else:
+                # demangled with the leading arguments lost: the operand kind of A
+                # follows from the epilogue (the forward, data-gradient and Newton-
+                # Schulz GEMMs read A depth-contiguous, the weight gradient row-major)
+                m = re.search(r"gemm_kernel(?:_small|_tall)?<.*, (\d), (\d)>", kernel)
+                if not m:
+                    return None
+                t, bk, epi = "bf16", int(m.group(1)), int(m.group(2))
+                ak = 1 if epi == 3 else 0
+        if epi >= len(EPIS) or ak > 1 or bk > 1:
+            return None
+        return f"gemm_{t}_{OPS[ak]}_{OPS[bk]}_{EPIS[epi]}"
     for s in sorted(SIMPLE, key=len, reverse=True):
         if s + "_kernel" in kernel:
             return s
@@ -157,6 +164,44 @@ def traffic(args):
     print("\n".join(lines))
 
 
+def mfma(args):
+    counter = "SQ_INSTS_VALU_MFMA_MOPS_" + args.dtype.upper()
+    disp = per_dispatch(args.dir, counter)
+    with open(args.bench_log) as f:
+        lines = [ln for ln in f if ln.startswith("{")]
+    if not lines:
+        sys.exit(f"no JSON line in {args.bench_log}")
+    algo = {k["name"]: k["flops_per_launch"] for k in json.loads(lines[-1]).get("kernels", [])}
+    per = {}
+    for name, v in disp.values():
+        s = short_name(name)
+        if s and s.startswith("gemm_"):
+            per.setdefault(s, []).append(v * 512)
+    if not per:
+        sys.exit(f"no GEMM dispatches with {counter} under {args.dir}")
+    out = ["# Executed MFMA work against algorithmic flops, " + args.workload, "", "Command:", "", "```",
+           args.command, "```", "",
+           f"`{counter}` x 512 per dispatch (flops the matrix cores executed, padding included), averaged "
+           "over the run's dispatches of each kernel, against the algorithmic flops per launch (true member "
+           "widths, no padding) that the same run's library events report.  The ratio is the work added by "
+           "rounding member widths to tiles and by whole tiles on the diagonal of symmetric products.", "",
+           "| kernel | dispatches | executed GFLOP/launch | algorithmic GFLOP/launch | executed / algorithmic |",
+           "|---|---|---|---|---|"]
+    tot_e = tot_a = 0.0
+    for k, vals in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+        e = statistics.mean(vals)
+        a = algo.get(k)
+        if a:
+            tot_e += e * len(vals)
+            tot_a += a * len(vals)
+        out.append(f"| {k} | {len(vals)} | {e / 1e9:.2f} | {a / 1e9 if a else float('nan'):.2f} | "
+                   f"{e / a if a else float('nan'):.3f} |")
+    out += ["", f"All GEMM launches: executed / algorithmic = {tot_e / tot_a:.3f}."]
+    with open(args.out, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -170,8 +215,15 @@ def main():
     b.add_argument("workload")
     b.add_argument("out_prefix")
     b.add_argument("--command", default="")
+    c = sub.add_parser("mfma")
+    c.add_argument("dir")
+    c.add_argument("bench_log")
+    c.add_argument("workload")
+    c.add_argument("out")
+    c.add_argument("--dtype", default="bf16")
+    c.add_argument("--command", default="")
     args = ap.parse_args()
-    stats(args) if args.cmd == "stats" else traffic(args)
+    {"stats": stats, "traffic": traffic, "mfma": mfma}[args.cmd](args)
 
 
 if __name__ == "__main__":
