@@ -453,6 +453,7 @@ struct Plan {
 // tile).  Tall set: 256 x 128 tiles, rows as in the big set, the last column
 // tile partly filled.  Small set: 128 x 128 tiles only.
 void add_tiles(Plan& p, Launch& ln, int d, int M, int N, int kdepth) {
+  const size_t first = p.tiles.size();
   auto big_end = [&](int E) {
     const int r = E % kBigTile;
     return r == 0 ? E : (r > kSmallTile ? E - r + kBigTile : E - r);
@@ -475,6 +476,22 @@ void add_tiles(Plan& p, Launch& ln, int d, int M, int N, int kdepth) {
     for (int n0 = Nb; n0 < N; n0 += kSmallTile) push(m0, n0, kShapeSmall);
   for (int m0 = Mb; m0 < M; m0 += kSmallTile)
     for (int n0 = 0; n0 < N; n0 += kSmallTile) push(m0, n0, kShapeSmall);
+  // Wider than tall (the embedded first layer's dE = dZ_1 W_1 and dW_1 =
+  // dZ_1^T E, thousands of columns): tiles in column-strip order, so the row
+  // tiles sharing a strip of the wide operand run together and read it once
+  // while the narrow operand stays in L2 (row order re-reads every strip once
+  // per row tile).
+  if (N > M) {
+    std::vector<std::pair<Tile, int64_t>> v;
+    for (size_t i = first; i < p.tiles.size(); ++i) v.push_back({p.tiles[i], p.cost[i]});
+    std::stable_sort(v.begin(), v.end(), [](const std::pair<Tile, int64_t>& x, const std::pair<Tile, int64_t>& y) {
+      return x.first.n0 != y.first.n0 ? x.first.n0 < y.first.n0 : x.first.m0 < y.first.m0;
+    });
+    for (size_t i = 0; i < v.size(); ++i) {
+      p.tiles[first + i] = v[i].first;
+      p.cost[first + i] = v[i].second;
+    }
+  }
   ln.ntiles = (int)p.tiles.size() - ln.tile0;
 }
 
@@ -548,6 +565,13 @@ void split_members(pack_handle* h) {
     h->group[g].push_back(ck.second);
   }
   for (auto& v : h->group) std::sort(v.begin(), v.end());
+}
+
+// The largest first-layer width p_in among the given members.
+int max_pin(const pack_handle* h, const std::vector<int>& ids) {
+  int m = 0;
+  for (int k : ids) m = std::max(m, h->mem[k].p_in);
+  return m;
 }
 
 // Rows per head-backward block: up to 256, dividing Bp.
@@ -1427,7 +1451,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       for (int k : h->group[hf]) eb += (double)c.B * h->mem[k].p_in;
       HIP_TRY(timed(h, "embed_fwd", 1, 0.0, eb * h->elt() + (double)gk * c.B * c.d_in * 4.0, s, [&] {
         return launch_embed_fwd(h->prec, X, c.d_in, idx, c.B, 0, c.B, h->Bp, h->b.d_mem,
-                                h->b.d_members + h->member0[hf], gk, 0, h->b.theta, h->b.H0, s);
+                                h->b.d_members + h->member0[hf], gk, max_pin(h, h->group[hf]), h->b.theta,
+                                h->b.H0, s);
       }));
     } else {
       HIP_TRY(timed(h, "gather", 1, 0.0, (double)gk * c.B * c.d_in * (4.0 + h->elt()), s, [&] {
@@ -1489,8 +1514,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                       [&] { return launch_gemm(h->prec, OP_KMAJ, OP_RMAJ, EPI_DW, ae, s); }));
         const int gk = h->member0[hf + 1] - h->member0[hf];
         HIP_TRY(timed(h, "embed_bwd", 1, 0.0, h->de[hf].bytes, s, [&] {
-          return launch_embed_bwd(X, c.d_in, idx, c.B, h->b.d_mem, h->b.d_members + h->member0[hf], gk, h->b.theta,
-                                  h->b.dE, h->b.grad, s);
+          return launch_embed_bwd(h->prec, X, c.d_in, idx, c.B, h->b.d_mem, h->b.d_members + h->member0[hf], gk,
+                                  max_pin(h, h->group[hf]), h->b.theta, h->b.dE, h->b.grad, s);
         }));
       }
       GemmArgs al = for_launch(a, h->dw[hf][l - 1]);
@@ -1541,7 +1566,7 @@ hipError_t eval_forward(pack_handle* h, GemmArgs a, const float* X, int64_t r0, 
   hipError_t e;
   if (h->emb)
     e = launch_embed_fwd(h->prec, X, c.d_in, nullptr, c.B, r0, a.rows_valid, h->Bp, h->b.d_mem, h->b.d_active,
-                         (int)h->active_ids.size(), 0, h->b.theta, h->b.H0, stream);
+                         (int)h->active_ids.size(), max_pin(h, h->active_ids), h->b.theta, h->b.H0, stream);
   else
     e = launch_gather(h->prec, X, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, nullptr,
                       stream);

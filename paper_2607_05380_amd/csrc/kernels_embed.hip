@@ -12,6 +12,8 @@
 namespace tabpack {
 namespace {
 
+constexpr int kEmbRows = 64;  // rows per forward workgroup (the padded batch is a multiple)
+
 template <typename T>
 __device__ __forceinline__ T to_gemm(float x);
 template <>
@@ -23,91 +25,167 @@ __device__ __forceinline__ float to_gemm<float>(float x) {
   return x;
 }
 
-// One workgroup per (row, member); threads stride over the row's columns.
-template <typename T>
-__global__ __launch_bounds__(256) void embed_fwd_kernel(const float* X, int d_in, const int32_t* idx, int B,
-                                                        int64_t row_base, int rows_valid, const MemberDev* mem,
-                                                        const int32_t* members, const float* theta, T* E) {
-  const int r = blockIdx.x;
-  const int k = members[blockIdx.y];
-  const MemberDev md = mem[k];
-  T* out = E + md.e_act + (int64_t)r * md.p_in;
-  const int ncol = d_in * md.d_emb;
-  const bool valid = r < rows_valid;
-  const float* xr = nullptr;
-  if (valid) xr = X + (idx ? (int64_t)idx[(int64_t)k * B + r] : row_base + r) * d_in;
-  for (int col = threadIdx.x; col < md.p_in; col += 256) {
-    float v = 0.0f;
-    if (valid && col < ncol) {
-      const int i = col / md.d_emb, j = col - i * md.d_emb;
-      const float x = xr[i];
-      const float a = theta[md.e_a + col], be = theta[md.e_be + col];
-      if (j == 0) {
-        v = a * x + be;
-      } else {
-        const int64_t wi = (int64_t)i * (md.d_emb - 1) + j - 1;
-        v = a * cosf(theta[md.e_w + wi] * x + theta[md.e_b + wi]) + be;
-      }
-    }
-    out[col] = to_gemm<T>(v);
+// cos and sin of a phase phi (radians) for the bf16 packs: the hardware's
+// v_cos_f32 / v_sin_f32 take revolutions, so t = phi / (2 pi) is reduced to
+// [-1/2, 1/2] by subtracting the nearest integer first.  The error (about 1e-6
+// absolute for phases up to a few hundred radians, most of it the rounding of
+// t) is far below the bf16 rounding of the embedded values.  fp32 packs use
+// cosf / sincosf.
+__device__ __forceinline__ float revolutions(float phi) {
+  const float t = phi * 0.15915494309189535f;
+  return t - rintf(t);
+}
+template <bool FAST>
+__device__ __forceinline__ float cos_of(float phi) {
+  if constexpr (FAST)
+    return __builtin_amdgcn_cosf(revolutions(phi));
+  else
+    return cosf(phi);
+}
+template <bool FAST>
+__device__ __forceinline__ void sincos_of(float phi, float* sn, float* cs) {
+  if constexpr (FAST) {
+    const float t = revolutions(phi);
+    *sn = __builtin_amdgcn_sinf(t);
+    *cs = __builtin_amdgcn_cosf(t);
+  } else {
+    sincosf(phi, sn, cs);
   }
 }
 
-// One workgroup per (feature i, member): thread t takes embedding column
-// j = t % 32 (j < d_emb) over the rows r = t / 32 + 8 m, accumulating the four
-// gradient sums in fp32; the 8 row groups are then added in a fixed order.
+// Parameters of embedding column col (< d_in d_emb) of a member: feature i,
+// position j, alpha, beta and (j >= 1) w, b.
+struct EmbCol {
+  int i, j;
+  float a, be, w, b;
+};
+__device__ __forceinline__ EmbCol emb_col(const MemberDev& md, const float* theta, int col) {
+  EmbCol e;
+  e.i = col / md.d_emb;
+  e.j = col - e.i * md.d_emb;
+  e.a = theta[md.e_a + col];
+  e.be = theta[md.e_be + col];
+  e.w = e.b = 0.0f;
+  if (e.j > 0) {
+    const int64_t wi = (int64_t)e.i * (md.d_emb - 1) + e.j - 1;
+    e.w = theta[md.e_w + wi];
+    e.b = theta[md.e_b + wi];
+  }
+  return e;
+}
+
+// The features a workgroup's 256 columns starting at c0 read, [i0, i0 + nf):
+// at most 255 / d_emb + 2 of them (d_emb >= 2).
+constexpr int kEmbFeat = 130;
+struct FeatRange {
+  int i0, nf;
+};
+__device__ __forceinline__ FeatRange feat_range(int c0, int d_emb, int d_in) {
+  const int i0 = c0 / d_emb;
+  return FeatRange{i0, min(d_in - 1, (c0 + 255) / d_emb) - i0 + 1};
+}
+
+// xs[r][f] = x of feature i0 + f in row r of the chunk (zero for rows whose
+// xrow is negative).
+__device__ __forceinline__ void stage_features(const float* X, const int64_t* xrow, int nrows, FeatRange fr,
+                                               float (*xs)[kEmbFeat]) {
+  for (int e = threadIdx.x; e < nrows * fr.nf; e += 256) {
+    const int r = e / fr.nf, f = e - r * fr.nf;
+    const int64_t xo = xrow[r];
+    xs[r][f] = xo >= 0 ? X[xo + fr.i0 + f] : 0.0f;
+  }
+}
+
+// One workgroup per (256 columns, member, kEmbRows rows): the chunk's feature
+// values are staged in LDS, each thread keeps its column's parameters in
+// registers and writes the column down the rows (a row's 256 columns are one
+// contiguous store per workgroup).
+template <typename T, bool FAST>
+__global__ __launch_bounds__(256) void embed_fwd_kernel(const float* X, int d_in, const int32_t* idx, int B,
+                                                        int64_t row_base, int rows_valid, const MemberDev* mem,
+                                                        const int32_t* members, const float* theta, T* E) {
+  __shared__ int64_t xrow[kEmbRows];
+  __shared__ float xs[kEmbRows][kEmbFeat];
+  const int k = members[blockIdx.y];
+  const MemberDev md = mem[k];
+  const int c0 = blockIdx.x * 256;
+  if (c0 >= md.p_in) return;  // uniform: past this member's columns
+  const int r0 = blockIdx.z * kEmbRows;
+  if (threadIdx.x < kEmbRows) {
+    const int r = r0 + threadIdx.x;
+    xrow[threadIdx.x] = r < rows_valid ? (idx ? (int64_t)idx[(int64_t)k * B + r] : row_base + r) * d_in : -1;
+  }
+  __syncthreads();
+  const FeatRange fr = feat_range(min(c0, d_in * md.d_emb - 1), md.d_emb, d_in);
+  stage_features(X, xrow, kEmbRows, fr, xs);
+  __syncthreads();
+  const int col = c0 + threadIdx.x;
+  if (col >= md.p_in) return;
+  const bool on = col < d_in * md.d_emb;  // else a padding column: zeros
+  EmbCol e{0, 0, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (on) e = emb_col(md, theta, col);
+  const int f = on ? e.i - fr.i0 : 0;
+  T* out = E + md.e_act + (int64_t)r0 * md.p_in + col;
+#pragma unroll 8
+  for (int rr = 0; rr < kEmbRows; ++rr) {
+    float v = 0.0f;
+    if (on && xrow[rr] >= 0) {
+      const float x = xs[rr][f];
+      v = e.j == 0 ? e.a * x + e.be : e.a * cos_of<FAST>(e.w * x + e.b) + e.be;
+    }
+    out[(int64_t)rr * md.p_in] = to_gemm<T>(v);
+  }
+}
+
+// One workgroup per (256 columns, member): each thread sums its column's four
+// gradient terms over the batch rows in row order (fp32), reading dE one row of
+// 256 columns at a time; the rows' data indices go through LDS 256 at a time.
+// (Staging the feature values in LDS as the forward does, 64 rows per chunk,
+// measured twice as slow: three barriers per chunk expose every load.)
+template <bool FAST>
 __global__ __launch_bounds__(256) void embed_bwd_kernel(const float* X, int d_in, const int32_t* idx, int B,
                                                         const MemberDev* mem, const int32_t* members,
                                                         const float* theta, const float* dE, float* grad) {
-  __shared__ float red[4][8][32];
-  const int i = blockIdx.x;
+  __shared__ int64_t xrow[256];
   const int k = members[blockIdx.y];
   const MemberDev md = mem[k];
-  const int j = threadIdx.x & 31, rg = threadIdx.x >> 5;
-  const bool on = j < md.d_emb;
-  const int col = i * md.d_emb + j;
+  if ((int)blockIdx.x * 256 >= md.p_in) return;  // uniform
+  const int col = blockIdx.x * 256 + threadIdx.x;
+  const bool on = col < d_in * md.d_emb;
+  EmbCol e{0, 0, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (on) e = emb_col(md, theta, col);
+  const float* de = dE + md.e_act + (on ? col : 0);
   float ga = 0.0f, gbe = 0.0f, gw = 0.0f, gb = 0.0f;
-  if (on) {
-    const float* de = dE + md.e_act + col;
-    float w = 0.0f, bb = 0.0f, alpha = theta[md.e_a + col];
-    if (j > 0) {
-      w = theta[md.e_w + (int64_t)i * (md.d_emb - 1) + j - 1];
-      bb = theta[md.e_b + (int64_t)i * (md.d_emb - 1) + j - 1];
-    }
-    for (int r = rg; r < B; r += 8) {
-      const float x = X[(int64_t)idx[(int64_t)k * B + r] * d_in + i];
-      const float g = de[(int64_t)r * md.p_in];
+  for (int rc = 0; rc < B; rc += 256) {
+    const int n = min(256, B - rc);
+    __syncthreads();  // the previous chunk's indices are no longer read
+    if ((int)threadIdx.x < n) xrow[threadIdx.x] = (int64_t)idx[(int64_t)k * B + rc + threadIdx.x] * d_in;
+    __syncthreads();
+    if (!on) continue;
+#pragma unroll 8
+    for (int rr = 0; rr < n; ++rr) {
+      const float x = X[xrow[rr] + e.i];
+      const float g = de[(int64_t)(rc + rr) * md.p_in];
       gbe += g;
-      if (j == 0) {
+      if (e.j == 0) {
         ga += g * x;
       } else {
         float sn, cs;
-        sincosf(w * x + bb, &sn, &cs);
+        sincos_of<FAST>(e.w * x + e.b, &sn, &cs);
         ga += g * cs;
-        const float t = -g * alpha * sn;
+        const float t = -g * e.a * sn;
         gb += t;
         gw += t * x;
       }
     }
   }
-  red[0][rg][j] = ga;
-  red[1][rg][j] = gbe;
-  red[2][rg][j] = gw;
-  red[3][rg][j] = gb;
-  __syncthreads();
-  if (rg == 0 && on) {
-    float s[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      s[q] = ((red[q][0][j] + red[q][1][j]) + (red[q][2][j] + red[q][3][j])) +
-             ((red[q][4][j] + red[q][5][j]) + (red[q][6][j] + red[q][7][j]));
-    grad[md.e_a + col] = s[0];
-    grad[md.e_be + col] = s[1];
-    if (j > 0) {
-      const int64_t wi = (int64_t)i * (md.d_emb - 1) + j - 1;
-      grad[md.e_w + wi] = s[2];
-      grad[md.e_b + wi] = s[3];
-    }
+  if (!on) return;
+  grad[md.e_a + col] = ga;
+  grad[md.e_be + col] = gbe;
+  if (e.j > 0) {
+    const int64_t wi = (int64_t)e.i * (md.d_emb - 1) + e.j - 1;
+    grad[md.e_w + wi] = gw;
+    grad[md.e_b + wi] = gb;
   }
 }
 
@@ -116,24 +194,29 @@ __global__ __launch_bounds__(256) void embed_bwd_kernel(const float* X, int d_in
 hipError_t launch_embed_fwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, int64_t row_base,
                             int rows_valid, int Bp, const MemberDev* mem, const int32_t* members, int nmembers,
                             int max_pin, const float* theta, void* E, hipStream_t s) {
-  (void)max_pin;
-  if (nmembers <= 0) return hipSuccess;
-  const dim3 grid(Bp, nmembers);
+  if (nmembers <= 0 || max_pin <= 0) return hipSuccess;
+  if (Bp % kEmbRows) return hipErrorInvalidValue;
+  const dim3 grid((max_pin + 255) / 256, nmembers, Bp / kEmbRows);
   if (prec == Prec::BF16)
-    hipLaunchKernelGGL((embed_fwd_kernel<__bf16>), grid, dim3(256), 0, s, X, d_in, idx, B, row_base, rows_valid, mem,
-                       members, theta, static_cast<__bf16*>(E));
+    hipLaunchKernelGGL((embed_fwd_kernel<__bf16, true>), grid, dim3(256), 0, s, X, d_in, idx, B, row_base,
+                       rows_valid, mem, members, theta, static_cast<__bf16*>(E));
   else
-    hipLaunchKernelGGL((embed_fwd_kernel<float>), grid, dim3(256), 0, s, X, d_in, idx, B, row_base, rows_valid, mem,
-                       members, theta, static_cast<float*>(E));
+    hipLaunchKernelGGL((embed_fwd_kernel<float, false>), grid, dim3(256), 0, s, X, d_in, idx, B, row_base,
+                       rows_valid, mem, members, theta, static_cast<float*>(E));
   return hipGetLastError();
 }
 
-hipError_t launch_embed_bwd(const float* X, int d_in, const int32_t* idx, int B, const MemberDev* mem,
-                            const int32_t* members, int nmembers, const float* theta, const float* dE, float* grad,
-                            hipStream_t s) {
-  if (nmembers <= 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_bwd_kernel, dim3(d_in, nmembers), dim3(256), 0, s, X, d_in, idx, B, mem, members, theta,
-                     dE, grad);
+hipError_t launch_embed_bwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, const MemberDev* mem,
+                            const int32_t* members, int nmembers, int max_pin, const float* theta, const float* dE,
+                            float* grad, hipStream_t s) {
+  if (nmembers <= 0 || max_pin <= 0) return hipSuccess;
+  const dim3 grid((max_pin + 255) / 256, nmembers);
+  if (prec == Prec::BF16)
+    hipLaunchKernelGGL((embed_bwd_kernel<true>), grid, dim3(256), 0, s, X, d_in, idx, B, mem, members, theta, dE,
+                       grad);
+  else
+    hipLaunchKernelGGL((embed_bwd_kernel<false>), grid, dim3(256), 0, s, X, d_in, idx, B, mem, members, theta, dE,
+                       grad);
   return hipGetLastError();
 }
 

@@ -180,12 +180,14 @@ hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hip
 // Periodic embeddings (kernels_embed.hip).  E of member k = members[g], row r:
 // the embedded row X[idx[k * B + r]] (idx == nullptr: X[row_base + r]) for
 // r < rows_valid, zero above; dE -> the gradients of w, b, alpha, beta.
+// max_pin: the largest first-layer width p_in of the listed members (the
+// grid's column extent); Bp a multiple of 64.
 hipError_t launch_embed_fwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, int64_t row_base,
                             int rows_valid, int Bp, const MemberDev* mem, const int32_t* members, int nmembers,
                             int max_pin, const float* theta, void* E, hipStream_t s);
-hipError_t launch_embed_bwd(const float* X, int d_in, const int32_t* idx, int B, const MemberDev* mem,
-                            const int32_t* members, int nmembers, const float* theta, const float* dE, float* grad,
-                            hipStream_t s);
+hipError_t launch_embed_bwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, const MemberDev* mem,
+                            const int32_t* members, int nmembers, int max_pin, const float* theta, const float* dE,
+                            float* grad, hipStream_t s);
 // members: the K member ids whose rows of pred are scored (nullptr: 0 .. K-1)
 hipError_t launch_eval_score(Task task, const float* pred, const void* yv, int K, int64_t Nv,
                              double* score_out, const int32_t* members, hipStream_t s);
