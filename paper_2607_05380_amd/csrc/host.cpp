@@ -101,7 +101,7 @@ struct Bufs {
   float *theta = nullptr, *grad = nullptr, *m = nullptr, *v = nullptr;
   uint16_t* shadow = nullptr;
   char* H0 = nullptr;  // first-layer inputs: gathered batches [Bp, Pin], or embedded batches E [Bp, p_in], per member
-  float* dE = nullptr; // embeddings: the gradient of E (fp32), same layout
+  float* dE = nullptr; // embeddings: at each member's E offset / 16, the dE GEMM's sums [Bp / 64][4][p_in] (fp32)
   char* H = nullptr;   // L activation buffers H_1..H_L
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
   float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / kPartRows floats
@@ -443,7 +443,8 @@ struct Plan {
   std::vector<MuonTile> mtiles;
   std::vector<int32_t> mtile0;
   Launch nsA[2]{}, nsB{}, nsX[2]{};
-  // embeddings: dE = dZ_1 W_1 per group (the first layer's data gradient, fp32)
+  // embeddings: dE = dZ_1 W_1 per group (the first layer's data gradient,
+  // reduced in the epilogue into the embedding-gradient sums)
   Launch de[kGroups]{};
 };
 
@@ -930,7 +931,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       d.lda = m.dp;
       d.B = wptr(k, 1);  // W_1 [dp, p_in] read as rows-contiguous: element (n, k) at W_1[k * p_in + n]
       d.ldb = m.p_in;
-      d.C = bf.dE + m.h0_off;
+      d.C = bf.dE + m.h0_off / 16;
       d.ldc = m.p_in;
       d.M = h->Bp;
       d.N = m.p_in;
@@ -941,7 +942,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       ++ln.ndesc;
       const double e = (double)c.d_in * m.d_emb;
       ln.flops += 2.0 * c.B * m.width * e;
-      ln.bytes += (double)h->elt() * (c.B * m.width + m.width * e) + 4.0 * c.B * e;
+      // dZ_1 and W_1 read, x of the rows' features, four fp32 sums per column and 64-row block
+      ln.bytes += (double)h->elt() * (c.B * m.width + m.width * e) + 4.0 * c.B * c.d_in + 16.0 * (h->Bp / 64) * e;
     }
     sort_launch(p, ln);
   }
@@ -984,7 +986,9 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf) {
   bf.v = cv.take<float>(h->P);
   bf.shadow = h->prec == Prec::BF16 ? cv.take<uint16_t>(h->P) : nullptr;
   bf.H0 = cv.take<char>((size_t)h->H0e * h->elt());
-  bf.dE = h->emb ? cv.take<float>((size_t)h->H0e) : nullptr;
+  // each member's sums at its E offset / 16 (Bp is a multiple of 256, so the
+  // offsets divide; a member's [Bp / 64][4][p_in] sums fill Bp p_in / 16)
+  bf.dE = h->emb ? cv.take<float>((size_t)h->H0e / 16) : nullptr;
   bf.H = cv.take<char>((size_t)c.L * h->A * h->elt());
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
   bf.colpart = cv.take<float>((size_t)h->A / kPartRows);
@@ -1198,7 +1202,7 @@ hipError_t muon_step(pack_handle* h, const GemmArgs& base, hipStream_t stream) {
 
 const char* gemm_name(Prec p, OpKind a, OpKind b, EpiKind e) {
   static const char* ops[] = {"kmaj", "rmaj", "xgk", "xgr"};
-  static const char* epis[] = {"fwd", "fwd_eval", "dx", "dw", "ns"};
+  static const char* epis[] = {"fwd", "fwd_eval", "dx", "dw", "ns", "de"};
   static thread_local char buf[64];
   snprintf(buf, sizeof buf, "gemm_%s_%s_%s_%s", p == Prec::BF16 ? "bf16" : "f32", ops[a], ops[b], epis[e]);
   return buf;
@@ -1507,15 +1511,23 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
         }));
       }
       if (l == 1 && h->emb) {
-        // dE = dZ_1 W_1 (fp32), before W_1 is updated, then the embedding gradients
+        // dE = dZ_1 W_1, before W_1 is updated, reduced in the GEMM's epilogue
+        // into per-64-row-block gradient sums; then the sums over the blocks
         GemmArgs ae = for_launch(a, h->de[hf]);
         ae.tile_set = TILES_SMALL;
-        HIP_TRY(timed(h, gemm_name(h->prec, OP_KMAJ, OP_RMAJ, EPI_DW), 0, h->de[hf].flops, h->de[hf].bytes, s,
-                      [&] { return launch_gemm(h->prec, OP_KMAJ, OP_RMAJ, EPI_DW, ae, s); }));
+        ae.emb_x = X;
+        ae.emb_theta = h->b.theta;
+        ae.emb_idx = idx;
+        ae.emb_mem = h->b.d_mem;
+        ae.emb_d_in = c.d_in;
+        HIP_TRY(timed(h, gemm_name(h->prec, OP_KMAJ, OP_RMAJ, EPI_DE), 0, h->de[hf].flops, h->de[hf].bytes, s,
+                      [&] { return launch_gemm(h->prec, OP_KMAJ, OP_RMAJ, EPI_DE, ae, s); }));
         const int gk = h->member0[hf + 1] - h->member0[hf];
-        HIP_TRY(timed(h, "embed_bwd", 1, 0.0, h->de[hf].bytes, s, [&] {
-          return launch_embed_bwd(h->prec, X, c.d_in, idx, c.B, h->b.d_mem, h->b.d_members + h->member0[hf], gk,
-                                  max_pin(h, h->group[hf]), h->b.theta, h->b.dE, h->b.grad, s);
+        double gbytes = 0.0;
+        for (int k : h->group[hf]) gbytes += 4.0 * c.d_in * h->mem[k].d_emb * (4.0 * (h->Bp / 64) + 4.0);
+        HIP_TRY(timed(h, "embed_grad", 1, 0.0, gbytes, s, [&] {
+          return launch_embed_grad(c.d_in, h->Bp, h->b.d_mem, h->b.d_members + h->member0[hf], gk,
+                                   max_pin(h, h->group[hf]), h->b.dE, h->b.grad, s);
         }));
       }
       GemmArgs al = for_launch(a, h->dw[hf][l - 1]);

@@ -5,8 +5,10 @@
 // and the first layer reads the row's d_in * d_emb values.  Each member has its
 // own d_emb and parameters, so its embedded batch E [Bp, p_in] is written per
 // step (GEMM precision) and read by the first-layer forward and weight-gradient
-// GEMMs; the backward pass reduces dE [Bp, p_in] (fp32, from the first layer's
-// data-gradient GEMM) over the rows into the parameters' gradients.
+// GEMMs.  In the backward pass the first layer's data-gradient GEMM reduces
+// dE = dZ_1 W_1 in its epilogue (fp32 accumulators) into per-64-row-block sums
+// of the four gradient terms; embed_grad_kernel adds the blocks.
+#include "emb_trig.h"
 #include "pack_internal.h"
 
 namespace tabpack {
@@ -23,34 +25,6 @@ __device__ __forceinline__ __bf16 to_gemm<__bf16>(float x) {
 template <>
 __device__ __forceinline__ float to_gemm<float>(float x) {
   return x;
-}
-
-// cos and sin of a phase phi (radians) for the bf16 packs: the hardware's
-// v_cos_f32 / v_sin_f32 take revolutions, so t = phi / (2 pi) is reduced to
-// [-1/2, 1/2] by subtracting the nearest integer first.  The error (about 1e-6
-// absolute for phases up to a few hundred radians, most of it the rounding of
-// t) is far below the bf16 rounding of the embedded values.  fp32 packs use
-// cosf / sincosf.
-__device__ __forceinline__ float revolutions(float phi) {
-  const float t = phi * 0.15915494309189535f;
-  return t - rintf(t);
-}
-template <bool FAST>
-__device__ __forceinline__ float cos_of(float phi) {
-  if constexpr (FAST)
-    return __builtin_amdgcn_cosf(revolutions(phi));
-  else
-    return cosf(phi);
-}
-template <bool FAST>
-__device__ __forceinline__ void sincos_of(float phi, float* sn, float* cs) {
-  if constexpr (FAST) {
-    const float t = revolutions(phi);
-    *sn = __builtin_amdgcn_sinf(t);
-    *cs = __builtin_amdgcn_cosf(t);
-  } else {
-    sincosf(phi, sn, cs);
-  }
 }
 
 // Parameters of embedding column col (< d_in d_emb) of a member: feature i,
@@ -131,61 +105,35 @@ __global__ __launch_bounds__(256) void embed_fwd_kernel(const float* X, int d_in
     float v = 0.0f;
     if (on && xrow[rr] >= 0) {
       const float x = xs[rr][f];
-      v = e.j == 0 ? e.a * x + e.be : e.a * cos_of<FAST>(e.w * x + e.b) + e.be;
+      v = e.j == 0 ? e.a * x + e.be : e.a * emb_cos<FAST>(e.w * x + e.b) + e.be;
     }
     out[(int64_t)rr * md.p_in] = to_gemm<T>(v);
   }
 }
 
-// One workgroup per (256 columns, member): each thread sums its column's four
-// gradient terms over the batch rows in row order (fp32), reading dE one row of
-// 256 columns at a time; the rows' data indices go through LDS 256 at a time.
-// (Staging the feature values in LDS as the forward does, 64 rows per chunk,
-// measured twice as slow: three barriers per chunk expose every load.)
-template <bool FAST>
-__global__ __launch_bounds__(256) void embed_bwd_kernel(const float* X, int d_in, const int32_t* idx, int B,
-                                                        const MemberDev* mem, const int32_t* members,
-                                                        const float* theta, const float* dE, float* grad) {
-  __shared__ int64_t xrow[256];
+// The embedding parameters' gradients from the first layer's data-gradient
+// GEMM: its epilogue leaves, per member, column and 64-row block pb, the four
+// sums over the block's rows (alpha, beta, w, b terms) at
+// part[e_act / 16 + (pb * 4 + q) * p_in + col]; here they are added over the
+// blocks in block order.  One thread per (column, member).
+__global__ __launch_bounds__(256) void embed_grad_kernel(int d_in, int nblk, const MemberDev* mem,
+                                                         const int32_t* members, const float* part, float* grad) {
   const int k = members[blockIdx.y];
   const MemberDev md = mem[k];
-  if ((int)blockIdx.x * 256 >= md.p_in) return;  // uniform
   const int col = blockIdx.x * 256 + threadIdx.x;
-  const bool on = col < d_in * md.d_emb;
-  EmbCol e{0, 0, 0.0f, 0.0f, 0.0f, 0.0f};
-  if (on) e = emb_col(md, theta, col);
-  const float* de = dE + md.e_act + (on ? col : 0);
-  float ga = 0.0f, gbe = 0.0f, gw = 0.0f, gb = 0.0f;
-  for (int rc = 0; rc < B; rc += 256) {
-    const int n = min(256, B - rc);
-    __syncthreads();  // the previous chunk's indices are no longer read
-    if ((int)threadIdx.x < n) xrow[threadIdx.x] = (int64_t)idx[(int64_t)k * B + rc + threadIdx.x] * d_in;
-    __syncthreads();
-    if (!on) continue;
-#pragma unroll 8
-    for (int rr = 0; rr < n; ++rr) {
-      const float x = X[xrow[rr] + e.i];
-      const float g = de[(int64_t)(rc + rr) * md.p_in];
-      gbe += g;
-      if (e.j == 0) {
-        ga += g * x;
-      } else {
-        float sn, cs;
-        sincos_of<FAST>(e.w * x + e.b, &sn, &cs);
-        ga += g * cs;
-        const float t = -g * e.a * sn;
-        gb += t;
-        gw += t * x;
-      }
-    }
-  }
-  if (!on) return;
-  grad[md.e_a + col] = ga;
-  grad[md.e_be + col] = gbe;
-  if (e.j > 0) {
-    const int64_t wi = (int64_t)e.i * (md.d_emb - 1) + e.j - 1;
-    grad[md.e_w + wi] = gw;
-    grad[md.e_b + wi] = gb;
+  if (col >= d_in * md.d_emb) return;
+  const float* p = part + md.e_act / 16 + col;
+  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int pb = 0; pb < nblk; ++pb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s[q] += p[(int64_t)(pb * 4 + q) * md.p_in];
+  grad[md.e_a + col] = s[0];
+  grad[md.e_be + col] = s[1];
+  const int i = col / md.d_emb, j = col - i * md.d_emb;
+  if (j > 0) {
+    const int64_t wi = (int64_t)i * (md.d_emb - 1) + j - 1;
+    grad[md.e_w + wi] = s[2];
+    grad[md.e_b + wi] = s[3];
   }
 }
 
@@ -206,17 +154,12 @@ hipError_t launch_embed_fwd(Prec prec, const float* X, int d_in, const int32_t* 
   return hipGetLastError();
 }
 
-hipError_t launch_embed_bwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, const MemberDev* mem,
-                            const int32_t* members, int nmembers, int max_pin, const float* theta, const float* dE,
-                            float* grad, hipStream_t s) {
+hipError_t launch_embed_grad(int d_in, int Bp, const MemberDev* mem, const int32_t* members, int nmembers,
+                             int max_pin, const float* part, float* grad, hipStream_t s) {
   if (nmembers <= 0 || max_pin <= 0) return hipSuccess;
-  const dim3 grid((max_pin + 255) / 256, nmembers);
-  if (prec == Prec::BF16)
-    hipLaunchKernelGGL((embed_bwd_kernel<true>), grid, dim3(256), 0, s, X, d_in, idx, B, mem, members, theta, dE,
-                       grad);
-  else
-    hipLaunchKernelGGL((embed_bwd_kernel<false>), grid, dim3(256), 0, s, X, d_in, idx, B, mem, members, theta, dE,
-                       grad);
+  if (Bp % 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_grad_kernel, dim3((max_pin + 255) / 256, nmembers), dim3(256), 0, s, d_in, Bp / 64, mem,
+                     members, part, grad);
   return hipGetLastError();
 }
 

@@ -56,12 +56,16 @@
 //                 LDS and streamed by the workgroup)
 //   EPI_NS        alpha * Y + beta * acc -> C in the GEMM precision (the
 //                 products of the Newton-Schulz iteration of the Muon optimizer)
+//   EPI_DE        the embedded first layer's dE = dZ_1 W_1 reduced over each
+//                 64-row block into the four embedding-gradient sums per column
+//                 (dE itself is never stored)
 // Every output element is owned by exactly one workgroup and reduced over the
 // full depth in a fixed order: no atomics, bit-reproducible.
 #include <algorithm>
 
-#include "pack_internal.h"
 #include "adamw.h"
+#include "emb_trig.h"
+#include "pack_internal.h"
 
 namespace tabpack {
 namespace {
@@ -1109,6 +1113,86 @@ __device__ __forceinline__ void wait_stage(int newer) {
 // LDS with direct loads in NS stages of KS 16-deep MFMA steps: NS-1 K steps are
 // in flight while one is computed.  fp32 operands go through registers with
 // two stages.
+// EPI_DE: the tile's block of dE = dZ_1 W_1 (rows: batch rows, columns: the
+// embedded inputs i d_emb + j) reduced into the embedding parameters' gradient
+// terms.  The x values of the tile's rows and features are staged in LDS
+// first (the operand buffers are free); each lane then walks the 16 rows it
+// holds of each 32 x 32 block, the lanes l and l + 32 holding the other rows
+// of the same column are added, and each wave writes its 64-row block's four
+// sums per column.  Batch rows >= rows_valid are left out.
+constexpr int kDeFeat = 66;  // features of 128 columns: at most 127 / d_emb + 2 (d_emb >= 2)
+template <typename T, int SH>
+__device__ __forceinline__ void epilogue_de(const GemmArgs& a, const GemmDesc& d, const Tile& t,
+                                            f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn,
+                                            int lane, int tid, char* lds0) {
+  static_assert(SH == kShapeSmall, "dE tiles are small tiles");
+  constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM;
+  constexpr bool FAST = sizeof(T) == 2;
+  const MemberDev& md = a.emb_mem[d.member];
+  const int d_emb = md.d_emb, d_in = a.emb_d_in, ncol = d_in * d_emb;
+  int64_t* rowoff = reinterpret_cast<int64_t*>(lds0);                    // [TM]
+  float(*xs)[kDeFeat] = reinterpret_cast<float(*)[kDeFeat]>(lds0 + TM * 8);  // [TM][kDeFeat]
+  const int i0 = min(t.n0, ncol - 1) / d_emb;
+  const int nf = min(d_in - 1, (min(t.n0 + TM, ncol) - 1) / d_emb) - i0 + 1;
+  if (tid < TM) {
+    const int r = t.m0 + tid;
+    rowoff[tid] = r < a.rows_valid ? (int64_t)a.emb_idx[(int64_t)d.member * a.rows_valid + r] * d_in : -1;
+  }
+  __syncthreads();
+  for (int e = tid; e < TM * nf; e += NT) {
+    const int r = e / nf, f = e - r * nf;
+    const int64_t xo = rowoff[r];
+    xs[r][f] = xo >= 0 ? a.emb_x[xo + i0 + f] : 0.0f;
+  }
+  __syncthreads();
+  const int hv = lane >> 5;
+  float* part = static_cast<float*>(d.C) + (int64_t)((t.m0 >> 6) + wm) * 4 * d.ldc;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int col = t.n0 + wn * NB * 32 + 32 * j + (lane & 31);
+    const bool on = col < ncol;
+    float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+    if (on) {
+      const int fi = col / d_emb, fj = col - fi * d_emb, f = fi - i0;
+      const float al = a.emb_theta[md.e_a + col];
+      float w = 0.0f, b = 0.0f;
+      if (fj > 0) {
+        w = a.emb_theta[md.e_w + (int64_t)fi * (d_emb - 1) + fj - 1];
+        b = a.emb_theta[md.e_b + (int64_t)fi * (d_emb - 1) + fj - 1];
+      }
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rl = wm * MB * 32 + 32 * i + 8 * (r >> 2) + 4 * hv + (r & 3);
+          if (t.m0 + rl >= a.rows_valid) continue;
+          const float g = acc[i][j][r], x = xs[rl][f];
+          s1 += g;
+          if (fj == 0) {
+            s0 += g * x;
+          } else {
+            float sn, cs;
+            emb_sincos<FAST>(w * x + b, &sn, &cs);
+            s0 += g * cs;
+            const float tt = -g * al * sn;
+            s3 += tt;
+            s2 += tt * x;
+          }
+        }
+    }
+    s0 += __shfl_xor(s0, 32, 64);
+    s1 += __shfl_xor(s1, 32, 64);
+    s2 += __shfl_xor(s2, 32, 64);
+    s3 += __shfl_xor(s3, 32, 64);
+    if (on && hv == 0) {
+      part[col] = s0;
+      part[d.ldc + col] = s1;
+      part[2 * d.ldc + col] = s2;
+      part[3 * d.ldc + col] = s3;
+    }
+  }
+}
+
 template <typename T, int AK, int BK_, int EPI, int SH, int KS, int NS>
 __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, const Tile& t, char* lds0, int tid,
                                          int wave) {
@@ -1202,7 +1286,10 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
       return;
     }
   }
-  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * Shape<SH>::STAGE, pre);
+  if constexpr (EPI == EPI_DE)
+    epilogue_de<T, SH>(a, d, t, acc, wm, wn, lane, tid, lds0);
+  else
+    epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * Shape<SH>::STAGE, pre);
 }
 
 // ----------------------------------------------------------------- kernel --
@@ -1294,9 +1381,9 @@ hipError_t launch_prec(OpKind ak, OpKind bk, EpiKind e, const GemmArgs& args, hi
     return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL>(args, s);
   if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DX) return launch_t<T, OP_KMAJ, OP_RMAJ, EPI_DX>(args, s);
   if (ak == OP_RMAJ && bk == OP_RMAJ && e == EPI_DW) return launch_t<T, OP_RMAJ, OP_RMAJ, EPI_DW>(args, s);
-  if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DW) {  // the embedding's dE: fp32 store, small tiles only
-    if (args.tile_set != TILES_SMALL || args.theta) return hipErrorInvalidValue;
-    return launch_small<T, OP_KMAJ, OP_RMAJ, EPI_DW>(args, s);
+  if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DE) {  // the embedding's dE reduction: small tiles only
+    if (args.tile_set != TILES_SMALL) return hipErrorInvalidValue;
+    return launch_small<T, OP_KMAJ, OP_RMAJ, EPI_DE>(args, s);
   }
   if (e == EPI_NS) {  // Newton-Schulz products
     if (ak == OP_KMAJ && bk == OP_KMAJ) return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_NS>(args, s);

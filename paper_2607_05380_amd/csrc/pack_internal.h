@@ -33,7 +33,9 @@ enum class Task : int { REG = 0, BIN = 1, MULTI = 2 };
 //   KMAJ    element (r, k) at P[r * ld + k]         -- depth contiguous
 //   RMAJ    element (r, k) at P[k * ld + r]         -- rows contiguous (transposed on load)
 enum OpKind : int { OP_KMAJ = 0, OP_RMAJ = 1 };
-enum EpiKind : int { EPI_FWD = 0, EPI_FWD_EVAL = 1, EPI_DX = 2, EPI_DW = 3, EPI_NS = 4 };
+enum EpiKind : int { EPI_FWD = 0, EPI_FWD_EVAL = 1, EPI_DX = 2, EPI_DW = 3, EPI_NS = 4, EPI_DE = 5 };
+
+struct MemberDev;
 
 // One member's GEMM problem C[m, n] = sum_k A(m, k) B(n, k) in one grouped launch.
 struct GemmDesc {
@@ -89,6 +91,17 @@ struct GemmArgs {
   // symmetric C and every tile above it also stores its transpose
   float ns_alpha, ns_beta;
   int32_t ns_sym;
+  // EPI_DE only (the embedded first layer's dE = dZ_1 W_1, never stored): the
+  // epilogue reduces each wave's 64 rows of dE into the four embedding-gradient
+  // terms per column (alpha: dE f, beta: dE, w: -dE alpha sin(phi) x, b:
+  // -dE alpha sin(phi); f = x or cos(phi), phi = w x + b) and writes them at
+  // C + ((row0 / 64) * 4 + q) * ldc + col.  x of batch row r (< rows_valid) is
+  // emb_x[emb_idx[member * rows_valid + r] * emb_d_in + feature].
+  const float* emb_x;
+  const float* emb_theta;  // the parameters (w, b, alpha at the member's offsets)
+  const int32_t* emb_idx;
+  const MemberDev* emb_mem;
+  int32_t emb_d_in;
 };
 
 // AdamW constants of one step.
@@ -179,15 +192,16 @@ hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, fl
 hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hipStream_t s);
 // Periodic embeddings (kernels_embed.hip).  E of member k = members[g], row r:
 // the embedded row X[idx[k * B + r]] (idx == nullptr: X[row_base + r]) for
-// r < rows_valid, zero above; dE -> the gradients of w, b, alpha, beta.
+// r < rows_valid, zero above.
 // max_pin: the largest first-layer width p_in of the listed members (the
 // grid's column extent); Bp a multiple of 64.
 hipError_t launch_embed_fwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, int64_t row_base,
                             int rows_valid, int Bp, const MemberDev* mem, const int32_t* members, int nmembers,
                             int max_pin, const float* theta, void* E, hipStream_t s);
-hipError_t launch_embed_bwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, const MemberDev* mem,
-                            const int32_t* members, int nmembers, int max_pin, const float* theta, const float* dE,
-                            float* grad, hipStream_t s);
+// grad of w, b, alpha, beta from the EPI_DE partial sums (in the dE buffer at
+// each member's e_act / 16: [Bp / 64][4][p_in])
+hipError_t launch_embed_grad(int d_in, int Bp, const MemberDev* mem, const int32_t* members, int nmembers,
+                             int max_pin, const float* part, float* grad, hipStream_t s);
 // members: the K member ids whose rows of pred are scored (nullptr: 0 .. K-1)
 hipError_t launch_eval_score(Task task, const float* pred, const void* yv, int K, int64_t Nv,
                              double* score_out, const int32_t* members, hipStream_t s);
