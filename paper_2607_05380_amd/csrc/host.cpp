@@ -79,6 +79,7 @@ struct Launch {
   int tile0, ntiles;
   double flops;  // algorithmic flops of the launch (true member shapes)
   double bytes;  // algorithmic HBM bytes: operands read once, outputs written once
+  TileSet ts = TILES_SMALL;  // tile set of its tiles (set by add_tiles / add_tiles_sym)
 };
 
 // One timed launch: events recorded on the launch stream around it.
@@ -115,6 +116,7 @@ struct Bufs {
   int64_t* d_bias_off = nullptr;  // [L][K] offsets of b_l
   GemmDesc* d_descs = nullptr;
   Tile* d_tiles = nullptr;
+  size_t tile_cap = 0;  // entries of d_tiles
   ColTile* d_coltiles = nullptr;
   HeadTile* d_headtiles = nullptr;
   int32_t* d_members = nullptr;
@@ -177,6 +179,9 @@ struct pack_handle {
   int head_rb = 0;  // rows per head-backward block
   uint64_t t = 0;
   TileSet tiles = TILES_SMALL;  // tile set of the bf16 GEMMs (fp32 GEMMs run small tiles only)
+  // tile sets of the forward, data- and weight-gradient GEMMs: -1 chooses per
+  // launch (launch_tiles), else a fixed TileSet
+  int tiles_fwd = -1, tiles_dx = -1, tiles_dw = -1;
   TileSet ns_tiles = TILES_SMALL;  // tile set of the Newton-Schulz GEMMs
   // side stream for ALU-bound work that overlaps memory-bound kernels of the
   // caller's stream, joined back through events (created by pack_bind)
@@ -455,6 +460,7 @@ struct Plan {
 // tile partly filled.  Small set: 128 x 128 tiles only.
 void add_tiles(Plan& p, Launch& ln, int d, int M, int N, int kdepth) {
   const size_t first = p.tiles.size();
+  ln.ts = p.tile_set;
   auto big_end = [&](int E) {
     const int r = E % kBigTile;
     return r == 0 ? E : (r > kSmallTile ? E - r + kBigTile : E - r);
@@ -616,6 +622,7 @@ void muon_sizes(const pack_handle* h, It begin, It end, int64_t& xe, int64_t& ae
 // tiles on and above its own diagonal, and the columns right of it take the
 // tile set's large tiles (a remainder of at most 128 columns small ones).
 void add_tiles_sym(Plan& p, Launch& ln, int d, int S, int kdepth) {
+  ln.ts = p.tile_set;
   auto push = [&](int m0, int n0, int shape) {
     const int tm = shape == kShapeSmall ? kSmallTile : kBigTile;
     const int tw = shape == kShapeBig ? kBigTile : kSmallTile;
@@ -763,10 +770,29 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
   p.tile_set = saved;
 }
 
+// Tile set of one forward / data-gradient / weight-gradient launch whose
+// 128 x 128 tiles number n_small: fixed by `forced` (>= 0), else 256 x 128 tiles
+// when there are at least kTallMinTiles small ones (two full rounds of tall
+// tiles at two workgroups per CU), small tiles otherwise.  Measured (ms per
+// step, all small / all tall / chosen): 64 members of widths 64..2048 at batch
+// 2048 (launches of 700..2800 small tiles) 6.29 / 5.76; 64 of widths
+// 256..1024 at batch 1024 (500..840) 1.45 / 1.53 (tall dW alone 1.53);
+// 32 of 256..1024 (~440) 0.63 / 0.67.
+constexpr int kTallMinTiles = 1024;
+TileSet launch_tiles(const pack_handle* h, int forced, int64_t n_small) {
+  if (forced >= 0) return (TileSet)forced;
+  if (h->prec != Prec::BF16) return TILES_SMALL;
+  return n_small >= kTallMinTiles ? TILES_TALL : TILES_SMALL;
+}
+int64_t small_tiles(int M, int N) { return (int64_t)((M + kSmallTile - 1) / kSmallTile) * ((N + kSmallTile - 1) / kSmallTile); }
+
 // Launch tables over the members of `group` (the active members split into
 // streams; carve() sizes the workspace with every member in one group).
-Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&group)[kGroups]) {
+Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&group)[kGroups],
+                bool sizing = false) {
   Plan p;
+  // sizing: small tiles for the main GEMMs (the largest tile count of any choice)
+  auto choose = [&](int forced, int64_t n_small) { return sizing ? TILES_SMALL : launch_tiles(h, forced, n_small); };
   p.tile_set = h->tiles;
   const pack_config& c = h->cfg;
   const size_t es = h->elt();
@@ -790,6 +816,10 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     // forward: Z_l = H_{l-1} W_l^T + b_l, rows = batch (Bp), cols = dp; members
     // with fewer than l hidden blocks are not in the launch
     Launch f{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
+    int64_t nsm = 0;
+    for (int k : group[hf])
+      if (h->mem[k].depth >= l) nsm += small_tiles(h->Bp, h->mem[k].dp);
+    p.tile_set = choose(h->tiles_fwd, nsm);
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
       if (m.depth < l) continue;
@@ -826,7 +856,12 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
   {
     // evaluation, layer 1: every member reads the same validation rows (H_0 block 0)
     Launch f{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
-    for (int hf = 0; hf < kGroups; ++hf) f.ndesc += (int)group[hf].size();
+    int64_t nsm = 0;
+    for (int hf = 0; hf < kGroups; ++hf) {
+      f.ndesc += (int)group[hf].size();
+      for (int k : group[hf]) nsm += small_tiles(h->Bp, h->mem[k].dp);
+    }
+    p.tile_set = choose(h->tiles_fwd, nsm);
     for (int hf = 0; hf < kGroups; ++hf)
       for (int i = 0; i < (int)group[hf].size(); ++i) {
         const int k = group[hf][i];
@@ -842,6 +877,10 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
   for (int l = 1; l <= c.L; ++l) {
     // weight gradient: dW_l^T[out, in] = sum_rows dZ_l[row, out] H_{l-1}[row, in]
     Launch w{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
+    int64_t nsm = 0;
+    for (int k : group[hf])
+      if (h->mem[k].depth >= l) nsm += small_tiles(h->mem[k].dp, l == 1 ? h->mem[k].p_in : h->mem[k].dp);
+    p.tile_set = choose(h->tiles_dw, nsm);
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
       if (m.depth < l) continue;
@@ -876,6 +915,10 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     // data gradient (l >= 2): dZ_{l-1} = (dZ_l W_l) * [H_{l-1} > 0] * s_k
     Launch x{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0};
     if (l >= 2) {
+      int64_t nsx = 0;
+      for (int k : group[hf])
+        if (h->mem[k].depth >= l) nsx += small_tiles(h->Bp, h->mem[k].dp);
+      p.tile_set = choose(h->tiles_dx, nsx);
       for (int k : group[hf]) {
         const Member& m = h->mem[k];
         if (m.depth < l) continue;
@@ -1011,7 +1054,11 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf) {
     bf.mA = cv.take<char>((size_t)ae * h->elt());
     bf.mB = cv.take<char>((size_t)ae * h->elt());
   }
-  Plan plan = build_plan(h, bf, all);
+  // The tables are sized by a plan with every member in one launch per layer
+  // and small tiles for the main GEMMs: any tile set, and any split of the
+  // members, takes at most as many tiles.
+  Plan plan = build_plan(h, bf, all, true);
+  bf.tile_cap = plan.tiles.size();
   if (h->muon) {
     bf.mpart = cv.take<double>(plan.mtiles.size());
     bf.minv = cv.take<float>(plan.mmats.size());
@@ -1052,6 +1099,7 @@ GemmArgs base_args(const pack_handle* h) {
 GemmArgs for_launch(GemmArgs a, const Launch& ln) {
   a.tiles += ln.tile0;
   a.ntiles = ln.ntiles;
+  a.tile_set = ln.ts;
   return a;
 }
 
@@ -1103,6 +1151,9 @@ void set_active_ids(pack_handle* h) {
 int upload_plan(pack_handle* h, hipStream_t stream) {
   const pack_config& c = h->cfg;
   Plan plan = build_plan(h, h->b, h->group);
+  if (plan.tiles.size() > h->b.tile_cap)
+    return fail(PACK_EINVAL, "internal: the plan holds %zu GEMM tiles, the device table %zu", plan.tiles.size(),
+                h->b.tile_cap);
   std::vector<uint32_t> aux;
   for (uint32_t ch : h->aux_chunks)
     if (h->active[h->chunk_tab[ch] & 0x7FFFFFFFu]) aux.push_back(ch);
@@ -1226,14 +1277,26 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
   h->prec = cfg->precision == PACK_PREC_BF16 ? Prec::BF16 : Prec::FP32;
   h->task = (Task)cfg->task;
   h->q = cfg->quantum ? cfg->quantum : 32;
-  // 128x128 tiles at two workgroups per CU measure faster on the packed
-  // workloads than 256x256 tiles at one; TABPACK_GEMM_TILES=big|tall|small overrides
+  // The tile sets of the main GEMMs are chosen per launch (launch_tiles);
+  // TABPACK_GEMM_TILES=big|tall|small fixes them all, TABPACK_TILES_FWD / _DX /
+  // _DW one kind.  h->tiles: the set of the remaining bf16 GEMM launches.
   h->tiles = TILES_SMALL;
   if (const char* e = getenv("TABPACK_GEMM_TILES")) {
     const std::string v(e);
     h->tiles = v == "big" ? TILES_BIG : (v == "tall" ? TILES_TALL : TILES_SMALL);
   }
   if (h->prec == Prec::FP32) h->tiles = TILES_SMALL;
+  auto tile_env = [&](const char* name) {
+    const char* e = getenv(name);
+    if (h->prec == Prec::FP32) return (int)TILES_SMALL;
+    if (!e) e = getenv("TABPACK_GEMM_TILES");
+    if (!e) return -1;
+    const std::string v(e);
+    return (int)(v == "big" ? TILES_BIG : (v == "tall" ? TILES_TALL : TILES_SMALL));
+  };
+  h->tiles_fwd = tile_env("TABPACK_TILES_FWD");
+  h->tiles_dx = tile_env("TABPACK_TILES_DX");
+  h->tiles_dw = tile_env("TABPACK_TILES_DW");
   // Newton-Schulz GEMMs: small tiles measured 3.79 ms per Muon step on the
   // 64-member regression workload, tall 4.03, big 5.53; TABPACK_NS_TILES overrides
   h->ns_tiles = TILES_SMALL;
