@@ -248,7 +248,8 @@ def measured_traffic(workload, kernel):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--steps", type=int, default=0,
+                    help="timed steps (default: one epoch of the workload, n_train // B: 683 for regression_large)")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="regression_large")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -277,6 +278,8 @@ def main():
     Xtr, ytr, Xva, yva = synth.make_data_device(cfg, dev)
     orders = synth.epoch_orders_device(cfg, 0, cfg["n_train"], dev)
     steps_per_epoch = cfg["n_train"] // cfg["B"]
+    if a.steps <= 0:
+        a.steps = steps_per_epoch
     total = a.warmup + a.steps + a.profile_steps
     idx_all = torch.stack([orders[:, (s % steps_per_epoch) * cfg["B"]:(s % steps_per_epoch + 1) * cfg["B"]]
                            for s in range(total)]).contiguous()
