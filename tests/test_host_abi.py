@@ -175,3 +175,18 @@ def test_embedding_hparams_and_init_match_oracle():
             np.testing.assert_array_equal(W, Wr.astype(np.float32))
             np.testing.assert_array_equal(b, br.astype(np.float32))
         assert pk.param_count(k) == sum(a.size for a in emb.values()) + sum(W.size + b.size for W, b in layers)
+
+
+def test_workspace_independent_of_tile_sets(monkeypatch):
+    # The GEMM tile sets are chosen per launch (or forced by the environment);
+    # the device tile table is sized for the largest choice (small tiles), so
+    # the workspace is the same under every setting.  multiclass_lognormal's
+    # evaluation launch of all 32 members has 1,280 small tiles: tall by default.
+    sizes = {}
+    for v in (None, "small", "tall", "big"):
+        if v is None:
+            monkeypatch.delenv("TABPACK_GEMM_TILES", raising=False)
+        else:
+            monkeypatch.setenv("TABPACK_GEMM_TILES", v)
+        sizes[v] = tabpack.Pack(configs.workload("multiclass_lognormal")).workspace_bytes()
+    assert len(set(sizes.values())) == 1, sizes
