@@ -778,10 +778,16 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
 // 2048 (launches of 700..2800 small tiles) 6.29 / 5.76; 64 of widths
 // 256..1024 at batch 1024 (500..840) 1.45 / 1.53 (tall dW alone 1.53);
 // 32 of 256..1024 (~440) 0.63 / 0.67.
-constexpr int kTallMinTiles = 1024;
-TileSet launch_tiles(const pack_handle* h, int forced, int64_t n_small) {
+// Weight-gradient launches also need a depth (padded batch) of at least
+// kTallMinDepthDw: their small tiles stream the fused optimizer over the whole
+// staged gradient tile, which the tall tiles do not, and at a 1024-row batch
+// that epilogue outweighs the tall tiles' faster main loop (the embedded first
+// layer's dW: 7.05 ms small, 7.99 ms tall), at 2048 rows it does not
+// (widths 64..2048: 6.29 -> 6.09 ms per step with tall dW tiles alone).
+constexpr int kTallMinTiles = 1024, kTallMinDepthDw = 2048;
+TileSet launch_tiles(const pack_handle* h, int forced, int64_t n_small, int min_depth = 0) {
   if (forced >= 0) return (TileSet)forced;
-  if (h->prec != Prec::BF16) return TILES_SMALL;
+  if (h->prec != Prec::BF16 || h->Bp < min_depth) return TILES_SMALL;
   return n_small >= kTallMinTiles ? TILES_TALL : TILES_SMALL;
 }
 int64_t small_tiles(int M, int N) { return (int64_t)((M + kSmallTile - 1) / kSmallTile) * ((N + kSmallTile - 1) / kSmallTile); }
@@ -792,7 +798,9 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
                 bool sizing = false) {
   Plan p;
   // sizing: small tiles for the main GEMMs (the largest tile count of any choice)
-  auto choose = [&](int forced, int64_t n_small) { return sizing ? TILES_SMALL : launch_tiles(h, forced, n_small); };
+  auto choose = [&](int forced, int64_t n_small, int min_depth = 0) {
+    return sizing ? TILES_SMALL : launch_tiles(h, forced, n_small, min_depth);
+  };
   p.tile_set = h->tiles;
   const pack_config& c = h->cfg;
   const size_t es = h->elt();
@@ -880,7 +888,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     int64_t nsm = 0;
     for (int k : group[hf])
       if (h->mem[k].depth >= l) nsm += small_tiles(h->mem[k].dp, l == 1 ? h->mem[k].p_in : h->mem[k].dp);
-    p.tile_set = choose(h->tiles_dw, nsm);
+    p.tile_set = choose(h->tiles_dw, nsm, kTallMinDepthDw);
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
       if (m.depth < l) continue;
