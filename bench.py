@@ -255,8 +255,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=10)
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="before the timed steps, copy a 256 MiB buffer 3 times (the reference dispatches that "
-                         "scale hardware byte counters in a profiler run)")
+                    help="accepted for older profiler commands: the 256 MiB copies that scale the hardware byte "
+                         "counters run in every invocation (they also time the copy bandwidth)")
     ap.add_argument("--online-epochs", type=int, default=1,
                     help="epochs of the online driver timed after the steps (0: none)")
     ap.add_argument("--no-per-epoch", action="store_true", help="skip the per-epoch measurements")
@@ -294,14 +294,22 @@ def main():
         pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
     torch.cuda.synchronize()
     log(f"warmup done, losses[:4] = {loss[:4].tolist()}")
-    if a.copy_calibration:
-        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    # device-to-device copy bandwidth (read + write), the measured reference for
+    # the HBM-bound kernels; in a profiler run the same copies scale the byte
+    # counters (profiles_summary traffic)
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(3):
+        dst.copy_(src)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 2 * 3 * COPY_BYTES / (c0.elapsed_time(c1) / 1e3) / 1e9
+    del src, dst
+    log(f"device-to-device copy: {copy_gbps:.0f} GB/s (read + write)")
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -354,6 +362,9 @@ def main():
                     "busy_us_per_step": round(dom["busy_ms"] * 1e3 / a.profile_steps, 2),
                     "launches_per_step": dom["launches"] / a.profile_steps,
                     "achieved_per_launch": round(work / (dom["avg_ms"] / 1e3) / scale, 2)}
+        if dom["kind"] != "mfma":
+            roofline["copy_gb_per_s"] = round(copy_gbps, 1)
+            roofline["frac_of_copy"] = round(achieved / copy_gbps, 4)
     out = {
         "metric": METRIC, "value": round(msamples, 1), "unit": "member-samples/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
