@@ -155,7 +155,9 @@ struct pack_handle {
   Launch de[kGroups]{};
   int ns_steps = 5;
   int n_mmats = 0, n_mtiles = 0;     // Muon matrices and tiles of the active members
-  Launch nsA[2]{}, nsB{}, nsX[2]{};
+  // per member group g: matrices [mmat0[g], mmat0[g+1]), tiles [mtileg[g], mtileg[g+1])
+  int mmat0[kGroups + 1]{}, mtileg[kGroups + 1]{};
+  Launch nsA[2][kGroups]{}, nsB[kGroups]{}, nsX[2][kGroups]{};
 
   bool bound = false;
   Bufs b;
@@ -447,7 +449,8 @@ struct Plan {
   std::vector<MuonMat> mmats;
   std::vector<MuonTile> mtiles;
   std::vector<int32_t> mtile0;
-  Launch nsA[2]{}, nsB{}, nsX[2]{};
+  int mmat0[kGroups + 1]{}, mtileg[kGroups + 1]{};  // per member group: first matrix, first tile
+  Launch nsA[2][kGroups]{}, nsB[kGroups]{}, nsX[2][kGroups]{};
   // embeddings: dE = dZ_1 W_1 per group (the first layer's data gradient,
   // reduced in the epilogue into the embedding-gradient sums)
   Launch de[kGroups]{};
@@ -659,18 +662,18 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
   const size_t es = h->elt();
   const TileSet saved = p.tile_set;
   p.tile_set = h->ns_tiles;
-  for (int par = 0; par < 2; ++par) {
-    p.nsA[par] = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
-    p.nsX[par] = Launch{};
-  }
   int64_t xo = 0, ao = 0;
   struct Item {
     MuonShape q;
     int64_t xoff, aoff;
   };
-  std::vector<Item> items;
+  auto xp = [&](int par, int64_t off) { return (void*)(bf.mX[par] + (size_t)off * es); };
+  auto ap = [&](const char* base, int64_t off) { return (void*)(base + (size_t)off * es); };
   p.mtile0.push_back(0);
-  for (int hf = 0; hf < kGroups; ++hf)
+  for (int hf = 0; hf < kGroups; ++hf) {
+    p.mmat0[hf] = (int)p.mmats.size();
+    p.mtileg[hf] = (int)p.mtiles.size();
+    std::vector<Item> items;
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
       for (int l = 1; l <= m.depth; ++l) {
@@ -695,78 +698,79 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
         ao += round_up((int64_t)q.S * q.S, kChunk);
       }
     }
-  auto xp = [&](int par, int64_t off) { return (void*)(bf.mX[par] + (size_t)off * es); };
-  auto ap = [&](const char* base, int64_t off) { return (void*)(base + (size_t)off * es); };
-  // A = X X^T, one launch per parity of the X buffer it reads
-  for (int par = 0; par < 2; ++par) {
-    Launch& ln = p.nsA[par];
-    ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
-    for (const Item& it : items) {
-      GemmDesc d{};
-      d.A = d.B = xp(par, it.xoff);
-      d.lda = d.ldb = it.q.L;
-      d.C = ap(bf.mA, it.aoff);
-      d.ldc = it.q.S;
-      d.M = d.N = it.q.S;
-      d.Kd = it.q.L;
-      add_tiles_sym(p, ln, (int)p.descs.size(), it.q.S, d.Kd);
-      p.descs.push_back(d);
-      ++ln.ndesc;
-      const double s = std::min(it.q.r, it.q.c), l = std::max(it.q.r, it.q.c);
-      ln.flops += s * (s + 1) * l;  // a symmetric result: the upper triangle
-      ln.bytes += es * (s * l + s * s);
+    // A = X X^T, one launch per parity of the X buffer it reads
+    for (int par = 0; par < 2; ++par) {
+      Launch& ln = p.nsA[par][hf];
+      ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
+      for (const Item& it : items) {
+        GemmDesc d{};
+        d.A = d.B = xp(par, it.xoff);
+        d.lda = d.ldb = it.q.L;
+        d.C = ap(bf.mA, it.aoff);
+        d.ldc = it.q.S;
+        d.M = d.N = it.q.S;
+        d.Kd = it.q.L;
+        add_tiles_sym(p, ln, (int)p.descs.size(), it.q.S, d.Kd);
+        p.descs.push_back(d);
+        ++ln.ndesc;
+        const double s = std::min(it.q.r, it.q.c), l = std::max(it.q.r, it.q.c);
+        ln.flops += s * (s + 1) * l;  // a symmetric result: the upper triangle
+        ln.bytes += es * (s * l + s * s);
+      }
+      sort_launch(p, ln);
     }
-    sort_launch(p, ln);
-  }
-  // B' = b A + c A A: A is stored exactly symmetric (mirrored tiles), so A A =
-  // A A^T reads both operands depth-contiguous, and B' is symmetric too
-  {
-    Launch& ln = p.nsB;
-    ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
-    for (const Item& it : items) {
-      GemmDesc d{};
-      d.A = d.B = ap(bf.mA, it.aoff);
-      d.lda = d.ldb = it.q.S;
-      d.C = ap(bf.mB, it.aoff);
-      d.ldc = it.q.S;
-      d.Y = ap(bf.mA, it.aoff);
-      d.ldy = it.q.S;
-      d.M = d.N = d.Kd = it.q.S;
-      add_tiles_sym(p, ln, (int)p.descs.size(), it.q.S, d.Kd);
-      p.descs.push_back(d);
-      ++ln.ndesc;
-      const double s = std::min(it.q.r, it.q.c);
-      ln.flops += s * (s + 1) * s;  // a symmetric result: the upper triangle
-      ln.bytes += es * 3.0 * s * s;
+    // B' = b A + c A A: A is stored exactly symmetric (mirrored tiles), so A A =
+    // A A^T reads both operands depth-contiguous, and B' is symmetric too
+    {
+      Launch& ln = p.nsB[hf];
+      ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
+      for (const Item& it : items) {
+        GemmDesc d{};
+        d.A = d.B = ap(bf.mA, it.aoff);
+        d.lda = d.ldb = it.q.S;
+        d.C = ap(bf.mB, it.aoff);
+        d.ldc = it.q.S;
+        d.Y = ap(bf.mA, it.aoff);
+        d.ldy = it.q.S;
+        d.M = d.N = d.Kd = it.q.S;
+        add_tiles_sym(p, ln, (int)p.descs.size(), it.q.S, d.Kd);
+        p.descs.push_back(d);
+        ++ln.ndesc;
+        const double s = std::min(it.q.r, it.q.c);
+        ln.flops += s * (s + 1) * s;  // a symmetric result: the upper triangle
+        ln.bytes += es * 3.0 * s * s;
+      }
+      sort_launch(p, ln);
     }
-    sort_launch(p, ln);
-  }
-  // X' = a X + B' X, reading X from buffer par and writing buffer 1 - par
-  for (int par = 0; par < 2; ++par) {
-    Launch& ln = p.nsX[par];
-    ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
-    for (const Item& it : items) {
-      GemmDesc d{};
-      d.A = ap(bf.mB, it.aoff);
-      d.lda = it.q.S;
-      d.B = xp(par, it.xoff);
-      d.ldb = it.q.L;
-      d.C = xp(par ^ 1, it.xoff);
-      d.ldc = it.q.L;
-      d.Y = xp(par, it.xoff);
-      d.ldy = it.q.L;
-      d.M = it.q.S;
-      d.N = it.q.L;
-      d.Kd = it.q.S;
-      add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
-      p.descs.push_back(d);
-      ++ln.ndesc;
-      const double s = std::min(it.q.r, it.q.c), l = std::max(it.q.r, it.q.c);
-      ln.flops += 2.0 * s * s * l;
-      ln.bytes += es * (s * s + 2.0 * s * l);
+    // X' = a X + B' X, reading X from buffer par and writing buffer 1 - par
+    for (int par = 0; par < 2; ++par) {
+      Launch& ln = p.nsX[par][hf];
+      ln = Launch{(int)p.descs.size(), 0, (int)p.tiles.size(), 0, 0.0, 0.0};
+      for (const Item& it : items) {
+        GemmDesc d{};
+        d.A = ap(bf.mB, it.aoff);
+        d.lda = it.q.S;
+        d.B = xp(par, it.xoff);
+        d.ldb = it.q.L;
+        d.C = xp(par ^ 1, it.xoff);
+        d.ldc = it.q.L;
+        d.Y = xp(par, it.xoff);
+        d.ldy = it.q.L;
+        d.M = it.q.S;
+        d.N = it.q.L;
+        d.Kd = it.q.S;
+        add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
+        p.descs.push_back(d);
+        ++ln.ndesc;
+        const double s = std::min(it.q.r, it.q.c), l = std::max(it.q.r, it.q.c);
+        ln.flops += 2.0 * s * s * l;
+        ln.bytes += es * (s * s + 2.0 * s * l);
+      }
+      sort_launch(p, ln);
     }
-    sort_launch(p, ln);
   }
+  p.mmat0[kGroups] = (int)p.mmats.size();
+  p.mtileg[kGroups] = (int)p.mtiles.size();
   p.tile_set = saved;
 }
 
@@ -1184,11 +1188,17 @@ int upload_plan(pack_handle* h, hipStream_t stream) {
   HIP_TRY(hipStreamSynchronize(stream));
   h->n_mmats = (int)plan.mmats.size();
   h->n_mtiles = (int)plan.mtiles.size();
-  for (int par = 0; par < 2; ++par) {
-    h->nsA[par] = plan.nsA[par];
-    h->nsX[par] = plan.nsX[par];
+  for (int g = 0; g <= kGroups; ++g) {
+    h->mmat0[g] = plan.mmat0[g];
+    h->mtileg[g] = plan.mtileg[g];
   }
-  h->nsB = plan.nsB;
+  for (int g = 0; g < kGroups; ++g) {
+    for (int par = 0; par < 2; ++par) {
+      h->nsA[par][g] = plan.nsA[par][g];
+      h->nsX[par][g] = plan.nsX[par][g];
+    }
+    h->nsB[g] = plan.nsB[g];
+  }
   for (int hf = 0; hf < kGroups; ++hf) h->de[hf] = plan.de[hf];
   for (int hf = 0; hf < kGroups; ++hf) {
     h->fwd[0][hf] = plan.fwd[0][hf];
@@ -1211,51 +1221,55 @@ int upload_plan(pack_handle* h, hipStream_t stream) {
 
 const char* gemm_name(Prec p, OpKind a, OpKind b, EpiKind e);
 
-// Muon step of every active member's hidden weights (their gradients are in
-// grad): momentum and tile norms, inverse norms, X0, ns_steps Newton-Schulz
-// iterations of three grouped GEMMs, update.  On `stream`, after the members'
-// backward passes.
-hipError_t muon_step(pack_handle* h, const GemmArgs& base, hipStream_t stream) {
-  if (h->n_mmats == 0) return hipSuccess;
+// Muon step of the hidden weights of member group g's active members (their
+// gradients are in grad): momentum and tile norms, inverse norms, X0, ns_steps
+// Newton-Schulz iterations of three grouped GEMMs, update.  On the group's
+// stream after its backward pass, so one group's step overlaps the others'
+// backward passes and Muon steps.
+hipError_t muon_step(pack_handle* h, const GemmArgs& base, int g, hipStream_t stream) {
+  const int mat0 = h->mmat0[g], nmats = h->mmat0[g + 1] - mat0;
+  const int tile0 = h->mtileg[g], ntiles = h->mtileg[g + 1] - tile0;
+  if (nmats == 0) return hipSuccess;
   const pack_config& c = h->cfg;
   const float mu = (float)c.muon_momentum;
   const int nest = c.muon_nesterov ? 1 : 0;
-  const double wbytes = (double)h->n_mtiles * 64 * 64;  // upper bound of the weights' elements
+  const MuonTile* tiles = h->b.d_mtiles + tile0;
+  const double wbytes = (double)ntiles * 64 * 64;  // upper bound of the weights' elements
   hipError_t e = timed(h, "muon_prep", 1, 0.0, wbytes * 12.0, stream, [&] {
-    return launch_muon_prep(h->b.d_mmats, h->b.d_mtiles, h->n_mtiles, h->b.grad, h->b.m, mu, nest, h->b.mpart,
-                            stream);
+    return launch_muon_prep(h->b.d_mmats, tiles, ntiles, h->b.grad, h->b.m, mu, nest, h->b.mpart + tile0, stream);
   });
   if (e != hipSuccess) return e;
-  e = timed(h, "muon_norm", 1, 0.0, 8.0 * h->n_mtiles, stream,
-            [&] { return launch_muon_norm(h->b.d_mtile0, h->n_mmats, h->b.mpart, h->b.minv, stream); });
+  e = timed(h, "muon_norm", 1, 0.0, 8.0 * ntiles, stream, [&] {
+    return launch_muon_norm(h->b.d_mtile0 + mat0, nmats, h->b.mpart, h->b.minv + mat0, stream);
+  });
   if (e != hipSuccess) return e;
   e = timed(h, "muon_convert", 1, 0.0, wbytes * (8.0 + h->elt()), stream, [&] {
-    return launch_muon_convert(h->prec, h->b.d_mmats, h->b.d_mtiles, h->n_mtiles, h->b.grad, h->b.m, mu, nest,
-                               h->b.minv, h->b.mX[0], stream);
+    return launch_muon_convert(h->prec, h->b.d_mmats, tiles, ntiles, h->b.grad, h->b.m, mu, nest, h->b.minv,
+                               h->b.mX[0], stream);
   });
   if (e != hipSuccess) return e;
   static const float kA = 3.4445f, kB = -4.7750f, kC = 2.0315f;
   auto ns = [&](const Launch& ln, OpKind bk, float alpha, float beta, bool sym) {
-    GemmArgs g = base;
-    g.tiles += ln.tile0;
-    g.ntiles = ln.ntiles;
-    g.tile_set = h->ns_tiles;
-    g.ns_alpha = alpha;
-    g.ns_beta = beta;
-    g.ns_sym = sym ? 1 : 0;
+    GemmArgs ga = base;
+    ga.tiles += ln.tile0;
+    ga.ntiles = ln.ntiles;
+    ga.tile_set = h->ns_tiles;
+    ga.ns_alpha = alpha;
+    ga.ns_beta = beta;
+    ga.ns_sym = sym ? 1 : 0;
     return timed(h, gemm_name(h->prec, OP_KMAJ, bk, EPI_NS), 0, ln.flops, ln.bytes, stream,
-                 [&] { return launch_gemm(h->prec, OP_KMAJ, bk, EPI_NS, g, stream); });
+                 [&] { return launch_gemm(h->prec, OP_KMAJ, bk, EPI_NS, ga, stream); });
   };
   for (int it = 0; it < h->ns_steps; ++it) {
     const int par = it & 1;
-    if ((e = ns(h->nsA[par], OP_KMAJ, 0.0f, 1.0f, true)) != hipSuccess) return e;
-    if ((e = ns(h->nsB, OP_KMAJ, kB, kC, true)) != hipSuccess) return e;
-    if ((e = ns(h->nsX[par], OP_RMAJ, kA, 1.0f, false)) != hipSuccess) return e;
+    if ((e = ns(h->nsA[par][g], OP_KMAJ, 0.0f, 1.0f, true)) != hipSuccess) return e;
+    if ((e = ns(h->nsB[g], OP_KMAJ, kB, kC, true)) != hipSuccess) return e;
+    if ((e = ns(h->nsX[par][g], OP_RMAJ, kA, 1.0f, false)) != hipSuccess) return e;
   }
   return timed(h, "muon_update", 1, 0.0, wbytes * (8.0 + h->elt() + (h->prec == Prec::BF16 ? 2.0 : 0.0)), stream,
                [&] {
-                 return launch_muon_update(h->prec, h->b.d_mmats, h->b.d_mtiles, h->n_mtiles, h->b.theta,
-                                           h->b.shadow, h->b.mX[h->ns_steps & 1], stream);
+                 return launch_muon_update(h->prec, h->b.d_mmats, tiles, ntiles, h->b.theta, h->b.shadow,
+                                           h->b.mX[h->ns_steps & 1], stream);
                });
 }
 
@@ -1621,8 +1635,9 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW), 1, h->dw[hf][l - 1].flops,
                     h->dw[hf][l - 1].bytes, s, [&] { return launch_gemm(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW, al, s); }));
     }
+  if (h->muon)
+    for (int hf = 0; hf < ng; ++hf) HIP_TRY(muon_step(h, a, hf, hs[hf]));
   HIP_TRY(merge());
-  if (h->muon) HIP_TRY(muon_step(h, a, stream));
   double naux = 0;
   for (int k : h->active_ids) {
     const Member& m = h->mem[k];
