@@ -837,13 +837,28 @@ __device__ __forceinline__ void dw_adamw_small(const GemmArgs& a, const GemmDesc
   float* th_p = a.theta + d.poff;
   float* m_p = a.am + d.poff;
   float* v_p = a.av + d.poff;
+  f32x4 th[kAdamAhead], m[kAdamAhead], vv[kAdamAhead];
 #pragma unroll 1
   for (int pass = 0; pass < NPASS; ++pass) {
     const int prow0 = pass * kDwPassRows;  // first tile row of this pass
+    const int64_t e0 = (int64_t)(t.m0 + prow0 + r0) * d.ldc + t.n0 + c;  // element offset of vector 0
+    auto ok = [&](int u) { return colok && prow0 + 8 * u + r0 < mrows; };
+    auto load = [&](int u) {
+      const int64_t e = e0 + u * estep;
+      if (ok(u)) {
+        th[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(th_p + e));
+        m[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(m_p + e));
+        vv[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(v_p + e));
+      }
+    };
     if (pass > 0) {
       wait_vm<63, true>();
       bar();  // every thread is done reading the previous pass
     }
+    // the first vectors' optimizer state is requested before the gradient
+    // tile is staged, so its latency overlaps the staging and the barrier
+#pragma unroll
+    for (int u = 0; u < kAdamAhead; ++u) load(u);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -854,21 +869,8 @@ __device__ __forceinline__ void dw_adamw_small(const GemmArgs& a, const GemmDesc
           const int col = wn * 64 + 32 * j + (lane & 31);
           if (row >= 0 && row < kDwPassRows) *reinterpret_cast<float*>(lds0 + dwt_off(row, col)) = acc[i][j][r];
         }
-    wait_vm<63, true>();  // this wave's LDS writes are done
+    wait_vm<63, true>();  // this wave's LDS writes are done (the state loads may still be in flight)
     bar();
-    const int64_t e0 = (int64_t)(t.m0 + prow0 + r0) * d.ldc + t.n0 + c;  // element offset of vector 0
-    f32x4 th[kAdamAhead], m[kAdamAhead], vv[kAdamAhead];
-    auto ok = [&](int u) { return colok && prow0 + 8 * u + r0 < mrows; };
-    auto load = [&](int u) {
-      const int64_t e = e0 + u * estep;
-      if (ok(u)) {
-        th[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(th_p + e));
-        m[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(m_p + e));
-        vv[u % kAdamAhead] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(v_p + e));
-      }
-    };
-#pragma unroll
-    for (int u = 0; u < kAdamAhead; ++u) load(u);
 #pragma unroll
     for (int u = 0; u < NV; ++u) {
       const int b = u % kAdamAhead;
