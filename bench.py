@@ -150,13 +150,17 @@ def variable_depth(cfg, Xtr, ytr, steps=20):
             "step_ms": round(e0.elapsed_time(e1) / steps, 4), "gemm_work_vs_full_depth": round(work / full, 4)}
 
 
+MUON_OPTS = dict(optimizer="muon", muon_lr_lo=1e-3, muon_lr_hi=1e-1)
+EMB_OPTS = dict(emb_lo=8, emb_hi=32, emb_step=4, sigma_lo=1e-2, sigma_hi=10.0)
+
+
 def muon_optimizer(cfg, Xtr, ytr, steps=20):
     """Step time of the same workload with the paper's default optimizer split:
     Muon for the hidden weights (Newton-Schulz on the grouped GEMMs), AdamW for
     biases and heads; and the Newton-Schulz GEMMs' rate (library events)."""
     import torch
     from paper_2607_05380_amd import tabpack
-    pk = tabpack.Pack(dict(cfg, keep_grads=0, optimizer="muon", muon_lr_lo=1e-3, muon_lr_hi=1e-1)).bind(Xtr.device)
+    pk = tabpack.Pack(dict(cfg, keep_grads=0, **MUON_OPTS)).bind(Xtr.device)
     idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
     pk.train_step(Xtr, ytr, idx, 1, loss)
@@ -193,8 +197,7 @@ def embeddings(cfg, Xtr, ytr, steps=10):
     library's events."""
     import torch
     from paper_2607_05380_amd import tabpack
-    pk = tabpack.Pack(dict(cfg, keep_grads=0, emb_lo=8, emb_hi=32, emb_step=4, sigma_lo=1e-2,
-                           sigma_hi=10.0)).bind(Xtr.device)
+    pk = tabpack.Pack(dict(cfg, keep_grads=0, **EMB_OPTS)).bind(Xtr.device)
     hp = pk.hparams()
     idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
@@ -262,6 +265,9 @@ def main():
     ap.add_argument("--no-per-epoch", action="store_true", help="skip the per-epoch measurements")
     ap.add_argument("--keep-grads", action="store_true",
                     help="also write every gradient out (an inspection aid; the optimizer does not need it)")
+    ap.add_argument("--variant", choices=["adamw", "muon", "embeddings"], default="adamw",
+                    help="the timed step's options: AdamW for everything (the metric), Muon for the hidden "
+                         "weights, or periodic feature embeddings (for profiling those steps on their own)")
     a = ap.parse_args()
     if a.gpus != 1:
         print(f"bench.py measures one GPU: the packed step runs all members on one device and this "
@@ -285,7 +291,8 @@ def main():
                            for s in range(total)]).contiguous()
     # keep_grads=0: hidden-layer weight gradients go straight into the fused
     # AdamW update of the weight-gradient GEMM instead of being stored as well
-    pk = tabpack.Pack(dict(cfg, keep_grads=int(a.keep_grads))).bind(dev)
+    variant = {"adamw": {}, "muon": MUON_OPTS, "embeddings": EMB_OPTS}[a.variant]
+    pk = tabpack.Pack(dict(cfg, keep_grads=int(a.keep_grads), **variant)).bind(dev)
     log(f"bound: workspace {pk.workspace_bytes() / 2**30:.2f} GiB")
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=dev)
     step = 0
@@ -371,7 +378,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": cfg["precision"], "data": "synthetic",
         "config": {"workload": cfg["name"], "K": cfg["K"], "B": cfg["B"], "d_in": cfg["d_in"], "L": cfg["L"],
                    "widths": [cfg["width_lo"], cfg["width_hi"]], "n_train": cfg["n_train"],
-                   "task": cfg["task"], "keep_grads": int(a.keep_grads)},
+                   "task": cfg["task"], "keep_grads": int(a.keep_grads),
+                   **({} if a.variant == "adamw" else {"variant": a.variant})},
         "roofline": roofline,
         "kernels": [{"name": s["name"], "bound": s["kind"], "avg_us": round(s["avg_ms"] * 1e3, 2),
                      "busy_ms_per_step": round(s["busy_ms"] / a.profile_steps, 4),
@@ -389,7 +397,7 @@ def main():
         log(f"  Muon optimizer: {json.dumps(out['muon'])}")
         out["embeddings"] = embeddings(cfg, Xtr, ytr)
         log(f"  periodic embeddings: {json.dumps(out['embeddings'])}")
-    if not a.no_cpu_baseline:
+    if not a.no_cpu_baseline and a.variant == "adamw":
         log("timing the fp64 oracle on the host (bounded sample)")
         out["cpu_baseline"] = cpu_baseline(cfg, Xtr, ytr, idx_all[0])
     print(json.dumps(out), flush=True)
