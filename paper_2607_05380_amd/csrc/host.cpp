@@ -176,6 +176,7 @@ struct pack_handle {
   int member0[kGroups + 1] = {};     // group g's members: d_members[member0[g] .. member0[g+1])
   hipStream_t gstream[kGroups] = {};  // streams of groups 1.. (entry 0 unused)
   hipEvent_t ev_split = nullptr, ev_merge[kGroups] = {};
+  hipEvent_t ev_gather[kGroups] = {};  // group g's gather done (group g + 1 gathers after it)
   int ncoltiles = 0;
   int nheadtiles = 0;
   int head_rb = 0;  // rows per head-backward block
@@ -1382,6 +1383,8 @@ int pack_destroy(pack_handle* h) {
       if (h->ev_merge[g]) (void)hipEventDestroy(h->ev_merge[g]);
       if (h->gstream[g]) (void)hipStreamDestroy(h->gstream[g]);
     }
+    for (hipEvent_t e : h->ev_gather)
+      if (e) (void)hipEventDestroy(e);
   }
   delete h;
   return PACK_OK;
@@ -1421,6 +1424,7 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
       HIP_TRY(hipStreamCreateWithFlags(&h->gstream[g], hipStreamNonBlocking));
       HIP_TRY(hipEventCreateWithFlags(&h->ev_merge[g], hipEventDisableTiming));
     }
+    for (hipEvent_t& e : h->ev_gather) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
   h->keep_ready = 0;
   HIP_TRY(hipMemsetAsync(workspace, 0, need, stream));
@@ -1544,10 +1548,15 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                                 h->b.H0, s);
       }));
     } else {
+      // the groups' gathers (HBM-bound) run one after another, so a group's
+      // forward GEMMs overlap the next group's gather instead of every group
+      // waiting for three concurrent gathers
+      if (hf > 0) HIP_TRY(hipStreamWaitEvent(s, h->ev_gather[hf - 1], 0));
       HIP_TRY(timed(h, "gather", 1, 0.0, (double)gk * c.B * c.d_in * (4.0 + h->elt()), s, [&] {
         return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, gk, h->Bp, h->b.H0,
                              h->b.d_members + h->member0[hf], s);
       }));
+      HIP_TRY(hipEventRecord(h->ev_gather[hf], s));
     }
     HIP_TRY(hipStreamWaitEvent(s, h->ev_keep[par], 0));
   }
