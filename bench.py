@@ -265,6 +265,9 @@ def main():
     ap.add_argument("--no-per-epoch", action="store_true", help="skip the per-epoch measurements")
     ap.add_argument("--keep-grads", action="store_true",
                     help="also write every gradient out (an inspection aid; the optimizer does not need it)")
+    ap.add_argument("--members", type=int, default=0,
+                    help="pack size K (default: the workload's; other values measure packing efficiency, "
+                         "not the metric's configuration)")
     ap.add_argument("--variant", choices=["adamw", "muon", "embeddings"], default="adamw",
                     help="the timed step's options: AdamW for everything (the metric), Muon for the hidden "
                          "weights, or periodic feature embeddings (for profiling those steps on their own)")
@@ -277,7 +280,7 @@ def main():
     import torch
     from paper_2607_05380_amd import configs, synth, tabpack
 
-    cfg = configs.workload(a.workload)
+    cfg = configs.workload(a.workload, **({"K": a.members} if a.members > 0 else {}))
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     log(f"generating {cfg['name']} on device: {cfg['n_train']} x {cfg['d_in']}")
