@@ -175,7 +175,10 @@ int pack_set_active(pack_handle* h, const uint8_t* active, hipStream_t stream);
  * sum of the members' losses, so each member receives exactly its own
  * gradient.
  *   X        device fp32 [N, d_in]; y device fp32 [N] or int32 [N] (CE)
- *   idx      device int32 [K, B], every entry in [0, N)
+ *   idx      device int32 [K, B], every entry in [0, N).  An entry outside
+ *            that range is not an error of the call (the step runs
+ *            asynchronously): the step reads row 0 in its place and raises
+ *            PACK_STATUS_IDX_RANGE, which pack_status() reports.
  *   step     1-based AdamW step t; must be the previous step + 1 (PACK_ESTATE
  *            otherwise).  It is also the dropout counter of this step.
  *   loss_out device fp32 [K]: batch-mean loss of each member before the update
@@ -210,6 +213,21 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
  * snapshots (explicit hyperparameters, pack_set_params) predicts with the
  * ensemble. */
 int pack_predict(pack_handle* h, const float* X, int64_t N, int32_t mode, float* out, hipStream_t stream);
+
+/* Asynchronous error flags raised by the kernels since the last call
+ * (PACK_STATUS_* bits; 0: none): waits for `stream`, returns the flags in
+ * *flags and clears them.  PACK_STATUS_IDX_RANGE: a pack_train_step() batch
+ * index lay outside [0, N). */
+#define PACK_STATUS_IDX_RANGE 1u
+int pack_status(pack_handle* h, uint32_t* flags, hipStream_t stream);
+
+/* Measurement aid: dst <- src over `bytes` (a multiple of 16; both addresses
+ * 16-byte aligned; the ranges must not overlap) with the non-temporal 16-byte
+ * loads and stores of the optimizer epilogues, asynchronously on `stream`.  A
+ * kernel of known HBM traffic (bytes read + bytes written) against which
+ * hardware byte counters and the streaming rate are calibrated.  Allocates
+ * nothing. */
+int pack_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
 /* Scratch bytes pack_select() needs for C candidates over Nv rows. */
 int pack_select_workspace_size(int32_t C, int64_t Nv, size_t* bytes);

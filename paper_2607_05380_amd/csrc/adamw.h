@@ -16,8 +16,8 @@ __device__ __forceinline__ void adamw_elem(float& th, float g, float& m, float& 
                                            const AdamConst& c) {
 #pragma clang fp contract(off)
   th *= decay;
-  m = c.beta1 * m + (1.0f - c.beta1) * g;
-  v = c.beta2 * v + (1.0f - c.beta2) * g * g;
+  m = c.beta1 * m + c.omb1 * g;
+  v = c.beta2 * v + c.omb2 * g * g;
   th -= step * m / (sqrtf(v) / c.bc2_sqrt + c.eps);
 }
 

@@ -132,6 +132,8 @@ struct Bufs {
   MuonTile* d_mtiles = nullptr;
   int32_t* d_mtile0 = nullptr;
   float* headpart = nullptr;  // head backward partials, (Bp / RB) * (d_out + 1) * A / Bp floats
+  int32_t* idx_ok = nullptr;  // the step's batch indices, entries outside [0, N) replaced by 0 [K * B]
+  uint32_t* status = nullptr; // asynchronous error flags (pack_status)
 };
 
 struct pack_handle {
@@ -1086,6 +1088,8 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf) {
   bf.d_members = cv.take<int32_t>(plan.members.size());
   bf.d_active = cv.take<int32_t>(c.K);
   bf.headpart = cv.take<float>((size_t)(h->Bp / head_rows(h)) * (c.d_out + 1) * (h->A / h->Bp));
+  bf.idx_ok = cv.take<int32_t>((size_t)c.K * c.B);
+  bf.status = cv.take<uint32_t>(64);
   return (size_t)round_up((int64_t)cv.off, 256);
 }
 
@@ -1523,6 +1527,11 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                                   h->A / 32, h->b.keepw + (size_t)p * c.L * (h->A / 32), h->b.d_active, h->side);
     });
   };
+  // indices outside [0, N) are replaced (and flagged) before any kernel reads X or y through them
+  HIP_TRY(timed(h, "idx_check", 1, 0.0, 8.0 * c.K * c.B, stream, [&] {
+    return launch_idx_check(idx, (int64_t)c.K * c.B, N, h->b.idx_ok, h->b.status, stream);
+  }));
+  idx = h->b.idx_ok;
   if (h->keep_ready != step) {
     HIP_TRY(hipEventRecord(h->ev_fork, stream));
     HIP_TRY(hipStreamWaitEvent(h->side, h->ev_fork, 0));
@@ -1531,7 +1540,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   }
   const double bc1 = 1.0 - std::pow(c.beta1, (double)step);
   const double bc2 = 1.0 - std::pow(c.beta2, (double)step);
-  const AdamConst ac{(float)c.beta1, (float)c.beta2, (float)c.eps, (float)bc1, (float)std::sqrt(bc2)};
+  const AdamConst ac{(float)c.beta1, (float)c.beta2, (float)c.eps, (float)(1.0 - c.beta1), (float)(1.0 - c.beta2),
+                     (float)bc1, (float)std::sqrt(bc2)};
   // Each member group runs its whole chain -- gather, forward GEMMs, head,
   // loss, backward GEMMs with the fused optimizer -- on its own stream; the
   // groups join before the bias/head AdamW.
@@ -1634,11 +1644,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       al.am = h->b.m;
       al.av = h->b.v;
       al.shadow = h->b.shadow;
-      al.beta1 = ac.beta1;
-      al.beta2 = ac.beta2;
-      al.eps = ac.eps;
-      al.bc1 = ac.bc1;
-      al.bc2_sqrt = ac.bc2_sqrt;
+      al.adam = ac;
       al.keep_grad = c.keep_grads ? 1 : 0;
       // AdamW fused: the weight update traffic dominates, so the HBM roofline applies
       HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW), 1, h->dw[hf][l - 1].flops,
@@ -1647,6 +1653,11 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   if (h->muon)
     for (int hf = 0; hf < ng; ++hf) HIP_TRY(muon_step(h, a, hf, hs[hf]));
   HIP_TRY(merge());
+  // the next step's keep words join the caller's stream too, so that a sync of
+  // that stream (or later work on it, such as a re-plan that rewrites the
+  // member table the keep-word kernel reads) orders after them
+  HIP_TRY(hipEventRecord(h->ev_join, h->side));
+  HIP_TRY(hipStreamWaitEvent(stream, h->ev_join, 0));
   double naux = 0;
   for (int k : h->active_ids) {
     const Member& m = h->mem[k];
@@ -1738,6 +1749,30 @@ int pack_predict(pack_handle* h, const float* X, int64_t N, int32_t mode, float*
       HIP_TRY(launch_ensemble_mean(h->b.dY, nact, h->Bp, a.rows_valid, c.d_out, r0, out, stream));
     }
   }
+  return PACK_OK;
+}
+
+int pack_status(pack_handle* h, uint32_t* flags, hipStream_t stream) {
+  if (!h || !flags) return fail(PACK_EINVAL, "NULL argument");
+  if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
+  uint32_t v = 0;
+  HIP_TRY(hipMemcpyAsync(&v, h->b.status, sizeof(v), hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  if (v) {
+    const uint32_t zero = 0;
+    HIP_TRY(hipMemcpyAsync(h->b.status, &zero, sizeof(zero), hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipStreamSynchronize(stream));
+  }
+  *flags = v;
+  return PACK_OK;
+}
+
+int pack_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
+  if (!src || !dst) return fail(PACK_EINVAL, "NULL device pointer");
+  if (bytes % 16 || reinterpret_cast<uintptr_t>(src) % 16 || reinterpret_cast<uintptr_t>(dst) % 16)
+    return fail(PACK_EINVAL, "bytes and both addresses must be multiples of 16");
+  if (bytes == 0) return PACK_OK;
+  HIP_TRY(launch_stream_copy(src, dst, (int64_t)(bytes / 16), stream));
   return PACK_OK;
 }
 

@@ -436,6 +436,41 @@ __global__ __launch_bounds__(256) void gather_kernel(const float* X, int d_in, i
   }
 }
 
+// -------------------------------------------------------------- idx check --
+// The batch indices come from the caller: every entry outside [0, N) is
+// replaced by row 0 in the copy the step's kernels read, and flags bit 0 of
+// the status word, so that no kernel ever reads outside X or y.  The flag
+// store is predicated on a per-lane condition (a plain vector store; every
+// writer stores the same value).
+__global__ __launch_bounds__(256) void idx_check_kernel(const int32_t* __restrict__ idx, int64_t n, int64_t N,
+                                                        int32_t* __restrict__ out, uint32_t* status) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int32_t v = idx[i];
+  const bool bad = v < 0 || (int64_t)v >= N;
+  out[i] = bad ? 0 : v;
+  if (bad) status[0] = 1u;
+}
+
+// ----------------------------------------------------------- stream copy --
+// dst <- src in 16-byte vectors with non-temporal loads and stores (the
+// access pattern of the optimizer epilogues): a kernel of known HBM traffic
+// for calibrating hardware byte counters and the achievable streaming rate.
+// Each thread keeps four vectors in flight.
+__global__ __launch_bounds__(256) void stream_copy_kernel(const f32x4* __restrict__ src, f32x4* __restrict__ dst,
+                                                          int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  for (; i + 3 * stride < n; i += 4 * stride) {
+    f32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = __builtin_nontemporal_load(src + i + u * stride);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) __builtin_nontemporal_store(v[u], dst + i + u * stride);
+  }
+  for (; i < n; i += stride) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+}
+
 // ------------------------------------------------------------------ AdamW --
 // One wave per 256-element chunk of the packed parameter buffer; every chunk
 // belongs to one member and is all-weight or all-bias, so (lr_k, wd_k) and the
@@ -811,6 +846,20 @@ hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int
   else
     hipLaunchKernelGGL((gather_kernel<float>), grid, dim3(256), 0, s, X, d_in, Pin, idx, B, row_base,
                        rows_valid, Bp, static_cast<float*>(H0), member_ids);
+  return hipGetLastError();
+}
+
+hipError_t launch_idx_check(const int32_t* idx, int64_t n, int64_t N, int32_t* out, uint32_t* status,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(idx_check_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, idx, n, N, out, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_stream_copy(const void* src, void* dst, int64_t n16, hipStream_t s) {
+  // eight workgroups per CU, each thread streaming 16 bytes x 4 per round
+  const int64_t blocks = std::min<int64_t>(grid_for(n16, 256), 256 * 8);
+  hipLaunchKernelGGL(stream_copy_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const f32x4*>(src),
+                     static_cast<f32x4*>(dst), n16);
   return hipGetLastError();
 }
 

@@ -757,9 +757,9 @@ __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmD
   // beside the 128 or 256 of the tall and big tiles
   constexpr int G = MB * NB <= 4 ? S::PER_LANE : 4;
   static_assert(S::PER_LANE % G == 0, "whole groups");
-  const AdamConst ac{a.beta1, a.beta2, a.eps, a.bc1, a.bc2_sqrt};
+  const AdamConst ac = a.adam;
   const float decay = 1.0f - d.lr * d.wd;
-  const float step = d.lr / a.bc1;
+  const float step = d.lr / ac.bc1;
 #pragma unroll 1
   for (int it0 = 0; it0 < S::PER_LANE; it0 += G) {
     f32x4 g[G], th[G], m[G], vv[G];
@@ -826,9 +826,9 @@ __device__ __forceinline__ void dw_adamw_small(const GemmArgs& a, const GemmDesc
   constexpr int NPASS = 128 / kDwPassRows;
   constexpr int NV = kDwPassRows / 8;  // vectors per thread per pass
   const int hv = lane >> 5;
-  const AdamConst ac{a.beta1, a.beta2, a.eps, a.bc1, a.bc2_sqrt};
+  const AdamConst ac = a.adam;
   const float decay = 1.0f - d.lr * d.wd;
-  const float step = d.lr / a.bc1;
+  const float step = d.lr / ac.bc1;
   const int mrows = min(d.M - t.m0, 128), ncols = min(d.N - t.n0, 128);
   // vector u of this thread in a pass: row 8 u + tid / 32 of the pass, columns 4 (tid % 32) .. +3
   const int r0 = tid >> 5, c = (tid & 31) * 4;

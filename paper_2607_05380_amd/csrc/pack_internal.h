@@ -67,6 +67,13 @@ struct Tile {
   int32_t shape;       // kShapeBig or kShapeSmall
 };
 
+struct AdamConst {
+  float beta1, beta2, eps;
+  float omb1, omb2;  // 1 - beta1, 1 - beta2, formed in double precision on the host
+  float bc1;         // 1 - beta1^t
+  float bc2_sqrt;    // sqrt(1 - beta2^t)
+};
+
 struct GemmArgs {
   const GemmDesc* descs;
   const Tile* tiles;
@@ -84,7 +91,7 @@ struct GemmArgs {
   float* am;
   float* av;
   uint16_t* shadow;
-  float beta1, beta2, eps, bc1, bc2_sqrt;
+  AdamConst adam;
   int32_t keep_grad;
   // EPI_NS only: C = ns_alpha * Y + ns_beta * (A B^T), stored in the GEMM precision;
   // with ns_sym the launch holds only tiles on or above the diagonal of a
@@ -105,11 +112,6 @@ struct GemmArgs {
 };
 
 // AdamW constants of one step.
-struct AdamConst {
-  float beta1, beta2, eps;
-  float bc1;       // 1 - beta1^t
-  float bc2_sqrt;  // sqrt(1 - beta2^t)
-};
 
 // Per-member table used by the small kernels.
 struct MemberDev {
@@ -185,6 +187,11 @@ hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, co
 hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
                          int64_t row_base, int rows_valid, int members, int Bp, void* H0,
                          const int32_t* member_ids, hipStream_t s);
+// out[i] = idx[i], or 0 with status[0] = 1 where idx[i] lies outside [0, N)
+hipError_t launch_idx_check(const int32_t* idx, int64_t n, int64_t N, int32_t* out, uint32_t* status,
+                            hipStream_t s);
+// dst <- src, n16 16-byte vectors, non-temporal loads and stores
+hipError_t launch_stream_copy(const void* src, void* dst, int64_t n16, hipStream_t s);
 // shadow: where the bf16 copy of the updated parameters goes, or nullptr for none
 hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, float* v,
                         uint16_t* shadow, const uint32_t* chunk_tab, const uint32_t* list,

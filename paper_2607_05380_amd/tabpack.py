@@ -18,13 +18,15 @@ PACK_OK = 0
 TASKS = {"reg": 0, "bin": 1, "multi": 2}
 PRECISIONS = {"bf16": 0, "fp32": 1}
 PREDICT_MEMBERS, PREDICT_ENSEMBLE = 0, 1
+STATUS_IDX_RANGE = 1
 OPTIMIZERS = {"adamw": 0, "muon": 1}
 
 SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "pack_workspace_size",
            "pack_bind", "pack_train_step", "pack_eval_members", "pack_select_workspace_size",
            "pack_select", "pack_member_param_count", "pack_get_params", "pack_set_params",
            "pack_get_grads", "pack_get_moments", "pack_debug_dropout_mask", "pack_debug_activation",
-           "pack_profile_enable", "pack_profile_read", "pack_set_active", "pack_predict"]
+           "pack_profile_enable", "pack_profile_read", "pack_set_active", "pack_predict", "pack_status",
+           "pack_stream_copy"]
 
 
 class MemberHP(ctypes.Structure):
@@ -100,6 +102,8 @@ def load_library(path=LIB_PATH):
         "pack_profile_read": ([H, ctypes.POINTER(KernelStat), i32, ctypes.POINTER(i32)], ctypes.c_int),
         "pack_set_active": ([H, vp, vp], ctypes.c_int),
         "pack_predict": ([H, vp, i64, i32, vp, vp], ctypes.c_int),
+        "pack_status": ([H, ctypes.POINTER(ctypes.c_uint32), vp], ctypes.c_int),
+        "pack_stream_copy": ([vp, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -222,6 +226,14 @@ class Pack:
         _check(self.lib.pack_train_step(self.h, X.data_ptr(), y.data_ptr(), X.shape[0], idx.data_ptr(),
                                         int(step), loss_out.data_ptr(), _stream()))
         return loss_out
+
+    def status(self):
+        """Asynchronous error flags raised since the last call (waits for the
+        current stream, then clears them): STATUS_IDX_RANGE when a batch index
+        lay outside [0, N)."""
+        flags = ctypes.c_uint32()
+        _check(self.lib.pack_status(self.h, ctypes.byref(flags), _stream()))
+        return flags.value
 
     def set_active(self, active, stream=None):
         """active: K booleans; removed members are frozen and leave the launches."""
@@ -359,3 +371,11 @@ class Pack:
         out = np.empty((self.B, w), dtype=np.float32)
         _check(self.lib.pack_debug_activation(self.h, layer, k, out.ctypes.data))
         return out
+
+
+def stream_copy(src, dst):
+    """dst <- src (device tensors of equal byte size, 16-byte multiples) with the
+    library's non-temporal streaming kernel, on the current stream."""
+    n = src.numel() * src.element_size()
+    assert src.is_cuda and dst.is_cuda and dst.numel() * dst.element_size() == n
+    _check(load_library().pack_stream_copy(src.data_ptr(), dst.data_ptr(), n, _stream()))
