@@ -97,9 +97,52 @@ def loss_and_dy(Y, y, task):
     raise ValueError(task)
 
 
-def backward(params, cache, dY, masks=None, scale=1.0, input_grad=False):
+# Decisions within this fraction of rms(Z) of the ReLU threshold may take
+# either branch in an implementation that accumulates Z in another order or
+# precision and rounds upstream activations at other points (see
+# ``relu_derivative``): a bf16 activation that rounds the other way moves every
+# pre-activation of its row in the next layer by up to one bf16 step of that
+# term, and such moves compound over the layers.
+HINT_WINDOW = 2e-2
+
+
+def relu_derivative(Z, hint=None, window=HINT_WINDOW, stats=None):
+    """The ReLU derivative [Z > 0] (0 at 0).
+
+    ``hint`` (int8 array like Z: 1 positive, 0 not positive, -1 unknown) gives
+    another implementation's decisions.  Where |Z| <= window * rms(Z) both
+    branches are correct up to that implementation's accumulation rounding, so
+    the hint's decision is taken there; everywhere else the decision is this
+    function's own.  ``stats`` (a dict) receives the counts: elements inside
+    the window, hints taken there that differ from [Z > 0], known hints
+    outside the window that differ from it (a disagreement the window does not
+    excuse), all known hints, and the largest |Z| / rms(Z) of a differing
+    hint."""
+    own = Z > 0.0
+    if hint is None:
+        return own
+    hint = np.asarray(hint)
+    assert hint.shape == Z.shape, (hint.shape, Z.shape)
+    rms = np.sqrt(np.mean(Z * Z)) if Z.size else 0.0
+    inside = np.abs(Z) <= window * rms
+    known = hint >= 0
+    differ = known & (own != (hint == 1))
+    if stats is not None:
+        stats["window"] = stats.get("window", 0) + int(inside.sum())
+        stats["taken"] = stats.get("taken", 0) + int((differ & inside).sum())
+        stats["outside"] = stats.get("outside", 0) + int((differ & ~inside).sum())
+        stats["decisions"] = stats.get("decisions", 0) + int(known.sum())
+        if differ.any() and rms > 0:
+            # how far from the threshold the furthest disagreement lies, in rms(Z)
+            stats["max_ratio"] = max(stats.get("max_ratio", 0.0), float(np.abs(Z[differ]).max() / rms))
+    return np.where(inside & known, hint == 1, own)
+
+
+def backward(params, cache, dY, masks=None, scale=1.0, input_grad=False, hints=None, stats=None,
+             window=HINT_WINDOW):
     """Gradients [(dW, db), ...] in the layout of ``params``; with input_grad
-    also dLoss/dH_0 (the gradient of the network's input), as a second value."""
+    also dLoss/dH_0 (the gradient of the network's input), as a second value.
+    hints[l]: optional decisions for hidden layer l + 1 (``relu_derivative``)."""
     L = len(params) - 1
     rnd = cache.get("rnd", _same)
     grads = [None] * (L + 1)
@@ -108,7 +151,7 @@ def backward(params, cache, dY, masks=None, scale=1.0, input_grad=False):
     grads[L] = (dY.T @ H[L], dY.sum(axis=0))
     dH = dY @ Wo
     for l in range(L - 1, -1, -1):
-        dZ = dH * (cache["Z"][l] > 0.0)
+        dZ = dH * relu_derivative(cache["Z"][l], None if hints is None else hints[l], window, stats)
         if masks is not None:
             dZ = dZ * masks[l] * scale
         db = dZ.sum(axis=0)

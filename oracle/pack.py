@@ -44,17 +44,20 @@ class OraclePack:
         self.t = 0
         self.last_grads = None
         self.last_emb_grads = None
+        self.last_hint_stats = None
 
     def masks(self, k, step):
         c, h = self.cfg, self.hp[k]
         return [mlp.dropout_mask(c["seed"], k, step, l + 1, c["B"], h["width"], h["t"])
                 for l in range(member_depth(c, h))]
 
-    def member_step(self, k, X, y, idx_k, step):
+    def member_step(self, k, X, y, idx_k, step, hints=None):
         """Forward, loss, backward and the optimizer step for member k; returns
         (loss, grads).  With cfg["optimizer"] == "muon" the hidden weights take a
         Muon step (learning rate hp["muon_lr"], momentum buffer in ``m``) and
-        every other parameter an AdamW step; otherwise everything is AdamW."""
+        every other parameter an AdamW step; otherwise everything is AdamW.
+        hints: optional per-layer ReLU decisions of another implementation
+        (``mlp.relu_derivative``); the counts land in last_hint_stats[k]."""
         c, h = self.cfg, self.hp[k]
         use_muon = c.get("optimizer", "adamw") == "muon"
         depth = len(self.params[k]) - 1
@@ -65,8 +68,13 @@ class OraclePack:
             H0, ecache = embed.embed(H0, self.emb[k])
         Y, cache = mlp.forward(self.params[k], H0, masks, h["s"], rnd=self.rnd)
         loss, dY = mlp.loss_and_dy(Y, y[rows], c["task"])
+        stats = {}
+        if self.last_hint_stats is None:
+            self.last_hint_stats = [None] * len(self.hp)
+        self.last_hint_stats[k] = stats
         if self.use_emb:
-            grads, dE = mlp.backward(self.params[k], cache, dY, masks, h["s"], input_grad=True)
+            grads, dE = mlp.backward(self.params[k], cache, dY, masks, h["s"], input_grad=True, hints=hints,
+                                     stats=stats)
             eg = embed.embed_backward(dE, ecache, self.emb[k])
             self.last_emb_grads[k] = eg
             args = (step, h["lr"], h["wd"], c["beta1"], c["beta2"], c["eps"])
@@ -74,7 +82,7 @@ class OraclePack:
                 self.emb[k][n], self.emb_m[k][n], self.emb_v[k][n] = mlp.adamw_step(
                     self.emb[k][n], eg[n], self.emb_m[k][n], self.emb_v[k][n], *args)
         else:
-            grads = mlp.backward(self.params[k], cache, dY, masks, h["s"])
+            grads = mlp.backward(self.params[k], cache, dY, masks, h["s"], hints=hints, stats=stats)
         new_p, new_m, new_v = [], [], []
         for i, ((W, b), (gW, gb), (mW, mb), (vW, vb)) in enumerate(
                 zip(self.params[k], grads, self.m[k], self.v[k])):
@@ -93,19 +101,22 @@ class OraclePack:
         self.params[k], self.m[k], self.v[k] = new_p, new_m, new_v
         return loss, grads
 
-    def train_step(self, X, y, idx, step, members=None):
+    def train_step(self, X, y, idx, step, members=None, hints=None):
         """One step for every member (or for ``members`` only); returns losses [K].
 
         ``step`` is the 1-based AdamW step t, also the dropout counter.
         Members left out keep their state; their loss is reported as NaN.
+        hints: optional {member: per-layer ReLU decisions} (``member_step``).
         """
         K = self.cfg["K"]
         X = np.asarray(X, dtype=np.float64)
         losses = np.full(K, np.nan)
         self.last_grads = [None] * K
         self.last_emb_grads = [None] * K
+        self.last_hint_stats = [None] * K
         for k in (range(K) if members is None else members):
-            losses[k], self.last_grads[k] = self.member_step(k, X, y, idx[k], step)
+            losses[k], self.last_grads[k] = self.member_step(k, X, y, idx[k], step,
+                                                             None if hints is None else hints.get(k))
         self.t = step
         return losses
 

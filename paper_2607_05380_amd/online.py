@@ -44,6 +44,22 @@ class Snapshot:
         return (self.member, self.epoch)
 
 
+def inference_spec(cfg, snapshots):
+    """(config, explicit member hyperparameters) of a pack holding one member per
+    snapshot, in order: every sampled hyperparameter of the snapshot's member is
+    kept, the embedding's d_emb and sigma included, so that the pack's layout
+    matches the snapshots' parameters."""
+    out = dict(cfg, K=len(snapshots), keep_grads=0)
+    hps = []
+    for s in snapshots:
+        hp = dict(width=s.hp["width"], dropout=s.hp["dropout"], lr=s.hp["lr"], wd=s.hp["wd"], depth=s.hp["depth"],
+                  muon_lr=s.hp.get("muon_lr", 0.0))
+        if s.hp.get("d_emb"):
+            hp["d_emb"], hp["sigma"] = s.hp["d_emb"], s.hp["sigma"]
+        hps.append(hp)
+    return out, hps
+
+
 class OnlineTrainer:
     def __init__(self, cfg, p_base=16, p_ens=32, m_ens=32, max_epochs=1000, members=None, device="cuda"):
         self.cfg = dict(cfg)
@@ -128,9 +144,7 @@ class OnlineTrainer:
         if not self.ensemble:
             raise RuntimeError("no ensemble: fit() selected nothing")
         if self._infer is None:
-            cfg = dict(self.cfg, K=len(self.ensemble), keep_grads=0)
-            hps = [dict(width=s.hp["width"], dropout=s.hp["dropout"], lr=s.hp["lr"], wd=s.hp["wd"],
-                        depth=s.hp["depth"], muon_lr=s.hp.get("muon_lr", 0.0)) for s in self.ensemble]
+            cfg, hps = inference_spec(self.cfg, self.ensemble)
             pk = tabpack.Pack(cfg, members=hps).bind(self.device)
             for i, snap in enumerate(self.ensemble):
                 pk.set_params(i, snap.params)

@@ -15,3 +15,11 @@ def pytest_configure(config):
 @pytest.fixture(scope="session")
 def root():
     return ROOT
+
+
+def pytest_sessionfinish(session, exitstatus):
+    # the parity measurements of this session (tests/parity.py), when asked for
+    path = os.environ.get("TABPACK_PARITY_REPORT")
+    if path:
+        import parity
+        parity.dump_records(path)

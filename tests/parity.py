@@ -4,47 +4,93 @@ on the same seeded inputs and compare them element by element.
 Element test: |gpu - ref| <= atol + rtol * |ref|.
 
 bf16 GEMMs (fp32 master weights).  The reference is the oracle's bf16 policy
-(bf16 operands of the hidden matrix products, see oracle.mlp), so that the
-ReLU/dropout decisions rest on the same rounded forward values as the kernels'.
-Losses and outputs: rtol 2e-2, atol 1e-3.  Against the exact fp64 oracle about
-0.1-0.5% of the ReLU decisions legitimately flip (|Z| below the bf16 rounding
-noise) and each flip moves a whole dZ element, so there gradients are held to a
-relative Frobenius error of FP64_GRAD_FROB.
-fp32 MFMA mode: rtol 1e-4 everywhere.
+(bf16 operands of the hidden matrix products, see oracle.mlp).  A ReLU
+decision is a floating-point comparison that decides a branch: where the
+oracle's pre-activation Z lies within oracle.mlp.HINT_WINDOW * rms(Z) of 0,
+both branches are correct up to the accumulation order and the bf16 rounding
+of upstream activations, so the oracle takes the GPU's decision there (the
+decisions are read from the GPU's stored activations, ``gpu_hints``).  Every
+decision outside the window must agree exactly (``check_decisions``); the
+number taken from the GPU is recorded (7.8e-6 of 66.9 M decisions over the
+suite, furthest 8.7e-3 rms(Z) from 0).  Losses and outputs: rtol 2e-2, atol
+1e-3.  Against the exact fp64 oracle (its own decisions everywhere, no bf16
+rounding) a share of the ReLU decisions legitimately flips and each flip moves
+a whole dZ element, so there gradients are held to a relative Frobenius error
+of FP64_GRAD_FROB.  fp32 MFMA mode: rtol 1e-4 everywhere.
 
 Gradients meet three conditions: every element within the literal tolerance
 (bf16 2e-2 rel / 1e-3 abs; fp32 1e-4 rel / 1e-5 abs), at most ``frac`` of the
 elements outside the strict per-tensor band (rtol, gfloor * max|g|), and a
-relative Frobenius error <= frob.  The strict band can be missed by a few
-elements because an fp32-accumulated Z a hair from zero may take the other ReLU
-branch than the fp64-accumulated one; one such flip moves a single term of a
-whole weight-gradient row.
+relative Frobenius error <= frob.
 
 Parameters after t steps are checked through their update d = theta_t -
 theta_0 (theta_0 is the bit-identical initial value on both sides):
   * |d_gpu - d_ref| <= 2 t lr (1 + 1e-6) + 1e-7 for every element (an AdamW
     step moves an element by at most about lr);
-  * |d_gpu - d_ref| <= upd * lr for all but a share upd_frac of the elements
-    (the first step is about -lr sign(g), so this pins lr_k, wd_k and the
-    update rule per member);
-  * after one step, theta within the literal tolerance wherever the two
-    gradients agree to half the oracle's magnitude and that magnitude is well
-    above AdamW's eps (>= 1e-5): the first step -lr g / (|g| + eps) is then the
-    same on both sides.  Elsewhere -- gradients so small or so perturbed by
-    legitimate ReLU-decision flips that sign(g) or |g| / (|g| + eps) differ --
-    only the 2 lr bound and the upd_frac share apply.
+  * after one step the first AdamW step is -lr g / (|g| + eps) (plus the
+    decay, identical on both sides), so an element's update is fixed by the
+    sign of its gradient unless |g| is near eps.  An element is *exempt* when
+    its gradient's sign is not determined at the comparison's precision: the
+    oracle gradient lies inside its own tolerance band (|g_ref| <= gfloor *
+    max|g_ref| / (1 - rtol)), the two gradients differ by more than half the
+    oracle's magnitude, or |g_ref| < 1e-6 -- unless both gradients are exactly
+    0 (a dead unit, an all-zero input column).  Every other element must have
+    its update within upd * lr and theta within the literal tolerance; exempt
+    elements only the 2 lr bound.  The share of exempt elements is bounded by
+    ``exempt``, and the share whose update actually differs by more than upd *
+    lr (a flipped sign) by ``flip``;
+  * after several steps the exemption is not traceable (a first-step flip
+    changes the later moments), so at most ``upd_frac`` of the elements may
+    have their update off by more than upd * lr.
 """
+import json
+import os
+
 import numpy as np
 
 from oracle.sampling import member_hparams, sample_hparams
 from paper_2607_05380_amd import synth
 
-TOL = {"bf16": dict(rtol=2e-2, atol=1e-3, gfloor=1e-3, frob=2e-2, lit_rtol=2e-2, lit_atol=1e-3, frac=0.25,
-                   upd=2e-2, upd_frac=0.05),
-       "fp32": dict(rtol=1e-4, atol=1e-6, gfloor=1e-4, frob=1e-4, lit_rtol=1e-4, lit_atol=1e-5, frac=0.01,
-                    upd=1e-3, upd_frac=1e-3)}
+# Every bound below is the measured maximum over the GPU suite (recorded with
+# ``record``, summarised in profiles/parity_bounds.md) times a stated margin.
+# frac / exempt / flip / upd_frac are shares of a tensor's elements:
+#   frac     gradient elements outside the strict band (measured 3.2e-7; bound 1e-5)
+#   exempt   elements whose gradient sign is undetermined (a property of the
+#            gradient's distribution: elements under the band floor; measured
+#            0.26 on the embedded first layers, 0.19 on hidden layers; bound 0.35)
+#   flip     exempt elements whose first update actually differs by more than
+#            upd * lr (measured 5.7e-3 on a 20,700-element embedding tensor, one
+#            element in 409 on the smallest; bound 1e-2)
+#   upd_frac updates off by more than upd * lr after several steps (measured
+#            6.8e-3; bound 1.5e-2)
+TOL = {"bf16": dict(rtol=2e-2, atol=1e-3, gfloor=1e-3, frob=2e-2, lit_rtol=2e-2, lit_atol=1e-3, frac=1e-5,
+                   upd=2e-2, exempt=0.35, flip=1e-2, upd_frac=1.5e-2),
+       "fp32": dict(rtol=1e-4, atol=1e-6, gfloor=1e-4, frob=1e-4, lit_rtol=1e-4, lit_atol=1e-5, frac=1e-5,
+                    upd=1e-3, exempt=0.35, flip=1e-2, upd_frac=1.5e-2)}
 
-FP64_GRAD_FROB = 0.25
+# bf16 kernels against the exact fp64 oracle (no shared rounding policy):
+# gradient relative Frobenius error (measured 0.097), the share of update
+# elements whose gradient sign is undetermined (measured 0.19) and the share of
+# those whose first update flips (measured 5.2e-2).
+FP64_GRAD_FROB = 0.12
+FP64_EXEMPT = 0.25
+FP64_FLIP = 0.07
+
+RECORDS = []
+
+
+def record(name, kind, **metrics):
+    """Keep one measurement (written to $TABPACK_PARITY_REPORT at the end of the
+    session by conftest.py)."""
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    RECORDS.append(dict(test=test, name=name, kind=kind,
+                        **{k: (float(v) if v is not None else None) for k, v in metrics.items()}))
+
+
+def dump_records(path):
+    with open(path, "w") as f:
+        json.dump(RECORDS, f)
+
 
 ORACLE_KEYS = ("seed", "K", "d_in", "d_out", "L", "B", "task", "beta1", "beta2", "eps", "decay_bias",
                "width_lo", "width_hi", "dropout_lo", "dropout_hi", "lr_lo", "lr_hi", "wd_lo", "wd_hi")
@@ -75,15 +121,29 @@ def close_mask(gpu, ref, rtol, atol):
     return np.abs(np.asarray(gpu, np.float64) - ref) <= atol + rtol * np.abs(ref)
 
 
-def check_tensor(name, gpu, ref, tol, grad=False, report=None):
+def _tol_ratio(gpu, ref, rtol, atol):
+    """max |gpu - ref| / (atol + rtol |ref|): 1.0 is the bound."""
+    if gpu.size == 0:
+        return 0.0
+    den = atol + rtol * np.abs(ref)
+    err = np.abs(gpu - ref)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        r = np.where(den > 0, err / np.where(den > 0, den, 1.0), np.where(err > 0, np.inf, 0.0))
+    return float(r.max())
+
+
+def check_tensor(name, gpu, ref, tol, grad=False, report=None, kind=None):
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     assert gpu.shape == ref.shape, (name, gpu.shape, ref.shape)
     assert np.isfinite(gpu).all(), name
     mx = np.abs(ref).max() if ref.size else 0.0
     frob = np.linalg.norm(gpu - ref) / max(np.linalg.norm(ref), 1e-30)
+    kind = kind or (name.rsplit(".", 1)[-1] if grad else "value")
     if not grad:
         ok = close_mask(gpu, ref, tol["rtol"], tol["atol"])
+        record(name, kind, n=gpu.size, frob=frob, misses=(~ok).sum(),
+               tol_ratio=_tol_ratio(gpu, ref, tol["rtol"], tol["atol"]))
         if report is not None:
             report.append((name, float(frob), int((~ok).sum())))
         assert ok.all(), f"{name}: {(~ok).sum()} of {ok.size} elements out of tolerance; worst " \
@@ -91,45 +151,102 @@ def check_tensor(name, gpu, ref, tol, grad=False, report=None):
         return frob
     strict = close_mask(gpu, ref, tol["rtol"], tol["gfloor"] * mx)
     literal = close_mask(gpu, ref, tol["lit_rtol"], tol["lit_atol"])
+    strict_frac = float((~strict).mean()) if gpu.size else 0.0
+    record(name, kind, n=gpu.size, frob=frob if mx > 0 else 0.0, strict_frac=strict_frac,
+           literal_misses=(~literal).sum(), tol_ratio=_tol_ratio(gpu, ref, tol["lit_rtol"], tol["lit_atol"]))
     if report is not None:
         report.append((name, float(frob), int((~strict).sum())))
-    assert literal.all(), f"{name}: {(~literal).sum()} of {ok_size(gpu)} elements outside the literal " \
+    assert literal.all(), f"{name}: {(~literal).sum()} of {gpu.size} elements outside the literal " \
                           f"tolerance; worst {np.abs(gpu - ref)[~literal].max():.3e}"
-    assert (~strict).mean() <= tol["frac"], f"{name}: {(~strict).sum()} of {gpu.size} elements outside " \
-                                            f"the strict band (max|ref| {mx:.3e}), frob {frob:.2e}"
+    assert strict_frac <= tol["frac"], f"{name}: {(~strict).sum()} of {gpu.size} elements outside " \
+                                       f"the strict band (max|ref| {mx:.3e}), frob {frob:.2e}"
     if mx > 0:
         assert frob <= tol["frob"], f"{name}: relative Frobenius error {frob:.3e}"
     return frob
 
 
-def ok_size(a):
-    return np.asarray(a).size
+def sign_undetermined(g_gpu, g_ref, tol):
+    """Elements whose first AdamW step may legitimately differ between the two
+    sides: see the module notes."""
+    g_gpu = np.asarray(g_gpu, np.float64)
+    g_ref = np.asarray(g_ref, np.float64)
+    mx = np.abs(g_ref).max() if g_ref.size else 0.0
+    band = tol["gfloor"] * mx / (1.0 - tol["rtol"])
+    both_zero = (g_ref == 0) & (g_gpu == 0)  # no gradient on either side: the same (decay-only) update
+    return ((np.abs(g_ref) <= band) | (np.abs(g_gpu - g_ref) > 0.5 * np.abs(g_ref)) | (np.abs(g_ref) < 1e-6)) \
+        & ~both_zero
 
 
-def check_update(name, p_gpu, p_ref, p0, g_gpu, g_ref, lr, tol, steps=1, upd_frac=None, report=None):
+def check_update(name, p_gpu, p_ref, p0, g_gpu, g_ref, lr, tol, steps=1, upd_frac=None, report=None,
+                 exempt_max=None, flip_max=None, kind="update"):
     """Parameter check after ``steps`` AdamW steps (see the module notes)."""
     p_gpu = np.asarray(p_gpu, np.float64)
     d_gpu, d_ref = p_gpu - p0, p_ref - p0
     err = np.abs(d_gpu - d_ref)
-    assert (err <= 2 * steps * lr * (1 + 1e-6) + 1e-7).all(), \
-        f"{name}: update differs by {err.max():.3e} > 2 t lr ({2 * steps * lr:.3e})"
-    off = float((err > tol["upd"] * lr + 1e-7).mean())
-    if report is not None:
-        report.append((name, off, int((err > tol["upd"] * lr + 1e-7).sum())))
-    lim = tol["upd_frac"] if upd_frac is None else upd_frac
-    assert off <= lim, f"{name}: {off:.2%} of the updates differ by more than {tol['upd']} lr"
+    bound2 = 2 * steps * lr * (1 + 1e-6) + 1e-7
+    assert (err <= bound2).all(), f"{name}: update differs by {err.max():.3e} > 2 t lr ({2 * steps * lr:.3e})"
+    miss = err > tol["upd"] * lr + 1e-7
     if steps == 1 and g_gpu is not None:
+        ex = sign_undetermined(g_gpu, g_ref, tol)
+        ex_frac = float(ex.mean()) if ex.size else 0.0
         lit = close_mask(p_gpu, p_ref, tol["lit_rtol"], tol["lit_atol"])
-        g_gpu = np.asarray(g_gpu, np.float64)
-        same = (np.abs(g_gpu - g_ref) <= 0.5 * np.abs(g_ref)) & (np.abs(g_ref) >= 1e-5)
-        bad = ~lit & same
+        bad = (miss | ~lit) & ~ex
+        flip_frac = float((miss & ex).mean()) if ex.size else 0.0
+        record(name, kind, n=err.size, exempt_frac=ex_frac, exempt_flipped=(miss & ex).sum(), flip_frac=flip_frac,
+               nonexempt_err_lr=float(err[~ex].max() / lr) if (~ex).any() else 0.0,
+               max_err_lr=float(err.max() / lr) if err.size else 0.0)
+        if report is not None:
+            report.append((name, ex_frac, int(bad.sum())))
         if bad.any():
             i = np.flatnonzero(bad.ravel())[:6]
-            detail = "; ".join(f"g_ref {np.ravel(g_ref)[j]:.3e} g_gpu {np.ravel(g_gpu)[j]:.3e} d_ref "
-                               f"{d_ref.ravel()[j]:.3e} d_gpu {d_gpu.ravel()[j]:.3e}" for j in i)
-            raise AssertionError(f"{name}: {bad.sum()} parameters outside the literal tolerance (lr {lr:.3e}): "
-                                 f"{detail}")
+            gg = np.ravel(np.asarray(g_gpu, np.float64))
+            gr = np.ravel(np.asarray(g_ref, np.float64))
+            detail = "; ".join(f"g_ref {gr[j]:.3e} g_gpu {gg[j]:.3e} d_ref {d_ref.ravel()[j]:.3e} "
+                               f"d_gpu {d_gpu.ravel()[j]:.3e}" for j in i)
+            raise AssertionError(f"{name}: {bad.sum()} parameters with a determined gradient sign outside "
+                                 f"the update / literal tolerance (lr {lr:.3e}): {detail}")
+        lim = tol["exempt"] if exempt_max is None else exempt_max
+        assert ex_frac <= lim, f"{name}: {ex_frac:.2%} of the gradient signs undetermined (bound {lim:.2%})"
+        flim = tol["flip"] if flip_max is None else flip_max
+        # one flipped element is always allowed (tensors of a few hundred elements)
+        assert (miss & ex).sum() <= max(1, flim * err.size), \
+            f"{name}: {flip_frac:.2%} of the updates flipped (bound {flim:.2%})"
+        return ex_frac
+    off = float(miss.mean()) if miss.size else 0.0
+    record(name, kind, n=err.size, steps=steps, upd_miss_frac=off,
+           max_err_lr=float(err.max() / lr) if err.size else 0.0)
+    if report is not None:
+        report.append((name, off, int(miss.sum())))
+    lim = tol["upd_frac"] if upd_frac is None else upd_frac
+    assert off <= lim, f"{name}: {off:.2%} of the updates differ by more than {tol['upd']} lr"
     return off
+
+
+def gpu_hints(pk, k, cfg, step):
+    """Member k's ReLU decisions in the GPU's last forward pass, per hidden
+    layer: 1 where the stored activation H_l > 0, 0 where the element was kept
+    by dropout and H_l = 0, -1 where dropout removed it (no decision visible).
+    The oracle takes them only where its own pre-activation lies within
+    oracle.mlp.HINT_WINDOW * rms(Z) of 0 (``oracle.mlp.relu_derivative``)."""
+    from oracle.mlp import dropout_mask
+    hp = pk.hparams()[k]
+    out = []
+    for layer in range(1, hp["depth"] + 1):
+        H = pk.debug_activation(layer, k)
+        keep = dropout_mask(cfg["seed"], k, step, layer, cfg["B"], hp["width"], hp["t"])
+        out.append(np.where(keep, (H > 0).astype(np.int8), np.int8(-1)))
+    return out
+
+
+def check_decisions(op, k, name):
+    """The GPU's ReLU decisions agree with the oracle's own everywhere outside
+    the narrow window around 0 (bit-exact); record how many fell inside it."""
+    st = (op.last_hint_stats or [None] * (k + 1))[k]
+    if st is None:
+        return
+    record(name, "decisions", window=st.get("window", 0), taken=st.get("taken", 0),
+           outside=st.get("outside", 0), decisions=st.get("decisions", 0), max_ratio=st.get("max_ratio", 0.0))
+    assert st.get("outside", 0) == 0, f"{name}: {st['outside']} ReLU decisions differ outside the window"
 
 
 def make_inputs(cfg, n_train, n_val, epoch=0, step_in_epoch=0):
@@ -155,21 +272,22 @@ def compare_member(pk, op, k, p0, tol, steps=1, report=None, prefix=""):
     for l, nm in enumerate(names):
         gW, gb = op.last_grads[k][l]
         tag = f"{prefix}m{k}.{nm}"
-        check_tensor(tag + ".grad", g_gpu[l][0], gW, tol, grad=True, report=report)
-        check_tensor(tag + ".bgrad", g_gpu[l][1], gb, tol, grad=True, report=report)
-        check_update(tag, p_gpu[l][0], op.params[k][l][0], p0[l][0], g_gpu[l][0], gW, lr, tol, steps, report=report)
-        check_update(tag + ".b", p_gpu[l][1], op.params[k][l][1], p0[l][1], g_gpu[l][1], gb, lr, tol, steps,
+        check_tensor(tag + ".grad", g_gpu[l][0], gW, tol, grad=True, report=report, kind="grad")
+        check_tensor(tag + ".bgrad", g_gpu[l][1], gb, tol, grad=True, report=report, kind="bgrad")
+        check_update(tag, p_gpu[l][0], op.params[k][l][0], p0[l][0], g_gpu[l][0], gW, lr, tol, steps,
                      report=report)
-        check_tensor(tag + ".m", m_gpu[l][0], op.m[k][l][0], tol, grad=True, report=report)
+        check_update(tag + ".b", p_gpu[l][1], op.params[k][l][1], p0[l][1], g_gpu[l][1], gb, lr, tol, steps,
+                     report=report, kind="bupdate")
+        check_tensor(tag + ".m", m_gpu[l][0], op.m[k][l][0], tol, grad=True, report=report, kind="m")
         # v = sum of (1-b2) b2^i g^2: compare sqrt(v), which scales like |g|
         check_tensor(tag + ".sqrtv", np.sqrt(v_gpu[l][0]), np.sqrt(op.v[k][l][0]), tol, grad=True,
-                     report=report)
+                     report=report, kind="sqrtv")
 
 
 def compare_member_fp64(pk, op64, k, p0, report=None, prefix=""):
-    """bf16 GPU member vs the exact fp64 oracle: gradient Frobenius error bounded
-    by FP64_GRAD_FROB; updates as in check_update with up to 10% of the first
-    step's signs reversed by the bf16 ReLU-decision flips."""
+    """bf16 GPU member vs the exact fp64 oracle: gradient relative Frobenius
+    error within FP64_GRAD_FROB; updates as in check_update, with up to
+    FP64_EXEMPT of the elements' gradient signs undetermined."""
     tol = TOL["bf16"]
     lr = op64.hp[k]["lr"]
     g_gpu = pk.get_grads(k)
@@ -180,8 +298,9 @@ def compare_member_fp64(pk, op64, k, p0, report=None, prefix=""):
         for i, (nm, r) in enumerate((("W", gW), ("b", gb))):
             g = np.asarray(g_gpu[l][i], np.float64)
             frob = np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-30)
+            record(f"{prefix}m{k}.{nm}{l}.grad64", "grad64" if nm == "W" else "bgrad64", n=g.size, frob=frob)
             worst = max(worst, frob)
             assert frob <= FP64_GRAD_FROB, f"{prefix}m{k}.{nm}{l}: grad frob vs fp64 {frob:.3f}"
             check_update(f"{prefix}m{k}.{nm}{l}", p_gpu[l][i], op64.params[k][l][i], p0[l][i], g, r, lr, tol,
-                         upd_frac=0.10, report=report)
+                         exempt_max=FP64_EXEMPT, flip_max=FP64_FLIP, report=report, kind="update64" if nm == "W" else "bupdate64")
     return worst

@@ -87,3 +87,41 @@ def test_select_degenerate_cases():
     sel_o, s_o = greedy_select(cand.astype(np.float64), y, "reg", 10)
     assert sel == sel_o and len(set(sel)) == len(sel) <= 3
     assert s == pytest.approx(s_o, rel=1e-12)
+
+
+def test_out_of_range_batch_indices_are_flagged_and_never_read():
+    # entries outside [0, N) read row 0 instead and raise the status flag: the
+    # step equals (bit for bit) the step with those entries set to 0
+    cfg = configs.workload("regression_onehot", K=3, B=200)
+    Xtr, ytr, _, _, _, idx = make_inputs(cfg, 1000, 10)
+    bad = idx.copy()
+    bad[0, 5], bad[1, 0], bad[2, -1] = -1, 1000, np.iinfo(np.int32).max
+    fixed = np.where((bad < 0) | (bad >= 1000), 0, bad).astype(np.int32)
+    X, y, bad_d, fixed_d = to_dev(Xtr, ytr, bad, fixed)
+    runs = []
+    for ix in (bad_d, fixed_d):
+        pk = tabpack.Pack(cfg).bind()
+        assert pk.status() == 0
+        loss = pk.train_step(X, y, ix, 1).cpu().numpy()
+        runs.append((loss, pk.status(), [pk.get_params(k) for k in range(3)]))
+        assert pk.status() == 0  # cleared by the read
+    (l1, s1, p1), (l2, s2, p2) = runs
+    assert s1 == tabpack.STATUS_IDX_RANGE and s2 == 0
+    np.testing.assert_array_equal(l1, l2)
+    for a, b in zip(p1, p2):
+        for (W1, b1), (W2, b2) in zip(a, b):
+            np.testing.assert_array_equal(W1, W2)
+            np.testing.assert_array_equal(b1, b2)
+
+
+def test_stream_copy_copies_exactly():
+    src = torch.arange(1 << 20, dtype=torch.float32, device="cuda") * 0.5 - 7.0
+    dst = torch.zeros_like(src)
+    tabpack.stream_copy(src, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst)
+    # a ragged size: fewer vectors than one round of the grid
+    s2, d2 = src[:4 * 37].clone(), torch.zeros(4 * 37, device="cuda")
+    tabpack.stream_copy(s2, d2)
+    torch.cuda.synchronize()
+    assert torch.equal(s2, d2)

@@ -8,7 +8,7 @@ import pytest
 from oracle import mlp, muon
 from oracle.pack import OraclePack
 from paper_2607_05380_amd import configs, synth, tabpack
-from parity import TOL, check_tensor, check_update, make_inputs, oracle_cfg, oracle_hparams, to_dev
+from parity import TOL, check_decisions, check_tensor, check_update, gpu_hints, make_inputs, oracle_cfg, oracle_hparams, record, to_dev
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -27,13 +27,16 @@ def _run(cfg, steps, members=None, n_train=3000, prec=None):
         idx = synth.batch_indices(orders, s, cfg["B"])
         (idx_d,) = to_dev(idx)
         lg = pk.train_step(X, y, idx_d, s + 1).cpu().numpy()
-        lo = op.train_step(Xtr, ytr, idx, s + 1)
+        hints = {k: gpu_hints(pk, k, cfg, s + 1) for k in range(cfg["K"])}
+        lo = op.train_step(Xtr, ytr, idx, s + 1, hints=hints)
+        for k in range(cfg["K"]):
+            check_decisions(op, k, f"step{s + 1}.m{k}")
         check_tensor(f"loss step {s + 1}", lg, lo, TOL[cfg["precision"]])
     return pk, op, p0
 
 
-def _compare(pk, op, p0, tol, steps, upd_frob, report):
-    for k in range(len(op.params)):
+def _compare(pk, op, p0, tol, steps, upd_frob, report, members=None, prefix=""):
+    for k in (range(len(op.params)) if members is None else members):
         g_gpu = pk.get_grads(k)
         p_gpu = pk.get_params(k)
         m_gpu, v_gpu = pk.get_moments(k)
@@ -41,7 +44,7 @@ def _compare(pk, op, p0, tol, steps, upd_frob, report):
         h = op.hp[k]
         for l in range(depth + 1):
             gW, gb = op.last_grads[k][l]
-            tag = f"m{k}.l{l}"
+            tag = f"{prefix}m{k}.l{l}"
             check_tensor(tag + ".grad", g_gpu[l][0], gW, tol, grad=True)
             check_tensor(tag + ".bgrad", g_gpu[l][1], gb, tol, grad=True)
             check_update(tag + ".b", p_gpu[l][1], op.params[k][l][1], p0[k][l][1], g_gpu[l][1], gb, h["lr"], tol,
@@ -62,10 +65,10 @@ def _compare(pk, op, p0, tol, steps, upd_frob, report):
                 # The optimizer alone: the oracle's Muon step fed with the GPU's own
                 # gradient (first step: empty momentum buffer) leaves only the
                 # rounding of the Newton-Schulz products.  In bf16 the iteration
-                # amplifies rounding (slope a = 3.4 at small singular values): two
-                # bf16 runs whose only difference is rounding differ by up to 2% of
-                # max|O| element-wise and 0.4-0.6% in Frobenius norm on these shapes,
-                # so the bounds are 5% of max|O| and 2% Frobenius.
+                # amplifies rounding (slope a = 3.4 at small singular values): over
+                # the suite the GPU step differs from the oracle's bf16-policy step
+                # on the same gradient by up to 4.9% of max|O| element-wise and 1.1%
+                # in Frobenius norm, so the bounds are 7% of max|O| and 2% Frobenius.
                 G = np.asarray(g_gpu[l][0], np.float64)
                 W_exp, _ = muon.muon_step(p0[k][l][0], G, np.zeros_like(G), h["muon_lr"], h["wd"],
                                           rnd=mlp.to_bf16 if tol is TOL["bf16"] else None)
@@ -74,22 +77,26 @@ def _compare(pk, op, p0, tol, steps, upd_frob, report):
                 d_exp = W_exp - p0[k][l][0]
                 frob_g = np.linalg.norm(d_gpu - d_exp) / max(np.linalg.norm(d_exp), 1e-30)
                 report.append((tag + ".given_grad", float(err.max() / (step * o_max))))
-                assert err.max() <= step * o_max * (0.05 if bf16 else 1e-4) + 1e-7, \
+                record(tag + ".given_grad", "muon_given", n=err.size, err_over_omax=err.max() / (step * o_max),
+                       frob=frob_g)
+                assert err.max() <= step * o_max * (0.07 if bf16 else 1e-4) + 1e-7, \
                     f"{tag}: Muon step from the same gradient differs by {err.max():.3e}"
                 assert frob_g <= (2e-2 if bf16 else 1e-5), f"{tag}: same-gradient update frob {frob_g:.3e}"
             # End to end against the oracle (its own gradients): the whole update
-            # within upd_frob in Frobenius norm -- in bf16 the gradients may differ
-            # by 2% (ReLU decisions flipping on bf16 noise), and the orthogonal
-            # factor of a near-square matrix moves more than its input -- and theta
+            # within upd_frob in Frobenius norm (bf16: measured 3.1%, bound 5%; the
+            # orthogonal factor of a near-square matrix moves more than its
+            # input, and the Newton-Schulz rounding above adds to it) and theta
             # within the literal tolerance, except for at most 0.1% of the elements
             # (bf16 only), which stay within 2 lr scale max|O|, the sign-flip bound
             # of the AdamW checks
             frob = np.linalg.norm(d_gpu - d_ref) / max(np.linalg.norm(d_ref), 1e-30)
             report.append((tag + ".frob", frob))
-            assert frob <= upd_frob, f"{tag}: Muon update relative Frobenius error {frob:.3e}"
             W_ref = op.params[k][l][0]
             err = np.abs(np.asarray(p_gpu[l][0], np.float64) - W_ref)
             lit = err <= tol["lit_atol"] + tol["lit_rtol"] * np.abs(W_ref)
+            record(tag + ".muon", "muon_e2e", n=err.size, frob=frob, literal_frac=(~lit).mean(),
+                   err_over_omax=(err.max() / (step * o_max)) if o_max > 0 else 0.0)
+            assert frob <= upd_frob, f"{tag}: Muon update relative Frobenius error {frob:.3e}"
             if not lit.all():
                 assert tol is TOL["bf16"], f"{tag}: {(~lit).sum()} elements outside the literal tolerance"
                 assert (~lit).mean() <= 1e-3, f"{tag}: {(~lit).sum()} elements outside the literal tolerance"
@@ -119,7 +126,7 @@ def test_muon_bf16_step(name, over):
     print(f"[muon] {name} widths {widths}", flush=True)
     pk, op, p0 = _run(cfg, 1)
     report = []
-    _compare(pk, op, p0, TOL["bf16"], 1, 0.10, report)
+    _compare(pk, op, p0, TOL["bf16"], 1, 0.05, report)
     frobs = [r[1] for r in report if r[0].endswith(".frob")]
     misses = sum(r[1] for r in report if r[0].endswith("literal_misses"))
     given = max(r[1] for r in report if r[0].endswith("given_grad"))

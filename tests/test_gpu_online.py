@@ -10,11 +10,15 @@ import pytest
 from oracle.online import ensemble_predict, run_online
 from oracle.pack import OraclePack
 from paper_2607_05380_amd import configs, synth, tabpack
-from paper_2607_05380_amd.online import OnlineTrainer
-from parity import TOL, check_tensor, check_update, make_inputs, oracle_cfg, oracle_hparams, to_dev
+from paper_2607_05380_amd.online import OnlineTrainer, Snapshot
+from parity import TOL, check_tensor, check_update, make_inputs, oracle_cfg, oracle_hparams, record, to_dev
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
+
+# fp32 online loop against the fp64 oracle loop over several epochs: relative
+# difference of the per-member and ensemble validation scores
+ONLINE_SCORE_REL = 1e-4  # measured 4.8e-5
 
 MEMBERS = [dict(width=w, dropout=p, lr=2e-3, wd=1e-3)
            for w, p in ((96, 0.1), (200, 0.0), (257, 0.3), (40, 0.2), (300, 0.4), (130, 0.1))]
@@ -136,15 +140,20 @@ def _oracle_loop(cfg, Xtr, ytr, Xva, yva, p_base, p_ens, m_ens, epochs, precisio
         return {k: preds[k] for k in members}, {k: scores[k] for k in members}
 
     def snapshot(k):
-        return [(W.copy(), b.copy()) for W, b in op.params[k]]
+        layers = [(W.copy(), b.copy()) for W, b in op.params[k]]
+        if op.use_emb:
+            return {n: a.copy() for n, a in op.emb[k].items()}, layers
+        return layers
 
     return op, run_online(epoch_fn, snapshot, cfg["K"], yva, cfg["task"], p_base, p_ens, m_ens, epochs)
 
 
+EMB_ONLINE = dict(emb_lo=8, emb_hi=16, emb_step=4, sigma_lo=0.1, sigma_hi=3.0)
+
+
 def test_online_loop_matches_oracle_fp32():
     # learning rates from [3e-3, 2e-2] so that members overfit within a few
-    # epochs: the run removes members at three epochs and stops on the
-    # ensemble's patience
+    # epochs: the run removes members and stops on the ensemble's patience
     cfg = configs.workload("binary_small", lr_lo=3e-3, lr_hi=2e-2)
     Xtr, ytr, Xva, yva = synth.make_data(cfg)
     p_base, p_ens, m_ens, epochs = 1, 2, 3, 10
@@ -156,11 +165,14 @@ def test_online_loop_matches_oracle_fp32():
     assert len(tr.history) == len(hist)
     for a, b in zip(tr.history, hist):
         assert a["members"] == b["members"], (a, b)
+        rel = [abs(a["scores"][k] - b["scores"][k]) / abs(b["scores"][k]) for k in a["members"]]
+        record(f"online.epoch{a['epoch']}.scores", "online_score", n=len(rel), max_rel=max(rel),
+               ens_rel=abs(a["score"] - b["score"]) / abs(b["score"]))
         for k in a["members"]:
-            assert a["scores"][k] == pytest.approx(b["scores"][k], rel=2e-4), (a["epoch"], k)
+            assert a["scores"][k] == pytest.approx(b["scores"][k], rel=ONLINE_SCORE_REL), (a["epoch"], k)
         assert a["ensemble"] == b["ensemble"], (a, b)
         assert a["removed"] == b["removed"]
-        assert a["score"] == pytest.approx(b["score"], rel=2e-4)
+        assert a["score"] == pytest.approx(b["score"], rel=ONLINE_SCORE_REL)
     assert [x.key for x in tr.ensemble] == [x.key for x in ens]
     # the final ensemble's prediction on fresh rows vs the oracle's snapshots
     Xte, _, _, _ = synth.make_data(dict(cfg, seed=cfg["seed"] + 99), n_train=900, n_val=1)
@@ -176,14 +188,52 @@ def test_online_loop_matches_oracle_fp32():
     # trajectories that drift apart slowly: probabilities within 2e-3, and a
     # relative Frobenius error of the whole prediction within 1e-3
     err = np.abs(got - ref)
+    frob = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    record("online.final_prediction", "online_predict", n=err.size, max_abs=err.max(), frob=frob)
     assert err.max() <= 2e-3, err.max()
-    assert np.linalg.norm(got - ref) <= 1e-3 * np.linalg.norm(ref)
+    assert frob <= 1e-3, frob
 
 
-def test_online_loop_bf16_decisions_follow_the_rules():
+def test_embedded_inference_pack_matches_oracle():
+    # The final ensemble of a pack with periodic embeddings (the paper's default
+    # backbone): snapshots taken from the oracle's own loop at several epochs,
+    # each with its member's embedding, are loaded into the trainer's inference
+    # pack, whose ensemble prediction on fresh rows must match the oracle's mean
+    # over the same snapshots.  The GPU's own embedded loop is checked against
+    # the selection and patience rules on its own scores
+    # (test_online_loop_bf16_decisions_follow_the_rules): compared with the
+    # fp64 oracle's trajectory, a single ReLU decision within rounding noise of
+    # 0 changes the sign-like first AdamW steps of the embedding after a dozen
+    # fp32 steps, and the two trajectories part.
+    cfg = configs.workload("binary_small", lr_lo=3e-3, lr_hi=2e-2, **EMB_ONLINE)
+    Xtr, ytr, Xva, yva = synth.make_data(cfg)
+    op, (ens, s, hist) = _oracle_loop(cfg, Xtr, ytr, Xva, yva, 1, 2, 3, 10, "fp64")
+    assert len({x.member for x in ens}) >= 2 and len({x.epoch for x in ens}) >= 2
+    tr = OnlineTrainer(cfg, p_base=1, p_ens=2, m_ens=3, max_epochs=1)
+    assert all(h["d_emb"] > 0 for h in tr.hp)
+    tr.ensemble = [Snapshot(x.member, x.epoch, tr.hp[x.member], [x.params[0]] + list(x.params[1]), None)
+                   for x in ens]
+    Xte, _, _, _ = synth.make_data(dict(cfg, seed=cfg["seed"] + 99), n_train=900, n_val=1)
+    got = tr.predict(to_dev(Xte)[0]).cpu().numpy()
+    hp = oracle_hparams(cfg)
+
+    def predict(inst):
+        emb_p, layers = inst.params
+        one = OraclePack(dict(oracle_cfg(cfg), K=1), hparams=[hp[inst.member]], params=[layers])
+        one.emb[0] = emb_p
+        return one.predict_values(0, Xte)
+
+    ref = ensemble_predict(ens, predict)
+    check_tensor("embedded ensemble prediction", got, ref, dict(TOL["fp32"], atol=1e-6))
+
+
+@pytest.mark.parametrize("emb", [{}, EMB_ONLINE], ids=["plain", "embeddings"])
+def test_online_loop_bf16_decisions_follow_the_rules(emb):
     # bf16 run on the GPU; its own per-epoch validation values, replayed through
-    # the oracle's loop, must give the same removals, ensembles and stop
-    cfg = configs.workload("regression_onehot", K=6, B=256)
+    # the oracle's loop, must give the same removals, ensembles and stop; with
+    # periodic embeddings the final ensemble's inference pack is rebuilt with
+    # every snapshot's embedding
+    cfg = configs.workload("regression_onehot", K=6, B=256, **emb)
     Xtr, ytr, Xva, yva = synth.make_data(cfg, n_train=2048, n_val=600)
     X, y, Xv, yv = to_dev(Xtr, ytr, Xva, yva)
     tr = OnlineTrainer(cfg, p_base=1, p_ens=1, m_ens=4, max_epochs=8)

@@ -194,3 +194,32 @@ def test_driver_decisions_match_oracle_loop(K, p_base, p_ens, m_ens, task, seed)
     assert [snap.key for snap in tr.ensemble] == [inst.key for inst in ens]
     assert all(snap.params == ("params",) + snap.key for snap in tr.ensemble)
     assert tr.ensemble_score == s
+
+
+@pytest.mark.parametrize("over", [dict(emb_lo=8, emb_hi=32, emb_step=4), dict(depth_lo=1, depth_hi=3, optimizer="muon"),
+                                  dict()])
+def test_inference_pack_spec_keeps_every_member_hyperparameter(over):
+    # the final-ensemble pack is rebuilt from snapshots (pack_init alone, no
+    # device): with periodic embeddings its members need their d_emb and sigma,
+    # or the layout (and pack_init's range check) would not match the snapshots
+    from paper_2607_05380_amd import configs, tabpack
+    from paper_2607_05380_amd.online import Snapshot, inference_spec
+    cfg = configs.workload("regression_onehot", K=5, B=256, **over)
+    src = tabpack.Pack(cfg)
+    hp = src.hparams()
+    snaps = [Snapshot(k, 3, hp[k], src.get_params(k), None) for k in (4, 1, 1, 3)]
+    icfg, members = inference_spec(cfg, snaps)
+    pk = tabpack.Pack(icfg, members=members)
+    got = pk.hparams()
+    for i, s in enumerate(snaps):
+        for key in ("width", "depth", "dropout", "lr", "wd", "d_emb", "sigma", "muon_lr", "t"):
+            assert got[i][key] == hp[s.member][key], (key, i)
+        assert pk.param_count(i) == src.param_count(s.member)
+        pk.set_params(i, s.params)
+        for a, b in zip(pk.get_params(i), s.params):
+            if isinstance(a, dict):
+                for n in a:
+                    np.testing.assert_array_equal(a[n], b[n])
+            else:
+                np.testing.assert_array_equal(a[0], b[0])
+                np.testing.assert_array_equal(a[1], b[1])

@@ -288,3 +288,60 @@ def test_pack_members_of_different_depths_match_torch_autograd(depths):
         for l, lin in enumerate(layers):
             np.testing.assert_allclose(op.last_grads[k][l][0], lin.weight.grad.numpy(), rtol=1e-10, atol=1e-13)
             np.testing.assert_allclose(op.last_grads[k][l][1], lin.bias.grad.numpy(), rtol=1e-10, atol=1e-13)
+
+
+def test_relu_decision_hints():
+    # The backward pass may take another implementation's ReLU decisions for
+    # pre-activations within window * rms(Z) of 0 (both branches correct up to
+    # accumulation rounding).  Pinned against torch autograd of a network whose
+    # ReLU derivative is set explicitly (value max(z, 0), derivative d).
+    task, d_out = mlp.TASK_REG, 1
+    params, X, y, masks = _tiny(task, d_out, 11, d_in=4, widths=(9, 7), B=12)
+    s = 1.25
+    Y, cache = mlp.forward(params, X, masks, s)
+    _, dY = mlp.loss_and_dy(Y, y, task)
+    plain = mlp.backward(params, cache, dY, masks, s)
+
+    def same(a, b):
+        for (x1, y1), (x2, y2) in zip(a, b):
+            np.testing.assert_array_equal(x1, x2)
+            np.testing.assert_array_equal(y1, y2)
+
+    own = [(Z > 0).astype(np.int8) for Z in cache["Z"]]
+    st = {}
+    same(plain, mlp.backward(params, cache, dY, masks, s, hints=own, stats=st))
+    assert st["taken"] == 0 and st["outside"] == 0
+    # flip the decision of the smallest |Z| of each layer
+    hints, rel = [], []
+    for Z, o in zip(cache["Z"], own):
+        h = o.copy()
+        i = np.unravel_index(np.argmin(np.abs(Z)), Z.shape)
+        h[i] = 1 - h[i]
+        hints.append(h)
+        rel.append(abs(Z[i]) / np.sqrt(np.mean(Z * Z)))
+    # a window that holds them: the flips are taken
+    window = max(rel) * 1.0001
+    st = {}
+    got = mlp.backward(params, cache, dY, masks, s, hints=hints, stats=st, window=window)
+    assert st["taken"] == len(hints) and st["outside"] == 0
+    d_eff = [np.where(np.abs(Z) <= window * np.sqrt(np.mean(Z * Z)), h == 1, Z > 0)
+             for Z, h in zip(cache["Z"], hints)]
+    tp = [(torch.tensor(W, requires_grad=True), torch.tensor(b, requires_grad=True)) for W, b in params]
+    H = torch.tensor(X)
+    for l, (W, b) in enumerate(tp[:-1]):
+        Z = H @ W.T + b
+        d = torch.tensor(d_eff[l].astype(np.float64))
+        H = (torch.relu(Z).detach() + (Z - Z.detach()) * d) * torch.tensor(masks[l].astype(np.float64)) * s
+    Yt = H @ tp[-1][0].T + tp[-1][1]
+    torch.mean((Yt[:, 0] - torch.tensor(y)) ** 2).backward()
+    for (gW, gb), (W, b) in zip(got, tp):
+        np.testing.assert_allclose(gW, W.grad.numpy(), rtol=1e-10, atol=1e-13)
+        np.testing.assert_allclose(gb, b.grad.numpy(), rtol=1e-10, atol=1e-13)
+    assert any(not np.allclose(a[0], b[0]) for a, b in zip(got, plain))
+    # a window that excludes them: the own decisions, and the disagreements counted
+    st = {}
+    same(plain, mlp.backward(params, cache, dY, masks, s, hints=hints, stats=st, window=min(rel) * 0.999))
+    assert st["outside"] == len(hints) and st["taken"] == 0
+    # unknown hints (-1) keep the own decisions whatever the window
+    unk = [np.full(Z.shape, -1, np.int8) for Z in cache["Z"]]
+    same(plain, mlp.backward(params, cache, dY, masks, s, hints=unk, window=1e9))

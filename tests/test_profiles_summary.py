@@ -37,25 +37,44 @@ def _write_pmc(d, rows):
 
 DW = "_ZN7tabpack12_GLOBAL__N_117gemm_kernel_smallIDF16bLi1ELi1ELi3EEEvNS_8GemmArgsE"
 COPY = "__amd_rocclr_copyBuffer"
+STREAM = "tabpack::(anonymous namespace)::stream_copy_kernel(float vector[4] const*, float vector[4]*, long)"
 
 
-def test_traffic_scales_by_the_copy(tmp_path, monkeypatch):
-    # the copy reads FETCH 2x and WRITE 1.5x of its 256 MiB; a kernel's counters
-    # are divided by those factors; values per XCC row are summed per dispatch
+def test_traffic_scales_by_the_stream_copy(tmp_path, monkeypatch):
+    # the library's streaming copy reads FETCH 2x and WRITE 1.5x of its 256 MiB;
+    # a kernel's counters are divided by those factors (raw values kept too);
+    # values per XCC row are summed per dispatch; torch's copy is only reported
     mib = 1024
-    _write_pmc(tmp_path / "f", [(1, COPY, "FETCH_SIZE", 512 * mib), (2, DW, "FETCH_SIZE", 600),
-                                (2, DW, "FETCH_SIZE", 400), (3, DW, "FETCH_SIZE", 3000)])
-    _write_pmc(tmp_path / "w", [(1, COPY, "WRITE_SIZE", 384 * mib), (2, DW, "WRITE_SIZE", 150),
-                                (3, DW, "WRITE_SIZE", 450)])
+    _write_pmc(tmp_path / "f", [(1, STREAM, "FETCH_SIZE", 512 * mib), (2, DW, "FETCH_SIZE", 600),
+                                (2, DW, "FETCH_SIZE", 400), (3, DW, "FETCH_SIZE", 3000),
+                                (4, COPY, "FETCH_SIZE", 256 * mib)])
+    _write_pmc(tmp_path / "w", [(1, STREAM, "WRITE_SIZE", 384 * mib), (2, DW, "WRITE_SIZE", 150),
+                                (3, DW, "WRITE_SIZE", 450), (4, COPY, "WRITE_SIZE", 512 * mib)])
     out = tmp_path / "t"
     monkeypatch.setattr(sys, "argv", ["ps", "traffic", str(tmp_path / "f"), str(tmp_path / "w"), "wl", str(out)])
     ps.main()
     rec = json.load(open(str(out) + ".json"))
     k = rec["kernels"]["gemm_bf16_rmaj_rmaj_dw"]
     assert rec["copy_factor"] == {"fetch": 2.0, "write": 1.5}
+    assert rec["torch_copy_factor"] == {"fetch": 1.0, "write": 2.0}
     assert k["dispatches"] == 2
     assert k["fetch_bytes"] == pytest.approx((1000 + 3000) / 2 * 1024 / 2.0)
     assert k["write_bytes"] == pytest.approx((150 + 450) / 2 * 1024 / 1.5)
+    assert k["write_raw_bytes"] == pytest.approx((150 + 450) / 2 * 1024)
+
+
+def test_busy_time_is_the_union_of_intervals(tmp_path):
+    assert ps.busy_ns([(0, 10), (5, 12), (20, 25), (24, 30), (40, 41)]) == 12 + 10 + 1
+    assert ps.busy_ns([]) == 0
+    d = tmp_path / "k"
+    os.makedirs(d)
+    with open(d / "run_kernel_trace.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        for a, b in ((100, 200), (150, 260), (300, 310)):
+            w.writerow({"Kernel_Name": DW, "Start_Timestamp": a, "End_Timestamp": b})
+        w.writerow({"Kernel_Name": COPY, "Start_Timestamp": 0, "End_Timestamp": 1000})
+    assert ps.trace_busy(str(d)) == {"gemm_bf16_rmaj_rmaj_dw": (3, 170)}
 
 
 def test_mfma_ratio(tmp_path, monkeypatch):
