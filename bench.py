@@ -50,7 +50,45 @@ def cpu_baseline(cfg, X, y, idx0, budget_s=15.0):
         done += 1
     return {"value": done * B / dt, "unit": "member-samples/s", "cores": int(threads), "kind": "oracle",
             "sample": f"members 0..{done - 1} of step 1 of {cfg['name']} (fp64 numpy, one member at a time), "
-                      f"{dt:.1f} s"}
+                      f"{dt:.1f} s",
+            "cpu_model": cpu_model(), "logical_cpus": os.cpu_count(), "blas": blas_vendor()}
+
+
+def cpu_model():
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def blas_vendor():
+    """The BLAS library numpy calls (threadpoolctl's view; numpy's build config as a fallback)."""
+    try:
+        from threadpoolctl import threadpool_info
+        libs = [f"{p.get('internal_api')} {p.get('version')} ({p.get('threading_layer')}, "
+                f"{p.get('num_threads')} threads)" for p in threadpool_info() if p.get("user_api") == "blas"]
+        if libs:
+            return "; ".join(libs)
+    except Exception:
+        pass
+    try:
+        import numpy as np
+        cfg = np.show_config(mode="dicts")
+        return cfg["Build Dependencies"]["blas"]["name"]
+    except Exception:
+        return None
 
 
 def per_epoch(cfg, pk, Xtr, ytr, Xva, yva, step, online_epochs):
@@ -304,22 +342,28 @@ def main():
         pk.train_step(Xtr, ytr, idx_all[step - 1], step, loss)
     torch.cuda.synchronize()
     log(f"warmup done, losses[:4] = {loss[:4].tolist()}")
-    # device-to-device copy bandwidth (read + write), the measured reference for
-    # the HBM-bound kernels; in a profiler run the same copies scale the byte
-    # counters (profiles_summary traffic)
+    # streaming copy bandwidth (read + write) with the library's non-temporal
+    # copy kernel, the measured reference for the HBM-bound kernels, and
+    # torch's copy for comparison; in a profiler run the same copies scale the
+    # byte counters (profiles_summary traffic)
     src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
-    dst.copy_(src)
-    torch.cuda.synchronize()
-    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    c0.record()
-    for _ in range(3):
-        dst.copy_(src)
-    c1.record()
-    torch.cuda.synchronize()
-    copy_gbps = 2 * 3 * COPY_BYTES / (c0.elapsed_time(c1) / 1e3) / 1e9
+
+    def copy_rate(fn):
+        fn()
+        torch.cuda.synchronize()
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for _ in range(3):
+            fn()
+        c1.record()
+        torch.cuda.synchronize()
+        return 2 * 3 * COPY_BYTES / (c0.elapsed_time(c1) / 1e3) / 1e9
+
+    copy_gbps = copy_rate(lambda: tabpack.stream_copy(src, dst))
+    torch_copy_gbps = copy_rate(lambda: dst.copy_(src))
     del src, dst
-    log(f"device-to-device copy: {copy_gbps:.0f} GB/s (read + write)")
+    log(f"streaming copy: {copy_gbps:.0f} GB/s, torch copy {torch_copy_gbps:.0f} GB/s (read + write)")
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -353,27 +397,33 @@ def main():
             f"{s['bytes'] * s['launches'] / s['busy_ms'] / 1e6:7.1f} GB/s  [{s['kind']}]")
     roofline = None
     if stats:
-        # Launches of the concurrent member groups overlap, so the rate is the
-        # kernel's total work over its busy time (the union of its launches'
-        # intervals); the rate of one launch in isolation of the others is
-        # reported beside it.
+        # The dominant kernel (largest busy time per step).  achieved = the
+        # algorithmic work of one launch / the launch's average duration (HIP
+        # events on the stream it runs on; rocprofv3's average duration of the
+        # same kernel in profiles/ must agree).  Launches of the concurrent
+        # member groups overlap and share the chip, so a launch's duration
+        # includes the time other groups' kernels hold CUs; the rate over the
+        # kernel's busy time (the union of its launches' intervals) is
+        # reported beside it, labelled.
         dom = max(stats, key=lambda s: s["busy_ms"])
         if dom["kind"] == "mfma":
             peak = PEAK["mfma_bf16"] if cfg["precision"] == "bf16" else PEAK["mfma_fp32"]
             work, unit, scale = dom["flops"], "TFLOP/s", 1e12
         else:
             peak, work, unit, scale = PEAK["hbm"], dom["bytes"], "GB/s", 1e9
-        achieved = work * dom["launches"] / (dom["busy_ms"] / 1e3) / scale
+        achieved = work / (dom["avg_ms"] / 1e3) / scale
+        busy_rate = work * dom["launches"] / (dom["busy_ms"] / 1e3) / scale
         roofline = {"bound": dom["kind"], "kernel": dom["name"], "achieved": round(achieved, 2), "peak": peak,
                     "unit": unit, "frac": round(achieved / peak, 4),
                     "traffic": measured_traffic(cfg["name"], dom["name"]),
                     "work_per_launch": work, "flops_per_launch": dom["flops"], "bytes_per_launch": dom["bytes"],
                     "avg_launch_us": round(dom["avg_ms"] * 1e3, 2),
-                    "busy_us_per_step": round(dom["busy_ms"] * 1e3 / a.profile_steps, 2),
                     "launches_per_step": dom["launches"] / a.profile_steps,
-                    "achieved_per_launch": round(work / (dom["avg_ms"] / 1e3) / scale, 2)}
+                    "busy_time": {"us_per_step": round(dom["busy_ms"] * 1e3 / a.profile_steps, 2),
+                                  "achieved": round(busy_rate, 2), "frac": round(busy_rate / peak, 4)}}
         if dom["kind"] != "mfma":
             roofline["copy_gb_per_s"] = round(copy_gbps, 1)
+            roofline["torch_copy_gb_per_s"] = round(torch_copy_gbps, 1)
             roofline["frac_of_copy"] = round(achieved / copy_gbps, 4)
     out = {
         "metric": METRIC, "value": round(msamples, 1), "unit": "member-samples/s", "n_gpus": 1,

@@ -39,6 +39,10 @@ int fail(int code, const char* fmt, ...) {
 
 constexpr uint32_t kTagHparam = 1, kTagInit = 2;
 constexpr int kGroups = 4;  // at most this many member groups run their GEMM chains concurrently
+#ifndef TABPACK_STAGGER
+#define TABPACK_STAGGER 0
+#endif
+constexpr int kStaggerLayer = TABPACK_STAGGER;  // see the forward pass of pack_train_step
 
 int64_t round_up(int64_t x, int64_t q) { return (x + q - 1) / q * q; }
 
@@ -179,6 +183,7 @@ struct pack_handle {
   hipStream_t gstream[kGroups] = {};  // streams of groups 1.. (entry 0 unused)
   hipEvent_t ev_split = nullptr, ev_merge[kGroups] = {};
   hipEvent_t ev_gather[kGroups] = {};  // group g's gather done (group g + 1 gathers after it)
+  hipEvent_t ev_fwd[kGroups] = {};     // group g's forward pass through layer kStaggerLayer done
   int ncoltiles = 0;
   int nheadtiles = 0;
   int head_rb = 0;  // rows per head-backward block
@@ -1389,6 +1394,8 @@ int pack_destroy(pack_handle* h) {
     }
     for (hipEvent_t e : h->ev_gather)
       if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : h->ev_fwd)
+      if (e) (void)hipEventDestroy(e);
   }
   delete h;
   return PACK_OK;
@@ -1429,6 +1436,7 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
       HIP_TRY(hipEventCreateWithFlags(&h->ev_merge[g], hipEventDisableTiming));
     }
     for (hipEvent_t& e : h->ev_gather) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    for (hipEvent_t& e : h->ev_fwd) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
   h->keep_ready = 0;
   HIP_TRY(hipMemsetAsync(workspace, 0, need, stream));
@@ -1570,8 +1578,17 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     }
     HIP_TRY(hipStreamWaitEvent(s, h->ev_keep[par], 0));
   }
-  for (int l = 1; l <= c.L; ++l)
-    for (int hf = 0; hf < ng; ++hf) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
+  // Staggered groups: group g starts its forward GEMMs once group g - 1 has
+  // finished its forward pass through layer kStaggerLayer, so one group's
+  // HBM-bound backward pass (the fused optimizer) overlaps the next group's
+  // MFMA-bound forward pass instead of every group reaching its optimizer
+  // epilogues at once (0: the groups run side by side).
+  for (int hf = 0; hf < ng; ++hf)
+    for (int l = 1; l <= c.L; ++l) {
+      if (kStaggerLayer > 0 && l == 1 && hf > 0) HIP_TRY(hipStreamWaitEvent(hs[hf], h->ev_fwd[hf - 1], 0));
+      HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
+      if (l == std::min(kStaggerLayer, c.L)) HIP_TRY(hipEventRecord(h->ev_fwd[hf], hs[hf]));
+    }
   for (int hf = 0; hf < ng; ++hf) {
     const hipStream_t s = hs[hf];
     const int32_t* gm = h->b.d_members + h->member0[hf];

@@ -33,7 +33,7 @@ EPIS = ["fwd", "fwd_eval", "dx", "dw", "ns", "de"]
 SIMPLE = ["dropout_words", "head_grad_reduce", "head_fwd", "head_bwd", "loss_reduce", "bias_from_partials",
           "gather", "adamw", "to_shadow", "eval_score", "dropout_mask", "select_partial", "select_pick",
           "select_update", "select_init", "select_final", "ensemble_mean", "muon_prep", "muon_norm",
-          "muon_convert", "muon_update", "embed_fwd", "embed_grad"]
+          "muon_convert", "muon_update", "embed_fwd", "embed_grad", "idx_check", "stream_copy"]
 
 
 def source_digest():
@@ -85,6 +85,34 @@ def is_copy(kernel):
     return "copyBuffer" in kernel or "CopyBuffer" in kernel
 
 
+def busy_ns(intervals):
+    """Length of the union of [start, end) intervals."""
+    tot, cur_s, cur_e = 0, None, None
+    for a, b in sorted(intervals):
+        if cur_e is None or a > cur_e:
+            if cur_e is not None:
+                tot += cur_e - cur_s
+            cur_s, cur_e = a, b
+        else:
+            cur_e = max(cur_e, b)
+    if cur_e is not None:
+        tot += cur_e - cur_s
+    return tot
+
+
+def trace_busy(d):
+    """{kernel: (dispatches, union of its dispatch intervals in ns)} from the
+    kernel_trace.csv files of a --kernel-trace run."""
+    iv = {}
+    for f in glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                name = short_name(r["Kernel_Name"])
+                if name:
+                    iv.setdefault(name, []).append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    return {k: (len(v), busy_ns(v)) for k, v in iv.items()}
+
+
 def stats(args):
     rows = []
     for f in glob.glob(os.path.join(args.dir, "**", "*kernel_stats.csv"), recursive=True):
@@ -99,13 +127,18 @@ def stats(args):
         a[0] += int(r["Calls"])
         a[1] += float(r["TotalDurationNs"])
     total = sum(v[1] for v in agg.values())
+    busy = trace_busy(args.dir)
     lines = [f"# Kernel time summary ({os.path.basename(args.out)[:-3]})", "", "Command:", "", "```",
              args.command, "```", "",
              "Library kernels only; the share is of the library's kernel time.  Other dispatches of the run "
-             f"(synthetic data generation in torch): {other[0]} calls, {other[1] / 1e6:.3f} ms.", "",
-             "| kernel | calls | avg us | total ms | share |", "|---|---|---|---|---|"]
+             f"(synthetic data generation in torch): {other[0]} calls, {other[1] / 1e6:.3f} ms.  "
+             "Busy ms: the union of the kernel's dispatch intervals in the kernel trace (launches of the "
+             "concurrent member-group streams overlap, so it can be less than the total).", "",
+             "| kernel | calls | avg us | total ms | busy ms | share |", "|---|---|---|---|---|---|"]
     for name, (calls, ns) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
-        lines.append(f"| {name} | {calls} | {ns / calls / 1e3:.1f} | {ns / 1e6:.3f} | {100 * ns / total:.1f}% |")
+        b = busy.get(name, (0, 0))[1]
+        lines.append(f"| {name} | {calls} | {ns / calls / 1e3:.1f} | {ns / 1e6:.3f} | {b / 1e6:.3f} | "
+                     f"{100 * ns / total:.1f}% |")
     with open(args.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -127,38 +160,57 @@ def per_dispatch(d, counter):
     return out
 
 
+def fmt(x):
+    return "n/a" if x is None else f"{x:.3f}"
+
+
 def traffic(args):
     res = {}
     factors = {}
+    torch_factors = {}
     for counter, d in (("FETCH_SIZE", args.fetch), ("WRITE_SIZE", args.write)):
         disp = per_dispatch(d, counter)
-        copies = [v for name, v in disp.values() if is_copy(name) and v * 1024 >= 0.5 * COPY_BYTES]
-        if not copies:
-            sys.exit(f"no calibration copy found in the {counter} run")
-        factor = statistics.median(copies) * 1024 / COPY_BYTES  # counter bytes per true byte
+        # calibration: the library's non-temporal streaming copy of 256 MiB
+        # (the access pattern of the optimizer epilogues); torch's copy kernel
+        # is reported beside it
+        cal = [v for name, v in disp.values() if short_name(name) == "stream_copy" and v * 1024 >= 0.5 * COPY_BYTES]
+        if not cal:
+            sys.exit(f"no calibration stream_copy found in the {counter} run")
+        factor = statistics.median(cal) * 1024 / COPY_BYTES  # counter bytes per true byte
         factors[counter] = factor
+        tc = [v for name, v in disp.values() if is_copy(name) and v * 1024 >= 0.5 * COPY_BYTES]
+        torch_factors[counter] = statistics.median(tc) * 1024 / COPY_BYTES if tc else None
         per = {}
         for name, v in disp.values():
             s = short_name(name)
             if s:
-                per.setdefault(s, []).append(v * 1024 / factor)
+                per.setdefault(s, []).append(v * 1024)
         for s, vals in per.items():
-            res.setdefault(s, {})["fetch_bytes" if counter == "FETCH_SIZE" else "write_bytes"] = statistics.mean(vals)
+            key = "fetch" if counter == "FETCH_SIZE" else "write"
+            res.setdefault(s, {})[key + "_bytes"] = statistics.mean(vals) / factor
+            res[s][key + "_raw_bytes"] = statistics.mean(vals)
             res[s]["dispatches"] = len(vals)
     rec = {"workload": args.workload, "source_sha256": source_digest(), "command": args.command,
            "copy_factor": {"fetch": factors["FETCH_SIZE"], "write": factors["WRITE_SIZE"]},
+           "torch_copy_factor": {"fetch": torch_factors["FETCH_SIZE"], "write": torch_factors["WRITE_SIZE"]},
            "kernels": {k: v for k, v in res.items() if "fetch_bytes" in v and "write_bytes" in v}}
     with open(args.out_prefix + ".json", "w") as f:
         json.dump(rec, f, indent=1)
     lines = [f"# HBM traffic per launch, {args.workload}", "", "Commands (FETCH_SIZE run, then WRITE_SIZE run):",
              "", "```", args.command, "```", "",
-             f"Copy calibration: a 256 MiB device-to-device copy reads FETCH_SIZE x {factors['FETCH_SIZE']:.3f} "
-             f"and WRITE_SIZE x {factors['WRITE_SIZE']:.3f} of its true bytes; the figures below are divided "
-             "by these factors.", "",
-             "| kernel | dispatches | fetch MB | write MB | total MB |", "|---|---|---|---|---|"]
+             "Calibration: the library's non-temporal streaming copy (`pack_stream_copy`, 256 MiB read and "
+             f"256 MiB written) reads FETCH_SIZE x {factors['FETCH_SIZE']:.3f} and WRITE_SIZE x "
+             f"{factors['WRITE_SIZE']:.3f} of its true bytes; the scaled figures below are divided by these "
+             "factors, the raw ones are the counters as read (KiB x 1024).  torch's device-to-device copy of the "
+             f"same size reads FETCH_SIZE x {fmt(torch_factors['FETCH_SIZE'])} and WRITE_SIZE x "
+             f"{fmt(torch_factors['WRITE_SIZE'])}.  Bytes served by the 256 MB last-level cache do not reach "
+             "HBM and are not counted.", "",
+             "| kernel | dispatches | fetch MB | write MB | total MB | raw fetch MB | raw write MB |",
+             "|---|---|---|---|---|---|---|"]
     for k, v in sorted(rec["kernels"].items(), key=lambda kv: -(kv[1]["fetch_bytes"] + kv[1]["write_bytes"])):
         lines.append(f"| {k} | {v['dispatches']} | {v['fetch_bytes'] / 1e6:.1f} | {v['write_bytes'] / 1e6:.1f} | "
-                     f"{(v['fetch_bytes'] + v['write_bytes']) / 1e6:.1f} |")
+                     f"{(v['fetch_bytes'] + v['write_bytes']) / 1e6:.1f} | {v['fetch_raw_bytes'] / 1e6:.1f} | "
+                     f"{v['write_raw_bytes'] / 1e6:.1f} |")
     with open(args.out_prefix + ".md", "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
