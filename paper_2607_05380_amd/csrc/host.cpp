@@ -109,7 +109,7 @@ struct Bufs {
   float* dE = nullptr; // embeddings: at each member's E offset / 16, the dE GEMM's sums [Bp / 64][4][p_in] (fp32)
   char* H = nullptr;   // L activation buffers H_1..H_L
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
-  float* colpart = nullptr;  // bias-gradient partials of the dX epilogue, A / kPartRows floats
+  float* colpart = nullptr;  // bias-gradient partials of the dX epilogues, (L - 1) x A / kPartRows floats
   uint32_t* mask = nullptr;  // ReLU/dropout keep bits of H_1..H_L, L * A / 32 words
   uint32_t* keepw = nullptr; // dropout keep words, 2 copies of L * A / 32 words
   char* zeros = nullptr;     // 256 zero bytes: GEMM loads of out-of-range elements read them
@@ -184,6 +184,7 @@ struct pack_handle {
   hipEvent_t ev_split = nullptr, ev_merge[kGroups] = {};
   hipEvent_t ev_gather[kGroups] = {};  // group g's gather done (group g + 1 gathers after it)
   hipEvent_t ev_fwd[kGroups] = {};     // group g's forward pass through layer kStaggerLayer done
+  hipEvent_t ev_bias[kGroups] = {};    // group g's last data-gradient launch done
   int ncoltiles = 0;
   int nheadtiles = 0;
   int head_rb = 0;  // rows per head-backward block
@@ -565,7 +566,6 @@ void sort_launch(Plan& p, const Launch& ln) {
 // (measured on the 64-member workloads: 1 group 1.80 ms, 2 groups 1.63 ms,
 // 3 groups 1.60 ms per step; 4 groups exceed the four hardware queues).
 void split_members(pack_handle* h) {
-  const pack_config& c = h->cfg;
   int ng = 3;
   if (const char* e = getenv("TABPACK_STREAMS")) ng = std::max(1, std::min(kGroups, atoi(e)));
   h->ngroups = std::max(1, std::min(ng, (int)h->active_ids.size()));
@@ -950,7 +950,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
         d.ldb = m.dp;
         d.C = act(dzb(l - 1), k);
         d.mask = maskp(l - 1, k);
-        d.colpart = bf.colpart + h->mem[k].act_off / kPartRows;
+        d.colpart = bf.colpart + (size_t)(l - 2) * (h->A / kPartRows) + h->mem[k].act_off / kPartRows;
         d.ldc = m.dp;
         d.M = h->Bp;
         d.N = m.dp;
@@ -978,7 +978,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       if (l >= 2)
         for (int k : group[hf])
           if (h->mem[k].depth >= l)
-            for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0});
+            for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0, l - 2});
     }
   p.coltile0[(size_t)kGroups * c.L] = (int)p.coltiles.size();
   const TileSet saved_ts = p.tile_set;
@@ -1054,7 +1054,7 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf) {
   bf.dE = h->emb ? cv.take<float>((size_t)h->H0e / 16) : nullptr;
   bf.H = cv.take<char>((size_t)c.L * h->A * h->elt());
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
-  bf.colpart = cv.take<float>((size_t)h->A / kPartRows);
+  bf.colpart = cv.take<float>((size_t)std::max(1, c.L - 1) * (h->A / kPartRows));
   bf.mask = cv.take<uint32_t>((size_t)c.L * (h->A / 32));
   bf.keepw = cv.take<uint32_t>((size_t)2 * c.L * (h->A / 32));
   bf.zeros = cv.take<char>(256);
@@ -1396,6 +1396,8 @@ int pack_destroy(pack_handle* h) {
       if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : h->ev_fwd)
       if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : h->ev_bias)
+      if (e) (void)hipEventDestroy(e);
   }
   delete h;
   return PACK_OK;
@@ -1437,6 +1439,7 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
     }
     for (hipEvent_t& e : h->ev_gather) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     for (hipEvent_t& e : h->ev_fwd) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    for (hipEvent_t& e : h->ev_bias) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
   h->keep_ready = 0;
   HIP_TRY(hipMemsetAsync(workspace, 0, need, stream));
@@ -1625,11 +1628,20 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       // dX_l reads W_l, so it runs before the weight-gradient GEMM updates W_l in place
       if (l > 1) {
         HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[hf][l - 1], l, s));
-        HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 / h->elt() / kPartRows / ng, s, [&] {
-          const int t0 = h->coltile0[(size_t)hf * c.L + l - 1], t1 = h->coltile0[(size_t)hf * c.L + l];
-          return launch_bias_from_partials(h->b.colpart, h->b.d_mem, h->b.d_coltiles + t0, t1 - t0, h->Bp / kPartRows,
-                                           h->b.d_bias_off + (size_t)(l - 2) * c.K, h->b.grad, s);
-        }));
+        if (l == 2) {
+          // the group's last dX launch: the sums of every layer's bias-gradient
+          // partials (each layer has its own partial buffer) run on the side
+          // stream, off the group's chain; the final bias AdamW waits for them
+          HIP_TRY(hipEventRecord(h->ev_bias[hf], s));
+          HIP_TRY(hipStreamWaitEvent(h->side, h->ev_bias[hf], 0));
+          HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 * (c.L - 1) / h->elt() / kPartRows / ng,
+                        h->side, [&] {
+                          const int t0 = h->coltile0[(size_t)hf * c.L + 1], t1 = h->coltile0[(size_t)hf * c.L + c.L];
+                          return launch_bias_from_partials(h->b.colpart, h->A / kPartRows, h->b.d_mem,
+                                                           h->b.d_coltiles + t0, t1 - t0, h->Bp / kPartRows,
+                                                           h->b.d_bias_off, c.K, h->b.grad, h->side);
+                        }));
+        }
       }
       if (l == 1 && h->emb) {
         // dE = dZ_1 W_1, before W_1 is updated, reduced in the GEMM's epilogue
@@ -1825,6 +1837,7 @@ int pack_select(pack_handle* h, const float* cand, const void* yv, int32_t C, in
   HIP_TRY(launch_select_final(state, best, n_sel_out, score_out, stream));
   return PACK_OK;
 }
+
 
 int pack_member_param_count(const pack_handle* h, int32_t member, int64_t* count) {
   int rc = check_member(h, member);

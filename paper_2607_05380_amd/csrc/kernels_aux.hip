@@ -373,18 +373,23 @@ __global__ __launch_bounds__(256) void head_grad_reduce_kernel(const float* part
 }
 
 // db_l[c] = sum of the per-row-block column partials written by the dX epilogue,
-// in a fixed order; 64 columns of one member per workgroup.
-__global__ __launch_bounds__(64) void bias_from_partials_kernel(const float* part, const MemberDev* mem,
-                                                                const ColTile* tiles, int nparts,
-                                                                const int64_t* bias_off, float* grad) {
-  const ColTile ct = tiles[blockIdx.x];
+// in a fixed order; one wave per 64 columns of one member and layer (the
+// partials of bias layer j at part + j * part_stride, its offsets at
+// bias_off[j * K + member]).
+__global__ __launch_bounds__(256) void bias_from_partials_kernel(const float* part, int64_t part_stride,
+                                                                 const MemberDev* mem, const ColTile* tiles,
+                                                                 int ntiles, int nparts, const int64_t* bias_off,
+                                                                 int K, float* grad) {
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= ntiles) return;
+  const ColTile ct = tiles[w];
   const MemberDev md = mem[ct.member];
-  const int c = ct.c0 + threadIdx.x;
+  const int c = ct.c0 + (threadIdx.x & 63);
   if (c >= md.dp) return;
-  const float* p = part + md.act_off / kPartRows;
+  const float* p = part + ct.part * part_stride + md.act_off / kPartRows;
   float s = 0.0f;
   for (int r = 0; r < nparts; ++r) s += p[(int64_t)r * md.dp + c];
-  grad[bias_off[ct.member] + c] = s;
+  grad[bias_off[(int64_t)ct.part * K + ct.member] + c] = s;
 }
 
 // ----------------------------------------------------------------- gather --
@@ -826,12 +831,12 @@ hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int 
   return hipGetLastError();
 }
 
-hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, const ColTile* tiles,
-                                     int ntiles, int nparts, const int64_t* bias_off, float* grad,
-                                     hipStream_t s) {
+hipError_t launch_bias_from_partials(const float* part, int64_t part_stride, const MemberDev* mem,
+                                     const ColTile* tiles, int ntiles, int nparts, const int64_t* bias_off, int K,
+                                     float* grad, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL(bias_from_partials_kernel, dim3(ntiles), dim3(64), 0, s, part, mem, tiles, nparts,
-                     bias_off, grad);
+  hipLaunchKernelGGL(bias_from_partials_kernel, dim3((ntiles + 3) / 4), dim3(256), 0, s, part, part_stride, mem,
+                     tiles, ntiles, nparts, bias_off, K, grad);
   return hipGetLastError();
 }
 

@@ -1102,13 +1102,16 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
 // still in flight and this wave's LDS reads are done.
 template <int PS, int NS>
 __device__ __forceinline__ void wait_stage(int newer) {
-  static_assert(NS <= 4 && 2 * PS < 64, "up to 2 newer steps");
-  if (newer <= 0)
-    wait_vm<0, true>();
-  else if (newer == 1)
-    wait_vm<PS, true>();
-  else
-    wait_vm<2 * PS, true>();
+  static_assert(NS >= 2 && NS <= 8 && (NS - 2) * PS < 64, "vmcnt holds the newer steps' loads");
+  switch (newer < NS - 2 ? (newer < 0 ? 0 : newer) : NS - 2) {
+    case 0: wait_vm<0, true>(); break;
+    case 1: wait_vm<(NS > 2 ? PS : 0), true>(); break;
+    case 2: wait_vm<(NS > 3 ? 2 * PS : 0), true>(); break;
+    case 3: wait_vm<(NS > 4 ? 3 * PS : 0), true>(); break;
+    case 4: wait_vm<(NS > 5 ? 4 * PS : 0), true>(); break;
+    case 5: wait_vm<(NS > 6 ? 5 * PS : 0), true>(); break;
+    default: wait_vm<(NS > 7 ? 6 * PS : 0), true>(); break;
+  }
 }
 
 // One output tile over the member's whole depth.  bf16 operands stream into

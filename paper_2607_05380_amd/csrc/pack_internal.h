@@ -156,9 +156,10 @@ struct HeadTile {            // (member, first column, first row) block of the h
   int32_t member, c0, r0;
 };
 
-struct ColTile {            // (member, first column) work item of the column-sweep kernels
+struct ColTile {            // (member, first column, bias layer) work item of the bias-gradient sums
   int32_t member;
   int32_t c0;
+  int32_t part;             // b_{part + 1}: the partials of the dX launch of layer part + 2
 };
 
 // Launchers (kernels_gemm.hip).
@@ -181,9 +182,9 @@ hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const M
 hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int K, int max_dp, int Bp, int RB,
                                    int d_out, float* grad, const int32_t* members, hipStream_t s);
 int head_bwd_cols(int d_out);  // columns one head-backward block covers
-hipError_t launch_bias_from_partials(const float* part, const MemberDev* mem, const ColTile* tiles,
-                                     int ntiles, int nparts, const int64_t* bias_off, float* grad,
-                                     hipStream_t s);
+hipError_t launch_bias_from_partials(const float* part, int64_t part_stride, const MemberDev* mem,
+                                     const ColTile* tiles, int ntiles, int nparts, const int64_t* bias_off, int K,
+                                     float* grad, hipStream_t s);
 hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
                          int64_t row_base, int rows_valid, int members, int Bp, void* H0,
                          const int32_t* member_ids, hipStream_t s);
