@@ -248,6 +248,20 @@ int pack_select(pack_handle* h, const float* cand, const void* yv, int32_t C, in
                 int32_t m_ens, void* work, size_t work_bytes, int32_t* sel_out,
                 int32_t* n_sel_out, double* score_out, hipStream_t stream);
 
+/* pack_select() for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same selection, with the same arguments and results, but its scratch is
+ * a file-scope device array of PACK_SELECT_STATIC_BYTES inside the library
+ * (one per GPU, held until the process ends) instead of `work`.  Allocates
+ * nothing.  Returns PACK_EINVAL when pack_select_workspace_size(C, Nv)
+ * exceeds PACK_SELECT_STATIC_BYTES (e.g. Nv beyond about 500,000 rows).
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (from concurrent streams or threads) race and give undefined results. */
+#define PACK_SELECT_STATIC_BYTES ((size_t)4 << 20)
+int pack_select_static(pack_handle* h, const float* cand, const void* yv, int32_t C, int64_t Nv,
+                       int32_t m_ens, int32_t* sel_out, int32_t* n_sel_out, double* score_out,
+                       hipStream_t stream);
+
 /* Number of floats in member k's dense parameter vector: for l = 1..L_k the
  * row-major [d_k, fan_in] weight then its [d_k] bias, then the head's
  * [d_out, d_k] weight and [d_out] bias (torch.nn.Linear layout). */

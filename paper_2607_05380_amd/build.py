@@ -7,7 +7,7 @@ import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = ["kernels_gemm.hip", "kernels_aux.hip", "kernels_muon.hip", "kernels_embed.hip", "host.cpp"]
+SRC = ["kernels_gemm.hip", "kernels_aux.hip", "kernels_muon.hip", "kernels_embed.hip", "select_static.hip", "host.cpp"]
 LIB = os.path.join(HERE, "libtabpack.so")
 
 FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-Wall",

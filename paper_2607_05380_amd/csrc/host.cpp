@@ -1812,9 +1812,10 @@ int pack_select_workspace_size(int32_t C, int64_t Nv, size_t* bytes) {
   return PACK_OK;
 }
 
-int pack_select(pack_handle* h, const float* cand, const void* yv, int32_t C, int64_t Nv, int32_t m_ens,
-                void* work, size_t work_bytes, int32_t* sel_out, int32_t* n_sel_out, double* score_out,
-                hipStream_t stream) {
+extern "C++" {
+int tabpack::select_with_scratch(pack_handle* h, const float* cand, const void* yv, int32_t C, int64_t Nv,
+                                 int32_t m_ens, void* work, size_t work_bytes, int32_t* sel_out, int32_t* n_sel_out,
+                                 double* score_out, hipStream_t stream) {
   if (!h) return fail(PACK_EINVAL, "handle is NULL");
   if (!cand || !yv || !work || !n_sel_out || !score_out || (m_ens > 0 && !sel_out))
     return fail(PACK_EINVAL, "NULL device pointer");
@@ -1837,7 +1838,15 @@ int pack_select(pack_handle* h, const float* cand, const void* yv, int32_t C, in
   HIP_TRY(launch_select_final(state, best, n_sel_out, score_out, stream));
   return PACK_OK;
 }
+}  // extern "C++"
 
+int pack_select(pack_handle* h, const float* cand, const void* yv, int32_t C, int64_t Nv, int32_t m_ens,
+                void* work, size_t work_bytes, int32_t* sel_out, int32_t* n_sel_out, double* score_out,
+                hipStream_t stream) {
+  return select_with_scratch(h, cand, yv, C, Nv, m_ens, work, work_bytes, sel_out, n_sel_out, score_out, stream);
+}
+
+extern "C++" int tabpack::set_error(int code, const char* msg) { return fail(code, "%s", msg); }
 
 int pack_member_param_count(const pack_handle* h, int32_t member, int64_t* count) {
   int rc = check_member(h, member);

@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+struct pack_handle;  // the library handle (include/tabpack.h)
+
 namespace tabpack {
 
 constexpr int kChunk = 256;        // AdamW chunk: elements of one member, one kind (weight / bias)
@@ -182,6 +184,14 @@ hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const M
 hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int K, int max_dp, int Bp, int RB,
                                    int d_out, float* grad, const int32_t* members, hipStream_t s);
 int head_bwd_cols(int d_out);  // columns one head-backward block covers
+// The greedy selection of pack_select() with the caller's scratch `work`
+// (pack_select_workspace_size() bytes, 256-byte aligned); returns a PACK_*
+// code and sets the library's last error.
+int select_with_scratch(pack_handle* h, const float* cand, const void* yv, int32_t C, int64_t Nv, int32_t m_ens,
+                        void* work, size_t work_bytes, int32_t* sel_out, int32_t* n_sel_out, double* score_out,
+                        hipStream_t stream);
+// Sets the library's last error message; returns code.
+int set_error(int code, const char* msg);
 hipError_t launch_bias_from_partials(const float* part, int64_t part_stride, const MemberDev* mem,
                                      const ColTile* tiles, int ntiles, int nparts, const int64_t* bias_off, int K,
                                      float* grad, hipStream_t s);

@@ -26,7 +26,7 @@ SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "
            "pack_select", "pack_member_param_count", "pack_get_params", "pack_set_params",
            "pack_get_grads", "pack_get_moments", "pack_debug_dropout_mask", "pack_debug_activation",
            "pack_profile_enable", "pack_profile_read", "pack_set_active", "pack_predict", "pack_status",
-           "pack_stream_copy"]
+           "pack_stream_copy", "pack_select_static"]
 
 
 class MemberHP(ctypes.Structure):
@@ -91,6 +91,7 @@ def load_library(path=LIB_PATH):
         "pack_eval_members": ([H, vp, vp, i64, vp, vp, vp], ctypes.c_int),
         "pack_select_workspace_size": ([i32, i64, ctypes.POINTER(sz)], ctypes.c_int),
         "pack_select": ([H, vp, vp, i32, i64, i32, vp, sz, vp, vp, vp, vp], ctypes.c_int),
+        "pack_select_static": ([H, vp, vp, i32, i64, i32, vp, vp, vp, vp], ctypes.c_int),
         "pack_member_param_count": ([H, i32, ctypes.POINTER(i64)], ctypes.c_int),
         "pack_get_params": ([H, i32, vp], ctypes.c_int),
         "pack_set_params": ([H, i32, vp], ctypes.c_int),
@@ -282,6 +283,15 @@ class Pack:
         torch.cuda.current_stream().synchronize()
         k = int(nsel.item())
         return [int(x) for x in sel[:k].cpu()], float(score.item())
+
+    def select_static(self, cand, yv, m_ens, sel, nsel, score):
+        """pack_select_static: the selection of ``select`` into caller-provided
+        device outputs (sel int32 [>= max(m_ens, 1)], nsel int32 [1], score fp64
+        [1]) with the library's static scratch, on the current stream: no
+        allocation and no synchronisation."""
+        C, Nv = cand.shape
+        _check(self.lib.pack_select_static(self.h, cand.data_ptr(), yv.data_ptr(), C, Nv, m_ens, sel.data_ptr(),
+                                           nsel.data_ptr(), score.data_ptr(), _stream()))
 
     # ------------------------------------------------------------ state access
     def param_count(self, k):
