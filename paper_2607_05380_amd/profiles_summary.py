@@ -8,6 +8,9 @@
       `--pmc WRITE_SIZE` runs of `bench.py --copy-calibration`: each counter (KiB per
       dispatch) is scaled by what it reads for the 256 MiB device-to-device copies of
       that run; writes OUT_PREFIX.json (read by bench.py) and OUT_PREFIX.md
+  python -m paper_2607_05380_amd.profiles_summary counters WORKLOAD OUT.md PMC_DIR... --command "..."
+      per-kernel hardware counters of `--pmc` runs (MFMA busy share, wave
+      wait states, L2 hit rate and latency, LDS bank conflicts)
   python -m paper_2607_05380_amd.profiles_summary mfma PMC_DIR BENCH_LOG WORKLOAD OUT.md --command "..."
       executed MFMA work per launch of every GEMM kernel from a `--pmc
       SQ_INSTS_VALU_MFMA_MOPS_BF16` (or _F32) run of `bench.py --profile-steps N`
@@ -254,6 +257,84 @@ def mfma(args):
     print("\n".join(out))
 
 
+def counter_means(dirs):
+    """{kernel: ({counter: mean per dispatch}, dispatches, mean duration ns)} over
+    the counter_collection.csv files of one or more --pmc runs."""
+    vals, durs = {}, {}
+    for d in dirs:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            seen = set()
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    s = short_name(r["Kernel_Name"])
+                    if not s:
+                        continue
+                    vals.setdefault(s, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                    key = (f, r["Dispatch_Id"])
+                    if key not in seen:
+                        seen.add(key)
+                        durs.setdefault((d, s), []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    out = {}
+    for s, cs in vals.items():
+        d_all = [x for (dd, ss), v in durs.items() if ss == s for x in v]
+        n = max(len(v) for (dd, ss), v in durs.items() if ss == s)
+        out[s] = ({c: statistics.mean(v) for c, v in cs.items()}, n, statistics.mean(d_all))
+    return out
+
+
+def counters(args):
+    """Where the GEMM kernels' time goes: per-dispatch hardware counters (each
+    kernel measured alone: counter collection serialises the dispatches)."""
+    res = counter_means(args.dirs)
+    cyc = args.clock_ghz * 1e9
+    simds = args.cus * 4
+    out = ["# Hardware counters of the library kernels, " + args.workload, "", "Commands (one run per counter set):",
+           "", "```", args.command, "```", "",
+           "Counter collection serialises dispatches, so each kernel runs alone here (in the training step the "
+           f"member groups' launches overlap).  Derived per dispatch, at the {args.clock_ghz} GHz shader clock "
+           f"measured during the bench (amd-smi) and {args.cus} CUs x 4 SIMDs:", "",
+           "* MFMA busy: `SQ_VALU_MFMA_BUSY_CYCLES` / (duration x clock x SIMDs) -- the share of the matrix "
+           "cores' cycles spent on MFMA work (one v_mfma_f32_32x32x16_bf16 holds a SIMD for 32 cycles);",
+           "* wave states, shares of `SQ_WAVE_CYCLES`: `SQ_WAIT_ANY` (waiting on a counter: memory or LDS "
+           "data), `SQ_WAIT_INST_ANY` (ready but not issued), `SQ_ACTIVE_INST_ANY` (issuing);",
+           "* L2 hit rate `TCC_HIT` / (`TCC_HIT` + `TCC_MISS`) and mean L2 read latency "
+           "`TCP_TCC_READ_REQ_LATENCY` / `TCP_TCC_READ_REQ` (cycles);",
+           "* LDS bank conflicts: `SQ_LDS_BANK_CONFLICT` / `SQ_ACTIVE_INST_LDS` (conflict cycles per active LDS "
+           "cycle).", "",
+           "| kernel | dispatches | avg us | MFMA busy | wait | ready, not issued | issuing | L2 hit | "
+           "L2 latency (cyc) | LDS conflict |",
+           "|---|---|---|---|---|---|---|---|---|---|"]
+
+    def g(c, k):
+        return c.get(k)
+
+    for s, (c, n, dur) in sorted(res.items(), key=lambda kv: -kv[1][2] * kv[1][1]):
+        if not s.startswith("gemm_") and s not in args.also:
+            continue
+        wc = g(c, "SQ_WAVE_CYCLES") or 0.0
+        mf = g(c, "SQ_VALU_MFMA_BUSY_CYCLES")
+        busy = mf / (dur * 1e-9 * cyc * simds) if mf is not None and dur > 0 else None
+        hit, miss = g(c, "TCC_HIT_sum"), g(c, "TCC_MISS_sum")
+        lat, req = g(c, "TCP_TCC_READ_REQ_LATENCY_sum"), g(c, "TCP_TCC_READ_REQ_sum")
+        lc, la = g(c, "SQ_LDS_BANK_CONFLICT"), g(c, "SQ_ACTIVE_INST_LDS")
+
+        def pct(x):
+            return "n/a" if x is None else f"{100 * x:.1f}%"
+
+        def frac(k):
+            v = g(c, k)
+            return None if v is None or wc <= 0 else v / wc
+
+        out.append(f"| {s} | {n} | {dur / 1e3:.1f} | {pct(busy)} | {pct(frac('SQ_WAIT_ANY'))} | "
+                   f"{pct(frac('SQ_WAIT_INST_ANY'))} | {pct(frac('SQ_ACTIVE_INST_ANY'))} | "
+                   f"{pct(hit / (hit + miss) if hit is not None and miss is not None and hit + miss > 0 else None)} | "
+                   f"{lat / req if lat is not None and req else float('nan'):.0f} | "
+                   f"{pct(lc / la if lc is not None and la else None)} |")
+    with open(args.out, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -274,8 +355,16 @@ def main():
     c.add_argument("out")
     c.add_argument("--dtype", default="bf16")
     c.add_argument("--command", default="")
+    e = sub.add_parser("counters")
+    e.add_argument("workload")
+    e.add_argument("out")
+    e.add_argument("dirs", nargs="+")
+    e.add_argument("--clock-ghz", type=float, default=2.38)
+    e.add_argument("--cus", type=int, default=256)
+    e.add_argument("--also", nargs="*", default=[])
+    e.add_argument("--command", default="")
     args = ap.parse_args()
-    {"stats": stats, "traffic": traffic, "mfma": mfma}[args.cmd](args)
+    {"stats": stats, "traffic": traffic, "mfma": mfma, "counters": counters}[args.cmd](args)
 
 
 if __name__ == "__main__":
