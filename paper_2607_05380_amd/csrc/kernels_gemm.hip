@@ -80,7 +80,18 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int NT = 256;                 // threads per workgroup (2 x 2 waves)
 constexpr int KV = 8;                   // 16-byte vectors of depth per row per K step
 constexpr int ROW = KV * 16;            // 128 bytes of depth per row per K step
-constexpr int kLdsBig = 2 * 2 * 256 * ROW;    // two 64-deep stages of both 256-row operand tiles (128 KB)
+// Big-tile bf16 pipeline: kBigNs stages of kBigKs 16-deep steps of both
+// 256-row operand tiles (the fp32 big path is not used: fp32 runs small tiles).
+#ifndef TABPACK_BIG_KS
+#define TABPACK_BIG_KS 4
+#endif
+#ifndef TABPACK_BIG_NS
+#define TABPACK_BIG_NS 2
+#endif
+constexpr int kBigKs = TABPACK_BIG_KS, kBigNs = TABPACK_BIG_NS;
+constexpr int kLdsBig = kBigNs * 2 * 256 * 32 * kBigKs > 2 * 2 * 256 * ROW ? kBigNs * 2 * 256 * 32 * kBigKs
+                                                                          : 2 * 2 * 256 * ROW;
+static_assert(kLdsBig <= 160 * 1024, "one big-tile workgroup per CU");
 // Small-tile bf16 pipeline: kSmallNs stages of kSmallKs 16-deep MFMA steps.
 #ifndef TABPACK_SMALL_KS
 #define TABPACK_SMALL_KS 4
@@ -1308,7 +1319,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   if (t.shape == kShapeBig) {
-    run_tile<T, AK, BK_, EPI, kShapeBig, 4, 2>(a, d, t, smem, tid, wave);
+    run_tile<T, AK, BK_, EPI, kShapeBig, kBigKs, kBigNs>(a, d, t, smem, tid, wave);
     return;
   }
   run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave);
