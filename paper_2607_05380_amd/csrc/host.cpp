@@ -39,10 +39,6 @@ int fail(int code, const char* fmt, ...) {
 
 constexpr uint32_t kTagHparam = 1, kTagInit = 2;
 constexpr int kGroups = 4;  // at most this many member groups run their GEMM chains concurrently
-#ifndef TABPACK_STAGGER
-#define TABPACK_STAGGER 0
-#endif
-constexpr int kStaggerLayer = TABPACK_STAGGER;  // see the forward pass of pack_train_step
 
 int64_t round_up(int64_t x, int64_t q) { return (x + q - 1) / q * q; }
 
@@ -177,14 +173,13 @@ struct pack_handle {
   // measured faster than one launch over all members.
   int ngroups = 1;
   std::vector<int> group[kGroups];
-  std::vector<int> coltile0;         // bias-partial column tiles of group g, layer l: [coltile0[g L + l - 1], next)
+  int sumtile0[kGroups + 1] = {};    // gradient-sum work items of group g: [sumtile0[g], sumtile0[g + 1])
   int headtile0[kGroups + 1] = {};   // head-backward tiles of group g
   int member0[kGroups + 1] = {};     // group g's members: d_members[member0[g] .. member0[g+1])
   hipStream_t gstream[kGroups] = {};  // streams of groups 1.. (entry 0 unused)
   hipEvent_t ev_split = nullptr, ev_merge[kGroups] = {};
   hipEvent_t ev_gather[kGroups] = {};  // group g's gather done (group g + 1 gathers after it)
-  hipEvent_t ev_fwd[kGroups] = {};     // group g's forward pass through layer kStaggerLayer done
-  hipEvent_t ev_bias[kGroups] = {};    // group g's last data-gradient launch done
+  hipEvent_t ev_bias[kGroups] = {};    // group g's last backward producer done (its gradient sums follow)
   int ncoltiles = 0;
   int nheadtiles = 0;
   int head_rb = 0;  // rows per head-backward block
@@ -448,7 +443,7 @@ struct Plan {
   std::vector<HeadTile> headtiles;
   std::vector<Launch> fwd[2][kGroups], dx[kGroups], dw[kGroups];
   Launch fwd1_eval{};
-  std::vector<int> coltile0;     // [kGroups * L + 1], see build_plan
+  int sumtile0[kGroups + 1] = {};  // see build_plan
   int headtile0[kGroups + 1] = {};
   std::vector<int32_t> members;  // member ids in group order
   int member0[kGroups + 1] = {};
@@ -968,19 +963,22 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     }
     p.dx[hf].push_back(x);
   }
-  // bias-gradient column tiles of the dX launch of layer l (l >= 2) of group g:
-  // coltiles[coltile0[g * L + l - 1] .. coltile0[g * L + l]), the group's members
-  // with at least l hidden blocks
-  p.coltile0.assign((size_t)kGroups * c.L + 1, 0);
-  for (int hf = 0; hf < kGroups; ++hf)
-    for (int l = 1; l <= c.L; ++l) {
-      p.coltile0[(size_t)hf * c.L + l - 1] = (int)p.coltiles.size();
-      if (l >= 2)
-        for (int k : group[hf])
-          if (h->mem[k].depth >= l)
-            for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0, l - 2});
-    }
-  p.coltile0[(size_t)kGroups * c.L] = (int)p.coltiles.size();
+  // gradient-sum work items of group g (one launch after the group's last
+  // backward launch): coltiles[sumtile0[g] .. sumtile0[g + 1]) -- the bias
+  // columns of every dX launch (layer l >= 2: b_{l-1} of the members with at
+  // least l hidden blocks), then every member's head columns, then one loss
+  // item per member
+  for (int hf = 0; hf < kGroups; ++hf) {
+    p.sumtile0[hf] = (int)p.coltiles.size();
+    for (int l = 2; l <= c.L; ++l)
+      for (int k : group[hf])
+        if (h->mem[k].depth >= l)
+          for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0, l - 2});
+    for (int k : group[hf])
+      for (int c0 = 0; c0 < h->mem[k].dp; c0 += 64) p.coltiles.push_back(ColTile{k, c0, kSumHead});
+    for (int k : group[hf]) p.coltiles.push_back(ColTile{k, 0, kSumLoss});
+  }
+  p.sumtile0[kGroups] = (int)p.coltiles.size();
   const TileSet saved_ts = p.tile_set;
   p.tile_set = TILES_SMALL;  // the embedding's data-gradient GEMM runs small tiles only
   for (int hf = 0; hf < kGroups; ++hf) {
@@ -1217,7 +1215,7 @@ int upload_plan(pack_handle* h, hipStream_t stream) {
     h->dw[hf] = plan.dw[hf];
   }
   h->fwd1_eval = plan.fwd1_eval;
-  h->coltile0 = plan.coltile0;
+  for (int g = 0; g <= kGroups; ++g) h->sumtile0[g] = plan.sumtile0[g];
   for (int i = 0; i <= kGroups; ++i) {
     h->headtile0[i] = plan.headtile0[i];
     h->member0[i] = plan.member0[i];
@@ -1394,8 +1392,6 @@ int pack_destroy(pack_handle* h) {
     }
     for (hipEvent_t e : h->ev_gather)
       if (e) (void)hipEventDestroy(e);
-    for (hipEvent_t e : h->ev_fwd)
-      if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : h->ev_bias)
       if (e) (void)hipEventDestroy(e);
   }
@@ -1438,7 +1434,6 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
       HIP_TRY(hipEventCreateWithFlags(&h->ev_merge[g], hipEventDisableTiming));
     }
     for (hipEvent_t& e : h->ev_gather) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    for (hipEvent_t& e : h->ev_fwd) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     for (hipEvent_t& e : h->ev_bias) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
   h->keep_ready = 0;
@@ -1581,17 +1576,26 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     }
     HIP_TRY(hipStreamWaitEvent(s, h->ev_keep[par], 0));
   }
-  // Staggered groups: group g starts its forward GEMMs once group g - 1 has
-  // finished its forward pass through layer kStaggerLayer, so one group's
-  // HBM-bound backward pass (the fused optimizer) overlaps the next group's
-  // MFMA-bound forward pass instead of every group reaching its optimizer
-  // epilogues at once (0: the groups run side by side).
-  for (int hf = 0; hf < ng; ++hf)
-    for (int l = 1; l <= c.L; ++l) {
-      if (kStaggerLayer > 0 && l == 1 && hf > 0) HIP_TRY(hipStreamWaitEvent(hs[hf], h->ev_fwd[hf - 1], 0));
-      HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
-      if (l == std::min(kStaggerLayer, c.L)) HIP_TRY(hipEventRecord(h->ev_fwd[hf], hs[hf]));
-    }
+  // The group's gradient sums (hidden biases from the dX partials, head
+  // weights and last hidden bias from the head partials, loss and head bias
+  // from the per-row values) run as one launch on the side stream once the
+  // group's last producer (its last dX launch, or the head backward for
+  // one-block packs) is done: off the group's chain; the final bias and head
+  // AdamW waits for them.
+  auto grad_sums = [&](int hf) -> hipError_t {
+    hipError_t e = hipEventRecord(h->ev_bias[hf], hs[hf]);
+    if (e == hipSuccess) e = hipStreamWaitEvent(h->side, h->ev_bias[hf], 0);
+    if (e != hipSuccess) return e;
+    const int t0 = h->sumtile0[hf], t1 = h->sumtile0[hf + 1];
+    const double nb = 4.0 * (h->Bp / kPartRows) * 64.0 * (t1 - t0);
+    return timed(h, "grad_sums", 1, 0.0, nb, h->side, [&] {
+      return launch_grad_sums(h->b.colpart, h->A / kPartRows, h->b.headpart, h->head_rb, h->b.rowloss, h->b.dY,
+                              h->b.d_mem, h->b.d_coltiles + t0, t1 - t0, h->Bp, c.B, c.d_out, h->b.d_bias_off, c.K,
+                              h->b.grad, loss_out, h->side);
+    });
+  };
+  for (int l = 1; l <= c.L; ++l)
+    for (int hf = 0; hf < ng; ++hf) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
   for (int hf = 0; hf < ng; ++hf) {
     const hipStream_t s = hs[hf];
     const int32_t* gm = h->b.d_members + h->member0[hf];
@@ -1600,20 +1604,12 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       return launch_head_fwd(h->prec, h->task, kHeadTrain, h->b.H, h->b.theta, h->b.d_mem, gk, h->Bp, c.d_out, y,
                              idx, c.B, c.B, 0, 0, h->b.dY, h->b.rowloss, nullptr, gm, s);
     }));
-    HIP_TRY(timed(h, "loss_reduce", 1, 0.0, (double)gk * c.B * 4 * (1 + c.d_out), s, [&] {
-      return launch_loss_reduce(h->b.rowloss, h->b.dY, h->b.d_mem, gk, h->Bp, c.B, c.d_out, h->b.grad, loss_out,
-                                gm, s);
-    }));
     HIP_TRY(timed(h, "head_bwd", 1, 0.0, 2.0 * act_bytes / ng, s, [&] {
       return launch_head_bwd(h->prec, h->b.H, h->b.theta, h->b.d_mem, h->b.d_headtiles + h->headtile0[hf],
                              h->headtile0[hf + 1] - h->headtile0[hf], h->Bp, h->head_rb, c.d_out, h->b.dY,
                              h->b.dz, h->b.headpart, s);
     }));
-    HIP_TRY(timed(h, "head_grad_reduce", 1, 0.0, 4.0 * (h->Bp / h->head_rb) * (c.d_out + 1) * (h->A / h->Bp) / ng, s,
-                  [&] {
-                    return launch_head_grad_reduce(h->b.headpart, h->b.d_mem, gk, max_dp, h->Bp, h->head_rb,
-                                                   c.d_out, h->b.grad, gm, s);
-                  }));
+    if (c.L == 1) HIP_TRY(grad_sums(hf));
   }
   // the next step's keep words go to the other buffer (last read by the
   // previous step's forward pass) while this step's backward runs
@@ -1628,20 +1624,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       // dX_l reads W_l, so it runs before the weight-gradient GEMM updates W_l in place
       if (l > 1) {
         HIP_TRY(gemm(OP_KMAJ, OP_RMAJ, EPI_DX, h->dx[hf][l - 1], l, s));
-        if (l == 2) {
-          // the group's last dX launch: the sums of every layer's bias-gradient
-          // partials (each layer has its own partial buffer) run on the side
-          // stream, off the group's chain; the final bias AdamW waits for them
-          HIP_TRY(hipEventRecord(h->ev_bias[hf], s));
-          HIP_TRY(hipStreamWaitEvent(h->side, h->ev_bias[hf], 0));
-          HIP_TRY(timed(h, "bias_from_partials", 1, 0.0, act_bytes * 4 * (c.L - 1) / h->elt() / kPartRows / ng,
-                        h->side, [&] {
-                          const int t0 = h->coltile0[(size_t)hf * c.L + 1], t1 = h->coltile0[(size_t)hf * c.L + c.L];
-                          return launch_bias_from_partials(h->b.colpart, h->A / kPartRows, h->b.d_mem,
-                                                           h->b.d_coltiles + t0, t1 - t0, h->Bp / kPartRows,
-                                                           h->b.d_bias_off, c.K, h->b.grad, h->side);
-                        }));
-        }
+        if (l == 2) HIP_TRY(grad_sums(hf));
       }
       if (l == 1 && h->emb) {
         // dE = dZ_1 W_1, before W_1 is updated, reduced in the GEMM's epilogue

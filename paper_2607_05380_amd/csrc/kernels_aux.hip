@@ -223,25 +223,6 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, co
   rowloss[(int64_t)k * Bp + row] = loss;
 }
 
-// Per-member batch-mean loss and head-bias gradient (fixed-order fp64 sums).
-__global__ __launch_bounds__(256) void loss_reduce_kernel(const float* rowloss, const float* dY,
-                                                          const MemberDev* mem, int Bp, int B,
-                                                          int d_out, float* grad, float* loss_out,
-                                                          const int32_t* members) {
-  __shared__ double sh[4];
-  const int k = members ? members[blockIdx.x] : (int)blockIdx.x;
-  double s = 0.0;
-  for (int r = threadIdx.x; r < B; r += 256) s += (double)rowloss[(int64_t)k * Bp + r];
-  s = block_sum_d(s, sh);
-  if (threadIdx.x == 0) loss_out[k] = (float)(s / (double)B);
-  for (int o = 0; o < d_out; ++o) {
-    double g = 0.0;
-    for (int r = threadIdx.x; r < B; r += 256) g += (double)dY[((int64_t)k * Bp + r) * d_out + o];
-    g = block_sum_d(g, sh);
-    if (threadIdx.x == 0) grad[mem[k].b_out_off + o] = (float)g;
-  }
-}
-
 // CPT consecutive activations of one row.
 template <typename T, int CPT>
 struct VecN;
@@ -352,44 +333,56 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* 
   }
 }
 
-// dW_out and db_L of every member from the head backward's row-block partials
-// (fixed order over the row blocks).
-__global__ __launch_bounds__(256) void head_grad_reduce_kernel(const float* part, const MemberDev* mem, int Bp,
-                                                               int nrb, int d_out, float* grad,
-                                                               const int32_t* members) {
-  const int k = members ? members[blockIdx.y] : (int)blockIdx.y;
-  const MemberDev md = mem[k];
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= md.dp) return;
-  const float* pk = part + (int64_t)nrb * (d_out + 1) * (md.act_off / Bp);
-  for (int o = 0; o <= d_out; ++o) {
-    float s = 0.0f;
-    for (int rb = 0; rb < nrb; ++rb) s += pk[((int64_t)rb * (d_out + 1) + o) * md.dp + c];
-    if (o < d_out)
-      grad[md.w_out_off + (int64_t)o * md.dp + c] = s;
-    else
-      grad[md.b_last_off + c] = s;
-  }
-}
-
-// db_l[c] = sum of the per-row-block column partials written by the dX epilogue,
-// in a fixed order; one wave per 64 columns of one member and layer (the
-// partials of bias layer j at part + j * part_stride, its offsets at
-// bias_off[j * K + member]).
-__global__ __launch_bounds__(256) void bias_from_partials_kernel(const float* part, int64_t part_stride,
-                                                                 const MemberDev* mem, const ColTile* tiles,
-                                                                 int ntiles, int nparts, const int64_t* bias_off,
-                                                                 int K, float* grad) {
+// The gradient sums of a member group, one wave per ColTile (fixed orders):
+//   part >= 0: db_{part+1}[c] = sum over the 64-row blocks of the dX
+//     epilogue's column partials (bias layer part at colpart + part * part_stride);
+//   kSumHead:  dW_out[o][c] and db_L[c] = sums over the head backward's row blocks;
+//   kSumLoss:  the batch-mean loss of the member (fp64 over its B rows) and
+//     db_out[o] = sum of dY over the rows (fp64).
+__global__ __launch_bounds__(256) void grad_sums_kernel(const float* colpart, int64_t part_stride,
+                                                        const float* headpart, int RB, const float* rowloss,
+                                                        const float* dY, const MemberDev* mem, const ColTile* tiles,
+                                                        int ntiles, int Bp, int B, int d_out,
+                                                        const int64_t* bias_off, int K, float* grad,
+                                                        float* loss_out) {
   const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (w >= ntiles) return;
   const ColTile ct = tiles[w];
   const MemberDev md = mem[ct.member];
-  const int c = ct.c0 + (threadIdx.x & 63);
+  const int lane = threadIdx.x & 63;
+  if (ct.part == kSumLoss) {
+    const int64_t r0 = (int64_t)ct.member * Bp;
+    double s = 0.0;
+    for (int r = lane; r < B; r += 64) s += (double)rowloss[r0 + r];
+    s = wave_sum_d(s);
+    if (lane == 0) loss_out[ct.member] = (float)(s / (double)B);
+    for (int o = 0; o < d_out; ++o) {
+      double g = 0.0;
+      for (int r = lane; r < B; r += 64) g += (double)dY[(r0 + r) * d_out + o];
+      g = wave_sum_d(g);
+      if (lane == 0) grad[md.b_out_off + o] = (float)g;
+    }
+    return;
+  }
+  const int c = ct.c0 + lane;
   if (c >= md.dp) return;
-  const float* p = part + ct.part * part_stride + md.act_off / kPartRows;
-  float s = 0.0f;
-  for (int r = 0; r < nparts; ++r) s += p[(int64_t)r * md.dp + c];
-  grad[bias_off[(int64_t)ct.part * K + ct.member] + c] = s;
+  if (ct.part == kSumHead) {
+    const int nrb = Bp / RB;
+    const float* pk = headpart + (int64_t)nrb * (d_out + 1) * (md.act_off / Bp);
+    for (int o = 0; o <= d_out; ++o) {
+      float v = 0.0f;
+      for (int rb = 0; rb < nrb; ++rb) v += pk[((int64_t)rb * (d_out + 1) + o) * md.dp + c];
+      if (o < d_out)
+        grad[md.w_out_off + (int64_t)o * md.dp + c] = v;
+      else
+        grad[md.b_last_off + c] = v;
+    }
+    return;
+  }
+  const float* p = colpart + ct.part * part_stride + md.act_off / kPartRows;
+  float v = 0.0f;
+  for (int r = 0; r < Bp / kPartRows; ++r) v += p[(int64_t)r * md.dp + c];
+  grad[bias_off[(int64_t)ct.part * K + ct.member] + c] = v;
 }
 
 // ----------------------------------------------------------------- gather --
@@ -802,14 +795,6 @@ void head_bwd_d(int d_out, int ntiles, hipStream_t s, const void* H, const float
 
 int head_bwd_cols(int d_out) { return d_out <= 4 ? 256 : 128; }
 
-hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const MemberDev* mem, int K,
-                              int Bp, int B, int d_out, float* grad, float* loss_out, const int32_t* members,
-                              hipStream_t s) {
-  if (K <= 0) return hipSuccess;
-  hipLaunchKernelGGL(loss_reduce_kernel, dim3(K), dim3(256), 0, s, rowloss, dY, mem, Bp, B, d_out,
-                     grad, loss_out, members);
-  return hipGetLastError();
-}
 
 hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const MemberDev* mem,
                            const HeadTile* tiles, int ntiles, int Bp, int RB, int d_out, const float* dY,
@@ -823,20 +808,15 @@ hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const M
   return hipGetLastError();
 }
 
-hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int K, int max_dp, int Bp, int RB,
-                                   int d_out, float* grad, const int32_t* members, hipStream_t s) {
-  if (K <= 0) return hipSuccess;
-  hipLaunchKernelGGL(head_grad_reduce_kernel, dim3((max_dp + 255) / 256, K), dim3(256), 0, s, part, mem, Bp, Bp / RB,
-                     d_out, grad, members);
-  return hipGetLastError();
-}
 
-hipError_t launch_bias_from_partials(const float* part, int64_t part_stride, const MemberDev* mem,
-                                     const ColTile* tiles, int ntiles, int nparts, const int64_t* bias_off, int K,
-                                     float* grad, hipStream_t s) {
+hipError_t launch_grad_sums(const float* colpart, int64_t part_stride, const float* headpart, int RB,
+                            const float* rowloss, const float* dY, const MemberDev* mem, const ColTile* tiles,
+                            int ntiles, int Bp, int B, int d_out, const int64_t* bias_off, int K, float* grad,
+                            float* loss_out, hipStream_t s) {
+  if (RB <= 0 || Bp % RB != 0 || Bp % kPartRows != 0) return hipErrorInvalidValue;
   if (ntiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL(bias_from_partials_kernel, dim3((ntiles + 3) / 4), dim3(256), 0, s, part, part_stride, mem,
-                     tiles, ntiles, nparts, bias_off, K, grad);
+  hipLaunchKernelGGL(grad_sums_kernel, dim3((ntiles + 3) / 4), dim3(256), 0, s, colpart, part_stride, headpart, RB,
+                     rowloss, dY, mem, tiles, ntiles, Bp, B, d_out, bias_off, K, grad, loss_out);
   return hipGetLastError();
 }
 

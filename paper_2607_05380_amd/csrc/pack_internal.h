@@ -158,11 +158,14 @@ struct HeadTile {            // (member, first column, first row) block of the h
   int32_t member, c0, r0;
 };
 
-struct ColTile {            // (member, first column, bias layer) work item of the bias-gradient sums
+struct ColTile {            // (member, first column, kind) work item of the gradient sums
   int32_t member;
   int32_t c0;
-  int32_t part;             // b_{part + 1}: the partials of the dX launch of layer part + 2
+  int32_t part;             // >= 0: b_{part + 1} from the partials of the dX launch of layer part + 2;
+                            // kSumHead: W_out and b_L from the head backward's partials;
+                            // kSumLoss: the member's batch-mean loss and b_out (c0 = 0)
 };
+constexpr int32_t kSumHead = -1, kSumLoss = -2;
 
 // Launchers (kernels_gemm.hip).
 hipError_t launch_gemm(Prec prec, OpKind a, OpKind b, EpiKind e, const GemmArgs& args, hipStream_t s);
@@ -175,14 +178,9 @@ hipError_t launch_head_fwd(Prec prec, Task task, int mode, const void* H, const 
                            const MemberDev* mem, int K, int Bp, int d_out, const void* y,
                            const int32_t* idx, int B, int rows_valid, int64_t row_base, int64_t Nv,
                            float* dY, float* rowloss, float* pred, const int32_t* members, hipStream_t s);
-hipError_t launch_loss_reduce(const float* rowloss, const float* dY, const MemberDev* mem, int K,
-                              int Bp, int B, int d_out, float* grad, float* loss_out, const int32_t* members,
-                              hipStream_t s);
 hipError_t launch_head_bwd(Prec prec, const void* H, const float* theta, const MemberDev* mem,
                            const HeadTile* tiles, int ntiles, int Bp, int RB, int d_out, const float* dY,
                            void* dZ, float* part, hipStream_t s);
-hipError_t launch_head_grad_reduce(const float* part, const MemberDev* mem, int K, int max_dp, int Bp, int RB,
-                                   int d_out, float* grad, const int32_t* members, hipStream_t s);
 int head_bwd_cols(int d_out);  // columns one head-backward block covers
 // The greedy selection of pack_select() with the caller's scratch `work`
 // (pack_select_workspace_size() bytes, 256-byte aligned); returns a PACK_*
@@ -192,9 +190,16 @@ int select_with_scratch(pack_handle* h, const float* cand, const void* yv, int32
                         hipStream_t stream);
 // Sets the library's last error message; returns code.
 int set_error(int code, const char* msg);
-hipError_t launch_bias_from_partials(const float* part, int64_t part_stride, const MemberDev* mem,
-                                     const ColTile* tiles, int ntiles, int nparts, const int64_t* bias_off, int K,
-                                     float* grad, hipStream_t s);
+// The gradient sums of one member group after its last backward launch (one
+// wave per ColTile): hidden-layer bias gradients from the dX epilogues'
+// partials (bias layer j at colpart + j * part_stride), the head weight and
+// last hidden bias gradients from the head backward's partials (RB rows per
+// block), and each member's loss (loss_out) and head-bias gradient from the
+// per-row losses and dY.  Fixed summation orders.
+hipError_t launch_grad_sums(const float* colpart, int64_t part_stride, const float* headpart, int RB,
+                            const float* rowloss, const float* dY, const MemberDev* mem, const ColTile* tiles,
+                            int ntiles, int Bp, int B, int d_out, const int64_t* bias_off, int K, float* grad,
+                            float* loss_out, hipStream_t s);
 hipError_t launch_gather(Prec prec, const float* X, int d_in, int Pin, const int32_t* idx, int B,
                          int64_t row_base, int rows_valid, int members, int Bp, void* H0,
                          const int32_t* member_ids, hipStream_t s);

@@ -33,7 +33,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 COPY_BYTES = 256 << 20
 OPS = ["kmaj", "rmaj"]
 EPIS = ["fwd", "fwd_eval", "dx", "dw", "ns", "de"]
-SIMPLE = ["dropout_words", "head_grad_reduce", "head_fwd", "head_bwd", "loss_reduce", "bias_from_partials",
+SIMPLE = ["dropout_words", "grad_sums", "head_grad_reduce", "head_fwd", "head_bwd", "loss_reduce", "bias_from_partials",
           "gather", "adamw", "to_shadow", "eval_score", "dropout_mask", "select_partial", "select_pick",
           "select_update", "select_init", "select_final", "ensemble_mean", "muon_prep", "muon_norm",
           "muon_convert", "muon_update", "embed_fwd", "embed_grad", "idx_check", "stream_copy"]
