@@ -116,6 +116,17 @@ def test_explicit_edge_members_fp32():
         compare_member(pk, op, k, run_step.p0[k], TOL["fp32"])
 
 
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_one_block_pack(prec):
+    # L = 1: the head backward is the group's last producer, so the gradient
+    # sums (loss, head and bias gradients) follow it directly
+    cfg = configs.workload("multiclass_lognormal", K=5, B=300, L=1, precision=prec)
+    pk, op, losses, _ = run_step(cfg)
+    check_tensor("loss", losses[0][0], losses[0][1], TOL[prec])
+    for k in range(cfg["K"]):
+        compare_member(pk, op, k, run_step.p0[k], TOL[prec])
+
+
 def test_dropout_masks_bit_exact_and_applied():
     cfg = configs.workload("regression_large", K=4, B=300)
     pk, op, _, _ = run_step(cfg)
