@@ -163,7 +163,7 @@ def per_epoch(cfg, pk, Xtr, ytr, Xva, yva, step, online_epochs):
     return res, step
 
 
-def variable_depth(cfg, Xtr, ytr, steps=20):
+def variable_depth(cfg, Xtr, ytr, steps=20, stream_rows=True):
     """Step time of the same workload with member depths ~ UniformInt[1, L]
     (App. F samples the number of layers): shallower members leave the deeper
     layers' launches, so the step should scale with the GEMM work."""
@@ -171,6 +171,8 @@ def variable_depth(cfg, Xtr, ytr, steps=20):
     from paper_2607_05380_amd import tabpack
     L, d_in = cfg["L"], cfg["d_in"]
     pk = tabpack.Pack(dict(cfg, depth_lo=1, depth_hi=L, keep_grads=0)).bind(Xtr.device)
+    if stream_rows and pk.can_bind_data():
+        pk.bind_data(Xtr)
     hp = pk.hparams()
     idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
@@ -192,13 +194,15 @@ MUON_OPTS = dict(optimizer="muon", muon_lr_lo=1e-3, muon_lr_hi=1e-1)
 EMB_OPTS = dict(emb_lo=8, emb_hi=32, emb_step=4, sigma_lo=1e-2, sigma_hi=10.0)
 
 
-def muon_optimizer(cfg, Xtr, ytr, steps=20):
+def muon_optimizer(cfg, Xtr, ytr, steps=20, stream_rows=True):
     """Step time of the same workload with the paper's default optimizer split:
     Muon for the hidden weights (Newton-Schulz on the grouped GEMMs), AdamW for
     biases and heads; and the Newton-Schulz GEMMs' rate (library events)."""
     import torch
     from paper_2607_05380_amd import tabpack
     pk = tabpack.Pack(dict(cfg, keep_grads=0, **MUON_OPTS)).bind(Xtr.device)
+    if stream_rows and pk.can_bind_data():
+        pk.bind_data(Xtr)
     idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
     pk.train_step(Xtr, ytr, idx, 1, loss)
@@ -309,6 +313,10 @@ def main():
     ap.add_argument("--variant", choices=["adamw", "muon", "embeddings"], default="adamw",
                     help="the timed step's options: AdamW for everything (the metric), Muon for the hidden "
                          "weights, or periodic feature embeddings (for profiling those steps on their own)")
+    ap.add_argument("--rows", choices=["stream", "gather"], default="stream",
+                    help="how the first layer gets its batch rows: read straight from a bf16 copy of X through "
+                         "the batch indices (pack_bind_data; bf16 packs without embeddings), or gathered into a "
+                         "dense batch before the first GEMM")
     a = ap.parse_args()
     if a.gpus != 1:
         print(f"bench.py measures one GPU: the packed step runs all members on one device and this "
@@ -335,6 +343,10 @@ def main():
     variant = {"adamw": {}, "muon": MUON_OPTS, "embeddings": EMB_OPTS}[a.variant]
     pk = tabpack.Pack(dict(cfg, keep_grads=int(a.keep_grads), **variant)).bind(dev)
     log(f"bound: workspace {pk.workspace_bytes() / 2**30:.2f} GiB")
+    stream_rows = a.rows == "stream" and pk.can_bind_data()
+    if stream_rows:
+        pk.bind_data(Xtr)  # one bf16 copy of X, made before any step (like the data upload)
+        log(f"first-layer rows streamed from a bf16 copy of X ({pk.xb.numel() * 2 / 2**30:.2f} GiB)")
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=dev)
     step = 0
     for _ in range(a.warmup):
@@ -432,6 +444,7 @@ def main():
         "config": {"workload": cfg["name"], "K": cfg["K"], "B": cfg["B"], "d_in": cfg["d_in"], "L": cfg["L"],
                    "widths": [cfg["width_lo"], cfg["width_hi"]], "n_train": cfg["n_train"],
                    "task": cfg["task"], "keep_grads": int(a.keep_grads),
+                   "first_layer_rows": "streamed" if stream_rows else "gathered",
                    **({} if a.variant == "adamw" else {"variant": a.variant})},
         "roofline": roofline,
         "kernels": [{"name": s["name"], "bound": s["kind"], "avg_us": round(s["avg_ms"] * 1e3, 2),
@@ -444,9 +457,9 @@ def main():
         log("per-epoch work: validation, selection, member removal, online driver")
         out["per_epoch"], step = per_epoch(cfg, pk, Xtr, ytr, Xva, yva, step, a.online_epochs)
         log(f"  {json.dumps(out['per_epoch'])}")
-        out["variable_depth"] = variable_depth(cfg, Xtr, ytr)
+        out["variable_depth"] = variable_depth(cfg, Xtr, ytr, stream_rows=stream_rows)
         log(f"  variable depth: {json.dumps(out['variable_depth'])}")
-        out["muon"] = muon_optimizer(cfg, Xtr, ytr)
+        out["muon"] = muon_optimizer(cfg, Xtr, ytr, stream_rows=stream_rows)
         log(f"  Muon optimizer: {json.dumps(out['muon'])}")
         out["embeddings"] = embeddings(cfg, Xtr, ytr)
         log(f"  periodic embeddings: {json.dumps(out['embeddings'])}")

@@ -188,6 +188,25 @@ int pack_set_active(pack_handle* h, const uint8_t* active, hipStream_t stream);
 int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N,
                     const int32_t* idx, uint64_t step, float* loss_out, hipStream_t stream);
 
+/* Optional: take the first layer's batch rows straight from the training
+ * data (Section 3.3: each member's base batch is a set of rows of X chosen by
+ * its indices).  Converts X once into xb (bf16, N rows of d_in rounded up to
+ * a multiple of 8, zero-filled) on `stream`; the first layer's forward GEMM of
+ * every later pack_train_step() then loads its rows from xb through the batch
+ * indices, and so does its weight-gradient GEMM: no gathered copy of the
+ * batch is made.  Results are bit-identical to the unbound step.
+ *   X      device fp32 [N, d_in], the X every following pack_train_step()
+ *          passes (same pointer and N; PACK_EINVAL otherwise); NULL unbinds
+ *          (the step then gathers the batch before the first GEMM again)
+ *   xb     device buffer owned by the caller, 16-byte aligned, at least
+ *          N * round_up(d_in, 8) * 2 bytes (at most 2 GiB), kept until the
+ *          data is unbound or the pack destroyed.  The steps read the copy:
+ *          after a change of X's contents, call pack_bind_data() again
+ * bf16 packs without feature embeddings and with B <= PACK_BIND_DATA_MAX_B
+ * only (PACK_EINVAL otherwise). */
+#define PACK_BIND_DATA_MAX_B 2048
+int pack_bind_data(pack_handle* h, const float* X, int64_t N, void* xb, size_t xb_bytes, hipStream_t stream);
+
 /* Evaluate every active member on validation rows without dropout (Section
  * 3.5 / 3.6: per-epoch validation scoring feeds early stopping and selection).
  *   pred_out  device fp32 [K, Nv]: the per-row value an ensemble averages --

@@ -141,6 +141,13 @@ struct pack_handle {
   Prec prec;
   Task task;
   int q, Bp, Pin;
+  // pack_bind_data: the first layer's forward and weight-gradient GEMMs read
+  // the batch rows straight from a bf16 copy of X (xb, data_N rows of Pin)
+  // through the batch indices; no H_0 is gathered
+  bool stream_rows = false;
+  const float* data_X = nullptr;
+  int64_t data_N = 0;
+  void* xb = nullptr;
   std::vector<Member> mem;
   int64_t P = 0;     // packed parameter count (multiple of kChunk)
   int64_t A = 0;     // elements of one activation buffer (all members)
@@ -856,6 +863,13 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       d.drop_s = (float)m.scale;
       d.mask = maskp(l, k);
       d.keepw = keepw(par, l, k);
+      if (l == 1 && h->stream_rows && m.d_emb == 0 && !sizing) {  // rows straight from the data copy
+        d.A = h->xb;
+        d.lda = h->Pin;
+        d.xrows = bf.idx_ok + (size_t)k * c.B;
+        d.xrows_n = c.B;
+        d.xsrc_rows = h->data_N;
+      }
       add_tiles(p, f, (int)p.descs.size(), h->Bp, m.dp, d.Kd);
       p.descs.push_back(d);
       {
@@ -882,6 +896,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
         const int k = group[hf][i];
         GemmDesc d = p.descs[p.fwd[0][hf][0].desc0 + i];
         if (h->mem[k].d_emb == 0) d.A = h0(0);  // embedded members read their own E block
+        d.xrows = nullptr;                      // evaluation reads the gathered validation rows
         add_tiles(p, f, (int)p.descs.size(), h->Bp, h->mem[k].dp, d.Kd);
         p.descs.push_back(d);
       }
@@ -914,6 +929,13 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       d.poff = m.toff[2 * (l - 1)];
       d.lr = (float)m.lr;
       d.wd = (float)m.wd;
+      if (l == 1 && h->stream_rows && m.d_emb == 0 && !sizing) {  // rows straight from the data copy
+        d.B = h->xb;
+        d.ldb = h->Pin;
+        d.xrows = bf.idx_ok + (size_t)k * c.B;
+        d.xrows_n = c.B;
+        d.xsrc_rows = h->data_N;
+      }
       add_tiles(p, w, (int)p.descs.size(), d.M, d.N, d.Kd);
       p.descs.push_back(d);
       {
@@ -1483,6 +1505,9 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   if (step != h->t + 1) return fail(PACK_ESTATE, "step %llu given, %llu expected", (unsigned long long)step,
                                     (unsigned long long)(h->t + 1));
   if (h->active_ids.empty()) return fail(PACK_ESTATE, "no member is active");
+  if (h->stream_rows && (X != h->data_X || N != h->data_N))
+    return fail(PACK_EINVAL, "X / N differ from the data bound with pack_bind_data (bind it again, or unbind "
+                             "it with X = NULL)");
   const pack_config& c = h->cfg;
   const int nact = (int)h->active_ids.size();
   GemmArgs a = base_args(h);
@@ -1563,7 +1588,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
                                 h->b.d_members + h->member0[hf], gk, max_pin(h, h->group[hf]), h->b.theta,
                                 h->b.H0, s);
       }));
-    } else {
+    } else if (!h->stream_rows) {
       // the groups' gathers (HBM-bound) run one after another, so a group's
       // forward GEMMs overlap the next group's gather instead of every group
       // waiting for three concurrent gathers
@@ -1777,6 +1802,35 @@ int pack_status(pack_handle* h, uint32_t* flags, hipStream_t stream) {
   }
   *flags = v;
   return PACK_OK;
+}
+
+static_assert(kMapRows == PACK_BIND_DATA_MAX_B, "the weight-gradient kernels' row table holds a whole batch");
+
+int pack_bind_data(pack_handle* h, const float* X, int64_t N, void* xb, size_t xb_bytes, hipStream_t stream) {
+  if (!h) return fail(PACK_EINVAL, "handle is NULL");
+  if (!h->bound) return fail(PACK_ESTATE, "pack_bind() has not been called");
+  if (!X) {  // unbind: the batch gather feeds the first layer again
+    h->stream_rows = false;
+    h->data_X = nullptr;
+    h->data_N = 0;
+    h->xb = nullptr;
+    return upload_plan(h, stream);
+  }
+  if (h->prec != Prec::BF16 || h->emb)
+    return fail(PACK_EINVAL, "pack_bind_data needs a bf16 pack without feature embeddings");
+  if (N < 1 || !xb) return fail(PACK_EINVAL, "N must be positive and xb set");
+  if (h->cfg.B > kMapRows) return fail(PACK_EINVAL, "streamed rows take batches of at most %d rows", kMapRows);
+  const size_t need = (size_t)N * h->Pin * 2;
+  if (xb_bytes < need) return fail(PACK_EINVAL, "xb has %zu bytes, %zu needed", xb_bytes, need);
+  if (reinterpret_cast<uintptr_t>(xb) % 16) return fail(PACK_EINVAL, "xb must be 16-byte aligned");
+  if (need + 16 >= ((size_t)1 << 31))
+    return fail(PACK_EINVAL, "N x d_in too large for streamed rows (%zu bytes; at most 2 GiB)", need);
+  HIP_TRY(launch_rows_to_bf16(X, N, h->cfg.d_in, h->Pin, xb, stream));
+  h->stream_rows = true;
+  h->data_X = X;
+  h->data_N = N;
+  h->xb = xb;
+  return upload_plan(h, stream);  // the first layer's descriptors read xb through the batch indices
 }
 
 int pack_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {

@@ -507,6 +507,26 @@ __global__ __launch_bounds__(256) void adamw_kernel(float* theta, const float* g
   }
 }
 
+// xb row r = X row r in bf16, zero-padded from d_in to Pin columns: one
+// thread per 8 output columns (one 16-byte store).
+__global__ __launch_bounds__(256) void rows_to_bf16_kernel(const float* X, int64_t N, int d_in, int Pin,
+                                                           __bf16* xb) {
+  const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int vpr = Pin / 8;
+  if (v >= N * vpr) return;
+  const int64_t r = v / vpr;
+  const int c0 = (int)(v - r * vpr) * 8;
+  const float* x = X + r * d_in;
+  uint32_t w[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int c = c0 + 2 * q;
+    const float a = c < d_in ? x[c] : 0.0f, b = c + 1 < d_in ? x[c + 1] : 0.0f;
+    w[q] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)a) | ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)b) << 16);
+  }
+  *reinterpret_cast<uint4*>(xb + r * Pin + c0) = uint4{w[0], w[1], w[2], w[3]};
+}
+
 __global__ void to_shadow_kernel(const float* theta, uint16_t* shadow, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
@@ -869,6 +889,15 @@ hipError_t launch_ensemble_mean(const float* part, int n, int Bp, int rows, int 
   const int64_t ne = (int64_t)rows * d_out;
   hipLaunchKernelGGL(ensemble_mean_kernel, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, s, part, n, Bp, rows,
                      d_out, row_base, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_to_bf16(const float* X, int64_t N, int d_in, int Pin, void* xb, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  if (Pin % 8 || Pin < d_in) return hipErrorInvalidValue;
+  const int64_t nv = N * (Pin / 8);
+  hipLaunchKernelGGL(rows_to_bf16_kernel, dim3((unsigned)((nv + 255) / 256)), dim3(256), 0, s, X, N, d_in, Pin,
+                     static_cast<__bf16*>(xb));
   return hipGetLastError();
 }
 

@@ -123,6 +123,12 @@ constexpr int kTallKs = TABPACK_TALL_KS, kTallNs = TABPACK_TALL_NS;
 constexpr int kLdsTallBf16 = kTallNs * (256 + 128) * 32 * kTallKs;
 constexpr int kLdsTall = kLdsTallBf16 > kLdsSmallBf16 ? kLdsTallBf16 : kLdsSmallBf16;
 static_assert(kLdsTall <= 80 * 1024, "two tall-tile workgroups per CU");
+// LDS table of the batch rows' row numbers in the data copy for the weight
+// gradient of the first layer (bf16 kernels of EPI_DW only)
+template <typename T, int EPI>
+constexpr int XMapBytes = (EPI == EPI_DW && sizeof(T) == 2) ? kMapRows * 4 : 0;
+static_assert((kLdsSmallBf16 + kMapRows * 4) * kSmallWpeBf16 <= 160 * 1024, "small weight-gradient occupancy");
+static_assert(kLdsBig + kMapRows * 4 <= 160 * 1024, "one big-tile workgroup per CU");
 
 template <int SH>
 struct Shape;
@@ -336,6 +342,7 @@ struct LoadRmajF32 {
 // offset past the buffer's range and reads zeros; depth beyond K can only
 // occur in the last K step, which checks it per lane.
 typedef void __attribute__((address_space(3)))* lptr_t;
+typedef __attribute__((address_space(3))) int32_t lds_i32;
 
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff, uint32_t soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lptr_t)lds, 16, voff, soff, 0, 0);
@@ -356,8 +363,11 @@ struct DmaKmaj {
   uint32_t voff[PER];  // byte offset (depth 0) of this lane's vector in block p, or kOob
   int kofs[2];         // depth offset (elements) of this lane's vector per block parity
   int wave;
-  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int, int wave_, int lane) {
-    rsrc = make_rsrc(P, (int64_t)rbound * ld * 2);
+  // rows != nullptr: row r < nrows of the operand is row rows[r] of P (src_rows
+  // rows), rows >= nrows read as zero
+  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int, int wave_, int lane,
+                       const int32_t* rows = nullptr, int nrows = 0, int64_t src_rows = 0) {
+    rsrc = make_rsrc(P, (rows ? src_rows : (int64_t)rbound) * ld * 2);
     wave = wave_;
     const int r = lane / CPR;
 #pragma unroll
@@ -367,8 +377,11 @@ struct DmaKmaj {
     }
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
-      const int row = (wave * PER + p) * BR + r;
-      voff[p] = row0 + row < rbound ? (uint32_t)(((int64_t)(row0 + row) * ld + kofs[p & 1]) * 2) : kOob;
+      const int row = row0 + (wave * PER + p) * BR + r;
+      if (rows)
+        voff[p] = row < nrows ? (uint32_t)(((int64_t)rows[row] * ld + kofs[p & 1]) * 2) : kOob;
+      else
+        voff[p] = row < rbound ? (uint32_t)(((int64_t)row * ld + kofs[p & 1]) * 2) : kOob;
     }
   }
   __device__ void issue(char* lds, int k0, int kd) const {
@@ -395,10 +408,17 @@ struct DmaRmaj {
   uint32_t voff[PER];  // byte offset (depth 0) of the vector this lane fetches for chunk p, or kOob
   int krow[PER];       // its depth row inside a K step
   int wave;
-  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int kd, int wave_, int lane) {
-    rsrc = make_rsrc(P, (int64_t)kd * ld * 2);
+  // map != nullptr: depth row k < nmap is row map[k] (an LDS table) of P
+  // (src_rows rows), depth rows >= nmap read as zero
+  const lds_i32* map;
+  int nmap;
+  __device__ void init(const __bf16* P, int64_t ld, int row0, int rbound, int kd, int wave_, int lane,
+                       const lds_i32* map_ = nullptr, int nmap_ = 0, int64_t src_rows = 0) {
+    rsrc = make_rsrc(P, (map_ ? src_rows : (int64_t)kd) * ld * 2);
     wave = wave_;
     ldb = (uint32_t)(ld * 2);
+    map = map_;
+    nmap = nmap_;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int pos = (wave * PER + p) * 1024 + lane * 16;
@@ -406,10 +426,20 @@ struct DmaRmaj {
       const int chunk = (b >> 5) ^ ((k & 3) << 1);
       const int col = chunk * 16 + ((b >> 4) & 1) * 8;
       krow[p] = k;
-      voff[p] = row0 + col < rbound ? (uint32_t)(k * (int64_t)ldb + (int64_t)(row0 + col) * 2) : kOob;
+      const int64_t dep = map_ ? 0 : k * (int64_t)ldb;
+      voff[p] = row0 + col < rbound ? (uint32_t)(dep + (int64_t)(row0 + col) * 2) : kOob;
     }
   }
   __device__ void issue(char* lds, int k0, int kd) const {
+    if (map) {  // wave-uniform
+#pragma unroll
+      for (int p = 0; p < PER; ++p) {
+        const int k = k0 + krow[p];
+        const uint32_t o = k < nmap && voff[p] != kOob ? (uint32_t)map[k] * ldb + voff[p] : kOob;
+        dma16(rsrc, lds + (wave * PER + p) * 1024, o, 0);
+      }
+      return;
+    }
     const uint32_t soff = (uint32_t)k0 * ldb;
     if (k0 + 16 * KS <= kd) {
 #pragma unroll
@@ -1211,7 +1241,7 @@ __device__ __forceinline__ void epilogue_de(const GemmArgs& a, const GemmDesc& d
 
 template <typename T, int AK, int BK_, int EPI, int SH, int KS, int NS>
 __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, const Tile& t, char* lds0, int tid,
-                                         int wave) {
+                                         int wave, char* xmap = nullptr) {
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM, TN = Shape<SH>::TN;
   using LA = LoaderFor<T, AK, TM, KS>;
   using LB = LoaderFor<T, BK_, TN, KS>;
@@ -1244,8 +1274,22 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
     constexpr int TA = TM * 32 * KS, TB = TN * 32 * KS;  // operand tile bytes per K step
     constexpr int PS = LA::type::PER + LB::type::PER;  // direct loads per wave per K step
     const int nk = (d.Kd + BKE - 1) / BKE;
-    la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane);
-    lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane);
+    if constexpr (AK == OP_KMAJ && (EPI == EPI_FWD || EPI == EPI_FWD_EVAL))
+      la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane, d.xrows, d.xrows_n, d.xsrc_rows);
+    else
+      la.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane);
+    if constexpr (BK_ == OP_RMAJ && EPI == EPI_DW) {
+      if (d.xrows) {  // the batch rows' row numbers, for every K step's loads (one table per tile)
+        lds_i32* m = (lds_i32*)xmap;
+        for (int i = tid; i < d.xrows_n; i += NT) m[i] = d.xrows[i];
+        __syncthreads();
+        lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane, m, d.xrows_n, d.xsrc_rows);
+      } else {
+        lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane);
+      }
+    } else {
+      lb.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane);
+    }
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
       if (s < nk) {
@@ -1313,16 +1357,16 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
 // stages (128 KB of LDS), one workgroup (one wave per SIMD) per CU.
 template <typename T, int AK, int BK_, int EPI>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[kLdsBig];
+  __shared__ __attribute__((aligned(16))) char smem[kLdsBig + XMapBytes<T, EPI>];
   const Tile t = a.tiles[blockIdx.x];
   const GemmDesc d = a.descs[t.desc];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   if (t.shape == kShapeBig) {
-    run_tile<T, AK, BK_, EPI, kShapeBig, kBigKs, kBigNs>(a, d, t, smem, tid, wave);
+    run_tile<T, AK, BK_, EPI, kShapeBig, kBigKs, kBigNs>(a, d, t, smem, tid, wave, smem + kLdsBig);
     return;
   }
-  run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave);
+  run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave, smem + kLdsBig);
 }
 
 // Launches of small tiles only: 64 KB of LDS, two workgroups per CU, so one
@@ -1332,13 +1376,14 @@ template <typename T, int AK, int BK_, int EPI>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     sizeof(T) == 2 ? kSmallWpeBf16 : kSmallWpeF32, sizeof(T) == 2 ? kSmallWpeBf16 : kSmallWpeF32))) void
 gemm_kernel_small(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[sizeof(T) == 2 ? kLdsSmallBf16 : kLdsSmallF32];
+  constexpr int kOps = sizeof(T) == 2 ? kLdsSmallBf16 : kLdsSmallF32;
+  __shared__ __attribute__((aligned(16))) char smem[kOps + XMapBytes<T, EPI>];
   const Tile t = a.tiles[blockIdx.x];
   const GemmDesc d = a.descs[t.desc];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   if constexpr (sizeof(T) == 2)
-    run_tile<T, AK, BK_, EPI, kShapeSmall, kSmallKs, kSmallNs>(a, d, t, smem, tid, wave);
+    run_tile<T, AK, BK_, EPI, kShapeSmall, kSmallKs, kSmallNs>(a, d, t, smem, tid, wave, smem + kOps);
   else
     run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave);
 }
@@ -1347,16 +1392,17 @@ gemm_kernel_small(GemmArgs a) {
 // workgroups per CU, each with kTallNs stages of the tall pipeline.
 template <int AK, int BK_, int EPI>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_kernel_tall(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[kLdsTall];
+  static_assert(kLdsTall + XMapBytes<__bf16, EPI> <= 80 * 1024, "two tall-tile workgroups per CU");
+  __shared__ __attribute__((aligned(16))) char smem[kLdsTall + XMapBytes<__bf16, EPI>];
   const Tile t = a.tiles[blockIdx.x];
   const GemmDesc d = a.descs[t.desc];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   if (t.shape == kShapeTall) {
-    run_tile<__bf16, AK, BK_, EPI, kShapeTall, kTallKs, kTallNs>(a, d, t, smem, tid, wave);
+    run_tile<__bf16, AK, BK_, EPI, kShapeTall, kTallKs, kTallNs>(a, d, t, smem, tid, wave, smem + kLdsTall);
     return;
   }
-  run_tile<__bf16, AK, BK_, EPI, kShapeSmall, kSmallKs, kSmallNs>(a, d, t, smem, tid, wave);
+  run_tile<__bf16, AK, BK_, EPI, kShapeSmall, kSmallKs, kSmallNs>(a, d, t, smem, tid, wave, smem + kLdsTall);
 }
 
 template <typename T, int AK, int BK_, int EPI>

@@ -40,6 +40,9 @@ enum EpiKind : int { EPI_FWD = 0, EPI_FWD_EVAL = 1, EPI_DX = 2, EPI_DW = 3, EPI_
 struct MemberDev;
 
 // One member's GEMM problem C[m, n] = sum_k A(m, k) B(n, k) in one grouped launch.
+// most batch rows a weight-gradient GEMM can take straight from the data copy
+constexpr int kMapRows = 2048;
+
 struct GemmDesc {
   const void* A;
   const void* B;
@@ -60,6 +63,14 @@ struct GemmDesc {
   int64_t poff;        // EPI_DW with fused AdamW: element offset of the weight tensor
   const void* Y;       // EPI_NS: the matrix added to the product (GEMM precision), or nullptr
   int64_t ldy;
+  // bf16 only: the batch rows of the operand that holds the data, taken
+  // straight from a bf16 copy of X (xsrc_rows rows): when xrows is set, batch
+  // row r < xrows_n is row xrows[r] of that copy, rows >= xrows_n read as
+  // zero.  EPI_FWD: the rows of A (depth-contiguous, lda); EPI_DW: the depth
+  // rows of B (rows-contiguous, ldb), at most kMapRows of them.
+  const int32_t* xrows;
+  int32_t xrows_n;
+  int64_t xsrc_rows;
 };
 
 struct Tile {
@@ -213,6 +224,8 @@ hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, fl
                         uint16_t* shadow, const uint32_t* chunk_tab, const uint32_t* list,
                         const MemberDev* mem, int64_t nchunks, const AdamConst& ac, hipStream_t s);
 hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hipStream_t s);
+// xb[r][c] = bf16(X[r][c]) for c < d_in, 0 for d_in <= c < Pin; N rows
+hipError_t launch_rows_to_bf16(const float* X, int64_t N, int d_in, int Pin, void* xb, hipStream_t s);
 // Periodic embeddings (kernels_embed.hip).  E of member k = members[g], row r:
 // the embedded row X[idx[k * B + r]] (idx == nullptr: X[row_base + r]) for
 // r < rows_valid, zero above.

@@ -85,6 +85,8 @@ class OnlineTrainer:
         if orders is None:
             def orders(e):
                 return synth.epoch_orders_device(self.cfg, e, N, X.device)
+        if self.pack.can_bind_data():  # the first layer reads its rows straight from X
+            self.pack.bind_data(X)
         active = [True] * K
         best = [math.inf] * K
         bad = [0] * K

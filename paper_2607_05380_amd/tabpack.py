@@ -19,6 +19,7 @@ TASKS = {"reg": 0, "bin": 1, "multi": 2}
 PRECISIONS = {"bf16": 0, "fp32": 1}
 PREDICT_MEMBERS, PREDICT_ENSEMBLE = 0, 1
 STATUS_IDX_RANGE = 1
+BIND_DATA_MAX_B = 2048  # PACK_BIND_DATA_MAX_B
 OPTIMIZERS = {"adamw": 0, "muon": 1}
 
 SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "pack_workspace_size",
@@ -26,7 +27,7 @@ SYMBOLS = ["pack_last_error", "pack_init", "pack_destroy", "pack_get_hparams", "
            "pack_select", "pack_member_param_count", "pack_get_params", "pack_set_params",
            "pack_get_grads", "pack_get_moments", "pack_debug_dropout_mask", "pack_debug_activation",
            "pack_profile_enable", "pack_profile_read", "pack_set_active", "pack_predict", "pack_status",
-           "pack_stream_copy", "pack_select_static"]
+           "pack_stream_copy", "pack_select_static", "pack_bind_data"]
 
 
 class MemberHP(ctypes.Structure):
@@ -105,6 +106,7 @@ def load_library(path=LIB_PATH):
         "pack_predict": ([H, vp, i64, i32, vp, vp], ctypes.c_int),
         "pack_status": ([H, ctypes.POINTER(ctypes.c_uint32), vp], ctypes.c_int),
         "pack_stream_copy": ([vp, vp, sz, vp], ctypes.c_int),
+        "pack_bind_data": ([H, vp, i64, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -187,6 +189,7 @@ class Pack:
         self.d_in, self.d_out = c.d_in, c.d_out
         self.workspace = None
         self._select_ws = None
+        self.xb = None
         self.active = [True] * self.K
 
     def __del__(self):
@@ -227,6 +230,30 @@ class Pack:
         _check(self.lib.pack_train_step(self.h, X.data_ptr(), y.data_ptr(), X.shape[0], idx.data_ptr(),
                                         int(step), loss_out.data_ptr(), _stream()))
         return loss_out
+
+    def can_bind_data(self):
+        """Whether bind_data applies: bf16 packs without feature embeddings and
+        with B <= BIND_DATA_MAX_B."""
+        c = self.cfg
+        return (c.get("precision", "bf16") == "bf16" and int(c.get("emb_lo", 0) or 0) == 0
+                and self.B <= BIND_DATA_MAX_B)
+
+    def bind_data(self, X):
+        """Let the first layer's forward and weight-gradient GEMMs read the batch
+        rows straight from X (device fp32 [N, d_in]) through the batch indices,
+        with no gathered copy of the batch; every later train_step must pass
+        this X.  bind_data(None) unbinds.  Keeps the bf16 copy of X it makes."""
+        import torch
+        if X is None:
+            _check(self.lib.pack_bind_data(self.h, None, 0, None, 0, _stream()))
+            self.xb = None
+            return self
+        assert X.is_cuda and X.dtype == torch.float32 and X.is_contiguous() and X.shape[1] == self.d_in
+        pin = (self.d_in + 7) // 8 * 8
+        xb = torch.empty(X.shape[0] * pin, dtype=torch.bfloat16, device=X.device)
+        _check(self.lib.pack_bind_data(self.h, X.data_ptr(), X.shape[0], xb.data_ptr(), xb.numel() * 2, _stream()))
+        self.xb = xb
+        return self
 
     def status(self):
         """Asynchronous error flags raised since the last call (waits for the

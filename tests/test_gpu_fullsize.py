@@ -24,18 +24,23 @@ def _sample_members(hp, extra=()):
     return sorted(picks)
 
 
-def _fullsize_step(cfg, precisions=("bf16",), setup=None):
+def _fullsize_step(cfg, precisions=("bf16",), setup=None, rows="stream"):
     """One packed step at the workload's real shape on the GPU, and oracle packs
     (one per precision policy) holding only the sampled members, stepped on
     the same base batches.  ``setup(pk, ops, sample)`` may change initial
     parameters on both sides; it returns the sampled members' initial values
-    (default: the layer parameters)."""
+    (default: the layer parameters).  rows="stream": the first layer reads its
+    rows straight from the data where the pack allows it, as bench.py runs it;
+    "gather": the batch is gathered first."""
     name = cfg["name"]
     print(f"[fullsize] {name}: generating {cfg['n_train']} x {cfg['d_in']} on the device", flush=True)
     Xtr, ytr, _, _ = synth.make_data_device(cfg, "cuda", n_val=16)
     orders = synth.epoch_orders_device(cfg, 0, cfg["n_train"])
     idx = orders[:, :cfg["B"]].contiguous()
     pk = tabpack.Pack(cfg).bind()
+    if rows == "stream" and pk.can_bind_data():
+        pk.bind_data(Xtr)
+        print(f"[fullsize] {name}: first-layer rows streamed from the data", flush=True)
     hp = oracle_hparams(cfg)
     sample = _sample_members(hp)
     ops = [OraclePack(oracle_cfg(cfg), hparams=hp, precision=p, members=sample) for p in precisions]
@@ -68,10 +73,12 @@ def _fullsize_step(cfg, precisions=("bf16",), setup=None):
     return pk, ops, sample, p0
 
 
-@pytest.mark.parametrize("name", ["regression_onehot", "multiclass_lognormal", "binary_wide", "regression_large"])
-def test_fullsize_step_sampled_members(name):
+@pytest.mark.parametrize("name,rows", [("regression_onehot", "stream"), ("multiclass_lognormal", "stream"),
+                                       ("binary_wide", "stream"), ("regression_large", "stream"),
+                                       ("regression_large", "gather")])
+def test_fullsize_step_sampled_members(name, rows):
     cfg = configs.workload(name)
-    pk, (op, op64), sample, p0 = _fullsize_step(cfg, ("bf16", "fp64"))
+    pk, (op, op64), sample, p0 = _fullsize_step(cfg, ("bf16", "fp64"), rows=rows)
     for k in sample:
         compare_member(pk, op, k, p0[k], TOL["bf16"], prefix=f"{name}.")
         w64 = compare_member_fp64(pk, op64, k, p0[k], prefix=f"{name}.")

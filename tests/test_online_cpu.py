@@ -128,6 +128,9 @@ class ScriptedPack:
     def hparams(self):
         return [dict(width=8, dropout=0.0, lr=1e-3, wd=0.0)] * self.K
 
+    def can_bind_data(self):  # the driver then trains without a data copy
+        return False
+
     def train_step(self, X, y, idx, t, loss):
         self.steps.append(t)
         if len(self.trained) <= self.epoch:
