@@ -564,11 +564,13 @@ void sort_launch(Plan& p, const Launch& ln) {
 }
 
 // Members into ngroups groups of about equal GEMM work (longest first, each
-// to the lightest group).  TABPACK_STREAMS (1 .. 4) overrides the default 3
-// (measured on the 64-member workloads: 1 group 1.80 ms, 2 groups 1.63 ms,
-// 3 groups 1.60 ms per step; 4 groups exceed the four hardware queues).
+// to the lightest group).  Default: 2 groups, 3 with Muon, whose per-group
+// Newton-Schulz chains overlap better in three (regression_large: 1.398
+// against 1.409 ms per step, Muon 5.33 against 5.39 ms; one group 1.53 ms;
+// 4 groups exceed the four hardware queues).  TABPACK_STREAMS (1 .. 4)
+// overrides it.
 void split_members(pack_handle* h) {
-  int ng = 3;
+  int ng = h->muon ? 3 : 2;
   if (const char* e = getenv("TABPACK_STREAMS")) ng = std::max(1, std::min(kGroups, atoi(e)));
   h->ngroups = std::max(1, std::min(ng, (int)h->active_ids.size()));
   for (auto& v : h->group) v.clear();
@@ -1591,7 +1593,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     } else if (!h->stream_rows) {
       // the groups' gathers (HBM-bound) run one after another, so a group's
       // forward GEMMs overlap the next group's gather instead of every group
-      // waiting for three concurrent gathers
+      // waiting for all the groups' gathers at once
       if (hf > 0) HIP_TRY(hipStreamWaitEvent(s, h->ev_gather[hf - 1], 0));
       HIP_TRY(timed(h, "gather", 1, 0.0, (double)gk * c.B * c.d_in * (4.0 + h->elt()), s, [&] {
         return launch_gather(h->prec, X, c.d_in, h->Pin, idx, c.B, 0, c.B, gk, h->Bp, h->b.H0,
