@@ -62,7 +62,7 @@ typedef struct pack_member_hp {
   double wd;               /* AdamW decoupled weight decay, >= 0 */
   double scale;            /* out: inverted-dropout scale s_k = 1 / (1 - p_k) */
   double muon_lr;          /* Muon learning rate of the hidden weights (PACK_OPT_MUON), > 0 */
-  int32_t d_emb;           /* periodic embedding size per feature, 2 .. 32 (packs with embeddings) */
+  int32_t d_emb;           /* periodic embedding size per feature, 8 .. 32 (packs with embeddings) */
   int32_t reserved2;
   double sigma;            /* standard deviation of the embedding frequencies' initial values, > 0 */
 } pack_member_hp;
@@ -116,9 +116,12 @@ typedef struct pack_config {
    * d_emb), concatenated feature-major into the first layer's d_in * d_emb
    * inputs.  Initial values: w ~ N(0, sigma), b = alpha = beta = 0; trained
    * with AdamW.  d_emb ~ emb_lo + emb_step * UniformInt[0, (emb_hi - emb_lo) /
-   * emb_step] (2 <= lo <= hi <= 32), sigma ~ LogUniform[sigma_lo, sigma_hi].
-   * The member's dense parameter vector then starts with w, b, alpha, beta
-   * (row-major [d_in, d_emb - 1] / [d_in, d_emb]). */
+   * emb_step] (8 <= lo <= hi <= 32, the range App. F samples from), sigma ~
+   * LogUniform[sigma_lo, sigma_hi].  Requires B <= 2048.  The member's dense
+   * parameter vector then starts with w, b, alpha, beta (row-major
+   * [d_in, d_emb - 1] / [d_in, d_emb]); its dense W_1 has the d_in * d_emb
+   * columns in that order.  The embedded inputs are never stored: the first
+   * layer's GEMMs compute them from the data rows. */
   int32_t emb_lo, emb_hi, emb_step;
   int32_t reserved3;
   double sigma_lo, sigma_hi;

@@ -69,6 +69,7 @@ struct Member {
   int p_in = 0;          // columns of W_1 and of the first layer's input (padded d_in * d_emb, or Pin)
   int64_t eoff[4] = {};  // embedding parameters w, b, alpha, beta (offsets in theta)
   int64_t h0_off = 0;    // the member's first-layer input block (elements of the H_0 / E buffer)
+  int64_t etab_off = 0;  // the member's embedding column table (entries of the table buffer)
   uint32_t t;
   std::vector<int64_t> toff;  // packed offsets of W_1, b_1, ..., W_depth, b_depth, W_out, b_out
   int64_t act_off;
@@ -102,6 +103,7 @@ struct Bufs {
   float *theta = nullptr, *grad = nullptr, *m = nullptr, *v = nullptr;
   uint16_t* shadow = nullptr;
   char* H0 = nullptr;  // first-layer inputs: gathered batches [Bp, Pin], or embedded batches E [Bp, p_in], per member
+  float4* etab = nullptr;  // embeddings: the members' column tables (MemberDev::e_tab), rebuilt every step
   float* dE = nullptr; // embeddings: at each member's E offset / 16, the dE GEMM's sums [Bp / 64][4][p_in] (fp32)
   char* H = nullptr;   // L activation buffers H_1..H_L
   char* dz = nullptr;  // 2 ping-pong buffers for dZ_l
@@ -213,6 +215,7 @@ struct pack_handle {
   size_t elt() const { return prec == Prec::BF16 ? 2 : 4; }
   void* Hl(int l) const { return b.H + (size_t)(l - 1) * A * elt(); }  // H_l, l = 1..L
   int64_t H0e = 0;  // elements of the H_0 / E buffer (every member's first-layer input block)
+  int64_t Etab = 0; // entries of the embedding column tables (p_in per embedded member)
   void* dzb(int l) const { return b.dz + (size_t)(l & 1) * A * elt(); } // buffer holding dZ_l
 };
 
@@ -241,12 +244,14 @@ int validate(const pack_config* c) {
   if (!(c->beta1 >= 0 && c->beta1 < 1 && c->beta2 >= 0 && c->beta2 < 1 && c->eps > 0))
     return fail(PACK_EINVAL, "AdamW constants out of range");
   if (c->emb_lo != 0) {
-    if (c->emb_lo < 2 || c->emb_hi < c->emb_lo || c->emb_hi > 32 || c->emb_step < 1 ||
+    if (c->emb_lo < 8 || c->emb_hi < c->emb_lo || c->emb_hi > 32 || c->emb_step < 1 ||
         (c->emb_hi - c->emb_lo) % c->emb_step)
-      return fail(PACK_EINVAL, "embedding size range [%d, %d] step %d invalid (2 <= lo <= hi <= 32)", c->emb_lo,
+      return fail(PACK_EINVAL, "embedding size range [%d, %d] step %d invalid (8 <= lo <= hi <= 32)", c->emb_lo,
                   c->emb_hi, c->emb_step);
     if (!c->members && !(c->sigma_lo > 0 && c->sigma_hi >= c->sigma_lo))
       return fail(PACK_EINVAL, "embedding sigma range must be positive and ordered");
+    if (c->B > kMapRows)
+      return fail(PACK_EINVAL, "B=%d: periodic embeddings take batches of at most %d rows", c->B, kMapRows);
   }
   if (c->optimizer != PACK_OPT_ADAMW && c->optimizer != PACK_OPT_MUON)
     return fail(PACK_EINVAL, "unknown optimizer %d", c->optimizer);
@@ -301,18 +306,25 @@ void sample_members(pack_handle* h) {
 // weights with biases.  Padding rows/columns hold exact zeros forever: their
 // inputs or output gradients are zero, so their gradients and AdamW moments
 // stay zero.
+int emb_dp(int d_emb) { return (d_emb + 7) & ~7; }
+
 void plan_layout(pack_handle* h) {
   const pack_config& c = h->cfg;
   int64_t off = 0, aoff = 0;
   h->chunk_tab.clear();
   h->aux_chunks.clear();
-  int64_t h0 = 0;
+  int64_t h0 = 0, tab = 0;
   for (int k = 0; k < c.K; ++k) {
     Member& m = h->mem[k];
     m.dp = (int)round_up(m.width, h->q);
-    m.p_in = m.d_emb ? (int)round_up((int64_t)c.d_in * m.d_emb, 8) : h->Pin;
+    // embedded: feature i owns columns i dp .. i dp + dp - 1 of W_1 (dp = d_emb
+    // rounded up to 8, the last dp - d_emb zero padding), so that every
+    // 16-byte chunk of a row the GEMMs produce belongs to one feature
+    m.p_in = m.d_emb ? c.d_in * emb_dp(m.d_emb) : h->Pin;
     m.h0_off = h0;
     h0 += (int64_t)h->Bp * m.p_in;
+    m.etab_off = tab;
+    if (m.d_emb) tab += m.p_in;
     if (m.d_emb) {  // embedding parameters first: w, b [d_in, d_emb-1], alpha, beta [d_in, d_emb] (AdamW)
       const int64_t n[4] = {(int64_t)c.d_in * (m.d_emb - 1), (int64_t)c.d_in * (m.d_emb - 1),
                             (int64_t)c.d_in * m.d_emb, (int64_t)c.d_in * m.d_emb};
@@ -350,6 +362,12 @@ void plan_layout(pack_handle* h) {
   h->P = off;
   h->A = aoff;
   h->H0e = h0;
+  h->Etab = tab;
+}
+
+// Packed column of dense column cc (feature-major i d_emb + j) of W_1.
+int64_t w1_col(const Member& m, int64_t cc) {
+  return m.d_emb ? (cc / m.d_emb) * emb_dp(m.d_emb) + cc % m.d_emb : cc;
 }
 
 // torch.nn.Linear default initialisation, U(-1/sqrt(fan_in), 1/sqrt(fan_in)),
@@ -393,7 +411,7 @@ void init_params(pack_handle* h) {
           const double u = (double)(word >> 8) * (1.0 / 16777216.0);
           const float val = (float)((2.0 * u - 1.0) * bound);
           if (part == 0)
-            dst[(e / fan_in) * ld + (e % fan_in)] = val;
+            dst[(e / fan_in) * ld + (l == 0 ? w1_col(m, e % fan_in) : e % fan_in)] = val;
           else
             dst[e] = val;
         }
@@ -428,7 +446,7 @@ void for_each_dense(const pack_handle* h, int k, F f) {  // f(dense_index, packe
     const int cols = l == 0 ? (m.d_emb ? c.d_in * m.d_emb : c.d_in) : m.width;
     const int64_t ld = l == 0 ? m.p_in : m.dp;
     for (int r = 0; r < rows; ++r)
-      for (int cc = 0; cc < cols; ++cc) f(di++, m.toff[2 * l] + (int64_t)r * ld + cc);
+      for (int cc = 0; cc < cols; ++cc) f(di++, m.toff[2 * l] + (int64_t)r * ld + (l == 0 ? w1_col(m, cc) : cc));
     for (int r = 0; r < rows; ++r) f(di++, m.toff[2 * l + 1] + r);
   }
 }
@@ -843,13 +861,14 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     int64_t nsm = 0;
     for (int k : group[hf])
       if (h->mem[k].depth >= l) nsm += small_tiles(h->Bp, h->mem[k].dp);
-    p.tile_set = choose(h->tiles_fwd, nsm);
+    // the embedded first layer (E produced in the GEMM) runs small tiles only
+    p.tile_set = l == 1 && h->emb ? TILES_SMALL : choose(h->tiles_fwd, nsm);
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
       if (m.depth < l) continue;
       ++f.ndesc;
       GemmDesc d{};
-      d.A = l == 1 ? h0(k) : act(Hl(l - 1), k);
+      d.A = l == 1 ? (m.d_emb ? nullptr : h0(k)) : act(Hl(l - 1), k);  // the embedded E is produced in the GEMM
       d.lda = l == 1 ? m.p_in : m.dp;
       d.B = wptr(k, l);
       d.ldb = l == 1 ? m.p_in : m.dp;
@@ -877,8 +896,10 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       {
         const double fi = l == 1 ? (m.d_emb ? (double)c.d_in * m.d_emb : c.d_in) : m.width, w = m.width;
         f.flops += 2.0 * c.B * w * fi;
-        // H_{l-1} and W_l read, H_l written (2-byte elements in bf16), keep words read, mask words written
-        f.bytes += (double)h->elt() * (c.B * fi + fi * w + c.B * w) + c.B * w / 4.0;
+        // H_{l-1} and W_l read, H_l written (2-byte elements in bf16), keep words read, mask words written;
+        // the embedded first layer reads the batch's data rows and the column table instead of E
+        f.bytes += (double)h->elt() * (fi * w + c.B * w) + c.B * w / 4.0 +
+                   (l == 1 && m.d_emb ? 4.0 * c.B * c.d_in + 16.0 * fi : (double)h->elt() * c.B * fi);
       }
     }
     sort_launch(p, f);
@@ -892,7 +913,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       f.ndesc += (int)group[hf].size();
       for (int k : group[hf]) nsm += small_tiles(h->Bp, h->mem[k].dp);
     }
-    p.tile_set = choose(h->tiles_fwd, nsm);
+    p.tile_set = h->emb ? TILES_SMALL : choose(h->tiles_fwd, nsm);
     for (int hf = 0; hf < kGroups; ++hf)
       for (int i = 0; i < (int)group[hf].size(); ++i) {
         const int k = group[hf][i];
@@ -912,7 +933,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     int64_t nsm = 0;
     for (int k : group[hf])
       if (h->mem[k].depth >= l) nsm += small_tiles(h->mem[k].dp, l == 1 ? h->mem[k].p_in : h->mem[k].dp);
-    p.tile_set = choose(h->tiles_dw, nsm, kTallMinDepthDw);
+    p.tile_set = l == 1 && h->emb ? TILES_SMALL : choose(h->tiles_dw, nsm, kTallMinDepthDw);
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
       if (m.depth < l) continue;
@@ -920,7 +941,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       GemmDesc d{};
       d.A = act(dzb(l), k);
       d.lda = m.dp;
-      d.B = l == 1 ? h0(k) : act(Hl(l - 1), k);
+      d.B = l == 1 ? (m.d_emb ? nullptr : h0(k)) : act(Hl(l - 1), k);
       d.ldb = l == 1 ? m.p_in : m.dp;
       d.C = bf.grad + m.toff[2 * (l - 1)];
       d.ldc = l == 1 ? m.p_in : m.dp;
@@ -938,14 +959,20 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
         d.xrows_n = c.B;
         d.xsrc_rows = h->data_N;
       }
+      if (l == 1 && m.d_emb) {  // E produced in the GEMM from the batch rows' data rows
+        d.xrows = bf.idx_ok + (size_t)k * c.B;
+        d.xrows_n = c.B;
+      }
       add_tiles(p, w, (int)p.descs.size(), d.M, d.N, d.Kd);
       p.descs.push_back(d);
       {
         const double fi = l == 1 ? (m.d_emb ? (double)c.d_in * m.d_emb : c.d_in) : m.width, wd = m.width;
         w.flops += 2.0 * c.B * wd * fi;
-        // dZ_l and H_{l-1} read; per weight: the fused AdamW's theta, m, v read and written
-        // (24 B) and the bf16 shadow written (2 B), plus the fp32 gradient when it is kept
-        w.bytes += (double)h->elt() * c.B * (wd + fi) +
+        // dZ_l and H_{l-1} read (the embedded first layer: the data rows and the column table);
+        // per weight: the fused AdamW's theta, m, v read and written (24 B) and the bf16 shadow
+        // written (2 B), plus the fp32 gradient when it is kept
+        w.bytes += (double)h->elt() * c.B * wd +
+                   (l == 1 && m.d_emb ? 4.0 * c.B * c.d_in + 16.0 * fi : (double)h->elt() * c.B * fi) +
                    wd * fi * (24.0 + (h->prec == Prec::BF16 ? 2.0 : 0.0) + (c.keep_grads ? 4.0 : 0.0));
       }
     }
@@ -1070,10 +1097,12 @@ size_t carve(const pack_handle* h, char* base, Bufs& bf) {
   bf.m = cv.take<float>(h->P);
   bf.v = cv.take<float>(h->P);
   bf.shadow = h->prec == Prec::BF16 ? cv.take<uint16_t>(h->P) : nullptr;
-  bf.H0 = cv.take<char>((size_t)h->H0e * h->elt());
+  // embedded packs never store E (the first layer's GEMMs produce it)
+  bf.H0 = h->emb ? nullptr : cv.take<char>((size_t)h->H0e * h->elt());
   // each member's sums at its E offset / 16 (Bp is a multiple of 256, so the
   // offsets divide; a member's [Bp / 64][4][p_in] sums fill Bp p_in / 16)
   bf.dE = h->emb ? cv.take<float>((size_t)h->H0e / 16) : nullptr;
+  bf.etab = h->emb ? cv.take<float4>((size_t)h->Etab) : nullptr;
   bf.H = cv.take<char>((size_t)c.L * h->A * h->elt());
   bf.dz = cv.take<char>((size_t)2 * h->A * h->elt());
   bf.colpart = cv.take<float>((size_t)std::max(1, c.L - 1) * (h->A / kPartRows));
@@ -1147,6 +1176,19 @@ GemmArgs for_launch(GemmArgs a, const Launch& ln) {
   return a;
 }
 
+// The first-layer arguments of a GEMM that produces the embedded input E
+// (OP_EMB): the data X (N rows), and the batch indices (training forward) or
+// the first data row (idx == nullptr: evaluation).
+void set_emb(const pack_handle* h, GemmArgs& a, const float* X, int64_t N, const int32_t* idx, int64_t row_base) {
+  a.emb_x = X;
+  a.emb_x_rows = N;
+  a.emb_idx = idx;
+  a.emb_row_base = row_base;
+  a.emb_mem = h->b.d_mem;
+  a.emb_d_in = h->cfg.d_in;
+  a.emb_tab = h->b.etab;
+}
+
 hipEvent_t pool_event(pack_handle* h) {
   if (h->pool_used == h->event_pool.size()) {
     hipEvent_t e = nullptr;
@@ -1180,6 +1222,17 @@ hipError_t timed(pack_handle* h, const char* name, int kind, double flops, doubl
   h->groups[g].bytes += bytes;
   h->timed.push_back(TimedLaunch{g, a, b});
   return e;
+}
+
+// The column tables of the listed members' embeddings from their current
+// parameters (d_members: the same member ids in device memory).
+hipError_t emb_tables(pack_handle* h, const int32_t* d_members, const std::vector<int>& ids, hipStream_t s) {
+  double nb = 0;
+  for (int k : ids) nb += 32.0 * h->mem[k].p_in;  // four parameters read, one 16-byte entry written per column
+  return timed(h, "embed_table", 1, 0.0, nb, s, [&] {
+    return launch_embed_table(h->prec, h->cfg.d_in, h->b.d_mem, d_members, (int)ids.size(), max_pin(h, ids),
+                              h->b.theta, h->b.etab, s);
+  });
 }
 
 void set_active_ids(pack_handle* h) {
@@ -1306,7 +1359,7 @@ hipError_t muon_step(pack_handle* h, const GemmArgs& base, int g, hipStream_t st
 }
 
 const char* gemm_name(Prec p, OpKind a, OpKind b, EpiKind e) {
-  static const char* ops[] = {"kmaj", "rmaj", "xgk", "xgr"};
+  static const char* ops[] = {"kmaj", "rmaj", "emb"};
   static const char* epis[] = {"fwd", "fwd_eval", "dx", "dw", "ns", "de"};
   static thread_local char buf[64];
   snprintf(buf, sizeof buf, "gemm_%s_%s_%s_%s", p == Prec::BF16 ? "bf16" : "f32", ops[a], ops[b], epis[e]);
@@ -1371,7 +1424,7 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
       if (e.width < 1 || e.width > 16384 || !(e.dropout >= 0 && e.dropout < 1) || !(e.lr > 0) ||
           !(e.wd >= 0) || e.depth < 0 || e.depth > cfg->L ||
           (cfg->optimizer == PACK_OPT_MUON && !(e.muon_lr > 0)) ||
-          (cfg->emb_lo > 0 && (e.d_emb < 2 || e.d_emb > 32 || !(e.sigma > 0)))) {
+          (cfg->emb_lo > 0 && (e.d_emb < 8 || e.d_emb > 32 || !(e.sigma > 0)))) {
         delete h;
         return fail(PACK_EINVAL, "explicit hyperparameters of member %d out of range", k);
       }
@@ -1470,7 +1523,7 @@ int pack_bind(pack_handle* h, void* workspace, size_t bytes, hipStream_t stream)
     md[k] = MemberDev{m.width, m.dp, m.t, (float)m.scale, (float)m.lr, (float)m.wd, m.act_off,
                       m.toff[2 * m.depth], m.toff[2 * m.depth + 1], m.toff[2 * m.depth - 1],
                       (int64_t)(m.depth - 1) * h->A + m.act_off, (int64_t)(m.depth & 1) * h->A + m.act_off,
-                      m.depth, m.d_emb, m.eoff[0], m.eoff[1], m.eoff[2], m.eoff[3], m.h0_off, m.p_in, 0};
+                      m.depth, m.d_emb, m.eoff[0], m.eoff[1], m.eoff[2], m.eoff[3], m.h0_off, m.etab_off, m.p_in, 0};
     for (int l = 1; l <= m.depth; ++l) boff[(size_t)(l - 1) * h->cfg.K + k] = m.toff[2 * (l - 1) + 1];
   }
   HIP_TRY(hipMemcpyAsync(h->b.d_mem, md.data(), md.size() * sizeof(MemberDev), hipMemcpyHostToDevice, stream));
@@ -1523,6 +1576,7 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
   auto gemm = [&](OpKind ak, OpKind bk, EpiKind e, const Launch& ln, int layer, hipStream_t s) {
     GemmArgs al = for_launch(a, ln);
     al.layer = layer;
+    if (ak == OP_EMB || bk == OP_EMB) set_emb(h, al, X, N, idx, 0);
     return timed(h, gemm_name(h->prec, ak, bk, e), 0, ln.flops, ln.bytes, s,
                  [&] { return launch_gemm(h->prec, ak, bk, e, al, s); });
   };
@@ -1583,13 +1637,9 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     const hipStream_t s = hs[hf];
     const int gk = h->member0[hf + 1] - h->member0[hf];
     if (h->emb) {
-      double eb = 0;
-      for (int k : h->group[hf]) eb += (double)c.B * h->mem[k].p_in;
-      HIP_TRY(timed(h, "embed_fwd", 1, 0.0, eb * h->elt() + (double)gk * c.B * c.d_in * 4.0, s, [&] {
-        return launch_embed_fwd(h->prec, X, c.d_in, idx, c.B, 0, c.B, h->Bp, h->b.d_mem,
-                                h->b.d_members + h->member0[hf], gk, max_pin(h, h->group[hf]), h->b.theta,
-                                h->b.H0, s);
-      }));
+      // the column tables of the group's embeddings from the current parameters;
+      // the first-layer forward GEMM produces E from them
+      HIP_TRY(emb_tables(h, h->b.d_members + h->member0[hf], h->group[hf], s));
     } else if (!h->stream_rows) {
       // the groups' gathers (HBM-bound) run one after another, so a group's
       // forward GEMMs overlap the next group's gather instead of every group
@@ -1622,7 +1672,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
     });
   };
   for (int l = 1; l <= c.L; ++l)
-    for (int hf = 0; hf < ng; ++hf) HIP_TRY(gemm(OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
+    for (int hf = 0; hf < ng; ++hf)
+      HIP_TRY(gemm(l == 1 && h->emb ? OP_EMB : OP_KMAJ, OP_KMAJ, EPI_FWD, h->fwd[par][hf][l - 1], l, hs[hf]));
   for (int hf = 0; hf < ng; ++hf) {
     const hipStream_t s = hs[hf];
     const int32_t* gm = h->b.d_members + h->member0[hf];
@@ -1675,10 +1726,12 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       }
       GemmArgs al = for_launch(a, h->dw[hf][l - 1]);
       al.layer = l;
+      const OpKind bk = l == 1 && h->emb ? OP_EMB : OP_RMAJ;  // the embedded E is produced in the GEMM
       if (h->muon) {  // the gradient is stored; the Muon step below updates W_l
-        HIP_TRY(gemm(OP_RMAJ, OP_RMAJ, EPI_DW, h->dw[hf][l - 1], l, s));
+        HIP_TRY(gemm(OP_RMAJ, bk, EPI_DW, h->dw[hf][l - 1], l, s));
         continue;
       }
+      if (bk == OP_EMB) set_emb(h, al, X, N, idx, 0);
       al.theta = h->b.theta;
       al.am = h->b.m;
       al.av = h->b.v;
@@ -1686,8 +1739,8 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
       al.adam = ac;
       al.keep_grad = c.keep_grads ? 1 : 0;
       // AdamW fused: the weight update traffic dominates, so the HBM roofline applies
-      HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW), 1, h->dw[hf][l - 1].flops,
-                    h->dw[hf][l - 1].bytes, s, [&] { return launch_gemm(h->prec, OP_RMAJ, OP_RMAJ, EPI_DW, al, s); }));
+      HIP_TRY(timed(h, gemm_name(h->prec, OP_RMAJ, bk, EPI_DW), 1, h->dw[hf][l - 1].flops, h->dw[hf][l - 1].bytes, s,
+                    [&] { return launch_gemm(h->prec, OP_RMAJ, bk, EPI_DW, al, s); }));
     }
   if (h->muon)
     for (int hf = 0; hf < ng; ++hf) HIP_TRY(muon_step(h, a, hf, hs[hf]));
@@ -1715,16 +1768,15 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
 
 namespace {
 // Forward pass without dropout of every active member over rows r0 ..
-// r0 + a.rows_valid - 1 of X: the first-layer inputs (the rows gathered once
-// for all members, or each member's embedded rows), then the hidden layers;
-// the last hidden activations are left in H for the head.
-hipError_t eval_forward(pack_handle* h, GemmArgs a, const float* X, int64_t r0, hipStream_t stream) {
+// r0 + a.rows_valid - 1 of X (N rows): the first layer (on the rows gathered
+// once for all members, or, with embeddings, producing each member's
+// embedded rows in the GEMM from the column tables, which the caller has
+// built), then the hidden layers; the last hidden activations are left in H
+// for the head.
+hipError_t eval_forward(pack_handle* h, GemmArgs a, const float* X, int64_t N, int64_t r0, hipStream_t stream) {
   const pack_config& c = h->cfg;
-  hipError_t e;
-  if (h->emb)
-    e = launch_embed_fwd(h->prec, X, c.d_in, nullptr, c.B, r0, a.rows_valid, h->Bp, h->b.d_mem, h->b.d_active,
-                         (int)h->active_ids.size(), max_pin(h, h->active_ids), h->b.theta, h->b.H0, stream);
-  else
+  hipError_t e = hipSuccess;
+  if (!h->emb)
     e = launch_gather(h->prec, X, c.d_in, h->Pin, nullptr, c.B, r0, a.rows_valid, 1, h->Bp, h->b.H0, nullptr,
                       stream);
   if (e != hipSuccess) return e;
@@ -1732,7 +1784,9 @@ hipError_t eval_forward(pack_handle* h, GemmArgs a, const float* X, int64_t r0, 
     for (int hf = 0; hf < (l == 1 ? 1 : h->ngroups); ++hf) {
       GemmArgs al = for_launch(a, l == 1 ? h->fwd1_eval : h->fwd[0][hf][l - 1]);
       al.layer = l;
-      if ((e = launch_gemm(h->prec, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL, al, stream)) != hipSuccess) return e;
+      const OpKind ak = l == 1 && h->emb ? OP_EMB : OP_KMAJ;
+      if (ak == OP_EMB) set_emb(h, al, X, N, nullptr, r0);
+      if ((e = launch_gemm(h->prec, ak, OP_KMAJ, EPI_FWD_EVAL, al, stream)) != hipSuccess) return e;
     }
   }
   return hipSuccess;
@@ -1751,9 +1805,10 @@ int pack_eval_members(pack_handle* h, const float* Xv, const void* yv, int64_t N
   const pack_config& c = h->cfg;
   const int nact = (int)h->active_ids.size();
   GemmArgs a = base_args(h);
+  if (h->emb) HIP_TRY(emb_tables(h, h->b.d_active, h->active_ids, stream));
   for (int64_t r0 = 0; r0 < Nv; r0 += h->Bp) {
     a.rows_valid = (int)std::min<int64_t>(h->Bp, Nv - r0);
-    HIP_TRY(eval_forward(h, a, Xv, r0, stream));
+    HIP_TRY(eval_forward(h, a, Xv, Nv, r0, stream));
     HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadEval, h->b.H, h->b.theta, h->b.d_mem, nact, h->Bp, c.d_out,
                             yv, nullptr, c.B, a.rows_valid, r0, Nv, nullptr, nullptr, pred_out, h->b.d_active,
                             stream));
@@ -1772,9 +1827,10 @@ int pack_predict(pack_handle* h, const float* X, int64_t N, int32_t mode, float*
   const pack_config& c = h->cfg;
   const int nact = (int)h->active_ids.size();
   GemmArgs a = base_args(h);
+  if (h->emb) HIP_TRY(emb_tables(h, h->b.d_active, h->active_ids, stream));
   for (int64_t r0 = 0; r0 < N; r0 += h->Bp) {
     a.rows_valid = (int)std::min<int64_t>(h->Bp, N - r0);
-    HIP_TRY(eval_forward(h, a, X, r0, stream));
+    HIP_TRY(eval_forward(h, a, X, N, r0, stream));
     if (mode == PACK_PREDICT_MEMBERS) {
       // member i (i-th active id) writes rows r0.. of out[i, :, :]
       HIP_TRY(launch_head_fwd(h->prec, h->task, kHeadPredict, h->b.H, h->b.theta, h->b.d_mem, nact, h->Bp,

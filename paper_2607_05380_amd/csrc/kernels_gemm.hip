@@ -62,6 +62,7 @@
 // Every output element is owned by exactly one workgroup and reduced over the
 // full depth in a fixed order: no atomics, bit-reproducible.
 #include <algorithm>
+#include <type_traits>
 
 #include "adamw.h"
 #include "emb_trig.h"
@@ -76,6 +77,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int NT = 256;                 // threads per workgroup (2 x 2 waves)
 constexpr int KV = 8;                   // 16-byte vectors of depth per row per K step
@@ -126,7 +129,7 @@ static_assert(kLdsTall <= 80 * 1024, "two tall-tile workgroups per CU");
 // LDS table of the batch rows' row numbers in the data copy for the weight
 // gradient of the first layer (bf16 kernels of EPI_DW only)
 template <typename T, int EPI>
-constexpr int XMapBytes = (EPI == EPI_DW && sizeof(T) == 2) ? kMapRows * 4 : 0;
+constexpr int XMapBytes = EPI == EPI_DW ? kMapRows * 4 : 0;
 static_assert((kLdsSmallBf16 + kMapRows * 4) * kSmallWpeBf16 <= 160 * 1024, "small weight-gradient occupancy");
 static_assert(kLdsBig + kMapRows * 4 <= 160 * 1024, "one big-tile workgroup per CU");
 
@@ -448,6 +451,206 @@ struct DmaRmaj {
 #pragma unroll
       for (int p = 0; p < PER; ++p)
         dma16(rsrc, lds + (wave * PER + p) * 1024, k0 + krow[p] < kd ? voff[p] : kOob, soff);
+    }
+  }
+};
+
+// The embedded first-layer input E (App. "Feature Embeddings": feature x_i of
+// a row gives alpha_i0 x_i + beta_i0 and, for j >= 1, alpha_ij cos(w x_i + b)
+// + beta_ij) is never stored: the first layer's forward GEMM produces it as its
+// A operand and the weight-gradient GEMM as its B operand, from the data rows
+// and the member's column table.  Feature i owns the columns i dp .. i dp +
+// dp - 1 (dp = d_emb rounded up to 8; the columns j >= d_emb are zero
+// padding), so every 16-byte chunk of a row (8 bf16 or 4 fp32 columns, at a
+// multiple of 8 or 4) belongs to one feature.  Table entry c = {w, b, alpha,
+// beta} of column c (w = b = 0 at j = 0; zeros in the padding; bf16 packs
+// hold w and b in revolutions).
+
+// The value of one element: x is the row's value of the column's feature;
+// MAYBE_J0: the column may be a feature's first (j = 0, flagged by j0).
+template <bool FAST, bool MAYBE_J0>
+__device__ __forceinline__ float emb_value(const f32x4& tv, float x, bool j0) {
+  float g;
+  if constexpr (FAST)
+    g = __builtin_amdgcn_cosf(__builtin_amdgcn_fractf(fmaf(tv[0], x, tv[1])));
+  else
+    g = cosf(fmaf(tv[0], x, tv[1]));
+  if constexpr (MAYBE_J0) {
+    // computed for the element either way (the compiler would otherwise
+    // branch around the cosine): the choice below stays a select
+    asm volatile("" : "+v"(g));
+    g = j0 ? x : g;
+  }
+  return fmaf(tv[2], g, tv[3]);
+}
+
+// 16 bytes of the operand in the GEMM precision from 16 / sizeof(T) values
+template <typename T>
+__device__ __forceinline__ u32x4 emb_pack(const float* v) {
+  if constexpr (sizeof(T) == 2) {
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      o[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v[2 * q], v[2 * q + 1]}, bf16x2));
+    return o;
+  } else {
+    return u32x4{__builtin_bit_cast(uint32_t, v[0]), __builtin_bit_cast(uint32_t, v[1]),
+                 __builtin_bit_cast(uint32_t, v[2]), __builtin_bit_cast(uint32_t, v[3])};
+  }
+}
+
+struct EmbMember {
+  __amdgpu_buffer_rsrc_t tab;  // the member's column table, p_in entries
+  int dp, d_in1;
+  uint32_t magic;              // ceil(2^32 / dp): feature of column c = umulhi(c, magic)
+  __device__ void init(const GemmArgs& a, const GemmDesc& d) {
+    const MemberDev& md = a.emb_mem[d.member];
+    dp = (md.d_emb + 7) & ~7;
+    d_in1 = a.emb_d_in - 1;
+    magic = (uint32_t)((0x100000000ull + (uint64_t)dp - 1) / (uint64_t)dp);
+    tab = make_rsrc(a.emb_tab + md.e_tab, (int64_t)md.p_in * 16);
+  }
+  __device__ f32x4 entry(int c) const { return __builtin_bit_cast(f32x4, buf_load16(tab, (uint32_t)c * 16u)); }
+  // the feature of column c (clamped: columns past the table read zeros)
+  __device__ int feature(int c) const { return min((int)__umulhi((uint32_t)c, magic), d_in1); }
+  __device__ bool first(int c) const { return c == (int)__umulhi((uint32_t)c, magic) * dp; }  // j = 0
+};
+
+// A operand of the forward (rows: the tile's 128 batch rows, depth-contiguous
+// LDS layout): per K step, lane l of wave w produces chunk l / 8 of rows
+// l % 8 + 8 w + 32 i (i < 4), so the 8 lanes of a lane group share a chunk
+// and its table entries.  bf16: the K step's 64 table entries reach LDS with
+// one direct load of wave 0 (two steps ahead, beside the W_1 stage), and each
+// lane group reads its 8 from there (one address per group: no bank
+// conflicts); the rows' x are loaded into registers two steps ahead.  fp32:
+// each thread loads its chunk's entries itself.  Rows outside the batch read
+// data row 0 (finite values; the epilogue zeroes those rows).
+template <typename T>
+struct EmbRowsProducer {
+  static constexpr int VE = 16 / sizeof(T);  // columns per chunk
+  static constexpr int NR = 128 * 8 / NT;    // rows per thread
+  EmbMember em;
+  const float* xrow[NR];  // the rows' feature 0
+  int slot, rl0, lane, wave;
+  f32x4 tv[VE];           // the table entries of the step being produced
+  float x[2][NR];         // the rows' x, two K steps in flight (register set = step & 1)
+  __device__ void init(const GemmArgs& a, const GemmDesc& d, const Tile& t, int tid) {
+    em.init(a, d);
+    lane = tid % 64;
+    wave = tid / 64;
+    slot = lane / 8;
+    rl0 = lane % 8 + 8 * wave;
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      const int r = t.m0 + rl0 + 32 * i;
+      const int64_t row =
+          r < a.rows_valid ? (a.emb_idx ? (int64_t)a.emb_idx[(int64_t)d.member * a.rows_valid + r] : a.emb_row_base + r)
+                           : 0;
+      xrow[i] = a.emb_x + row * a.emb_d_in;
+    }
+  }
+  // bf16: the 64 entries of the step at k0 into tlds (wave 0; lane l: entry k0 + l)
+  __device__ void issue_tab(char* tlds, int k0) const {
+    if (wave == 0) dma16(em.tab, tlds, (uint32_t)lane * 16u, (uint32_t)k0 * 16u);
+  }
+  __device__ void read_tab(const char* tlds) {
+#pragma unroll
+    for (int e = 0; e < VE; ++e) tv[e] = *reinterpret_cast<const f32x4*>(tlds + (slot * VE + e) * 16);
+  }
+  template <int S>
+  __device__ void load_x(int k0) {
+    const int f = em.feature(k0 + slot * VE);
+#pragma unroll
+    for (int i = 0; i < NR; ++i) x[S][i] = *glob(xrow[i] + f);
+  }
+  // fp32: entries and x of the step at k0 (register set 0)
+  __device__ void load(int k0) {
+    const int c = k0 + slot * VE;
+#pragma unroll
+    for (int e = 0; e < VE; ++e) tv[e] = em.entry(c + e);
+    load_x<0>(k0);
+  }
+  // the chunk of the step at k0 from set S; off(row, slot): its byte offset in the A stage
+  template <int S, typename Off>
+  __device__ void store(char* lds, int k0, Off off) const {
+    const bool j0 = em.first(k0 + slot * VE);
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      float v[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e)
+        v[e] = e == 0 ? emb_value<sizeof(T) == 2, true>(tv[e], x[S][i], j0)
+                      : emb_value<sizeof(T) == 2, false>(tv[e], x[S][i], false);
+      *reinterpret_cast<u32x4*>(lds + off(rl0 + 32 * i, slot)) = emb_pack<T>(v);
+    }
+  }
+};
+
+// B operand of the weight gradient (columns: the tile's 128 embedding
+// columns, depth: batch rows).  The columns, their table entries and feature
+// are fixed for the tile; per K step each thread fetches the x of its depth
+// rows (data rows from the LDS map of the batch indices; rows past the batch
+// read another batch row, whose products meet zero gradient rows).
+//   bf16: chunk tid % 16 (8 columns) of depth rows tid / 16 + 16 i (i < 4),
+//         into the rows-contiguous layout (rmaj_off);
+//   fp32: column tid % 128 at depth rows 16 (tid / 128) .. + 15, four 16-byte
+//         depth vectors into the depth-contiguous layout (kmaj_off).
+template <typename T>
+struct EmbColsProducer {
+  static constexpr bool FAST = sizeof(T) == 2;
+  static constexpr int NC = FAST ? 8 : 1;    // columns per thread
+  static constexpr int NK = FAST ? 4 : 16;   // depth rows per thread per K step
+  EmbMember em;
+  f32x4 tv[NC];
+  bool j0;
+  int f;                        // the columns' feature
+  int col, kr0;                 // the thread's first column (tile-relative), first depth row
+  const float* X;
+  int d_in;
+  const lds_i32* map;
+  int nmap;
+  float x[FAST ? 2 : 1][NK];    // bf16: two K steps in flight (register sets S = step & 1)
+  __device__ void init(const GemmArgs& a, const GemmDesc& d, const Tile& t, int tid, const lds_i32* map_,
+                       int nmap_) {
+    em.init(a, d);
+    X = a.emb_x;
+    d_in = a.emb_d_in;
+    map = map_;
+    nmap = nmap_;
+    col = FAST ? (tid % 16) * 8 : tid % 128;
+    kr0 = FAST ? tid / 16 : (tid / 128) * 16;
+    const int c = t.n0 + col;
+#pragma unroll
+    for (int e = 0; e < NC; ++e) tv[e] = em.entry(c + e);
+    f = em.feature(c);
+    j0 = em.first(c);
+  }
+  __device__ int krow(int i) const { return FAST ? kr0 + 16 * i : kr0 + i; }
+  template <int S>
+  __device__ void load(int k0) {
+#pragma unroll
+    for (int i = 0; i < NK; ++i)  // rows past the batch read the batch's last row (any data row serves)
+      x[S][i] = *glob(X + (int64_t)map[min(k0 + krow(i), nmap - 1)] * d_in + f);
+  }
+  template <int S>
+  __device__ void store(char* lds) const {
+    if constexpr (FAST) {
+#pragma unroll
+      for (int i = 0; i < NK; ++i) {
+        float v[NC];
+#pragma unroll
+        for (int e = 0; e < NC; ++e)
+          v[e] = e == 0 ? emb_value<true, true>(tv[e], x[S][i], j0) : emb_value<true, false>(tv[e], x[S][i], false);
+        *reinterpret_cast<u32x4*>(lds + rmaj_off<128>(krow(i), col)) = emb_pack<T>(v);
+      }
+    } else {
+#pragma unroll
+      for (int s = 0; s < NK / 4; ++s) {
+        float v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = emb_value<false, true>(tv[0], x[S][4 * s + q], j0);
+        *reinterpret_cast<u32x4*>(lds + kmaj_off(col, kr0 / 4 + s)) = emb_pack<T>(v);
+      }
     }
   }
 };
@@ -1166,7 +1369,7 @@ __device__ __forceinline__ void wait_stage(int newer) {
 // holds of each 32 x 32 block, the lanes l and l + 32 holding the other rows
 // of the same column are added, and each wave writes its 64-row block's four
 // sums per column.  Batch rows >= rows_valid are left out.
-constexpr int kDeFeat = 66;  // features of 128 columns: at most 127 / d_emb + 2 (d_emb >= 2)
+constexpr int kDeFeat = 18;  // features of 128 columns: at most 127 / 8 + 2 (8 or more columns per feature)
 template <typename T, int SH>
 __device__ __forceinline__ void epilogue_de(const GemmArgs& a, const GemmDesc& d, const Tile& t,
                                             f32x16 (&acc)[Shape<SH>::MB][Shape<SH>::NB], int wm, int wn,
@@ -1175,11 +1378,12 @@ __device__ __forceinline__ void epilogue_de(const GemmArgs& a, const GemmDesc& d
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM;
   constexpr bool FAST = sizeof(T) == 2;
   const MemberDev& md = a.emb_mem[d.member];
-  const int d_emb = md.d_emb, d_in = a.emb_d_in, ncol = d_in * d_emb;
+  // feature i owns columns i dp .. i dp + dp - 1, the last dp - d_emb of them zero padding
+  const int d_emb = md.d_emb, dp = (d_emb + 7) & ~7, d_in = a.emb_d_in, ncol = d_in * dp;
   int64_t* rowoff = reinterpret_cast<int64_t*>(lds0);                    // [TM]
   float(*xs)[kDeFeat] = reinterpret_cast<float(*)[kDeFeat]>(lds0 + TM * 8);  // [TM][kDeFeat]
-  const int i0 = min(t.n0, ncol - 1) / d_emb;
-  const int nf = min(d_in - 1, (min(t.n0 + TM, ncol) - 1) / d_emb) - i0 + 1;
+  const int i0 = min(t.n0, ncol - 1) / dp;
+  const int nf = min(d_in - 1, (min(t.n0 + TM, ncol) - 1) / dp) - i0 + 1;
   if (tid < TM) {
     const int r = t.m0 + tid;
     rowoff[tid] = r < a.rows_valid ? (int64_t)a.emb_idx[(int64_t)d.member * a.rows_valid + r] * d_in : -1;
@@ -1196,11 +1400,11 @@ __device__ __forceinline__ void epilogue_de(const GemmArgs& a, const GemmDesc& d
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int col = t.n0 + wn * NB * 32 + 32 * j + (lane & 31);
-    const bool on = col < ncol;
+    const int fi = col / dp, fj = col - fi * dp, f = fi - i0;
+    const bool on = col < ncol && fj < d_emb;
     float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
     if (on) {
-      const int fi = col / d_emb, fj = col - fi * d_emb, f = fi - i0;
-      const float al = a.emb_theta[md.e_a + col];
+      const float al = a.emb_theta[md.e_a + (int64_t)fi * d_emb + fj];
       float w = 0.0f, b = 0.0f;
       if (fj > 0) {
         w = a.emb_theta[md.e_w + (int64_t)fi * (d_emb - 1) + fj - 1];
@@ -1352,6 +1556,183 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, const GemmDesc& d, c
     epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * Shape<SH>::STAGE, pre);
 }
 
+// Output tiles of the embedded first layer (small tiles): the forward, whose A
+// operand (E) EmbRowsProducer produces, and the weight gradient, whose B
+// operand (E) EmbColsProducer produces; the other operand streams as in
+// run_tile.  bf16: two stages of 64-deep steps; at step kt the producer's
+// loads and the other operand's direct loads for step kt + 1 are issued, the
+// MFMAs of step kt run, then the producer writes step kt + 1 into the other
+// stage (its loads have landed by then).  fp32: the register-staged two-stage
+// loop of run_tile with the producer as one of the loaders.
+template <int EPI, int SH>
+__device__ __forceinline__ void tile_extents(const GemmDesc& d, const Tile& t, int wm, int wn, int& mv, int& nv) {
+  constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB;
+  const int mrem = d.M - (t.m0 + wm * MB * 32), nrem = d.N - (t.n0 + wn * NB * 32);
+  mv = mrem <= 0 ? 0 : (mrem >= MB * 32 ? MB : (mrem + 31) / 32);
+  nv = nrem <= 0 ? 0 : (nrem >= NB * 32 ? NB : (nrem + 31) / 32);
+}
+
+template <typename T, int AK, int BK_, int EPI>
+__device__ __forceinline__ void run_tile_emb(const GemmArgs& a, const GemmDesc& d, const Tile& t, char* lds0, int tid,
+                                             int wave, char* xmap) {
+  constexpr int SH = kShapeSmall;
+  constexpr bool FWD = AK == OP_EMB;  // else the weight gradient (B produced)
+  static_assert(FWD ? BK_ == OP_KMAJ : (AK == OP_RMAJ && BK_ == OP_EMB && EPI == EPI_DW), "embedded operand");
+  constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM, TN = Shape<SH>::TN;
+  const int lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  int mv, nv;
+  tile_extents<EPI, SH>(d, t, wm, wn, mv, nv);
+  const bool compute = mv > 0 && nv > 0;
+  f32x16 acc[MB][NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  EpiPre<SH> pre;
+  epi_prefetch<EPI, SH>(d, t, wm, wn, lane, pre);
+  // the producer (A or B) and the streamed operand (B = W_1, or A = dZ_1)
+  std::conditional_t<FWD, EmbRowsProducer<T>, EmbColsProducer<T>> ep;
+  if constexpr (FWD) {
+    ep.init(a, d, t, tid);
+  } else {  // the batch rows' data rows, for every K step's x loads (one table per tile)
+    lds_i32* m = (lds_i32*)xmap;
+    for (int i = tid; i < d.xrows_n; i += NT) m[i] = d.xrows[i];
+    __syncthreads();
+    ep.init(a, d, t, tid, m, d.xrows_n);
+  }
+  if constexpr (sizeof(T) == 2) {
+    constexpr int KS = kSmallKs;
+    static_assert(KS == 4 && kSmallNs == 2, "the producers fill 64-deep steps of two stages");
+    using LS = std::conditional_t<FWD, DmaKmaj<TN, KS>, DmaRmaj<TM, KS>>;
+    constexpr int BKE = 16 * KS, TA = TM * 32 * KS, TB = TN * 32 * KS;
+    LS ls;
+    if constexpr (FWD)
+      ls.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane);
+    else
+      ls.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane);
+    const int nk = (d.Kd + BKE - 1) / BKE;
+    // stage k: the produced operand at prod(b), the streamed one at strm(b)
+    auto prod = [](char* b) { return FWD ? b : b + TA; };
+    auto strm = [](char* b) { return FWD ? b + TA : b; };
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    // forward: the table entries of step s in tab(s & 1), after both stages
+    auto tab = [&](int s) { return lds0 + 2 * (TA + TB) + (s & 1) * 1024; };
+    // the producer's loads of step s (register set s & 1; the forward's table two steps ahead too)
+    auto load = [&](int s, auto S) {
+      if constexpr (FWD) {
+        ep.template load_x<S.value>(s * BKE);
+        ep.issue_tab(tab(s), s * BKE);
+      } else {
+        ep.template load<S.value>(s * BKE);
+      }
+    };
+    auto store = [&](int s, auto S, char* b) {
+      if constexpr (FWD) {
+        ep.read_tab(tab(s));
+        ep.template store<S.value>(prod(b), s * BKE, [](int row, int sl) { return kmaj16_off<KS>(row, sl); });
+      } else {
+        ep.template store<S.value>(prod(b));
+      }
+    };
+    // The producer's loads run two K steps ahead (register set = step & 1), so
+    // their latency hides behind a whole step, as the direct loads' does.
+    // Memory operations keep their program order around the direct loads
+    // (empty asm statements); the wait at the top of a step covers both.
+    load(0, S0{});
+    load(min(1, nk - 1), S1{});
+    asm volatile("" ::: "memory");
+    ls.issue(strm(lds0), 0, d.Kd);
+    asm volatile("" ::: "memory");
+    if constexpr (FWD) {  // step 0's table entries
+      wait_vm<0, true>();
+      bar();
+    }
+    store(0, S0{}, lds0);
+    // step kt: the loads of step kt + 2 (set kt & 1, clamped to the last
+    // step, so the body has no conditional memory operations), the direct
+    // loads of step kt + 1, the MFMAs of step kt, then step kt + 1 produced
+    // from set S = (kt + 1) & 1
+    auto step = [&](int kt, auto S) {
+      wait_vm<0, true>();  // step kt's direct loads, the producer's loads and LDS writes are done
+      bar();
+      char* cur = lds0 + (kt & 1) * (TA + TB);
+      char* nxt = lds0 + ((kt + 1) & 1) * (TA + TB);
+      load(min(kt + 2, nk - 1), std::integral_constant<int, 1 - S.value>{});
+      asm volatile("" ::: "memory");
+      ls.issue(strm(nxt), (kt + 1) * BKE, d.Kd);
+      asm volatile("" ::: "memory");
+      if (compute) mma_step<T, SH, !FWD, !FWD, KS>(cur, cur + TA, acc, wm, wn, lane);
+      store(kt + 1, S, nxt);
+    };
+    for (int kt = 0; kt + 1 < nk;) {
+      step(kt, S1{});
+      if (++kt + 1 >= nk) break;
+      step(kt, S0{});
+      ++kt;
+    }
+    wait_vm<0, true>();
+    bar();
+    if (compute) {
+      char* cur = lds0 + ((nk - 1) & 1) * (TA + TB);
+      mma_step<T, SH, !FWD, !FWD, KS>(cur, cur + TA, acc, wm, wn, lane);
+    }
+    wait_vm<0, true>();
+    bar();  // the epilogue stages results in the operand buffers
+  } else {
+    constexpr int BKE = KV * Elem<T>::VE;
+    constexpr int TA = TM * ROW, TB = TN * ROW;
+    std::conditional_t<FWD, LoadKmaj<T, TN>, LoadRmajF32<TM>> ls;
+    if constexpr (FWD)
+      ls.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, tid);
+    else
+      ls.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, tid);
+    char* lds1 = lds0 + TA + TB;
+    const int nk = (d.Kd + BKE - 1) / BKE;
+    auto load = [&](int k0) {
+      if constexpr (FWD)
+        ep.load(k0);
+      else
+        ep.template load<0>(k0);
+    };
+    auto store = [&](char* b, int k0) {
+      if constexpr (FWD) {
+        ep.template store<0>(b, k0, [](int row, int sl) { return kmaj_off(row, sl); });
+        ls.store(b + TA, tid);
+      } else {
+        ls.store(b, tid);
+        ep.template store<0>(b + TA);
+      }
+    };
+    load(0);
+    ls.load(0, d.Kd, tid);
+    store(lds0, 0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      char* cur = (kt & 1) ? lds1 : lds0;
+      char* nxt = (kt & 1) ? lds0 : lds1;
+      const bool more = kt + 1 < nk;
+      if (more) {
+        load((kt + 1) * BKE);
+        ls.load((kt + 1) * BKE, d.Kd, tid);
+      }
+      if (compute) mma_step<T, SH, false, false, 4>(cur, cur + TA, acc, wm, wn, lane);
+      if (more) store(nxt, (kt + 1) * BKE);
+      __syncthreads();
+    }
+  }
+  if constexpr (EPI == EPI_DW && sizeof(T) == 2) {
+    if (a.theta) {  // uniform: the whole workgroup takes the staged-tile path
+      dw_adamw_small(a, d, t, acc, wm, wn, lane, tid, lds0);
+      return;
+    }
+  }
+  epilogue<T, EPI, SH>(a, d, t, acc, wm, wn, lane, mv, nv, lds0 + wave * Shape<SH>::STAGE, pre);
+}
+
 // ----------------------------------------------------------------- kernel --
 // Launches whose tiles include the big shape: 256x256 tiles with two 64-deep
 // stages (128 KB of LDS), one workgroup (one wave per SIMD) per CU.
@@ -1377,12 +1758,17 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(
     sizeof(T) == 2 ? kSmallWpeBf16 : kSmallWpeF32, sizeof(T) == 2 ? kSmallWpeBf16 : kSmallWpeF32))) void
 gemm_kernel_small(GemmArgs a) {
   constexpr int kOps = sizeof(T) == 2 ? kLdsSmallBf16 : kLdsSmallF32;
-  __shared__ __attribute__((aligned(16))) char smem[kOps + XMapBytes<T, EPI>];
+  // + the embedded forward's two 1 KB stages of column-table entries (bf16)
+  constexpr int kTab = AK == OP_EMB && sizeof(T) == 2 ? 2048 : 0;
+  static_assert(kTab == 0 || kLdsSmallBf16 == 2 * 2 * 128 * 32 * kSmallKs, "table stages follow the operand stages");
+  __shared__ __attribute__((aligned(16))) char smem[kOps + kTab + XMapBytes<T, EPI>];
   const Tile t = a.tiles[blockIdx.x];
   const GemmDesc d = a.descs[t.desc];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  if constexpr (sizeof(T) == 2)
+  if constexpr (AK == OP_EMB || BK_ == OP_EMB)
+    run_tile_emb<T, AK, BK_, EPI>(a, d, t, smem, tid, wave, smem + kOps + kTab);
+  else if constexpr (sizeof(T) == 2)
     run_tile<T, AK, BK_, EPI, kShapeSmall, kSmallKs, kSmallNs>(a, d, t, smem, tid, wave, smem + kOps);
   else
     run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave);
@@ -1443,6 +1829,14 @@ hipError_t launch_prec(OpKind ak, OpKind bk, EpiKind e, const GemmArgs& args, hi
     return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL>(args, s);
   if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DX) return launch_t<T, OP_KMAJ, OP_RMAJ, EPI_DX>(args, s);
   if (ak == OP_RMAJ && bk == OP_RMAJ && e == EPI_DW) return launch_t<T, OP_RMAJ, OP_RMAJ, EPI_DW>(args, s);
+  if (ak == OP_EMB || bk == OP_EMB) {  // the embedded first layer: small tiles
+    if (args.tile_set != TILES_SMALL || !args.emb_tab || !args.emb_x || !args.emb_mem) return hipErrorInvalidValue;
+    if (ak == OP_EMB && bk == OP_KMAJ && e == EPI_FWD) return launch_small<T, OP_EMB, OP_KMAJ, EPI_FWD>(args, s);
+    if (ak == OP_EMB && bk == OP_KMAJ && e == EPI_FWD_EVAL)
+      return launch_small<T, OP_EMB, OP_KMAJ, EPI_FWD_EVAL>(args, s);
+    if (ak == OP_RMAJ && bk == OP_EMB && e == EPI_DW) return launch_small<T, OP_RMAJ, OP_EMB, EPI_DW>(args, s);
+    return hipErrorInvalidValue;
+  }
   if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DE) {  // the embedding's dE reduction: small tiles only
     if (args.tile_set != TILES_SMALL) return hipErrorInvalidValue;
     return launch_small<T, OP_KMAJ, OP_RMAJ, EPI_DE>(args, s);

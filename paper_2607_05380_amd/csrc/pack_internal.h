@@ -34,7 +34,11 @@ enum class Task : int { REG = 0, BIN = 1, MULTI = 2 };
 // (the GEMM's M or N index) by BK depth (its K index):
 //   KMAJ    element (r, k) at P[r * ld + k]         -- depth contiguous
 //   RMAJ    element (r, k) at P[k * ld + r]         -- rows contiguous (transposed on load)
-enum OpKind : int { OP_KMAJ = 0, OP_RMAJ = 1 };
+//   EMB     the embedded first-layer input E (rows: batch rows, depth: the
+//           d_in * d_emb embedding columns), produced inside the GEMM from
+//           the member's data rows and embedding parameters (A operand of the
+//           first-layer forward of packs with periodic embeddings)
+enum OpKind : int { OP_KMAJ = 0, OP_RMAJ = 1, OP_EMB = 2 };
 enum EpiKind : int { EPI_FWD = 0, EPI_FWD_EVAL = 1, EPI_DX = 2, EPI_DW = 3, EPI_NS = 4, EPI_DE = 5 };
 
 struct MemberDev;
@@ -67,7 +71,9 @@ struct GemmDesc {
   // straight from a bf16 copy of X (xsrc_rows rows): when xrows is set, batch
   // row r < xrows_n is row xrows[r] of that copy, rows >= xrows_n read as
   // zero.  EPI_FWD: the rows of A (depth-contiguous, lda); EPI_DW: the depth
-  // rows of B (rows-contiguous, ldb), at most kMapRows of them.
+  // rows of B (rows-contiguous, ldb), at most kMapRows of them.  The embedded
+  // first layer's weight gradient (B = OP_EMB, bf16 or fp32) takes its batch
+  // rows' data rows from xrows the same way.
   const int32_t* xrows;
   int32_t xrows_n;
   int64_t xsrc_rows;
@@ -122,6 +128,16 @@ struct GemmArgs {
   const int32_t* emb_idx;
   const MemberDev* emb_mem;
   int32_t emb_d_in;
+  // OP_EMB only (the embedded first layer, E produced in the GEMM from the
+  // data and each member's column table emb_tab, see MemberDev::e_tab): x of
+  // batch row r is emb_x[row * emb_d_in + feature].  Forward: row =
+  // emb_idx[member * rows_valid + r] (training) or emb_row_base + r
+  // (emb_idx == nullptr: evaluation and prediction), for r < rows_valid.
+  // Weight gradient: row = desc.xrows[r] for r < desc.xrows_n.  emb_x has
+  // emb_x_rows rows.
+  const float4* emb_tab;
+  int64_t emb_row_base;
+  int64_t emb_x_rows;
 };
 
 // AdamW constants of one step.
@@ -142,6 +158,11 @@ struct MemberDev {
   // and alpha, beta [d_in, d_emb]; e_act: offset of the member's embedded batch E
   // [Bp, p_in] in the E buffer and of its gradient in the dE buffer
   int64_t e_w, e_b, e_a, e_be, e_act;
+  // first entry of the member's embedding column table (float4 units): entry
+  // c < p_in holds {w, b, alpha, beta} of column c = i d_emb + j (w = b = 0 for
+  // j = 0, zeros for the padding columns); bf16 packs store w and b divided by
+  // 2 pi (the phase in revolutions)
+  int64_t e_tab;
   int32_t p_in;             // columns of the first layer's input (padded d_in * d_emb, or d_in)
   int32_t pad_;
 };
@@ -226,14 +247,12 @@ hipError_t launch_adamw(Prec prec, float* theta, const float* grad, float* m, fl
 hipError_t launch_to_shadow(const float* theta, uint16_t* shadow, int64_t n, hipStream_t s);
 // xb[r][c] = bf16(X[r][c]) for c < d_in, 0 for d_in <= c < Pin; N rows
 hipError_t launch_rows_to_bf16(const float* X, int64_t N, int d_in, int Pin, void* xb, hipStream_t s);
-// Periodic embeddings (kernels_embed.hip).  E of member k = members[g], row r:
-// the embedded row X[idx[k * B + r]] (idx == nullptr: X[row_base + r]) for
-// r < rows_valid, zero above.
-// max_pin: the largest first-layer width p_in of the listed members (the
-// grid's column extent); Bp a multiple of 64.
-hipError_t launch_embed_fwd(Prec prec, const float* X, int d_in, const int32_t* idx, int B, int64_t row_base,
-                            int rows_valid, int Bp, const MemberDev* mem, const int32_t* members, int nmembers,
-                            int max_pin, const float* theta, void* E, hipStream_t s);
+// Periodic embeddings (kernels_embed.hip).  The listed members' embedding
+// column tables (MemberDev::e_tab) from their
+// current parameters in theta; max_pin: the largest first-layer width p_in of
+// the listed members (the grid's column extent).
+hipError_t launch_embed_table(Prec prec, int d_in, const MemberDev* mem, const int32_t* members, int nmembers,
+                              int max_pin, const float* theta, float4* tab, hipStream_t s);
 // grad of w, b, alpha, beta from the EPI_DE partial sums (in the dE buffer at
 // each member's e_act / 16: [Bp / 64][4][p_in])
 hipError_t launch_embed_grad(int d_in, int Bp, const MemberDev* mem, const int32_t* members, int nmembers,

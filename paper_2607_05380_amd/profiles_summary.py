@@ -31,12 +31,12 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 COPY_BYTES = 256 << 20
-OPS = ["kmaj", "rmaj"]
+OPS = ["kmaj", "rmaj", "emb"]
 EPIS = ["fwd", "fwd_eval", "dx", "dw", "ns", "de"]
 SIMPLE = ["dropout_words", "grad_sums", "head_grad_reduce", "head_fwd", "head_bwd", "loss_reduce", "bias_from_partials",
           "gather", "adamw", "to_shadow", "eval_score", "dropout_mask", "select_partial", "select_pick",
           "select_update", "select_init", "select_final", "ensemble_mean", "muon_prep", "muon_norm",
-          "muon_convert", "muon_update", "embed_fwd", "embed_grad", "idx_check", "stream_copy"]
+          "muon_convert", "muon_update", "embed_table", "embed_grad", "idx_check", "stream_copy"]
 
 
 def source_digest():
@@ -52,7 +52,8 @@ def source_digest():
 def short_name(kernel):
     """Library profiler name of a rocprofv3 kernel name (mangled, or demangled),
     or None for other kernels.  GEMM kernels are named by their template
-    arguments: element type, operand kinds (0 depth-contiguous, 1 row-major) and
+    arguments: element type, operand kinds (0 depth-contiguous, 1 row-major, 2 the
+    embedded first-layer input produced in the GEMM) and
     epilogue."""
     if "gemm_kernel" in kernel:
         m = re.search(r"gemm_kernel(?:_small|_tall)?I(DF16b|f)?(?:Li(\d)E)(?:Li(\d)E)(?:Li(\d)E)", kernel)
@@ -73,7 +74,7 @@ def short_name(kernel):
                     return None
                 t, bk, epi = "bf16", int(m.group(1)), int(m.group(2))
                 ak = 1 if epi == 3 else 0
-        if epi >= len(EPIS) or ak > 1 or bk > 1:
+        if epi >= len(EPIS) or ak >= len(OPS) or bk >= len(OPS):
             return None
         return f"gemm_{t}_{OPS[ak]}_{OPS[bk]}_{EPIS[epi]}"
     for s in sorted(SIMPLE, key=len, reverse=True):
