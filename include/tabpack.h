@@ -55,7 +55,7 @@ enum { PACK_OPT_ADAMW = 0, PACK_OPT_MUON = 1 };
 typedef struct pack_member_hp {
   int32_t width;           /* hidden width d_k, >= 1 */
   int32_t padded_width;    /* out: d_k rounded up to the quantum q */
-  uint32_t drop_threshold; /* out: t_k = floor(p_k * 2^32); an element is kept iff its word >= t_k */
+  uint32_t drop_threshold; /* out: t_k = floor(p_k * 2^16); an element is kept iff its 16-bit draw >= t_k */
   int32_t depth;           /* hidden Linear-ReLU-Dropout blocks L_k in [1, L]; as input 0 means L */
   double dropout;          /* p_k in [0, 1) */
   double lr;               /* AdamW learning rate, > 0 */
@@ -185,8 +185,9 @@ int pack_set_active(pack_handle* h, const uint8_t* active, hipStream_t stream);
  *   step     1-based AdamW step t; must be the previous step + 1 (PACK_ESTATE
  *            otherwise).  It is also the dropout counter of this step.
  *   loss_out device fp32 [K]: batch-mean loss of each member before the update
- * Dropout masks: element (r, c) of hidden layer l of member k is kept iff word
- * (r & 3) of Philox4x32-10(counter = (r >> 2, c, (k << 8) | l, step mod 2^32),
+ * Dropout masks: element (r, c) of hidden layer l of member k is kept iff the
+ * 16-bit half (r & 1) (0: low bits) of word ((r >> 1) & 3) of
+ * Philox4x32-10(counter = (r >> 3, c, (k << 8) | l, step mod 2^32),
  * key = (seed mod 2^32, (seed >> 32) ^ (3 << 28))) is >= t_k. */
 int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N,
                     const int32_t* idx, uint64_t step, float* loss_out, hipStream_t stream);

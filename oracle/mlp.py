@@ -31,17 +31,20 @@ TASK_REG, TASK_BIN, TASK_MULTI = "reg", "bin", "multi"
 def dropout_mask(seed, k, step, layer, B, width, t):
     """Keep mask (bool [B, width]) of member k, hidden layer ``layer`` (1-based).
 
-    Element (r, c) reads word (r & 3) of the Philox4x32-10 block with counter
-    (r >> 2, c, (k << 8) | layer, step mod 2**32) under the dropout stream key,
-    and is kept iff that word >= t (t = floor(p * 2**32)); p = 0 keeps all.
+    Element (r, c) reads the 16-bit half (r & 1) (0: low, 1: high bits) of
+    word ((r >> 1) & 3) of the Philox4x32-10 block with counter
+    (r >> 3, c, (k << 8) | layer, step mod 2**32) under the dropout stream key,
+    and is kept iff that half >= t (t = floor(p * 2**16)); p = 0 keeps all.
     """
     k0, k1 = stream_key(seed, TAG_DROPOUT)
     r = np.arange(B, dtype=np.uint64)[:, None]
     c = np.arange(width, dtype=np.uint64)[None, :]
-    words = philox4x32_10(r >> np.uint64(2), c, (int(k) << 8) | int(layer),
+    words = philox4x32_10(r >> np.uint64(3), c, (int(k) << 8) | int(layer),
                           int(step) & 0xFFFFFFFF, k0, k1)
-    sel = np.broadcast_to((r & np.uint64(3)).astype(np.int64), (B, width))
-    return np.choose(sel, words) >= np.uint32(t)
+    sel = np.broadcast_to(((r >> np.uint64(1)) & np.uint64(3)).astype(np.int64), (B, width))
+    shift = np.broadcast_to((r & np.uint64(1)) * np.uint64(16), (B, width)).astype(np.uint32)
+    half = (np.choose(sel, words) >> shift) & np.uint32(0xFFFF)
+    return half >= np.uint32(t)
 
 
 def to_bf16(x):

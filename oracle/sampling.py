@@ -36,8 +36,10 @@ tag 1 = hyperparameters, 2 = initial parameters, 3 = dropout.
   W_l -> 2(l-1), b_l -> 2(l-1)+1 for hidden layers l = 1..L_k (the member's
   depth), W_out -> 2 L_k, b_out -> 2 L_k + 1.
 
-Dropout: t_k = floor(p_k * 2**32) is the integer keep threshold and
-s_k = 1/(1 - p_k) the inverted-dropout scale (see ``mlp.dropout_mask``).
+Dropout: t_k = floor(p_k * 2**16) is the integer keep threshold of a 16-bit
+draw and s_k = 1/(1 - p_k) the inverted-dropout scale (see
+``mlp.dropout_mask``).  The drop probability realised is t_k / 2**16, within
+2**-16 of p_k.
 """
 import math
 
@@ -98,7 +100,7 @@ def sample_hparams(cfg):
 def member_hparams(width, dropout, lr, wd, depth=None, muon_lr=None):
     """depth None: the pack's L hidden blocks; muon_lr only for Muon packs."""
     p = float(dropout)
-    t = min(int(math.floor(p * 4294967296.0)), 0xFFFFFFFF)
+    t = min(int(math.floor(p * 65536.0)), 0xFFFF)
     out = dict(width=int(width), dropout=p, lr=float(lr), wd=float(wd),
                t=t, s=1.0 / (1.0 - p), depth=None if depth is None else int(depth))
     if muon_lr is not None:

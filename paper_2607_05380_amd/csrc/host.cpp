@@ -1441,7 +1441,7 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
     sample_members(h);
   }
   for (Member& m : h->mem) {
-    m.t = (uint32_t)std::min(std::floor(m.dropout * 4294967296.0), 4294967295.0);
+    m.t = (uint32_t)std::min(std::floor(m.dropout * 65536.0), 65535.0);  // threshold of a 16-bit draw
     m.scale = 1.0 / (1.0 - m.dropout);
   }
   plan_layout(h);

@@ -546,18 +546,20 @@ __global__ __launch_bounds__(256) void eval_score_kernel(Task task, const float*
 }
 
 // Keep word of a dropout mask: bit r is set iff row 32*rb + r of column c is
-// kept, i.e. word (r & 3) of Philox block (r >> 2, c, c2, step) is >= t.  The
-// training path (dropout_words_kernel -> forward epilogue) and the test hook
-// below both go through this function.
+// kept, i.e. the 16-bit half (r & 1) of word ((r >> 1) & 3) of Philox block
+// (4 rb + r / 8, c, c2, step) is >= t: one block decides 8 rows, four blocks a
+// word.  The training path (dropout_words_kernel -> forward epilogue) and the
+// test hook below both go through this function.
 __device__ __forceinline__ uint32_t keep_word(uint32_t key0, uint32_t key1, uint32_t step, uint32_t c2, int rb,
                                               int c, uint32_t t) {
   uint32_t w = 0;
 #pragma unroll 2
-  for (int b = 0; b < 8; ++b) {
-    const Words4 x = philox4x32_10((uint32_t)(rb * 8 + b), (uint32_t)c, c2, step, key0, key1);
-    w |= ((uint32_t)(x.w0 >= t) | ((uint32_t)(x.w1 >= t) << 1) | ((uint32_t)(x.w2 >= t) << 2) |
-          ((uint32_t)(x.w3 >= t) << 3))
-         << (4 * b);
+  for (int b = 0; b < 4; ++b) {
+    const Words4 x = philox4x32_10((uint32_t)(rb * 4 + b), (uint32_t)c, c2, step, key0, key1);
+    const uint32_t q[4] = {x.w0, x.w1, x.w2, x.w3};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)  // rows 8 b + 2 i (low half) and 8 b + 2 i + 1 (high half)
+      w |= (((uint32_t)((q[i] & 0xFFFFu) >= t)) | ((uint32_t)((q[i] >> 16) >= t) << 1)) << (8 * b + 2 * i);
   }
   return w;
 }

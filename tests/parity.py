@@ -54,7 +54,11 @@ from paper_2607_05380_amd import synth
 # Every bound below is the measured maximum over the GPU suite (recorded with
 # ``record``, summarised in profiles/parity_bounds.md) times a stated margin.
 # frac / exempt / flip / upd_frac are shares of a tensor's elements:
-#   frac     gradient elements outside the strict band (measured 3.2e-7; bound 1e-5)
+#   frac     gradient elements outside the strict band: at most frac of a tensor's
+#            elements or `few` elements, whichever is more (measured: 3 elements,
+#            in a 159,201-element W_3 and in a 461,824-element W_1, with the
+#            masks of 16-bit dropout draws; 1 element with 32-bit draws; bounds
+#            1e-5 and 8 elements)
 #   exempt   elements whose gradient sign is undetermined (a property of the
 #            gradient's distribution: elements under the band floor; measured
 #            0.26 on the embedded first layers, 0.19 on hidden layers; bound 0.35)
@@ -63,9 +67,9 @@ from paper_2607_05380_amd import synth
 #            element in 409 on the smallest; bound 1e-2)
 #   upd_frac updates off by more than upd * lr after several steps (measured
 #            6.8e-3; bound 1.5e-2)
-TOL = {"bf16": dict(rtol=2e-2, atol=1e-3, gfloor=1e-3, frob=2e-2, lit_rtol=2e-2, lit_atol=1e-3, frac=1e-5,
+TOL = {"bf16": dict(rtol=2e-2, atol=1e-3, gfloor=1e-3, frob=2e-2, lit_rtol=2e-2, lit_atol=1e-3, frac=1e-5, few=8,
                    upd=2e-2, exempt=0.35, flip=1e-2, upd_frac=1.5e-2),
-       "fp32": dict(rtol=1e-4, atol=1e-6, gfloor=1e-4, frob=1e-4, lit_rtol=1e-4, lit_atol=1e-5, frac=1e-5,
+       "fp32": dict(rtol=1e-4, atol=1e-6, gfloor=1e-4, frob=1e-4, lit_rtol=1e-4, lit_atol=1e-5, frac=1e-5, few=8,
                     upd=1e-3, exempt=0.35, flip=1e-2, upd_frac=1.5e-2)}
 
 # bf16 kernels against the exact fp64 oracle (no shared rounding policy):
@@ -153,12 +157,14 @@ def check_tensor(name, gpu, ref, tol, grad=False, report=None, kind=None):
     literal = close_mask(gpu, ref, tol["lit_rtol"], tol["lit_atol"])
     strict_frac = float((~strict).mean()) if gpu.size else 0.0
     record(name, kind, n=gpu.size, frob=frob if mx > 0 else 0.0, strict_frac=strict_frac,
+           strict_misses=int((~strict).sum()),
            literal_misses=(~literal).sum(), tol_ratio=_tol_ratio(gpu, ref, tol["lit_rtol"], tol["lit_atol"]))
     if report is not None:
         report.append((name, float(frob), int((~strict).sum())))
     assert literal.all(), f"{name}: {(~literal).sum()} of {gpu.size} elements outside the literal " \
                           f"tolerance; worst {np.abs(gpu - ref)[~literal].max():.3e}"
-    assert strict_frac <= tol["frac"], f"{name}: {(~strict).sum()} of {gpu.size} elements outside " \
+    assert (~strict).sum() <= max(tol["frac"] * gpu.size, tol["few"]), \
+        f"{name}: {(~strict).sum()} of {gpu.size} elements outside " \
                                        f"the strict band (max|ref| {mx:.3e}), frob {frob:.2e}"
     if mx > 0:
         assert frob <= tol["frob"], f"{name}: relative Frobenius error {frob:.3e}"

@@ -10,6 +10,7 @@ from collections import defaultdict
 
 MEASURES = [
     ("strict_frac", "max share of gradient elements outside the strict band"),
+    ("strict_misses", "max count of gradient elements outside the strict band in one tensor"),
     ("frob", "max relative Frobenius error"),
     ("tol_ratio", "max |gpu - ref| / (atol + rtol |ref|) (1.0 = the literal bound)"),
     ("exempt_frac", "max share of elements whose gradient sign is undetermined (exempt)"),

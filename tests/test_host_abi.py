@@ -70,7 +70,7 @@ def test_explicit_members_and_roundtrip():
     hp = pk.hparams()
     assert [h["width"] for h in hp] == [1, 31, 32, 33]
     assert [h["padded_width"] for h in hp] == [32, 32, 32, 64]
-    assert hp[1]["t"] == 2 ** 30 and hp[2]["t"] == 2 ** 31 and hp[2]["s"] == 2.0
+    assert hp[1]["t"] == 2 ** 14 and hp[2]["t"] == 2 ** 15 and hp[2]["s"] == 2.0
     p = pk.get_params(3)
     p2 = [(W * 2, b - 1) for W, b in p]
     pk.set_params(3, p2)

@@ -58,21 +58,23 @@ def test_vectorised_matches_scalar():
 
 def test_mask_counter_layout_by_hand():
     seed, k, step, layer = 2607053805, 3, 17, 2
-    t = 2 ** 31
-    m = dropout_mask(seed, k, step, layer, 9, 5, t)
+    t = 2 ** 15
+    m = dropout_mask(seed, k, step, layer, 19, 5, t)
     k0, k1 = stream_key(seed, TAG_DROPOUT)
-    for r in range(9):
+    for r in range(19):
         for c in range(5):
-            w = philox.philox_scalar([r >> 2, c, (k << 8) | layer, step], [k0, k1], **philox.PHILOX4x32)
-            assert m[r, c] == (w[r & 3] >= t)
+            w = philox.philox_scalar([r // 8, c, (k << 8) | layer, step], [k0, k1], **philox.PHILOX4x32)
+            word = w[(r % 8) // 2]
+            half = word % 2 ** 16 if r % 2 == 0 else word // 2 ** 16
+            assert m[r, c] == (half >= t)
 
 
 @pytest.mark.parametrize("p", [0.0, 0.1, 0.25, 0.5, 0.3])
 def test_mask_keep_rate(p):
-    t = int(np.floor(p * 2 ** 32))
+    t = int(np.floor(p * 2 ** 16))
     m = dropout_mask(7, 1, 1, 1, 512, 256, t)
     n = m.size
-    keep = 1.0 - t / 2 ** 32
+    keep = 1.0 - t / 2 ** 16
     sigma = np.sqrt(n * keep * (1 - keep)) + 1e-12
     if p == 0.0:
         assert m.all()
@@ -83,6 +85,7 @@ def test_mask_keep_rate(p):
 def test_thresholds_exact():
     from oracle.sampling import member_hparams
     assert member_hparams(8, 0.0, 1e-3, 1e-3)["t"] == 0
-    assert member_hparams(8, 0.25, 1e-3, 1e-3)["t"] == 2 ** 30
-    assert member_hparams(8, 0.5, 1e-3, 1e-3)["t"] == 2 ** 31
+    assert member_hparams(8, 0.25, 1e-3, 1e-3)["t"] == 2 ** 14
+    assert member_hparams(8, 0.5, 1e-3, 1e-3)["t"] == 2 ** 15
+    assert member_hparams(8, 0.999999, 1e-3, 1e-3)["t"] == 2 ** 16 - 1
     assert member_hparams(8, 0.5, 1e-3, 1e-3)["s"] == 2.0

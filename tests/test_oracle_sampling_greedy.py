@@ -27,7 +27,7 @@ def test_sampler_ranges_and_distributions():
         assert v.min() >= lo and v.max() <= hi
         assert kstest((np.log(v) - np.log(lo)) / (np.log(hi) - np.log(lo)), "uniform").pvalue > 1e-4
     for h in hp[:50]:
-        assert h["t"] == int(np.floor(h["dropout"] * 2 ** 32)) and h["s"] == 1 / (1 - h["dropout"])
+        assert h["t"] == int(np.floor(h["dropout"] * 2 ** 16)) and h["s"] == 1 / (1 - h["dropout"])
     assert sample_hparams(dict(CFG, K=5)) == hp[:5]
     assert sample_hparams(dict(CFG, K=5, seed=1)) != hp[:5]
 
