@@ -130,6 +130,9 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(Task task, const T* H, co
   float acc[D];
 #pragma unroll
   for (int o = 0; o < D; ++o) acc[o] = 0.0f;
+  // unrolled so that several rows' loads are in flight at once (the loop is
+  // latency-bound otherwise: one 16-byte load per lane per iteration)
+#pragma unroll 4
   for (int c = sub * 8; c < md.dp; c += 64) {
     float x[8];
     Vec8<T>::load(h + c, x);
@@ -290,6 +293,8 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* 
   T* dz = dZ + md.dz_last;
   const float* dyk = dY + (int64_t)ht.member * Bp * d_out;
   const int r1 = min(ht.r0 + RB, Bp);
+  // unrolled so that several rows' loads are in flight at once
+#pragma unroll 4
   for (int r = ht.r0 + slot; r < r1; r += 8) {
     float dy[D];
 #pragma unroll
