@@ -1710,10 +1710,10 @@ int pack_train_step(pack_handle* h, const float* X, const void* y, int64_t N, co
         GemmArgs ae = for_launch(a, h->de[hf]);
         ae.tile_set = TILES_SMALL;
         ae.emb_x = X;
-        ae.emb_theta = h->b.theta;
         ae.emb_idx = idx;
         ae.emb_mem = h->b.d_mem;
         ae.emb_d_in = c.d_in;
+        ae.emb_tab = h->b.etab;
         HIP_TRY(timed(h, gemm_name(h->prec, OP_KMAJ, OP_RMAJ, EPI_DE), 0, h->de[hf].flops, h->de[hf].bytes, s,
                       [&] { return launch_gemm(h->prec, OP_KMAJ, OP_RMAJ, EPI_DE, ae, s); }));
         const int gk = h->member0[hf + 1] - h->member0[hf];

@@ -65,7 +65,6 @@
 #include <type_traits>
 
 #include "adamw.h"
-#include "emb_trig.h"
 #include "pack_internal.h"
 
 namespace tabpack {
@@ -1397,48 +1396,58 @@ __device__ __forceinline__ void epilogue_de(const GemmArgs& a, const GemmDesc& d
   __syncthreads();
   const int hv = lane >> 5;
   float* part = static_cast<float*>(d.C) + (int64_t)((t.m0 >> 6) + wm) * 4 * d.ldc;
+  const bool all_rows = t.m0 + TM <= a.rows_valid;  // uniform
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int col = t.n0 + wn * NB * 32 + 32 * j + (lane & 31);
-    const int fi = col / dp, fj = col - fi * dp, f = fi - i0;
-    const bool on = col < ncol && fj < d_emb;
-    float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
-    if (on) {
-      const float al = a.emb_theta[md.e_a + (int64_t)fi * d_emb + fj];
-      float w = 0.0f, b = 0.0f;
-      if (fj > 0) {
-        w = a.emb_theta[md.e_w + (int64_t)fi * (d_emb - 1) + fj - 1];
-        b = a.emb_theta[md.e_b + (int64_t)fi * (d_emb - 1) + fj - 1];
-      }
+    const int fi = col / dp, fj = col - fi * dp;
+    const int f = min(fi - i0, nf - 1);  // padding columns past the last feature read a staged one
+    const bool on = col < ncol && fj < d_emb, j0 = fj == 0;
+    // the column's table entry {w, b, alpha, beta} (bf16 packs: w, b in revolutions; zeros in the
+    // padding), as the producers of E use it
+    const f32x4 te = on ? __builtin_bit_cast(f32x4, a.emb_tab[md.e_tab + col]) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    // s0 = sum g f (f = x at j = 0, else cos), s1 = sum g, u = sum g sin, v = sum g sin x; the w and b
+    // terms are -alpha v and -alpha u (unused at j = 0), every element computed the same way
+    float s0 = 0.0f, s1 = 0.0f, u = 0.0f, v = 0.0f;
+    // ALL: every row of the tile is a batch row (the common case: a loop without the row test)
+    auto sums = [&](auto ALL) {
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int rl = wm * MB * 32 + 32 * i + 8 * (r >> 2) + 4 * hv + (r & 3);
-          if (t.m0 + rl >= a.rows_valid) continue;
-          const float g = acc[i][j][r], x = xs[rl][f];
-          s1 += g;
-          if (fj == 0) {
-            s0 += g * x;
-          } else {
-            float sn, cs;
-            emb_sincos<FAST>(w * x + b, &sn, &cs);
-            s0 += g * cs;
-            const float tt = -g * al * sn;
-            s3 += tt;
-            s2 += tt * x;
-          }
+      for (int r = 0; r < 16; ++r) {
+        const int rl = wm * MB * 32 + 32 * i + 8 * (r >> 2) + 4 * hv + (r & 3);
+        float g = acc[i][j][r];
+        if constexpr (!ALL.value)
+          if (t.m0 + rl >= a.rows_valid) g = 0.0f;
+        const float x = xs[rl][f];
+        float sn, cs;
+        if constexpr (FAST) {
+          const float rev = __builtin_amdgcn_fractf(fmaf(te[0], x, te[1]));
+          sn = __builtin_amdgcn_sinf(rev);
+          cs = __builtin_amdgcn_cosf(rev);
+        } else {
+          sincosf(fmaf(te[0], x, te[1]), &sn, &cs);
         }
-    }
+        s1 += g;
+        s0 = fmaf(g, j0 ? x : cs, s0);
+        const float gs = g * sn;
+        u += gs;
+        v = fmaf(gs, x, v);
+      }
+    };
+    if (all_rows)
+      sums(std::true_type{});
+    else
+      sums(std::false_type{});
     s0 += __shfl_xor(s0, 32, 64);
     s1 += __shfl_xor(s1, 32, 64);
-    s2 += __shfl_xor(s2, 32, 64);
-    s3 += __shfl_xor(s3, 32, 64);
+    u += __shfl_xor(u, 32, 64);
+    v += __shfl_xor(v, 32, 64);
     if (on && hv == 0) {
       part[col] = s0;
       part[d.ldc + col] = s1;
-      part[2 * d.ldc + col] = s2;
-      part[3 * d.ldc + col] = s3;
+      part[2 * d.ldc + col] = -te[2] * v;
+      part[3 * d.ldc + col] = -te[2] * u;
     }
   }
 }

@@ -122,9 +122,9 @@ struct GemmArgs {
   // terms per column (alpha: dE f, beta: dE, w: -dE alpha sin(phi) x, b:
   // -dE alpha sin(phi); f = x or cos(phi), phi = w x + b) and writes them at
   // C + ((row0 / 64) * 4 + q) * ldc + col.  x of batch row r (< rows_valid) is
-  // emb_x[emb_idx[member * rows_valid + r] * emb_d_in + feature].
+  // emb_x[emb_idx[member * rows_valid + r] * emb_d_in + feature]; w, b and
+  // alpha come from the column table emb_tab (below).
   const float* emb_x;
-  const float* emb_theta;  // the parameters (w, b, alpha at the member's offsets)
   const int32_t* emb_idx;
   const MemberDev* emb_mem;
   int32_t emb_d_in;
