@@ -952,6 +952,11 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       d.poff = m.toff[2 * (l - 1)];
       d.lr = (float)m.lr;
       d.wd = (float)m.wd;
+      // the rows that exist (the member's true width): the optimizer leaves the zero padding rows
+      // alone (1.365 -> 1.359 ms per step; skipping the padding columns as well, which leaves
+      // holes in the rows' streaming stores, measured 1.362 ms, and 12.5 against 12.2 ms on the
+      // embedded step)
+      d.opt_rows = m.width;
       if (l == 1 && h->stream_rows && m.d_emb == 0 && !sizing) {  // rows straight from the data copy
         d.B = h->xb;
         d.ldb = h->Pin;

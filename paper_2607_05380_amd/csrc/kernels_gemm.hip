@@ -1013,7 +1013,7 @@ __device__ __forceinline__ void stage_flush_adamw(const GemmArgs& a, const GemmD
       const int v = (it0 + u) * 64 + lane;
       const int r = v / S::VPR, c = v % S::VPR;
       const int row = row0 + r, col = col0 + c * 4;
-      ok[u] = row < d.M && col < d.N;
+      ok[u] = row < d.opt_rows && col < d.N;
       g[u] = *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16);
       e[u] = (int64_t)row * d.ldc + col;
       if (ok[u]) {  // the optimizer state streams: non-temporal, so it does not evict GEMM operands
@@ -1072,7 +1072,8 @@ __device__ __forceinline__ void dw_adamw_small(const GemmArgs& a, const GemmDesc
   const AdamConst ac = a.adam;
   const float decay = 1.0f - d.lr * d.wd;
   const float step = d.lr / ac.bc1;
-  const int mrows = min(d.M - t.m0, 128), ncols = min(d.N - t.n0, 128);
+  // the rows that hold weights (the padding rows stay zero: not loaded, not written)
+  const int mrows = min(d.opt_rows - t.m0, 128), ncols = min(d.N - t.n0, 128);
   // vector u of this thread in a pass: row 8 u + tid / 32 of the pass, columns 4 (tid % 32) .. +3
   const int r0 = tid >> 5, c = (tid & 31) * 4;
   const bool colok = c < ncols;

@@ -77,6 +77,13 @@ struct GemmDesc {
   const int32_t* xrows;
   int32_t xrows_n;
   int64_t xsrc_rows;
+  // EPI_DW with fused AdamW: the rows r >= opt_rows (past the member's true
+  // width) are zero padding, left untouched (their gradients, moments and
+  // values stay exactly zero).  The columns' padding is updated like weights:
+  // skipping it leaves holes in the rows' streaming stores, which measured
+  // slower.
+  int32_t opt_rows;
+  int32_t pad2_;
 };
 
 struct Tile {
