@@ -198,6 +198,7 @@ struct pack_handle {
   // launch (launch_tiles), else a fixed TileSet
   int tiles_fwd = -1, tiles_dx = -1, tiles_dw = -1;
   TileSet ns_tiles = TILES_SMALL;  // tile set of the Newton-Schulz GEMMs
+  TileSet emb_tiles = TILES_SMALL;  // tile set of the embedded first layer's forward (training and evaluation)
   // side stream for ALU-bound work that overlaps memory-bound kernels of the
   // caller's stream, joined back through events (created by pack_bind)
   hipStream_t side = nullptr;
@@ -497,6 +498,22 @@ void add_tiles(Plan& p, Launch& ln, int d, int M, int N, int kdepth) {
     const int r = E % kBigTile;
     return r == 0 ? E : (r > kSmallTile ? E - r + kBigTile : E - r);
   };
+  if (p.tile_set == TILES_WIDE) {
+    // 128 x 256 tiles; a last strip of at most 128 columns on 256 x 128 tiles
+    const int r = N % kBigTile, Nw = r > 0 && r <= kSmallTile ? N - r : N;
+    for (int m0 = 0; m0 < M; m0 += kSmallTile)
+      for (int n0 = 0; n0 < Nw; n0 += kBigTile) {
+        p.tiles.push_back(Tile{d, m0, n0, kShapeWide});
+        p.cost.push_back((int64_t)kdepth * std::min(kSmallTile, M - m0) * std::min(kBigTile, N - n0));
+      }
+    if (Nw < N)
+      for (int m0 = 0; m0 < M; m0 += kBigTile) {
+        p.tiles.push_back(Tile{d, m0, Nw, kShapeTall8});
+        p.cost.push_back((int64_t)kdepth * std::min(kBigTile, M - m0) * (N - Nw));
+      }
+    ln.ntiles = (int)p.tiles.size() - ln.tile0;
+    return;
+  }
   const bool big = p.tile_set == TILES_BIG, tall = p.tile_set == TILES_TALL;
   const int Mb = big || tall ? big_end(M) : 0;
   const int Nb = big ? big_end(N) : (tall ? (int)round_up(N, kSmallTile) : 0);
@@ -861,8 +878,8 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
     int64_t nsm = 0;
     for (int k : group[hf])
       if (h->mem[k].depth >= l) nsm += small_tiles(h->Bp, h->mem[k].dp);
-    // the embedded first layer (E produced in the GEMM) runs small tiles only
-    p.tile_set = l == 1 && h->emb ? TILES_SMALL : choose(h->tiles_fwd, nsm);
+    // the embedded first layer (E produced in the GEMM): its own tile set
+    p.tile_set = l == 1 && h->emb ? (sizing ? TILES_SMALL : h->emb_tiles) : choose(h->tiles_fwd, nsm);
     for (int k : group[hf]) {
       const Member& m = h->mem[k];
       if (m.depth < l) continue;
@@ -913,7 +930,7 @@ Plan build_plan(const pack_handle* h, const Bufs& bf, const std::vector<int> (&g
       f.ndesc += (int)group[hf].size();
       for (int k : group[hf]) nsm += small_tiles(h->Bp, h->mem[k].dp);
     }
-    p.tile_set = h->emb ? TILES_SMALL : choose(h->tiles_fwd, nsm);
+    p.tile_set = h->emb ? (sizing ? TILES_SMALL : h->emb_tiles) : choose(h->tiles_fwd, nsm);
     for (int hf = 0; hf < kGroups; ++hf)
       for (int i = 0; i < (int)group[hf].size(); ++i) {
         const int k = group[hf][i];
@@ -1417,6 +1434,11 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
     h->ns_tiles = v == "big" ? TILES_BIG : (v == "tall" ? TILES_TALL : TILES_SMALL);
   }
   if (h->prec == Prec::FP32) h->ns_tiles = TILES_SMALL;
+  // the embedded first layer's forward: wide tiles in bf16 (each produced E
+  // element feeds 256 output columns); TABPACK_EMB_TILES=small overrides
+  h->emb_tiles = h->prec == Prec::BF16 ? TILES_WIDE : TILES_SMALL;
+  if (const char* e = getenv("TABPACK_EMB_TILES"))
+    if (std::string(e) == "small") h->emb_tiles = TILES_SMALL;
   h->muon = cfg->optimizer == PACK_OPT_MUON;
   h->emb = cfg->emb_lo > 0;
   h->ns_steps = cfg->ns_steps ? cfg->ns_steps : 5;

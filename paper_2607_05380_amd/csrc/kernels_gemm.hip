@@ -149,6 +149,16 @@ struct Shape<kShapeTall> {
   static constexpr int MB = 4, NB = 2, TM = 256, TN = 128;
   static constexpr int STAGE = 32 * (NB * 128 + 32);
 };
+template <>
+struct Shape<kShapeWide> {
+  static constexpr int MB = 2, NB = 2, TM = 128, TN = 256;
+  static constexpr int STAGE = 32 * (NB * 128 + 32);
+};
+template <>
+struct Shape<kShapeTall8> {
+  static constexpr int MB = 2, NB = 2, TM = 256, TN = 128;
+  static constexpr int STAGE = 32 * (NB * 128 + 32);
+};
 
 template <typename T>
 struct Elem;
@@ -515,19 +525,20 @@ struct EmbMember {
   __device__ bool first(int c) const { return c == (int)__umulhi((uint32_t)c, magic) * dp; }  // j = 0
 };
 
-// A operand of the forward (rows: the tile's 128 batch rows, depth-contiguous
+// A operand of the forward (rows: the tile's TM batch rows, depth-contiguous
 // LDS layout): per K step, lane l of wave w produces chunk l / 8 of rows
-// l % 8 + 8 w + 32 i (i < 4), so the 8 lanes of a lane group share a chunk
-// and its table entries.  bf16: the K step's 64 table entries reach LDS with
+// l % 8 + 8 w + (NTH / 8) i (i < 8 TM / NTH, NTH threads), so the 8 lanes of
+// a lane group share a chunk and its table entries.  bf16: the K step's 64 table entries reach LDS with
 // one direct load of wave 0 (two steps ahead, beside the W_1 stage), and each
 // lane group reads its 8 from there (one address per group: no bank
 // conflicts); the rows' x are loaded into registers two steps ahead.  fp32:
 // each thread loads its chunk's entries itself.  Rows outside the batch read
 // data row 0 (finite values; the epilogue zeroes those rows).
-template <typename T>
+template <typename T, int TM = 128, int NTH = NT>
 struct EmbRowsProducer {
   static constexpr int VE = 16 / sizeof(T);  // columns per chunk
-  static constexpr int NR = 128 * 8 / NT;    // rows per thread
+  static constexpr int NR = TM * 8 / NTH;    // rows per thread
+  static constexpr int RS = NTH / 8;         // row stride between a thread's rows
   EmbMember em;
   const float* xrow[NR];  // the rows' feature 0
   int slot, rl0, lane, wave;
@@ -541,7 +552,7 @@ struct EmbRowsProducer {
     rl0 = lane % 8 + 8 * wave;
 #pragma unroll
     for (int i = 0; i < NR; ++i) {
-      const int r = t.m0 + rl0 + 32 * i;
+      const int r = t.m0 + rl0 + RS * i;
       const int64_t row =
           r < a.rows_valid ? (a.emb_idx ? (int64_t)a.emb_idx[(int64_t)d.member * a.rows_valid + r] : a.emb_row_base + r)
                            : 0;
@@ -580,7 +591,7 @@ struct EmbRowsProducer {
       for (int e = 0; e < VE; ++e)
         v[e] = e == 0 ? emb_value<sizeof(T) == 2, true>(tv[e], x[S][i], j0)
                       : emb_value<sizeof(T) == 2, false>(tv[e], x[S][i], false);
-      *reinterpret_cast<u32x4*>(lds + off(rl0 + 32 * i, slot)) = emb_pack<T>(v);
+      *reinterpret_cast<u32x4*>(lds + off(rl0 + RS * i, slot)) = emb_pack<T>(v);
     }
   }
 };
@@ -1582,15 +1593,20 @@ __device__ __forceinline__ void tile_extents(const GemmDesc& d, const Tile& t, i
   nv = nrem <= 0 ? 0 : (nrem >= NB * 32 ? NB : (nrem + 31) / 32);
 }
 
-template <typename T, int AK, int BK_, int EPI>
+// SH: small tiles (4 waves in 2 x 2) or, for the forward in bf16, wide tiles
+// (8 waves in 2 x 4: twice the output columns per produced A element) and
+// tall 8-wave tiles (4 x 2) for a last strip of at most 128 columns
+template <typename T, int AK, int BK_, int EPI, int SH = kShapeSmall>
 __device__ __forceinline__ void run_tile_emb(const GemmArgs& a, const GemmDesc& d, const Tile& t, char* lds0, int tid,
                                              int wave, char* xmap) {
-  constexpr int SH = kShapeSmall;
   constexpr bool FWD = AK == OP_EMB;  // else the weight gradient (B produced)
   static_assert(FWD ? BK_ == OP_KMAJ : (AK == OP_RMAJ && BK_ == OP_EMB && EPI == EPI_DW), "embedded operand");
+  constexpr bool WIDE = SH == kShapeWide, W8 = WIDE || SH == kShapeTall8;
+  static_assert(SH == kShapeSmall || (W8 && FWD && sizeof(T) == 2), "8-wave tiles: the bf16 forward");
+  constexpr int NW = W8 ? 8 : 4;  // waves
   constexpr int MB = Shape<SH>::MB, NB = Shape<SH>::NB, TM = Shape<SH>::TM, TN = Shape<SH>::TN;
   const int lane = tid & 63;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = WIDE ? wave >> 2 : wave >> 1, wn = WIDE ? wave & 3 : wave & 1;
   int mv, nv;
   tile_extents<EPI, SH>(d, t, wm, wn, mv, nv);
   const bool compute = mv > 0 && nv > 0;
@@ -1604,7 +1620,7 @@ __device__ __forceinline__ void run_tile_emb(const GemmArgs& a, const GemmDesc& 
   EpiPre<SH> pre;
   epi_prefetch<EPI, SH>(d, t, wm, wn, lane, pre);
   // the producer (A or B) and the streamed operand (B = W_1, or A = dZ_1)
-  std::conditional_t<FWD, EmbRowsProducer<T>, EmbColsProducer<T>> ep;
+  std::conditional_t<FWD, EmbRowsProducer<T, TM, 64 * NW>, EmbColsProducer<T>> ep;
   if constexpr (FWD) {
     ep.init(a, d, t, tid);
   } else {  // the batch rows' data rows, for every K step's x loads (one table per tile)
@@ -1616,17 +1632,21 @@ __device__ __forceinline__ void run_tile_emb(const GemmArgs& a, const GemmDesc& 
   if constexpr (sizeof(T) == 2) {
     constexpr int KS = kSmallKs;
     static_assert(KS == 4 && kSmallNs == 2, "the producers fill 64-deep steps of two stages");
-    using LS = std::conditional_t<FWD, DmaKmaj<TN, KS>, DmaRmaj<TM, KS>>;
+    // 8-wave tiles: waves 4 h .. 4 h + 3 load B rows h TN / 2 .. (h + 1) TN / 2 - 1
+    constexpr int BR = W8 ? TN / 2 : TN;
+    using LS = std::conditional_t<FWD, DmaKmaj<BR, KS>, DmaRmaj<TM, KS>>;
     constexpr int BKE = 16 * KS, TA = TM * 32 * KS, TB = TN * 32 * KS;
+    static_assert(!W8 || TA + TB == (128 + 256) * 32 * KS, "8-wave tiles share one LDS layout");
+    const int bh = W8 ? wave >> 2 : 0;  // B half of the wave (8-wave tiles)
     LS ls;
     if constexpr (FWD)
-      ls.init(static_cast<const T*>(d.B), d.ldb, t.n0, d.N, d.Kd, wave, lane);
+      ls.init(static_cast<const T*>(d.B), d.ldb, t.n0 + BR * bh, d.N, d.Kd, wave & 3, lane);
     else
       ls.init(static_cast<const T*>(d.A), d.lda, t.m0, d.M, d.Kd, wave, lane);
     const int nk = (d.Kd + BKE - 1) / BKE;
     // stage k: the produced operand at prod(b), the streamed one at strm(b)
     auto prod = [](char* b) { return FWD ? b : b + TA; };
-    auto strm = [](char* b) { return FWD ? b + TA : b; };
+    auto strm = [&](char* b) { return FWD ? b + TA + bh * (BR * 32 * KS) : b; };
     using S0 = std::integral_constant<int, 0>;
     using S1 = std::integral_constant<int, 1>;
     // forward: the table entries of step s in tab(s & 1), after both stages
@@ -1784,6 +1804,25 @@ gemm_kernel_small(GemmArgs a) {
     run_tile<T, AK, BK_, EPI, kShapeSmall, 4, 2>(a, d, t, smem, tid, wave);
 }
 
+// The embedded first layer's bf16 forward on wide tiles (128 x 256; a last
+// strip of at most 128 columns on tall 256 x 128 tiles): one workgroup of 8
+// waves per CU (two stages of 48 KB: 16 KB of produced E and 32 KB of W_1, or
+// the reverse; two 1 KB stages of column-table entries).
+template <int EPI>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_kernel_emb_wide(GemmArgs a) {
+  constexpr int kOps = 2 * (128 + 256) * 32 * kSmallKs;
+  static_assert(8 * Shape<kShapeWide>::STAGE <= kOps, "epilogue staging of 8 waves");
+  __shared__ __attribute__((aligned(16))) char smem[kOps + 2048];
+  const Tile t = a.tiles[blockIdx.x];
+  const GemmDesc d = a.descs[t.desc];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  if (t.shape == kShapeWide)
+    run_tile_emb<__bf16, OP_EMB, OP_KMAJ, EPI, kShapeWide>(a, d, t, smem, tid, wave, nullptr);
+  else
+    run_tile_emb<__bf16, OP_EMB, OP_KMAJ, EPI, kShapeTall8>(a, d, t, smem, tid, wave, nullptr);
+}
+
 // Launches of tall tiles (256 x 128) with small edge tiles, bf16 only: two
 // workgroups per CU, each with kTallNs stages of the tall pipeline.
 template <int AK, int BK_, int EPI>
@@ -1839,8 +1878,22 @@ hipError_t launch_prec(OpKind ak, OpKind bk, EpiKind e, const GemmArgs& args, hi
     return launch_t<T, OP_KMAJ, OP_KMAJ, EPI_FWD_EVAL>(args, s);
   if (ak == OP_KMAJ && bk == OP_RMAJ && e == EPI_DX) return launch_t<T, OP_KMAJ, OP_RMAJ, EPI_DX>(args, s);
   if (ak == OP_RMAJ && bk == OP_RMAJ && e == EPI_DW) return launch_t<T, OP_RMAJ, OP_RMAJ, EPI_DW>(args, s);
-  if (ak == OP_EMB || bk == OP_EMB) {  // the embedded first layer: small tiles
-    if (args.tile_set != TILES_SMALL || !args.emb_tab || !args.emb_x || !args.emb_mem) return hipErrorInvalidValue;
+  if (ak == OP_EMB || bk == OP_EMB) {  // the embedded first layer: small tiles (the bf16 forward: or wide)
+    if (!args.emb_tab || !args.emb_x || !args.emb_mem) return hipErrorInvalidValue;
+    if (args.tile_set == TILES_WIDE) {
+      if constexpr (sizeof(T) == 2) {
+        if (ak == OP_EMB && bk == OP_KMAJ && (e == EPI_FWD || e == EPI_FWD_EVAL)) {
+          if (args.ntiles <= 0) return hipSuccess;
+          if (e == EPI_FWD)
+            hipLaunchKernelGGL(gemm_kernel_emb_wide<EPI_FWD>, dim3(args.ntiles), dim3(512), 0, s, args);
+          else
+            hipLaunchKernelGGL(gemm_kernel_emb_wide<EPI_FWD_EVAL>, dim3(args.ntiles), dim3(512), 0, s, args);
+          return hipGetLastError();
+        }
+      }
+      return hipErrorInvalidValue;
+    }
+    if (args.tile_set != TILES_SMALL) return hipErrorInvalidValue;
     if (ak == OP_EMB && bk == OP_KMAJ && e == EPI_FWD) return launch_small<T, OP_EMB, OP_KMAJ, EPI_FWD>(args, s);
     if (ak == OP_EMB && bk == OP_KMAJ && e == EPI_FWD_EVAL)
       return launch_small<T, OP_EMB, OP_KMAJ, EPI_FWD_EVAL>(args, s);

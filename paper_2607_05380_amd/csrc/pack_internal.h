@@ -16,13 +16,17 @@ constexpr int kRowAlign = 256;     // base-batch rows are padded to a multiple o
 constexpr uint32_t kTagDropout = 3;
 
 // Grouped-GEMM output tiles: big 256 x 256 (4 waves of 128 x 128), tall
-// 256 x 128 (4 waves of 128 x 64) and small 128 x 128 (4 waves of 64 x 64).
-constexpr int kShapeBig = 0, kShapeSmall = 1, kShapeTall = 2;
+// 256 x 128 (4 waves of 128 x 64), small 128 x 128 (4 waves of 64 x 64), and
+// for the embedded first layer's forward wide 128 x 256 and tall 256 x 128
+// tiles of 8 waves of 64 x 64 (the latter for a last column strip of at most
+// 128 columns).
+constexpr int kShapeBig = 0, kShapeSmall = 1, kShapeTall = 2, kShapeWide = 3, kShapeTall8 = 4;
 constexpr int kBigTile = 256, kSmallTile = 128;
 // Tile sets of one launch (one kernel each): big tiles with small edge strips
-// (one workgroup per CU), small tiles only, or tall tiles with small edge
-// strips (two workgroups per CU each).
-enum TileSet : int { TILES_BIG = 0, TILES_SMALL = 1, TILES_TALL = 2 };
+// (one workgroup per CU), small tiles only, tall tiles with small edge strips
+// (two workgroups per CU each), or wide tiles with tall 8-wave tiles for a
+// narrow last column strip (one workgroup of 8 waves per CU).
+enum TileSet : int { TILES_BIG = 0, TILES_SMALL = 1, TILES_TALL = 2, TILES_WIDE = 3 };
 constexpr int kPartRows = 64;   // rows per bias-gradient partial written by the dX epilogue
 constexpr int kXcds = 8;        // MI355X: workgroups go round-robin to 8 XCDs
 static_assert(kRowAlign % kBigTile == 0, "row padding must cover whole GEMM row tiles");

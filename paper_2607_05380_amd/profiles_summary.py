@@ -55,6 +55,12 @@ def short_name(kernel):
     arguments: element type, operand kinds (0 depth-contiguous, 1 row-major, 2 the
     embedded first-layer input produced in the GEMM) and
     epilogue."""
+    if "gemm_kernel_emb_wide" in kernel:  # the embedded forward on 8-wave tiles: bf16, E x W_1
+        m = re.search(r"gemm_kernel_emb_wide(?:ILi(\d)EE|<(\d)>)", kernel)
+        if not m:
+            return None
+        epi = int(m.group(1) or m.group(2))
+        return f"gemm_bf16_{OPS[2]}_{OPS[0]}_{EPIS[epi]}" if epi < len(EPIS) else None
     if "gemm_kernel" in kernel:
         m = re.search(r"gemm_kernel(?:_small|_tall)?I(DF16b|f)?(?:Li(\d)E)(?:Li(\d)E)(?:Li(\d)E)", kernel)
         if m:

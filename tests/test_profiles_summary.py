@@ -18,6 +18,8 @@ from paper_2607_05380_amd import profiles_summary as ps
     ("_ZN7tabpack12_GLOBAL__N_116gemm_kernel_tallILi0ELi1ELi2EEEvNS_8GemmArgsE", "gemm_bf16_kmaj_rmaj_dx"),
     ("void tabpack::(anonymous namespace)::gemm_kernel<float, 0, 1, 4>(tabpack::GemmArgs)", "gemm_f32_kmaj_rmaj_ns"),
     ("_ZN7tabpack12_GLOBAL__N_111gemm_kernelIDF16bLi0ELi0ELi1EEEvNS_8GemmArgsE", "gemm_bf16_kmaj_kmaj_fwd_eval"),
+    ("_ZN7tabpack12_GLOBAL__N_120gemm_kernel_emb_wideILi0EEEvNS_8GemmArgsE", "gemm_bf16_emb_kmaj_fwd"),
+    ("void tabpack::(anonymous namespace)::gemm_kernel_emb_wide<1>(tabpack::GemmArgs)", "gemm_bf16_emb_kmaj_fwd_eval"),
     ("void tabpack::(anonymous namespace)::muon_update_kernel<__bf16>(...)", "muon_update"),
     ("void tabpack::(anonymous namespace)::select_partial_kernel(...)", "select_partial"),
     ("void at::native::elementwise_kernel<128, 4>(...)", None),
