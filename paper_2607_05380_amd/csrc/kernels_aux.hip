@@ -338,6 +338,24 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const T* H, const float* 
   }
 }
 
+// sum over i < ceil(n / step) of term(i), added in order of i; the terms are
+// fetched 8 at a time before they are added, so their loads overlap
+template <typename V, typename F>
+__device__ __forceinline__ V sum_in_order(int n, int step, F term) {
+  const int m = n <= 0 ? 0 : (n + step - 1) / step;
+  V s = 0;
+  int i = 0;
+  for (; i + 8 <= m; i += 8) {
+    V v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = term(i + u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  for (; i < m; ++i) s += term(i);
+  return s;
+}
+
 // The gradient sums of a member group, one wave per ColTile (fixed orders):
 //   part >= 0: db_{part+1}[c] = sum over the 64-row blocks of the dX
 //     epilogue's column partials (bias layer part at colpart + part * part_stride);
@@ -357,14 +375,12 @@ __global__ __launch_bounds__(256) void grad_sums_kernel(const float* colpart, in
   const int lane = threadIdx.x & 63;
   if (ct.part == kSumLoss) {
     const int64_t r0 = (int64_t)ct.member * Bp;
-    double s = 0.0;
-    for (int r = lane; r < B; r += 64) s += (double)rowloss[r0 + r];
-    s = wave_sum_d(s);
+    const double s =
+        wave_sum_d(sum_in_order<double>(B - lane, 64, [&](int i) { return (double)rowloss[r0 + lane + 64 * i]; }));
     if (lane == 0) loss_out[ct.member] = (float)(s / (double)B);
     for (int o = 0; o < d_out; ++o) {
-      double g = 0.0;
-      for (int r = lane; r < B; r += 64) g += (double)dY[(r0 + r) * d_out + o];
-      g = wave_sum_d(g);
+      const double g = wave_sum_d(
+          sum_in_order<double>(B - lane, 64, [&](int i) { return (double)dY[(r0 + lane + 64 * i) * d_out + o]; }));
       if (lane == 0) grad[md.b_out_off + o] = (float)g;
     }
     return;
@@ -375,8 +391,8 @@ __global__ __launch_bounds__(256) void grad_sums_kernel(const float* colpart, in
     const int nrb = Bp / RB;
     const float* pk = headpart + (int64_t)nrb * (d_out + 1) * (md.act_off / Bp);
     for (int o = 0; o <= d_out; ++o) {
-      float v = 0.0f;
-      for (int rb = 0; rb < nrb; ++rb) v += pk[((int64_t)rb * (d_out + 1) + o) * md.dp + c];
+      const float v =
+          sum_in_order<float>(nrb, 1, [&](int rb) { return pk[((int64_t)rb * (d_out + 1) + o) * md.dp + c]; });
       if (o < d_out)
         grad[md.w_out_off + (int64_t)o * md.dp + c] = v;
       else
@@ -385,9 +401,8 @@ __global__ __launch_bounds__(256) void grad_sums_kernel(const float* colpart, in
     return;
   }
   const float* p = colpart + ct.part * part_stride + md.act_off / kPartRows;
-  float v = 0.0f;
-  for (int r = 0; r < Bp / kPartRows; ++r) v += p[(int64_t)r * md.dp + c];
-  grad[bias_off[(int64_t)ct.part * K + ct.member] + c] = v;
+  grad[bias_off[(int64_t)ct.part * K + ct.member] + c] =
+      sum_in_order<float>(Bp / kPartRows, 1, [&](int r) { return p[(int64_t)r * md.dp + c]; });
 }
 
 // ----------------------------------------------------------------- gather --
