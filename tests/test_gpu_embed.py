@@ -132,3 +132,50 @@ def test_embedding_eval_predict_and_muon():
     mem = pk.predict(Xv).cpu().numpy()
     for k in range(cfg["K"]):
         check_tensor(f"predict {k}", mem[k], op.predict_values(k, Xva), TOL["bf16"])
+
+
+def test_embedded_tile_sets_and_streams_are_bit_identical(monkeypatch):
+    # The embedded forward's 8-wave tiles (128 x 256, a last strip of at most
+    # 128 columns on 256 x 128 tiles) reduce every output element over the
+    # full depth in the small tiles' order, and the epilogue is the same per
+    # element: training steps, states and evaluation predictions must be
+    # bit-identical to the small tiles', and to another split over streams.
+    # Padded widths 96, 256, 320, 416, 544, 1024: last strips of 96 (no wide
+    # tile), 0, 64, 160 (a wide tile with masked waves), 32 and 0 columns.
+    cfg = configs.workload("regression_large", K=6, B=300, **EMB)
+    members = [dict(width=w, dropout=p, lr=2e-3, wd=1e-3, d_emb=e, sigma=1.0)
+               for w, p, e in ((96, 0.1, 8), (256, 0.0, 12), (300, 0.3, 16), (416, 0.2, 20), (520, 0.4, 24),
+                               (1000, 0.1, 32))]
+    Xtr, ytr, Xva, yva, _, idx = make_inputs(cfg, 3000, 700)
+    X, y, idx_d, Xv, yv = to_dev(Xtr, ytr, idx, Xva, yva)
+    runs = {}
+    for tiles, streams in (("small", "2"), ("wide", "2"), ("wide", "1")):
+        if tiles == "small":
+            monkeypatch.setenv("TABPACK_EMB_TILES", "small")
+        else:
+            monkeypatch.delenv("TABPACK_EMB_TILES", raising=False)
+        monkeypatch.setenv("TABPACK_STREAMS", streams)
+        pk = tabpack.Pack(cfg, members=members).bind()
+        losses = [pk.train_step(X, y, idx_d, s).cpu().numpy() for s in (1, 2)]
+        pred, score = pk.eval_members(Xv, yv)
+        states = [(pk.get_params(k), pk.get_moments(k)) for k in range(cfg["K"])]
+        runs[(tiles, streams)] = (losses, pred.cpu().numpy(), score.cpu().numpy(), states)
+    ref = runs[("small", "2")]
+    for key, got in runs.items():
+        msg = str(key)
+        for a, b in zip(ref[0], got[0]):
+            np.testing.assert_array_equal(a, b, err_msg=msg)
+        np.testing.assert_array_equal(ref[1], got[1], err_msg=msg)
+        np.testing.assert_array_equal(ref[2], got[2], err_msg=msg)
+        for (p1, m1), (p2, m2) in zip(ref[3], got[3]):
+            for n in NAMES:
+                np.testing.assert_array_equal(p1[0][n], p2[0][n], err_msg=msg)
+            for (W1, b1), (W2, b2) in zip(p1[1:], p2[1:]):
+                np.testing.assert_array_equal(W1, W2, err_msg=msg)
+                np.testing.assert_array_equal(b1, b2, err_msg=msg)
+            for x1, x2 in zip(m1, m2):
+                for n in NAMES:
+                    np.testing.assert_array_equal(x1[0][n], x2[0][n], err_msg=msg)
+                for (W1, b1), (W2, b2) in zip(x1[1:], x2[1:]):
+                    np.testing.assert_array_equal(W1, W2, err_msg=msg)
+                    np.testing.assert_array_equal(b1, b2, err_msg=msg)
