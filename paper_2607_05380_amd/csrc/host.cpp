@@ -199,6 +199,7 @@ struct pack_handle {
   int tiles_fwd = -1, tiles_dx = -1, tiles_dw = -1;
   TileSet ns_tiles = TILES_SMALL;  // tile set of the Newton-Schulz GEMMs
   TileSet emb_tiles = TILES_SMALL;  // tile set of the embedded first layer's forward (training and evaluation)
+  bool muon_fused = true;  // the Muon update in the last Newton-Schulz GEMM's epilogue
   // side stream for ALU-bound work that overlaps memory-bound kernels of the
   // caller's stream, joined back through events (created by pack_bind)
   hipStream_t side = nullptr;
@@ -713,6 +714,7 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
   struct Item {
     MuonShape q;
     int64_t xoff, aoff;
+    int mi;  // its MuonMat in p.mmats
   };
   auto xp = [&](int par, int64_t off) { return (void*)(bf.mX[par] + (size_t)off * es); };
   auto ap = [&](const char* base, int64_t off) { return (void*)(base + (size_t)off * es); };
@@ -740,7 +742,7 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
         for (int r0 = 0; r0 < q.R; r0 += 64)
           for (int c0 = 0; c0 < q.Cp; c0 += 64) p.mtiles.push_back(MuonTile{mi, r0, c0, 0});
         p.mtile0.push_back((int32_t)p.mtiles.size());
-        items.push_back(Item{q, xo, ao});
+        items.push_back(Item{q, xo, ao, mi});
         xo += round_up((int64_t)q.S * q.L, kChunk);
         ao += round_up((int64_t)q.S * q.S, kChunk);
       }
@@ -806,6 +808,12 @@ void plan_muon(const pack_handle* h, const Bufs& bf, const std::vector<int> (&gr
         d.M = it.q.S;
         d.N = it.q.L;
         d.Kd = it.q.S;
+        // the weight the last iteration updates in its epilogue
+        const MuonMat& mm = p.mmats[it.mi];
+        d.poff = mm.woff;
+        d.ns_tall = mm.tall;
+        d.ns_decay = mm.decay;
+        d.ns_step = mm.step;
         add_tiles(p, ln, (int)p.descs.size(), d.M, d.N, d.Kd);
         p.descs.push_back(d);
         ++ln.ndesc;
@@ -1356,8 +1364,8 @@ hipError_t muon_step(pack_handle* h, const GemmArgs& base, int g, hipStream_t st
   });
   if (e != hipSuccess) return e;
   static const float kA = 3.4445f, kB = -4.7750f, kC = 2.0315f;
-  auto ns = [&](const Launch& ln, OpKind bk, float alpha, float beta, bool sym) {
-    GemmArgs ga = base;
+  auto ns_args = [&](const GemmArgs& b0, const Launch& ln, OpKind bk, float alpha, float beta, bool sym) {
+    GemmArgs ga = b0;
     ga.tiles += ln.tile0;
     ga.ntiles = ln.ntiles;
     ga.tile_set = h->ns_tiles;
@@ -1367,10 +1375,23 @@ hipError_t muon_step(pack_handle* h, const GemmArgs& base, int g, hipStream_t st
     return timed(h, gemm_name(h->prec, OP_KMAJ, bk, EPI_NS), 0, ln.flops, ln.bytes, stream,
                  [&] { return launch_gemm(h->prec, OP_KMAJ, bk, EPI_NS, ga, stream); });
   };
+  auto ns = [&](const Launch& ln, OpKind bk, float alpha, float beta, bool sym) {
+    return ns_args(base, ln, bk, alpha, beta, sym);
+  };
+  // the last iteration's X launch applies the update in its epilogue
+  // (TABPACK_MUON_FUSED_UPDATE=0: a separate update kernel reads the stored X)
+  const bool fused = h->muon_fused;
   for (int it = 0; it < h->ns_steps; ++it) {
     const int par = it & 1;
     if ((e = ns(h->nsA[par][g], OP_KMAJ, 0.0f, 1.0f, true)) != hipSuccess) return e;
     if ((e = ns(h->nsB[g], OP_KMAJ, kB, kC, true)) != hipSuccess) return e;
+    if (fused && it + 1 == h->ns_steps) {
+      GemmArgs fa = base;
+      fa.ns_theta = h->b.theta;
+      fa.ns_shadow = h->b.shadow;
+      if ((e = ns_args(fa, h->nsX[par][g], OP_RMAJ, kA, 1.0f, false)) != hipSuccess) return e;
+      return hipSuccess;
+    }
     if ((e = ns(h->nsX[par][g], OP_RMAJ, kA, 1.0f, false)) != hipSuccess) return e;
   }
   return timed(h, "muon_update", 1, 0.0, wbytes * (8.0 + h->elt() + (h->prec == Prec::BF16 ? 2.0 : 0.0)), stream,
@@ -1439,6 +1460,7 @@ int pack_init(const pack_config* cfg, pack_handle** out) {
   h->emb_tiles = h->prec == Prec::BF16 ? TILES_WIDE : TILES_SMALL;
   if (const char* e = getenv("TABPACK_EMB_TILES"))
     if (std::string(e) == "small") h->emb_tiles = TILES_SMALL;
+  if (const char* e = getenv("TABPACK_MUON_FUSED_UPDATE")) h->muon_fused = std::string(e) != "0";
   h->muon = cfg->optimizer == PACK_OPT_MUON;
   h->emb = cfg->emb_lo > 0;
   h->ns_steps = cfg->ns_steps ? cfg->ns_steps : 5;

@@ -997,6 +997,77 @@ __device__ __forceinline__ void stage_flush_ns_mirror(const char* stage, OT* C, 
   }
 }
 
+// The last Newton-Schulz iteration's rows with the Muon update fused: the new
+// X = alpha Y + beta (staged block), rounded to OT as it would be stored,
+// replaces the staged values; then each weight element w it orthogonalises
+// becomes w decay - step x (no contraction, as in the separate update), read
+// row-wise or, for tall weights (W = X^T), column-wise from the stage.
+template <typename OT, int NB>
+__device__ __forceinline__ void stage_update_ns(const GemmArgs& a, const GemmDesc& d, char* stage, int row0, int col0,
+                                                int lane) {
+  using S = Stage<float, NB>;
+  const OT* Y = static_cast<const OT*>(d.Y);
+#pragma unroll
+  for (int it = 0; it < S::PER_LANE; ++it) {
+    const int v = it * 64 + lane;
+    const int r = v / S::VPR, c = v % S::VPR;
+    const int row = row0 + r, col = col0 + c * 4;
+    if (row >= d.M || col >= d.N) continue;
+    f32x4& x = *reinterpret_cast<f32x4*>(stage + r * S::RS + c * 16);
+    const f32x4 xv = x;
+    float o[4] = {a.ns_beta * xv[0], a.ns_beta * xv[1], a.ns_beta * xv[2], a.ns_beta * xv[3]};
+    if (Y) {
+      const OT* yp = Y + (int64_t)row * d.ldy + col;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = a.ns_alpha * to_float(yp[q]) + o[q];
+    }
+    x = f32x4{to_float(from_float<OT>(o[0])), to_float(from_float<OT>(o[1])), to_float(from_float<OT>(o[2])),
+              to_float(from_float<OT>(o[3]))};
+  }
+  wave_sync_lds();
+  const float decay = d.ns_decay, step = d.ns_step;
+  auto update = [&](int64_t e, const f32x4& x) {
+    float* tp = a.ns_theta + d.poff + e;
+    f32x4 w = *glob(reinterpret_cast<const f32x4*>(tp));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma clang fp contract(off)
+      w[q] = w[q] * decay - step * x[q];
+    }
+    *glob(reinterpret_cast<f32x4*>(tp)) = w;
+    if (a.ns_shadow) {
+      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)w[0]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)w[1]) << 16);
+      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)w[2]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)w[3]) << 16);
+      *glob(reinterpret_cast<u32x2*>(a.ns_shadow + d.poff + e)) = u32x2{lo, hi};
+    }
+  };
+  if (!d.ns_tall) {  // W row = X row: the row-wise vectors above
+#pragma unroll
+    for (int it = 0; it < S::PER_LANE; ++it) {
+      const int v = it * 64 + lane;
+      const int r = v / S::VPR, c = v % S::VPR;
+      const int row = row0 + r, col = col0 + c * 4;
+      if (row >= d.M || col >= d.N) continue;
+      update((int64_t)row * d.N + col, *reinterpret_cast<const f32x4*>(stage + r * S::RS + c * 16));
+    }
+  } else {  // W row = X column: 4 consecutive staged rows of one staged column
+    constexpr int CV = 32 / 4;
+#pragma unroll
+    for (int it = 0; it < NB * 32 * CV / 64; ++it) {
+      const int v = it * 64 + lane;
+      const int c = v / CV, r = (v % CV) * 4;
+      const int wrow = col0 + c, wcol = row0 + r;
+      if (wrow >= d.N || wcol >= d.M) continue;
+      f32x4 x;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[q] = *reinterpret_cast<const float*>(stage + (r + q) * S::RS + c * 4);
+      update((int64_t)wrow * d.M + wcol, x);
+    }
+  }
+}
+
 // Weight-gradient rows with the optimizer fused: each staged vector holds the
 // gradients of 4 consecutive weights, which are updated in place (theta, both
 // moments, the bf16 shadow); the gradient itself is stored only on request.
@@ -1238,11 +1309,15 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const GemmDesc& d, c
             for (int q = 0; q < 4; ++q)
               stage_put<float, NB>(stage, j, g, q, lane, acc[i][j][4 * (p * S::GP + g) + q]);
         wave_sync_lds();
-        stage_flush_ns<T, NB>(stage, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.Y), d.ldy, a.ns_alpha,
-                              a.ns_beta, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
-        if (a.ns_sym && t.m0 < t.n0)  // uniform: a tile above the diagonal also writes its mirror image
-          stage_flush_ns_mirror<T, NB>(stage, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.Y), d.ldy,
-                                       a.ns_alpha, a.ns_beta, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
+        if (a.ns_theta) {  // uniform: the last iteration applies the Muon update instead of storing X
+          stage_update_ns<T, NB>(a, d, stage, row0 + 32 * i + S::ROWS * p, col0, lane);
+        } else {
+          stage_flush_ns<T, NB>(stage, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.Y), d.ldy, a.ns_alpha,
+                                a.ns_beta, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
+          if (a.ns_sym && t.m0 < t.n0)  // uniform: a tile above the diagonal also writes its mirror image
+            stage_flush_ns_mirror<T, NB>(stage, static_cast<T*>(d.C), d.ldc, static_cast<const T*>(d.Y), d.ldy,
+                                         a.ns_alpha, a.ns_beta, row0 + 32 * i + S::ROWS * p, col0, d.M, d.N, lane);
+        }
         wave_sync_lds();
       }
     }

@@ -68,7 +68,7 @@ struct GemmDesc {
   float drop_s;        // s_k
   float lr, wd;        // EPI_DW with fused AdamW: the member's learning rate and weight decay
   int32_t pad_;
-  int64_t poff;        // EPI_DW with fused AdamW: element offset of the weight tensor
+  int64_t poff;        // EPI_DW with fused AdamW, EPI_NS with the Muon update: element offset of the weight tensor
   const void* Y;       // EPI_NS: the matrix added to the product (GEMM precision), or nullptr
   int64_t ldy;
   // bf16 only: the batch rows of the operand that holds the data, taken
@@ -87,7 +87,11 @@ struct GemmDesc {
   // skipping it leaves holes in the rows' streaming stores, which measured
   // slower.
   int32_t opt_rows;
-  int32_t pad2_;
+  // EPI_NS with the Muon update: the weight is stored transposed to X (tall);
+  // its decay 1 - lr wd and step lr max(1, rows / cols)^(1/2)
+  int32_t ns_tall;
+  float ns_decay, ns_step;
+  int32_t pad3_;
 };
 
 struct Tile {
@@ -128,6 +132,13 @@ struct GemmArgs {
   // symmetric C and every tile above it also stores its transpose
   float ns_alpha, ns_beta;
   int32_t ns_sym;
+  // EPI_NS, the last Newton-Schulz iteration (ns_theta set): instead of
+  // storing the new X, the epilogue applies the Muon update to the weight
+  // whose X it is, W <- W ns_decay - ns_step O at desc.poff with O = X rounded
+  // to the GEMM precision (transposed back for tall weights: desc.ns_tall),
+  // and writes the bf16 copy of W to ns_shadow (if set) at the same offsets
+  float* ns_theta;
+  uint16_t* ns_shadow;
   // EPI_DE only (the embedded first layer's dE = dZ_1 W_1, never stored): the
   // epilogue reduces each wave's 64 rows of dE into the four embedding-gradient
   // terms per column (alpha: dE f, beta: dE, w: -dE alpha sin(phi) x, b:

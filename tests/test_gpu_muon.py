@@ -156,3 +156,35 @@ def test_muon_members_independent_of_streams_and_active_set(monkeypatch):
             for (W1, b1), (W2, b2) in zip(got[k], want):
                 np.testing.assert_array_equal(W1, W2)
                 np.testing.assert_array_equal(b1, b2)
+
+
+@pytest.mark.parametrize("name,over", [("regression_large", dict(K=6, B=300)), ("binary_small", dict(K=4)),
+                                       ("multiclass_lognormal", dict(K=4, B=260, depth_lo=1, depth_hi=3))])
+def test_fused_update_equals_separate_update(monkeypatch, name, over):
+    # The last Newton-Schulz GEMM applies the Muon update in its epilogue from
+    # the values it would have stored as X (rounded to the GEMM precision),
+    # with the separate update kernel's arithmetic: three steps must be
+    # bit-identical to the separate kernel's, for wide, square and tall
+    # weights (regression_large's first layers of width > 900 are tall), in
+    # bf16 and fp32 (binary_small).
+    cfg = configs.workload(name, **over, **MUON)
+    Xtr, ytr, _, _, _, idx = make_inputs(cfg, 3000, 10)
+    X, y, idx_d = to_dev(Xtr, ytr, idx)
+    runs = {}
+    for fused in ("1", "0"):
+        monkeypatch.setenv("TABPACK_MUON_FUSED_UPDATE", fused)
+        pk = tabpack.Pack(cfg).bind()
+        losses = [pk.train_step(X, y, idx_d, s).cpu().numpy() for s in (1, 2, 3)]
+        runs[fused] = (losses, [(pk.get_params(k), pk.get_moments(k)) for k in range(cfg["K"])])
+    for a, b in zip(runs["1"][0], runs["0"][0]):
+        np.testing.assert_array_equal(a, b)
+    tall = 0
+    for (p1, m1), (p2, m2) in zip(runs["1"][1], runs["0"][1]):
+        for (W1, b1), (W2, b2) in zip(p1, p2):
+            np.testing.assert_array_equal(W1, W2)
+            np.testing.assert_array_equal(b1, b2)
+            tall += W1.shape[0] > W1.shape[1]
+        for x1, x2 in zip(m1, m2):
+            for (W1, _), (W2, _) in zip(x1, x2):
+                np.testing.assert_array_equal(W1, W2)
+    print(f"[muon] {name}: fused update bit-identical, {tall} tall weights", flush=True)
