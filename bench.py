@@ -163,7 +163,7 @@ def per_epoch(cfg, pk, Xtr, ytr, Xva, yva, step, online_epochs):
     return res, step
 
 
-def variable_depth(cfg, Xtr, ytr, steps=20, stream_rows=True):
+def variable_depth(cfg, Xtr, ytr, steps=100, warmup=5, stream_rows=True):
     """Step time of the same workload with member depths ~ UniformInt[1, L]
     (App. F samples the number of layers): shallower members leave the deeper
     layers' launches, so the step should scale with the GEMM work."""
@@ -176,12 +176,13 @@ def variable_depth(cfg, Xtr, ytr, steps=20, stream_rows=True):
     hp = pk.hparams()
     idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
-    pk.train_step(Xtr, ytr, idx, 1, loss)
+    for s in range(warmup):
+        pk.train_step(Xtr, ytr, idx, s + 1, loss)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for s in range(steps):
-        pk.train_step(Xtr, ytr, idx, s + 2, loss)
+        pk.train_step(Xtr, ytr, idx, warmup + s + 1, loss)
     e1.record()
     torch.cuda.synchronize()
     work = sum(h["width"] * (d_in + (h["depth"] - 1) * h["width"]) for h in hp)
@@ -194,7 +195,7 @@ MUON_OPTS = dict(optimizer="muon", muon_lr_lo=1e-3, muon_lr_hi=1e-1)
 EMB_OPTS = dict(emb_lo=8, emb_hi=32, emb_step=4, sigma_lo=1e-2, sigma_hi=10.0)
 
 
-def muon_optimizer(cfg, Xtr, ytr, steps=20, stream_rows=True):
+def muon_optimizer(cfg, Xtr, ytr, steps=50, warmup=5, stream_rows=True):
     """Step time of the same workload with the paper's default optimizer split:
     Muon for the hidden weights (Newton-Schulz on the grouped GEMMs), AdamW for
     biases and heads; and the Newton-Schulz GEMMs' rate (library events)."""
@@ -205,18 +206,19 @@ def muon_optimizer(cfg, Xtr, ytr, steps=20, stream_rows=True):
         pk.bind_data(Xtr)
     idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
-    pk.train_step(Xtr, ytr, idx, 1, loss)
+    for s in range(warmup):
+        pk.train_step(Xtr, ytr, idx, s + 1, loss)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for s in range(steps):
-        pk.train_step(Xtr, ytr, idx, s + 2, loss)
+        pk.train_step(Xtr, ytr, idx, warmup + s + 1, loss)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     pk.profile(True)
     for s in range(3):
-        pk.train_step(Xtr, ytr, idx, steps + 2 + s, loss)
+        pk.train_step(Xtr, ytr, idx, warmup + steps + 1 + s, loss)
     stats = pk.profile_read()
     pk.profile(False)
     ns = [x for x in stats if x["name"].endswith("_ns")]
@@ -232,7 +234,7 @@ def muon_optimizer(cfg, Xtr, ytr, steps=20, stream_rows=True):
             "kernels_ms_per_step": {x["name"]: round(x["busy_ms"] / 3, 4) for x in stats}}
 
 
-def embeddings(cfg, Xtr, ytr, steps=10):
+def embeddings(cfg, Xtr, ytr, steps=20, warmup=3):
     """Step time of the same workload with periodic feature embeddings
     (d_emb ~ UniformInt[8, 32] step 4, sigma ~ LogUniform[1e-2, 10]): the first
     layer then reads d_in * d_emb columns per member; per-kernel rates from the
@@ -243,18 +245,19 @@ def embeddings(cfg, Xtr, ytr, steps=10):
     hp = pk.hparams()
     idx = synth_idx(cfg, Xtr.shape[0], Xtr.device)
     loss = torch.empty(cfg["K"], dtype=torch.float32, device=Xtr.device)
-    pk.train_step(Xtr, ytr, idx, 1, loss)
+    for s in range(warmup):
+        pk.train_step(Xtr, ytr, idx, s + 1, loss)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for s in range(steps):
-        pk.train_step(Xtr, ytr, idx, s + 2, loss)
+        pk.train_step(Xtr, ytr, idx, warmup + s + 1, loss)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     pk.profile(True)
     for s in range(2):
-        pk.train_step(Xtr, ytr, idx, steps + 2 + s, loss)
+        pk.train_step(Xtr, ytr, idx, warmup + steps + 1 + s, loss)
     stats = pk.profile_read()
     pk.profile(False)
     flops = sum(x["flops"] * x["launches"] for x in stats if x["kind"] == "mfma" or "gemm" in x["name"]) / 2
